@@ -1,0 +1,174 @@
+"""CPU reference scorer (oracle) -- TEST INFRASTRUCTURE ONLY.
+
+Only the test-suite, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  The product library never loads it and
+shares no code with it.  ``oracle.c`` holds the scoring arithmetic; this module
+only marshals numpy arrays through ctypes.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+import threading
+from typing import Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liboracle.so")
+SRC_PATH = os.path.join(_HERE, "oracle.c")
+
+INELIGIBLE = 1
+CAPACITY = 2
+
+SCORE_DTYPE = np.dtype([
+    ("makespan_us", "<i8"), ("p95_us", "<i8"), ("objective", "<f4"),
+    ("status", "<u4"), ("min_headroom_mib", "<i4"), ("n_loads", "<u2"),
+    ("n_evicts", "<u2"),
+])
+assert SCORE_DTYPE.itemsize == 32
+
+
+def build(force: bool = True, src: str = SRC_PATH, out: str = LIB_PATH) -> str:
+    """Compile liboracle.so with gcc (plain C99, no FMA contraction)."""
+    if force or not os.path.exists(out):
+        tmp = out + ".tmp"
+        subprocess.check_call([
+            "gcc", "-O2", "-std=c99", "-ffp-contract=off", "-fPIC", "-shared",
+            "-Wall", "-Wextra", "-I", _HERE, "-o", tmp, src])
+        os.replace(tmp, out)
+    return out
+
+
+class _Win(ctypes.Structure):
+    _fields_ = [
+        ("n_act", ctypes.c_int32), ("n_wf", ctypes.c_int32),
+        ("n_models", ctypes.c_int32), ("n_dev", ctypes.c_int32),
+        ("act_wf", ctypes.c_void_p), ("act_model", ctypes.c_void_p),
+        ("pred_off", ctypes.c_void_p), ("pred_idx", ctypes.c_void_p),
+        ("lat_us", ctypes.c_void_p), ("mem_mib", ctypes.c_void_p),
+        ("wf_arrival_us", ctypes.c_void_p), ("dev_cap_mib", ctypes.c_void_p),
+        ("model_mib", ctypes.c_void_p), ("load_us", ctypes.c_void_p),
+        ("init_resident", ctypes.c_void_p), ("dev_free0_us", ctypes.c_void_p),
+        ("w_makespan", ctypes.c_float), ("w_p95", ctypes.c_float),
+    ]
+
+
+_libs = {}
+_lock = threading.Lock()
+
+
+def _load(path: Optional[str] = None):
+    """Load (building on first use) the oracle library; ``path`` selects an
+    alternative build of oracle.c (the mutation tests use this)."""
+    path = path or LIB_PATH
+    with _lock:
+        if path not in _libs:
+            if path == LIB_PATH and not os.path.exists(path):
+                build(force=True)
+            lib = ctypes.CDLL(path)
+            lib.orc_score_plans.restype = ctypes.c_int
+            lib.orc_score_plans.argtypes = [ctypes.c_void_p] * 4 + [ctypes.c_int64] + [ctypes.c_void_p] * 5
+            lib.orc_levels.restype = ctypes.c_int
+            lib.orc_levels.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+            _libs[path] = lib
+    return _libs[path]
+
+
+class OracleError(RuntimeError):
+    pass
+
+
+def _c(a, dtype):
+    a = np.ascontiguousarray(a, dtype=dtype)
+    return a
+
+
+class _WinHolder:
+    """Keeps the contiguous arrays alive while the C struct points at them."""
+
+    def __init__(self, win):
+        self.keep = {
+            "act_wf": _c(win.act_wf, np.int32), "act_model": _c(win.act_model, np.int32),
+            "pred_off": _c(win.pred_off, np.int32), "pred_idx": _c(win.pred_idx, np.int32),
+            "lat_us": _c(win.lat_us, np.int32), "mem_mib": _c(win.mem_mib, np.int32),
+            "wf_arrival_us": _c(win.wf_arrival_us, np.int64),
+            "dev_cap_mib": _c(win.dev_cap_mib, np.int32), "model_mib": _c(win.model_mib, np.int32),
+            "load_us": _c(win.load_us, np.int32), "init_resident": _c(win.init_resident, np.uint64),
+            "dev_free0_us": None if win.dev_free0_us is None else _c(win.dev_free0_us, np.int64),
+        }
+        if self.keep["pred_idx"].size == 0:
+            self.keep["pred_idx"] = np.zeros(1, dtype=np.int32)
+        s = _Win()
+        s.n_act, s.n_wf, s.n_models, s.n_dev = win.n_act, win.n_wf, win.n_models, win.n_dev
+        for k, v in self.keep.items():
+            setattr(s, k, None if v is None else v.ctypes.data)
+        s.w_makespan, s.w_p95 = win.w_makespan, win.w_p95
+        self.struct = s
+
+
+def levels(win, lib_path: Optional[str] = None) -> np.ndarray:
+    lib = _load(lib_path)
+    h = _WinHolder(win)
+    out = np.zeros(max(1, win.n_act), dtype=np.int32)
+    rc = lib.orc_levels(ctypes.byref(h.struct), out.ctypes.data)
+    if rc:
+        raise OracleError(f"oracle rejected window (code {rc})")
+    return out[:win.n_act]
+
+
+def score(win, plans, begin: int = 0, end: Optional[int] = None, schedule: bool = False,
+          threads: int = 1, lib_path: Optional[str] = None):
+    """Score plans [begin, end) of ``plans``.  Returns a structured score
+    array, and with ``schedule=True`` also (start, finish, load_start, peak)."""
+    lib = _load(lib_path)
+    h = _WinHolder(win)
+    end = plans.n_plans if end is None else end
+    P = end - begin
+    N, D = win.n_act, win.n_dev
+    dev = np.ascontiguousarray(plans.dev[begin:end], dtype=np.int8)
+    prio = np.ascontiguousarray(plans.prio[begin:end], dtype=np.uint16)
+    flags = np.ascontiguousarray(plans.flags[begin:end], dtype=np.uint8)
+    scores = np.zeros(P, dtype=SCORE_DTYPE)
+    sched = None
+    if schedule:
+        sched = (np.zeros((P, N), np.int64), np.zeros((P, N), np.int64),
+                 np.zeros((P, N), np.int64), np.zeros((P, D), np.int32))
+    nb = (N + 3) // 4
+
+    def run(a, b):
+        if b <= a:
+            return 0
+
+        def ptr(arr):
+            return None if arr is None else arr.ctypes.data + a * arr.strides[0]
+
+        s0, s1, s2, s3 = sched if sched is not None else (None, None, None, None)
+        return lib.orc_score_plans(ctypes.byref(h.struct), ptr(dev), ptr(prio), ptr(flags),
+                                   b - a, ptr(scores), ptr(s0), ptr(s1), ptr(s2), ptr(s3))
+
+    if N == 0 or nb == 0:
+        # zero-width rows: give the C code a valid (unused) pointer
+        dev = np.zeros((P, 1), np.int8)
+        prio = np.zeros((P, 1), np.uint16)
+        flags = np.zeros((P, 1), np.uint8)
+    if threads <= 1 or P < 2 * threads:
+        rc = run(0, P)
+        if rc:
+            raise OracleError(f"oracle rejected window (code {rc})")
+    else:
+        bounds = np.linspace(0, P, threads + 1).astype(np.int64)
+        rcs = [0] * threads
+        def worker(t):
+            rcs[t] = run(int(bounds[t]), int(bounds[t + 1]))
+        ts = [threading.Thread(target=worker, args=(t,)) for t in range(threads)]
+        for t in ts:
+            t.start()
+        for t in ts:
+            t.join()
+        if any(rcs):
+            raise OracleError(f"oracle rejected window (codes {rcs})")
+    if schedule:
+        return scores, sched
+    return scores

@@ -1,0 +1,333 @@
+/*
+ * oracle.c -- plain CPU reference scorer (TEST INFRASTRUCTURE ONLY; see
+ * oracle.h).  Written for readability, not speed: one plan at a time, the
+ * steps in the order the paper's scheduler applies them, int64 arithmetic
+ * for every time and memory sum, no blocking, no fusion of steps.
+ *
+ * Build: gcc -O2 -std=c99 -ffp-contract=off -fPIC -shared (no fused
+ * multiply-add: the objective is two fp32 products and one fp32 sum, each
+ * rounded to nearest even).
+ */
+#include "oracle.h"
+
+#include <stdlib.h>
+#include <string.h>
+
+/* ---------------------------------------------------------------------- */
+/* window structure                                                        */
+/* ---------------------------------------------------------------------- */
+
+typedef struct {
+  int32_t *level;    /* topological level                                */
+  int32_t *n_succ;   /* number of successors                             */
+  int32_t *child;    /* the successor when n_succ == 1, else -1          */
+  uint8_t *fusible;  /* Eq. 3: single pred u, u has single succ, same model */
+} orc_struct;
+
+static void free_struct(orc_struct *s) {
+  free(s->level);
+  free(s->n_succ);
+  free(s->child);
+  free(s->fusible);
+}
+
+static int build_struct(const orc_window *w, orc_struct *s) {
+  const int32_t N = w->n_act;
+  memset(s, 0, sizeof *s);
+  if (N < 0 || w->n_wf < 0 || w->n_models < 1 || w->n_models > 64 || w->n_dev < 1)
+    return ORC_ERR_SIZE;
+  if (N > 0 && w->n_wf < 1) return ORC_ERR_SIZE;
+  size_t n = (size_t)(N > 0 ? N : 1);
+  s->level = (int32_t *)calloc(n, sizeof(int32_t));
+  s->n_succ = (int32_t *)calloc(n, sizeof(int32_t));
+  s->child = (int32_t *)calloc(n, sizeof(int32_t));
+  s->fusible = (uint8_t *)calloc(n, 1);
+  if (!s->level || !s->n_succ || !s->child || !s->fusible) {
+    free_struct(s);
+    return ORC_ERR_NOMEM;
+  }
+  /* levels: a source is level 0, otherwise one more than its deepest pred */
+  for (int32_t i = 0; i < N; ++i) {
+    int32_t lv = 0;
+    for (int32_t k = w->pred_off[i]; k < w->pred_off[i + 1]; ++k) {
+      int32_t p = w->pred_idx[k];
+      if (p < 0 || p >= i) return free_struct(s), ORC_ERR_PRED;
+      if (k > w->pred_off[i] && p <= w->pred_idx[k - 1]) return free_struct(s), ORC_ERR_PRED;
+      if (s->level[p] + 1 > lv) lv = s->level[p] + 1;
+    }
+    s->level[i] = lv;
+    if (i > 0 && lv < s->level[i - 1]) return free_struct(s), ORC_ERR_ORDER;
+    if (w->act_wf[i] < 0 || w->act_wf[i] >= w->n_wf) return free_struct(s), ORC_ERR_INDEX;
+    if (w->act_model[i] < 0 || w->act_model[i] >= w->n_models)
+      return free_struct(s), ORC_ERR_INDEX;
+  }
+  /* every workflow has at least one activation */
+  for (int32_t wf = 0; wf < w->n_wf; ++wf) {
+    int found = 0;
+    for (int32_t i = 0; i < N && !found; ++i) found = (w->act_wf[i] == wf);
+    if (!found) return free_struct(s), ORC_ERR_EMPTY_WF;
+  }
+  /* successor counts and the unique successor */
+  for (int32_t i = 0; i < N; ++i) s->child[i] = -1;
+  for (int32_t v = 0; v < N; ++v)
+    for (int32_t k = w->pred_off[v]; k < w->pred_off[v + 1]; ++k) {
+      int32_t u = w->pred_idx[k];
+      s->n_succ[u] += 1;
+      s->child[u] = v;
+    }
+  for (int32_t u = 0; u < N; ++u)
+    if (s->n_succ[u] != 1) s->child[u] = -1;
+  /* Eq. 3: edge (u, v) is fusible when pred(v) = {u}, succ(u) = {v} and both
+   * need the same deployment (every node is an agent node; one serving
+   * configuration per model) */
+  for (int32_t v = 0; v < N; ++v) {
+    if (w->pred_off[v + 1] - w->pred_off[v] != 1) continue;
+    int32_t u = w->pred_idx[w->pred_off[v]];
+    s->fusible[v] = (s->n_succ[u] == 1 && w->act_model[u] == w->act_model[v]);
+  }
+  return ORC_OK;
+}
+
+int orc_levels(const orc_window *w, int32_t *level_out) {
+  orc_struct s;
+  int rc = build_struct(w, &s);
+  if (rc) return rc;
+  for (int32_t i = 0; i < w->n_act; ++i) level_out[i] = s.level[i];
+  free_struct(&s);
+  return ORC_OK;
+}
+
+/* ---------------------------------------------------------------------- */
+/* ordering                                                                */
+/* ---------------------------------------------------------------------- */
+
+typedef struct {
+  int32_t level;
+  int32_t prio;
+  int32_t idx;
+} orc_key;
+
+static int cmp_key(const void *a, const void *b) {
+  const orc_key *x = (const orc_key *)a, *y = (const orc_key *)b;
+  if (x->level != y->level) return x->level < y->level ? -1 : 1;
+  if (x->prio != y->prio) return x->prio < y->prio ? -1 : 1;
+  if (x->idx != y->idx) return x->idx < y->idx ? -1 : 1;
+  return 0;
+}
+
+static int cmp_i64(const void *a, const void *b) {
+  int64_t x = *(const int64_t *)a, y = *(const int64_t *)b;
+  return x < y ? -1 : (x > y ? 1 : 0);
+}
+
+static int64_t max64(int64_t a, int64_t b) { return a > b ? a : b; }
+
+/* ---------------------------------------------------------------------- */
+/* scoring                                                                 */
+/* ---------------------------------------------------------------------- */
+
+int orc_score_plans(const orc_window *w, const int8_t *dev, const uint16_t *prio,
+                    const uint8_t *flags, int64_t n_plans, orc_score *scores,
+                    int64_t *start_out, int64_t *finish_out, int64_t *load_out,
+                    int32_t *peak_out) {
+  orc_struct st;
+  int rc = build_struct(w, &st);
+  if (rc) return rc;
+  const int32_t N = w->n_act, D = w->n_dev, M = w->n_models, W = w->n_wf;
+  const int32_t NB = (N + 3) / 4;
+  size_t n = (size_t)(N > 0 ? N : 1);
+  uint8_t *fuse = (uint8_t *)malloc(n), *pf = (uint8_t *)malloc(n), *member = (uint8_t *)malloc(n);
+  int64_t *unit_Mx = (int64_t *)malloc(n * 8);
+  orc_key *order = (orc_key *)malloc(n * sizeof(orc_key));
+  int64_t *start = (int64_t *)malloc(n * 8), *finish = (int64_t *)malloc(n * 8),
+          *load_start = (int64_t *)malloc(n * 8);
+  int64_t *comp = (int64_t *)malloc((size_t)(W > 0 ? W : 1) * 8);
+  int64_t *free_t = (int64_t *)malloc((size_t)D * 8), *used = (int64_t *)malloc((size_t)D * 8),
+          *peak = (int64_t *)malloc((size_t)D * 8);
+  uint64_t *res = (uint64_t *)malloc((size_t)D * 8);
+  int64_t *remaining = (int64_t *)malloc((size_t)D * M * 8), *last = (int64_t *)malloc((size_t)D * M * 8);
+  if (!fuse || !pf || !member || !unit_Mx || !order || !start || !finish ||
+      !load_start || !comp || !free_t || !used || !peak || !res || !remaining || !last) {
+    rc = ORC_ERR_NOMEM;
+    goto done;
+  }
+
+  for (int64_t p = 0; p < n_plans; ++p) {
+    const int8_t *pdev = dev + p * N;
+    const uint16_t *pprio = prio + p * N;
+    const uint8_t *pfl = flags + p * NB;
+    orc_score sc;
+    memset(&sc, 0, sizeof sc);
+
+    /* ---- unit formation (Eq. 3, Eq. 4, Eq. 9) ---- */
+    for (int32_t v = 0; v < N; ++v) {
+      fuse[v] = (pfl[v / 4] >> (2 * (v % 4))) & 1u;
+      pf[v] = (pfl[v / 4] >> (2 * (v % 4) + 1)) & 1u;
+    }
+    for (int32_t v = 0; v < N; ++v) member[v] = fuse[v] && st.fusible[v];
+    int32_t n_units = 0;
+    for (int32_t h = 0; h < N; ++h) {
+      if (member[h]) continue;
+      int32_t d = pdev[h];
+      if (d < 0 || d >= D) {
+        sc.status |= ORC_INELIGIBLE;
+        continue;
+      }
+      int64_t Mx = 0;
+      int32_t v = h;
+      for (;;) {
+        if (w->lat_us[(int64_t)v * D + d] < 0) sc.status |= ORC_INELIGIBLE;
+        if (w->mem_mib[(int64_t)v * D + d] > Mx) Mx = w->mem_mib[(int64_t)v * D + d];
+        int32_t c = st.child[v];
+        if (c >= 0 && member[c]) v = c;
+        else break;
+      }
+      unit_Mx[h] = Mx;
+      order[n_units].level = st.level[h];
+      order[n_units].prio = pprio[h];
+      order[n_units].idx = h;
+      ++n_units;
+    }
+    if (sc.status & ORC_INELIGIBLE) {
+      sc.status = ORC_INELIGIBLE;
+      scores[p] = sc;
+      continue;
+    }
+
+    /* ---- resource order (Eq. 10; ready before near-ready, then priority) ---- */
+    qsort(order, (size_t)n_units, sizeof(orc_key), cmp_key);
+    for (int32_t i = 0; i < D * M; ++i) remaining[i] = 0;
+    for (int32_t k = 0; k < n_units; ++k) {
+      int32_t h = order[k].idx;
+      remaining[pdev[h] * M + w->act_model[h]] += 1;
+    }
+
+    /* ---- pool snapshot ---- */
+    for (int32_t d = 0; d < D; ++d) {
+      free_t[d] = w->dev_free0_us ? w->dev_free0_us[d] : 0;
+      res[d] = w->init_resident[d];
+      used[d] = 0;
+      for (int32_t m = 0; m < M; ++m)
+        if ((res[d] >> m) & 1u) used[d] += w->model_mib[m];
+      peak[d] = used[d];
+      for (int32_t m = 0; m < M; ++m) last[d * M + m] = -1;
+    }
+    int64_t n_loads = 0, n_evicts = 0;
+
+    /* ---- propagate units in resource order ---- */
+    for (int32_t pos = 0; pos < n_units; ++pos) {
+      int32_t h = order[pos].idx;
+      int32_t d = pdev[h];
+      int32_t m = w->act_model[h];
+      int32_t wf = w->act_wf[h];
+      int64_t Mx = unit_Mx[h];
+      remaining[d * M + m] -= 1;
+
+      /* predicted release (Eq. 2): workflow arrival, or the latest
+       * predecessor completion */
+      int64_t r = w->wf_arrival_us[wf];
+      for (int32_t k = w->pred_off[h]; k < w->pred_off[h + 1]; ++k)
+        r = max64(r, finish[w->pred_idx[k]]);
+
+      /* lifecycle (Eq. 5) with reclamation and the cumulative check (Eq. 11) */
+      int miss = !((res[d] >> m) & 1u);
+      int64_t need = (miss ? (int64_t)w->model_mib[m] : 0) + Mx;
+      while (used[d] + need > w->dev_cap_mib[d]) {
+        uint64_t cand = res[d] & ~(1ull << m);
+        if (!cand) break;
+        int32_t victim = -1;
+        for (int32_t m2 = 0; m2 < M; ++m2) {
+          if (!((cand >> m2) & 1u)) continue;
+          if (victim < 0) {
+            victim = m2;
+            continue;
+          }
+          int alive2 = remaining[d * M + m2] > 0, aliveV = remaining[d * M + victim] > 0;
+          if (alive2 != aliveV) {
+            if (alive2 < aliveV) victim = m2;
+          } else if (last[d * M + m2] < last[d * M + victim]) {
+            victim = m2; /* equal keys keep the lower id (scanned first) */
+          }
+        }
+        res[d] &= ~(1ull << victim);
+        used[d] -= w->model_mib[victim];
+        n_evicts += 1;
+      }
+      if (used[d] + need > w->dev_cap_mib[d]) sc.status |= ORC_CAPACITY;
+
+      /* timeline (Eq. 7): a load waits for the device; it starts at the
+       * unit's release, or at the workflow's arrival when prefetched */
+      int64_t s;
+      if (miss) {
+        int64_t ls = max64(pf[h] ? w->wf_arrival_us[wf] : r, free_t[d]);
+        int64_t le = ls + w->load_us[m * D + d];
+        res[d] |= 1ull << m;
+        used[d] += w->model_mib[m];
+        n_loads += 1;
+        load_start[h] = ls;
+        s = max64(r, le);
+      } else {
+        load_start[h] = -1;
+        s = max64(r, free_t[d]);
+      }
+      if (used[d] + Mx > peak[d]) peak[d] = used[d] + Mx;
+
+      /* the unit's activations run back-to-back under one grant (Eq. 4) */
+      int32_t v = h;
+      for (;;) {
+        start[v] = s;
+        finish[v] = s + w->lat_us[(int64_t)v * D + d];
+        s = finish[v];
+        if (v != h) load_start[v] = -1;
+        int32_t c = st.child[v];
+        if (c >= 0 && member[c]) v = c;
+        else break;
+      }
+      free_t[d] = s;
+      last[d * M + m] = pos;
+    }
+
+    /* ---- reductions (Sec. 4 metrics) ---- */
+    if (N > 0) {
+      int64_t min_arr = w->wf_arrival_us[0], max_fin = finish[0];
+      for (int32_t wf = 1; wf < W; ++wf)
+        if (w->wf_arrival_us[wf] < min_arr) min_arr = w->wf_arrival_us[wf];
+      for (int32_t i = 1; i < N; ++i) max_fin = max64(max_fin, finish[i]);
+      sc.makespan_us = max_fin - min_arr;
+      for (int32_t wf = 0; wf < W; ++wf) comp[wf] = INT64_MIN;
+      for (int32_t i = 0; i < N; ++i) comp[w->act_wf[i]] = max64(comp[w->act_wf[i]], finish[i]);
+      for (int32_t wf = 0; wf < W; ++wf) comp[wf] -= w->wf_arrival_us[wf];
+      qsort(comp, (size_t)W, sizeof(int64_t), cmp_i64);
+      int32_t k = (95 * W + 99) / 100; /* nearest rank: ceil(0.95 W) */
+      sc.p95_us = comp[k - 1];
+    }
+    {
+      float a = (float)sc.makespan_us;
+      float b = (float)sc.p95_us;
+      float x = w->w_makespan * a;
+      float y = w->w_p95 * b;
+      sc.objective = x + y;
+    }
+    int64_t headroom = (int64_t)w->dev_cap_mib[0] - peak[0];
+    for (int32_t d = 1; d < D; ++d)
+      if ((int64_t)w->dev_cap_mib[d] - peak[d] < headroom) headroom = (int64_t)w->dev_cap_mib[d] - peak[d];
+    sc.min_headroom_mib = (int32_t)headroom;
+    sc.n_loads = (uint16_t)(n_loads > 65535 ? 65535 : n_loads);
+    sc.n_evicts = (uint16_t)(n_evicts > 65535 ? 65535 : n_evicts);
+    scores[p] = sc;
+
+    if (start_out) memcpy(start_out + p * N, start, (size_t)N * 8);
+    if (finish_out) memcpy(finish_out + p * N, finish, (size_t)N * 8);
+    if (load_out) memcpy(load_out + p * N, load_start, (size_t)N * 8);
+    if (peak_out)
+      for (int32_t d = 0; d < D; ++d) peak_out[p * D + d] = (int32_t)peak[d];
+  }
+  rc = ORC_OK;
+
+done:
+  free(fuse); free(pf); free(member); free(unit_Mx); free(order);
+  free(start); free(finish); free(load_start); free(comp); free(free_t); free(used);
+  free(peak); free(res); free(remaining); free(last);
+  free_struct(&st);
+  return rc;
+}

@@ -1,0 +1,289 @@
+"""Independent second formulations that pin the CPU oracle.
+
+Nothing here is shared with the oracle (C) or the GPU path (HIP): the same
+quantities are derived a different way, so that a dropped term, a swapped
+operand or a wrong index in the oracle disagrees with at least one of them.
+
+* levels        -- networkx ``topological_generations`` (library routine).
+* fusion        -- Eq. 3 written with explicit predecessor/successor sets.
+* lifecycle     -- for every unit the device's resident set is rebuilt by
+                   replaying the device's whole prefix from the snapshot;
+                   "remaining use" is a scan of the suffix, "last use" a scan
+                   of the prefix (the oracle keeps incremental counters).
+* timeline      -- Eq. 7 written literally as a constraint system over
+                   explicit load and execution operations (graph edges plus
+                   resource-order edges), solved by Kleene iteration to the
+                   least fixpoint (the oracle does one forward sweep).
+* p95           -- ``numpy.percentile(..., method="inverted_cdf")``, which
+                   is the nearest-rank percentile.
+* objective     -- numpy float32 arithmetic.
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import Dict, List
+
+import networkx as nx
+import numpy as np
+
+from paper_2609_03335_amd.workload import unpack_flags
+
+
+def nx_levels(win) -> np.ndarray:
+    g = nx.DiGraph()
+    g.add_nodes_from(range(win.n_act))
+    for v in range(win.n_act):
+        for u in win.preds(v):
+            g.add_edge(int(u), v)
+    lv = np.zeros(win.n_act, dtype=np.int64)
+    for k, gen in enumerate(nx.topological_generations(g)):
+        for v in gen:
+            lv[v] = k
+    return lv
+
+
+def fusible_set(win) -> set:
+    preds = {v: set(int(u) for u in win.preds(v)) for v in range(win.n_act)}
+    succs: Dict[int, set] = {v: set() for v in range(win.n_act)}
+    for v, ps in preds.items():
+        for u in ps:
+            succs[u].add(v)
+    out = set()
+    for v in range(win.n_act):
+        if len(preds[v]) == 1:
+            (u,) = tuple(preds[v])
+            if succs[u] == {v} and win.act_model[u] == win.act_model[v]:
+                out.add(v)
+    return out
+
+
+@dataclasses.dataclass
+class Unit:
+    head: int
+    chain: List[int]
+    device: int
+    model: int
+    wf: int
+    key: tuple
+
+
+def form_units(win, dev_row, prio_row, fuse_row):
+    """Units of one plan, or None when the plan is ineligible."""
+    D = win.n_dev
+    lat = np.asarray(win.lat_us).reshape(win.n_act, D)
+    fus = fusible_set(win)
+    lv = nx_levels(win)
+    members = {v for v in range(win.n_act) if fuse_row[v] and v in fus}
+    succ_of = {}
+    for v in members:
+        (u,) = tuple(int(x) for x in win.preds(v))
+        succ_of[u] = v
+    units = []
+    for h in range(win.n_act):
+        if h in members:
+            continue
+        d = int(dev_row[h])
+        if not 0 <= d < D:
+            return None
+        chain = [h]
+        while chain[-1] in succ_of:
+            chain.append(succ_of[chain[-1]])
+        if any(lat[v, d] < 0 for v in chain):
+            return None
+        units.append(Unit(h, chain, d, int(win.act_model[h]), int(win.act_wf[h]),
+                          (int(lv[h]), int(prio_row[h]), h)))
+    units.sort(key=lambda u: u.key)
+    return units
+
+
+def replay_lifecycle(win, units):
+    """Per unit: (miss, n_evicted, used_after, peak_candidate, over_capacity).
+
+    Each unit's state is recomputed from the snapshot by replaying its
+    device's prefix."""
+    M = win.n_models
+    W = np.asarray(win.model_mib, dtype=np.int64)
+    cap = np.asarray(win.dev_cap_mib, dtype=np.int64)
+    mem = np.asarray(win.mem_mib, dtype=np.int64).reshape(win.n_act, win.n_dev)
+    seqs: Dict[int, List[Unit]] = {}
+    for u in units:
+        seqs.setdefault(u.device, []).append(u)
+
+    def step(d, seq, k, resident):
+        """Apply unit seq[k] to a resident set; returns the decision."""
+        u = seq[k]
+        mx = max(int(mem[v, d]) for v in u.chain)
+        used = sum(int(W[m]) for m in resident)
+        miss = u.model not in resident
+        need = (int(W[u.model]) if miss else 0) + mx
+        evicted = 0
+        while used + need > cap[d]:
+            cands = [m for m in resident if m != u.model]
+            if not cands:
+                break
+
+            def key(m):
+                alive = any(s.model == m for s in seq[k + 1:])
+                last = max([j for j in range(k) if seq[j].model == m], default=-1)
+                return (alive, last, m)
+            victim = min(cands, key=key)
+            resident.discard(victim)
+            used -= int(W[victim])
+            evicted += 1
+        over = used + need > cap[d]
+        if miss:
+            resident.add(u.model)
+            used += int(W[u.model])
+        return miss, evicted, used, used + mx, over
+
+    out = {}
+    for d, seq in seqs.items():
+        init = {m for m in range(M) if (int(win.init_resident[d]) >> m) & 1}
+        for k in range(len(seq)):
+            resident = set(init)
+            for j in range(k):  # replay the prefix from the snapshot
+                step(d, seq, j, resident)
+            out[seq[k].head] = step(d, seq, k, resident)
+    return out
+
+
+def fixpoint_timeline(win, units, misses, pf_row):
+    """Eq. 7 as a constraint system: every operation starts at the max of
+    its release, its graph predecessors' completions and its resource
+    predecessor's completion; solved by iterating to the least fixpoint."""
+    D = win.n_dev
+    lat = np.asarray(win.lat_us, dtype=np.int64).reshape(win.n_act, D)
+    load = np.asarray(win.load_us, dtype=np.int64).reshape(win.n_models, D)
+    arr = np.asarray(win.wf_arrival_us, dtype=np.int64)
+    free0 = (np.zeros(D, np.int64) if win.dev_free0_us is None
+             else np.asarray(win.dev_free0_us, dtype=np.int64))
+    ops = []            # (kind, activation or unit head, device, duration)
+    exec_op = {}        # activation -> op id
+    load_op = {}        # unit head -> op id
+    res_pred = {}       # op id -> previous op on the same device
+    last_on_dev: Dict[int, int] = {}
+    for u in units:
+        d = u.device
+        if misses[u.head]:
+            oid = len(ops)
+            ops.append(("load", u.head, d, int(load[u.model, d])))
+            load_op[u.head] = oid
+            if d in last_on_dev:
+                res_pred[oid] = last_on_dev[d]
+            last_on_dev[d] = oid
+        for v in u.chain:
+            oid = len(ops)
+            ops.append(("exec", v, d, int(lat[v, d])))
+            exec_op[v] = oid
+            if d in last_on_dev:
+                res_pred[oid] = last_on_dev[d]
+            last_on_dev[d] = oid
+    unit_of = {v: u for u in units for v in u.chain}
+    first_op_of_dev = {}
+    for oid, (_, _, d, _) in enumerate(ops):
+        first_op_of_dev.setdefault(d, oid)
+    S = [0] * len(ops)
+    F = [0] * len(ops)
+
+    def release_of_unit(u):  # Eq. 2 with the workflow arrival as time origin
+        r = int(arr[u.wf])
+        for p in win.preds(u.head):
+            r = max(r, F[exec_op[int(p)]])
+        return r
+
+    changed = True
+    rounds = 0
+    while changed:
+        changed = False
+        rounds += 1
+        for oid, (kind, x, d, dur) in enumerate(ops):
+            lb = []
+            if oid in res_pred:
+                lb.append(F[res_pred[oid]])
+            elif first_op_of_dev[d] == oid:
+                lb.append(int(free0[d]))
+            if kind == "load":
+                u = unit_of[x]
+                lb.append(int(arr[u.wf]) if pf_row[u.head] else release_of_unit(u))
+            else:
+                u = unit_of[x]
+                if x == u.head:
+                    lb.append(release_of_unit(u))
+                    if u.head in load_op:
+                        lb.append(F[load_op[u.head]])
+                else:
+                    (p,) = tuple(int(q) for q in win.preds(x))
+                    lb.append(F[exec_op[p]])
+            s = max(lb)
+            if s != S[oid] or F[oid] != s + dur:
+                S[oid], F[oid] = s, s + dur
+                changed = True
+        assert rounds <= len(ops) + 2, "no fixpoint: cyclic constraints"
+    start = np.zeros(win.n_act, np.int64)
+    finish = np.zeros(win.n_act, np.int64)
+    load_start = np.full(win.n_act, -1, np.int64)
+    for v, oid in exec_op.items():
+        start[v], finish[v] = S[oid], F[oid]
+    for h, oid in load_op.items():
+        load_start[h] = S[oid]
+    return start, finish, load_start
+
+
+def independent_score(win, dev_row, prio_row, fuse_row, pf_row):
+    """Full score of one plan from the second formulation."""
+    units = form_units(win, dev_row, prio_row, fuse_row)
+    if units is None:
+        return dict(status=1)
+    life = replay_lifecycle(win, units)
+    misses = {h: life[h][0] for h in life}
+    start, finish, load_start = fixpoint_timeline(win, units, misses, pf_row)
+    D, W = win.n_dev, win.n_wf
+    arr = np.asarray(win.wf_arrival_us, dtype=np.int64)
+    cap = np.asarray(win.dev_cap_mib, dtype=np.int64)
+    Wm = np.asarray(win.model_mib, dtype=np.int64)
+    peak = np.array([sum(int(Wm[m]) for m in range(win.n_models)
+                         if (int(win.init_resident[d]) >> m) & 1) for d in range(D)], np.int64)
+    for u in units:
+        peak[u.device] = max(peak[u.device], life[u.head][3])
+    status = 2 if any(life[h][4] for h in life) else 0
+    if win.n_act:
+        makespan = int(finish.max() - arr.min())
+        comp = np.array([finish[np.asarray(win.act_wf) == w].max() - arr[w] for w in range(W)])
+        p95 = int(np.percentile(comp, 95, method="inverted_cdf"))
+    else:
+        makespan, p95 = 0, 0
+    obj = np.float32(np.float32(win.w_makespan) * np.float32(makespan)) + \
+        np.float32(np.float32(win.w_p95) * np.float32(p95))
+    return dict(status=status, makespan_us=makespan, p95_us=p95, objective=np.float32(obj),
+                min_headroom_mib=int((cap - peak).min()),
+                n_loads=min(65535, sum(1 for h in life if life[h][0])),
+                n_evicts=min(65535, sum(life[h][1] for h in life)),
+                start=start, finish=finish, load_start=load_start, peak=peak, units=units)
+
+
+def plan_rows(win, plans, p):
+    fuse, pf = unpack_flags(plans.flags[p:p + 1], win.n_act)
+    return plans.dev[p], plans.prio[p], fuse[0], pf[0]
+
+
+def compare_plan(win, plans, p, oracle_scores, oracle_sched) -> List[str]:
+    """Differences between the oracle and the second formulation on plan p."""
+    ref = independent_score(win, *plan_rows(win, plans, p))
+    sc = oracle_scores[p]
+    errs = []
+    if int(sc["status"]) != ref["status"]:
+        return [f"plan {p}: status {int(sc['status'])} != {ref['status']}"]
+    if ref["status"] & 1:
+        return []
+    for k in ("makespan_us", "p95_us", "min_headroom_mib", "n_loads", "n_evicts"):
+        if int(sc[k]) != int(ref[k]):
+            errs.append(f"plan {p}: {k} {int(sc[k])} != {int(ref[k])}")
+    if np.float32(sc["objective"]).view(np.uint32) != np.float32(ref["objective"]).view(np.uint32):
+        errs.append(f"plan {p}: objective {sc['objective']} != {ref['objective']}")
+    if oracle_sched is not None:
+        st, fi, ls, pk = (x[p] for x in oracle_sched)
+        for name, a, b in (("start", st, ref["start"]), ("finish", fi, ref["finish"]),
+                           ("load_start", ls, ref["load_start"]), ("peak", pk, ref["peak"])):
+            if not np.array_equal(np.asarray(a, np.int64), np.asarray(b, np.int64)):
+                errs.append(f"plan {p}: {name} differs")
+    return errs

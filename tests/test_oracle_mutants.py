@@ -1,0 +1,111 @@
+"""Mutation check of the pins: each plausible mistake planted in a copy of
+oracle.c (built on the CPU into a temporary library) must fail at least one
+of the oracle's pin tests.  The real oracle is never modified."""
+import os
+import shutil
+import tempfile
+
+import numpy as np
+import pytest
+
+import oracle
+
+import test_oracle_bruteforce as t_bf
+import test_oracle_independent as t_ind
+import test_oracle_paper_examples as t_pap
+import test_oracle_properties as t_prop
+
+# (name, original fragment, planted mistake)
+MUTANTS = [
+    ("release ignores arrival", "int64_t r = w->wf_arrival_us[wf];", "int64_t r = 0;"),
+    ("victim prefers live copies", "if (alive2 < aliveV) victim = m2;", "if (alive2 > aliveV) victim = m2;"),
+    ("victim most recently used", "} else if (last[d * M + m2] < last[d * M + victim]) {",
+     "} else if (last[d * M + m2] > last[d * M + victim]) {"),
+    ("prefetch ignored", "pf[h] ? w->wf_arrival_us[wf] : r", "r"),
+    ("peak without activation memory", "if (used[d] + Mx > peak[d]) peak[d] = used[d] + Mx;",
+     "if (used[d] > peak[d]) peak[d] = used[d];"),
+    ("start ignores release after load", "s = max64(r, le);", "s = le;"),
+    ("p95 rank rounded", "(95 * W + 99) / 100", "(95 * W + 50) / 100"),
+    ("priority ignored", "if (x->prio != y->prio) return x->prio < y->prio ? -1 : 1;", ""),
+    ("level ignored", "if (x->level != y->level) return x->level < y->level ? -1 : 1;", ""),
+    ("fusion ignores deployment", " && w->act_model[u] == w->act_model[v]", ""),
+    ("fusion ignores fan-out", "s->fusible[v] = (s->n_succ[u] == 1 &&", "s->fusible[v] = (s->n_succ[u] >= 1 &&"),
+    ("member runs on its own device", "finish[v] = s + w->lat_us[(int64_t)v * D + d];",
+     "finish[v] = s + w->lat_us[(int64_t)v * D + (pdev[v] >= 0 && pdev[v] < D ? pdev[v] : d)];"),
+    ("makespan from time zero", "sc.makespan_us = max_fin - min_arr;", "sc.makespan_us = max_fin;"),
+    ("load table transposed", "w->load_us[m * D + d]", "w->load_us[(d * M + m) % (M * D)]"),
+    ("capacity check inclusive", "if (used[d] + need > w->dev_cap_mib[d]) sc.status |= ORC_CAPACITY;",
+     "if (used[d] + need >= w->dev_cap_mib[d]) sc.status |= ORC_CAPACITY;"),
+    ("eviction ignores activation memory",
+     "int64_t need = (miss ? (int64_t)w->model_mib[m] : 0) + Mx;",
+     "int64_t need = (miss ? (int64_t)w->model_mib[m] : 0);"),
+    ("objective weight swapped", "float y = w->w_p95 * b;", "float y = w->w_makespan * b;"),
+    ("hit ignores busy device", "s = max64(r, free_t[d]);", "s = r;"),
+    ("loads double counted", "n_loads += 1;", "n_loads += 2;"),
+    ("evicts one too many", "while (used[d] + need > w->dev_cap_mib[d]) {",
+     "while (used[d] + need + 1 > w->dev_cap_mib[d]) {"),
+    ("snapshot memory ignored", "if ((res[d] >> m) & 1u) used[d] += w->model_mib[m];",
+     "if ((res[d] >> m) & 1u) used[d] += 0;"),
+    ("device free after head only", "free_t[d] = s;", "free_t[d] = finish[h];"),
+    ("completion from first arrival", "comp[wf] -= w->wf_arrival_us[wf];", "comp[wf] -= min_arr;"),
+    ("headroom maximum", "< headroom) headroom", "> headroom) headroom"),
+    ("load waits for release when prefetched", "int64_t ls = max64(pf[h] ? w->wf_arrival_us[wf] : r, free_t[d]);",
+     "int64_t ls = max64(r, free_t[d]);"),
+    ("pred finish ignored", "r = max64(r, finish[w->pred_idx[k]]);", "r = max64(r, start[w->pred_idx[k]]);"),
+]
+
+
+def _pin_checks():
+    """A fast selection of the pin tests (closed forms, second formulation,
+    paper examples, invariants, metamorphic relations, exhaustive search)."""
+    checks = []
+    checks += [lambda s=s: t_ind.test_random_windows(s) for s in range(12)]
+    checks += [lambda s=s: t_ind.test_tight_capacity(s) for s in range(4)]
+    checks += [t_ind.test_capacity_flag_seen]
+    checks += [lambda s=s: t_prop.test_single_device_closed_form(s) for s in range(3)]
+    checks += [lambda s=s: t_prop.test_contention_free_longest_path(s) for s in range(3)]
+    checks += [lambda s=s: t_prop.test_bounds_and_invariants(s) for s in range(6)]
+    checks += [lambda s=s: t_prop.test_prefetch_never_hurts(s) for s in range(3)]
+    checks += [lambda s=s: t_prop.test_time_shift_and_relabel(s) for s in range(3)]
+    checks += [t_prop.test_objective_is_fp32_of_integer_outputs, t_prop.test_p95_nearest_rank_against_numpy,
+               t_prop.test_p95_nearest_rank_many_workflow_counts]
+    checks += [lambda s=s: t_prop.test_exact_fit_boundary(s) for s in (-1, 0, 1)]
+    checks += [t_pap.test_fig4_one_load_one_prefetch_shared_by_two_workflows,
+               t_pap.test_qmsum_fused_chain_one_grant_one_replica]
+    checks += [lambda s=s: t_bf.test_exhaustive(s) for s in range(2)]
+    return checks
+
+
+@pytest.fixture(scope="module")
+def tmpdir_mod():
+    d = tempfile.mkdtemp(prefix="oracle_mutants_")
+    yield d
+    shutil.rmtree(d, ignore_errors=True)
+
+
+def test_unmutated_copy_passes(tmpdir_mod, monkeypatch):
+    src = open(oracle.SRC_PATH).read()
+    path = os.path.join(tmpdir_mod, "same.c")
+    open(path, "w").write(src)
+    lib = oracle.build(src=path, out=os.path.join(tmpdir_mod, "libsame.so"))
+    monkeypatch.setattr(oracle, "LIB_PATH", lib)
+    for check in _pin_checks():
+        check()
+
+
+@pytest.mark.parametrize("name,orig,mut", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_mutant_is_killed(name, orig, mut, tmpdir_mod, monkeypatch):
+    src = open(oracle.SRC_PATH).read()
+    assert src.count(orig) == 1, f"fragment for '{name}' not found exactly once"
+    tag = "".join(ch if ch.isalnum() else "_" for ch in name)
+    path = os.path.join(tmpdir_mod, tag + ".c")
+    open(path, "w").write(src.replace(orig, mut))
+    lib = oracle.build(src=path, out=os.path.join(tmpdir_mod, "lib" + tag + ".so"))
+    monkeypatch.setattr(oracle, "LIB_PATH", lib)
+    for check in _pin_checks():
+        try:
+            with np.errstate(all="ignore"):
+                check()
+        except (AssertionError, oracle.OracleError, IndexError, ValueError, KeyError):
+            return  # killed
+    pytest.fail(f"mutant '{name}' survived every pin")
