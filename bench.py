@@ -1,0 +1,162 @@
+"""Benchmark: candidate plans scored per second on one MI355X.
+
+A step is one pass of the whole hot path over one batch already resident in
+HBM: score every plan of the batch (plan decode, unit formation, resource
+order, lifecycle and memory simulation, timeline, reductions) and select the
+best feasible plan.  The default workload is the throughput configuration:
+one 256-activation window (16 workflows x 16 activations, 8 devices, 16
+models) and 1,048,576 candidate plans (about 0.9 GB of packed plans).
+
+Prints one JSON line (see the fields at the end of main()).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X published HBM3E bandwidth
+
+
+def algorithmic_bytes_per_plan(n_act: int) -> int:
+    """Packed plan row read once (int8 device + uint16 priority + 2 flag
+    bits per activation) plus the 32-byte score record written once."""
+    return 3 * n_act + (n_act + 3) // 4 + 32
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or "unknown"
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=4, help="benchmark configuration 0-4")
+    ap.add_argument("--plans", type=int, default=None, help="override the number of plans")
+    ap.add_argument("--cpu-sample", type=int, default=None,
+                    help="plans in the CPU-baseline sample (default: about 10 s of CPU work)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--check", type=int, default=4096,
+                    help="plans checked against the oracle before timing (0 = none)")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py scores plans on one GPU only; multi-GPU runs are not part of this "
+              "build (plans are independent: see DESIGN.md for how the batch would shard)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2609_03335_amd as pkg
+    from paper_2609_03335_amd import workload
+
+    assert torch.cuda.is_available(), "bench.py needs a HIP device"
+    t0 = time.time()
+    win, plans = workload.make_config(args.config, n_plans=args.plans)
+    P, N, D = plans.n_plans, win.n_act, win.n_dev
+    print(f"[bench] config {args.config}: N={N} W={win.n_wf} D={D} M={win.n_models} P={P} "
+          f"generated in {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
+
+    ctx = pkg.Context(0)
+    ctx.wf_plan_upload_window(win)
+    dev, prio, flags = pkg.device_plans(plans, "cuda:0")
+    scores = torch.empty((P, 32), dtype=torch.uint8, device="cuda:0")
+    best = torch.empty(1, dtype=torch.int64, device="cuda:0")
+    stream = torch.cuda.current_stream()
+
+    def step():
+        ctx.wf_plan_score_batch(dev, prio, flags, P, scores, None, stream)
+        ctx.wf_plan_argmin(scores, P, best, stream)
+
+    # correctness gate on a sample before timing
+    if args.check:
+        import oracle
+        step()
+        torch.cuda.synchronize()
+        idx = np.unique(np.linspace(0, P - 1, min(P, args.check)).astype(np.int64))
+        got = pkg.scores_to_numpy(scores, P)[idx]
+        ref = oracle.score(win, plans.take(idx), threads=min(16, os.cpu_count() or 1))
+        if got.tobytes() != ref.tobytes():
+            print("[bench] GPU scores differ from the oracle", file=sys.stderr)
+            sys.exit(1)
+        print(f"[bench] {len(idx)} sampled plans bit-exact vs oracle", file=sys.stderr, flush=True)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # per-launch durations of the scoring kernel, on the stream it runs on
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    if torch.distributed.is_available() and torch.distributed.is_initialized():
+        torch.distributed.barrier()
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for i in range(args.steps):
+        ev[i][0].record(stream)
+        ctx.wf_plan_score_batch(dev, prio, flags, P, scores, None, stream)
+        ev[i][1].record(stream)
+        ctx.wf_plan_argmin(scores, P, best, stream)
+    torch.cuda.synchronize()
+    t_total = time.perf_counter() - t_start
+    if torch.distributed.is_available() and torch.distributed.is_initialized():
+        torch.distributed.barrier()
+    kernel_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    ms_per_step = t_total * 1e3 / args.steps
+    value = P * args.steps / t_total
+
+    bpp = algorithmic_bytes_per_plan(N)
+    achieved = bpp * P / (kernel_ms * 1e-3) / 1e9
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "kernel": "score_plans", "kernel_ms": round(kernel_ms, 4),
+                "bytes_per_plan": bpp}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        threads = max(1, min(16, os.cpu_count() or 1))
+        n_cpu = args.cpu_sample or min(P, 400_000)
+        idx = np.arange(n_cpu) * max(1, P // n_cpu)
+        sample = plans.take(idx)
+        t = time.perf_counter()
+        oracle.score(win, sample, threads=threads)
+        dt = time.perf_counter() - t
+        cpu = {"value": round(n_cpu / dt, 1), "unit": "plans/s", "cores": threads, "kind": "oracle",
+               "sample": f"{n_cpu} evenly spaced plans of the same batch, {threads} threads, "
+                         f"{dt:.2f}s wall ({cpu_model()})"}
+
+    line = {
+        "metric": "candidate plans scored/sec at 1 GPU; achieved HBM GB/s vs peak",
+        "value": round(value, 1), "unit": "plans/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "int64", "data": "synthetic",
+        "config": {"workload": workload.CONFIGS[args.config]["name"], "n_act": N,
+                   "n_wf": win.n_wf, "n_dev": D, "n_models": win.n_models, "n_plans": P,
+                   "batch_bytes": bpp * P},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line))
+    ctx.close()
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,181 @@
+/*
+ * wf_plan.h -- C ABI of the MI355X (gfx950) candidate-plan scorer.
+ *
+ * The paper's scheduler (Sec. 3.5, Algorithm 1) ranks candidate physical
+ * execution plans of a planning window by their predicted consequences on one
+ * shared timeline; its Propagate step serialises co-located operations and
+ * checks Eq. 9-11.  This library evaluates that forecast for a whole batch of
+ * candidate plans at once on one GPU:
+ *
+ *   window (Sec. 3.2 window W_t of concurrent workflows, snapshot S_t of the
+ *   pool, Predictor table of Eq. 1)  +  plans (device, priority, fuse bit,
+ *   prefetch bit per activation)   ->   per-plan score and, optionally, the
+ *   per-activation schedule.
+ *
+ * Semantics of one plan (each step cites the passage it follows):
+ *   1. Units (Eq. 3, Eq. 4, Eq. 9).  Activation v is a chain member when its
+ *      fuse bit is set and edge (u,v) satisfies Eq. 3: pred(v) = {u},
+ *      succ(u) = {v}, same model.  Every other activation heads a unit: its
+ *      chain of members runs back to back on the head's device under one
+ *      grant; memory is the members' maximum; a member's own device entry
+ *      is ignored.
+ *   2. Resource order (Eq. 10; Sec. 3.5 tick-local planning).  Units are
+ *      taken in ascending (topological level, priority, activation index).
+ *   3. Lifecycle and memory (Eq. 5, Eq. 11; Sec. 3.5 reclamation).  A unit
+ *      reuses its model if resident on its device, else loads it.  While the
+ *      device cannot hold the resident models plus the load plus the unit's
+ *      memory, the lease-free victim with no remaining use on the device is
+ *      reclaimed first, then the least recently used, then the lower model
+ *      id.  If it still does not fit the plan is flagged WF_ST_CAPACITY
+ *      (memory equal to capacity fits).
+ *   4. Timeline (Eq. 2, Eq. 7).  Release r = max(workflow arrival, latest
+ *      predecessor finish).  A device runs one unit or one load at a time.
+ *      A load starts at max(r, device free) -- or max(arrival, device free)
+ *      when the prefetch bit is set (Eq. 5, alpha_N = Prefetch) -- and the
+ *      unit starts at max(r, load end); without a load at max(r, device
+ *      free).  Reclamation takes no time.
+ *   5. Score (Sec. 4 metrics).  makespan = last finish - first arrival;
+ *      p95 = nearest-rank 95th percentile (the ceil(0.95 W)-th smallest) of
+ *      per-workflow (last finish - arrival); objective = fp32(w_makespan *
+ *      fp32(makespan)) + fp32(w_p95 * fp32(p95)), each operation rounded to
+ *      nearest even, no fused multiply-add; min_headroom = min over devices
+ *      of (capacity - peak memory).
+ * Times are integer microseconds (int64), memory integer MiB (int32).
+ *
+ * Conventions
+ *   - All functions are C, never throw, and return wf_status (0 = OK).
+ *   - Validation failures return WF_EINVAL and change nothing; the message
+ *     is available from wf_plan_last_error().
+ *   - Plan, score, schedule and index buffers are caller-owned DEVICE
+ *     memory of the context's GPU; they must stay alive until the work
+ *     queued on the given stream has completed.  score_batch and argmin are
+ *     asynchronous on that stream (NULL = the default stream); launch errors
+ *     are reported on return as WF_EHIP.
+ *   - A context is not thread-safe; use one per host thread.  Work queued on
+ *     different streams of one context may run concurrently, but a new
+ *     upload must not race with queued scoring (synchronise first).
+ */
+#ifndef WF_PLAN_H
+#define WF_PLAN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  WF_OK = 0,
+  WF_EINVAL = 1,        /* invalid argument or window                       */
+  WF_ENOWINDOW = 2,     /* score/argmin before a successful upload          */
+  WF_ENOMEM = 3,        /* host or device allocation failed                 */
+  WF_EHIP = 4,          /* HIP runtime error (message has the HIP string)   */
+  WF_EUNSUPPORTED = 5   /* valid but outside this build's limits            */
+} wf_status;
+
+/* Limits of this build. */
+#define WF_MAX_ACT 65535    /* activations per window                     */
+#define WF_MAX_MODELS 64    /* models (resident sets are 64-bit masks)    */
+#define WF_MAX_DEV 64       /* devices in the pool                        */
+#define WF_MAX_MEM_MIB (1 << 28)   /* per weight / activation memory entry */
+#define WF_MAX_CAP_MIB (1 << 30)   /* per device capacity                   */
+#define WF_MAX_TIME_US (1LL << 62) /* arrivals and initial free times        */
+
+/* Plan status bits; a plan is feasible iff status == 0. */
+enum { WF_ST_INELIGIBLE = 1u, WF_ST_CAPACITY = 2u };
+
+typedef struct wf_plan_ctx wf_plan_ctx; /* opaque; owns the device copy of a window */
+
+/*
+ * A planning window (Sec. 3.2) with its snapshot (S_t) and prediction table
+ * (Eq. 1).  Host pointers, read during upload only (deep-copied).
+ * Activations must be numbered in non-decreasing topological level (level 0
+ * = no predecessor, else 1 + deepest predecessor).  Tables are row-major.
+ */
+typedef struct {
+  int32_t n_act;                  /* N, 0..WF_MAX_ACT                          */
+  int32_t n_wf;                   /* W >= 1 when N > 0; every workflow owns an activation */
+  int32_t n_models;               /* M, 1..WF_MAX_MODELS                       */
+  int32_t n_dev;                  /* D, 1..WF_MAX_DEV                          */
+  const int32_t *act_wf;          /* [N] workflow id in [0, W)                 */
+  const int32_t *act_model;       /* [N] model (deployment identity) in [0, M) */
+  const int32_t *pred_off;        /* [N+1] CSR offsets, pred_off[0] = 0        */
+  const int32_t *pred_idx;        /* [pred_off[N]] strictly increasing per row, each < its row */
+  const int32_t *lat_us;          /* [N*D] predicted run time; -1 = ineligible (Eq. 8 cut) */
+  const int32_t *mem_mib;         /* [N*D] activation memory M^inc (Eq. 11), 0..WF_MAX_MEM_MIB */
+  const int64_t *wf_arrival_us;   /* [W] 0..WF_MAX_TIME_US                     */
+  const int32_t *dev_cap_mib;     /* [D] 0..WF_MAX_CAP_MIB                     */
+  const int32_t *model_mib;       /* [M] weights, 0..WF_MAX_MEM_MIB            */
+  const int32_t *load_us;         /* [M*D] load time of model m on device d, >= 0 */
+  const uint64_t *init_resident;  /* [D] resident-model bitmask; must fit the capacity */
+  const int64_t *dev_free0_us;    /* [D] busy-until time, or NULL for all 0    */
+  float w_makespan, w_p95;        /* objective weights, finite and >= 0        */
+} wf_window_desc;
+
+/* Per-plan score, 32 bytes.  For a WF_ST_INELIGIBLE plan every other field
+ * is 0. */
+typedef struct {
+  int64_t makespan_us;
+  int64_t p95_us;
+  float objective;
+  uint32_t status;
+  int32_t min_headroom_mib;
+  uint16_t n_loads;   /* saturates at 65535 */
+  uint16_t n_evicts;  /* saturates at 65535 */
+} wf_plan_score;
+
+/* Optional schedule output (device pointers, row-major per plan).  Rows of
+ * WF_ST_INELIGIBLE plans are unspecified. */
+typedef struct {
+  int64_t *start_us;       /* [P][N] start of each activation                 */
+  int64_t *finish_us;      /* [P][N] finish of each activation                */
+  int64_t *load_start_us;  /* [P][N] load start of a unit head, -1 otherwise  */
+  int32_t *peak_mib;       /* [P][D] peak memory of each device               */
+} wf_plan_sched;
+
+/* Create a context on HIP device `hip_device`.  On failure *out is NULL and
+ * wf_plan_last_error(NULL) describes the error. */
+wf_status wf_plan_ctx_create(int hip_device, wf_plan_ctx **out);
+
+/* Free the context and its device tables (NULL is a no-op).  Work queued on
+ * the context must have completed. */
+void wf_plan_ctx_destroy(wf_plan_ctx *ctx);
+
+/* Message of the last failed call on `ctx` (or of the last failed
+ * wf_plan_ctx_create / validation of this thread when ctx is NULL); "" if
+ * none.  Valid until the next call on the context. */
+const char *wf_plan_last_error(const wf_plan_ctx *ctx);
+
+/* Host-only check of a window (no GPU needed): WF_OK or WF_EINVAL /
+ * WF_EUNSUPPORTED with a message copied into err (NUL-terminated, may be
+ * NULL). */
+wf_status wf_plan_validate_window(const wf_window_desc *w, char *err, size_t err_len);
+
+/* Validate the window, derive its structure (levels, Eq. 3 fusibility,
+ * unique successors) and copy it to the device, replacing any previous
+ * window.  Synchronous. */
+wf_status wf_plan_upload_window(wf_plan_ctx *ctx, const wf_window_desc *w);
+
+/* Score plans 0..n_plans-1.  dev [P][N] int8 device per activation; prio
+ * [P][N] uint16 priority; flags [P][ceil(N/4)] where activation i owns bit
+ * 2*(i%4) (fuse) and bit 2*(i%4)+1 (prefetch) of byte i/4 (padding bits are
+ * ignored).  Out-of-range devices make a plan WF_ST_INELIGIBLE.  scores
+ * [P]; sched may be NULL (scores only).  n_plans = 0 is a no-op. */
+wf_status wf_plan_score_batch(wf_plan_ctx *ctx, const int8_t *dev, const uint16_t *prio,
+                              const uint8_t *flags, int64_t n_plans, wf_plan_score *scores,
+                              const wf_plan_sched *sched, void *hip_stream);
+
+/* Among plans with status 0, the index of the smallest objective (lowest
+ * index on ties), or -1 if none is feasible, written to the device int64
+ * *out_index.  n_plans must be < 2^32; n_plans = 0 writes -1. */
+wf_status wf_plan_argmin(wf_plan_ctx *ctx, const wf_plan_score *scores, int64_t n_plans,
+                         int64_t *out_index, void *hip_stream);
+
+/* Library version string. */
+const char *wf_plan_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* WF_PLAN_H */

@@ -1,0 +1,206 @@
+"""ctypes binding of libwfplan.so.  Function names follow include/wf_plan.h;
+this module only marshals arguments (host arrays for the window, device
+pointers and a HIP stream for the plan batch).  Every step of scoring runs in
+the gfx950 kernels; there is no CPU fallback: if the library is missing or
+no GPU is present, calls raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libwfplan.so")
+
+WF_OK, WF_EINVAL, WF_ENOWINDOW, WF_ENOMEM, WF_EHIP, WF_EUNSUPPORTED = range(6)
+STATUS_NAMES = {0: "WF_OK", 1: "WF_EINVAL", 2: "WF_ENOWINDOW", 3: "WF_ENOMEM", 4: "WF_EHIP",
+                5: "WF_EUNSUPPORTED"}
+WF_ST_INELIGIBLE = 1
+WF_ST_CAPACITY = 2
+WF_MAX_ACT, WF_MAX_MODELS, WF_MAX_DEV = 65535, 64, 64
+
+SCORE_DTYPE = np.dtype([
+    ("makespan_us", "<i8"), ("p95_us", "<i8"), ("objective", "<f4"),
+    ("status", "<u4"), ("min_headroom_mib", "<i4"), ("n_loads", "<u2"),
+    ("n_evicts", "<u2"),
+])
+assert SCORE_DTYPE.itemsize == 32
+
+# every symbol declared in include/wf_plan.h
+EXPORTS = ("wf_plan_ctx_create", "wf_plan_ctx_destroy", "wf_plan_last_error",
+           "wf_plan_validate_window", "wf_plan_upload_window", "wf_plan_score_batch",
+           "wf_plan_argmin", "wf_plan_version")
+
+
+class WFError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {message}")
+        self.status = status
+        self.message = message
+
+
+class wf_window_desc(ctypes.Structure):
+    _fields_ = [
+        ("n_act", ctypes.c_int32), ("n_wf", ctypes.c_int32),
+        ("n_models", ctypes.c_int32), ("n_dev", ctypes.c_int32),
+        ("act_wf", ctypes.c_void_p), ("act_model", ctypes.c_void_p),
+        ("pred_off", ctypes.c_void_p), ("pred_idx", ctypes.c_void_p),
+        ("lat_us", ctypes.c_void_p), ("mem_mib", ctypes.c_void_p),
+        ("wf_arrival_us", ctypes.c_void_p), ("dev_cap_mib", ctypes.c_void_p),
+        ("model_mib", ctypes.c_void_p), ("load_us", ctypes.c_void_p),
+        ("init_resident", ctypes.c_void_p), ("dev_free0_us", ctypes.c_void_p),
+        ("w_makespan", ctypes.c_float), ("w_p95", ctypes.c_float),
+    ]
+
+
+class wf_plan_sched(ctypes.Structure):
+    _fields_ = [("start_us", ctypes.c_void_p), ("finish_us", ctypes.c_void_p),
+                ("load_start_us", ctypes.c_void_p), ("peak_mib", ctypes.c_void_p)]
+
+
+_lib = None
+
+
+def load(path: Optional[str] = None) -> ctypes.CDLL:
+    """Load libwfplan.so; raises if it has not been built."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    p = path or LIB_PATH
+    if not os.path.exists(p):
+        raise RuntimeError(f"{p} is missing: build the gfx950 library first "
+                           "(python -c 'import __graft_entry__ as g; g.build()')")
+    lib = ctypes.CDLL(p)
+    vp, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
+    lib.wf_plan_ctx_create.argtypes = [i32, ctypes.POINTER(vp)]
+    lib.wf_plan_ctx_create.restype = i32
+    lib.wf_plan_ctx_destroy.argtypes = [vp]
+    lib.wf_plan_ctx_destroy.restype = None
+    lib.wf_plan_last_error.argtypes = [vp]
+    lib.wf_plan_last_error.restype = ctypes.c_char_p
+    lib.wf_plan_validate_window.argtypes = [vp, ctypes.c_char_p, ctypes.c_size_t]
+    lib.wf_plan_validate_window.restype = i32
+    lib.wf_plan_upload_window.argtypes = [vp, vp]
+    lib.wf_plan_upload_window.restype = i32
+    lib.wf_plan_score_batch.argtypes = [vp, vp, vp, vp, i64, vp, vp, vp]
+    lib.wf_plan_score_batch.restype = i32
+    lib.wf_plan_argmin.argtypes = [vp, vp, i64, vp, vp]
+    lib.wf_plan_argmin.restype = i32
+    lib.wf_plan_version.argtypes = []
+    lib.wf_plan_version.restype = ctypes.c_char_p
+    if path is None:
+        _lib = lib
+    return lib
+
+
+class _Desc:
+    """A wf_window_desc plus the contiguous host arrays it points at."""
+
+    def __init__(self, win):
+        def c(a, dt):
+            a = np.ascontiguousarray(a, dtype=dt)
+            return a if a.size else np.zeros(1, dtype=dt)
+        self.keep = dict(
+            act_wf=c(win.act_wf, np.int32), act_model=c(win.act_model, np.int32),
+            pred_off=c(win.pred_off, np.int32), pred_idx=c(win.pred_idx, np.int32),
+            lat_us=c(win.lat_us, np.int32), mem_mib=c(win.mem_mib, np.int32),
+            wf_arrival_us=c(win.wf_arrival_us, np.int64), dev_cap_mib=c(win.dev_cap_mib, np.int32),
+            model_mib=c(win.model_mib, np.int32), load_us=c(win.load_us, np.int32),
+            init_resident=c(win.init_resident, np.uint64))
+        free0 = getattr(win, "dev_free0_us", None)
+        self.keep["dev_free0_us"] = None if free0 is None else c(free0, np.int64)
+        d = wf_window_desc()
+        d.n_act, d.n_wf, d.n_models, d.n_dev = win.n_act, win.n_wf, win.n_models, win.n_dev
+        for k, v in self.keep.items():
+            setattr(d, k, None if v is None else v.ctypes.data)
+        d.w_makespan, d.w_p95 = win.w_makespan, win.w_p95
+        self.desc = d
+
+
+def _ptr(x) -> Optional[int]:
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return int(x.data_ptr())
+
+
+def wf_plan_version() -> str:
+    return load().wf_plan_version().decode()
+
+
+def wf_plan_validate_window(win) -> tuple:
+    """Host-only validation: (status, message)."""
+    lib = load()
+    d = _Desc(win)
+    buf = ctypes.create_string_buffer(512)
+    st = lib.wf_plan_validate_window(ctypes.byref(d.desc), buf, len(buf))
+    return st, buf.value.decode()
+
+
+class Context:
+    """A wf_plan_ctx on one HIP device."""
+
+    def __init__(self, device: int = 0):
+        self.lib = load()
+        h = ctypes.c_void_p()
+        st = self.lib.wf_plan_ctx_create(device, ctypes.byref(h))
+        if st != WF_OK:
+            raise WFError(st, self.lib.wf_plan_last_error(None).decode())
+        self.handle = h
+        self.device = device
+
+    def _check(self, st):
+        if st != WF_OK:
+            raise WFError(st, self.lib.wf_plan_last_error(self.handle).decode())
+
+    def wf_plan_upload_window(self, win) -> None:
+        d = _Desc(win)
+        self._check(self.lib.wf_plan_upload_window(self.handle, ctypes.byref(d.desc)))
+
+    def wf_plan_score_batch(self, dev, prio, flags, n_plans: int, scores, sched=None,
+                            stream=None) -> None:
+        """dev/prio/flags/scores (and the four schedule arrays) are device
+        buffers: torch tensors or raw device addresses."""
+        s = None
+        if sched is not None:
+            s = wf_plan_sched(*(_ptr(x) for x in sched))
+        self._check(self.lib.wf_plan_score_batch(
+            self.handle, _ptr(dev), _ptr(prio), _ptr(flags), int(n_plans), _ptr(scores),
+            None if s is None else ctypes.byref(s), _stream(stream)))
+
+    def wf_plan_argmin(self, scores, n_plans: int, out_index, stream=None) -> None:
+        self._check(self.lib.wf_plan_argmin(self.handle, _ptr(scores), int(n_plans),
+                                            _ptr(out_index), _stream(stream)))
+
+    def close(self):
+        if getattr(self, "handle", None):
+            self.lib.wf_plan_ctx_destroy(self.handle)
+            self.handle = None
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        try:
+            import torch
+            return int(torch.cuda.current_stream().cuda_stream) or None
+        except Exception:
+            return None
+    if isinstance(stream, int):
+        return stream or None
+    return int(stream.cuda_stream) or None

@@ -1,0 +1,146 @@
+"""Host-side checks of the C ABI that need no GPU: the library loads, it
+exports every function include/wf_plan.h declares, the score record has the
+declared layout, and window validation rejects what it should."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2609_03335_amd as pkg
+from paper_2609_03335_amd import _lib, workload as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "wf_plan.h")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def built():
+    if not os.path.exists(_lib.LIB_PATH):
+        from paper_2609_03335_amd import build
+        build.build()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(wf_plan_\w+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol():
+    lib = ctypes.CDLL(_lib.LIB_PATH)
+    names = declared_functions()
+    assert set(names) == set(_lib.EXPORTS)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert pkg.wf_plan_version().startswith("wf_plan")
+
+
+def test_score_record_layout():
+    text = open(HEADER).read()
+    assert "int64_t makespan_us;" in text and "uint16_t n_evicts;" in text
+    assert pkg.SCORE_DTYPE.itemsize == 32
+    assert [pkg.SCORE_DTYPE.fields[k][1] for k in pkg.SCORE_DTYPE.names] == [0, 8, 16, 20, 24, 28, 30]
+
+
+def test_no_gpu_context_fails_cleanly():
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present")
+    with pytest.raises(pkg.WFError) as e:
+        pkg.Context(0)
+    assert e.value.status == pkg.WF_EHIP
+
+
+def _ok_window():
+    return W.make_window(0)
+
+
+def test_valid_windows_pass():
+    for cfg in range(5):
+        st, msg = pkg.wf_plan_validate_window(W.make_window(cfg))
+        assert st == pkg.WF_OK, msg
+    rng = np.random.default_rng(0)
+    for _ in range(20):
+        st, msg = pkg.wf_plan_validate_window(W.random_window(rng))
+        assert st == pkg.WF_OK, msg
+
+
+def _mutate(fn):
+    w = _ok_window()
+    w2 = W.Window(**{k: (v.copy() if isinstance(v, np.ndarray) else v) for k, v in w.arrays().items()})
+    fn(w2)
+    return w2
+
+
+BAD = {
+    "n_models_zero": lambda w: setattr(w, "n_models", 0),
+    "n_models_65": lambda w: setattr(w, "n_models", 65),
+    "n_dev_65": lambda w: setattr(w, "n_dev", 65),
+    "n_wf_zero": lambda w: setattr(w, "n_wf", 0),
+    "pred_self_loop": lambda w: w.pred_idx.__setitem__(0, int(np.nonzero(np.diff(w.pred_off))[0][0])),
+    "pred_off_nonzero_start": lambda w: w.pred_off.__setitem__(0, 1),
+    "model_out_of_range": lambda w: w.act_model.__setitem__(0, w.n_models),
+    "wf_out_of_range": lambda w: w.act_wf.__setitem__(0, -1),
+    "latency_below_minus_one": lambda w: w.lat_us.__setitem__(0, -2),
+    "negative_memory": lambda w: w.mem_mib.__setitem__(0, -5),
+    "huge_memory": lambda w: w.mem_mib.__setitem__(0, (1 << 28) + 1),
+    "negative_arrival": lambda w: w.wf_arrival_us.__setitem__(0, -1),
+    "negative_load": lambda w: w.load_us.__setitem__(0, -1),
+    "cap_too_big": lambda w: w.dev_cap_mib.__setitem__(0, (1 << 30) + 1),
+    "resident_unknown_model": lambda w: w.init_resident.__setitem__(0, np.uint64(1 << 10)),
+    "resident_over_capacity": lambda w: (w.model_mib.__setitem__(0, 30000),
+                                         w.init_resident.__setitem__(0, np.uint64(1))),
+    "negative_weight": lambda w: setattr(w, "w_p95", -0.5),
+    "nan_weight": lambda w: setattr(w, "w_makespan", float("nan")),
+    "empty_workflow": lambda w: (setattr(w, "n_wf", 3), setattr(w, "wf_arrival_us", np.zeros(3, np.int64))),
+    "negative_free0": lambda w: w.dev_free0_us.__setitem__(0, -3),
+}
+
+
+@pytest.mark.parametrize("name", sorted(BAD))
+def test_invalid_windows_rejected(name):
+    w = _mutate(BAD[name])
+    st, msg = pkg.wf_plan_validate_window(w)
+    assert st == pkg.WF_EINVAL and msg, (name, st, msg)
+
+
+def test_not_level_sorted_rejected():
+    # activation 1 depends on 0 (level 1); activation 2 is a source (level 0)
+    w = W.Window(n_act=3, n_wf=1, n_models=1, n_dev=1, act_wf=np.zeros(3, np.int32),
+                 act_model=np.zeros(3, np.int32), pred_off=np.array([0, 0, 1, 1], np.int32),
+                 pred_idx=np.array([0], np.int32), lat_us=np.ones(3, np.int32),
+                 mem_mib=np.ones(3, np.int32), wf_arrival_us=np.zeros(1, np.int64),
+                 dev_cap_mib=np.array([100], np.int32), model_mib=np.array([10], np.int32),
+                 load_us=np.array([5], np.int32), init_resident=np.zeros(1, np.uint64),
+                 dev_free0_us=np.zeros(1, np.int64))
+    st, msg = pkg.wf_plan_validate_window(w)
+    assert st == pkg.WF_EINVAL and "level" in msg
+    w.pred_off = np.array([0, 0, 0, 1], np.int32)  # 2 depends on 0: sorted
+    assert pkg.wf_plan_validate_window(w)[0] == pkg.WF_OK
+
+
+def test_duplicate_predecessor_rejected():
+    w = W.make_window(1)
+    row = int(np.nonzero(np.diff(w.pred_off) >= 2)[0][0])
+    w.pred_idx = w.pred_idx.copy()
+    w.pred_idx[w.pred_off[row] + 1] = w.pred_idx[w.pred_off[row]]
+    st, msg = pkg.wf_plan_validate_window(w)
+    assert st == pkg.WF_EINVAL and "increasing" in msg
+
+
+def test_empty_window_is_valid():
+    w = W.Window(n_act=0, n_wf=0, n_models=1, n_dev=1, act_wf=np.zeros(0, np.int32),
+                 act_model=np.zeros(0, np.int32), pred_off=np.zeros(1, np.int32),
+                 pred_idx=np.zeros(0, np.int32), lat_us=np.zeros(0, np.int32),
+                 mem_mib=np.zeros(0, np.int32), wf_arrival_us=np.zeros(0, np.int64),
+                 dev_cap_mib=np.array([10], np.int32), model_mib=np.array([1], np.int32),
+                 load_us=np.zeros(1, np.int32), init_resident=np.zeros(1, np.uint64),
+                 dev_free0_us=np.zeros(1, np.int64))
+    assert pkg.wf_plan_validate_window(w)[0] == pkg.WF_OK
+
+
+def test_binding_fails_loudly_without_library(tmp_path):
+    with pytest.raises(RuntimeError):
+        _lib.load(str(tmp_path / "missing.so"))

@@ -1,0 +1,237 @@
+"""GPU path (libwfplan.so, gfx950) against the CPU oracle, element by element.
+
+Bar: integer outputs (times, peaks, status, counts, argmin) bit-exact; the
+fp32 objective within 1e-5 relative (the arithmetic is designed to be
+identical, so a separate test also demands bitwise equality).
+"""
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_03335_amd as pkg
+from paper_2609_03335_amd import workload as W
+from enumerate_plans import best_plan, enumerate_plans, tiny_window
+
+pytestmark = pytest.mark.gpu
+OBJ_RTOL = 1e-5
+THREADS = max(1, min(16, os.cpu_count() or 1))
+
+
+def log(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def ctx():
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+    c = pkg.Context(0)
+    yield c
+    c.close()
+
+
+def gpu_score(ctx, win, plans, schedule=False, stream=None):
+    ctx.wf_plan_upload_window(win)
+    P = plans.n_plans
+    dev, prio, flags = pkg.device_plans(plans, "cuda:0")
+    out = pkg.score_batch(ctx, dev, prio, flags, P, schedule=schedule, n_act=win.n_act,
+                          n_dev=win.n_dev, stream=stream)
+    scores, sched = out if schedule else (out, None)
+    best = pkg.argmin(ctx, scores, P, stream=stream)
+    torch.cuda.synchronize()
+    got = pkg.scores_to_numpy(scores, P)
+    if sched is not None:
+        sched = tuple(x.cpu().numpy() for x in sched)
+    return got, sched, int(best.item())
+
+
+def assert_scores(got, ref, where=""):
+    assert got.shape == ref.shape
+    bad = np.nonzero(got["status"] != ref["status"])[0]
+    assert len(bad) == 0, f"{where}: status differs at plans {bad[:10]}"
+    for k in ("makespan_us", "p95_us", "min_headroom_mib", "n_loads", "n_evicts"):
+        bad = np.nonzero(got[k] != ref[k])[0]
+        assert len(bad) == 0, f"{where}: {k} differs at plans {bad[:10]}: {got[k][bad[:3]]} vs {ref[k][bad[:3]]}"
+    g, r = got["objective"].astype(np.float64), ref["objective"].astype(np.float64)
+    rel = np.abs(g - r) / np.maximum(np.abs(r), 1e-30)
+    assert (rel <= OBJ_RTOL).all(), f"{where}: objective rel err {rel.max()}"
+
+
+def assert_sched(got_s, ref_s, status, where=""):
+    ok = status & pkg.WF_ST_INELIGIBLE == 0
+    for name, a, b in zip(("start", "finish", "load_start", "peak"), got_s, ref_s):
+        a = a[ok][:, :b.shape[1]] if b.shape[1] else a[ok][:, :0]
+        bad = np.nonzero((a != b[ok]).any(axis=1))[0]
+        assert len(bad) == 0, f"{where}: {name} differs for plans {np.nonzero(ok)[0][bad[:10]]}"
+
+
+@pytest.mark.parametrize("cfg", [0, 1, 2, 3])
+def test_config_full_parity(ctx, cfg):
+    win, plans = W.make_config(cfg)
+    log(f"[parity] config {cfg}: N={win.n_act} D={win.n_dev} P={plans.n_plans}")
+    got, _, best = gpu_score(ctx, win, plans)
+    ref = oracle.score(win, plans, threads=THREADS)
+    assert_scores(got, ref, f"config {cfg}")
+    assert best == best_plan(ref)
+    assert got.tobytes() == ref.tobytes(), "score records not bitwise equal"
+
+
+@pytest.mark.parametrize("cfg,count", [(0, 512), (1, 1024), (2, 256), (3, 64), (4, 2048)])
+def test_config_schedule_parity(ctx, cfg, count):
+    win, plans = W.make_config(cfg, n_plans=count)
+    log(f"[sched] config {cfg}: P={count}")
+    got, gs, _ = gpu_score(ctx, win, plans, schedule=True)
+    ref, rs = oracle.score(win, plans, schedule=True, threads=THREADS)
+    assert_scores(got, ref, f"config {cfg}")
+    assert_sched(gs, rs, ref["status"], f"config {cfg}")
+
+
+def test_config4_full_size(ctx):
+    """The throughput configuration at full size (1,048,576 plans) in the
+    launch configuration the benchmark times; every plan checked."""
+    win, plans = W.make_config(4)
+    log(f"[parity] config 4 full: P={plans.n_plans}")
+    got, _, best = gpu_score(ctx, win, plans)
+    ref = oracle.score(win, plans, threads=THREADS)
+    assert_scores(got, ref, "config 4")
+    assert got.tobytes() == ref.tobytes()
+    assert best == best_plan(ref)
+
+
+@pytest.mark.parametrize("seed", range(60))
+def test_random_windows(ctx, seed):
+    rng = np.random.default_rng(10_000 + seed)
+    kind = seed % 4
+    if kind == 0:
+        win = W.random_window(rng, n_wf=int(rng.integers(1, 5)), nodes=(1, 9),
+                              n_dev=int(rng.integers(1, 5)), n_models=int(rng.integers(1, 7)))
+    elif kind == 1:  # tight memory: reclamation every step, over-capacity plans
+        win = W.random_window(rng, n_wf=3, nodes=(2, 8), n_dev=2, n_models=5,
+                              cap_range=(2500, 12000), w_range=(2000, 9000))
+    elif kind == 2:  # wide levels (several 64-bit mask words) and many workflows
+        win = W.random_window(rng, n_wf=int(rng.integers(20, 60)), nodes=(3, 6), n_dev=3,
+                              n_models=8, p_edge=0.3)
+    else:  # long same-model chains (fusion) and big device count
+        win = W.random_window(rng, n_wf=4, nodes=(4, 12), n_dev=int(rng.integers(5, 17)),
+                              n_models=3, same_model_bias=0.9, p_edge=0.25)
+    plans = W.random_plans(win, int(rng.integers(1, 200)), rng,
+                           p_bad_dev=[0.0, 0.01, 0.0, 0.002][kind],
+                           prio_mode=["any", "perm", "globalperm", "any"][seed % 3])
+    log(f"[random] seed {seed}: N={win.n_act} W={win.n_wf} D={win.n_dev} P={plans.n_plans}")
+    got, gs, best = gpu_score(ctx, win, plans, schedule=True)
+    ref, rs = oracle.score(win, plans, schedule=True)
+    assert_scores(got, ref, f"seed {seed}")
+    assert_sched(gs, rs, ref["status"], f"seed {seed}")
+    assert best == best_plan(ref)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_exhaustive_argmin(ctx, seed):
+    win = tiny_window(seed)
+    plans = enumerate_plans(win)
+    got, _, best = gpu_score(ctx, win, plans)
+    ref = oracle.score(win, plans)
+    assert_scores(got, ref, f"tiny {seed}")
+    assert best == best_plan(ref) and best >= 0
+
+
+@pytest.mark.parametrize("P", [1, 2, 7, 63, 65, 129, 1001])
+def test_ragged_batches(ctx, P):
+    win, plans = W.make_config(1, n_plans=P)
+    got, _, best = gpu_score(ctx, win, plans)
+    ref = oracle.score(win, plans)
+    assert got.tobytes() == ref.tobytes()
+    assert best == best_plan(ref)
+
+
+def test_empty_batch_and_no_feasible_plan(ctx):
+    win, plans = W.make_config(0, n_plans=4)
+    ctx.wf_plan_upload_window(win)
+    dev, prio, flags = pkg.device_plans(plans, "cuda:0")
+    scores = torch.zeros((1, 32), dtype=torch.uint8, device="cuda:0")
+    ctx.wf_plan_score_batch(dev, prio, flags, 0, scores)
+    best = pkg.argmin(ctx, scores, 0)
+    torch.cuda.synchronize()
+    assert int(best.item()) == -1
+    # every plan ineligible -> argmin -1
+    bad = W.PlanBatch(np.full_like(plans.dev, -1), plans.prio, plans.flags)
+    got, _, best = gpu_score(ctx, win, bad)
+    assert (got["status"] == pkg.WF_ST_INELIGIBLE).all() and best == -1
+
+
+def test_empty_window(ctx):
+    win = W.Window(n_act=0, n_wf=0, n_models=2, n_dev=3, act_wf=np.zeros(0, np.int32),
+                   act_model=np.zeros(0, np.int32), pred_off=np.zeros(1, np.int32),
+                   pred_idx=np.zeros(0, np.int32), lat_us=np.zeros(0, np.int32),
+                   mem_mib=np.zeros(0, np.int32), wf_arrival_us=np.zeros(0, np.int64),
+                   dev_cap_mib=np.array([100, 50, 70], np.int32), model_mib=np.array([30, 20], np.int32),
+                   load_us=np.zeros(6, np.int32), init_resident=np.array([3, 0, 2], np.uint64),
+                   dev_free0_us=np.zeros(3, np.int64))
+    plans = W.PlanBatch(np.zeros((5, 0), np.int8), np.zeros((5, 0), np.uint16), np.zeros((5, 0), np.uint8))
+    got, _, best = gpu_score(ctx, win, plans)
+    ref = oracle.score(win, plans)
+    assert got.tobytes() == ref.tobytes() and best == 0
+
+
+def test_device_and_model_limits(ctx):
+    """64 devices (one plan per wave) and 64 models (full 64-bit masks)."""
+    rng = np.random.default_rng(77)
+    win = W.random_window(rng, n_wf=6, nodes=(3, 8), n_dev=64, n_models=64,
+                          cap_range=(8000, 20000))
+    plans = W.random_plans(win, 50, rng)
+    got, gs, best = gpu_score(ctx, win, plans, schedule=True)
+    ref, rs = oracle.score(win, plans, schedule=True)
+    assert_scores(got, ref, "limits")
+    assert_sched(gs, rs, ref["status"], "limits")
+
+
+def test_large_window_global_scratch(ctx):
+    """A window whose per-plan finish times do not fit in LDS."""
+    rng = np.random.default_rng(5)
+    win = W.random_window(rng, n_wf=400, nodes=(40, 60), n_dev=4, n_models=8, p_edge=0.1)
+    assert win.n_act > 16000
+    plans = W.random_plans(win, 24, rng, prio_mode="perm")
+    log(f"[big] N={win.n_act} widest level present")
+    got, _, best = gpu_score(ctx, win, plans)
+    ref = oracle.score(win, plans)
+    assert_scores(got, ref, "big")
+
+
+def test_nondefault_stream(ctx):
+    win, plans = W.make_config(1, n_plans=300)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        got, _, best = gpu_score(ctx, win, plans, stream=s)
+    ref = oracle.score(win, plans)
+    assert got.tobytes() == ref.tobytes()
+
+
+def test_abi_errors_on_gpu(ctx):
+    fresh = pkg.Context(0)
+    win, plans = W.make_config(0, n_plans=8)
+    dev, prio, flags = pkg.device_plans(plans, "cuda:0")
+    scores = torch.zeros((8, 32), dtype=torch.uint8, device="cuda:0")
+    with pytest.raises(pkg.WFError) as e:
+        fresh.wf_plan_score_batch(dev, prio, flags, 8, scores)
+    assert e.value.status == pkg.WF_ENOWINDOW
+    fresh.wf_plan_upload_window(win)
+    bad = W.Window(**{k: (v.copy() if isinstance(v, np.ndarray) else v) for k, v in win.arrays().items()})
+    bad.act_model[0] = 99
+    with pytest.raises(pkg.WFError) as e:
+        fresh.wf_plan_upload_window(bad)
+    assert e.value.status == pkg.WF_EINVAL and "model" in e.value.message
+    # the previous window is still in place
+    fresh.wf_plan_score_batch(dev, prio, flags, 8, scores)
+    torch.cuda.synchronize()
+    assert pkg.scores_to_numpy(scores, 8).tobytes() == oracle.score(win, plans).tobytes()
+    with pytest.raises(pkg.WFError) as e:
+        fresh.wf_plan_score_batch(dev, prio, flags, 8, None)
+    assert e.value.status == pkg.WF_EINVAL
+    with pytest.raises(pkg.WFError) as e:
+        fresh.wf_plan_argmin(scores, 1 << 32, scores)
+    assert e.value.status == pkg.WF_EINVAL
+    fresh.close()
