@@ -20,11 +20,13 @@ __all__ = [
 
 def device_plans(plans, device="cuda"):
     """Copy a host PlanBatch (workload.PlanBatch) to device tensors."""
+    import numpy as np
     import torch
     n = plans.dev.shape[1]
-    dev = torch.from_numpy(plans.dev).to(device)
-    prio = torch.from_numpy(plans.prio.view("<i2")).to(device)
-    flags = torch.from_numpy(plans.flags).to(device)
+    # the kernels read row-major [P][N] buffers: force C order on both sides
+    dev = torch.from_numpy(np.ascontiguousarray(plans.dev)).to(device).contiguous()
+    prio = torch.from_numpy(np.ascontiguousarray(plans.prio).view("<i2")).to(device).contiguous()
+    flags = torch.from_numpy(np.ascontiguousarray(plans.flags)).to(device).contiguous()
     if n == 0:  # keep a valid (unused) allocation behind empty rows
         dev = torch.zeros((plans.dev.shape[0], 1), dtype=torch.int8, device=device)
         prio = torch.zeros((plans.dev.shape[0], 1), dtype=torch.int16, device=device)

@@ -121,10 +121,14 @@ class _Desc:
 
 
 def _ptr(x) -> Optional[int]:
+    """Device address of a buffer; tensors must be dense row-major (the ABI
+    takes flat row-major arrays)."""
     if x is None:
         return None
     if isinstance(x, int):
         return x
+    if hasattr(x, "is_contiguous") and not x.is_contiguous():
+        raise ValueError("device buffers must be contiguous row-major tensors")
     return int(x.data_ptr())
 
 

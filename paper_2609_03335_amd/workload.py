@@ -516,7 +516,8 @@ def random_plans(win: Window, n_plans: int, rng: np.random.Generator,
         raise ValueError(prio_mode)
     fuse = rng.random((n_plans, n)) < p_fuse
     pf = rng.random((n_plans, n)) < p_prefetch
-    return PlanBatch(dev, prio, pack_flags(fuse, pf))
+    return PlanBatch(np.ascontiguousarray(dev), np.ascontiguousarray(prio, dtype=np.uint16),
+                     np.ascontiguousarray(pack_flags(fuse, pf)))
 
 
 # --------------------------------------------------------------------------

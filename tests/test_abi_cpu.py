@@ -144,3 +144,21 @@ def test_empty_window_is_valid():
 def test_binding_fails_loudly_without_library(tmp_path):
     with pytest.raises(RuntimeError):
         _lib.load(str(tmp_path / "missing.so"))
+
+
+def test_device_buffers_are_row_major():
+    """Plan buffers handed to the library are dense row-major even when the
+    host arrays are not (a Fortran-ordered priority array once reached the
+    kernel transposed)."""
+    import torch
+    rng = np.random.default_rng(3)
+    win = W.random_window(rng)
+    plans = W.random_plans(win, 7, rng, prio_mode="globalperm")
+    fortran = W.PlanBatch(np.asfortranarray(plans.dev), np.asfortranarray(plans.prio),
+                          np.asfortranarray(plans.flags))
+    dev, prio, flags = pkg.device_plans(fortran, "cpu")
+    for t, a in ((dev, plans.dev), (prio, plans.prio.view(np.int16)), (flags, plans.flags)):
+        assert t.is_contiguous()
+        assert t.numpy().tobytes() == np.ascontiguousarray(a).tobytes()
+    with pytest.raises(ValueError):
+        _lib._ptr(torch.zeros((4, 3), dtype=torch.int16).t())
