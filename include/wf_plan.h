@@ -80,7 +80,8 @@ typedef enum {
 #define WF_MAX_DEV 64       /* devices in the pool                        */
 #define WF_MAX_MEM_MIB (1 << 28)   /* per weight / activation memory entry */
 #define WF_MAX_CAP_MIB (1 << 30)   /* per device capacity                   */
-#define WF_MAX_TIME_US (1LL << 62) /* arrivals and initial free times        */
+#define WF_MAX_TIME_US (1LL << 52) /* arrivals and initial free times; every
+                                      time then stays below 2^53 (exact in fp64) */
 
 /* Plan status bits; a plan is feasible iff status == 0. */
 enum { WF_ST_INELIGIBLE = 1u, WF_ST_CAPACITY = 2u };

@@ -8,6 +8,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <new>
 #include <string>
@@ -98,7 +99,7 @@ wf_status validate(const wf_window_desc* w, std::string* err, HostWindow* out) {
   for (int64_t f = 0; f < W; ++f) {
     if (!has_act[f]) return fail(err, WF_EINVAL, "workflow %lld has no activation", (long long)f);
     if (w->wf_arrival_us[f] < 0 || w->wf_arrival_us[f] > WF_MAX_TIME_US)
-      return fail(err, WF_EINVAL, "wf_arrival_us[%lld] outside [0, 2^62]", (long long)f);
+      return fail(err, WF_EINVAL, "wf_arrival_us[%lld] outside [0, 2^52]", (long long)f);
   }
   for (int64_t m = 0; m < M; ++m) {
     if (w->model_mib[m] < 0 || w->model_mib[m] > WF_MAX_MEM_MIB)
@@ -111,7 +112,7 @@ wf_status validate(const wf_window_desc* w, std::string* err, HostWindow* out) {
     if (w->dev_cap_mib[d] < 0 || w->dev_cap_mib[d] > WF_MAX_CAP_MIB)
       return fail(err, WF_EINVAL, "dev_cap_mib[%lld] = %d outside [0, %d]", (long long)d, w->dev_cap_mib[d], WF_MAX_CAP_MIB);
     if (w->dev_free0_us && (w->dev_free0_us[d] < 0 || w->dev_free0_us[d] > WF_MAX_TIME_US))
-      return fail(err, WF_EINVAL, "dev_free0_us[%lld] outside [0, 2^62]", (long long)d);
+      return fail(err, WF_EINVAL, "dev_free0_us[%lld] outside [0, 2^52]", (long long)d);
     const uint64_t r = w->init_resident[d];
     if (M < 64 && (r >> M) != 0)
       return fail(err, WF_EINVAL, "init_resident[%lld] names a model >= n_models", (long long)d);
@@ -183,11 +184,9 @@ wf_status validate(const wf_window_desc* w, std::string* err, HostWindow* out) {
 }
 
 struct DeviceWindow {
-  void* blob = nullptr;
-  size_t bytes = 0;
-  wfp::WindowDev view{};
-  wfp::ScoreLaunch launch{};
-  int64_t* scratch = nullptr;  // big-mode finish times and workflow maxima
+  void* tab = nullptr;          // table image in HBM
+  void* scratch = nullptr;      // per-wave regions for windows too big for LDS
+  wfp::ScoreParams sp{};
 };
 
 }  // namespace
@@ -211,64 +210,216 @@ wf_status hip_fail(wf_plan_ctx* ctx, hipError_t e, const char* what) {
 }
 
 void free_device_window(DeviceWindow& dw) {
-  if (dw.blob) (void)hipFree(dw.blob);
+  if (dw.tab) (void)hipFree(dw.tab);
   if (dw.scratch) (void)hipFree(dw.scratch);
   dw = DeviceWindow{};
 }
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-// Carve the scoring kernel's LDS for G plans per wave; returns total bytes.
-int lds_layout(const HostWindow& h, int G, bool big, wfp::ScoreLaunch& L) {
-  size_t off = 0;
-  auto take = [&](size_t bytes) {
-    size_t o = off;
-    off = align_up(off + bytes, 16);
-    return (int)o;
-  };
-  L.G = G;
-  L.big = big ? 1 : 0;
-  L.nwords = std::max(1, (h.wmax + 63) / 64);
-  L.off_pos = take((size_t)G * std::max(1, h.wmax) * 2);
-  L.off_claim = take((size_t)G * L.nwords * 8);
-  L.off_mask = take((size_t)G * h.D * L.nwords * 8);
-  L.off_cnt = take((size_t)G * h.D * h.M * 4);
-  L.off_last = take((size_t)G * h.D * h.M * 4);
-  L.off_acc = take((size_t)G * sizeof(wfp::PlanAcc));
-  if (!big) {
-    L.off_finish = take((size_t)G * std::max(1, h.N) * 8);
-    L.off_wfmax = take((size_t)G * std::max(1, h.W) * 8);
-    L.scratch_per_wave = 0;
-  } else {
-    L.off_finish = L.off_wfmax = 0;
-    L.scratch_per_wave = (int64_t)G * (std::max(1, h.N) + std::max(1, h.W));
+// Append a table to the image; returns its byte offset (16-byte aligned).
+struct Image {
+  std::vector<unsigned char> bytes;
+  int put(const void* p, size_t n) {
+    const size_t off = align_up(bytes.size(), 16);
+    bytes.resize(off + std::max<size_t>(n, 4), 0);
+    if (n) std::memcpy(bytes.data() + off, p, n);
+    return (int)off;
   }
-  L.lds_bytes = (int)off;
-  return L.lds_bytes;
+};
+
+// Per-wave LDS carve-up for G plans; returns the wave's byte size.
+int wave_layout(const HostWindow& h, int G, int tsz, bool nibble, int nwords, wfp::WaveOffsets& o) {
+  size_t off = 0;
+  auto take = [&](size_t n) {
+    const size_t at = off;
+    off = align_up(off + std::max<size_t>(n, 1), 16);
+    return (int)at;
+  };
+  const int NB = (h.N + 3) / 4, MH = (h.M + 1) / 2, wm = std::max(1, h.wmax);
+  o.dev = take((size_t)G * h.N);
+  o.prio = take((size_t)G * h.N * 2);
+  o.flags = take((size_t)G * NB);
+  o.fin = take((size_t)G * h.N * tsz);
+  o.rt = take((size_t)G * wm * tsz);
+  o.rec = take((size_t)G * wm * 16);
+  o.claim = take((size_t)G * nwords * 8);
+  o.mask = take((size_t)G * h.D * nwords * 8);
+  o.cnt = take((size_t)G * h.D * MH * 4);
+  o.last = take(nibble ? 0 : (size_t)G * h.D * h.M * 4);
+  o.wfm = take((size_t)G * std::max(1, h.W) * tsz);
+  o.acc = take((size_t)G * sizeof(wfp::PlanAcc));
+  o.bytes = (int)off;
+  return o.bytes;
 }
 
-wf_status plan_launch(wf_plan_ctx* ctx, const HostWindow& h, wfp::ScoreLaunch& L) {
-  const int gmax = std::max(1, 64 / h.D);
-  for (int pass = 0; pass < 2; ++pass) {
-    const bool big = pass == 1;
+// Build the table image and choose time width, LDS placement, plans per
+// wave and waves per workgroup for this window.
+wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, Image& img, wfp::ScoreParams& sp) {
+  const int N = h.N, D = h.D, M = h.M, W = h.W;
+  // time origin: earliest arrival or device free time
+  int64_t origin = INT64_MAX;
+  for (int32_t f = 0; f < W; ++f) origin = std::min(origin, h.arrival[f]);
+  for (int32_t d = 0; d < D; ++d) origin = std::min(origin, h.free0[d]);
+  if (origin == INT64_MAX) origin = 0;
+  // largest relative time any plan can reach: latest arrival/free time plus
+  // every activation's longest run and its model's longest load, in sequence
+  int64_t t0 = 0;
+  for (int32_t f = 0; f < W; ++f) t0 = std::max(t0, h.arrival[f] - origin);
+  for (int32_t d = 0; d < D; ++d) t0 = std::max(t0, h.free0[d] - origin);
+  int64_t bound = t0;
+  std::vector<int64_t> maxlat((size_t)std::max(N, 1), 0);
+  for (int32_t i = 0; i < N; ++i) {
+    int64_t ml = 0, mload = 0;
+    for (int32_t d = 0; d < D; ++d) {
+      ml = std::max<int64_t>(ml, h.lat[(size_t)i * D + d]);
+      mload = std::max<int64_t>(mload, h.load[(size_t)h.act_model[i] * D + d]);
+    }
+    maxlat[i] = ml;
+    bound += ml + mload;
+  }
+  // a fused chain's summed run time is carried as uint32
+  int64_t chain_max = 0;
+  std::vector<int64_t> csum((size_t)std::max(N, 1), 0);
+  for (int32_t i = N - 1; i >= 0; --i) {
+    csum[i] = maxlat[i] + (h.chain_next[i] >= 0 ? csum[h.chain_next[i]] : 0);
+    chain_max = std::max(chain_max, csum[i]);
+  }
+  if (chain_max >= (int64_t(1) << 32))
+    return fail(&ctx->err, WF_EUNSUPPORTED, "a fusible chain may run for 2^32 us or more");
+  const bool time64 = bound >= (int64_t(1) << 32);
+  const int tsz = time64 ? 8 : 4;
+
+  // ---- table image ----
+  std::vector<uint32_t> act((size_t)std::max(N, 1), 0);
+  std::vector<uint16_t> cnext((size_t)std::max(N, 1), 0xffff);
+  for (int32_t i = 0; i < N; ++i) {
+    act[i] = (uint32_t)h.act_model[i] | ((uint32_t)h.fusible[i] << 6) | ((uint32_t)h.act_wf[i] << 16);
+    cnext[i] = h.chain_next[i] >= 0 ? (uint16_t)h.chain_next[i] : (uint16_t)0xffff;
+  }
+  const int32_t E = N > 0 ? h.pred_off[N] : 0;
+  std::vector<uint32_t> edge((size_t)std::max(E, 1), 0);
+  for (int32_t v = 0; v < N; ++v)
+    for (int32_t k = h.pred_off[v]; k < h.pred_off[v + 1]; ++k)
+      edge[k] = (uint32_t)h.pred_idx[k] | ((uint32_t)v << 16);
+  std::vector<int32_t> eoff((size_t)h.n_levels + 1);
+  for (int32_t l = 0; l <= h.n_levels; ++l) eoff[l] = N > 0 ? h.pred_off[h.level_off[l]] : 0;
+  // activation memory: one value per activation when it is the same on every device
+  bool mem_uniform = true;
+  for (int32_t i = 0; i < N && mem_uniform; ++i)
+    for (int32_t d = 1; d < D; ++d)
+      if (h.mem[(size_t)i * D + d] != h.mem[(size_t)i * D]) {
+        mem_uniform = false;
+        break;
+      }
+  std::vector<int32_t> mem1;
+  if (mem_uniform) {
+    mem1.resize((size_t)std::max(N, 1), 0);
+    for (int32_t i = 0; i < N; ++i) mem1[i] = h.mem[(size_t)i * D];
+  }
+  std::vector<unsigned char> arr((size_t)std::max(W, 1) * tsz, 0), fr((size_t)D * tsz, 0);
+  for (int32_t f = 0; f < W; ++f) {
+    const int64_t r = h.arrival[f] - origin;
+    if (time64) { const double x = (double)r; std::memcpy(&arr[(size_t)f * 8], &x, 8); }
+    else { const uint32_t x = (uint32_t)r; std::memcpy(&arr[(size_t)f * 4], &x, 4); }
+  }
+  for (int32_t d = 0; d < D; ++d) {
+    const int64_t r = h.free0[d] - origin;
+    if (time64) { const double x = (double)r; std::memcpy(&fr[(size_t)d * 8], &x, 8); }
+    else { const uint32_t x = (uint32_t)r; std::memcpy(&fr[(size_t)d * 4], &x, 4); }
+  }
+  wfp::TabOffsets& t = sp.t;
+  t.act = img.put(act.data(), act.size() * 4);
+  t.cnext = img.put(cnext.data(), cnext.size() * 2);
+  t.edge = img.put(edge.data(), edge.size() * 4);
+  t.eoff = img.put(eoff.data(), eoff.size() * 4);
+  t.loff = img.put(h.level_off.data(), h.level_off.size() * 4);
+  t.lat = img.put(h.lat.data(), h.lat.size() * 4);
+  t.mem = mem_uniform ? img.put(mem1.data(), mem1.size() * 4) : img.put(h.mem.data(), h.mem.size() * 4);
+  t.load = img.put(h.load.data(), h.load.size() * 4);
+  t.wmib = img.put(h.wmib.data(), h.wmib.size() * 4);
+  t.cap = img.put(h.cap.data(), h.cap.size() * 4);
+  t.arr = img.put(arr.data(), arr.size());
+  t.res0 = img.put(h.init_res.data(), h.init_res.size() * 8);
+  t.free0 = img.put(fr.data(), fr.size());
+  img.bytes.resize(align_up(img.bytes.size(), 16), 0);
+  t.bytes = (int)img.bytes.size();
+
+  sp.N = N;
+  sp.W = W;
+  sp.M = M;
+  sp.D = D;
+  sp.NB = (N + 3) / 4;
+  sp.E = E;
+  sp.n_levels = h.n_levels;
+  sp.wmax = std::max(1, h.wmax);
+  sp.nwords = std::max(1, (h.wmax + 63) / 64);
+  sp.mem_si = mem_uniform ? 1 : D;
+  sp.mem_sd = mem_uniform ? 0 : 1;
+  sp.origin = origin;
+  sp.min_arrival = h.min_arrival;
+  sp.w_mk = h.w_mk;
+  sp.w_p95 = h.w_p95;
+  sp.time64 = time64 ? 1 : 0;
+  sp.nibble = M <= 16 ? 1 : 0;
+
+  // ---- plans per wave, waves per workgroup, table placement ----
+  const int lds_cu = std::min(ctx->lds_per_cu, 160 * 1024);
+  const int lds_blk = std::min(ctx->lds_per_block, lds_cu);
+  const int gmax = std::max(1, 64 / D);
+  double best = -1.0;
+  for (int tl = 1; tl >= 0; --tl) {
+    const int tab_lds = tl ? t.bytes : 0;
     for (int G = gmax; G >= 1; --G) {
-      if (lds_layout(h, G, big, L) <= ctx->lds_per_block) {
-        const int per_cu = std::max(1, std::min(32, ctx->lds_per_cu / std::max(1, L.lds_bytes)));
-        L.grid = ctx->n_cu * per_cu;
-        return WF_OK;
+      wfp::WaveOffsets o{};
+      const int wb = wave_layout(h, G, tsz, sp.nibble, sp.nwords, o);
+      int waves = std::min(8, (lds_blk - tab_lds) / std::max(wb, 1));
+      if (waves < 1) continue;
+      const int lds_wg = tab_lds + waves * wb;
+      const int wg_per_cu = std::max(1, lds_cu / lds_wg);
+      const int waves_cu = std::min(32, wg_per_cu * waves);
+      // walk lanes in flight per CU, table reads from LDS preferred
+      const double score = (double)std::min(G * D, 64) * std::min(waves_cu, 8) * (tl ? 1.0 : 0.6);
+      if (score > best) {
+        best = score;
+        sp.G = G;
+        sp.waves = waves;
+        sp.tab_in_lds = tl;
+        sp.lds_bytes = lds_wg;
+        sp.grid = ctx->n_cu * wg_per_cu;
+        sp.wo = o;
       }
     }
   }
-  return fail(&ctx->err, WF_EUNSUPPORTED,
-              "window needs more LDS than a workgroup may use (widest level %d, %d devices, %d models)",
-              h.wmax, h.D, h.M);
+  sp.wave_global = 0;
+  sp.scratch = nullptr;
+  if (best < 0) {
+    // per-wave regions in HBM: one plan per device lane group, a bounded grid
+    wfp::WaveOffsets o{};
+    const int G = gmax;
+    const int64_t wb = wave_layout(h, G, tsz, sp.nibble, sp.nwords, o);
+    const int64_t cap_bytes = int64_t(1) << 30;
+    const int waves = 4;
+    int64_t wgs = std::min<int64_t>((int64_t)ctx->n_cu * 2, cap_bytes / std::max<int64_t>(wb * waves, 1));
+    if (wgs < 1)
+      return fail(&ctx->err, WF_EUNSUPPORTED, "window too large (N=%d, widest level %d, D=%d, M=%d)",
+                  N, h.wmax, D, M);
+    sp.G = G;
+    sp.waves = waves;
+    sp.tab_in_lds = 0;
+    sp.wave_global = 1;
+    sp.lds_bytes = 0;
+    sp.grid = (int)wgs;
+    sp.wo = o;
+  }
+  return WF_OK;
 }
 
 }  // namespace
 
 extern "C" {
 
-const char* wf_plan_version(void) { return "wf_plan 0.1 (gfx950)"; }
+const char* wf_plan_version(void) { return "wf_plan 0.2 (gfx950)"; }
 
 const char* wf_plan_last_error(const wf_plan_ctx* ctx) {
   return ctx ? ctx->err.c_str() : g_thread_err.c_str();
@@ -277,9 +428,7 @@ const char* wf_plan_last_error(const wf_plan_ctx* ctx) {
 wf_status wf_plan_validate_window(const wf_window_desc* w, char* err, size_t err_len) {
   std::string msg;
   const wf_status st = validate(w, &msg, nullptr);
-  if (err && err_len) {
-    std::snprintf(err, err_len, "%s", st == WF_OK ? "" : msg.c_str());
-  }
+  if (err && err_len) std::snprintf(err, err_len, "%s", st == WF_OK ? "" : msg.c_str());
   g_thread_err = st == WF_OK ? "" : msg;
   return st;
 }
@@ -343,85 +492,47 @@ wf_status wf_plan_upload_window(wf_plan_ctx* ctx, const wf_window_desc* w) {
   HostWindow h;
   wf_status st = validate(w, &ctx->err, &h);
   if (st != WF_OK) return st;
-  wfp::ScoreLaunch L{};
-  st = plan_launch(ctx, h, L);
+  Image img;
+  wfp::ScoreParams sp{};
+  st = plan_window(ctx, h, img, sp);
   if (st != WF_OK) return st;
-
-  // one device allocation holding every table
-  std::vector<std::pair<const void*, size_t>> parts = {
-      {h.act_model.data(), h.act_model.size() * 4}, {h.act_wf.data(), h.act_wf.size() * 4},
-      {h.fusible.data(), h.fusible.size()},         {h.chain_next.data(), h.chain_next.size() * 4},
-      {h.pred_off.data(), h.pred_off.size() * 4},   {h.pred_idx.data(), h.pred_idx.size() * 4},
-      {h.lat.data(), h.lat.size() * 4},             {h.mem.data(), h.mem.size() * 4},
-      {h.arrival.data(), h.arrival.size() * 8},     {h.cap.data(), h.cap.size() * 4},
-      {h.wmib.data(), h.wmib.size() * 4},           {h.load.data(), h.load.size() * 4},
-      {h.init_res.data(), h.init_res.size() * 8},   {h.free0.data(), h.free0.size() * 8},
-      {h.level_off.data(), h.level_off.size() * 4}};
-  std::vector<size_t> offs;
-  size_t total = 0;
-  for (auto& p : parts) {
-    offs.push_back(total);
-    total = align_up(total + p.second, 256);
-  }
-  std::vector<unsigned char> staging(total, 0);
-  for (size_t i = 0; i < parts.size(); ++i)
-    if (parts[i].second) std::memcpy(staging.data() + offs[i], parts[i].first, parts[i].second);
 
   int prev = 0;
   (void)hipGetDevice(&prev);
   hipError_t e = hipSetDevice(ctx->device);
   if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
   DeviceWindow dw;
-  e = hipMalloc(&dw.blob, total);
+  e = hipMalloc(&dw.tab, img.bytes.size());
   if (e != hipSuccess) {
     (void)hipSetDevice(prev);
     ctx->err = "device allocation of the window failed";
     return WF_ENOMEM;
   }
-  if (L.big) {
-    e = hipMalloc(&dw.scratch, (size_t)L.grid * (size_t)L.scratch_per_wave * 8);
+  e = hipMemcpy(dw.tab, img.bytes.data(), img.bytes.size(), hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    free_device_window(dw);
+    (void)hipSetDevice(prev);
+    return hip_fail(ctx, e, "copying the window to the device");
+  }
+  if (sp.wave_global) {
+    e = hipMalloc(&dw.scratch, (size_t)sp.grid * sp.waves * (size_t)sp.wo.bytes);
     if (e != hipSuccess) {
       free_device_window(dw);
       (void)hipSetDevice(prev);
       ctx->err = "device allocation of the scoring scratch failed";
       return WF_ENOMEM;
     }
+    sp.scratch = static_cast<unsigned char*>(dw.scratch);
   }
-  e = hipMemcpy(dw.blob, staging.data(), total, hipMemcpyHostToDevice);
-  if (e != hipSuccess) {
-    free_device_window(dw);
-    (void)hipSetDevice(prev);
-    return hip_fail(ctx, e, "copying the window to the device");
-  }
-  dw.bytes = total;
-  unsigned char* b = static_cast<unsigned char*>(dw.blob);
-  wfp::WindowDev& v = dw.view;
-  v.N = h.N;
-  v.W = h.W;
-  v.M = h.M;
-  v.D = h.D;
-  v.NB = (h.N + 3) / 4;
-  v.n_levels = h.n_levels;
-  v.wmax = std::max(1, h.wmax);
-  v.min_arrival = h.min_arrival;
-  v.w_mk = h.w_mk;
-  v.w_p95 = h.w_p95;
-  v.act_model = reinterpret_cast<const int32_t*>(b + offs[0]);
-  v.act_wf = reinterpret_cast<const int32_t*>(b + offs[1]);
-  v.fusible = reinterpret_cast<const uint8_t*>(b + offs[2]);
-  v.chain_next = reinterpret_cast<const int32_t*>(b + offs[3]);
-  v.pred_off = reinterpret_cast<const int32_t*>(b + offs[4]);
-  v.pred_idx = reinterpret_cast<const int32_t*>(b + offs[5]);
-  v.lat = reinterpret_cast<const int32_t*>(b + offs[6]);
-  v.mem = reinterpret_cast<const int32_t*>(b + offs[7]);
-  v.arrival = reinterpret_cast<const int64_t*>(b + offs[8]);
-  v.cap = reinterpret_cast<const int32_t*>(b + offs[9]);
-  v.wmib = reinterpret_cast<const int32_t*>(b + offs[10]);
-  v.load = reinterpret_cast<const int32_t*>(b + offs[11]);
-  v.init_res = reinterpret_cast<const uint64_t*>(b + offs[12]);
-  v.free0 = reinterpret_cast<const int64_t*>(b + offs[13]);
-  v.level_off = reinterpret_cast<const int32_t*>(b + offs[14]);
-  dw.launch = L;
+  sp.tab = static_cast<const unsigned char*>(dw.tab);
+  dw.sp = sp;
+  if (std::getenv("WF_PLAN_VERBOSE"))
+    std::fprintf(stderr,
+                 "[wf_plan] N=%d W=%d D=%d M=%d levels=%d wmax=%d time=%s G=%d waves/wg=%d "
+                 "grid=%d tables=%s(%d B) wave=%d B lds/wg=%d reclaim=%s\n",
+                 sp.N, sp.W, sp.D, sp.M, sp.n_levels, sp.wmax, sp.time64 ? "fp64" : "u32", sp.G,
+                 sp.waves, sp.grid, sp.wave_global ? "hbm+scratch" : (sp.tab_in_lds ? "lds" : "hbm"),
+                 sp.t.bytes, sp.wo.bytes, sp.lds_bytes, sp.nibble ? "queue" : "scan");
   free_device_window(ctx->dw);
   ctx->dw = dw;
   ctx->host = std::move(h);
@@ -450,11 +561,11 @@ wf_status wf_plan_score_batch(wf_plan_ctx* ctx, const int8_t* dev, const uint16_
   (void)hipGetDevice(&prev);
   hipError_t e = hipSetDevice(ctx->device);
   if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
-  wfp::ScoreLaunch L = ctx->dw.launch;
-  const int64_t groups = (n_plans + L.G - 1) / L.G;
-  if (groups < L.grid) L.grid = (int)groups;
-  e = wfp::launch_score(ctx->dw.view, L, ctx->dw.scratch, dev, prio, flags, n_plans, scores, sched,
-                        static_cast<hipStream_t>(hip_stream));
+  wfp::ScoreParams sp = ctx->dw.sp;
+  const int64_t groups = (n_plans + sp.G - 1) / sp.G;
+  const int64_t wgs = (groups + sp.waves - 1) / sp.waves;
+  if (wgs < sp.grid) sp.grid = (int)wgs;
+  e = wfp::launch_score(sp, dev, prio, flags, n_plans, scores, sched, static_cast<hipStream_t>(hip_stream));
   (void)hipSetDevice(prev);
   if (e != hipSuccess) return hip_fail(ctx, e, "launching the scoring kernel");
   return WF_OK;

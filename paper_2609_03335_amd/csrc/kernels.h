@@ -9,47 +9,60 @@
 
 namespace wfp {
 
-// Window tables resident in HBM (one allocation owned by the context).
-struct WindowDev {
-  int32_t N, W, M, D, NB;   // NB = ceil(N / 4) flag bytes per plan row
-  int32_t n_levels, wmax;   // number of topological levels, widest level
-  int64_t min_arrival;      // first workflow arrival (0 when N == 0)
+// Byte offsets of the window tables inside the table image.  The host builds
+// the image once per window; the scoring kernel copies it into LDS (or reads
+// it from HBM when it is too large) and uses the same offsets either way.
+struct TabOffsets {
+  int act;     // u32 [N]    model | fusible << 6 | workflow << 16
+  int cnext;   // u16 [N]    successor v of u when Eq. 3 holds for (u, v), else 0xffff
+  int edge;    // u32 [E]    predecessor | activation << 16, grouped by activation (CSR order)
+  int eoff;    // i32 [L+1]  first edge of each level
+  int loff;    // i32 [L+1]  first activation of each level
+  int lat;     // i32 [N*D]  run time, -1 ineligible
+  int mem;     // i32        activation memory, element (i, d) at i * mem_si + d * mem_sd
+  int load;    // i32 [M*D]  load time
+  int wmib;    // i32 [M]    model weights
+  int cap;     // i32 [D]    device capacity
+  int arr;     // time [W]   workflow arrival relative to the window origin
+  int res0;    // u64 [D]    initial resident-model mask
+  int free0;   // time [D]   initial busy-until relative to the window origin
+  int bytes;
+};
+
+// Byte offsets inside one wave's LDS region (G plans scored together).
+struct WaveOffsets {
+  int dev, prio, flags;  // staged plan rows: G*N int8, G*N uint16, G*NB uint8
+  int fin;               // time [G][N]     finish of every activation
+  int rt;                // time [G][wmax]  release of the current level's activations
+  int rec;               // uint4 [G][wmax] unit record per resource-order slot
+  int claim;             // u64 [G][NW]     slot claims (fast ordering path)
+  int mask;              // u64 [G][D][NW]  per-device slot masks of the current level
+  int cnt;               // u32 [G*D][ceil(M/2)]  remaining uses per (device, model), two u16 per word
+  int last;              // i32 [G*D][M]    last use per (device, model) (general reclamation path)
+  int wfm;               // time [G][W]     latest finish per workflow
+  int acc;               // PlanAcc [G]
+  int bytes;
+};
+
+struct ScoreParams {
+  int32_t N, W, M, D, NB, E, n_levels, wmax, nwords;
+  int32_t mem_si, mem_sd;     // activation-memory table strides
+  int64_t origin;             // absolute time of relative time 0
+  int64_t min_arrival;        // first workflow arrival (absolute)
   float w_mk, w_p95;
-  const int32_t* act_model;   // [N]
-  const int32_t* act_wf;      // [N]
-  const uint8_t* fusible;     // [N] Eq. 3 holds for the edge into v
-  const int32_t* chain_next;  // [N] v when succ(u) = {v} and v is fusible, else -1
-  const int32_t* pred_off;    // [N+1]
-  const int32_t* pred_idx;    // [nnz]
-  const int32_t* lat;         // [N*D]
-  const int32_t* mem;         // [N*D]
-  const int64_t* arrival;     // [W]
-  const int32_t* cap;         // [D]
-  const int32_t* wmib;        // [M]
-  const int32_t* load;        // [M*D]
-  const uint64_t* init_res;   // [D]
-  const int64_t* free0;       // [D]
-  const int32_t* level_off;   // [n_levels+1]
+  const unsigned char* tab;   // table image in HBM
+  TabOffsets t;
+  WaveOffsets wo;
+  int G;                      // plans per wave (G * D <= 64)
+  int waves;                  // waves per workgroup
+  int tab_in_lds;             // 1: the table image is staged in LDS
+  int wave_global;            // 1: per-wave regions live in HBM scratch (windows too big for LDS)
+  unsigned char* scratch;     // per-wave regions when wave_global
+  int lds_bytes;              // dynamic LDS per workgroup
+  int grid;                   // workgroups (persistent)
+  int time64;                 // 1: fp64 times, 0: uint32 times
+  int nibble;                 // 1: M <= 16, in-register reclamation queue
 };
-
-// Launch geometry and LDS carve-up of the scoring kernel.
-struct ScoreLaunch {
-  int G;            // plans scored together by one wave (G * D <= 64)
-  int nwords;       // 64-bit words per level bitmask = ceil(wmax / 64)
-  int big;          // 1: finish times and workflow maxima live in global scratch
-  int off_pos, off_claim, off_mask, off_cnt, off_last, off_acc, off_finish, off_wfmax;
-  int lds_bytes;
-  int grid;         // persistent grid (waves)
-  int64_t scratch_per_wave;   // int64 entries of global scratch per wave (big mode)
-};
-
-hipError_t launch_score(const WindowDev& w, const ScoreLaunch& L, int64_t* scratch,
-                        const int8_t* dev, const uint16_t* prio, const uint8_t* flags,
-                        int64_t n_plans, wf_plan_score* scores, const wf_plan_sched* sched,
-                        hipStream_t stream);
-
-hipError_t launch_argmin(const wf_plan_score* scores, int64_t n_plans, int64_t* out_index,
-                         int grid, hipStream_t stream);
 
 // Per-plan accumulators kept in LDS by the scoring kernel.
 struct PlanAcc {
@@ -57,8 +70,15 @@ struct PlanAcc {
   int32_t headroom;
   uint32_t loads;
   uint32_t evicts;
-  unsigned long long max_finish;
-  long long p95;
+  unsigned long long max_finish;  // time bits
+  long long p95;                  // selected completion latency (time units)
 };
+
+hipError_t launch_score(const ScoreParams& sp, const int8_t* dev, const uint16_t* prio,
+                        const uint8_t* flags, int64_t n_plans, wf_plan_score* scores,
+                        const wf_plan_sched* sched, hipStream_t stream);
+
+hipError_t launch_argmin(const wf_plan_score* scores, int64_t n_plans, int64_t* out_index,
+                         int grid, hipStream_t stream);
 
 }  // namespace wfp
