@@ -228,8 +228,9 @@ struct Image {
   }
 };
 
-// Per-wave LDS carve-up for G plans; returns the wave's byte size.
-int wave_layout(const HostWindow& h, int G, int tsz, bool nibble, int nwords, wfp::WaveOffsets& o) {
+// Per-wave LDS carve-up for G plans; returns the wave's byte size.  The
+// staged device/priority rows and the walk-only arrays share one region.
+int wave_layout(const HostWindow& h, int G, int tsz, int nwa, wfp::WaveOffsets& o) {
   size_t off = 0;
   auto take = [&](size_t n) {
     const size_t at = off;
@@ -237,18 +238,22 @@ int wave_layout(const HostWindow& h, int G, int tsz, bool nibble, int nwords, wf
     return (int)at;
   };
   const int NB = (h.N + 3) / 4, MH = (h.M + 1) / 2, wm = std::max(1, h.wmax);
+  o.flags = take((size_t)G * NB);
+  o.rec = take((size_t)G * h.N * 4);
+  o.mask = take((size_t)G * h.D * nwa * 8);
+  o.claim = take((size_t)G * nwa * 8);
+  o.cnt = take((size_t)G * h.D * MH * 4);
+  o.fin = take((size_t)G * h.N * tsz);
+  o.acc = take((size_t)G * sizeof(wfp::PlanAcc));
+  const size_t shared = off;
   o.dev = take((size_t)G * h.N);
   o.prio = take((size_t)G * h.N * 2);
-  o.flags = take((size_t)G * NB);
-  o.fin = take((size_t)G * h.N * tsz);
+  const size_t end_rows = off;
+  off = shared;
   o.rt = take((size_t)G * wm * tsz);
-  o.rec = take((size_t)G * wm * 16);
-  o.claim = take((size_t)G * nwords * 8);
-  o.mask = take((size_t)G * h.D * nwords * 8);
-  o.cnt = take((size_t)G * h.D * MH * 4);
-  o.last = take(nibble ? 0 : (size_t)G * h.D * h.M * 4);
+  o.stamp = take((size_t)G * h.D * h.M * 2);
   o.wfm = take((size_t)G * std::max(1, h.W) * tsz);
-  o.acc = take((size_t)G * sizeof(wfp::PlanAcc));
+  off = std::max(off, end_rows);
   o.bytes = (int)off;
   return o.bytes;
 }
@@ -328,8 +333,17 @@ wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, Image& img, wfp::Sc
     if (time64) { const double x = (double)r; std::memcpy(&fr[(size_t)d * 8], &x, 8); }
     else { const uint32_t x = (uint32_t)r; std::memcpy(&fr[(size_t)d * 4], &x, 4); }
   }
+  std::vector<uint32_t> alv((size_t)std::max(N, 1), 0);
+  for (int32_t l = 0; l < h.n_levels; ++l)
+    for (int32_t i = h.level_off[l]; i < h.level_off[l + 1]; ++i)
+      alv[i] = (uint32_t)h.level_off[l] | ((uint32_t)(h.level_off[l + 1] - h.level_off[l]) << 16);
+  std::vector<unsigned char> aarr((size_t)std::max(N, 1) * tsz, 0);
+  for (int32_t i = 0; i < N; ++i)
+    std::memcpy(&aarr[(size_t)i * tsz], &arr[(size_t)h.act_wf[i] * tsz], tsz);
   wfp::TabOffsets& t = sp.t;
   t.act = img.put(act.data(), act.size() * 4);
+  t.alv = img.put(alv.data(), alv.size() * 4);
+  t.aarr = img.put(aarr.data(), aarr.size());
   t.cnext = img.put(cnext.data(), cnext.size() * 2);
   t.edge = img.put(edge.data(), edge.size() * 4);
   t.eoff = img.put(eoff.data(), eoff.size() * 4);
@@ -342,6 +356,18 @@ wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, Image& img, wfp::Sc
   t.arr = img.put(arr.data(), arr.size());
   t.res0 = img.put(h.init_res.data(), h.init_res.size() * 8);
   t.free0 = img.put(fr.data(), fr.size());
+  // activations with no successor in their own workflow: a workflow's
+  // latest finish is reached at one of them
+  std::vector<uint8_t> has_wf_succ((size_t)std::max(N, 1), 0);
+  for (int32_t v = 0; v < N; ++v)
+    for (int32_t k = h.pred_off[v]; k < h.pred_off[v + 1]; ++k)
+      if (h.act_wf[h.pred_idx[k]] == h.act_wf[v]) has_wf_succ[h.pred_idx[k]] = 1;
+  std::vector<uint32_t> sink;
+  for (int32_t i = 0; i < N; ++i)
+    if (!has_wf_succ[i]) sink.push_back((uint32_t)i | ((uint32_t)h.act_wf[i] << 16));
+  const int32_t S = (int32_t)sink.size();
+  if (sink.empty()) sink.push_back(0);
+  t.sink = img.put(sink.data(), sink.size() * 4);
   img.bytes.resize(align_up(img.bytes.size(), 16), 0);
   t.bytes = (int)img.bytes.size();
 
@@ -351,9 +377,10 @@ wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, Image& img, wfp::Sc
   sp.D = D;
   sp.NB = (N + 3) / 4;
   sp.E = E;
+  sp.S = S;
   sp.n_levels = h.n_levels;
   sp.wmax = std::max(1, h.wmax);
-  sp.nwords = std::max(1, (h.wmax + 63) / 64);
+  sp.nwa = std::max(1, (N + 63) / 64);
   sp.mem_si = mem_uniform ? 1 : D;
   sp.mem_sd = mem_uniform ? 0 : 1;
   sp.origin = origin;
@@ -372,7 +399,7 @@ wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, Image& img, wfp::Sc
     const int tab_lds = tl ? t.bytes : 0;
     for (int G = gmax; G >= 1; --G) {
       wfp::WaveOffsets o{};
-      const int wb = wave_layout(h, G, tsz, sp.nibble, sp.nwords, o);
+      const int wb = wave_layout(h, G, tsz, sp.nwa, o);
       int waves = std::min(8, (lds_blk - tab_lds) / std::max(wb, 1));
       if (waves < 1) continue;
       const int lds_wg = tab_lds + waves * wb;
@@ -397,7 +424,7 @@ wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, Image& img, wfp::Sc
     // per-wave regions in HBM: one plan per device lane group, a bounded grid
     wfp::WaveOffsets o{};
     const int G = gmax;
-    const int64_t wb = wave_layout(h, G, tsz, sp.nibble, sp.nwords, o);
+    const int64_t wb = wave_layout(h, G, tsz, sp.nwa, o);
     const int64_t cap_bytes = int64_t(1) << 30;
     const int waves = 4;
     int64_t wgs = std::min<int64_t>((int64_t)ctx->n_cu * 2, cap_bytes / std::max<int64_t>(wb * waves, 1));

@@ -14,6 +14,8 @@ namespace wfp {
 // it from HBM when it is too large) and uses the same offsets either way.
 struct TabOffsets {
   int act;     // u32 [N]    model | fusible << 6 | workflow << 16
+  int alv;     // u32 [N]    first index of the activation's level | level width << 16
+  int aarr;    // time [N]   arrival of the activation's workflow (relative)
   int cnext;   // u16 [N]    successor v of u when Eq. 3 holds for (u, v), else 0xffff
   int edge;    // u32 [E]    predecessor | activation << 16, grouped by activation (CSR order)
   int eoff;    // i32 [L+1]  first edge of each level
@@ -26,26 +28,31 @@ struct TabOffsets {
   int arr;     // time [W]   workflow arrival relative to the window origin
   int res0;    // u64 [D]    initial resident-model mask
   int free0;   // time [D]   initial busy-until relative to the window origin
+  int sink;    // u32 [S]    activations without successor in their workflow: index | workflow << 16
   int bytes;
 };
 
 // Byte offsets inside one wave's LDS region (G plans scored together).
+// The staged rows are only read while slots are assigned; the release,
+// use-stamp and workflow arrays are only used afterwards, so the two sets
+// share storage.
 struct WaveOffsets {
-  int dev, prio, flags;  // staged plan rows: G*N int8, G*N uint16, G*NB uint8
-  int fin;               // time [G][N]     finish of every activation
-  int rt;                // time [G][wmax]  release of the current level's activations
-  int rec;               // uint4 [G][wmax] unit record per resource-order slot
-  int claim;             // u64 [G][NW]     slot claims (fast ordering path)
-  int mask;              // u64 [G][D][NW]  per-device slot masks of the current level
+  int flags;             // u8 [G][NB]       staged fuse/prefetch rows
+  int rec;               // u32 [G][N]       unit head per resource-order slot (packed)
+  int mask;              // u64 [G][D][NWA]  slots of each device's units
+  int claim;             // u64 [G][NWA]     slot claims (fast ordering path)
   int cnt;               // u32 [G*D][ceil(M/2)]  remaining uses per (device, model), two u16 per word
-  int last;              // i32 [G*D][M]    last use per (device, model) (general reclamation path)
-  int wfm;               // time [G][W]     latest finish per workflow
+  int fin;               // time [G][N]      finish of every activation
   int acc;               // PlanAcc [G]
+  int dev, prio;         // staged rows: G*N int8, G*N uint16            (shared region)
+  int rt;                // time [G][wmax]   latest predecessor finish   (shared region)
+  int stamp;             // u16 [G*D][M]     last use of each model      (shared region)
+  int wfm;               // time [G][W]      latest finish per workflow  (shared region)
   int bytes;
 };
 
 struct ScoreParams {
-  int32_t N, W, M, D, NB, E, n_levels, wmax, nwords;
+  int32_t N, W, M, D, NB, E, S, n_levels, wmax, nwa;
   int32_t mem_si, mem_sd;     // activation-memory table strides
   int64_t origin;             // absolute time of relative time 0
   int64_t min_arrival;        // first workflow arrival (absolute)
@@ -72,6 +79,8 @@ struct PlanAcc {
   uint32_t evicts;
   unsigned long long max_finish;  // time bits
   long long p95;                  // selected completion latency (time units)
+  uint32_t bad;                   // ordering fast path failed for the current level
+  uint32_t pad[3];
 };
 
 hipError_t launch_score(const ScoreParams& sp, const int8_t* dev, const uint16_t* prio,

@@ -3,20 +3,18 @@
 // A workgroup of several waves first copies the window's table image into
 // LDS (shared by its waves).  Each wave then loops over groups of G plans
 // (persistent grid) and, per group:
-//   1. stages the G packed plan rows (device, priority, fuse/prefetch bits)
-//      into its own LDS region with 16-byte loads;
+//   1. stages the G packed device rows and flag rows into its own LDS
+//      region with 16-byte loads (priorities are read once, from HBM);
 //   2. counts unit heads per (device, model) -- the remaining uses that the
 //      reclamation rule consults (lanes over activations);
 //   3. for every topological level, per plan (lanes over activations):
-//        - releases r = max(arrival, latest predecessor finish) (Eq. 2), one
-//          lane per incoming edge, as an LDS atomic max on order-preserving
-//          time bits;
 //        - each unit head's slot in the resource order (priority, index)
 //          (Eq. 10): its priority minus the level's first index when the
-//          level's head priorities are distinct values in range (the common,
+//          level's head priorities are distinct values in range (the
 //          permutation case), else its rank by (priority, index);
-//        - the unit record at that slot: fused-chain run time (Eq. 4),
-//          chain memory maximum, model, prefetch bit, workflow;
+//        - releases r = max(arrival, latest predecessor finish) (Eq. 2): one
+//          lane per incoming edge, an LDS atomic max on order-preserving
+//          time bits;
 //      then lane (g, d) = (lane / D, lane % D) walks device d of plan g over
 //      the level's slots in order: reuse / reclaim / load (Eq. 5, Eq. 11)
 //      and the max-plus timeline of Eq. 7;
@@ -62,7 +60,7 @@ __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_wave_barrier();
 }
 
-// Copy nbytes from HBM to LDS with the widest aligned accesses.
+// Copy nbytes from HBM with the widest aligned accesses.
 __device__ __forceinline__ void stage(unsigned char* dst, const unsigned char* src, int nbytes,
                                       int lane) {
   const uintptr_t a = reinterpret_cast<uintptr_t>(src);
@@ -79,6 +77,14 @@ __device__ __forceinline__ void stage(unsigned char* dst, const unsigned char* s
   }
 }
 
+__device__ __forceinline__ int fuse_bit(const uint8_t* fl, int v) {
+  return (fl[v >> 2] >> ((v & 3) << 1)) & 1;
+}
+
+// slot entry: activation | model << 16 | prefetch << 22 | has fused successor << 23
+constexpr uint32_t kPf = 1u << 22;
+constexpr uint32_t kChain = 1u << 23;
+
 template <typename TT, bool TAB_LDS, bool NIBBLE, bool WAVE_GLOBAL>
 __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
                                                    const int8_t* __restrict__ dev_all,
@@ -91,7 +97,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   extern __shared__ __align__(16) unsigned char lds[];
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int N = sp.N, W = sp.W, M = sp.M, D = sp.D, NB = sp.NB, G = sp.G, WMAX = sp.wmax,
-            NW = sp.nwords;
+            NWA = sp.nwa;
   const int MH = (M + 1) >> 1;
 
   // ---- window tables ----
@@ -109,6 +115,8 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
     wave_base = 0;
   }
   const uint32_t* t_act = reinterpret_cast<const uint32_t*>(tb + sp.t.act);
+  const uint32_t* t_alv = reinterpret_cast<const uint32_t*>(tb + sp.t.alv);
+  const TB* t_aarr = reinterpret_cast<const TB*>(tb + sp.t.aarr);
   const uint16_t* t_cnext = reinterpret_cast<const uint16_t*>(tb + sp.t.cnext);
   const uint32_t* t_edge = reinterpret_cast<const uint32_t*>(tb + sp.t.edge);
   const int32_t* t_eoff = reinterpret_cast<const int32_t*>(tb + sp.t.eoff);
@@ -121,6 +129,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   const TB* t_arr = reinterpret_cast<const TB*>(tb + sp.t.arr);
   const unsigned long long* t_res0 = reinterpret_cast<const unsigned long long*>(tb + sp.t.res0);
   const TB* t_free0 = reinterpret_cast<const TB*>(tb + sp.t.free0);
+  const uint32_t* t_sink = reinterpret_cast<const uint32_t*>(tb + sp.t.sink);
 
   // ---- this wave's region (LDS, or HBM scratch for very large windows) ----
   unsigned char* wl;
@@ -128,18 +137,18 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
     wl = sp.scratch + ((int64_t)blockIdx.x * sp.waves + wid) * (int64_t)sp.wo.bytes;
   else
     wl = lds + wave_base + wid * sp.wo.bytes;
+  uint8_t* s_fl = reinterpret_cast<uint8_t*>(wl + sp.wo.flags);
+  uint32_t* s_rec = reinterpret_cast<uint32_t*>(wl + sp.wo.rec);
+  unsigned long long* s_mask = reinterpret_cast<unsigned long long*>(wl + sp.wo.mask);
+  unsigned long long* s_claim = reinterpret_cast<unsigned long long*>(wl + sp.wo.claim);
+  uint32_t* s_cnt = reinterpret_cast<uint32_t*>(wl + sp.wo.cnt);
+  TB* s_fin = reinterpret_cast<TB*>(wl + sp.wo.fin);
+  PlanAcc* s_acc = reinterpret_cast<PlanAcc*>(wl + sp.wo.acc);
   int8_t* s_dev = reinterpret_cast<int8_t*>(wl + sp.wo.dev);
   uint16_t* s_prio = reinterpret_cast<uint16_t*>(wl + sp.wo.prio);
-  uint8_t* s_fl = reinterpret_cast<uint8_t*>(wl + sp.wo.flags);
-  TB* s_fin = reinterpret_cast<TB*>(wl + sp.wo.fin);
   TB* s_rt = reinterpret_cast<TB*>(wl + sp.wo.rt);
-  uint4* s_rec = reinterpret_cast<uint4*>(wl + sp.wo.rec);
-  unsigned long long* s_claim = reinterpret_cast<unsigned long long*>(wl + sp.wo.claim);
-  unsigned long long* s_mask = reinterpret_cast<unsigned long long*>(wl + sp.wo.mask);
-  uint32_t* s_cnt = reinterpret_cast<uint32_t*>(wl + sp.wo.cnt);
-  int32_t* s_last = reinterpret_cast<int32_t*>(wl + sp.wo.last);
+  uint16_t* s_stamp = reinterpret_cast<uint16_t*>(wl + sp.wo.stamp);
   TB* s_wfm = reinterpret_cast<TB*>(wl + sp.wo.wfm);
-  PlanAcc* s_acc = reinterpret_cast<PlanAcc*>(wl + sp.wo.acc);
 
   const int g_me = lane / D;
   const int d_me = lane - g_me * D;
@@ -150,16 +159,15 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
     const int64_t p0 = grp * G;
     const int gc = (int)((P - p0) < G ? (P - p0) : G);
 
-    // ---- stage the group's plan rows ----
+    // ---- stage the group's rows ----
     stage(reinterpret_cast<unsigned char*>(s_dev),
           reinterpret_cast<const unsigned char*>(dev_all + p0 * N), gc * N, lane);
     stage(reinterpret_cast<unsigned char*>(s_prio),
           reinterpret_cast<const unsigned char*>(prio_all + p0 * N), gc * N * 2, lane);
     stage(s_fl, flags_all + p0 * NB, gc * NB, lane);
     for (int i = lane; i < G * D * MH; i += 64) s_cnt[i] = 0u;
-    if constexpr (!NIBBLE)
-      for (int i = lane; i < G * D * M; i += 64) s_last[i] = -1;
-    for (int i = lane; i < G * W; i += 64) s_wfm[i] = 0;
+    for (int i = lane; i < G * D * NWA; i += 64) s_mask[i] = 0ull;
+    for (int i = lane; i < G * NWA; i += 64) s_claim[i] = 0ull;
     if (lane < G) {
       s_acc[lane].status = 0u;
       s_acc[lane].headroom = 0x7fffffff;
@@ -170,261 +178,270 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
     }
     wave_sync();
 
-    // ---- unit heads per (device, model): remaining uses ----
+    // ---- resource order of every unit head, remaining uses per (device, model) ----
     for (int g = 0; g < gc; ++g) {
       const int8_t* pdev = s_dev + g * N;
+      const uint16_t* pprio = s_prio + g * N;
       const uint8_t* pfl = s_fl + g * NB;
+      uint32_t* cnt = s_cnt + g * D * MH;
+      uint32_t* rec = s_rec + g * N;
+      unsigned long long* mk = s_mask + g * D * NWA;
+      unsigned long long* cl = s_claim + g * NWA;
+      int bad = 0;
       for (int u = lane; u < N; u += 64) {
         const uint32_t a = t_act[u];
-        if (((pfl[u >> 2] >> ((u & 3) << 1)) & 1) && (a & 64u)) continue;  // chain member
+        const int fb = pfl[u >> 2] >> ((u & 3) << 1);
+        if ((fb & 1) && (a & 64u)) continue;  // chain member
         const int d = pdev[u];
         if ((unsigned)d >= (unsigned)D) {
           atomicOr(&s_acc[g].status, (uint32_t)WF_ST_INELIGIBLE);
           continue;
         }
         const int m = (int)(a & 63u);
-        atomicAdd(&s_cnt[(g * D + d) * MH + (m >> 1)], 1u << ((m & 1) << 4));
+        atomicAdd(&cnt[d * MH + (m >> 1)], 1u << ((m & 1) << 4));
+        // fast path: the slot is the priority when the level's head
+        // priorities are distinct values in the level's index range
+        const uint32_t lvw = t_alv[u];
+        const int slot = (int)pprio[u];
+        if ((unsigned)(slot - (int)(lvw & 0xffffu)) >= (lvw >> 16)) {
+          bad = 1;
+          continue;
+        }
+        const unsigned long long bit = 1ull << (slot & 63);
+        if (atomicOr(&cl[slot >> 6], bit) & bit) {
+          bad = 1;
+          continue;
+        }
+        const int c = t_cnext[u];
+        const uint32_t chain = (c != 0xffff && fuse_bit(pfl, c)) ? kChain : 0u;
+        rec[slot] = (uint32_t)u | ((a & 63u) << 16) | ((uint32_t)((fb >> 1) & 1) << 22) | chain;
+        atomicOr(&mk[d * NWA + (slot >> 6)], bit);
+      }
+      if (__any(bad)) {  // general path: rank by (priority, index) within each level
+        wave_sync();
+        for (int i = lane; i < D * NWA; i += 64) mk[i] = 0ull;
+        wave_sync();
+        for (int u = lane; u < N; u += 64) {
+          const uint32_t a = t_act[u];
+          const int fb = pfl[u >> 2] >> ((u & 3) << 1);
+          if ((fb & 1) && (a & 64u)) continue;
+          const int d = pdev[u];
+          if ((unsigned)d >= (unsigned)D) continue;
+          const uint32_t lvw = t_alv[u];
+          const int lo = (int)(lvw & 0xffffu), hi = lo + (int)(lvw >> 16);
+          const int pu = pprio[u];
+          int slot = lo;
+          for (int j = lo; j < hi; ++j) {
+            if (fuse_bit(pfl, j) && (t_act[j] & 64u)) continue;
+            if ((unsigned)pdev[j] >= (unsigned)D) continue;
+            const int pj = pprio[j];
+            slot += (pj < pu) || (pj == pu && j < u);
+          }
+          const int c = t_cnext[u];
+          const uint32_t chain = (c != 0xffff && fuse_bit(pfl, c)) ? kChain : 0u;
+          rec[slot] = (uint32_t)u | ((a & 63u) << 16) | ((uint32_t)((fb >> 1) & 1) << 22) | chain;
+          atomicOr(&mk[d * NWA + (slot >> 6)], 1ull << (slot & 63));
+        }
       }
     }
     wave_sync();
 
-    // ---- device-lane state ----
+    // ---- device-lane state (the staged rows are dead from here on) ----
+    for (int i = lane; i < G * W; i += 64) s_wfm[i] = 0;
     const bool act = g_me < gc;
     const int gme = act ? g_me : 0;
     const int64_t pw = p0 + gme;
-    const int cbase = (gme * D + d_me) * MH;
-    const int lbase = (gme * D + d_me) * M;
+    uint32_t* mycnt = s_cnt + (gme * D + d_me) * MH;
+    uint16_t* mystamp = s_stamp + (gme * D + d_me) * M;
+    const unsigned long long* mymask = s_mask + (gme * D + d_me) * NWA;
+    const uint32_t* myrec = s_rec + gme * N;
+    const TB* myrt = s_rt + gme * WMAX;
+    TB* myfin = s_fin + gme * N;
+    const uint8_t* myfl = s_fl + gme * NB;
     uint64_t res = 0;
     int32_t used = 0, peak = 0, capd = 0;
     TT freet = 0;
-    uint32_t nld = 0, nev = 0, capbad = 0;
-    int32_t seq = 0;
-    uint64_t Q = 0;  // reclamation queue, 4 bits per resident model, next victim lowest
-    int qlen = 0, qdead = 0;
+    uint32_t nld = 0, nev = 0, capbad = 0, inel = 0;
+    uint32_t seq = 1;
+    // reclamation queues (at most 16 models): resident models with no
+    // remaining use on this device (qd) and with remaining uses (qa), each in
+    // least-recently-used order (never used: by id), 4 bits per entry, next
+    // victim in the low bits; a victim comes from qd first
+    uint64_t qd = 0, qa = 0;
+    int nd = 0, na = 0;
     if (act) {
       res = t_res0[d_me];
       capd = t_cap[d_me];
       freet = TO::load(t_free0 + d_me);
-      for (int m = 0; m < M; ++m)
-        if ((res >> m) & 1ull) used += t_wmib[m];
-      peak = used;
-      if constexpr (NIBBLE) {
-        // models with no use on this device first (least recently used = by
-        // id), then the ones still needed (also by id)
-        for (int pass = 0; pass < 2; ++pass)
-          for (int m = 0; m < M; ++m) {
-            if (!((res >> m) & 1ull)) continue;
-            const uint32_t c = (s_cnt[cbase + (m >> 1)] >> ((m & 1) << 4)) & 0xffffu;
-            if ((c == 0u) == (pass == 0)) {
-              Q |= (uint64_t)m << (4 * qlen);
-              ++qlen;
-            }
+      for (uint64_t r = res; r; r &= r - 1) {
+        const int m = __builtin_ctzll(r);
+        used += t_wmib[m];
+        if constexpr (NIBBLE) {
+          if (((mycnt[m >> 1] >> ((m & 1) << 4)) & 0xffffu) == 0u) {
+            qd |= (uint64_t)m << (4 * nd);
+            ++nd;
+          } else {
+            qa |= (uint64_t)m << (4 * na);
+            ++na;
           }
-        for (int m = 0; m < M; ++m)
-          if (((res >> m) & 1ull) && ((s_cnt[cbase + (m >> 1)] >> ((m & 1) << 4)) & 0xffffu) == 0u)
-            ++qdead;
+        } else {
+          mystamp[m] = 0;
+        }
       }
+      peak = used;
     }
 
     for (int lv = 0; lv < sp.n_levels; ++lv) {
-      const int lo = t_loff[lv], hi = t_loff[lv + 1], wlv = hi - lo, nwl = (wlv + 63) >> 6;
+      const int lo = t_loff[lv], hi = t_loff[lv + 1], wlv = hi - lo;
       const int e0 = t_eoff[lv], e1 = t_eoff[lv + 1];
-
-      for (int g = 0; g < gc; ++g) {
-        TB* rt = s_rt + g * WMAX;
-        uint4* rec = s_rec + g * WMAX;
-        unsigned long long* cl = s_claim + g * NW;
-        unsigned long long* mk = s_mask + g * D * NW;
-        const TB* fin = s_fin + g * N;
-        const int8_t* pdev = s_dev + g * N;
-        const uint16_t* pprio = s_prio + g * N;
-        const uint8_t* pfl = s_fl + g * NB;
-        for (int i = lane; i < wlv; i += 64) rt[i] = 0;
-        for (int i = lane; i < nwl; i += 64) cl[i] = 0ull;
-        for (int i = lane; i < D * nwl; i += 64) mk[(i / nwl) * NW + (i % nwl)] = 0ull;
-        wave_sync();
-        // releases: latest predecessor finish (Eq. 2)
-        for (int e = e0 + lane; e < e1; e += 64) {
-          const uint32_t ed = t_edge[e];
-          atomicMax(&rt[(int)(ed >> 16) - lo], fin[ed & 0xffffu]);
-        }
-        // slots in the resource order and unit records
-        for (int pass = 0; pass < 2; ++pass) {
-          int bad = 0;
-          for (int u = lo + lane; u < hi; u += 64) {
-            const uint32_t a = t_act[u];
-            const int flb = pfl[u >> 2] >> ((u & 3) << 1);
-            if ((flb & 1) && (a & 64u)) continue;  // chain member
-            const int d = pdev[u];
-            if ((unsigned)d >= (unsigned)D) continue;
-            const int pu = pprio[u];
-            int k = pu - lo;
-            if (pass == 0) {
-              if ((unsigned)k >= (unsigned)wlv) {
-                bad = 1;
-                continue;
-              }
-              const unsigned long long bit = 1ull << (k & 63);
-              if (atomicOr(&cl[k >> 6], bit) & bit) {
-                bad = 1;
-                continue;
-              }
-            } else {
-              k = 0;  // rank by (priority, index) among the level's heads
-              for (int j = lo; j < hi; ++j) {
-                const uint32_t aj = t_act[j];
-                if (((pfl[j >> 2] >> ((j & 3) << 1)) & 1) && (aj & 64u)) continue;
-                if ((unsigned)pdev[j] >= (unsigned)D) continue;
-                const int pj = pprio[j];
-                k += (pj < pu) || (pj == pu && j < u);
-              }
-            }
-            // unit record: fused chain (Eq. 4), run time sum, memory max
-            uint32_t T = 0, mx = 0;
-            int inel = 0, chain = 0;
-            for (int v = u;;) {
-              const int32_t l = t_lat[v * D + d];
-              inel |= l < 0;
-              T += (uint32_t)l;
-              const uint32_t mv = (uint32_t)t_mem[v * sp.mem_si + d * sp.mem_sd];
-              mx = mv > mx ? mv : mx;
-              const int c = t_cnext[v];
-              if (c == 0xffff || !((pfl[c >> 2] >> ((c & 3) << 1)) & 1)) break;
-              v = c;
-              chain = 1;
-            }
-            if (inel) atomicOr(&s_acc[g].status, (uint32_t)WF_ST_INELIGIBLE);
-            const uint32_t meta = (uint32_t)u | ((a & 63u) << 16) | ((uint32_t)((flb >> 1) & 1) << 22) |
-                                  ((uint32_t)chain << 23);
-            rec[k] = make_uint4(T, mx, meta, a >> 16);
-            atomicOr(&mk[d * NW + (k >> 6)], 1ull << (k & 63));
-            atomicMax(&rt[u - lo], t_arr[a >> 16]);
-          }
-          if (pass == 0) {
-            if (!__any(bad)) break;
-            wave_sync();
-            for (int i = lane; i < D * nwl; i += 64) mk[(i / nwl) * NW + (i % nwl)] = 0ull;
-          }
+      // ---- latest predecessor finish of the level's activations (Eq. 2) ----
+      if (e1 > e0) {
+        for (int g = 0; g < gc; ++g) {
+          TB* rt = s_rt + g * WMAX;
+          for (int i = lane; i < wlv; i += 64) rt[i] = 0;
           wave_sync();
+          const TB* fin = s_fin + g * N;
+          for (int e = e0 + lane; e < e1; e += 64) {
+            const uint32_t ed = t_edge[e];
+            atomicMax(&rt[(int)(ed >> 16) - lo], fin[ed & 0xffffu]);
+          }
         }
+        wave_sync();
       }
-      wave_sync();
 
       // ---- device lanes walk their units of this level in slot order ----
       if (act) {
-        const uint4* rec = s_rec + gme * WMAX;
-        const TB* rt = s_rt + gme * WMAX;
-        const unsigned long long* mk = s_mask + (gme * D + d_me) * NW;
-        TB* fin = s_fin + gme * N;
-        const uint8_t* pfl = s_fl + gme * NB;
         const int d = d_me;
-        for (int j = 0; j < nwl; ++j) {
-          unsigned long long bits = mk[j];
+        const int j0 = lo >> 6, j1 = (hi - 1) >> 6;
+        for (int j = j0; j <= j1; ++j) {
+          unsigned long long bits = mymask[j];
+          if (j == j0) bits &= ~0ull << (lo & 63);
+          if (j == j1 && (hi & 63)) bits &= (1ull << (hi & 63)) - 1ull;
           while (bits) {
-            const int k = (j << 6) + __builtin_ctzll(bits);
+            const int slot = (j << 6) + __builtin_ctzll(bits);
             bits &= bits - 1;
-            const uint4 rc = rec[k];
-            const int u = (int)(rc.z & 0xffffu);
-            const int m = (int)((rc.z >> 16) & 63u);
-            const TT r = TO::load(rt + (u - lo));
-            // one remaining use of m on this device consumed
-            uint32_t* cw = &s_cnt[cbase + (m >> 1)];
-            const int sh = (m & 1) << 4;
-            const uint32_t cword = *cw - (1u << sh);
-            *cw = cword;
-            const uint64_t mb = 1ull << m;
-            const bool miss = !(res & mb);
-            const int32_t wm = t_wmib[m];
-            const int32_t mxu = (int32_t)rc.y;
-            const int32_t need = (miss ? wm : 0) + mxu;
-            if constexpr (NIBBLE) {
-              if (!miss) {  // take m out of the queue; it re-enters as most recent
-                const uint64_t x = Q ^ (0x1111111111111111ull * (uint64_t)m);
-                const uint64_t z = (x - 0x1111111111111111ull) & ~x & 0x8888888888888888ull;
-                const int pos = __builtin_ctzll(z) >> 2;
-                const uint64_t low = (pos == 0) ? 0ull : (Q & ((1ull << (4 * pos)) - 1ull));
-                Q = low | ((Q >> (4 * pos + 4)) << (4 * pos));
-                --qlen;
+            const uint32_t meta = myrec[slot];
+            const int u = (int)(meta & 0xffffu);
+            const int m = (int)((meta >> 16) & 63u);
+            const TT arrv = TO::load(t_aarr + u);
+            const TT r = (e1 > e0) ? TO::tmax(TO::load(myrt + (u - lo)), arrv) : arrv;
+            // run time (summed over a fused chain, Eq. 4) and memory (max)
+            const int32_t l0 = t_lat[u * D + d];
+            int32_t mxu = t_mem[u * sp.mem_si + d * sp.mem_sd];
+            inel |= (uint32_t)(l0 < 0);
+            uint32_t T = (uint32_t)l0;
+            if (meta & kChain) {
+              for (int v = t_cnext[u];;) {
+                const int32_t lv2 = t_lat[v * D + d];
+                const int32_t mv = t_mem[v * sp.mem_si + d * sp.mem_sd];
+                inel |= (uint32_t)(lv2 < 0);
+                T += (uint32_t)lv2;
+                mxu = mv > mxu ? mv : mxu;
+                const int c = t_cnext[v];
+                if (c == 0xffff || !fuse_bit(myfl, c)) break;
+                v = c;
               }
-              while (used + need > capd && qlen > 0) {  // reclaim the queue head
-                const int v = (int)(Q & 15ull);
-                Q >>= 4;
-                --qlen;
-                qdead -= (qdead > 0);
+            }
+            // one remaining use of m on this device consumed
+            const int sh = (m & 1) << 4;
+            const uint32_t cword = mycnt[m >> 1] - (1u << sh);
+            mycnt[m >> 1] = cword;
+            const bool last_use = ((cword >> sh) & 0xffffu) == 0u;
+            const uint64_t mb = 1ull << m;
+            const bool hit = (res & mb) != 0ull;
+            const int32_t wm = t_wmib[m];
+            const int32_t need = (hit ? 0 : wm) + mxu;
+            // reclaim (Sec. 3.5): a copy with no remaining use first, else the
+            // least recently used, else the lower model id
+            if constexpr (NIBBLE) {
+              if (hit) {  // m is in qa: take it out, it re-enters as most recent
+                const uint64_t x = qa ^ (0x1111111111111111ull * (uint64_t)m);
+                const uint64_t z = (x - 0x1111111111111111ull) & ~x & 0x8888888888888888ull;
+                const int s4 = __builtin_ctzll(z) & ~3;  // 4 * position
+                const uint64_t low = qa & ((1ull << s4) - 1ull);
+                const uint64_t high = (s4 >= 60) ? 0ull : ((qa >> (s4 + 4)) << s4);
+                qa = low | high;
+                --na;
+              }
+              while (used + need > capd && (nd | na)) {
+                int v;
+                if (nd) {
+                  v = (int)(qd & 15ull);
+                  qd >>= 4;
+                  --nd;
+                } else {
+                  v = (int)(qa & 15ull);
+                  qa >>= 4;
+                  --na;
+                }
                 res &= ~(1ull << v);
                 used -= t_wmib[v];
                 ++nev;
+              }
+              if (last_use) {
+                qd |= (uint64_t)m << (4 * nd);
+                ++nd;
+              } else {
+                qa |= (uint64_t)m << (4 * na);
+                ++na;
               }
             } else {
               while (used + need > capd) {
                 uint64_t cand = res & ~mb;
                 if (!cand) break;
-                int victim = 0, v_alive = 2, v_last = 0x7fffffff;
+                int v = 0;
+                uint32_t best = 0xffffffffu;
                 while (cand) {
                   const int m2 = __builtin_ctzll(cand);
                   cand &= cand - 1;
-                  const int al = ((s_cnt[cbase + (m2 >> 1)] >> ((m2 & 1) << 4)) & 0xffffu) != 0u;
-                  const int la = s_last[lbase + m2];
-                  if (al < v_alive || (al == v_alive && la < v_last)) {
-                    victim = m2;
-                    v_alive = al;
-                    v_last = la;
+                  const uint32_t alive = ((mycnt[m2 >> 1] >> ((m2 & 1) << 4)) & 0xffffu) != 0u;
+                  const uint32_t key = (alive << 16) | mystamp[m2];
+                  if (key < best) {
+                    best = key;
+                    v = m2;
                   }
                 }
-                res &= ~(1ull << victim);
-                used -= t_wmib[victim];
+                res &= ~(1ull << v);
+                used -= t_wmib[v];
                 ++nev;
               }
+              mystamp[m] = (uint16_t)seq++;
             }
             capbad |= (uint32_t)(used + need > capd);
-            TT s, ls = 0;
-            if (miss) {
-              const TT arrv = TO::load(t_arr + rc.w);
-              ls = TO::tmax(((rc.z >> 22) & 1u) ? arrv : r, freet);
-              const TT le = TO::add(ls, (uint32_t)t_load[m * D + d]);
+            // timeline (Eq. 7): a load waits for the device and starts at the
+            // release, or at the workflow arrival when prefetched
+            const TT ls = TO::tmax((meta & kPf) ? arrv : r, freet);
+            const TT le = TO::add(ls, (uint32_t)t_load[m * D + d]);
+            const TT s = TO::tmax(r, hit ? freet : le);
+            if (!hit) {
               res |= mb;
               used += wm;
               ++nld;
-              s = TO::tmax(r, le);
-            } else {
-              s = TO::tmax(r, freet);
             }
             peak = (used + mxu) > peak ? (used + mxu) : peak;
-            if constexpr (NIBBLE) {
-              if (((cword >> sh) & 0xffffu) == 0u) {  // last use: joins the no-use part
-                const uint64_t lowm = (qdead == 0) ? 0ull : ((1ull << (4 * qdead)) - 1ull);
-                Q = (Q & lowm) | ((uint64_t)m << (4 * qdead)) | ((Q & ~lowm) << 4);
-                ++qdead;
-              } else {
-                Q |= (uint64_t)m << (4 * qlen);
-              }
-              ++qlen;
-            } else {
-              s_last[lbase + m] = seq++;
-            }
-            const TT f = TO::add(s, rc.x);
+            const TT f = TO::add(s, T);
             freet = f;
-            if (!((rc.z >> 23) & 1u)) {
-              fin[u] = TO::bits(f);
+            if (!(meta & kChain)) {
+              myfin[u] = TO::bits(f);
               if (has_sched) {
                 sched.start_us[pw * N + u] = sp.origin + TO::i64(s);
                 sched.finish_us[pw * N + u] = sp.origin + TO::i64(f);
-                sched.load_start_us[pw * N + u] = miss ? sp.origin + TO::i64(ls) : (int64_t)-1;
+                sched.load_start_us[pw * N + u] = hit ? (int64_t)-1 : sp.origin + TO::i64(ls);
               }
             } else {
               TT t = s;
               for (int v = u;;) {
                 const TT tv = TO::add(t, (uint32_t)t_lat[v * D + d]);
-                fin[v] = TO::bits(tv);
+                myfin[v] = TO::bits(tv);
                 if (has_sched) {
                   sched.start_us[pw * N + v] = sp.origin + TO::i64(t);
                   sched.finish_us[pw * N + v] = sp.origin + TO::i64(tv);
                   sched.load_start_us[pw * N + v] =
-                      (v == u && miss) ? sp.origin + TO::i64(ls) : (int64_t)-1;
+                      (v == u && !hit) ? sp.origin + TO::i64(ls) : (int64_t)-1;
                 }
                 t = tv;
                 const int c = t_cnext[v];
-                if (c == 0xffff || !((pfl[c >> 2] >> ((c & 3) << 1)) & 1)) break;
+                if (c == 0xffff || !fuse_bit(myfl, c)) break;
                 v = c;
               }
             }
@@ -440,32 +457,38 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
       atomicAdd(&s_acc[gme].loads, nld);
       atomicAdd(&s_acc[gme].evicts, nev);
       if (capbad) atomicOr(&s_acc[gme].status, (uint32_t)WF_ST_CAPACITY);
+      if (inel) atomicOr(&s_acc[gme].status, (uint32_t)WF_ST_INELIGIBLE);
       if (has_sched) sched.peak_mib[pw * D + d_me] = peak;
     }
-    wave_sync();
+    // a workflow's completion is the latest finish among its activations
+    // without a successor in the same workflow
     for (int g = 0; g < gc; ++g) {
       const TB* fin = s_fin + g * N;
       TB* wm = s_wfm + g * W;
-      for (int u = lane; u < N; u += 64) {
-        const TB f = fin[u];
-        atomicMax(&s_acc[g].max_finish, (unsigned long long)f);
-        atomicMax(&wm[t_act[u] >> 16], f);
+      for (int i = lane; i < sp.S; i += 64) {
+        const uint32_t sk = t_sink[i];
+        atomicMax(&wm[sk >> 16], fin[sk & 0xffffu]);
       }
-      wave_sync();
-      // nearest-rank p95: the k-th smallest completion latency, k = ceil(0.95 W)
-      const int kk = (95 * W + 99) / 100;
-      for (int a = lane; a < W; a += 64) {
-        const int64_t ca = TO::i64(TO::load(wm + a)) - TO::i64(TO::load(t_arr + a));
-        int lt = 0, le = 0;
-        for (int b = 0; b < W; ++b) {
-          const int64_t cb = TO::i64(TO::load(wm + b)) - TO::i64(TO::load(t_arr + b));
-          lt += cb < ca;
-          le += cb <= ca;
-        }
-        if (lt < kk && kk <= le) s_acc[g].p95 = ca;
-      }
-      wave_sync();
     }
+    wave_sync();
+    // nearest-rank p95 (the ceil(0.95 W)-th smallest completion latency) and
+    // the latest finish, lanes over (plan, workflow)
+    const int kk = (95 * W + 99) / 100;
+    for (int it = lane; it < gc * W; it += 64) {
+      const int g = it / W, a = it - g * W;
+      const TB* wm = s_wfm + g * W;
+      const TT fa = TO::load(wm + a);
+      const int64_t ca = TO::i64(fa) - TO::i64(TO::load(t_arr + a));
+      int lt = 0, le = 0;
+      for (int b = 0; b < W; ++b) {
+        const int64_t cb = TO::i64(TO::load(wm + b)) - TO::i64(TO::load(t_arr + b));
+        lt += cb < ca;
+        le += cb <= ca;
+      }
+      if (lt < kk && kk <= le) s_acc[g].p95 = ca;
+      atomicMax(&s_acc[g].max_finish, (unsigned long long)TO::bits(fa));
+    }
+    wave_sync();
     if (lane < gc) {
       const PlanAcc a = s_acc[lane];
       wf_plan_score sc;

@@ -235,3 +235,22 @@ def test_abi_errors_on_gpu(ctx):
         fresh.wf_plan_argmin(scores, 1 << 32, scores)
     assert e.value.status == pkg.WF_EINVAL
     fresh.close()
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_cross_workflow_edges(ctx, seed):
+    """Workflow ids reassigned at random so that edges cross workflows (a
+    workflow's completion is then not only reached at its DAG sinks)."""
+    rng = np.random.default_rng(20_000 + seed)
+    win = W.random_window(rng, n_wf=4, nodes=(3, 8), n_dev=3, n_models=4, p_edge=0.5)
+    nw = int(rng.integers(2, 6))
+    wf = rng.integers(0, nw, size=win.n_act)
+    wf[:nw] = np.arange(nw)  # every workflow keeps an activation
+    win = W.Window(**{**win.arrays(), "act_wf": wf.astype(np.int32), "n_wf": nw,
+                      "wf_arrival_us": rng.integers(0, 5000, size=nw).astype(np.int64)})
+    plans = W.random_plans(win, 64, rng)
+    got, gs, best = gpu_score(ctx, win, plans, schedule=True)
+    ref, rs = oracle.score(win, plans, schedule=True)
+    assert_scores(got, ref, f"cross seed {seed}")
+    assert_sched(gs, rs, ref["status"], f"cross seed {seed}")
+    assert best == best_plan(ref)
