@@ -25,12 +25,55 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X published HBM3E bandwidth
+CSRC = os.path.join(ROOT, "paper_2609_03335_amd", "csrc")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "score_plans_traffic.json")
 
 
 def algorithmic_bytes_per_plan(n_act: int) -> int:
     """Packed plan row read once (int8 device + uint16 priority + 2 flag
     bits per activation) plus the 32-byte score record written once."""
     return 3 * n_act + (n_act + 3) // 4 + 32
+
+
+def kernel_source_digest() -> str:
+    """sha256 over the scoring kernel's sources and its launch planner: a
+    stored HBM-traffic measurement is only valid for the code it was taken
+    on."""
+    import hashlib
+    h = hashlib.sha256()
+    for name in ("score.hip", "kernels.h", "host.hip"):
+        with open(os.path.join(CSRC, name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(config: int, n_plans: int):
+    """HBM bytes per scoring launch from the committed counter runs
+    (FETCH_SIZE + WRITE_SIZE, each scaled by the copy-kernel factor), or None
+    when there is none for this workload or the kernel changed since."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    e = rec.get("configs", {}).get(str(config))
+    if not e or e.get("n_plans") != n_plans or rec.get("kernel_source_sha256") != kernel_source_digest():
+        return None
+    return int(e["fetch_bytes"] + e["write_bytes"])
+
+
+def copy_probe(nbytes: int) -> None:
+    """A plain streaming kernel of known size (read nbytes, write nbytes):
+    the calibration run for the HBM byte counters."""
+    import torch
+    src = torch.randint(0, 255, (nbytes,), dtype=torch.uint8, device="cuda:0")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        torch.bitwise_not(src, out=dst)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes_read": nbytes, "copy_probe_bytes_written": nbytes,
+                      "launches": 3, "kernel": "bitwise_not"}))
 
 
 def cpu_model() -> str:
@@ -55,6 +98,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--check", type=int, default=4096,
                     help="plans checked against the oracle before timing (0 = none)")
+    ap.add_argument("--copy-probe", type=int, default=None, metavar="BYTES",
+                    help="only run a plain copy kernel of BYTES bytes (counter calibration)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -68,6 +113,9 @@ def main():
     from paper_2609_03335_amd import workload
 
     assert torch.cuda.is_available(), "bench.py needs a HIP device"
+    if args.copy_probe:
+        copy_probe(args.copy_probe)
+        return
     t0 = time.time()
     win, plans = workload.make_config(args.config, n_plans=args.plans)
     P, N, D = plans.n_plans, win.n_act, win.n_dev
@@ -76,6 +124,8 @@ def main():
 
     ctx = pkg.Context(0)
     ctx.wf_plan_upload_window(win)
+    # times as uint32 offsets or fp64, memory as int32 MiB
+    dtype = {32: "u32", 64: "f64"}[ctx.wf_plan_time_bits()]
     dev, prio, flags = pkg.device_plans(plans, "cuda:0")
     scores = torch.empty((P, 32), dtype=torch.uint8, device="cuda:0")
     best = torch.empty(1, dtype=torch.int64, device="cuda:0")
@@ -124,8 +174,9 @@ def main():
 
     bpp = algorithmic_bytes_per_plan(N)
     achieved = bpp * P / (kernel_ms * 1e-3) / 1e9
+    traffic = measured_traffic(args.config, P)
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                 "kernel": "score_plans", "kernel_ms": round(kernel_ms, 4),
                 "bytes_per_plan": bpp}
 
@@ -133,21 +184,24 @@ def main():
     if not args.no_cpu_baseline:
         import oracle
         threads = max(1, min(16, os.cpu_count() or 1))
-        n_cpu = args.cpu_sample or min(P, 400_000)
+        # the whole batch is about 20 core-seconds of oracle work at the
+        # throughput workload; larger batches are sampled evenly
+        n_cpu = min(P, args.cpu_sample or 2_000_000)
         idx = np.arange(n_cpu) * max(1, P // n_cpu)
         sample = plans.take(idx)
-        t = time.perf_counter()
+        t, c = time.perf_counter(), time.process_time()
         oracle.score(win, sample, threads=threads)
-        dt = time.perf_counter() - t
+        dt, dc = time.perf_counter() - t, time.process_time() - c
+        what = "the whole batch" if n_cpu == P else f"{n_cpu} evenly spaced plans of the batch"
         cpu = {"value": round(n_cpu / dt, 1), "unit": "plans/s", "cores": threads, "kind": "oracle",
-               "sample": f"{n_cpu} evenly spaced plans of the same batch, {threads} threads, "
-                         f"{dt:.2f}s wall ({cpu_model()})"}
+               "sample": f"{what}, {threads} threads, {dt:.2f} s wall, {dc:.1f} s CPU "
+                         f"({cpu_model()})"}
 
     line = {
         "metric": "candidate plans scored/sec at 1 GPU; achieved HBM GB/s vs peak",
         "value": round(value, 1), "unit": "plans/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": "int64", "data": "synthetic",
+        "scaling": "weak", "vs_baseline": None, "dtype": dtype, "data": "synthetic",
         "config": {"workload": workload.CONFIGS[args.config]["name"], "n_act": N,
                    "n_wf": win.n_wf, "n_dev": D, "n_models": win.n_models, "n_plans": P,
                    "batch_bytes": bpp * P},

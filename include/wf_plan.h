@@ -173,6 +173,12 @@ wf_status wf_plan_score_batch(wf_plan_ctx *ctx, const int8_t *dev, const uint16_
 wf_status wf_plan_argmin(wf_plan_ctx *ctx, const wf_plan_score *scores, int64_t n_plans,
                          int64_t *out_index, void *hip_stream);
 
+/* Time arithmetic the kernels use for the uploaded window: 32 when every
+ * time of every plan provably stays below 2^32 us after the window origin
+ * (uint32 offsets), 64 otherwise (fp64, exact for integers below 2^53); 0
+ * when ctx is NULL or has no window.  Results are identical either way. */
+int wf_plan_time_bits(const wf_plan_ctx *ctx);
+
 /* Library version string. */
 const char *wf_plan_version(void);
 

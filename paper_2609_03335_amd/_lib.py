@@ -32,7 +32,7 @@ assert SCORE_DTYPE.itemsize == 32
 # every symbol declared in include/wf_plan.h
 EXPORTS = ("wf_plan_ctx_create", "wf_plan_ctx_destroy", "wf_plan_last_error",
            "wf_plan_validate_window", "wf_plan_upload_window", "wf_plan_score_batch",
-           "wf_plan_argmin", "wf_plan_version")
+           "wf_plan_argmin", "wf_plan_time_bits", "wf_plan_version")
 
 
 class WFError(RuntimeError):
@@ -89,6 +89,8 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.wf_plan_score_batch.restype = i32
     lib.wf_plan_argmin.argtypes = [vp, vp, i64, vp, vp]
     lib.wf_plan_argmin.restype = i32
+    lib.wf_plan_time_bits.argtypes = [vp]
+    lib.wf_plan_time_bits.restype = i32
     lib.wf_plan_version.argtypes = []
     lib.wf_plan_version.restype = ctypes.c_char_p
     if path is None:
@@ -179,6 +181,9 @@ class Context:
     def wf_plan_argmin(self, scores, n_plans: int, out_index, stream=None) -> None:
         self._check(self.lib.wf_plan_argmin(self.handle, _ptr(scores), int(n_plans),
                                             _ptr(out_index), _stream(stream)))
+
+    def wf_plan_time_bits(self) -> int:
+        return int(self.lib.wf_plan_time_bits(self.handle))
 
     def close(self):
         if getattr(self, "handle", None):

@@ -448,6 +448,11 @@ extern "C" {
 
 const char* wf_plan_version(void) { return "wf_plan 0.2 (gfx950)"; }
 
+int wf_plan_time_bits(const wf_plan_ctx* ctx) {
+  if (!ctx || !ctx->has_window) return 0;
+  return ctx->dw.sp.time64 ? 64 : 32;
+}
+
 const char* wf_plan_last_error(const wf_plan_ctx* ctx) {
   return ctx ? ctx->err.c_str() : g_thread_err.c_str();
 }

@@ -37,6 +37,10 @@ def test_exports_every_declared_symbol():
     assert pkg.wf_plan_version().startswith("wf_plan")
 
 
+def test_time_bits_without_window():
+    assert _lib.load().wf_plan_time_bits(None) == 0
+
+
 def test_score_record_layout():
     text = open(HEADER).read()
     assert "int64_t makespan_us;" in text and "uint16_t n_evicts;" in text

@@ -78,6 +78,9 @@ def test_config_full_parity(ctx, cfg):
     assert_scores(got, ref, f"config {cfg}")
     assert best == best_plan(ref)
     assert got.tobytes() == ref.tobytes(), "score records not bitwise equal"
+    # only the tiny window's time bound stays below 2^32 us: the others take
+    # the fp64 time path (the throughput window's bound, 4.11e9 us, fits)
+    assert ctx.wf_plan_time_bits() == (32 if cfg == 0 else 64)
 
 
 @pytest.mark.parametrize("cfg,count", [(0, 512), (1, 1024), (2, 256), (3, 64), (4, 2048)])
@@ -96,6 +99,7 @@ def test_config4_full_size(ctx):
     win, plans = W.make_config(4)
     log(f"[parity] config 4 full: P={plans.n_plans}")
     got, _, best = gpu_score(ctx, win, plans)
+    assert ctx.wf_plan_time_bits() == 32
     ref = oracle.score(win, plans, threads=THREADS)
     assert_scores(got, ref, "config 4")
     assert got.tobytes() == ref.tobytes()
@@ -212,6 +216,7 @@ def test_nondefault_stream(ctx):
 
 def test_abi_errors_on_gpu(ctx):
     fresh = pkg.Context(0)
+    assert fresh.wf_plan_time_bits() == 0
     win, plans = W.make_config(0, n_plans=8)
     dev, prio, flags = pkg.device_plans(plans, "cuda:0")
     scores = torch.zeros((8, 32), dtype=torch.uint8, device="cuda:0")
@@ -219,6 +224,7 @@ def test_abi_errors_on_gpu(ctx):
         fresh.wf_plan_score_batch(dev, prio, flags, 8, scores)
     assert e.value.status == pkg.WF_ENOWINDOW
     fresh.wf_plan_upload_window(win)
+    assert fresh.wf_plan_time_bits() == 32
     bad = W.Window(**{k: (v.copy() if isinstance(v, np.ndarray) else v) for k, v in win.arrays().items()})
     bad.act_model[0] = 99
     with pytest.raises(pkg.WFError) as e:
