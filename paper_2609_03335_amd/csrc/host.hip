@@ -228,32 +228,30 @@ struct Image {
   }
 };
 
-// Per-wave LDS carve-up for G plans; returns the wave's byte size.  The
-// staged device/priority rows and the walk-only arrays share one region.
-int wave_layout(const HostWindow& h, int G, int tsz, int nwa, wfp::WaveOffsets& o) {
+// Per-wave LDS carve-up for G plans; returns the wave's byte size.
+int wave_layout(const HostWindow& h, int G, int tsz, int nwa, bool nibble, wfp::WaveOffsets& o) {
   size_t off = 0;
   auto take = [&](size_t n) {
     const size_t at = off;
     off = align_up(off + std::max<size_t>(n, 1), 16);
     return (int)at;
   };
-  const int NB = (h.N + 3) / 4, MH = (h.M + 1) / 2, wm = std::max(1, h.wmax);
+  const int NB = (h.N + 3) / 4;
+  const size_t fin_bytes = (size_t)G * h.N * tsz, last_bytes = (size_t)G * h.D * h.M * 4;
   o.flags = take((size_t)G * NB);
   o.rec = take((size_t)G * h.N * 4);
   o.mask = take((size_t)G * h.D * nwa * 8);
-  o.claim = take((size_t)G * nwa * 8);
-  o.cnt = take((size_t)G * h.D * MH * 4);
-  o.fin = take((size_t)G * h.N * tsz);
   o.acc = take((size_t)G * sizeof(wfp::PlanAcc));
-  const size_t shared = off;
-  o.dev = take((size_t)G * h.N);
-  o.prio = take((size_t)G * h.N * 2);
-  const size_t end_rows = off;
-  off = shared;
-  o.rt = take((size_t)G * wm * tsz);
-  o.stamp = take((size_t)G * h.D * h.M * 2);
+  if (nibble) {
+    o.fin = take(std::max(fin_bytes, last_bytes));
+    o.last = o.fin;
+    o.stamp = 0;
+  } else {
+    o.fin = take(fin_bytes);
+    o.last = take(last_bytes);
+    o.stamp = take((size_t)G * h.D * h.M * 2);
+  }
   o.wfm = take((size_t)G * std::max(1, h.W) * tsz);
-  off = std::max(off, end_rows);
   o.bytes = (int)off;
   return o.bytes;
 }
@@ -352,6 +350,13 @@ wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, Image& img, wfp::Sc
   t.mem = mem_uniform ? img.put(mem1.data(), mem1.size() * 4) : img.put(h.mem.data(), h.mem.size() * 4);
   t.load = img.put(h.load.data(), h.load.size() * 4);
   t.wmib = img.put(h.wmib.data(), h.wmib.size() * 4);
+  std::vector<int32_t> lw((size_t)M * D * 2);
+  for (int32_t m = 0; m < M; ++m)
+    for (int32_t d = 0; d < D; ++d) {
+      lw[((size_t)m * D + d) * 2] = h.load[(size_t)m * D + d];
+      lw[((size_t)m * D + d) * 2 + 1] = h.wmib[m];
+    }
+  t.lw = img.put(lw.data(), lw.size() * 4);
   t.cap = img.put(h.cap.data(), h.cap.size() * 4);
   t.arr = img.put(arr.data(), arr.size());
   t.res0 = img.put(h.init_res.data(), h.init_res.size() * 8);
@@ -399,7 +404,7 @@ wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, Image& img, wfp::Sc
     const int tab_lds = tl ? t.bytes : 0;
     for (int G = gmax; G >= 1; --G) {
       wfp::WaveOffsets o{};
-      const int wb = wave_layout(h, G, tsz, sp.nwa, o);
+      const int wb = wave_layout(h, G, tsz, sp.nwa, sp.nibble != 0, o);
       int waves = std::min(8, (lds_blk - tab_lds) / std::max(wb, 1));
       if (waves < 1) continue;
       const int lds_wg = tab_lds + waves * wb;
@@ -424,7 +429,7 @@ wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, Image& img, wfp::Sc
     // per-wave regions in HBM: one plan per device lane group, a bounded grid
     wfp::WaveOffsets o{};
     const int G = gmax;
-    const int64_t wb = wave_layout(h, G, tsz, sp.nwa, o);
+    const int64_t wb = wave_layout(h, G, tsz, sp.nwa, sp.nibble != 0, o);
     const int64_t cap_bytes = int64_t(1) << 30;
     const int waves = 4;
     int64_t wgs = std::min<int64_t>((int64_t)ctx->n_cu * 2, cap_bytes / std::max<int64_t>(wb * waves, 1));

@@ -23,6 +23,7 @@ struct TabOffsets {
   int lat;     // i32 [N*D]  run time, -1 ineligible
   int mem;     // i32        activation memory, element (i, d) at i * mem_si + d * mem_sd
   int load;    // i32 [M*D]  load time
+  int lw;      // i32x2 [M*D] {load time, model weights}
   int wmib;    // i32 [M]    model weights
   int cap;     // i32 [D]    device capacity
   int arr;     // time [W]   workflow arrival relative to the window origin
@@ -33,21 +34,17 @@ struct TabOffsets {
 };
 
 // Byte offsets inside one wave's LDS region (G plans scored together).
-// The staged rows are only read while slots are assigned; the release,
-// use-stamp and workflow arrays are only used afterwards, so the two sets
-// share storage.
 struct WaveOffsets {
-  int flags;             // u8 [G][NB]       staged fuse/prefetch rows
-  int rec;               // u32 [G][N]       unit head per resource-order slot (packed)
-  int mask;              // u64 [G][D][NWA]  slots of each device's units
-  int claim;             // u64 [G][NWA]     slot claims (fast ordering path)
-  int cnt;               // u32 [G*D][ceil(M/2)]  remaining uses per (device, model), two u16 per word
-  int fin;               // time [G][N]      finish of every activation
-  int acc;               // PlanAcc [G]
-  int dev, prio;         // staged rows: G*N int8, G*N uint16            (shared region)
-  int rt;                // time [G][wmax]   latest predecessor finish   (shared region)
-  int stamp;             // u16 [G*D][M]     last use of each model      (shared region)
-  int wfm;               // time [G][W]      latest finish per workflow  (shared region)
+  int flags;   // u8 [G][NB]       staged fuse/prefetch rows
+  int rec;     // u32 [G][N]       slot entry per resource-order slot (packed)
+  int mask;    // u64 [G][D][NWA]  slots of each device's units
+  int last;    // u32 [G][D][M]    1 + slot of the last unit of each (device, model), 0 = none;
+               //                  with the in-register reclamation queues it shares storage
+               //                  with fin (dead before the first finish is written)
+  int fin;     // time [G][N]      latest predecessor finish, then the activation's own finish
+  int acc;     // PlanAcc [G]
+  int stamp;   // u16 [G*D][M]     last use of each model (general reclamation only)
+  int wfm;     // time [G][W]      latest finish per workflow
   int bytes;
 };
 
@@ -79,8 +76,10 @@ struct PlanAcc {
   uint32_t evicts;
   unsigned long long max_finish;  // time bits
   long long p95;                  // selected completion latency (time units)
-  uint32_t bad;                   // ordering fast path failed for the current level
-  uint32_t pad[3];
+  uint32_t heads;                 // unit heads given a slot by the fast ordering path
+  uint32_t claimed;               // distinct slots they occupy
+  uint32_t bad;                   // a head priority outside its level's index range
+  uint32_t pad;
 };
 
 hipError_t launch_score(const ScoreParams& sp, const int8_t* dev, const uint16_t* prio,

@@ -81,9 +81,24 @@ __device__ __forceinline__ int fuse_bit(const uint8_t* fl, int v) {
   return (fl[v >> 2] >> ((v & 3) << 1)) & 1;
 }
 
-// slot entry: activation | model << 16 | prefetch << 22 | has fused successor << 23
+// slot entry: activation | model << 16 | prefetch << 22 | has fused successor << 23 |
+// device << 24 | last unit of its model on the device << 30
 constexpr uint32_t kPf = 1u << 22;
 constexpr uint32_t kChain = 1u << 23;
+constexpr uint32_t kLast = 1u << 30;
+
+// What the device walk needs about one unit that does not depend on the
+// device's sequential state; it is loaded one unit ahead of its use.
+template <typename TT>
+struct UnitPre {
+  uint32_t meta;  // slot entry
+  int slot;       // resource-order slot, -1 past the device's last unit
+  TT arrv;        // workflow arrival
+  TT rtv;         // latest predecessor finish (0 for a source)
+  int32_t lat;    // head run time on the device (-1: ineligible)
+  int32_t mem;    // head activation memory on the device
+  int2 lw;        // model load time on the device, model weights
+};
 
 template <typename TT, bool TAB_LDS, bool NIBBLE, bool WAVE_GLOBAL>
 __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
@@ -96,9 +111,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   using TB = typename TO::bits_t;
   extern __shared__ __align__(16) unsigned char lds[];
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  const int N = sp.N, W = sp.W, M = sp.M, D = sp.D, NB = sp.NB, G = sp.G, WMAX = sp.wmax,
-            NWA = sp.nwa;
-  const int MH = (M + 1) >> 1;
+  const int N = sp.N, W = sp.W, M = sp.M, D = sp.D, NB = sp.NB, G = sp.G, NWA = sp.nwa;
 
   // ---- window tables ----
   const unsigned char* tb;
@@ -123,13 +136,14 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   const int32_t* t_loff = reinterpret_cast<const int32_t*>(tb + sp.t.loff);
   const int32_t* t_lat = reinterpret_cast<const int32_t*>(tb + sp.t.lat);
   const int32_t* t_mem = reinterpret_cast<const int32_t*>(tb + sp.t.mem);
-  const int32_t* t_load = reinterpret_cast<const int32_t*>(tb + sp.t.load);
+  const int2* t_lw = reinterpret_cast<const int2*>(tb + sp.t.lw);
   const int32_t* t_wmib = reinterpret_cast<const int32_t*>(tb + sp.t.wmib);
   const int32_t* t_cap = reinterpret_cast<const int32_t*>(tb + sp.t.cap);
   const TB* t_arr = reinterpret_cast<const TB*>(tb + sp.t.arr);
   const unsigned long long* t_res0 = reinterpret_cast<const unsigned long long*>(tb + sp.t.res0);
   const TB* t_free0 = reinterpret_cast<const TB*>(tb + sp.t.free0);
   const uint32_t* t_sink = reinterpret_cast<const uint32_t*>(tb + sp.t.sink);
+  const int mem_si = sp.mem_si;
 
   // ---- this wave's region (LDS, or HBM scratch for very large windows) ----
   unsigned char* wl;
@@ -140,13 +154,9 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   uint8_t* s_fl = reinterpret_cast<uint8_t*>(wl + sp.wo.flags);
   uint32_t* s_rec = reinterpret_cast<uint32_t*>(wl + sp.wo.rec);
   unsigned long long* s_mask = reinterpret_cast<unsigned long long*>(wl + sp.wo.mask);
-  unsigned long long* s_claim = reinterpret_cast<unsigned long long*>(wl + sp.wo.claim);
-  uint32_t* s_cnt = reinterpret_cast<uint32_t*>(wl + sp.wo.cnt);
+  uint32_t* s_last = reinterpret_cast<uint32_t*>(wl + sp.wo.last);
   TB* s_fin = reinterpret_cast<TB*>(wl + sp.wo.fin);
   PlanAcc* s_acc = reinterpret_cast<PlanAcc*>(wl + sp.wo.acc);
-  int8_t* s_dev = reinterpret_cast<int8_t*>(wl + sp.wo.dev);
-  uint16_t* s_prio = reinterpret_cast<uint16_t*>(wl + sp.wo.prio);
-  TB* s_rt = reinterpret_cast<TB*>(wl + sp.wo.rt);
   uint16_t* s_stamp = reinterpret_cast<uint16_t*>(wl + sp.wo.stamp);
   TB* s_wfm = reinterpret_cast<TB*>(wl + sp.wo.wfm);
 
@@ -154,131 +164,216 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   const int d_me = lane - g_me * D;
   const int64_t n_groups = (P + G - 1) / G;
   const int64_t stride = (int64_t)gridDim.x * sp.waves;
+  // per-device table rows of this lane's device
+  const int32_t* lat_d = t_lat + d_me;
+  const int32_t* mem_d = t_mem + d_me * sp.mem_sd;
+  const int2* lw_d = t_lw + d_me;
 
   for (int64_t grp = (int64_t)blockIdx.x * sp.waves + wid; grp < n_groups; grp += stride) {
     const int64_t p0 = grp * G;
     const int gc = (int)((P - p0) < G ? (P - p0) : G);
 
-    // ---- stage the group's rows ----
-    stage(reinterpret_cast<unsigned char*>(s_dev),
-          reinterpret_cast<const unsigned char*>(dev_all + p0 * N), gc * N, lane);
-    stage(reinterpret_cast<unsigned char*>(s_prio),
-          reinterpret_cast<const unsigned char*>(prio_all + p0 * N), gc * N * 2, lane);
+    // ---- stage the group's flag rows, clear the ordering state ----
     stage(s_fl, flags_all + p0 * NB, gc * NB, lane);
-    for (int i = lane; i < G * D * MH; i += 64) s_cnt[i] = 0u;
+    for (int i = lane; i < G * D * M; i += 64) s_last[i] = 0u;
     for (int i = lane; i < G * D * NWA; i += 64) s_mask[i] = 0ull;
-    for (int i = lane; i < G * NWA; i += 64) s_claim[i] = 0ull;
     if (lane < G) {
-      s_acc[lane].status = 0u;
-      s_acc[lane].headroom = 0x7fffffff;
-      s_acc[lane].loads = 0u;
-      s_acc[lane].evicts = 0u;
-      s_acc[lane].max_finish = 0ull;
-      s_acc[lane].p95 = 0;
+      PlanAcc a0;
+      a0.status = 0u;
+      a0.headroom = 0x7fffffff;
+      a0.loads = 0u;
+      a0.evicts = 0u;
+      a0.max_finish = 0ull;
+      a0.p95 = 0;
+      a0.heads = 0u;
+      a0.claimed = 0u;
+      a0.bad = 0u;
+      a0.pad = 0u;
+      s_acc[lane] = a0;
     }
     wave_sync();
 
-    // ---- resource order of every unit head, remaining uses per (device, model) ----
-    for (int g = 0; g < gc; ++g) {
-      const int8_t* pdev = s_dev + g * N;
-      const uint16_t* pprio = s_prio + g * N;
+    // ---- resource order (Eq. 10), first try: a unit head's slot is its
+    // priority, valid when each level's head priorities are distinct values
+    // in the level's index range (checked below by counting) ----
+    // one activation u of plan g with device d and priority pr
+    auto order_fast = [&](int g, int u, int d, int pr, uint32_t a, uint32_t lvw, uint32_t c,
+                          uint32_t fb, uint32_t& nh, uint32_t& nbad, uint32_t& ninel) {
       const uint8_t* pfl = s_fl + g * NB;
-      uint32_t* cnt = s_cnt + g * D * MH;
+      const uint32_t cbyte = pfl[(c != 0xffffu ? c : (uint32_t)u) >> 2];
+      const bool head = !((fb & 1u) && (a & 64u));  // not a fused chain member
+      const bool okd = (unsigned)d < (unsigned)D;
+      const bool inr = (unsigned)(pr - (int)(lvw & 0xffffu)) < (lvw >> 16);
+      const bool chain = c != 0xffffu && ((cbyte >> ((c & 3u) << 1)) & 1u);
+      ninel |= (uint32_t)(head && !okd);
+      nbad |= (uint32_t)(head && okd && !inr);
+      if (head && okd && inr) {
+        const uint32_t m = a & 63u;
+        s_rec[g * N + pr] = (uint32_t)u | (m << 16) | ((fb & 2u) << 21) | (chain ? kChain : 0u) |
+                            ((uint32_t)d << 24);
+        atomicOr(&s_mask[(g * D + d) * NWA + (pr >> 6)], 1ull << (pr & 63));
+        atomicMax(&s_last[(g * D + d) * M + (int)m], (uint32_t)pr + 1u);
+        ++nh;
+      }
+    };
+    auto order_flush = [&](int g, uint32_t nh, uint32_t nbad, uint32_t ninel) {
+      if (ninel) atomicOr(&s_acc[g].status, (uint32_t)WF_ST_INELIGIBLE);
+      if (nbad) atomicOr(&s_acc[g].bad, 1u);
+      if (nh) atomicAdd(&s_acc[g].heads, nh);
+    };
+    if ((N & 3) == 0 && (reinterpret_cast<uintptr_t>(dev_all) & 3) == 0 &&
+        (reinterpret_cast<uintptr_t>(prio_all) & 7) == 0) {
+      // four consecutive activations per lane: one 4-byte device load, one
+      // 8-byte priority load and one flag byte per plan, issued for up to
+      // eight plans before any is used
+      constexpr int kB = 8;
+      for (int base = 0; base < N; base += 256) {
+        const int u0 = base + 4 * lane;
+        const bool live = u0 < N;
+        const int uc = live ? u0 : 0;
+        const uint4 act4 = *reinterpret_cast<const uint4*>(t_act + uc);
+        const uint4 alv4 = *reinterpret_cast<const uint4*>(t_alv + uc);
+        const uint2 cn4 = *reinterpret_cast<const uint2*>(t_cnext + uc);
+        for (int g0 = 0; g0 < gc; g0 += kB) {
+          uint32_t dv[kB];
+          uint2 pv[kB];
+#pragma unroll
+          for (int k = 0; k < kB; ++k) {
+            const int g = (g0 + k < gc) ? g0 + k : gc - 1;
+            dv[k] = *reinterpret_cast<const uint32_t*>(dev_all + (p0 + g) * N + uc);
+            pv[k] = *reinterpret_cast<const uint2*>(prio_all + (p0 + g) * N + uc);
+          }
+#pragma unroll
+          for (int k = 0; k < kB; ++k) {
+            const int g = g0 + k;
+            if (g >= gc) break;
+            uint32_t nh = 0, nbad = 0, ninel = 0;
+            if (live) {
+              const uint32_t fl = s_fl[g * NB + (uc >> 2)];
+              order_fast(g, uc, (int)(int8_t)(dv[k] & 0xffu), (int)(pv[k].x & 0xffffu), act4.x,
+                         alv4.x, cn4.x & 0xffffu, fl, nh, nbad, ninel);
+              order_fast(g, uc + 1, (int)(int8_t)((dv[k] >> 8) & 0xffu), (int)(pv[k].x >> 16),
+                         act4.y, alv4.y, cn4.x >> 16, fl >> 2, nh, nbad, ninel);
+              order_fast(g, uc + 2, (int)(int8_t)((dv[k] >> 16) & 0xffu), (int)(pv[k].y & 0xffffu),
+                         act4.z, alv4.z, cn4.y & 0xffffu, fl >> 4, nh, nbad, ninel);
+              order_fast(g, uc + 3, (int)(int8_t)(dv[k] >> 24), (int)(pv[k].y >> 16), act4.w,
+                         alv4.w, cn4.y >> 16, fl >> 6, nh, nbad, ninel);
+            }
+            order_flush(g, nh, nbad, ninel);
+          }
+        }
+      }
+    } else {
+      for (int g = 0; g < gc; ++g) {
+        const int8_t* pdev = dev_all + (p0 + g) * N;
+        const uint16_t* pprio = prio_all + (p0 + g) * N;
+        uint32_t nh = 0, nbad = 0, ninel = 0;
+        for (int u = lane; u < N; u += 64) {
+          const uint32_t fb = (uint32_t)s_fl[g * NB + (u >> 2)] >> ((u & 3) << 1);
+          order_fast(g, u, pdev[u], pprio[u], t_act[u], t_alv[u], t_cnext[u], fb, nh, nbad, ninel);
+        }
+        order_flush(g, nh, nbad, ninel);
+      }
+    }
+    wave_sync();
+    // distinct slots claimed per plan: the union of its devices' masks
+    for (int i = lane; i < gc * NWA; i += 64) {
+      const int g = i / NWA, w = i - g * NWA;
+      unsigned long long x = 0ull;
+      for (int d = 0; d < D; ++d) x |= s_mask[(g * D + d) * NWA + w];
+      if (x) atomicAdd(&s_acc[g].claimed, (uint32_t)__popcll(x));
+    }
+    wave_sync();
+    // general path: rank by (priority, index) within each level
+    for (int g = 0; g < gc; ++g) {
+      if (!s_acc[g].bad && s_acc[g].heads == s_acc[g].claimed) continue;
+      const int8_t* pdev = dev_all + (p0 + g) * N;
+      const uint16_t* pprio = prio_all + (p0 + g) * N;
+      const uint8_t* pfl = s_fl + g * NB;
       uint32_t* rec = s_rec + g * N;
       unsigned long long* mk = s_mask + g * D * NWA;
-      unsigned long long* cl = s_claim + g * NWA;
-      int bad = 0;
+      uint32_t* lastp = s_last + g * D * M;
+      for (int i = lane; i < D * NWA; i += 64) mk[i] = 0ull;
+      for (int i = lane; i < D * M; i += 64) lastp[i] = 0u;
+      wave_sync();
       for (int u = lane; u < N; u += 64) {
         const uint32_t a = t_act[u];
         const int fb = pfl[u >> 2] >> ((u & 3) << 1);
-        if ((fb & 1) && (a & 64u)) continue;  // chain member
+        if ((fb & 1) && (a & 64u)) continue;
         const int d = pdev[u];
-        if ((unsigned)d >= (unsigned)D) {
-          atomicOr(&s_acc[g].status, (uint32_t)WF_ST_INELIGIBLE);
-          continue;
-        }
-        const int m = (int)(a & 63u);
-        atomicAdd(&cnt[d * MH + (m >> 1)], 1u << ((m & 1) << 4));
-        // fast path: the slot is the priority when the level's head
-        // priorities are distinct values in the level's index range
+        if ((unsigned)d >= (unsigned)D) continue;
         const uint32_t lvw = t_alv[u];
-        const int slot = (int)pprio[u];
-        if ((unsigned)(slot - (int)(lvw & 0xffffu)) >= (lvw >> 16)) {
-          bad = 1;
-          continue;
-        }
-        const unsigned long long bit = 1ull << (slot & 63);
-        if (atomicOr(&cl[slot >> 6], bit) & bit) {
-          bad = 1;
-          continue;
+        const int lo = (int)(lvw & 0xffffu), hi = lo + (int)(lvw >> 16);
+        const int pu = pprio[u];
+        int slot = lo;
+        for (int j = lo; j < hi; ++j) {
+          if (fuse_bit(pfl, j) && (t_act[j] & 64u)) continue;
+          if ((unsigned)pdev[j] >= (unsigned)D) continue;
+          const int pj = pprio[j];
+          slot += (pj < pu) || (pj == pu && j < u);
         }
         const int c = t_cnext[u];
         const uint32_t chain = (c != 0xffff && fuse_bit(pfl, c)) ? kChain : 0u;
-        rec[slot] = (uint32_t)u | ((a & 63u) << 16) | ((uint32_t)((fb >> 1) & 1) << 22) | chain;
-        atomicOr(&mk[d * NWA + (slot >> 6)], bit);
+        rec[slot] = (uint32_t)u | ((a & 63u) << 16) | ((uint32_t)((fb >> 1) & 1) << 22) | chain |
+                    ((uint32_t)d << 24);
+        atomicOr(&mk[d * NWA + (slot >> 6)], 1ull << (slot & 63));
+        atomicMax(&lastp[d * M + (int)(a & 63u)], (uint32_t)slot + 1u);
       }
-      if (__any(bad)) {  // general path: rank by (priority, index) within each level
-        wave_sync();
-        for (int i = lane; i < D * NWA; i += 64) mk[i] = 0ull;
-        wave_sync();
-        for (int u = lane; u < N; u += 64) {
-          const uint32_t a = t_act[u];
-          const int fb = pfl[u >> 2] >> ((u & 3) << 1);
-          if ((fb & 1) && (a & 64u)) continue;
-          const int d = pdev[u];
-          if ((unsigned)d >= (unsigned)D) continue;
-          const uint32_t lvw = t_alv[u];
-          const int lo = (int)(lvw & 0xffffu), hi = lo + (int)(lvw >> 16);
-          const int pu = pprio[u];
-          int slot = lo;
-          for (int j = lo; j < hi; ++j) {
-            if (fuse_bit(pfl, j) && (t_act[j] & 64u)) continue;
-            if ((unsigned)pdev[j] >= (unsigned)D) continue;
-            const int pj = pprio[j];
-            slot += (pj < pu) || (pj == pu && j < u);
-          }
-          const int c = t_cnext[u];
-          const uint32_t chain = (c != 0xffff && fuse_bit(pfl, c)) ? kChain : 0u;
-          rec[slot] = (uint32_t)u | ((a & 63u) << 16) | ((uint32_t)((fb >> 1) & 1) << 22) | chain;
-          atomicOr(&mk[d * NWA + (slot >> 6)], 1ull << (slot & 63));
+      wave_sync();
+    }
+    wave_sync();
+    if constexpr (NIBBLE) {
+      // mark each (device, model)'s last unit in its slot entry: the
+      // reclamation queues need only that bit, and last[] dies here
+      for (int g = 0; g < gc; ++g) {
+        uint32_t* rec = s_rec + g * N;
+        const unsigned long long* mk = s_mask + g * D * NWA;
+        const uint32_t* lastp = s_last + g * D * M;
+        for (int sl = lane; sl < N; sl += 64) {
+          const uint32_t e = rec[sl];
+          const int d = (int)((e >> 24) & 63u);
+          const int m = (int)((e >> 16) & 63u);
+          // entries of empty slots are stale: d, m may be anything below 64
+          const bool occ = d < D && m < M && ((mk[d * NWA + (sl >> 6)] >> (sl & 63)) & 1ull);
+          if (occ && lastp[d * M + m] == (uint32_t)sl + 1u) rec[sl] = e | kLast;
         }
       }
     }
-    wave_sync();
 
-    // ---- device-lane state (the staged rows are dead from here on) ----
-    for (int i = lane; i < G * W; i += 64) s_wfm[i] = 0;
+    // ---- device-lane state ----
     const bool act = g_me < gc;
     const int gme = act ? g_me : 0;
     const int64_t pw = p0 + gme;
-    uint32_t* mycnt = s_cnt + (gme * D + d_me) * MH;
+    const uint32_t* mylast = s_last + (gme * D + d_me) * M;
     uint16_t* mystamp = s_stamp + (gme * D + d_me) * M;
     const unsigned long long* mymask = s_mask + (gme * D + d_me) * NWA;
     const uint32_t* myrec = s_rec + gme * N;
-    const TB* myrt = s_rt + gme * WMAX;
     TB* myfin = s_fin + gme * N;
     const uint8_t* myfl = s_fl + gme * NB;
+    const int d = d_me;
     uint64_t res = 0;
     int32_t used = 0, peak = 0, capd = 0;
     TT freet = 0;
     uint32_t nld = 0, nev = 0, capbad = 0, inel = 0;
     uint32_t seq = 1;
-    // reclamation queues (at most 16 models): resident models with no
-    // remaining use on this device (qd) and with remaining uses (qa), each in
-    // least-recently-used order (never used: by id), 4 bits per entry, next
-    // victim in the low bits; a victim comes from qd first
-    uint64_t qd = 0, qa = 0;
-    int nd = 0, na = 0;
+    // reclamation queue (at most 16 models), 4 bits per entry, next victim
+    // in the low bits: first the nd resident models with no remaining use on
+    // this device, then those still needed, each part in least-recently-used
+    // order (never used: by id); nq entries in all
+    uint64_t Q = 0;
+    int nd = 0, nq = 0;
     if (act) {
-      res = t_res0[d_me];
-      capd = t_cap[d_me];
-      freet = TO::load(t_free0 + d_me);
+      res = t_res0[d];
+      capd = t_cap[d];
+      freet = TO::load(t_free0 + d);
+      uint64_t qa = 0;
+      int na = 0;
       for (uint64_t r = res; r; r &= r - 1) {
         const int m = __builtin_ctzll(r);
         used += t_wmib[m];
         if constexpr (NIBBLE) {
-          if (((mycnt[m >> 1] >> ((m & 1) << 4)) & 0xffffu) == 0u) {
-            qd |= (uint64_t)m << (4 * nd);
+          if (mylast[m] == 0u) {
+            Q |= (uint64_t)m << (4 * nd);
             ++nd;
           } else {
             qa |= (uint64_t)m << (4 * na);
@@ -288,22 +383,31 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
           mystamp[m] = 0;
         }
       }
+      if constexpr (NIBBLE) {
+        if (na) Q |= qa << (4 * nd);  // nd + na <= 16, so nd < 16 here
+        nq = nd + na;
+      }
       peak = used;
     }
+    if constexpr (NIBBLE) wave_sync();  // last[] (aliasing fin) is read above
+    // every finish starts at 0: it accumulates the latest predecessor finish
+    // before its level, then holds the activation's own finish
+    for (int i = lane; i < G * N; i += 64) s_fin[i] = 0;
+    for (int i = lane; i < G * W; i += 64) s_wfm[i] = 0;
+    wave_sync();
 
     for (int lv = 0; lv < sp.n_levels; ++lv) {
-      const int lo = t_loff[lv], hi = t_loff[lv + 1], wlv = hi - lo;
+      const int lo = t_loff[lv], hi = t_loff[lv + 1];
       const int e0 = t_eoff[lv], e1 = t_eoff[lv + 1];
-      // ---- latest predecessor finish of the level's activations (Eq. 2) ----
+      // ---- latest predecessor finish of the level's activations (Eq. 2):
+      // one lane per incoming edge.  A fused chain member already holds its
+      // own finish, which is later than its only predecessor's ----
       if (e1 > e0) {
         for (int g = 0; g < gc; ++g) {
-          TB* rt = s_rt + g * WMAX;
-          for (int i = lane; i < wlv; i += 64) rt[i] = 0;
-          wave_sync();
-          const TB* fin = s_fin + g * N;
+          TB* fin = s_fin + g * N;
           for (int e = e0 + lane; e < e1; e += 64) {
             const uint32_t ed = t_edge[e];
-            atomicMax(&rt[(int)(ed >> 16) - lo], fin[ed & 0xffffu]);
+            atomicMax(&fin[ed >> 16], fin[ed & 0xffffu]);
           }
         }
         wave_sync();
@@ -311,141 +415,176 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
 
       // ---- device lanes walk their units of this level in slot order ----
       if (act) {
-        const int d = d_me;
-        const int j0 = lo >> 6, j1 = (hi - 1) >> 6;
-        for (int j = j0; j <= j1; ++j) {
-          unsigned long long bits = mymask[j];
-          if (j == j0) bits &= ~0ull << (lo & 63);
-          if (j == j1 && (hi & 63)) bits &= (1ull << (hi & 63)) - 1ull;
-          while (bits) {
-            const int slot = (j << 6) + __builtin_ctzll(bits);
-            bits &= bits - 1;
-            const uint32_t meta = myrec[slot];
-            const int u = (int)(meta & 0xffffu);
-            const int m = (int)((meta >> 16) & 63u);
-            const TT arrv = TO::load(t_aarr + u);
-            const TT r = (e1 > e0) ? TO::tmax(TO::load(myrt + (u - lo)), arrv) : arrv;
-            // run time (summed over a fused chain, Eq. 4) and memory (max)
-            const int32_t l0 = t_lat[u * D + d];
-            int32_t mxu = t_mem[u * sp.mem_si + d * sp.mem_sd];
-            inel |= (uint32_t)(l0 < 0);
-            uint32_t T = (uint32_t)l0;
-            if (meta & kChain) {
-              for (int v = t_cnext[u];;) {
-                const int32_t lv2 = t_lat[v * D + d];
-                const int32_t mv = t_mem[v * sp.mem_si + d * sp.mem_sd];
-                inel |= (uint32_t)(lv2 < 0);
-                T += (uint32_t)lv2;
-                mxu = mv > mxu ? mv : mxu;
-                const int c = t_cnext[v];
-                if (c == 0xffff || !fuse_bit(myfl, c)) break;
-                v = c;
-              }
-            }
-            // one remaining use of m on this device consumed
-            const int sh = (m & 1) << 4;
-            const uint32_t cword = mycnt[m >> 1] - (1u << sh);
-            mycnt[m >> 1] = cword;
-            const bool last_use = ((cword >> sh) & 0xffffu) == 0u;
-            const uint64_t mb = 1ull << m;
-            const bool hit = (res & mb) != 0ull;
-            const int32_t wm = t_wmib[m];
-            const int32_t need = (hit ? 0 : wm) + mxu;
-            // reclaim (Sec. 3.5): a copy with no remaining use first, else the
-            // least recently used, else the lower model id
-            if constexpr (NIBBLE) {
-              if (hit) {  // m is in qa: take it out, it re-enters as most recent
-                const uint64_t x = qa ^ (0x1111111111111111ull * (uint64_t)m);
-                const uint64_t z = (x - 0x1111111111111111ull) & ~x & 0x8888888888888888ull;
-                const int s4 = __builtin_ctzll(z) & ~3;  // 4 * position
-                const uint64_t low = qa & ((1ull << s4) - 1ull);
-                const uint64_t high = (s4 >= 60) ? 0ull : ((qa >> (s4 + 4)) << s4);
-                qa = low | high;
-                --na;
-              }
-              while (used + need > capd && (nd | na)) {
-                int v;
-                if (nd) {
-                  v = (int)(qd & 15ull);
-                  qd >>= 4;
-                  --nd;
-                } else {
-                  v = (int)(qa & 15ull);
-                  qa >>= 4;
-                  --na;
-                }
-                res &= ~(1ull << v);
-                used -= t_wmib[v];
-                ++nev;
-              }
-              if (last_use) {
-                qd |= (uint64_t)m << (4 * nd);
-                ++nd;
-              } else {
-                qa |= (uint64_t)m << (4 * na);
-                ++na;
-              }
-            } else {
-              while (used + need > capd) {
-                uint64_t cand = res & ~mb;
-                if (!cand) break;
-                int v = 0;
-                uint32_t best = 0xffffffffu;
-                while (cand) {
-                  const int m2 = __builtin_ctzll(cand);
-                  cand &= cand - 1;
-                  const uint32_t alive = ((mycnt[m2 >> 1] >> ((m2 & 1) << 4)) & 0xffffu) != 0u;
-                  const uint32_t key = (alive << 16) | mystamp[m2];
-                  if (key < best) {
-                    best = key;
-                    v = m2;
-                  }
-                }
-                res &= ~(1ull << v);
-                used -= t_wmib[v];
-                ++nev;
-              }
-              mystamp[m] = (uint16_t)seq++;
-            }
-            capbad |= (uint32_t)(used + need > capd);
-            // timeline (Eq. 7): a load waits for the device and starts at the
-            // release, or at the workflow arrival when prefetched
-            const TT ls = TO::tmax((meta & kPf) ? arrv : r, freet);
-            const TT le = TO::add(ls, (uint32_t)t_load[m * D + d]);
-            const TT s = TO::tmax(r, hit ? freet : le);
-            if (!hit) {
-              res |= mb;
-              used += wm;
-              ++nld;
-            }
-            peak = (used + mxu) > peak ? (used + mxu) : peak;
-            const TT f = TO::add(s, T);
-            freet = f;
-            if (!(meta & kChain)) {
-              myfin[u] = TO::bits(f);
-              if (has_sched) {
-                sched.start_us[pw * N + u] = sp.origin + TO::i64(s);
-                sched.finish_us[pw * N + u] = sp.origin + TO::i64(f);
-                sched.load_start_us[pw * N + u] = hit ? (int64_t)-1 : sp.origin + TO::i64(ls);
-              }
-            } else {
-              TT t = s;
-              for (int v = u;;) {
-                const TT tv = TO::add(t, (uint32_t)t_lat[v * D + d]);
-                myfin[v] = TO::bits(tv);
-                if (has_sched) {
-                  sched.start_us[pw * N + v] = sp.origin + TO::i64(t);
-                  sched.finish_us[pw * N + v] = sp.origin + TO::i64(tv);
-                  sched.load_start_us[pw * N + v] =
-                      (v == u && !hit) ? sp.origin + TO::i64(ls) : (int64_t)-1;
-                }
-                t = tv;
-                const int c = t_cnext[v];
-                if (c == 0xffff || !fuse_bit(myfl, c)) break;
-                v = c;
-              }
+        const int j1 = (hi - 1) >> 6;
+        const unsigned long long hmask = (hi & 63) ? ((1ull << (hi & 63)) - 1ull) : ~0ull;
+        int j = lo >> 6;
+        unsigned long long bits = mymask[j] & (~0ull << (lo & 63));
+        if (j == j1) bits &= hmask;
+        // the device's next slot in the level, -1 when there is none
+        auto next_slot = [&]() -> int {
+          while (!bits && j < j1) {
+            ++j;
+            bits = mymask[j];
+            if (j == j1) bits &= hmask;
+          }
+          if (!bits) return -1;
+          const int sl = (j << 6) + __builtin_ctzll(bits);
+          bits &= bits - 1ull;
+          return sl;
+        };
+        // slot entry; past the end a stand-in (activation lo, model 0) keeps
+        // every address below in range
+        auto entry = [&](int sl) -> uint32_t {
+          const uint32_t keep = (uint32_t)~(sl >> 31);  // all ones for a real slot
+          const uint32_t raw = myrec[(int)((uint32_t)sl & keep)];
+          return (raw & keep) | ((uint32_t)lo & ~keep);
+        };
+        auto fetch = [&](int sl, uint32_t meta, UnitPre<TT>& p) {
+          const uint32_t u = meta & 0xffffu, m = (meta >> 16) & 63u;
+          p.meta = meta;
+          p.slot = sl;
+          p.arrv = TO::load(t_aarr + u);
+          p.rtv = TO::load(myfin + u);
+          p.lat = lat_d[__umul24(u, (uint32_t)D)];
+          p.mem = mem_d[__umul24(u, (uint32_t)mem_si)];
+          p.lw = lw_d[__umul24(m, (uint32_t)D)];
+        };
+        UnitPre<TT> A;
+        {
+          const int sa = next_slot();
+          fetch(sa, entry(sa), A);
+        }
+        int sb = A.slot >= 0 ? next_slot() : -1;
+        uint32_t mb_next = entry(sb);
+        while (A.slot >= 0) {
+          const int u = (int)(A.meta & 0xffffu);
+          const int m = (int)((A.meta >> 16) & 63u);
+          const uint64_t mbit = 1ull << m;
+          const bool hit = ((res >> m) & 1ull) != 0ull;
+          int32_t w0 = 0, w1 = 0;
+          if constexpr (NIBBLE) {
+            // a hit model sits in the still-needed part: take it out, it
+            // re-enters as the most recent
+            const uint64_t x = Q ^ (0x1111111111111111ull * (uint64_t)m);
+            const uint64_t z = (x - 0x1111111111111111ull) & ~x & 0x8888888888888888ull;
+            const int s4 = __builtin_ctzll(z | (1ull << 63)) & ~3;  // 4 * position
+            const uint64_t low = Q & ((1ull << s4) - 1ull);
+            const uint64_t high = (s4 >= 60) ? 0ull : ((Q >> (s4 + 4)) << s4);
+            Q = hit ? (low | high) : Q;
+            nq -= hit ? 1 : 0;
+            // the first two victims' weights, looked up ahead of need
+            w0 = t_wmib[(int)(Q & 15ull)];
+            w1 = t_wmib[(int)((Q >> 4) & 15ull)];
+          }
+          // the next unit's tables and the one after's slot entry
+          UnitPre<TT> B;
+          fetch(sb, mb_next, B);
+          const int sc = sb >= 0 ? next_slot() : -1;
+          const uint32_t mc = entry(sc);
+
+          const TT r = TO::tmax(A.rtv, A.arrv);
+          // run time (summed over a fused chain, Eq. 4) and memory (max)
+          int32_t mxu = A.mem;
+          inel |= (uint32_t)(A.lat < 0);
+          uint32_t T = (uint32_t)A.lat;
+          if (A.meta & kChain) {
+            for (int v = t_cnext[u];;) {
+              const int32_t lv2 = lat_d[__umul24((uint32_t)v, (uint32_t)D)];
+              const int32_t mv = mem_d[__umul24((uint32_t)v, (uint32_t)mem_si)];
+              inel |= (uint32_t)(lv2 < 0);
+              T += (uint32_t)lv2;
+              mxu = mv > mxu ? mv : mxu;
+              const int c = t_cnext[v];
+              if (c == 0xffff || !fuse_bit(myfl, c)) break;
+              v = c;
             }
           }
+          const int32_t need = (hit ? 0 : A.lw.y) + mxu;
+          // reclaim (Sec. 3.5): a copy with no remaining use first, else the
+          // least recently used, else the lower model id
+          if constexpr (NIBBLE) {
+            int t = 0;
+            while (used + need > capd && nq > 0) {
+              const int v = (int)(Q & 15ull);
+              Q >>= 4;
+              --nq;
+              nd = nd > 0 ? nd - 1 : 0;
+              int32_t wv = t ? w1 : w0;
+              if (t >= 2) wv = t_wmib[v];
+              res &= ~(1ull << v);
+              used -= wv;
+              ++nev;
+              ++t;
+            }
+            // m re-enters after the no-remaining-use part when this was its
+            // last unit on the device, else at the end
+            const bool last_use = (A.meta & kLast) != 0u;
+            const int pos = 4 * (last_use ? nd : nq);  // nq <= 15 here
+            const uint64_t lowm = (1ull << pos) - 1ull;
+            Q = (Q & lowm) | ((uint64_t)m << pos) | ((Q & ~lowm) << 4);
+            nd += last_use ? 1 : 0;
+            ++nq;
+          } else {
+            while (used + need > capd) {
+              uint64_t cand = res & ~mbit;
+              if (!cand) break;
+              int v = 0;
+              uint32_t best = 0xffffffffu;
+              while (cand) {
+                const int m2 = __builtin_ctzll(cand);
+                cand &= cand - 1;
+                const uint32_t alive = mylast[m2] > (uint32_t)A.slot + 1u;
+                const uint32_t key = (alive << 16) | mystamp[m2];
+                if (key < best) {
+                  best = key;
+                  v = m2;
+                }
+              }
+              res &= ~(1ull << v);
+              used -= t_wmib[v];
+              ++nev;
+            }
+            mystamp[m] = (uint16_t)seq++;
+          }
+          capbad |= (uint32_t)(used + need > capd);
+          // timeline (Eq. 7): a load waits for the device and starts at the
+          // release, or at the workflow arrival when prefetched
+          const TT ls = TO::tmax((A.meta & kPf) ? A.arrv : r, freet);
+          const TT le = TO::add(ls, (uint32_t)A.lw.x);
+          const TT s = TO::tmax(r, hit ? freet : le);
+          res |= mbit;
+          used += hit ? 0 : A.lw.y;
+          nld += hit ? 0u : 1u;
+          peak = (used + mxu) > peak ? (used + mxu) : peak;
+          const TT f = TO::add(s, T);
+          freet = f;
+          if (!(A.meta & kChain)) {
+            myfin[u] = TO::bits(f);
+            if (has_sched) {
+              sched.start_us[pw * N + u] = sp.origin + TO::i64(s);
+              sched.finish_us[pw * N + u] = sp.origin + TO::i64(f);
+              sched.load_start_us[pw * N + u] = hit ? (int64_t)-1 : sp.origin + TO::i64(ls);
+            }
+          } else {
+            TT t = s;
+            for (int v = u;;) {
+              const TT tv = TO::add(t, (uint32_t)lat_d[__umul24((uint32_t)v, (uint32_t)D)]);
+              myfin[v] = TO::bits(tv);
+              if (has_sched) {
+                sched.start_us[pw * N + v] = sp.origin + TO::i64(t);
+                sched.finish_us[pw * N + v] = sp.origin + TO::i64(tv);
+                sched.load_start_us[pw * N + v] =
+                    (v == u && !hit) ? sp.origin + TO::i64(ls) : (int64_t)-1;
+              }
+              t = tv;
+              const int c = t_cnext[v];
+              if (c == 0xffff || !fuse_bit(myfl, c)) break;
+              v = c;
+            }
+          }
+          A = B;
+          sb = sc;
+          mb_next = mc;
         }
       }
       wave_sync();
