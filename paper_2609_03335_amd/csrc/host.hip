@@ -394,6 +394,8 @@ wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, Image& img, wfp::Sc
   sp.w_p95 = h.w_p95;
   sp.time64 = time64 ? 1 : 0;
   sp.nibble = M <= 16 ? 1 : 0;
+  sp.has_chains = 0;
+  for (int32_t i = 0; i < N; ++i) sp.has_chains |= h.chain_next[i] >= 0 ? 1 : 0;
 
   // ---- plans per wave, waves per workgroup, table placement ----
   const int lds_cu = std::min(ctx->lds_per_cu, 160 * 1024);

@@ -66,6 +66,7 @@ struct ScoreParams {
   int grid;                   // workgroups (persistent)
   int time64;                 // 1: fp64 times, 0: uint32 times
   int nibble;                 // 1: M <= 16, in-register reclamation queue
+  int has_chains;             // 1: some activation satisfies Eq. 3 (fused units possible)
 };
 
 // Per-plan accumulators kept in LDS by the scoring kernel.

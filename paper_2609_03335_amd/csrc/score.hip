@@ -42,6 +42,7 @@ struct TimeOps<uint32_t> {
   __device__ static bits_t bits(uint32_t t) { return t; }
   __device__ static uint32_t tmax(uint32_t a, uint32_t b) { return a > b ? a : b; }
   __device__ static uint32_t add(uint32_t a, uint32_t d) { return a + d; }
+  __device__ static uint32_t sub(uint32_t a, uint32_t b) { return a - b; }
   __device__ static int64_t i64(uint32_t t) { return (int64_t)t; }
 };
 
@@ -52,6 +53,7 @@ struct TimeOps<double> {
   __device__ static bits_t bits(double t) { return (bits_t)__double_as_longlong(t); }
   __device__ static double tmax(double a, double b) { return fmax(a, b); }
   __device__ static double add(double a, uint32_t d) { return a + (double)d; }
+  __device__ static double sub(double a, double b) { return a - b; }
   __device__ static int64_t i64(double t) { return (int64_t)t; }
 };
 
@@ -169,6 +171,31 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   const int32_t* mem_d = t_mem + d_me * sp.mem_sd;
   const int2* lw_d = t_lw + d_me;
 
+  // rows read four activations per lane with 4- and 8-byte loads
+  const bool vec = (N & 3) == 0 && (reinterpret_cast<uintptr_t>(dev_all) & 3) == 0 &&
+                   (reinterpret_cast<uintptr_t>(prio_all) & 7) == 0;
+  // one 256-activation chunk and at most eight plans per group: the next
+  // group's device and priority rows are loaded while this group is walked
+  constexpr int kB = 8;
+  const bool pre = vec && N <= 256 && G <= kB;
+  uint32_t dvp[kB];
+  uint2 pvp[kB];
+  auto load_rows = [&](int64_t grp_, uint32_t* dv, uint2* pv) {
+    const int64_t q0 = grp_ * G;
+    const int gq = (int)((P - q0) < G ? (P - q0) : G);
+    const int uc = 4 * lane < N ? 4 * lane : 0;
+#pragma unroll
+    for (int k = 0; k < kB; ++k) {
+      const int g = k < gq ? k : gq - 1;
+      dv[k] = *reinterpret_cast<const uint32_t*>(dev_all + (q0 + g) * N + uc);
+      pv[k] = *reinterpret_cast<const uint2*>(prio_all + (q0 + g) * N + uc);
+    }
+  };
+  {
+    const int64_t g_first = (int64_t)blockIdx.x * sp.waves + wid;
+    if (pre && g_first < n_groups) load_rows(g_first, dvp, pvp);
+  }
+
   for (int64_t grp = (int64_t)blockIdx.x * sp.waves + wid; grp < n_groups; grp += stride) {
     const int64_t p0 = grp * G;
     const int gc = (int)((P - p0) < G ? (P - p0) : G);
@@ -196,11 +223,11 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
     // ---- resource order (Eq. 10), first try: a unit head's slot is its
     // priority, valid when each level's head priorities are distinct values
     // in the level's index range (checked below by counting) ----
-    // one activation u of plan g with device d and priority pr
+    // one activation u of plan g with device d and priority pr; cbyte is the
+    // flag byte of u's chain successor
     auto order_fast = [&](int g, int u, int d, int pr, uint32_t a, uint32_t lvw, uint32_t c,
-                          uint32_t fb, uint32_t& nh, uint32_t& nbad, uint32_t& ninel) {
-      const uint8_t* pfl = s_fl + g * NB;
-      const uint32_t cbyte = pfl[(c != 0xffffu ? c : (uint32_t)u) >> 2];
+                          uint32_t fb, uint32_t cbyte, uint32_t& nh, uint32_t& nbad,
+                          uint32_t& ninel) {
       const bool head = !((fb & 1u) && (a & 64u));  // not a fused chain member
       const bool okd = (unsigned)d < (unsigned)D;
       const bool inr = (unsigned)(pr - (int)(lvw & 0xffffu)) < (lvw >> 16);
@@ -216,17 +243,38 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
         ++nh;
       }
     };
-    auto order_flush = [&](int g, uint32_t nh, uint32_t nbad, uint32_t ninel) {
-      if (ninel) atomicOr(&s_acc[g].status, (uint32_t)WF_ST_INELIGIBLE);
-      if (nbad) atomicOr(&s_acc[g].bad, 1u);
-      if (nh) atomicAdd(&s_acc[g].heads, nh);
+    // per-plan totals from uniform control flow, at most 4 heads per lane:
+    // wave ballots instead of 64 conflicting LDS atomics
+    auto order_flush4 = [&](int g, uint32_t nh, uint32_t nbad, uint32_t ninel) {
+      const uint32_t tot = (uint32_t)__popcll(__ballot(nh & 1u)) +
+                           2u * (uint32_t)__popcll(__ballot(nh & 2u)) +
+                           4u * (uint32_t)__popcll(__ballot(nh & 4u));
+      const bool any_bad = __ballot(nbad != 0u) != 0ull;
+      const bool any_inel = __ballot(ninel != 0u) != 0ull;
+      if (lane == 0) {
+        if (any_inel) s_acc[g].status |= (uint32_t)WF_ST_INELIGIBLE;
+        if (any_bad) s_acc[g].bad = 1u;
+        s_acc[g].heads += tot;
+      }
     };
-    if ((N & 3) == 0 && (reinterpret_cast<uintptr_t>(dev_all) & 3) == 0 &&
-        (reinterpret_cast<uintptr_t>(prio_all) & 7) == 0) {
+    // the rows of plans g0 .. g0 + kB - 1 at activations uc .. uc + 3
+    auto rows4 = [&](int g0, int uc, uint32_t* dv, uint2* pv) {
+#pragma unroll
+      for (int k = 0; k < kB; ++k) {
+        const int g = (g0 + k < gc) ? g0 + k : gc - 1;
+        if (pre) {
+          dv[k] = dvp[k];
+          pv[k] = pvp[k];
+        } else {
+          dv[k] = *reinterpret_cast<const uint32_t*>(dev_all + (p0 + g) * N + uc);
+          pv[k] = *reinterpret_cast<const uint2*>(prio_all + (p0 + g) * N + uc);
+        }
+      }
+    };
+    if (vec) {
       // four consecutive activations per lane: one 4-byte device load, one
-      // 8-byte priority load and one flag byte per plan, issued for up to
-      // eight plans before any is used
-      constexpr int kB = 8;
+      // 8-byte priority load and one flag byte per plan; every load of a
+      // batch of plans is issued before any of it is used
       for (int base = 0; base < N; base += 256) {
         const int u0 = base + 4 * lane;
         const bool live = u0 < N;
@@ -234,14 +282,19 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
         const uint4 act4 = *reinterpret_cast<const uint4*>(t_act + uc);
         const uint4 alv4 = *reinterpret_cast<const uint4*>(t_alv + uc);
         const uint2 cn4 = *reinterpret_cast<const uint2*>(t_cnext + uc);
+        const uint32_t cn[4] = {cn4.x & 0xffffu, cn4.x >> 16, cn4.y & 0xffffu, cn4.y >> 16};
         for (int g0 = 0; g0 < gc; g0 += kB) {
-          uint32_t dv[kB];
+          uint32_t dv[kB], fl[kB], cb[kB][4];
           uint2 pv[kB];
+          rows4(g0, uc, dv, pv);
 #pragma unroll
           for (int k = 0; k < kB; ++k) {
             const int g = (g0 + k < gc) ? g0 + k : gc - 1;
-            dv[k] = *reinterpret_cast<const uint32_t*>(dev_all + (p0 + g) * N + uc);
-            pv[k] = *reinterpret_cast<const uint2*>(prio_all + (p0 + g) * N + uc);
+            fl[k] = s_fl[g * NB + (uc >> 2)];
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+              cb[k][j] = sp.has_chains ? s_fl[g * NB + ((cn[j] != 0xffffu ? cn[j] : (uint32_t)uc) >> 2)]
+                                       : 0u;
           }
 #pragma unroll
           for (int k = 0; k < kB; ++k) {
@@ -249,17 +302,16 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
             if (g >= gc) break;
             uint32_t nh = 0, nbad = 0, ninel = 0;
             if (live) {
-              const uint32_t fl = s_fl[g * NB + (uc >> 2)];
               order_fast(g, uc, (int)(int8_t)(dv[k] & 0xffu), (int)(pv[k].x & 0xffffu), act4.x,
-                         alv4.x, cn4.x & 0xffffu, fl, nh, nbad, ninel);
+                         alv4.x, cn[0], fl[k], cb[k][0], nh, nbad, ninel);
               order_fast(g, uc + 1, (int)(int8_t)((dv[k] >> 8) & 0xffu), (int)(pv[k].x >> 16),
-                         act4.y, alv4.y, cn4.x >> 16, fl >> 2, nh, nbad, ninel);
+                         act4.y, alv4.y, cn[1], fl[k] >> 2, cb[k][1], nh, nbad, ninel);
               order_fast(g, uc + 2, (int)(int8_t)((dv[k] >> 16) & 0xffu), (int)(pv[k].y & 0xffffu),
-                         act4.z, alv4.z, cn4.y & 0xffffu, fl >> 4, nh, nbad, ninel);
+                         act4.z, alv4.z, cn[2], fl[k] >> 4, cb[k][2], nh, nbad, ninel);
               order_fast(g, uc + 3, (int)(int8_t)(dv[k] >> 24), (int)(pv[k].y >> 16), act4.w,
-                         alv4.w, cn4.y >> 16, fl >> 6, nh, nbad, ninel);
+                         alv4.w, cn[3], fl[k] >> 6, cb[k][3], nh, nbad, ninel);
             }
-            order_flush(g, nh, nbad, ninel);
+            order_flush4(g, nh, nbad, ninel);
           }
         }
       }
@@ -267,12 +319,17 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
       for (int g = 0; g < gc; ++g) {
         const int8_t* pdev = dev_all + (p0 + g) * N;
         const uint16_t* pprio = prio_all + (p0 + g) * N;
+        const uint8_t* pfl = s_fl + g * NB;
         uint32_t nh = 0, nbad = 0, ninel = 0;
         for (int u = lane; u < N; u += 64) {
-          const uint32_t fb = (uint32_t)s_fl[g * NB + (u >> 2)] >> ((u & 3) << 1);
-          order_fast(g, u, pdev[u], pprio[u], t_act[u], t_alv[u], t_cnext[u], fb, nh, nbad, ninel);
+          const uint32_t fb = (uint32_t)pfl[u >> 2] >> ((u & 3) << 1);
+          const uint32_t c = t_cnext[u];
+          const uint32_t cbyte = pfl[(c != 0xffffu ? c : (uint32_t)u) >> 2];
+          order_fast(g, u, pdev[u], pprio[u], t_act[u], t_alv[u], c, fb, cbyte, nh, nbad, ninel);
         }
-        order_flush(g, nh, nbad, ninel);
+        if (ninel) atomicOr(&s_acc[g].status, (uint32_t)WF_ST_INELIGIBLE);
+        if (nbad) atomicOr(&s_acc[g].bad, 1u);
+        if (nh) atomicAdd(&s_acc[g].heads, nh);
       }
     }
     wave_sync();
@@ -284,9 +341,17 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
       if (x) atomicAdd(&s_acc[g].claimed, (uint32_t)__popcll(x));
     }
     wave_sync();
+    // plans whose priorities are not a permutation of each level's heads'
+    // index range (one lane per plan)
+    uint64_t rankedm;
+    {
+      const PlanAcc& ag = s_acc[lane < gc ? lane : 0];  // G <= 64
+      const bool rk = lane < gc && (ag.bad != 0u || ag.heads != ag.claimed);
+      rankedm = __ballot(rk);
+    }
     // general path: rank by (priority, index) within each level
-    for (int g = 0; g < gc; ++g) {
-      if (!s_acc[g].bad && s_acc[g].heads == s_acc[g].claimed) continue;
+    for (uint64_t rm = rankedm; rm; rm &= rm - 1ull) {
+      const int g = __builtin_ctzll(rm);
       const int8_t* pdev = dev_all + (p0 + g) * N;
       const uint16_t* pprio = prio_all + (p0 + g) * N;
       const uint8_t* pfl = s_fl + g * NB;
@@ -321,11 +386,66 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
       }
       wave_sync();
     }
-    wave_sync();
     if constexpr (NIBBLE) {
       // mark each (device, model)'s last unit in its slot entry: the
       // reclamation queues need only that bit, and last[] dies here
+      if (vec) {
+        // plans ordered by priority: re-derive each head's (device, slot,
+        // model) from its row; all loads first, then the marks
+        for (int base = 0; base < N; base += 256) {
+          const int u0 = base + 4 * lane;
+          const bool live = u0 < N;
+          const int uc = live ? u0 : 0;
+          const uint4 act4 = *reinterpret_cast<const uint4*>(t_act + uc);
+          const uint4 alv4 = *reinterpret_cast<const uint4*>(t_alv + uc);
+          const uint32_t av[4] = {act4.x, act4.y, act4.z, act4.w};
+          const uint32_t lv[4] = {alv4.x, alv4.y, alv4.z, alv4.w};
+          for (int g0 = 0; g0 < gc; g0 += kB) {
+            uint32_t dv[kB];
+            uint2 pv[kB];
+            rows4(g0, uc, dv, pv);
+            uint32_t fl[kB];
+#pragma unroll
+            for (int k = 0; k < kB; ++k) {
+              const int g = (g0 + k < gc) ? g0 + k : gc - 1;
+              fl[k] = s_fl[g * NB + (uc >> 2)];
+            }
+            int idx[kB][4], prs[kB][4];
+            bool ok[kB][4];
+            uint32_t lst[kB][4];
+#pragma unroll
+            for (int k = 0; k < kB; ++k) {
+              const int g = g0 + k;
+              const bool plan_ok = live && g < gc && !((rankedm >> (g & 63)) & 1ull);
+#pragma unroll
+              for (int j = 0; j < 4; ++j) {
+                const int d = (int)(int8_t)((dv[k] >> (8 * j)) & 0xffu);
+                const int pr = (int)(((j < 2 ? pv[k].x : pv[k].y) >> (16 * (j & 1))) & 0xffffu);
+                const uint32_t fb = fl[k] >> (2 * j);
+                const bool head = !((fb & 1u) && (av[j] & 64u));
+                const bool okd = (unsigned)d < (unsigned)D;
+                const bool inr = (unsigned)(pr - (int)(lv[j] & 0xffffu)) < (lv[j] >> 16);
+                ok[k][j] = plan_ok && head && okd && inr;
+                prs[k][j] = pr;
+                idx[k][j] = ok[k][j] ? (g * D + d) * M + (int)(av[j] & 63u) : 0;
+              }
+            }
+#pragma unroll
+            for (int k = 0; k < kB; ++k)
+#pragma unroll
+              for (int j = 0; j < 4; ++j) lst[k][j] = s_last[idx[k][j]];
+#pragma unroll
+            for (int k = 0; k < kB; ++k)
+#pragma unroll
+              for (int j = 0; j < 4; ++j)
+                if (ok[k][j] && lst[k][j] == (uint32_t)prs[k][j] + 1u)
+                  atomicOr(&s_rec[(g0 + k) * N + prs[k][j]], kLast);
+          }
+        }
+      }
+      // ranked plans (and every plan without the vector path): by slot
       for (int g = 0; g < gc; ++g) {
+        if (vec && !((rankedm >> g) & 1ull)) continue;
         uint32_t* rec = s_rec + g * N;
         const unsigned long long* mk = s_mask + g * D * NWA;
         const uint32_t* lastp = s_last + g * D * M;
@@ -338,7 +458,10 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
           if (occ && lastp[d * M + m] == (uint32_t)sl + 1u) rec[sl] = e | kLast;
         }
       }
+      wave_sync();
     }
+
+    if (pre && grp + stride < n_groups) load_rows(grp + stride, dvp, pvp);
 
     // ---- device-lane state ----
     const bool act = g_me < gc;
@@ -403,11 +526,19 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
       // one lane per incoming edge.  A fused chain member already holds its
       // own finish, which is later than its only predecessor's ----
       if (e1 > e0) {
-        for (int g = 0; g < gc; ++g) {
-          TB* fin = s_fin + g * N;
-          for (int e = e0 + lane; e < e1; e += 64) {
-            const uint32_t ed = t_edge[e];
-            atomicMax(&fin[ed >> 16], fin[ed & 0xffffu]);
+        for (int e = e0 + lane; e < e1; e += 64) {
+          const uint32_t ed = t_edge[e];
+          const int src = (int)(ed & 0xffffu), dst = (int)(ed >> 16);
+          for (int g0 = 0; g0 < gc; g0 += kB) {
+            TB f[kB];
+#pragma unroll
+            for (int k = 0; k < kB; ++k) {
+              const int g = (g0 + k < gc) ? g0 + k : gc - 1;
+              f[k] = s_fin[g * N + src];
+            }
+#pragma unroll
+            for (int k = 0; k < kB; ++k)
+              if (g0 + k < gc) atomicMax(&s_fin[(g0 + k) * N + dst], f[k]);
           }
         }
         wave_sync();
@@ -417,23 +548,29 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
       if (act) {
         const int j1 = (hi - 1) >> 6;
         const unsigned long long hmask = (hi & 63) ? ((1ull << (hi & 63)) - 1ull) : ~0ull;
+        // slots of this device in the level: the current word's remaining
+        // bits, and the next word already loaded
         int j = lo >> 6;
         unsigned long long bits = mymask[j] & (~0ull << (lo & 63));
         if (j == j1) bits &= hmask;
-        // the device's next slot in the level, -1 when there is none
+        unsigned long long wnext = 0ull;
+        if (j < j1) wnext = mymask[j + 1] & ((j + 1 == j1) ? hmask : ~0ull);
+        // the device's next slot in the level; -1 when there is none, -2 for
+        // a trip with no unit (an exhausted word followed by an empty one)
         auto next_slot = [&]() -> int {
-          while (!bits && j < j1) {
-            ++j;
-            bits = mymask[j];
-            if (j == j1) bits &= hmask;
-          }
-          if (!bits) return -1;
-          const int sl = (j << 6) + __builtin_ctzll(bits);
+          const bool adv = bits == 0ull && j < j1;
+          bits = adv ? wnext : bits;
+          j += adv ? 1 : 0;
+          const int jn = j + 1 <= j1 ? j + 1 : j1;
+          const unsigned long long wl2 = mymask[jn] & ((jn == j1) ? hmask : ~0ull);
+          wnext = adv ? (j < j1 ? wl2 : 0ull) : wnext;
+          const int sl = (j << 6) + __builtin_ctzll(bits | (1ull << 63));
+          const bool have = bits != 0ull;
           bits &= bits - 1ull;
-          return sl;
+          return have ? sl : (j < j1 ? -2 : -1);
         };
-        // slot entry; past the end a stand-in (activation lo, model 0) keeps
-        // every address below in range
+        // slot entry; without a slot a stand-in (activation lo, model 0)
+        // keeps every address below in range
         auto entry = [&](int sl) -> uint32_t {
           const uint32_t keep = (uint32_t)~(sl >> 31);  // all ones for a real slot
           const uint32_t raw = myrec[(int)((uint32_t)sl & keep)];
@@ -454,132 +591,133 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
           const int sa = next_slot();
           fetch(sa, entry(sa), A);
         }
-        int sb = A.slot >= 0 ? next_slot() : -1;
+        int sb = A.slot != -1 ? next_slot() : -1;
         uint32_t mb_next = entry(sb);
-        while (A.slot >= 0) {
-          const int u = (int)(A.meta & 0xffffu);
-          const int m = (int)((A.meta >> 16) & 63u);
-          const uint64_t mbit = 1ull << m;
-          const bool hit = ((res >> m) & 1ull) != 0ull;
-          int32_t w0 = 0, w1 = 0;
-          if constexpr (NIBBLE) {
-            // a hit model sits in the still-needed part: take it out, it
-            // re-enters as the most recent
-            const uint64_t x = Q ^ (0x1111111111111111ull * (uint64_t)m);
-            const uint64_t z = (x - 0x1111111111111111ull) & ~x & 0x8888888888888888ull;
-            const int s4 = __builtin_ctzll(z | (1ull << 63)) & ~3;  // 4 * position
-            const uint64_t low = Q & ((1ull << s4) - 1ull);
-            const uint64_t high = (s4 >= 60) ? 0ull : ((Q >> (s4 + 4)) << s4);
-            Q = hit ? (low | high) : Q;
-            nq -= hit ? 1 : 0;
-            // the first two victims' weights, looked up ahead of need
-            w0 = t_wmib[(int)(Q & 15ull)];
-            w1 = t_wmib[(int)((Q >> 4) & 15ull)];
-          }
+        while (A.slot != -1) {
           // the next unit's tables and the one after's slot entry
           UnitPre<TT> B;
           fetch(sb, mb_next, B);
-          const int sc = sb >= 0 ? next_slot() : -1;
+          const int sc = sb != -1 ? next_slot() : -1;
           const uint32_t mc = entry(sc);
-
-          const TT r = TO::tmax(A.rtv, A.arrv);
-          // run time (summed over a fused chain, Eq. 4) and memory (max)
-          int32_t mxu = A.mem;
-          inel |= (uint32_t)(A.lat < 0);
-          uint32_t T = (uint32_t)A.lat;
-          if (A.meta & kChain) {
-            for (int v = t_cnext[u];;) {
-              const int32_t lv2 = lat_d[__umul24((uint32_t)v, (uint32_t)D)];
-              const int32_t mv = mem_d[__umul24((uint32_t)v, (uint32_t)mem_si)];
-              inel |= (uint32_t)(lv2 < 0);
-              T += (uint32_t)lv2;
-              mxu = mv > mxu ? mv : mxu;
-              const int c = t_cnext[v];
-              if (c == 0xffff || !fuse_bit(myfl, c)) break;
-              v = c;
+          if (A.slot >= 0) {
+            const int u = (int)(A.meta & 0xffffu);
+            const int m = (int)((A.meta >> 16) & 63u);
+            const uint64_t mbit = 1ull << m;
+            const bool hit = ((res >> m) & 1ull) != 0ull;
+            int32_t w0 = 0, w1 = 0;
+            if constexpr (NIBBLE) {
+              // a hit model sits in the still-needed part: take it out, it
+              // re-enters as the most recent
+              const uint64_t x = Q ^ (0x1111111111111111ull * (uint64_t)m);
+              const uint64_t z = (x - 0x1111111111111111ull) & ~x & 0x8888888888888888ull;
+              const int s4 = __builtin_ctzll(z | (1ull << 63)) & ~3;  // 4 * position
+              const uint64_t low = Q & ((1ull << s4) - 1ull);
+              const uint64_t high = (s4 >= 60) ? 0ull : ((Q >> (s4 + 4)) << s4);
+              Q = hit ? (low | high) : Q;
+              nq -= hit ? 1 : 0;
+              // the first two victims' weights, looked up ahead of need
+              w0 = t_wmib[(int)(Q & 15ull)];
+              w1 = t_wmib[(int)((Q >> 4) & 15ull)];
             }
-          }
-          const int32_t need = (hit ? 0 : A.lw.y) + mxu;
-          // reclaim (Sec. 3.5): a copy with no remaining use first, else the
-          // least recently used, else the lower model id
-          if constexpr (NIBBLE) {
-            int t = 0;
-            while (used + need > capd && nq > 0) {
-              const int v = (int)(Q & 15ull);
-              Q >>= 4;
-              --nq;
-              nd = nd > 0 ? nd - 1 : 0;
-              int32_t wv = t ? w1 : w0;
-              if (t >= 2) wv = t_wmib[v];
-              res &= ~(1ull << v);
-              used -= wv;
-              ++nev;
-              ++t;
+            const TT r = TO::tmax(A.rtv, A.arrv);
+            // run time (summed over a fused chain, Eq. 4) and memory (max)
+            int32_t mxu = A.mem;
+            inel |= (uint32_t)(A.lat < 0);
+            uint32_t T = (uint32_t)A.lat;
+            if (sp.has_chains && (A.meta & kChain)) {
+              for (int v = t_cnext[u];;) {
+                const int32_t lv2 = lat_d[__umul24((uint32_t)v, (uint32_t)D)];
+                const int32_t mv = mem_d[__umul24((uint32_t)v, (uint32_t)mem_si)];
+                inel |= (uint32_t)(lv2 < 0);
+                T += (uint32_t)lv2;
+                mxu = mv > mxu ? mv : mxu;
+                const int c = t_cnext[v];
+                if (c == 0xffff || !fuse_bit(myfl, c)) break;
+                v = c;
+              }
             }
-            // m re-enters after the no-remaining-use part when this was its
-            // last unit on the device, else at the end
-            const bool last_use = (A.meta & kLast) != 0u;
-            const int pos = 4 * (last_use ? nd : nq);  // nq <= 15 here
-            const uint64_t lowm = (1ull << pos) - 1ull;
-            Q = (Q & lowm) | ((uint64_t)m << pos) | ((Q & ~lowm) << 4);
-            nd += last_use ? 1 : 0;
-            ++nq;
-          } else {
-            while (used + need > capd) {
-              uint64_t cand = res & ~mbit;
-              if (!cand) break;
-              int v = 0;
-              uint32_t best = 0xffffffffu;
-              while (cand) {
-                const int m2 = __builtin_ctzll(cand);
-                cand &= cand - 1;
-                const uint32_t alive = mylast[m2] > (uint32_t)A.slot + 1u;
-                const uint32_t key = (alive << 16) | mystamp[m2];
-                if (key < best) {
-                  best = key;
-                  v = m2;
+            const int32_t need = (hit ? 0 : A.lw.y) + mxu;
+            // reclaim (Sec. 3.5): a copy with no remaining use first, else the
+            // least recently used, else the lower model id
+            if constexpr (NIBBLE) {
+              int t = 0;
+              while (used + need > capd && nq > 0) {
+                const int v = (int)(Q & 15ull);
+                Q >>= 4;
+                --nq;
+                nd = nd > 0 ? nd - 1 : 0;
+                int32_t wv = t ? w1 : w0;
+                if (t >= 2) wv = t_wmib[v];
+                res &= ~(1ull << v);
+                used -= wv;
+                ++nev;
+                ++t;
+              }
+              // m re-enters after the no-remaining-use part when this was its
+              // last unit on the device, else at the end
+              const bool last_use = (A.meta & kLast) != 0u;
+              const int pos = 4 * (last_use ? nd : nq);  // nq <= 15 here
+              const uint64_t lowm = (1ull << pos) - 1ull;
+              Q = (Q & lowm) | ((uint64_t)m << pos) | ((Q & ~lowm) << 4);
+              nd += last_use ? 1 : 0;
+              ++nq;
+            } else {
+              while (used + need > capd) {
+                uint64_t cand = res & ~mbit;
+                if (!cand) break;
+                int v = 0;
+                uint32_t best = 0xffffffffu;
+                while (cand) {
+                  const int m2 = __builtin_ctzll(cand);
+                  cand &= cand - 1;
+                  const uint32_t alive = mylast[m2] > (uint32_t)A.slot + 1u;
+                  const uint32_t key = (alive << 16) | mystamp[m2];
+                  if (key < best) {
+                    best = key;
+                    v = m2;
+                  }
                 }
+                res &= ~(1ull << v);
+                used -= t_wmib[v];
+                ++nev;
               }
-              res &= ~(1ull << v);
-              used -= t_wmib[v];
-              ++nev;
+              mystamp[m] = (uint16_t)seq++;
             }
-            mystamp[m] = (uint16_t)seq++;
-          }
-          capbad |= (uint32_t)(used + need > capd);
-          // timeline (Eq. 7): a load waits for the device and starts at the
-          // release, or at the workflow arrival when prefetched
-          const TT ls = TO::tmax((A.meta & kPf) ? A.arrv : r, freet);
-          const TT le = TO::add(ls, (uint32_t)A.lw.x);
-          const TT s = TO::tmax(r, hit ? freet : le);
-          res |= mbit;
-          used += hit ? 0 : A.lw.y;
-          nld += hit ? 0u : 1u;
-          peak = (used + mxu) > peak ? (used + mxu) : peak;
-          const TT f = TO::add(s, T);
-          freet = f;
-          if (!(A.meta & kChain)) {
-            myfin[u] = TO::bits(f);
-            if (has_sched) {
-              sched.start_us[pw * N + u] = sp.origin + TO::i64(s);
-              sched.finish_us[pw * N + u] = sp.origin + TO::i64(f);
-              sched.load_start_us[pw * N + u] = hit ? (int64_t)-1 : sp.origin + TO::i64(ls);
-            }
-          } else {
-            TT t = s;
-            for (int v = u;;) {
-              const TT tv = TO::add(t, (uint32_t)lat_d[__umul24((uint32_t)v, (uint32_t)D)]);
-              myfin[v] = TO::bits(tv);
+            capbad |= (uint32_t)(used + need > capd);
+            // timeline (Eq. 7): a load waits for the device and starts at the
+            // release, or at the workflow arrival when prefetched
+            const TT ls = TO::tmax((A.meta & kPf) ? A.arrv : r, freet);
+            const TT le = TO::add(ls, (uint32_t)A.lw.x);
+            const TT s = TO::tmax(r, hit ? freet : le);
+            res |= mbit;
+            used += hit ? 0 : A.lw.y;
+            nld += hit ? 0u : 1u;
+            peak = (used + mxu) > peak ? (used + mxu) : peak;
+            const TT f = TO::add(s, T);
+            freet = f;
+            if (!sp.has_chains || !(A.meta & kChain)) {
+              myfin[u] = TO::bits(f);
               if (has_sched) {
-                sched.start_us[pw * N + v] = sp.origin + TO::i64(t);
-                sched.finish_us[pw * N + v] = sp.origin + TO::i64(tv);
-                sched.load_start_us[pw * N + v] =
-                    (v == u && !hit) ? sp.origin + TO::i64(ls) : (int64_t)-1;
+                sched.start_us[pw * N + u] = sp.origin + TO::i64(s);
+                sched.finish_us[pw * N + u] = sp.origin + TO::i64(f);
+                sched.load_start_us[pw * N + u] = hit ? (int64_t)-1 : sp.origin + TO::i64(ls);
               }
-              t = tv;
-              const int c = t_cnext[v];
-              if (c == 0xffff || !fuse_bit(myfl, c)) break;
-              v = c;
+            } else {
+              TT t = s;
+              for (int v = u;;) {
+                const TT tv = TO::add(t, (uint32_t)lat_d[__umul24((uint32_t)v, (uint32_t)D)]);
+                myfin[v] = TO::bits(tv);
+                if (has_sched) {
+                  sched.start_us[pw * N + v] = sp.origin + TO::i64(t);
+                  sched.finish_us[pw * N + v] = sp.origin + TO::i64(tv);
+                  sched.load_start_us[pw * N + v] =
+                      (v == u && !hit) ? sp.origin + TO::i64(ls) : (int64_t)-1;
+                }
+                t = tv;
+                const int c = t_cnext[v];
+                if (c == 0xffff || !fuse_bit(myfl, c)) break;
+                v = c;
+              }
             }
           }
           A = B;
@@ -601,31 +739,45 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
     }
     // a workflow's completion is the latest finish among its activations
     // without a successor in the same workflow
-    for (int g = 0; g < gc; ++g) {
-      const TB* fin = s_fin + g * N;
-      TB* wm = s_wfm + g * W;
-      for (int i = lane; i < sp.S; i += 64) {
-        const uint32_t sk = t_sink[i];
-        atomicMax(&wm[sk >> 16], fin[sk & 0xffffu]);
+    for (int i = lane; i < sp.S; i += 64) {
+      const uint32_t sk = t_sink[i];
+      const int src = (int)(sk & 0xffffu), wf = (int)(sk >> 16);
+      for (int g0 = 0; g0 < gc; g0 += kB) {
+        TB f[kB];
+#pragma unroll
+        for (int k = 0; k < kB; ++k) {
+          const int g = (g0 + k < gc) ? g0 + k : gc - 1;
+          f[k] = s_fin[g * N + src];
+        }
+#pragma unroll
+        for (int k = 0; k < kB; ++k)
+          if (g0 + k < gc) atomicMax(&s_wfm[(g0 + k) * W + wf], f[k]);
       }
     }
     wave_sync();
-    // nearest-rank p95 (the ceil(0.95 W)-th smallest completion latency) and
-    // the latest finish, lanes over (plan, workflow)
-    const int kk = (95 * W + 99) / 100;
+    // completion latencies in place, and the latest finish
     for (int it = lane; it < gc * W; it += 64) {
       const int g = it / W, a = it - g * W;
-      const TB* wm = s_wfm + g * W;
-      const TT fa = TO::load(wm + a);
-      const int64_t ca = TO::i64(fa) - TO::i64(TO::load(t_arr + a));
+      const TB fb = s_wfm[it];
+      atomicMax(&s_acc[g].max_finish, (unsigned long long)fb);
+      s_wfm[it] = TO::bits(TO::sub(TO::load(&fb), TO::load(t_arr + a)));
+    }
+    wave_sync();
+    // nearest-rank p95: the ceil(0.95 W)-th smallest completion latency,
+    // lanes over (plan, workflow)
+    const int kk = (95 * W + 99) / 100;
+    for (int it = lane; it < gc * W; it += 64) {
+      const int g = it / W;
+      const TB* cw = s_wfm + g * W;
+      const TT ca = TO::load(cw + (it - g * W));
       int lt = 0, le = 0;
+#pragma unroll 8
       for (int b = 0; b < W; ++b) {
-        const int64_t cb = TO::i64(TO::load(wm + b)) - TO::i64(TO::load(t_arr + b));
+        const TT cb = TO::load(cw + b);
         lt += cb < ca;
         le += cb <= ca;
       }
-      if (lt < kk && kk <= le) s_acc[g].p95 = ca;
-      atomicMax(&s_acc[g].max_finish, (unsigned long long)TO::bits(fa));
+      if (lt < kk && kk <= le) s_acc[g].p95 = TO::i64(ca);
     }
     wave_sync();
     if (lane < gc) {
