@@ -260,3 +260,71 @@ def test_cross_workflow_edges(ctx, seed):
     assert_scores(got, ref, f"cross seed {seed}")
     assert_sched(gs, rs, ref["status"], f"cross seed {seed}")
     assert best == best_plan(ref)
+
+
+def test_misaligned_plan_buffers(ctx):
+    """Plan rows at addresses that rule out the kernel's 4- and 8-byte row
+    loads (the same window otherwise takes them)."""
+    win, plans = W.make_config(1, n_plans=300)
+    P, N = plans.n_plans, win.n_act
+    ctx.wf_plan_upload_window(win)
+    dev_buf = torch.zeros(P * N + 1, dtype=torch.int8, device="cuda:0")
+    prio_buf = torch.zeros(P * N + 1, dtype=torch.int16, device="cuda:0")
+    fl_buf = torch.zeros(plans.flags.size + 3, dtype=torch.uint8, device="cuda:0")
+    dev_buf[1:] = torch.from_numpy(np.ascontiguousarray(plans.dev).reshape(-1)).to("cuda:0")
+    prio_buf[1:] = torch.from_numpy(np.ascontiguousarray(plans.prio).view("<i2").reshape(-1)).to("cuda:0")
+    fl_buf[3:] = torch.from_numpy(np.ascontiguousarray(plans.flags).reshape(-1)).to("cuda:0")
+    scores = torch.empty((P, 32), dtype=torch.uint8, device="cuda:0")
+    ctx.wf_plan_score_batch(dev_buf.data_ptr() + 1, prio_buf.data_ptr() + 2, fl_buf.data_ptr() + 3,
+                            P, scores)
+    torch.cuda.synchronize()
+    got = pkg.scores_to_numpy(scores, P)
+    ref = oracle.score(win, plans)
+    assert got.tobytes() == ref.tobytes()
+
+
+def _fan_window(rng, n_children, n_dev=3, n_models=4):
+    """One source feeding n_children activations: a single wide level."""
+    n = 1 + n_children
+    off = np.concatenate([[0, 0], np.arange(1, n_children + 1)]).astype(np.int32)
+    return W.Window(
+        n_act=n, n_wf=1, n_models=n_models, n_dev=n_dev,
+        act_wf=np.zeros(n, np.int32), act_model=rng.integers(0, n_models, n).astype(np.int32),
+        pred_off=off, pred_idx=np.zeros(n_children, np.int32),
+        lat_us=rng.integers(1, 1000, n * n_dev).astype(np.int32),
+        mem_mib=rng.integers(100, 2000, n * n_dev).astype(np.int32),
+        wf_arrival_us=np.zeros(1, np.int64),
+        dev_cap_mib=np.full(n_dev, 30000, np.int32),
+        model_mib=rng.integers(2000, 12000, n_models).astype(np.int32),
+        load_us=rng.integers(0, 3000, n_models * n_dev).astype(np.int32),
+        init_resident=np.zeros(n_dev, np.uint64), dev_free0_us=np.zeros(n_dev, np.int64),
+        name="fan")
+
+
+@pytest.mark.parametrize("n_children", [203, 250])
+def test_wide_level_sparse_device(ctx, n_children):
+    """A device whose units of a 200+-slot level sit in its first and last
+    64-slot words only: its slot iterator crosses empty words."""
+    rng = np.random.default_rng(31 + n_children)
+    win = _fan_window(rng, n_children)
+    P, N = 96, win.n_act
+    dev = rng.integers(0, 2, size=(P, N)).astype(np.int8)
+    prio = np.empty((P, N), np.uint16)
+    prio[:, 0] = 0
+    for p in range(P):
+        perm = 1 + rng.permutation(n_children)
+        prio[p, 1:] = perm
+        # device 2 gets the level's first and last slot, and sometimes one
+        # in the middle
+        first, last = int(np.argmin(perm)) + 1, int(np.argmax(perm)) + 1
+        dev[p, first] = dev[p, last] = 2
+        if p % 3 == 0:
+            dev[p, 1 + int(np.argsort(perm)[n_children // 2])] = 2
+    flags = W.pack_flags(rng.random((P, N)) < 0.3, rng.random((P, N)) < 0.3)
+    plans = W.PlanBatch(dev, prio, flags)
+    got, gs, best = gpu_score(ctx, win, plans, schedule=True)
+    ref, rs = oracle.score(win, plans, schedule=True)
+    assert_scores(got, ref, "fan")
+    assert_sched(gs, rs, ref["status"], "fan")
+    assert got.tobytes() == ref.tobytes()
+    assert best == best_plan(ref)
