@@ -412,8 +412,10 @@ wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, Image& img, wfp::Sc
       const int lds_wg = tab_lds + waves * wb;
       const int wg_per_cu = std::max(1, lds_cu / lds_wg);
       const int waves_cu = std::min(32, wg_per_cu * waves);
-      // walk lanes in flight per CU, table reads from LDS preferred
-      const double score = (double)std::min(G * D, 64) * std::min(waves_cu, 8) * (tl ? 1.0 : 0.6);
+      // walk lanes in flight per CU (at most 8 waves: two per SIMD at the
+      // kernel's register use); cached table reads cost about as much as
+      // LDS reads, so the table stays in LDS only when that costs no wave
+      const double score = (double)std::min(G * D, 64) * std::min(waves_cu, 8) * (tl ? 1.0 : 0.99);
       if (score > best) {
         best = score;
         sp.G = G;

@@ -586,31 +586,25 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
           p.mem = mem_d[__umul24(u, (uint32_t)mem_si)];
           p.lw = lw_d[__umul24(m, (uint32_t)D)];
         };
-        UnitPre<TT> A;
-        {
-          const int sa = next_slot();
-          fetch(sa, entry(sa), A);
-        }
-        int sb = A.slot != -1 ? next_slot() : -1;
-        uint32_t mb_next = entry(sb);
-        while (A.slot != -1) {
-          // the next unit's tables and the one after's slot entry
-          UnitPre<TT> B;
-          fetch(sb, mb_next, B);
-          const int sc = sb != -1 ? next_slot() : -1;
-          const uint32_t mc = entry(sc);
-          if (A.slot >= 0) {
-            const int u = (int)(A.meta & 0xffffu);
-            const int m = (int)((A.meta >> 16) & 63u);
+        // one unit of the device's sequence: reuse / reclaim / load, then
+        // the timeline
+        auto process = [&](const UnitPre<TT>& X) {
+          if (X.slot >= 0) {
+            const int u = (int)(X.meta & 0xffffu);
+            const int m = (int)((X.meta >> 16) & 63u);
             const uint64_t mbit = 1ull << m;
-            const bool hit = ((res >> m) & 1ull) != 0ull;
+            bool hit;
             int32_t w0 = 0, w1 = 0;
+            if constexpr (!NIBBLE) hit = ((res >> m) & 1ull) != 0ull;
             if constexpr (NIBBLE) {
-              // a hit model sits in the still-needed part: take it out, it
-              // re-enters as the most recent
+              // the queue holds exactly the resident models: m is resident
+              // when it is found among the first nq entries (in the
+              // still-needed part); it is taken out and re-enters as the most
+              // recent
               const uint64_t x = Q ^ (0x1111111111111111ull * (uint64_t)m);
               const uint64_t z = (x - 0x1111111111111111ull) & ~x & 0x8888888888888888ull;
               const int s4 = __builtin_ctzll(z | (1ull << 63)) & ~3;  // 4 * position
+              hit = z != 0ull && (s4 >> 2) < nq;
               const uint64_t low = Q & ((1ull << s4) - 1ull);
               const uint64_t high = (s4 >= 60) ? 0ull : ((Q >> (s4 + 4)) << s4);
               Q = hit ? (low | high) : Q;
@@ -619,12 +613,12 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
               w0 = t_wmib[(int)(Q & 15ull)];
               w1 = t_wmib[(int)((Q >> 4) & 15ull)];
             }
-            const TT r = TO::tmax(A.rtv, A.arrv);
+            const TT r = TO::tmax(X.rtv, X.arrv);
             // run time (summed over a fused chain, Eq. 4) and memory (max)
-            int32_t mxu = A.mem;
-            inel |= (uint32_t)(A.lat < 0);
-            uint32_t T = (uint32_t)A.lat;
-            if (sp.has_chains && (A.meta & kChain)) {
+            int32_t mxu = X.mem;
+            inel |= (uint32_t)(X.lat < 0);
+            uint32_t T = (uint32_t)X.lat;
+            if (sp.has_chains && (X.meta & kChain)) {
               for (int v = t_cnext[u];;) {
                 const int32_t lv2 = lat_d[__umul24((uint32_t)v, (uint32_t)D)];
                 const int32_t mv = mem_d[__umul24((uint32_t)v, (uint32_t)mem_si)];
@@ -636,7 +630,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
                 v = c;
               }
             }
-            const int32_t need = (hit ? 0 : A.lw.y) + mxu;
+            const int32_t need = (hit ? 0 : X.lw.y) + mxu;
             // reclaim (Sec. 3.5): a copy with no remaining use first, else the
             // least recently used, else the lower model id
             if constexpr (NIBBLE) {
@@ -648,20 +642,21 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
                 nd = nd > 0 ? nd - 1 : 0;
                 int32_t wv = t ? w1 : w0;
                 if (t >= 2) wv = t_wmib[v];
-                res &= ~(1ull << v);
                 used -= wv;
                 ++nev;
                 ++t;
               }
               // m re-enters after the no-remaining-use part when this was its
               // last unit on the device, else at the end
-              const bool last_use = (A.meta & kLast) != 0u;
+              const bool last_use = (X.meta & kLast) != 0u;
               const int pos = 4 * (last_use ? nd : nq);  // nq <= 15 here
               const uint64_t lowm = (1ull << pos) - 1ull;
               Q = (Q & lowm) | ((uint64_t)m << pos) | ((Q & ~lowm) << 4);
               nd += last_use ? 1 : 0;
               ++nq;
             } else {
+              (void)w0;
+              (void)w1;
               while (used + need > capd) {
                 uint64_t cand = res & ~mbit;
                 if (!cand) break;
@@ -670,7 +665,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
                 while (cand) {
                   const int m2 = __builtin_ctzll(cand);
                   cand &= cand - 1;
-                  const uint32_t alive = mylast[m2] > (uint32_t)A.slot + 1u;
+                  const uint32_t alive = mylast[m2] > (uint32_t)X.slot + 1u;
                   const uint32_t key = (alive << 16) | mystamp[m2];
                   if (key < best) {
                     best = key;
@@ -686,16 +681,16 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
             capbad |= (uint32_t)(used + need > capd);
             // timeline (Eq. 7): a load waits for the device and starts at the
             // release, or at the workflow arrival when prefetched
-            const TT ls = TO::tmax((A.meta & kPf) ? A.arrv : r, freet);
-            const TT le = TO::add(ls, (uint32_t)A.lw.x);
+            const TT ls = TO::tmax((X.meta & kPf) ? X.arrv : r, freet);
+            const TT le = TO::add(ls, (uint32_t)X.lw.x);
             const TT s = TO::tmax(r, hit ? freet : le);
-            res |= mbit;
-            used += hit ? 0 : A.lw.y;
+            if constexpr (!NIBBLE) res |= mbit;
+            used += hit ? 0 : X.lw.y;
             nld += hit ? 0u : 1u;
             peak = (used + mxu) > peak ? (used + mxu) : peak;
             const TT f = TO::add(s, T);
             freet = f;
-            if (!sp.has_chains || !(A.meta & kChain)) {
+            if (!sp.has_chains || !(X.meta & kChain)) {
               myfin[u] = TO::bits(f);
               if (has_sched) {
                 sched.start_us[pw * N + u] = sp.origin + TO::i64(s);
@@ -720,9 +715,25 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
               }
             }
           }
-          A = B;
-          sb = sc;
-          mb_next = mc;
+        };
+        // two units per trip so that the prefetched unit needs no copy
+        UnitPre<TT> A, B;
+        {
+          const int sa = next_slot();
+          fetch(sa, entry(sa), A);
+        }
+        int sb = A.slot != -1 ? next_slot() : -1;
+        uint32_t mb_next = entry(sb);
+        while (A.slot != -1) {
+          fetch(sb, mb_next, B);
+          const int sc = sb != -1 ? next_slot() : -1;
+          const uint32_t mc = entry(sc);
+          process(A);
+          if (B.slot == -1) break;
+          fetch(sc, mc, A);
+          sb = sc != -1 ? next_slot() : -1;
+          mb_next = entry(sb);
+          process(B);
         }
       }
       wave_sync();
