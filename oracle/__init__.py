@@ -72,6 +72,11 @@ def _load(path: Optional[str] = None):
             lib.orc_score_plans.argtypes = [ctypes.c_void_p] * 4 + [ctypes.c_int64] + [ctypes.c_void_p] * 5
             lib.orc_levels.restype = ctypes.c_int
             lib.orc_levels.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+            lib.orc_philox4x32_10.restype = None
+            lib.orc_philox4x32_10.argtypes = [ctypes.c_void_p] * 3
+            lib.orc_search_candidates.restype = ctypes.c_int
+            lib.orc_search_candidates.argtypes = ([ctypes.c_void_p] * 4 + [ctypes.c_uint64, ctypes.c_int32,
+                                                  ctypes.c_int64, ctypes.c_int64] + [ctypes.c_void_p] * 3)
             _libs[path] = lib
     return _libs[path]
 
@@ -172,3 +177,40 @@ def score(win, plans, begin: int = 0, end: Optional[int] = None, schedule: bool 
     if schedule:
         return scores, sched
     return scores
+
+
+def philox4x32_10(ctr, key, lib_path: Optional[str] = None) -> np.ndarray:
+    """Philox4x32-10 of one 4-word counter under a 2-word key."""
+    lib = _load(lib_path)
+    c = np.ascontiguousarray(ctr, dtype=np.uint32)
+    k = np.ascontiguousarray(key, dtype=np.uint32)
+    out = np.zeros(4, dtype=np.uint32)
+    lib.orc_philox4x32_10(c.ctypes.data, k.ctypes.data, out.ctypes.data)
+    return out
+
+
+def search_candidates(win, dev, prio, flags, seed: int, n_mut: int, first: int, count: int,
+                      lib_path: Optional[str] = None):
+    """Rows (dev, prio, flags) of candidates first .. first+count-1 around the
+    incumbent rows (one plan each)."""
+    lib = _load(lib_path)
+    h = _WinHolder(win)
+    N = win.n_act
+    nb = (N + 3) // 4
+    d = np.ascontiguousarray(dev, dtype=np.int8).reshape(-1)
+    p = np.ascontiguousarray(prio, dtype=np.uint16).reshape(-1)
+    f = np.ascontiguousarray(flags, dtype=np.uint8).reshape(-1)
+    assert d.size == N and p.size == N and f.size == nb
+    od = np.zeros((count, max(N, 1)), np.int8)
+    op = np.zeros((count, max(N, 1)), np.uint16)
+    of = np.zeros((count, max(nb, 1)), np.uint8)
+    dd = d if N else np.zeros(1, np.int8)
+    pp = p if N else np.zeros(1, np.uint16)
+    ff = f if nb else np.zeros(1, np.uint8)
+    rc = lib.orc_search_candidates(ctypes.byref(h.struct), dd.ctypes.data, pp.ctypes.data,
+                                   ff.ctypes.data, int(seed) & ((1 << 64) - 1), int(n_mut),
+                                   int(first), int(count), od.ctypes.data, op.ctypes.data,
+                                   of.ctypes.data)
+    if rc:
+        raise OracleError(f"oracle rejected window (code {rc})")
+    return od[:, :N].copy(), op[:, :N].copy(), of[:, :nb].copy()

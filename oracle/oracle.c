@@ -331,3 +331,91 @@ done:
   free_struct(&st);
   return rc;
 }
+
+/* ---------------------------------------------------------------------- */
+/* candidate generation                                                    */
+/* ---------------------------------------------------------------------- */
+
+void orc_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4]) {
+  uint32_t x0 = ctr[0], x1 = ctr[1], x2 = ctr[2], x3 = ctr[3];
+  uint32_t k0 = key[0], k1 = key[1];
+  for (int round = 0; round < 10; ++round) {
+    const uint64_t p0 = (uint64_t)0xD2511F53u * x0; /* multipliers of Philox-4x32 */
+    const uint64_t p1 = (uint64_t)0xCD9E8D57u * x2;
+    const uint32_t y0 = (uint32_t)(p1 >> 32) ^ x1 ^ k0;
+    const uint32_t y1 = (uint32_t)p1;
+    const uint32_t y2 = (uint32_t)(p0 >> 32) ^ x3 ^ k1;
+    const uint32_t y3 = (uint32_t)p0;
+    x0 = y0;
+    x1 = y1;
+    x2 = y2;
+    x3 = y3;
+    k0 += 0x9E3779B9u; /* Weyl sequence: golden ratio and sqrt(3) - 1 */
+    k1 += 0xBB67AE85u;
+  }
+  out[0] = x0;
+  out[1] = x1;
+  out[2] = x2;
+  out[3] = x3;
+}
+
+/* floor(r * n / 2^32): a draw r scaled to [0, n) */
+static uint32_t scale32(uint32_t r, uint32_t n) { return (uint32_t)(((uint64_t)r * n) >> 32); }
+
+int orc_search_candidates(const orc_window *w, const int8_t *dev, const uint16_t *prio,
+                          const uint8_t *flags, uint64_t seed, int32_t n_mut, int64_t first,
+                          int64_t count, int8_t *out_dev, uint16_t *out_prio,
+                          uint8_t *out_flags) {
+  orc_struct st;
+  int rc = build_struct(w, &st);
+  if (rc) return rc;
+  const int32_t N = w->n_act, D = w->n_dev, NB = (N + 3) / 4;
+  const uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+  for (int64_t k = 0; k < count; ++k) {
+    int8_t *cd = out_dev + k * N;
+    uint16_t *cp = out_prio + k * N;
+    uint8_t *cf = out_flags + k * NB;
+    memcpy(cd, dev, (size_t)N);
+    memcpy(cp, prio, (size_t)N * 2);
+    memcpy(cf, flags, (size_t)NB);
+    if (N == 0) continue;
+    const uint64_t c = (uint64_t)(first + k);
+    for (int32_t t = 0; t < n_mut; ++t) {
+      const uint32_t ctr[4] = {(uint32_t)c, (uint32_t)(c >> 32), (uint32_t)t, 0u};
+      uint32_t r[4];
+      orc_philox4x32_10(ctr, key, r);
+      const int32_t i = (int32_t)scale32(r[1], (uint32_t)N);
+      const uint32_t kind = r[0] >> 30;
+      if (kind == 0) {
+        /* another eligible device (Eq. 8) */
+        int32_t n_elig = 0;
+        for (int32_t d = 0; d < D; ++d) n_elig += w->lat_us[(int64_t)i * D + d] >= 0;
+        if (n_elig == 0) continue;
+        int32_t pick = (int32_t)scale32(r[2], (uint32_t)n_elig);
+        for (int32_t d = 0; d < D; ++d) {
+          if (w->lat_us[(int64_t)i * D + d] < 0) continue;
+          if (pick == 0) {
+            cd[i] = (int8_t)d;
+            break;
+          }
+          --pick;
+        }
+      } else if (kind == 1) {
+        /* another order inside i's level (Eq. 10) */
+        int32_t lo = i, hi = i + 1;
+        while (lo > 0 && st.level[lo - 1] == st.level[i]) --lo;
+        while (hi < N && st.level[hi] == st.level[i]) ++hi;
+        const int32_t j = lo + (int32_t)scale32(r[2], (uint32_t)(hi - lo));
+        const uint16_t tmp = cp[i];
+        cp[i] = cp[j];
+        cp[j] = tmp;
+      } else if (kind == 2) {
+        cf[i / 4] ^= (uint8_t)(1u << (2 * (i % 4)));     /* fuse bit (Eq. 3) */
+      } else {
+        cf[i / 4] ^= (uint8_t)(1u << (2 * (i % 4) + 1)); /* prefetch bit (Eq. 5) */
+      }
+    }
+  }
+  free_struct(&st);
+  return ORC_OK;
+}

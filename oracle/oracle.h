@@ -88,6 +88,39 @@ int orc_score_plans(const orc_window *w, const int8_t *dev, const uint16_t *prio
  * code as above. */
 int orc_levels(const orc_window *w, int32_t *level_out);
 
+/*
+ * Candidate plans around an incumbent (the alternatives Algorithm 1 weighs
+ * before Propagate: another eligible device for a unit -- the binding choice
+ * filtered by Eq. 8 --, another order among a level's units -- the ranked
+ * order of Eq. 10 --, another fusion choice -- Eq. 3 --, another lifecycle
+ * choice for near-ready work -- Eq. 5, alpha_N = Prefetch).
+ *
+ * Candidate c is the incumbent with n_mut mutations applied in order
+ * t = 0 .. n_mut-1.  Mutation t draws (r0, r1, r2, r3) = Philox4x32-10 with
+ * counter (c mod 2^32, c div 2^32, t, 0) and key (seed mod 2^32,
+ * seed div 2^32), then with i = (r1 * N) div 2^32 and kind = r0 div 2^30:
+ *   kind 0: the devices d with lat[i][d] >= 0, ascending, form E; when E is
+ *           not empty, dev[i] = E[(r2 * |E|) div 2^32];
+ *   kind 1: [lo, lo + w) is the index range of i's topological level;
+ *           j = lo + (r2 * w) div 2^32; prio[i] and prio[j] are swapped;
+ *   kind 2: the fuse bit of i is toggled;
+ *   kind 3: the prefetch bit of i is toggled.
+ * r3 is not used.  With N = 0 a candidate is the incumbent.
+ */
+
+/* Philox4x32-10 (Salmon, Moraes, Dror and Shaw, SC'11): ten rounds of the
+ * Philox-4x32 bijection on the counter, the key bumped by the Weyl
+ * constants after every round. */
+void orc_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4]);
+
+/* Rows of candidates first .. first+count-1 (out_dev [count][N], out_prio
+ * [count][N], out_flags [count][ceil(N/4)]) around the incumbent rows dev,
+ * prio, flags of one plan.  Returns an error code as above. */
+int orc_search_candidates(const orc_window *w, const int8_t *dev, const uint16_t *prio,
+                          const uint8_t *flags, uint64_t seed, int32_t n_mut, int64_t first,
+                          int64_t count, int8_t *out_dev, uint16_t *out_prio,
+                          uint8_t *out_flags);
+
 #ifdef __cplusplus
 }
 #endif

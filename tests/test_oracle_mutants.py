@@ -14,9 +14,22 @@ import test_oracle_bruteforce as t_bf
 import test_oracle_independent as t_ind
 import test_oracle_paper_examples as t_pap
 import test_oracle_properties as t_prop
+import test_oracle_search as t_search
 
 # (name, original fragment, planted mistake)
 MUTANTS = [
+    # candidate generator
+    ("philox multiplier swapped", "(uint64_t)0xD2511F53u * x0", "(uint64_t)0xCD9E8D57u * x0"),
+    ("philox key not bumped", "k1 += 0xBB67AE85u;", ""),
+    ("mutation kind from the low bits", "r[0] >> 30", "r[0] & 3u"),
+    ("mutation site from the wrong word", "scale32(r[1], (uint32_t)N)", "scale32(r[2], (uint32_t)N)"),
+    ("swap partner outside the level", "const int32_t j = lo + (int32_t)scale32(r[2], (uint32_t)(hi - lo));",
+     "const int32_t j = (int32_t)scale32(r[2], (uint32_t)N);"),
+    ("re-place ignores eligibility", "          if (w->lat_us[(int64_t)i * D + d] < 0) continue;\n          if (pick == 0) {",
+     "          if (pick == 0) {"),
+    ("fuse flip toggles prefetch", "cf[i / 4] ^= (uint8_t)(1u << (2 * (i % 4)));", "cf[i / 4] ^= (uint8_t)(1u << (2 * (i % 4) + 1));"),
+    ("counter words swapped", "{(uint32_t)c, (uint32_t)(c >> 32), (uint32_t)t, 0u}",
+     "{(uint32_t)t, (uint32_t)(c >> 32), (uint32_t)c, 0u}"),
     ("release ignores arrival", "int64_t r = w->wf_arrival_us[wf];", "int64_t r = 0;"),
     ("victim prefers live copies", "if (alive2 < aliveV) victim = m2;", "if (alive2 > aliveV) victim = m2;"),
     ("victim most recently used", "} else if (last[d * M + m2] < last[d * M + victim]) {",
@@ -73,6 +86,9 @@ def _pin_checks():
     checks += [t_pap.test_fig4_one_load_one_prefetch_shared_by_two_workflows,
                t_pap.test_qmsum_fused_chain_one_grant_one_replica]
     checks += [lambda s=s: t_bf.test_exhaustive(s) for s in range(2)]
+    checks += [lambda k=k: t_search.test_philox_known_answers(*k) for k in t_search.KAT]
+    checks += [t_search.test_one_mutation_decoded_site_by_site, t_search.test_ranges_are_independent_of_splitting]
+    checks += [lambda n=n: t_search.test_candidate_structure(n) for n in (1, 4)]
     return checks
 
 
