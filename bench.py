@@ -98,6 +98,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--check", type=int, default=4096,
                     help="plans checked against the oracle before timing (0 = none)")
+    ap.add_argument("--search-mut", type=int, default=2,
+                    help="mutations per generated candidate in the search leg (-1 = skip it)")
     ap.add_argument("--copy-probe", type=int, default=None, metavar="BYTES",
                     help="only run a plain copy kernel of BYTES bytes (counter calibration)")
     args = ap.parse_args()
@@ -180,6 +182,39 @@ def main():
                 "kernel": "score_plans", "kernel_ms": round(kernel_ms, 4),
                 "bytes_per_plan": bpp}
 
+    # candidates generated around plan 0 on the GPU and scored (no plan rows
+    # in HBM): the same number of plans, same window
+    search = None
+    if args.search_mut >= 0:
+        sd, sp_, sf = dev[0].contiguous(), prio[0].contiguous(), flags[0].contiguous()
+        seed = 0x5EED
+        if args.check:
+            import oracle
+            n_chk = min(P, args.check)
+            ctx.wf_plan_search_batch(sd, sp_, sf, seed, args.search_mut, 0, n_chk, scores, stream)
+            torch.cuda.synchronize()
+            inc = (plans.dev[0], plans.prio[0], plans.flags[0])
+            cand = workload.PlanBatch(*oracle.search_candidates(win, *inc, seed, args.search_mut, 0, n_chk))
+            ref = oracle.score(win, cand, threads=min(16, os.cpu_count() or 1))
+            if pkg.scores_to_numpy(scores, n_chk).tobytes() != ref.tobytes():
+                print("[bench] generated candidates differ from the oracle", file=sys.stderr)
+                sys.exit(1)
+        for _ in range(args.warmup):
+            ctx.wf_plan_search_batch(sd, sp_, sf, seed, args.search_mut, 0, P, scores, stream)
+        torch.cuda.synchronize()
+        sev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(args.steps)]
+        for i in range(args.steps):
+            sev[i][0].record(stream)
+            ctx.wf_plan_search_batch(sd, sp_, sf, seed, args.search_mut, i * P, P, scores, stream)
+            sev[i][1].record(stream)
+        torch.cuda.synchronize()
+        s_ms = float(np.mean([a.elapsed_time(b) for a, b in sev]))
+        search = {"value": round(P / (s_ms * 1e-3), 1), "unit": "candidates/s",
+                  "kernel_ms": round(s_ms, 4), "n_mut": args.search_mut,
+                  "note": "candidates generated around one incumbent plan inside the scoring "
+                          "kernel (no plan rows in HBM), same window and count"}
+
     cpu = None
     if not args.no_cpu_baseline:
         import oracle
@@ -207,6 +242,7 @@ def main():
                    "batch_bytes": bpp * P},
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "search": search,
     }
     print(json.dumps(line))
     ctx.close()

@@ -82,6 +82,7 @@ typedef enum {
 #define WF_MAX_CAP_MIB (1 << 30)   /* per device capacity                   */
 #define WF_MAX_TIME_US (1LL << 52) /* arrivals and initial free times; every
                                       time then stays below 2^53 (exact in fp64) */
+#define WF_MAX_MUT 64              /* mutations per generated candidate        */
 
 /* Plan status bits; a plan is feasible iff status == 0. */
 enum { WF_ST_INELIGIBLE = 1u, WF_ST_CAPACITY = 2u };
@@ -172,6 +173,48 @@ wf_status wf_plan_score_batch(wf_plan_ctx *ctx, const int8_t *dev, const uint16_
  * *out_index.  n_plans must be < 2^32; n_plans = 0 writes -1. */
 wf_status wf_plan_argmin(wf_plan_ctx *ctx, const wf_plan_score *scores, int64_t n_plans,
                          int64_t *out_index, void *hip_stream);
+
+/*
+ * Candidate generation fused with scoring.  Algorithm 1 weighs alternatives
+ * before Propagate checks one: another eligible device for a unit (the
+ * binding choice, filtered by Eq. 8), another order among a level's units
+ * (the ranked order of Eq. 10), another fusion choice (Eq. 3), another
+ * lifecycle choice for near-ready work (Eq. 5, alpha_N = Prefetch).  These
+ * calls draw such alternatives around an incumbent plan on the GPU, so the
+ * candidates never exist in HBM.
+ *
+ * Candidate c is the incumbent with n_mut mutations applied in order
+ * t = 0 .. n_mut-1.  Mutation t draws (r0, r1, r2, r3) = Philox4x32-10
+ * (Salmon, Moraes, Dror and Shaw, SC'11) with counter (c mod 2^32,
+ * c div 2^32, t, 0) and key (seed mod 2^32, seed div 2^32); then with
+ * i = (r1 * N) div 2^32 and kind = r0 div 2^30:
+ *   kind 0: the devices d with lat_us[i][d] >= 0, ascending, form E; when E
+ *           is not empty, dev[i] = E[(r2 * |E|) div 2^32];
+ *   kind 1: [lo, lo + w) is the index range of i's topological level;
+ *           j = lo + (r2 * w) div 2^32; prio[i] and prio[j] are swapped;
+ *   kind 2: the fuse bit of i is toggled;
+ *   kind 3: the prefetch bit of i is toggled.
+ * r3 is not used.  With N = 0 a candidate is the incumbent.
+ *
+ * dev [N], prio [N], flags [ceil(N/4)] are the incumbent's rows (device
+ * memory, layout of wf_plan_score_batch).  Candidates first ..
+ * first+n_candidates-1 are generated; 0 <= n_mut <= WF_MAX_MUT, first >= 0
+ * and first + n_candidates <= 2^62, else WF_EINVAL.
+ */
+
+/* Score the candidates: scores[k] is candidate first+k scored exactly as
+ * wf_plan_score_batch would score its rows.  Asynchronous on hip_stream. */
+wf_status wf_plan_search_batch(wf_plan_ctx *ctx, const int8_t *dev, const uint16_t *prio,
+                               const uint8_t *flags, uint64_t seed, int32_t n_mut, int64_t first,
+                               int64_t n_candidates, wf_plan_score *scores, void *hip_stream);
+
+/* Write the candidates' rows (out_dev [n][N], out_prio [n][N], out_flags
+ * [n][ceil(N/4)], device memory) -- to adopt a winner found by
+ * wf_plan_search_batch and wf_plan_argmin.  Asynchronous on hip_stream. */
+wf_status wf_plan_search_rows(wf_plan_ctx *ctx, const int8_t *dev, const uint16_t *prio,
+                              const uint8_t *flags, uint64_t seed, int32_t n_mut, int64_t first,
+                              int64_t n_candidates, int8_t *out_dev, uint16_t *out_prio,
+                              uint8_t *out_flags, void *hip_stream);
 
 /* Time arithmetic the kernels use for the uploaded window: 32 when every
  * time of every plan provably stays below 2^32 us after the window origin

@@ -20,7 +20,7 @@ STATUS_NAMES = {0: "WF_OK", 1: "WF_EINVAL", 2: "WF_ENOWINDOW", 3: "WF_ENOMEM", 4
                 5: "WF_EUNSUPPORTED"}
 WF_ST_INELIGIBLE = 1
 WF_ST_CAPACITY = 2
-WF_MAX_ACT, WF_MAX_MODELS, WF_MAX_DEV = 65535, 64, 64
+WF_MAX_ACT, WF_MAX_MODELS, WF_MAX_DEV, WF_MAX_MUT = 65535, 64, 64, 64
 
 SCORE_DTYPE = np.dtype([
     ("makespan_us", "<i8"), ("p95_us", "<i8"), ("objective", "<f4"),
@@ -32,7 +32,8 @@ assert SCORE_DTYPE.itemsize == 32
 # every symbol declared in include/wf_plan.h
 EXPORTS = ("wf_plan_ctx_create", "wf_plan_ctx_destroy", "wf_plan_last_error",
            "wf_plan_validate_window", "wf_plan_upload_window", "wf_plan_score_batch",
-           "wf_plan_argmin", "wf_plan_time_bits", "wf_plan_version")
+           "wf_plan_argmin", "wf_plan_search_batch", "wf_plan_search_rows",
+           "wf_plan_time_bits", "wf_plan_version")
 
 
 class WFError(RuntimeError):
@@ -89,6 +90,11 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.wf_plan_score_batch.restype = i32
     lib.wf_plan_argmin.argtypes = [vp, vp, i64, vp, vp]
     lib.wf_plan_argmin.restype = i32
+    u64 = ctypes.c_uint64
+    lib.wf_plan_search_batch.argtypes = [vp, vp, vp, vp, u64, ctypes.c_int32, i64, i64, vp, vp]
+    lib.wf_plan_search_batch.restype = i32
+    lib.wf_plan_search_rows.argtypes = [vp, vp, vp, vp, u64, ctypes.c_int32, i64, i64, vp, vp, vp, vp]
+    lib.wf_plan_search_rows.restype = i32
     lib.wf_plan_time_bits.argtypes = [vp]
     lib.wf_plan_time_bits.restype = i32
     lib.wf_plan_version.argtypes = []
@@ -181,6 +187,22 @@ class Context:
     def wf_plan_argmin(self, scores, n_plans: int, out_index, stream=None) -> None:
         self._check(self.lib.wf_plan_argmin(self.handle, _ptr(scores), int(n_plans),
                                             _ptr(out_index), _stream(stream)))
+
+    def wf_plan_search_batch(self, dev, prio, flags, seed: int, n_mut: int, first: int,
+                             n_candidates: int, scores, stream=None) -> None:
+        """Score candidates first .. first+n_candidates-1 generated around the
+        incumbent rows dev/prio/flags (device buffers of one plan)."""
+        self._check(self.lib.wf_plan_search_batch(
+            self.handle, _ptr(dev), _ptr(prio), _ptr(flags), int(seed) & ((1 << 64) - 1),
+            int(n_mut), int(first), int(n_candidates), _ptr(scores), _stream(stream)))
+
+    def wf_plan_search_rows(self, dev, prio, flags, seed: int, n_mut: int, first: int,
+                            n_candidates: int, out_dev, out_prio, out_flags, stream=None) -> None:
+        """Write the rows of candidates first .. first+n_candidates-1."""
+        self._check(self.lib.wf_plan_search_rows(
+            self.handle, _ptr(dev), _ptr(prio), _ptr(flags), int(seed) & ((1 << 64) - 1),
+            int(n_mut), int(first), int(n_candidates), _ptr(out_dev), _ptr(out_prio),
+            _ptr(out_flags), _stream(stream)))
 
     def wf_plan_time_bits(self) -> int:
         return int(self.lib.wf_plan_time_bits(self.handle))

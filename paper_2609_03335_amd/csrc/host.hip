@@ -186,7 +186,8 @@ wf_status validate(const wf_window_desc* w, std::string* err, HostWindow* out) {
 struct DeviceWindow {
   void* tab = nullptr;          // table image in HBM
   void* scratch = nullptr;      // per-wave regions for windows too big for LDS
-  wfp::ScoreParams sp{};
+  wfp::ScoreParams sp{};        // scoring plans read from HBM
+  wfp::ScoreParams sp_search{}; // scoring candidates generated around an incumbent
 };
 
 }  // namespace
@@ -229,7 +230,8 @@ struct Image {
 };
 
 // Per-wave LDS carve-up for G plans; returns the wave's byte size.
-int wave_layout(const HostWindow& h, int G, int tsz, int nwa, bool nibble, wfp::WaveOffsets& o) {
+int wave_layout(const HostWindow& h, int G, int tsz, int nwa, bool nibble, bool search,
+                wfp::WaveOffsets& o) {
   size_t off = 0;
   auto take = [&](size_t n) {
     const size_t at = off;
@@ -242,15 +244,21 @@ int wave_layout(const HostWindow& h, int G, int tsz, int nwa, bool nibble, wfp::
   o.rec = take((size_t)G * h.N * 4);
   o.mask = take((size_t)G * h.D * nwa * 8);
   o.acc = take((size_t)G * sizeof(wfp::PlanAcc));
+  // generated candidates keep their device and priority rows in fin's
+  // storage (after last[] when that shares it) while the order is built
+  const size_t rows_at = nibble ? align_up(last_bytes, 16) : 0;
+  const size_t rows_bytes = search ? align_up((size_t)G * h.N, 16) + (size_t)G * h.N * 2 : 0;
   if (nibble) {
-    o.fin = take(std::max(fin_bytes, last_bytes));
+    o.fin = take(std::max(std::max(fin_bytes, last_bytes), rows_at + rows_bytes));
     o.last = o.fin;
     o.stamp = 0;
   } else {
-    o.fin = take(fin_bytes);
+    o.fin = take(std::max(fin_bytes, rows_bytes));
     o.last = take(last_bytes);
     o.stamp = take((size_t)G * h.D * h.M * 2);
   }
+  o.rows = o.fin + (int)rows_at;
+  o.rows_prio = o.rows + (int)align_up((size_t)G * h.N, 16);
   o.wfm = take((size_t)G * std::max(1, h.W) * tsz);
   o.bytes = (int)off;
   return o.bytes;
@@ -357,6 +365,11 @@ wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, Image& img, wfp::Sc
       lw[((size_t)m * D + d) * 2 + 1] = h.wmib[m];
     }
   t.lw = img.put(lw.data(), lw.size() * 4);
+  std::vector<uint64_t> elig((size_t)std::max(N, 1), 0);
+  for (int32_t i = 0; i < N; ++i)
+    for (int32_t d = 0; d < D; ++d)
+      if (h.lat[(size_t)i * D + d] >= 0) elig[i] |= uint64_t(1) << d;
+  t.elig = img.put(elig.data(), elig.size() * 8);
   t.cap = img.put(h.cap.data(), h.cap.size() * 4);
   t.arr = img.put(arr.data(), arr.size());
   t.res0 = img.put(h.init_res.data(), h.init_res.size() * 8);
@@ -397,16 +410,23 @@ wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, Image& img, wfp::Sc
   sp.has_chains = 0;
   for (int32_t i = 0; i < N; ++i) sp.has_chains |= h.chain_next[i] >= 0 ? 1 : 0;
 
-  // ---- plans per wave, waves per workgroup, table placement ----
+  return WF_OK;
+}
+
+// Plans per wave, waves per workgroup and table placement for one kernel
+// mode (scoring rows from HBM, or scoring generated candidates).
+wf_status plan_launch(wf_plan_ctx* ctx, const HostWindow& h, bool search, wfp::ScoreParams& sp) {
+  const int D = h.D;
+  const int tsz = sp.time64 ? 8 : 4;
   const int lds_cu = std::min(ctx->lds_per_cu, 160 * 1024);
   const int lds_blk = std::min(ctx->lds_per_block, lds_cu);
   const int gmax = std::max(1, 64 / D);
   double best = -1.0;
   for (int tl = 1; tl >= 0; --tl) {
-    const int tab_lds = tl ? t.bytes : 0;
+    const int tab_lds = tl ? sp.t.bytes : 0;
     for (int G = gmax; G >= 1; --G) {
       wfp::WaveOffsets o{};
-      const int wb = wave_layout(h, G, tsz, sp.nwa, sp.nibble != 0, o);
+      const int wb = wave_layout(h, G, tsz, sp.nwa, sp.nibble != 0, search, o);
       int waves = std::min(8, (lds_blk - tab_lds) / std::max(wb, 1));
       if (waves < 1) continue;
       const int lds_wg = tab_lds + waves * wb;
@@ -433,13 +453,13 @@ wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, Image& img, wfp::Sc
     // per-wave regions in HBM: one plan per device lane group, a bounded grid
     wfp::WaveOffsets o{};
     const int G = gmax;
-    const int64_t wb = wave_layout(h, G, tsz, sp.nwa, sp.nibble != 0, o);
+    const int64_t wb = wave_layout(h, G, tsz, sp.nwa, sp.nibble != 0, search, o);
     const int64_t cap_bytes = int64_t(1) << 30;
     const int waves = 4;
     int64_t wgs = std::min<int64_t>((int64_t)ctx->n_cu * 2, cap_bytes / std::max<int64_t>(wb * waves, 1));
     if (wgs < 1)
       return fail(&ctx->err, WF_EUNSUPPORTED, "window too large (N=%d, widest level %d, D=%d, M=%d)",
-                  N, h.wmax, D, M);
+                  h.N, h.wmax, D, h.M);
     sp.G = G;
     sp.waves = waves;
     sp.tab_in_lds = 0;
@@ -537,6 +557,11 @@ wf_status wf_plan_upload_window(wf_plan_ctx* ctx, const wf_window_desc* w) {
   wfp::ScoreParams sp{};
   st = plan_window(ctx, h, img, sp);
   if (st != WF_OK) return st;
+  wfp::ScoreParams sps = sp;
+  st = plan_launch(ctx, h, false, sp);
+  if (st != WF_OK) return st;
+  st = plan_launch(ctx, h, true, sps);
+  if (st != WF_OK) return st;
 
   int prev = 0;
   (void)hipGetDevice(&prev);
@@ -555,18 +580,23 @@ wf_status wf_plan_upload_window(wf_plan_ctx* ctx, const wf_window_desc* w) {
     (void)hipSetDevice(prev);
     return hip_fail(ctx, e, "copying the window to the device");
   }
-  if (sp.wave_global) {
-    e = hipMalloc(&dw.scratch, (size_t)sp.grid * sp.waves * (size_t)sp.wo.bytes);
+  if (sp.wave_global || sps.wave_global) {
+    const size_t need = std::max(sp.wave_global ? (size_t)sp.grid * sp.waves * (size_t)sp.wo.bytes : 0,
+                                 sps.wave_global ? (size_t)sps.grid * sps.waves * (size_t)sps.wo.bytes : 0);
+    e = hipMalloc(&dw.scratch, need);
     if (e != hipSuccess) {
       free_device_window(dw);
       (void)hipSetDevice(prev);
       ctx->err = "device allocation of the scoring scratch failed";
       return WF_ENOMEM;
     }
-    sp.scratch = static_cast<unsigned char*>(dw.scratch);
+    if (sp.wave_global) sp.scratch = static_cast<unsigned char*>(dw.scratch);
+    if (sps.wave_global) sps.scratch = static_cast<unsigned char*>(dw.scratch);
   }
   sp.tab = static_cast<const unsigned char*>(dw.tab);
+  sps.tab = static_cast<const unsigned char*>(dw.tab);
   dw.sp = sp;
+  dw.sp_search = sps;
   if (std::getenv("WF_PLAN_VERBOSE"))
     std::fprintf(stderr,
                  "[wf_plan] N=%d W=%d D=%d M=%d levels=%d wmax=%d time=%s G=%d waves/wg=%d "
@@ -606,9 +636,75 @@ wf_status wf_plan_score_batch(wf_plan_ctx* ctx, const int8_t* dev, const uint16_
   const int64_t groups = (n_plans + sp.G - 1) / sp.G;
   const int64_t wgs = (groups + sp.waves - 1) / sp.waves;
   if (wgs < sp.grid) sp.grid = (int)wgs;
-  e = wfp::launch_score(sp, dev, prio, flags, n_plans, scores, sched, static_cast<hipStream_t>(hip_stream));
+  e = wfp::launch_score(sp, dev, prio, flags, n_plans, scores, sched, nullptr,
+                        static_cast<hipStream_t>(hip_stream));
   (void)hipSetDevice(prev);
   if (e != hipSuccess) return hip_fail(ctx, e, "launching the scoring kernel");
+  return WF_OK;
+}
+
+// Shared argument checks of the candidate-generation calls.
+static wf_status search_args(wf_plan_ctx* ctx, const int8_t* dev, const uint16_t* prio,
+                             const uint8_t* flags, int32_t n_mut, int64_t first,
+                             int64_t n_candidates) {
+  if (!ctx) {
+    g_thread_err = "ctx is NULL";
+    return WF_EINVAL;
+  }
+  if (!ctx->has_window) return fail(&ctx->err, WF_ENOWINDOW, "no window uploaded");
+  if (n_mut < 0 || n_mut > WF_MAX_MUT)
+    return fail(&ctx->err, WF_EINVAL, "n_mut must be in [0, %d]", WF_MAX_MUT);
+  if (n_candidates < 0) return fail(&ctx->err, WF_EINVAL, "n_candidates is negative");
+  if (first < 0 || first > (int64_t(1) << 62) - n_candidates)
+    return fail(&ctx->err, WF_EINVAL, "candidates must lie in [0, 2^62)");
+  if (ctx->host.N > 0 && (!dev || !prio || !flags))
+    return fail(&ctx->err, WF_EINVAL, "an incumbent row (dev, prio, flags) is NULL");
+  return WF_OK;
+}
+
+wf_status wf_plan_search_batch(wf_plan_ctx* ctx, const int8_t* dev, const uint16_t* prio,
+                               const uint8_t* flags, uint64_t seed, int32_t n_mut, int64_t first,
+                               int64_t n_candidates, wf_plan_score* scores, void* hip_stream) {
+  wf_status st = search_args(ctx, dev, prio, flags, n_mut, first, n_candidates);
+  if (st != WF_OK) return st;
+  if (n_candidates == 0) return WF_OK;
+  if (!scores) return fail(&ctx->err, WF_EINVAL, "scores is NULL");
+  int prev = 0;
+  (void)hipGetDevice(&prev);
+  hipError_t e = hipSetDevice(ctx->device);
+  if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
+  wfp::ScoreParams sp = ctx->dw.sp_search;
+  const int64_t groups = (n_candidates + sp.G - 1) / sp.G;
+  const int64_t wgs = (groups + sp.waves - 1) / sp.waves;
+  if (wgs < sp.grid) sp.grid = (int)wgs;
+  const wfp::SearchArgs sa{seed, n_mut, first};
+  e = wfp::launch_score(sp, dev, prio, flags, n_candidates, scores, nullptr, &sa,
+                        static_cast<hipStream_t>(hip_stream));
+  (void)hipSetDevice(prev);
+  if (e != hipSuccess) return hip_fail(ctx, e, "launching the scoring kernel");
+  return WF_OK;
+}
+
+wf_status wf_plan_search_rows(wf_plan_ctx* ctx, const int8_t* dev, const uint16_t* prio,
+                              const uint8_t* flags, uint64_t seed, int32_t n_mut, int64_t first,
+                              int64_t n_candidates, int8_t* out_dev, uint16_t* out_prio,
+                              uint8_t* out_flags, void* hip_stream) {
+  wf_status st = search_args(ctx, dev, prio, flags, n_mut, first, n_candidates);
+  if (st != WF_OK) return st;
+  if (n_candidates == 0 || ctx->host.N == 0) return WF_OK;
+  if (!out_dev || !out_prio || !out_flags)
+    return fail(&ctx->err, WF_EINVAL, "an output row array is NULL");
+  if (n_candidates >= (int64_t(1) << 31))
+    return fail(&ctx->err, WF_EINVAL, "n_candidates must be below 2^31");
+  int prev = 0;
+  (void)hipGetDevice(&prev);
+  hipError_t e = hipSetDevice(ctx->device);
+  if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
+  const wfp::SearchArgs sa{seed, n_mut, first};
+  e = wfp::launch_search_rows(ctx->dw.sp_search, dev, prio, flags, sa, n_candidates, out_dev,
+                              out_prio, out_flags, static_cast<hipStream_t>(hip_stream));
+  (void)hipSetDevice(prev);
+  if (e != hipSuccess) return hip_fail(ctx, e, "launching the candidate-row kernel");
   return WF_OK;
 }
 

@@ -30,6 +30,7 @@ struct TabOffsets {
   int res0;    // u64 [D]    initial resident-model mask
   int free0;   // time [D]   initial busy-until relative to the window origin
   int sink;    // u32 [S]    activations without successor in their workflow: index | workflow << 16
+  int elig;    // u64 [N]    devices d with lat[i][d] >= 0
   int bytes;
 };
 
@@ -44,6 +45,11 @@ struct WaveOffsets {
   int fin;     // time [G][N]      latest predecessor finish, then the activation's own finish
   int acc;     // PlanAcc [G]
   int stamp;   // u16 [G*D][M]     last use of each model (general reclamation only)
+  int rows;    // generated candidates only: int8 [G][N] devices, then u16 [G][N]
+               //                  priorities at rows + rows_prio; they live in fin's
+               //                  storage (after last[] when that shares it) until
+               //                  the order is built
+  int rows_prio;
   int wfm;     // time [G][W]      latest finish per workflow
   int bytes;
 };
@@ -83,9 +89,26 @@ struct PlanAcc {
   uint32_t pad;
 };
 
+// Candidates generated around an incumbent plan instead of read from HBM.
+struct SearchArgs {
+  uint64_t seed;
+  int32_t n_mut;
+  int64_t first;  // index of the first candidate
+};
+
+// Scores plans read from dev/prio/flags ([P][N] rows), or -- with search --
+// candidates first .. first+P-1 generated around the incumbent rows dev/prio/
+// flags ([N] each).
 hipError_t launch_score(const ScoreParams& sp, const int8_t* dev, const uint16_t* prio,
                         const uint8_t* flags, int64_t n_plans, wf_plan_score* scores,
-                        const wf_plan_sched* sched, hipStream_t stream);
+                        const wf_plan_sched* sched, const SearchArgs* search,
+                        hipStream_t stream);
+
+// Rows of candidates first .. first+P-1 around the incumbent rows.
+hipError_t launch_search_rows(const ScoreParams& sp, const int8_t* dev, const uint16_t* prio,
+                              const uint8_t* flags, const SearchArgs& search, int64_t n,
+                              int8_t* out_dev, uint16_t* out_prio, uint8_t* out_flags,
+                              hipStream_t stream);
 
 hipError_t launch_argmin(const wf_plan_score* scores, int64_t n_plans, int64_t* out_index,
                          int grid, hipStream_t stream);

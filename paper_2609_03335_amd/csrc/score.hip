@@ -62,6 +62,19 @@ __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_wave_barrier();
 }
 
+// Copy nbytes with 4-byte accesses when source, destination and size allow.
+__device__ __forceinline__ void copy_row(unsigned char* dst, const unsigned char* src, int nbytes,
+                                         int lane) {
+  if (((reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(dst) | (uintptr_t)nbytes) &
+       3) == 0) {
+    const uint32_t* s = reinterpret_cast<const uint32_t*>(src);
+    uint32_t* d = reinterpret_cast<uint32_t*>(dst);
+    for (int i = lane; i < (nbytes >> 2); i += 64) d[i] = s[i];
+  } else {
+    for (int i = lane; i < nbytes; i += 64) dst[i] = src[i];
+  }
+}
+
 // Copy nbytes from HBM with the widest aligned accesses.
 __device__ __forceinline__ void stage(unsigned char* dst, const unsigned char* src, int nbytes,
                                       int lane) {
@@ -83,6 +96,54 @@ __device__ __forceinline__ int fuse_bit(const uint8_t* fl, int v) {
   return (fl[v >> 2] >> ((v & 3) << 1)) & 1;
 }
 
+// Philox4x32-10 (Salmon, Moraes, Dror and Shaw, SC'11): ten rounds of the
+// Philox-4x32 bijection of the counter x, the key bumped by the Weyl
+// constants after every round.
+__device__ __forceinline__ void philox4x32_10(uint32_t x[4], uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int round = 0; round < 10; ++round) {
+    const uint32_t a = x[0], c = x[2];
+    x[0] = __umulhi(0xCD9E8D57u, c) ^ x[1] ^ k0;
+    x[1] = 0xCD9E8D57u * c;
+    x[2] = __umulhi(0xD2511F53u, a) ^ x[3] ^ k1;
+    x[3] = 0xD2511F53u * a;
+    k0 += 0x9E3779B9u;
+    k1 += 0xBB67AE85u;
+  }
+}
+
+// Turns rows (dev, prio, flags) holding the incumbent into candidate c: the
+// n_mut mutations drawn from Philox4x32-10 with counter (c, t) and the
+// seed as key -- another eligible device for activation i, a swap of two
+// priorities inside i's level, or a toggled fuse / prefetch bit of i.
+__device__ __forceinline__ void mutate(uint64_t c, const SearchArgs& sa, int N,
+                                       const unsigned long long* elig, const uint32_t* alv,
+                                       int8_t* rd, uint16_t* rp, uint8_t* rf) {
+  if (N <= 0) return;
+  for (int t = 0; t < sa.n_mut; ++t) {
+    uint32_t x[4] = {(uint32_t)c, (uint32_t)(c >> 32), (uint32_t)t, 0u};
+    philox4x32_10(x, (uint32_t)sa.seed, (uint32_t)(sa.seed >> 32));
+    const int i = (int)__umulhi(x[1], (uint32_t)N);
+    const uint32_t kind = x[0] >> 30;
+    if (kind == 0u) {
+      unsigned long long e = elig[i];
+      const uint32_t n = (uint32_t)__popcll(e);
+      if (n) {
+        for (uint32_t k = __umulhi(x[2], n); k; --k) e &= e - 1ull;
+        rd[i] = (int8_t)__builtin_ctzll(e);
+      }
+    } else if (kind == 1u) {
+      const uint32_t lvw = alv[i];
+      const int j = (int)(lvw & 0xffffu) + (int)__umulhi(x[2], lvw >> 16);
+      const uint16_t pi = rp[i];
+      rp[i] = rp[j];
+      rp[j] = pi;
+    } else {
+      rf[i >> 2] ^= (uint8_t)(1u << (((i & 3) << 1) + (kind == 3u ? 1 : 0)));
+    }
+  }
+}
+
 // slot entry: activation | model << 16 | prefetch << 22 | has fused successor << 23 |
 // device << 24 | last unit of its model on the device << 30
 constexpr uint32_t kPf = 1u << 22;
@@ -102,13 +163,16 @@ struct UnitPre {
   int2 lw;        // model load time on the device, model weights
 };
 
-template <typename TT, bool TAB_LDS, bool NIBBLE, bool WAVE_GLOBAL>
+// SEARCH: plans are candidates generated around the incumbent rows dev_all,
+// prio_all, flags_all ([N] each) rather than [P][N] rows read from HBM.
+template <typename TT, bool TAB_LDS, bool NIBBLE, bool WAVE_GLOBAL, bool SEARCH>
 __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
                                                    const int8_t* __restrict__ dev_all,
                                                    const uint16_t* __restrict__ prio_all,
                                                    const uint8_t* __restrict__ flags_all, int64_t P,
                                                    wf_plan_score* __restrict__ scores,
-                                                   wf_plan_sched sched, int has_sched) {
+                                                   wf_plan_sched sched, int has_sched,
+                                                   SearchArgs sa) {
   using TO = TimeOps<TT>;
   using TB = typename TO::bits_t;
   extern __shared__ __align__(16) unsigned char lds[];
@@ -145,6 +209,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   const unsigned long long* t_res0 = reinterpret_cast<const unsigned long long*>(tb + sp.t.res0);
   const TB* t_free0 = reinterpret_cast<const TB*>(tb + sp.t.free0);
   const uint32_t* t_sink = reinterpret_cast<const uint32_t*>(tb + sp.t.sink);
+  const unsigned long long* t_elig = reinterpret_cast<const unsigned long long*>(tb + sp.t.elig);
   const int mem_si = sp.mem_si;
 
   // ---- this wave's region (LDS, or HBM scratch for very large windows) ----
@@ -161,6 +226,8 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   PlanAcc* s_acc = reinterpret_cast<PlanAcc*>(wl + sp.wo.acc);
   uint16_t* s_stamp = reinterpret_cast<uint16_t*>(wl + sp.wo.stamp);
   TB* s_wfm = reinterpret_cast<TB*>(wl + sp.wo.wfm);
+  int8_t* s_rdev = reinterpret_cast<int8_t*>(wl + sp.wo.rows);         // generated candidates
+  uint16_t* s_rprio = reinterpret_cast<uint16_t*>(wl + sp.wo.rows_prio);
 
   const int g_me = lane / D;
   const int d_me = lane - g_me * D;
@@ -172,12 +239,12 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   const int2* lw_d = t_lw + d_me;
 
   // rows read four activations per lane with 4- and 8-byte loads
-  const bool vec = (N & 3) == 0 && (reinterpret_cast<uintptr_t>(dev_all) & 3) == 0 &&
-                   (reinterpret_cast<uintptr_t>(prio_all) & 7) == 0;
+  const bool vec = (N & 3) == 0 && (SEARCH || ((reinterpret_cast<uintptr_t>(dev_all) & 3) == 0 &&
+                                               (reinterpret_cast<uintptr_t>(prio_all) & 7) == 0));
   // one 256-activation chunk and at most eight plans per group: the next
   // group's device and priority rows are loaded while this group is walked
   constexpr int kB = 8;
-  const bool pre = vec && N <= 256 && G <= kB;
+  const bool pre = !SEARCH && vec && N <= 256 && G <= kB;
   uint32_t dvp[kB];
   uint2 pvp[kB];
   auto load_rows = [&](int64_t grp_, uint32_t* dv, uint2* pv) {
@@ -201,7 +268,23 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
     const int gc = (int)((P - p0) < G ? (P - p0) : G);
 
     // ---- stage the group's flag rows, clear the ordering state ----
-    stage(s_fl, flags_all + p0 * NB, gc * NB, lane);
+    if constexpr (SEARCH) {
+      // every plan of the group starts as the incumbent, then takes its
+      // candidate's mutations (one lane per plan, in order)
+      for (int g = 0; g < gc; ++g) {
+        copy_row(reinterpret_cast<unsigned char*>(s_rdev + g * N),
+                 reinterpret_cast<const unsigned char*>(dev_all), N, lane);
+        copy_row(reinterpret_cast<unsigned char*>(s_rprio + g * N),
+                 reinterpret_cast<const unsigned char*>(prio_all), 2 * N, lane);
+        copy_row(s_fl + g * NB, flags_all, NB, lane);
+      }
+      wave_sync();
+      if (lane < gc)
+        mutate((uint64_t)(sa.first + p0 + lane), sa, N, t_elig, t_alv, s_rdev + lane * N,
+               s_rprio + lane * N, s_fl + lane * NB);
+    } else {
+      stage(s_fl, flags_all + p0 * NB, gc * NB, lane);
+    }
     for (int i = lane; i < G * D * M; i += 64) s_last[i] = 0u;
     for (int i = lane; i < G * D * NWA; i += 64) s_mask[i] = 0ull;
     if (lane < G) {
@@ -257,6 +340,15 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
         s_acc[g].heads += tot;
       }
     };
+    // device and priority rows of plan g: HBM, or the generated candidate
+    auto row_dev = [&](int g) -> const int8_t* {
+      if constexpr (SEARCH) return s_rdev + g * N;
+      else return dev_all + (p0 + g) * N;
+    };
+    auto row_prio = [&](int g) -> const uint16_t* {
+      if constexpr (SEARCH) return s_rprio + g * N;
+      else return prio_all + (p0 + g) * N;
+    };
     // the rows of plans g0 .. g0 + kB - 1 at activations uc .. uc + 3
     auto rows4 = [&](int g0, int uc, uint32_t* dv, uint2* pv) {
 #pragma unroll
@@ -266,8 +358,8 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
           dv[k] = dvp[k];
           pv[k] = pvp[k];
         } else {
-          dv[k] = *reinterpret_cast<const uint32_t*>(dev_all + (p0 + g) * N + uc);
-          pv[k] = *reinterpret_cast<const uint2*>(prio_all + (p0 + g) * N + uc);
+          dv[k] = *reinterpret_cast<const uint32_t*>(row_dev(g) + uc);
+          pv[k] = *reinterpret_cast<const uint2*>(row_prio(g) + uc);
         }
       }
     };
@@ -317,8 +409,8 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
       }
     } else {
       for (int g = 0; g < gc; ++g) {
-        const int8_t* pdev = dev_all + (p0 + g) * N;
-        const uint16_t* pprio = prio_all + (p0 + g) * N;
+        const int8_t* pdev = row_dev(g);
+        const uint16_t* pprio = row_prio(g);
         const uint8_t* pfl = s_fl + g * NB;
         uint32_t nh = 0, nbad = 0, ninel = 0;
         for (int u = lane; u < N; u += 64) {
@@ -352,8 +444,8 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
     // general path: rank by (priority, index) within each level
     for (uint64_t rm = rankedm; rm; rm &= rm - 1ull) {
       const int g = __builtin_ctzll(rm);
-      const int8_t* pdev = dev_all + (p0 + g) * N;
-      const uint16_t* pprio = prio_all + (p0 + g) * N;
+      const int8_t* pdev = row_dev(g);
+      const uint16_t* pprio = row_prio(g);
       const uint8_t* pfl = s_fl + g * NB;
       uint32_t* rec = s_rec + g * N;
       unsigned long long* mk = s_mask + g * D * NWA;
@@ -824,47 +916,98 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   }
 }
 
-template <typename TT, bool TAB_LDS, bool NIBBLE, bool WAVE_GLOBAL>
+template <typename TT, bool TAB_LDS, bool NIBBLE, bool WAVE_GLOBAL, bool SEARCH>
 hipError_t launch_variant(const ScoreParams& sp, const int8_t* dev, const uint16_t* prio,
                           const uint8_t* flags, int64_t n_plans, wf_plan_score* scores,
-                          const wf_plan_sched& s, int has, hipStream_t stream) {
-  auto k = score_plans<TT, TAB_LDS, NIBBLE, WAVE_GLOBAL>;
+                          const wf_plan_sched& s, int has, const SearchArgs& sa,
+                          hipStream_t stream) {
+  auto k = score_plans<TT, TAB_LDS, NIBBLE, WAVE_GLOBAL, SEARCH>;
   (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k),
                             hipFuncAttributeMaxDynamicSharedMemorySize, sp.lds_bytes);
   hipLaunchKernelGGL(k, dim3(sp.grid), dim3(64 * sp.waves), sp.lds_bytes, stream, sp, dev, prio,
-                     flags, n_plans, scores, s, has);
+                     flags, n_plans, scores, s, has, sa);
   return hipGetLastError();
 }
 
-template <typename TT, bool NIBBLE>
+template <typename TT, bool NIBBLE, bool SEARCH>
 hipError_t launch_place(const ScoreParams& sp, const int8_t* dev, const uint16_t* prio,
                         const uint8_t* flags, int64_t n_plans, wf_plan_score* scores,
-                        const wf_plan_sched& s, int has, hipStream_t stream) {
+                        const wf_plan_sched& s, int has, const SearchArgs& sa, hipStream_t stream) {
   if (sp.wave_global)
-    return launch_variant<TT, false, NIBBLE, true>(sp, dev, prio, flags, n_plans, scores, s, has, stream);
+    return launch_variant<TT, false, NIBBLE, true, SEARCH>(sp, dev, prio, flags, n_plans, scores,
+                                                           s, has, sa, stream);
   if (sp.tab_in_lds)
-    return launch_variant<TT, true, NIBBLE, false>(sp, dev, prio, flags, n_plans, scores, s, has, stream);
-  return launch_variant<TT, false, NIBBLE, false>(sp, dev, prio, flags, n_plans, scores, s, has, stream);
+    return launch_variant<TT, true, NIBBLE, false, SEARCH>(sp, dev, prio, flags, n_plans, scores,
+                                                           s, has, sa, stream);
+  return launch_variant<TT, false, NIBBLE, false, SEARCH>(sp, dev, prio, flags, n_plans, scores,
+                                                          s, has, sa, stream);
+}
+
+template <typename TT, bool SEARCH>
+hipError_t launch_time(const ScoreParams& sp, const int8_t* dev, const uint16_t* prio,
+                       const uint8_t* flags, int64_t n_plans, wf_plan_score* scores,
+                       const wf_plan_sched& s, int has, const SearchArgs& sa, hipStream_t stream) {
+  if (sp.nibble)
+    return launch_place<TT, true, SEARCH>(sp, dev, prio, flags, n_plans, scores, s, has, sa, stream);
+  return launch_place<TT, false, SEARCH>(sp, dev, prio, flags, n_plans, scores, s, has, sa, stream);
 }
 
 template <typename TT>
-hipError_t launch_time(const ScoreParams& sp, const int8_t* dev, const uint16_t* prio,
+hipError_t launch_mode(const ScoreParams& sp, const int8_t* dev, const uint16_t* prio,
                        const uint8_t* flags, int64_t n_plans, wf_plan_score* scores,
-                       const wf_plan_sched& s, int has, hipStream_t stream) {
-  if (sp.nibble) return launch_place<TT, true>(sp, dev, prio, flags, n_plans, scores, s, has, stream);
-  return launch_place<TT, false>(sp, dev, prio, flags, n_plans, scores, s, has, stream);
+                       const wf_plan_sched& s, int has, const SearchArgs* search,
+                       hipStream_t stream) {
+  if (search)
+    return launch_time<TT, true>(sp, dev, prio, flags, n_plans, scores, s, 0, *search, stream);
+  return launch_time<TT, false>(sp, dev, prio, flags, n_plans, scores, s, has, SearchArgs{}, stream);
+}
+
+// One workgroup per candidate: the incumbent's rows, then its mutations.
+__global__ __launch_bounds__(64) void search_rows(const int8_t* __restrict__ dev,
+                                                  const uint16_t* __restrict__ prio,
+                                                  const uint8_t* __restrict__ flags, SearchArgs sa,
+                                                  int N, const unsigned long long* elig,
+                                                  const uint32_t* alv, int8_t* out_dev,
+                                                  uint16_t* out_prio, uint8_t* out_flags) {
+  const int64_t k = blockIdx.x;
+  const int NB = (N + 3) / 4;
+  int8_t* rd = out_dev + k * N;
+  uint16_t* rp = out_prio + k * N;
+  uint8_t* rf = out_flags + k * NB;
+  for (int i = threadIdx.x; i < N; i += 64) {
+    rd[i] = dev[i];
+    rp[i] = prio[i];
+  }
+  for (int i = threadIdx.x; i < NB; i += 64) rf[i] = flags[i];
+  __syncthreads();
+  if (threadIdx.x == 0) mutate((uint64_t)(sa.first + k), sa, N, elig, alv, rd, rp, rf);
 }
 
 }  // namespace
 
 hipError_t launch_score(const ScoreParams& sp, const int8_t* dev, const uint16_t* prio,
                         const uint8_t* flags, int64_t n_plans, wf_plan_score* scores,
-                        const wf_plan_sched* sched, hipStream_t stream) {
+                        const wf_plan_sched* sched, const SearchArgs* search,
+                        hipStream_t stream) {
   wf_plan_sched s{};
   if (sched) s = *sched;
   const int has = sched != nullptr;
-  if (sp.time64) return launch_time<double>(sp, dev, prio, flags, n_plans, scores, s, has, stream);
-  return launch_time<uint32_t>(sp, dev, prio, flags, n_plans, scores, s, has, stream);
+  if (sp.time64)
+    return launch_mode<double>(sp, dev, prio, flags, n_plans, scores, s, has, search, stream);
+  return launch_mode<uint32_t>(sp, dev, prio, flags, n_plans, scores, s, has, search, stream);
 }
+
+hipError_t launch_search_rows(const ScoreParams& sp, const int8_t* dev, const uint16_t* prio,
+                              const uint8_t* flags, const SearchArgs& search, int64_t n,
+                              int8_t* out_dev, uint16_t* out_prio, uint8_t* out_flags,
+                              hipStream_t stream) {
+  const unsigned long long* elig =
+      reinterpret_cast<const unsigned long long*>(sp.tab + sp.t.elig);
+  const uint32_t* alv = reinterpret_cast<const uint32_t*>(sp.tab + sp.t.alv);
+  hipLaunchKernelGGL(search_rows, dim3((unsigned)n), dim3(64), 0, stream, dev, prio, flags, search,
+                     sp.N, elig, alv, out_dev, out_prio, out_flags);
+  return hipGetLastError();
+}
+
 
 }  // namespace wfp
