@@ -62,6 +62,14 @@ __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_wave_barrier();
 }
 
+// Zero nbytes at a 16-byte aligned address: 16-byte stores, then the tail.
+__device__ __forceinline__ void zero_bytes(unsigned char* dst, int nbytes, int lane) {
+  uint4* d = reinterpret_cast<uint4*>(dst);
+  const int n16 = nbytes >> 4;
+  for (int i = lane; i < n16; i += 64) d[i] = make_uint4(0u, 0u, 0u, 0u);
+  for (int i = (n16 << 4) + lane; i < nbytes; i += 64) dst[i] = 0;
+}
+
 // Copy nbytes with 4-byte accesses when source, destination and size allow.
 __device__ __forceinline__ void copy_row(unsigned char* dst, const unsigned char* src, int nbytes,
                                          int lane) {
@@ -285,8 +293,8 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
     } else {
       stage(s_fl, flags_all + p0 * NB, gc * NB, lane);
     }
-    for (int i = lane; i < G * D * M; i += 64) s_last[i] = 0u;
-    for (int i = lane; i < G * D * NWA; i += 64) s_mask[i] = 0ull;
+    zero_bytes(reinterpret_cast<unsigned char*>(s_last), G * D * M * 4, lane);
+    zero_bytes(reinterpret_cast<unsigned char*>(s_mask), G * D * NWA * 8, lane);
     if (lane < G) {
       PlanAcc a0;
       a0.status = 0u;
@@ -607,8 +615,8 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
     if constexpr (NIBBLE) wave_sync();  // last[] (aliasing fin) is read above
     // every finish starts at 0: it accumulates the latest predecessor finish
     // before its level, then holds the activation's own finish
-    for (int i = lane; i < G * N; i += 64) s_fin[i] = 0;
-    for (int i = lane; i < G * W; i += 64) s_wfm[i] = 0;
+    zero_bytes(reinterpret_cast<unsigned char*>(s_fin), G * N * (int)sizeof(TB), lane);
+    zero_bytes(reinterpret_cast<unsigned char*>(s_wfm), G * W * (int)sizeof(TB), lane);
     wave_sync();
 
     for (int lv = 0; lv < sp.n_levels; ++lv) {
