@@ -171,6 +171,31 @@ def main():
     if torch.distributed.is_available() and torch.distributed.is_initialized():
         torch.distributed.barrier()
     kernel_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    # the argmin on its own
+    aev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    for a, b in aev:
+        a.record(stream)
+        ctx.wf_plan_argmin(scores, P, best, stream)
+        b.record(stream)
+    torch.cuda.synchronize()
+    argmin_ms = float(np.mean([a.elapsed_time(b) for a, b in aev]))
+    # a plain streaming kernel over the same number of bytes: the bandwidth
+    # this GPU actually delivers
+    bpp0 = algorithmic_bytes_per_plan(N)
+    nbytes = bpp0 * P // 2
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda:0")
+    dst = torch.empty_like(src)
+    torch.bitwise_not(src, out=dst)
+    cev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(5)]
+    for a, b in cev:
+        a.record(stream)
+        torch.bitwise_not(src, out=dst)
+        b.record(stream)
+    torch.cuda.synchronize()
+    copy_gbs = 2 * nbytes / (float(np.median([a.elapsed_time(b) for a, b in cev])) * 1e-3) / 1e9
+    del src, dst
     ms_per_step = t_total * 1e3 / args.steps
     value = P * args.steps / t_total
 
@@ -180,7 +205,8 @@ def main():
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                 "kernel": "score_plans", "kernel_ms": round(kernel_ms, 4),
-                "bytes_per_plan": bpp}
+                "bytes_per_plan": bpp, "copy_gbs_measured": round(copy_gbs, 1),
+                "frac_of_copy": round(achieved / copy_gbs, 4), "argmin_ms": round(argmin_ms, 4)}
 
     # candidates generated around plan 0 on the GPU and scored (no plan rows
     # in HBM): the same number of plans, same window
@@ -228,9 +254,16 @@ def main():
         oracle.score(win, sample, threads=threads)
         dt, dc = time.perf_counter() - t, time.process_time() - c
         what = "the whole batch" if n_cpu == P else f"{n_cpu} evenly spaced plans of the batch"
+        # one thread on a smaller evenly spaced sample
+        n1 = min(P, 50_000)
+        s1 = plans.take(np.arange(n1) * max(1, P // n1))
+        t = time.perf_counter()
+        oracle.score(win, s1, threads=1)
+        d1 = time.perf_counter() - t
         cpu = {"value": round(n_cpu / dt, 1), "unit": "plans/s", "cores": threads, "kind": "oracle",
                "sample": f"{what}, {threads} threads, {dt:.2f} s wall, {dc:.1f} s CPU "
-                         f"({cpu_model()})"}
+                         f"({cpu_model()}, {os.cpu_count()} logical CPUs visible)",
+               "value_1_thread": round(n1 / d1, 1)}
 
     line = {
         "metric": "candidate plans scored/sec at 1 GPU; achieved HBM GB/s vs peak",
@@ -239,7 +272,9 @@ def main():
         "scaling": "weak", "vs_baseline": None, "dtype": dtype, "data": "synthetic",
         "config": {"workload": workload.CONFIGS[args.config]["name"], "n_act": N,
                    "n_wf": win.n_wf, "n_dev": D, "n_models": win.n_models, "n_plans": P,
-                   "batch_bytes": bpp * P},
+                   "batch_bytes": bpp * P,
+                   # batches below the 256 MB last-level cache can be read from it
+                   "cache_resident": bool(bpp * P < 256 * 2 ** 20)},
         "roofline": roofline,
         "cpu_baseline": cpu,
         "search": search,
