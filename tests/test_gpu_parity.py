@@ -328,3 +328,31 @@ def test_wide_level_sparse_device(ctx, n_children):
     assert_sched(gs, rs, ref["status"], "fan")
     assert got.tobytes() == ref.tobytes()
     assert best == best_plan(ref)
+
+
+def test_two_contexts_on_two_host_threads():
+    """One context per host thread, each with its own window and stream,
+    scoring at the same time."""
+    import threading
+    jobs = [W.make_config(1, n_plans=2000), W.make_config(0, n_plans=512)]
+    out = [None, None]
+
+    def run(k):
+        win, plans = jobs[k]
+        s = torch.cuda.Stream()
+        with pkg.Context(0) as c, torch.cuda.stream(s):
+            c.wf_plan_upload_window(win)
+            dev, prio, flags = pkg.device_plans(plans, "cuda:0")
+            for _ in range(3):
+                sc = pkg.score_batch(c, dev, prio, flags, plans.n_plans, stream=s)
+            s.synchronize()
+            out[k] = pkg.scores_to_numpy(sc, plans.n_plans)
+
+    ts = [threading.Thread(target=run, args=(k,)) for k in range(2)]
+    for t in ts:
+        t.start()
+    for t in ts:
+        t.join()
+    for k in range(2):
+        win, plans = jobs[k]
+        assert out[k] is not None and out[k].tobytes() == oracle.score(win, plans).tobytes()
