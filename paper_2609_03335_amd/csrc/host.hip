@@ -356,7 +356,6 @@ wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, Image& img, wfp::Sc
   t.loff = img.put(h.level_off.data(), h.level_off.size() * 4);
   t.lat = img.put(h.lat.data(), h.lat.size() * 4);
   t.mem = mem_uniform ? img.put(mem1.data(), mem1.size() * 4) : img.put(h.mem.data(), h.mem.size() * 4);
-  t.load = img.put(h.load.data(), h.load.size() * 4);
   t.wmib = img.put(h.wmib.data(), h.wmib.size() * 4);
   std::vector<int32_t> lw((size_t)M * D * 2);
   for (int32_t m = 0; m < M; ++m)
@@ -394,10 +393,8 @@ wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, Image& img, wfp::Sc
   sp.M = M;
   sp.D = D;
   sp.NB = (N + 3) / 4;
-  sp.E = E;
   sp.S = S;
   sp.n_levels = h.n_levels;
-  sp.wmax = std::max(1, h.wmax);
   sp.nwa = std::max(1, (N + 63) / 64);
   sp.mem_si = mem_uniform ? 1 : D;
   sp.mem_sd = mem_uniform ? 0 : 1;
@@ -601,7 +598,7 @@ wf_status wf_plan_upload_window(wf_plan_ctx* ctx, const wf_window_desc* w) {
     std::fprintf(stderr,
                  "[wf_plan] N=%d W=%d D=%d M=%d levels=%d wmax=%d time=%s G=%d waves/wg=%d "
                  "grid=%d tables=%s(%d B) wave=%d B lds/wg=%d reclaim=%s\n",
-                 sp.N, sp.W, sp.D, sp.M, sp.n_levels, sp.wmax, sp.time64 ? "fp64" : "u32", sp.G,
+                 sp.N, sp.W, sp.D, sp.M, sp.n_levels, h.wmax, sp.time64 ? "fp64" : "u32", sp.G,
                  sp.waves, sp.grid, sp.wave_global ? "hbm+scratch" : (sp.tab_in_lds ? "lds" : "hbm"),
                  sp.t.bytes, sp.wo.bytes, sp.lds_bytes, sp.nibble ? "queue" : "scan");
   free_device_window(ctx->dw);

@@ -22,7 +22,6 @@ struct TabOffsets {
   int loff;    // i32 [L+1]  first activation of each level
   int lat;     // i32 [N*D]  run time, -1 ineligible
   int mem;     // i32        activation memory, element (i, d) at i * mem_si + d * mem_sd
-  int load;    // i32 [M*D]  load time
   int lw;      // i32x2 [M*D] {load time, model weights}
   int wmib;    // i32 [M]    model weights
   int cap;     // i32 [D]    device capacity
@@ -55,7 +54,7 @@ struct WaveOffsets {
 };
 
 struct ScoreParams {
-  int32_t N, W, M, D, NB, E, S, n_levels, wmax, nwa;
+  int32_t N, W, M, D, NB, S, n_levels, nwa;
   int32_t mem_si, mem_sd;     // activation-memory table strides
   int64_t origin;             // absolute time of relative time 0
   int64_t min_arrival;        // first workflow arrival (absolute)

@@ -1,24 +1,24 @@
 // Batched scoring of candidate physical execution plans on gfx950.
 //
-// A workgroup of several waves first copies the window's table image into
-// LDS (shared by its waves).  Each wave then loops over groups of G plans
-// (persistent grid) and, per group:
-//   1. stages the G packed device rows and flag rows into its own LDS
-//      region with 16-byte loads (priorities are read once, from HBM);
-//   2. counts unit heads per (device, model) -- the remaining uses that the
-//      reclamation rule consults (lanes over activations);
-//   3. for every topological level, per plan (lanes over activations):
-//        - each unit head's slot in the resource order (priority, index)
-//          (Eq. 10): its priority minus the level's first index when the
-//          level's head priorities are distinct values in range (the
-//          permutation case), else its rank by (priority, index);
-//        - releases r = max(arrival, latest predecessor finish) (Eq. 2): one
-//          lane per incoming edge, an LDS atomic max on order-preserving
-//          time bits;
-//      then lane (g, d) = (lane / D, lane % D) walks device d of plan g over
-//      the level's slots in order: reuse / reclaim / load (Eq. 5, Eq. 11)
-//      and the max-plus timeline of Eq. 7;
-//   4. reduces makespan, nearest-rank p95, objective and headroom.
+// A persistent grid of waves loops over groups of G plans; lane (g, d) =
+// (lane / D, lane % D) owns device d of plan g.  The window's table image is
+// read from LDS (one copy per workgroup) or through the cache.  Per group:
+//   1. flag rows are staged into the wave's LDS region; device and priority
+//      rows are read four activations per lane (or built in LDS for
+//      candidates generated around an incumbent);
+//   2. resource order (Eq. 10): each unit head's slot is its priority when
+//      every level's head priorities are distinct values in the level's index
+//      range (checked by counting heads against distinct slots), else its rank
+//      by (priority, index) within the level; slot entries, per-device slot
+//      masks and each (device, model)'s last slot are recorded, and the last
+//      unit of each model on each device is marked;
+//   3. per topological level: releases r = max(arrival, latest predecessor
+//      finish) (Eq. 2) by LDS atomic max over the level's incoming edges,
+//      accumulated in the finish array itself; then each device lane walks its
+//      units of the level in slot order -- reuse / reclaim / load (Eq. 5,
+//      Eq. 11) and the max-plus timeline of Eq. 7 -- with everything that
+//      does not depend on the device's sequential state loaded a unit ahead;
+//   4. makespan, nearest-rank p95, objective, headroom and counts.
 // Residency, reclamation and memory depend only on each device's unit
 // sequence, never on times, so device lanes are independent within a level;
 // every predecessor sits at a lower level, so releases are final when a
