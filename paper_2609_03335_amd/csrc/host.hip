@@ -403,7 +403,23 @@ wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, Image& img, wfp::Sc
   sp.w_mk = h.w_mk;
   sp.w_p95 = h.w_p95;
   sp.time64 = time64 ? 1 : 0;
-  sp.nibble = M <= 16 ? 1 : 0;
+  // with M <= 16 the resident set is a queue of 4-bit model ids; it fits in
+  // 32 bits when no device can ever hold more than 8 models: a device holds
+  // its initial set, or models whose weights sum to at most its capacity, or
+  // (after a load that overflows) the one model just loaded
+  sp.nibble = 0;
+  if (M <= 16) {
+    std::vector<int32_t> w(h.wmib.begin(), h.wmib.begin() + M);
+    std::sort(w.begin(), w.end());
+    int qcap = 1;
+    for (int32_t d = 0; d < D; ++d) {
+      int k = 0;
+      int64_t sum = 0;
+      while (k < M && sum + w[k] <= h.cap[d]) sum += w[k++];
+      qcap = std::max(qcap, std::max(k, __builtin_popcountll(h.init_res[d])));
+    }
+    sp.nibble = qcap <= 8 ? 32 : 64;
+  }
   sp.has_chains = 0;
   for (int32_t i = 0; i < N; ++i) sp.has_chains |= h.chain_next[i] >= 0 ? 1 : 0;
 
@@ -600,7 +616,7 @@ wf_status wf_plan_upload_window(wf_plan_ctx* ctx, const wf_window_desc* w) {
                  "grid=%d tables=%s(%d B) wave=%d B lds/wg=%d reclaim=%s\n",
                  sp.N, sp.W, sp.D, sp.M, sp.n_levels, h.wmax, sp.time64 ? "fp64" : "u32", sp.G,
                  sp.waves, sp.grid, sp.wave_global ? "hbm+scratch" : (sp.tab_in_lds ? "lds" : "hbm"),
-                 sp.t.bytes, sp.wo.bytes, sp.lds_bytes, sp.nibble ? "queue" : "scan");
+                 sp.t.bytes, sp.wo.bytes, sp.lds_bytes, sp.nibble == 32 ? "queue32" : sp.nibble == 64 ? "queue64" : "scan");
   free_device_window(ctx->dw);
   ctx->dw = dw;
   ctx->host = std::move(h);

@@ -70,7 +70,7 @@ struct ScoreParams {
   int lds_bytes;              // dynamic LDS per workgroup
   int grid;                   // workgroups (persistent)
   int time64;                 // 1: fp64 times, 0: uint32 times
-  int nibble;                 // 1: M <= 16, in-register reclamation queue
+  int nibble;                 // reclamation queue width in bits (32 or 64), 0: scan
   int has_chains;             // 1: some activation satisfies Eq. 3 (fused units possible)
 };
 

@@ -27,6 +27,8 @@
 // Times are relative to the window origin (earliest arrival or free time):
 // uint32 when the host has proven no time of any plan can reach 2^32, else
 // fp64 (every time is an integer below 2^53, so fp64 max/add are exact).
+#include <type_traits>
+
 #include "kernels.h"
 
 namespace wfp {
@@ -173,7 +175,7 @@ struct UnitPre {
 
 // SEARCH: plans are candidates generated around the incumbent rows dev_all,
 // prio_all, flags_all ([N] each) rather than [P][N] rows read from HBM.
-template <typename TT, bool TAB_LDS, bool NIBBLE, bool WAVE_GLOBAL, bool SEARCH>
+template <typename TT, bool TAB_LDS, int QB, bool WAVE_GLOBAL, bool SEARCH>
 __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
                                                    const int8_t* __restrict__ dev_all,
                                                    const uint16_t* __restrict__ prio_all,
@@ -183,6 +185,12 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
                                                    SearchArgs sa) {
   using TO = TimeOps<TT>;
   using TB = typename TO::bits_t;
+  // reclamation queue: QB bits of 4-bit model ids (QB = 0: no queue, the
+  // resident set is scanned instead)
+  constexpr bool NIBBLE = QB != 0;
+  using QT = std::conditional_t<QB == 32, uint32_t, uint64_t>;
+  constexpr QT kOnes = (QT)0x1111111111111111ull, kHigh = (QT)0x8888888888888888ull;
+  constexpr int kQBits = (int)sizeof(QT) * 8;
   extern __shared__ __align__(16) unsigned char lds[];
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int N = sp.N, W = sp.W, M = sp.M, D = sp.D, NB = sp.NB, G = sp.G, NWA = sp.nwa;
@@ -583,23 +591,23 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
     // in the low bits: first the nd resident models with no remaining use on
     // this device, then those still needed, each part in least-recently-used
     // order (never used: by id); nq entries in all
-    uint64_t Q = 0;
+    QT Q = 0;
     int nd = 0, nq = 0;
     if (act) {
       res = t_res0[d];
       capd = t_cap[d];
       freet = TO::load(t_free0 + d);
-      uint64_t qa = 0;
+      QT qa = 0;
       int na = 0;
       for (uint64_t r = res; r; r &= r - 1) {
         const int m = __builtin_ctzll(r);
         used += t_wmib[m];
         if constexpr (NIBBLE) {
           if (mylast[m] == 0u) {
-            Q |= (uint64_t)m << (4 * nd);
+            Q |= (QT)m << (4 * nd);
             ++nd;
           } else {
-            qa |= (uint64_t)m << (4 * na);
+            qa |= (QT)m << (4 * na);
             ++na;
           }
         } else {
@@ -607,7 +615,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
         }
       }
       if constexpr (NIBBLE) {
-        if (na) Q |= qa << (4 * nd);  // nd + na <= 16, so nd < 16 here
+        if (na) Q |= qa << (4 * nd);  // nd + na <= QB / 4, so 4 * nd < QB here
         nq = nd + na;
       }
       peak = used;
@@ -701,17 +709,24 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
               // when it is found among the first nq entries (in the
               // still-needed part); it is taken out and re-enters as the most
               // recent
-              const uint64_t x = Q ^ (0x1111111111111111ull * (uint64_t)m);
-              const uint64_t z = (x - 0x1111111111111111ull) & ~x & 0x8888888888888888ull;
-              const int s4 = __builtin_ctzll(z | (1ull << 63)) & ~3;  // 4 * position
-              hit = z != 0ull && (s4 >> 2) < nq;
-              const uint64_t low = Q & ((1ull << s4) - 1ull);
-              const uint64_t high = (s4 >= 60) ? 0ull : ((Q >> (s4 + 4)) << s4);
+              const uint32_t m8 = (uint32_t)m * 0x11111111u;  // m in every nibble
+              QT mq = (QT)m8;
+              if constexpr (QB == 64) mq |= (QT)m8 << 32;
+              const QT x = Q ^ mq;
+              const QT z = (x - kOnes) & ~x & kHigh;  // lowest flag: first zero nibble
+              int s4;  // 4 * position
+              if constexpr (QB == 64)
+                s4 = __builtin_ctzll(z | (1ull << 63)) & ~3;
+              else
+                s4 = __builtin_ctz(z | (1u << 31)) & ~3;
+              hit = z != (QT)0 && (s4 >> 2) < nq;
+              const QT low = Q & (((QT)1 << s4) - (QT)1);
+              const QT high = (s4 >= kQBits - 4) ? (QT)0 : ((Q >> (s4 + 4)) << s4);
               Q = hit ? (low | high) : Q;
               nq -= hit ? 1 : 0;
               // the first two victims' weights, looked up ahead of need
-              w0 = t_wmib[(int)(Q & 15ull)];
-              w1 = t_wmib[(int)((Q >> 4) & 15ull)];
+              w0 = t_wmib[(int)(Q & (QT)15)];
+              w1 = t_wmib[(int)((Q >> 4) & (QT)15)];
             }
             const TT r = TO::tmax(X.rtv, X.arrv);
             // run time (summed over a fused chain, Eq. 4) and memory (max)
@@ -736,7 +751,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
             if constexpr (NIBBLE) {
               int t = 0;
               while (used + need > capd && nq > 0) {
-                const int v = (int)(Q & 15ull);
+                const int v = (int)(Q & (QT)15);
                 Q >>= 4;
                 --nq;
                 nd = nd > 0 ? nd - 1 : 0;
@@ -749,9 +764,9 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
               // m re-enters after the no-remaining-use part when this was its
               // last unit on the device, else at the end
               const bool last_use = (X.meta & kLast) != 0u;
-              const int pos = 4 * (last_use ? nd : nq);  // nq <= 15 here
-              const uint64_t lowm = (1ull << pos) - 1ull;
-              Q = (Q & lowm) | ((uint64_t)m << pos) | ((Q & ~lowm) << 4);
+              const int pos = 4 * (last_use ? nd : nq);  // nq < QB / 4 here
+              const QT lowm = ((QT)1 << pos) - (QT)1;
+              Q = (Q & lowm) | ((QT)m << pos) | ((Q & ~lowm) << 4);
               nd += last_use ? 1 : 0;
               ++nq;
             } else {
@@ -924,12 +939,12 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   }
 }
 
-template <typename TT, bool TAB_LDS, bool NIBBLE, bool WAVE_GLOBAL, bool SEARCH>
+template <typename TT, bool TAB_LDS, int QB, bool WAVE_GLOBAL, bool SEARCH>
 hipError_t launch_variant(const ScoreParams& sp, const int8_t* dev, const uint16_t* prio,
                           const uint8_t* flags, int64_t n_plans, wf_plan_score* scores,
                           const wf_plan_sched& s, int has, const SearchArgs& sa,
                           hipStream_t stream) {
-  auto k = score_plans<TT, TAB_LDS, NIBBLE, WAVE_GLOBAL, SEARCH>;
+  auto k = score_plans<TT, TAB_LDS, QB, WAVE_GLOBAL, SEARCH>;
   (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k),
                             hipFuncAttributeMaxDynamicSharedMemorySize, sp.lds_bytes);
   hipLaunchKernelGGL(k, dim3(sp.grid), dim3(64 * sp.waves), sp.lds_bytes, stream, sp, dev, prio,
@@ -937,17 +952,17 @@ hipError_t launch_variant(const ScoreParams& sp, const int8_t* dev, const uint16
   return hipGetLastError();
 }
 
-template <typename TT, bool NIBBLE, bool SEARCH>
+template <typename TT, int QB, bool SEARCH>
 hipError_t launch_place(const ScoreParams& sp, const int8_t* dev, const uint16_t* prio,
                         const uint8_t* flags, int64_t n_plans, wf_plan_score* scores,
                         const wf_plan_sched& s, int has, const SearchArgs& sa, hipStream_t stream) {
   if (sp.wave_global)
-    return launch_variant<TT, false, NIBBLE, true, SEARCH>(sp, dev, prio, flags, n_plans, scores,
+    return launch_variant<TT, false, QB, true, SEARCH>(sp, dev, prio, flags, n_plans, scores,
                                                            s, has, sa, stream);
   if (sp.tab_in_lds)
-    return launch_variant<TT, true, NIBBLE, false, SEARCH>(sp, dev, prio, flags, n_plans, scores,
+    return launch_variant<TT, true, QB, false, SEARCH>(sp, dev, prio, flags, n_plans, scores,
                                                            s, has, sa, stream);
-  return launch_variant<TT, false, NIBBLE, false, SEARCH>(sp, dev, prio, flags, n_plans, scores,
+  return launch_variant<TT, false, QB, false, SEARCH>(sp, dev, prio, flags, n_plans, scores,
                                                           s, has, sa, stream);
 }
 
@@ -955,9 +970,11 @@ template <typename TT, bool SEARCH>
 hipError_t launch_time(const ScoreParams& sp, const int8_t* dev, const uint16_t* prio,
                        const uint8_t* flags, int64_t n_plans, wf_plan_score* scores,
                        const wf_plan_sched& s, int has, const SearchArgs& sa, hipStream_t stream) {
-  if (sp.nibble)
-    return launch_place<TT, true, SEARCH>(sp, dev, prio, flags, n_plans, scores, s, has, sa, stream);
-  return launch_place<TT, false, SEARCH>(sp, dev, prio, flags, n_plans, scores, s, has, sa, stream);
+  if (sp.nibble == 32)
+    return launch_place<TT, 32, SEARCH>(sp, dev, prio, flags, n_plans, scores, s, has, sa, stream);
+  if (sp.nibble == 64)
+    return launch_place<TT, 64, SEARCH>(sp, dev, prio, flags, n_plans, scores, s, has, sa, stream);
+  return launch_place<TT, 0, SEARCH>(sp, dev, prio, flags, n_plans, scores, s, has, sa, stream);
 }
 
 template <typename TT>

@@ -193,6 +193,30 @@ def test_device_and_model_limits(ctx):
     assert_sched(gs, rs, ref["status"], "limits")
 
 
+@pytest.mark.parametrize("fit,width", [(8, "queue32"), (9, "queue64"), (16, "queue64")])
+def test_reclamation_queue_width(ctx, fit, width, capfd, monkeypatch):
+    """Sixteen equal-weight models, capacity for exactly `fit` of them: the
+    resident set reaches its bound, so the 32-bit queue (at most 8 models)
+    and the 64-bit one are both driven full, with reclamation on most
+    loads."""
+    rng = np.random.default_rng(500 + fit)
+    win = W.random_window(rng, n_wf=6, nodes=(6, 14), n_dev=2, n_models=16,
+                          cap_range=(fit * 1000 + 200, fit * 1000 + 200), w_range=(1000, 1000),
+                          mem_range=(0, 200), q_inel=0.0, same_model_bias=0.0)
+    plans = W.random_plans(win, 300, rng, prio_mode="perm")
+    monkeypatch.setenv("WF_PLAN_VERBOSE", "1")
+    got, gs, best = gpu_score(ctx, win, plans, schedule=True)
+    assert f"reclaim={width}" in capfd.readouterr().err
+    ref, rs = oracle.score(win, plans, schedule=True)
+    if fit < 16:
+        assert (ref["n_evicts"] > 0).mean() > 0.5
+    else:  # nothing is reclaimed, and some plan puts 9 or more models on one device
+        assert ref["n_evicts"].max() == 0 and ref["n_loads"].max() > 16
+    assert_scores(got, ref, f"fit {fit}")
+    assert_sched(gs, rs, ref["status"], f"fit {fit}")
+    assert best == best_plan(ref)
+
+
 def test_large_window_global_scratch(ctx):
     """A window whose per-plan finish times do not fit in LDS."""
     rng = np.random.default_rng(5)
