@@ -656,16 +656,32 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
       if (act) {
         const int j1 = (hi - 1) >> 6;
         const unsigned long long hmask = (hi & 63) ? ((1ull << (hi & 63)) - 1ull) : ~0ull;
-        // slots of this device in the level: the current word's remaining
-        // bits, and the next word already loaded
+        // a level of at most 64 slots: this device's slots of the level as
+        // one word, slot lo at bit 0
+        const int width = hi - lo;
+        const bool narrow = width <= 64;
         int j = lo >> 6;
-        unsigned long long bits = mymask[j] & (~0ull << (lo & 63));
-        if (j == j1) bits &= hmask;
-        unsigned long long wnext = 0ull;
-        if (j < j1) wnext = mymask[j + 1] & ((j + 1 == j1) ? hmask : ~0ull);
+        unsigned long long bits, wnext = 0ull;
+        if (narrow) {
+          const int sh = lo & 63;
+          bits = mymask[j] >> sh;
+          if (sh + width > 64) bits |= mymask[j + 1] << (64 - sh);  // then j + 1 <= j1
+          if (width < 64) bits &= (1ull << width) - 1ull;
+        } else {
+          // wider: the current word's remaining bits, and the next word
+          // already loaded
+          bits = mymask[j] & (~0ull << (lo & 63));
+          if (j < j1) wnext = mymask[j + 1] & ((j + 1 == j1) ? hmask : ~0ull);
+        }
         // the device's next slot in the level; -1 when there is none, -2 for
         // a trip with no unit (an exhausted word followed by an empty one)
-        auto next_slot = [&]() -> int {
+        auto next_narrow = [&]() -> int {
+          const int sl = lo + __builtin_ctzll(bits | (1ull << 63));
+          const bool have = bits != 0ull;
+          bits &= bits - 1ull;
+          return have ? sl : -1;
+        };
+        auto next_wide = [&]() -> int {
           const bool adv = bits == 0ull && j < j1;
           bits = adv ? wnext : bits;
           j += adv ? 1 : 0;
@@ -831,25 +847,32 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
             }
           }
         };
-        // two units per trip so that the prefetched unit needs no copy
-        UnitPre<TT> A, B;
-        {
-          const int sa = next_slot();
-          fetch(sa, entry(sa), A);
-        }
-        int sb = A.slot != -1 ? next_slot() : -1;
-        uint32_t mb_next = entry(sb);
-        while (A.slot != -1) {
-          fetch(sb, mb_next, B);
-          const int sc = sb != -1 ? next_slot() : -1;
-          const uint32_t mc = entry(sc);
-          process(A);
-          if (B.slot == -1) break;
-          fetch(sc, mc, A);
-          sb = sc != -1 ? next_slot() : -1;
-          mb_next = entry(sb);
-          process(B);
-        }
+        // two units per trip so that the prefetched unit needs no copy; one
+        // copy of the loop per kind of level
+        auto run = [&](auto&& next_slot) {
+          UnitPre<TT> A, B;
+          {
+            const int sa = next_slot();
+            fetch(sa, entry(sa), A);
+          }
+          int sb = A.slot != -1 ? next_slot() : -1;
+          uint32_t mb_next = entry(sb);
+          while (A.slot != -1) {
+            fetch(sb, mb_next, B);
+            const int sc = sb != -1 ? next_slot() : -1;
+            const uint32_t mc = entry(sc);
+            process(A);
+            if (B.slot == -1) break;
+            fetch(sc, mc, A);
+            sb = sc != -1 ? next_slot() : -1;
+            mb_next = entry(sb);
+            process(B);
+          }
+        };
+        if (narrow)
+          run(next_narrow);
+        else
+          run(next_wide);
       }
       wave_sync();
     }
