@@ -315,19 +315,6 @@ wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, Image& img, wfp::Sc
       edge[k] = (uint32_t)h.pred_idx[k] | ((uint32_t)v << 16);
   std::vector<int32_t> eoff((size_t)h.n_levels + 1);
   for (int32_t l = 0; l <= h.n_levels; ++l) eoff[l] = N > 0 ? h.pred_off[h.level_off[l]] : 0;
-  // activation memory: one value per activation when it is the same on every device
-  bool mem_uniform = true;
-  for (int32_t i = 0; i < N && mem_uniform; ++i)
-    for (int32_t d = 1; d < D; ++d)
-      if (h.mem[(size_t)i * D + d] != h.mem[(size_t)i * D]) {
-        mem_uniform = false;
-        break;
-      }
-  std::vector<int32_t> mem1;
-  if (mem_uniform) {
-    mem1.resize((size_t)std::max(N, 1), 0);
-    for (int32_t i = 0; i < N; ++i) mem1[i] = h.mem[(size_t)i * D];
-  }
   std::vector<unsigned char> arr((size_t)std::max(W, 1) * tsz, 0), fr((size_t)D * tsz, 0);
   for (int32_t f = 0; f < W; ++f) {
     const int64_t r = h.arrival[f] - origin;
@@ -343,19 +330,24 @@ wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, Image& img, wfp::Sc
   for (int32_t l = 0; l < h.n_levels; ++l)
     for (int32_t i = h.level_off[l]; i < h.level_off[l + 1]; ++i)
       alv[i] = (uint32_t)h.level_off[l] | ((uint32_t)(h.level_off[l + 1] - h.level_off[l]) << 16);
-  std::vector<unsigned char> aarr((size_t)std::max(N, 1) * tsz, 0);
+  // the walk's per-unit record: run time, memory and workflow arrival in one
+  // 16-byte load
+  std::vector<uint32_t> ud((size_t)std::max(N * D, 1) * 4, 0);
   for (int32_t i = 0; i < N; ++i)
-    std::memcpy(&aarr[(size_t)i * tsz], &arr[(size_t)h.act_wf[i] * tsz], tsz);
+    for (int32_t d = 0; d < D; ++d) {
+      uint32_t* r = &ud[((size_t)i * D + d) * 4];
+      r[0] = (uint32_t)h.lat[(size_t)i * D + d];
+      r[1] = (uint32_t)h.mem[(size_t)i * D + d];
+      std::memcpy(&r[2], &arr[(size_t)h.act_wf[i] * tsz], tsz);
+    }
   wfp::TabOffsets& t = sp.t;
   t.act = img.put(act.data(), act.size() * 4);
   t.alv = img.put(alv.data(), alv.size() * 4);
-  t.aarr = img.put(aarr.data(), aarr.size());
   t.cnext = img.put(cnext.data(), cnext.size() * 2);
   t.edge = img.put(edge.data(), edge.size() * 4);
   t.eoff = img.put(eoff.data(), eoff.size() * 4);
   t.loff = img.put(h.level_off.data(), h.level_off.size() * 4);
-  t.lat = img.put(h.lat.data(), h.lat.size() * 4);
-  t.mem = mem_uniform ? img.put(mem1.data(), mem1.size() * 4) : img.put(h.mem.data(), h.mem.size() * 4);
+  t.ud = img.put(ud.data(), ud.size() * 4);
   t.wmib = img.put(h.wmib.data(), h.wmib.size() * 4);
   std::vector<int32_t> lw((size_t)M * D * 2);
   for (int32_t m = 0; m < M; ++m)
@@ -396,8 +388,6 @@ wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, Image& img, wfp::Sc
   sp.S = S;
   sp.n_levels = h.n_levels;
   sp.nwa = std::max(1, (N + 63) / 64);
-  sp.mem_si = mem_uniform ? 1 : D;
-  sp.mem_sd = mem_uniform ? 0 : 1;
   sp.origin = origin;
   sp.min_arrival = h.min_arrival;
   sp.w_mk = h.w_mk;

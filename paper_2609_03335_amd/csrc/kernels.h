@@ -15,13 +15,13 @@ namespace wfp {
 struct TabOffsets {
   int act;     // u32 [N]    model | fusible << 6 | workflow << 16
   int alv;     // u32 [N]    first index of the activation's level | level width << 16
-  int aarr;    // time [N]   arrival of the activation's workflow (relative)
   int cnext;   // u16 [N]    successor v of u when Eq. 3 holds for (u, v), else 0xffff
   int edge;    // u32 [E]    predecessor | activation << 16, grouped by activation (CSR order)
   int eoff;    // i32 [L+1]  first edge of each level
   int loff;    // i32 [L+1]  first activation of each level
-  int lat;     // i32 [N*D]  run time, -1 ineligible
-  int mem;     // i32        activation memory, element (i, d) at i * mem_si + d * mem_sd
+  int ud;      // 16 B [N*D] per (activation, device): {run time (-1 ineligible), activation
+               //            memory, arrival of the activation's workflow (relative time,
+               //            low word / high word for fp64)}
   int lw;      // i32x2 [M*D] {load time, model weights}
   int wmib;    // i32 [M]    model weights
   int cap;     // i32 [D]    device capacity
@@ -55,7 +55,6 @@ struct WaveOffsets {
 
 struct ScoreParams {
   int32_t N, W, M, D, NB, S, n_levels, nwa;
-  int32_t mem_si, mem_sd;     // activation-memory table strides
   int64_t origin;             // absolute time of relative time 0
   int64_t min_arrival;        // first workflow arrival (absolute)
   float w_mk, w_p95;

@@ -41,6 +41,7 @@ template <>
 struct TimeOps<uint32_t> {
   using bits_t = uint32_t;
   __device__ static uint32_t load(const bits_t* p) { return *p; }
+  __device__ static uint32_t words(uint32_t lo, uint32_t) { return lo; }
   __device__ static bits_t bits(uint32_t t) { return t; }
   __device__ static uint32_t tmax(uint32_t a, uint32_t b) { return a > b ? a : b; }
   __device__ static uint32_t add(uint32_t a, uint32_t d) { return a + d; }
@@ -52,6 +53,9 @@ template <>
 struct TimeOps<double> {
   using bits_t = unsigned long long;
   __device__ static double load(const bits_t* p) { return __longlong_as_double((long long)*p); }
+  __device__ static double words(uint32_t lo, uint32_t hi) {
+    return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
+  }
   __device__ static bits_t bits(double t) { return (bits_t)__double_as_longlong(t); }
   __device__ static double tmax(double a, double b) { return fmax(a, b); }
   __device__ static double add(double a, uint32_t d) { return a + (double)d; }
@@ -155,10 +159,12 @@ __device__ __forceinline__ void mutate(uint64_t c, const SearchArgs& sa, int N,
 }
 
 // slot entry: activation | model << 16 | prefetch << 22 | has fused successor << 23 |
-// device << 24 | last unit of its model on the device << 30
+// device << 24 | last unit of its model on the device << 30 | finish written by
+// the general path (a fused chain, or schedule output requested) << 31
 constexpr uint32_t kPf = 1u << 22;
 constexpr uint32_t kChain = 1u << 23;
 constexpr uint32_t kLast = 1u << 30;
+constexpr uint32_t kSlow = 1u << 31;
 
 // What the device walk needs about one unit that does not depend on the
 // device's sequential state; it is loaded one unit ahead of its use.
@@ -211,13 +217,11 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   }
   const uint32_t* t_act = reinterpret_cast<const uint32_t*>(tb + sp.t.act);
   const uint32_t* t_alv = reinterpret_cast<const uint32_t*>(tb + sp.t.alv);
-  const TB* t_aarr = reinterpret_cast<const TB*>(tb + sp.t.aarr);
   const uint16_t* t_cnext = reinterpret_cast<const uint16_t*>(tb + sp.t.cnext);
   const uint32_t* t_edge = reinterpret_cast<const uint32_t*>(tb + sp.t.edge);
   const int32_t* t_eoff = reinterpret_cast<const int32_t*>(tb + sp.t.eoff);
   const int32_t* t_loff = reinterpret_cast<const int32_t*>(tb + sp.t.loff);
-  const int32_t* t_lat = reinterpret_cast<const int32_t*>(tb + sp.t.lat);
-  const int32_t* t_mem = reinterpret_cast<const int32_t*>(tb + sp.t.mem);
+  const uint4* t_ud = reinterpret_cast<const uint4*>(tb + sp.t.ud);
   const int2* t_lw = reinterpret_cast<const int2*>(tb + sp.t.lw);
   const int32_t* t_wmib = reinterpret_cast<const int32_t*>(tb + sp.t.wmib);
   const int32_t* t_cap = reinterpret_cast<const int32_t*>(tb + sp.t.cap);
@@ -226,7 +230,6 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   const TB* t_free0 = reinterpret_cast<const TB*>(tb + sp.t.free0);
   const uint32_t* t_sink = reinterpret_cast<const uint32_t*>(tb + sp.t.sink);
   const unsigned long long* t_elig = reinterpret_cast<const unsigned long long*>(tb + sp.t.elig);
-  const int mem_si = sp.mem_si;
 
   // ---- this wave's region (LDS, or HBM scratch for very large windows) ----
   unsigned char* wl;
@@ -246,12 +249,14 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   uint16_t* s_rprio = reinterpret_cast<uint16_t*>(wl + sp.wo.rows_prio);
 
   const int g_me = lane / D;
+  // every unit's finish goes through the general path when the schedule is
+  // written out
+  const uint32_t slow0 = has_sched ? kSlow : 0u;
   const int d_me = lane - g_me * D;
   const int64_t n_groups = (P + G - 1) / G;
   const int64_t stride = (int64_t)gridDim.x * sp.waves;
   // per-device table rows of this lane's device
-  const int32_t* lat_d = t_lat + d_me;
-  const int32_t* mem_d = t_mem + d_me * sp.mem_sd;
+  const uint4* ud_d = t_ud + d_me;
   const int2* lw_d = t_lw + d_me;
 
   // rows read four activations per lane with 4- and 8-byte loads
@@ -335,8 +340,8 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
       nbad |= (uint32_t)(head && okd && !inr);
       if (head && okd && inr) {
         const uint32_t m = a & 63u;
-        s_rec[g * N + pr] = (uint32_t)u | (m << 16) | ((fb & 2u) << 21) | (chain ? kChain : 0u) |
-                            ((uint32_t)d << 24);
+        s_rec[g * N + pr] = (uint32_t)u | (m << 16) | ((fb & 2u) << 21) |
+                            (chain ? kChain | kSlow : slow0) | ((uint32_t)d << 24);
         atomicOr(&s_mask[(g * D + d) * NWA + (pr >> 6)], 1ull << (pr & 63));
         atomicMax(&s_last[(g * D + d) * M + (int)m], (uint32_t)pr + 1u);
         ++nh;
@@ -488,7 +493,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
         const int c = t_cnext[u];
         const uint32_t chain = (c != 0xffff && fuse_bit(pfl, c)) ? kChain : 0u;
         rec[slot] = (uint32_t)u | ((a & 63u) << 16) | ((uint32_t)((fb >> 1) & 1) << 22) | chain |
-                    ((uint32_t)d << 24);
+                    (chain ? kSlow : slow0) | ((uint32_t)d << 24);
         atomicOr(&mk[d * NWA + (slot >> 6)], 1ull << (slot & 63));
         atomicMax(&lastp[d * M + (int)(a & 63u)], (uint32_t)slot + 1u);
       }
@@ -704,10 +709,11 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
           const uint32_t u = meta & 0xffffu, m = (meta >> 16) & 63u;
           p.meta = meta;
           p.slot = sl;
-          p.arrv = TO::load(t_aarr + u);
+          const uint4 r = ud_d[__umul24(u, (uint32_t)D)];
+          p.lat = (int32_t)r.x;
+          p.mem = (int32_t)r.y;
+          p.arrv = TO::words(r.z, r.w);
           p.rtv = TO::load(myfin + u);
-          p.lat = lat_d[__umul24(u, (uint32_t)D)];
-          p.mem = mem_d[__umul24(u, (uint32_t)mem_si)];
           p.lw = lw_d[__umul24(m, (uint32_t)D)];
         };
         // one unit of the device's sequence: reuse / reclaim / load, then
@@ -749,10 +755,10 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
             int32_t mxu = X.mem;
             inel |= (uint32_t)(X.lat < 0);
             uint32_t T = (uint32_t)X.lat;
-            if (sp.has_chains && (X.meta & kChain)) {
+            if (X.meta & kChain) {
               for (int v = t_cnext[u];;) {
-                const int32_t lv2 = lat_d[__umul24((uint32_t)v, (uint32_t)D)];
-                const int32_t mv = mem_d[__umul24((uint32_t)v, (uint32_t)mem_si)];
+                const int2 lm = *reinterpret_cast<const int2*>(ud_d + __umul24((uint32_t)v, (uint32_t)D));
+                const int32_t lv2 = lm.x, mv = lm.y;
                 inel |= (uint32_t)(lv2 < 0);
                 T += (uint32_t)lv2;
                 mxu = mv > mxu ? mv : mxu;
@@ -821,17 +827,13 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
             peak = (used + mxu) > peak ? (used + mxu) : peak;
             const TT f = TO::add(s, T);
             freet = f;
-            if (!sp.has_chains || !(X.meta & kChain)) {
+            if (!(X.meta & kSlow)) {
               myfin[u] = TO::bits(f);
-              if (has_sched) {
-                sched.start_us[pw * N + u] = sp.origin + TO::i64(s);
-                sched.finish_us[pw * N + u] = sp.origin + TO::i64(f);
-                sched.load_start_us[pw * N + u] = hit ? (int64_t)-1 : sp.origin + TO::i64(ls);
-              }
             } else {
               TT t = s;
               for (int v = u;;) {
-                const TT tv = TO::add(t, (uint32_t)lat_d[__umul24((uint32_t)v, (uint32_t)D)]);
+                const TT tv =
+                    TO::add(t, ud_d[__umul24((uint32_t)v, (uint32_t)D)].x);
                 myfin[v] = TO::bits(tv);
                 if (has_sched) {
                   sched.start_us[pw * N + v] = sp.origin + TO::i64(t);
