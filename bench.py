@@ -25,6 +25,10 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X published HBM3E bandwidth
+# 32-bit vector lane operations per second: 256 CUs x 64 lanes x 2.4 GHz (the
+# published 157.3 TFLOP/s fp32 vector peak counts an FMA as two operations and
+# packed fp32 as two more)
+VALU_PEAK_TLANE = 256 * 64 * 2.4e9 / 1e12
 CSRC = os.path.join(ROOT, "paper_2609_03335_amd", "csrc")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "score_plans_traffic.json")
 
@@ -47,10 +51,9 @@ def kernel_source_digest() -> str:
     return h.hexdigest()
 
 
-def measured_traffic(config: int, n_plans: int):
-    """HBM bytes per scoring launch from the committed counter runs
-    (FETCH_SIZE + WRITE_SIZE, each scaled by the copy-kernel factor), or None
-    when there is none for this workload or the kernel changed since."""
+def measured_counters(config: int, n_plans: int):
+    """The committed counter record of this workload, or None when there is
+    none or the kernel changed since it was taken."""
     try:
         with open(TRAFFIC_FILE) as f:
             rec = json.load(f)
@@ -59,7 +62,33 @@ def measured_traffic(config: int, n_plans: int):
     e = rec.get("configs", {}).get(str(config))
     if not e or e.get("n_plans") != n_plans or rec.get("kernel_source_sha256") != kernel_source_digest():
         return None
-    return int(e["fetch_bytes"] + e["write_bytes"])
+    return e
+
+
+def measured_traffic(config: int, n_plans: int):
+    """HBM bytes per scoring launch (FETCH_SIZE + WRITE_SIZE, each scaled by
+    the copy-kernel factor), or None."""
+    e = measured_counters(config, n_plans)
+    return int(e["fetch_bytes"] + e["write_bytes"]) if e else None
+
+
+def valu_roofline(config: int, n_plans: int, kernel_ms: float):
+    """Vector-instruction issue of the scoring launch against the chip's
+    32-bit lane-operation peak, from the committed SQ counters (wave
+    instructions per dispatch) and this run's kernel time; None without a
+    counter record for the current kernel."""
+    e = measured_counters(config, n_plans)
+    sq = (e or {}).get("sq_per_dispatch")
+    if not sq or "SQ_INSTS_VALU" not in sq:
+        return None
+    achieved = sq["SQ_INSTS_VALU"] * 64 / (kernel_ms * 1e-3) / 1e12
+    out = {"bound": "valu-issue", "achieved": round(achieved, 2), "peak": round(VALU_PEAK_TLANE, 2),
+           "unit": "Tlane-op/s", "frac": round(achieved / VALU_PEAK_TLANE, 4),
+           "valu_insts_per_plan": round(sq["SQ_INSTS_VALU"] / n_plans, 1)}
+    for k, name in (("SQ_INSTS_SALU", "salu_insts_per_plan"), ("SQ_INSTS_LDS", "lds_insts_per_plan")):
+        if k in sq:
+            out[name] = round(sq[k] / n_plans, 1)
+    return out
 
 
 def copy_probe(nbytes: int) -> None:
@@ -276,6 +305,8 @@ def main():
                    # batches below the 256 MB last-level cache can be read from it
                    "cache_resident": bool(bpp * P < 256 * 2 ** 20)},
         "roofline": roofline,
+        # the bound that holds: vector-instruction issue of the per-device walk
+        "valu_roofline": valu_roofline(args.config, P, kernel_ms),
         "cpu_baseline": cpu,
         "search": search,
     }
