@@ -29,6 +29,13 @@ SCORE_DTYPE = np.dtype([
 ])
 assert SCORE_DTYPE.itemsize == 32
 
+MAX_CLASSES = 4
+PHI_DTYPE = np.dtype([
+    ("c_ready_us", "<i8"), ("h_life_us", "<i8"), ("admitted", "<u2", (MAX_CLASSES,)),
+    ("timely_prefetch", "<u2"), ("pad", "<u2"), ("status", "<u4"),
+])
+assert PHI_DTYPE.itemsize == 32
+
 
 def build(force: bool = True, src: str = SRC_PATH, out: str = LIB_PATH) -> str:
     """Compile liboracle.so with gcc (plain C99, no FMA contraction)."""
@@ -70,6 +77,8 @@ def _load(path: Optional[str] = None):
             lib = ctypes.CDLL(path)
             lib.orc_score_plans.restype = ctypes.c_int
             lib.orc_score_plans.argtypes = [ctypes.c_void_p] * 4 + [ctypes.c_int64] + [ctypes.c_void_p] * 5
+            lib.orc_phi_keys.restype = ctypes.c_int
+            lib.orc_phi_keys.argtypes = [ctypes.c_void_p] * 5 + [ctypes.c_int64, ctypes.c_void_p]
             lib.orc_levels.restype = ctypes.c_int
             lib.orc_levels.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
             lib.orc_philox4x32_10.restype = None
@@ -123,6 +132,38 @@ def levels(win, lib_path: Optional[str] = None) -> np.ndarray:
     return out[:win.n_act]
 
 
+def _plan_rows(win, plans, begin, end):
+    N = win.n_act
+    P = end - begin
+    if N == 0:
+        # zero-width rows: give the C code a valid (unused) pointer
+        return np.zeros((P, 1), np.int8), np.zeros((P, 1), np.uint16), np.zeros((P, 1), np.uint8)
+    return (np.ascontiguousarray(plans.dev[begin:end], dtype=np.int8),
+            np.ascontiguousarray(plans.prio[begin:end], dtype=np.uint16),
+            np.ascontiguousarray(plans.flags[begin:end], dtype=np.uint8))
+
+
+def _run_split(run, P, threads):
+    """run(a, b) over [0, P), split into contiguous ranges on threads."""
+    if threads <= 1 or P < 2 * threads:
+        rc = run(0, P)
+        if rc:
+            raise OracleError(f"oracle rejected window (code {rc})")
+        return
+    bounds = np.linspace(0, P, threads + 1).astype(np.int64)
+    rcs = [0] * threads
+
+    def worker(t):
+        rcs[t] = run(int(bounds[t]), int(bounds[t + 1]))
+    ts = [threading.Thread(target=worker, args=(t,)) for t in range(threads)]
+    for t in ts:
+        t.start()
+    for t in ts:
+        t.join()
+    if any(rcs):
+        raise OracleError(f"oracle rejected window (codes {rcs})")
+
+
 def score(win, plans, begin: int = 0, end: Optional[int] = None, schedule: bool = False,
           threads: int = 1, lib_path: Optional[str] = None):
     """Score plans [begin, end) of ``plans``.  Returns a structured score
@@ -132,15 +173,12 @@ def score(win, plans, begin: int = 0, end: Optional[int] = None, schedule: bool 
     end = plans.n_plans if end is None else end
     P = end - begin
     N, D = win.n_act, win.n_dev
-    dev = np.ascontiguousarray(plans.dev[begin:end], dtype=np.int8)
-    prio = np.ascontiguousarray(plans.prio[begin:end], dtype=np.uint16)
-    flags = np.ascontiguousarray(plans.flags[begin:end], dtype=np.uint8)
+    dev, prio, flags = _plan_rows(win, plans, begin, end)
     scores = np.zeros(P, dtype=SCORE_DTYPE)
     sched = None
     if schedule:
         sched = (np.zeros((P, N), np.int64), np.zeros((P, N), np.int64),
                  np.zeros((P, N), np.int64), np.zeros((P, D), np.int32))
-    nb = (N + 3) // 4
 
     def run(a, b):
         if b <= a:
@@ -153,30 +191,43 @@ def score(win, plans, begin: int = 0, end: Optional[int] = None, schedule: bool 
         return lib.orc_score_plans(ctypes.byref(h.struct), ptr(dev), ptr(prio), ptr(flags),
                                    b - a, ptr(scores), ptr(s0), ptr(s1), ptr(s2), ptr(s3))
 
-    if N == 0 or nb == 0:
-        # zero-width rows: give the C code a valid (unused) pointer
-        dev = np.zeros((P, 1), np.int8)
-        prio = np.zeros((P, 1), np.uint16)
-        flags = np.zeros((P, 1), np.uint8)
-    if threads <= 1 or P < 2 * threads:
-        rc = run(0, P)
-        if rc:
-            raise OracleError(f"oracle rejected window (code {rc})")
-    else:
-        bounds = np.linspace(0, P, threads + 1).astype(np.int64)
-        rcs = [0] * threads
-        def worker(t):
-            rcs[t] = run(int(bounds[t]), int(bounds[t + 1]))
-        ts = [threading.Thread(target=worker, args=(t,)) for t in range(threads)]
-        for t in ts:
-            t.start()
-        for t in ts:
-            t.join()
-        if any(rcs):
-            raise OracleError(f"oracle rejected window (codes {rcs})")
+    _run_split(run, P, threads)
     if schedule:
         return scores, sched
     return scores
+
+
+def phi_keys(win, plans, begin: int = 0, end: Optional[int] = None, threads: int = 1,
+             lib_path: Optional[str] = None) -> np.ndarray:
+    """Ranking keys (Eq. 12) of plans [begin, end) as a PHI_DTYPE array; the
+    workflow classes come from ``win.wf_class`` (None: all class 0)."""
+    lib = _load(lib_path)
+    h = _WinHolder(win)
+    end = plans.n_plans if end is None else end
+    P = end - begin
+    dev, prio, flags = _plan_rows(win, plans, begin, end)
+    cls = getattr(win, "wf_class", None)
+    cls = None if cls is None else np.ascontiguousarray(cls, dtype=np.uint8)
+    keys = np.zeros(P, dtype=PHI_DTYPE)
+
+    def run(a, b):
+        if b <= a:
+            return 0
+        return lib.orc_phi_keys(ctypes.byref(h.struct), None if cls is None else cls.ctypes.data,
+                                dev.ctypes.data + a * dev.strides[0],
+                                prio.ctypes.data + a * prio.strides[0],
+                                flags.ctypes.data + a * flags.strides[0], b - a,
+                                keys.ctypes.data + a * keys.strides[0])
+
+    _run_split(run, P, threads)
+    return keys
+
+
+def phi_order_key(k) -> tuple:
+    """The lexicographic key of Eq. 12 for one PHI_DTYPE record:
+    (-A_1, ..., -A_K, C_F, -P_N, H_life)."""
+    return tuple(-int(a) for a in k["admitted"]) + (int(k["c_ready_us"]), -int(k["timely_prefetch"]),
+                                                    int(k["h_life_us"]))
 
 
 def philox4x32_10(ctr, key, lib_path: Optional[str] = None) -> np.ndarray:

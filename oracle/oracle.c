@@ -126,10 +126,15 @@ static int64_t max64(int64_t a, int64_t b) { return a > b ? a : b; }
 /* scoring                                                                 */
 /* ---------------------------------------------------------------------- */
 
-int orc_score_plans(const orc_window *w, const int8_t *dev, const uint16_t *prio,
-                    const uint8_t *flags, int64_t n_plans, orc_score *scores,
-                    int64_t *start_out, int64_t *finish_out, int64_t *load_out,
-                    int32_t *peak_out) {
+/* The propagation of every plan; scores, the schedule rows and the ranking
+ * keys (Eq. 12) are each written when their pointer is not NULL. */
+static int simulate(const orc_window *w, const uint8_t *wf_class, const int8_t *dev,
+                    const uint16_t *prio, const uint8_t *flags, int64_t n_plans,
+                    orc_score *scores, int64_t *start_out, int64_t *finish_out,
+                    int64_t *load_out, int32_t *peak_out, orc_phi *keys) {
+  if (wf_class)
+    for (int32_t f = 0; f < w->n_wf; ++f)
+      if (wf_class[f] >= ORC_MAX_CLASSES) return ORC_ERR_CLASS;
   orc_struct st;
   int rc = build_struct(w, &st);
   if (rc) return rc;
@@ -145,9 +150,11 @@ int orc_score_plans(const orc_window *w, const int8_t *dev, const uint16_t *prio
   int64_t *free_t = (int64_t *)malloc((size_t)D * 8), *used = (int64_t *)malloc((size_t)D * 8),
           *peak = (int64_t *)malloc((size_t)D * 8);
   uint64_t *res = (uint64_t *)malloc((size_t)D * 8);
+  uint64_t *reclaimed = (uint64_t *)malloc((size_t)D * 8);
   int64_t *remaining = (int64_t *)malloc((size_t)D * M * 8), *last = (int64_t *)malloc((size_t)D * M * 8);
   if (!fuse || !pf || !member || !unit_Mx || !order || !start || !finish ||
-      !load_start || !comp || !free_t || !used || !peak || !res || !remaining || !last) {
+      !load_start || !comp || !free_t || !used || !peak || !res || !reclaimed || !remaining ||
+      !last) {
     rc = ORC_ERR_NOMEM;
     goto done;
   }
@@ -190,7 +197,11 @@ int orc_score_plans(const orc_window *w, const int8_t *dev, const uint16_t *prio
     }
     if (sc.status & ORC_INELIGIBLE) {
       sc.status = ORC_INELIGIBLE;
-      scores[p] = sc;
+      if (scores) scores[p] = sc;
+      if (keys) {
+        memset(&keys[p], 0, sizeof keys[p]);
+        keys[p].status = ORC_INELIGIBLE;
+      }
       continue;
     }
 
@@ -211,8 +222,11 @@ int orc_score_plans(const orc_window *w, const int8_t *dev, const uint16_t *prio
         if ((res[d] >> m) & 1u) used[d] += w->model_mib[m];
       peak[d] = used[d];
       for (int32_t m = 0; m < M; ++m) last[d * M + m] = -1;
+      reclaimed[d] = 0;
     }
     int64_t n_loads = 0, n_evicts = 0;
+    /* ranking-key terms (Eq. 12) */
+    int64_t admitted[ORC_MAX_CLASSES] = {0, 0, 0, 0}, c_ready = 0, h_life = 0, timely = 0;
 
     /* ---- propagate units in resource order ---- */
     for (int32_t pos = 0; pos < n_units; ++pos) {
@@ -252,8 +266,15 @@ int orc_score_plans(const orc_window *w, const int8_t *dev, const uint16_t *prio
         res[d] &= ~(1ull << victim);
         used[d] -= w->model_mib[victim];
         n_evicts += 1;
+        reclaimed[d] |= 1ull << victim;
       }
-      if (used[d] + need > w->dev_cap_mib[d]) sc.status |= ORC_CAPACITY;
+      const int fits = !(used[d] + need > w->dev_cap_mib[d]);
+      if (!fits) sc.status |= ORC_CAPACITY;
+
+      /* ready work (F_t): no predecessor, and the workflow has arrived by
+       * the window time 0 */
+      const int ready = w->pred_off[h] == w->pred_off[h + 1] && w->wf_arrival_us[wf] <= 0;
+      const int64_t free_before = free_t[d];
 
       /* timeline (Eq. 7): a load waits for the device; it starts at the
        * unit's release, or at the workflow's arrival when prefetched */
@@ -266,6 +287,12 @@ int orc_score_plans(const orc_window *w, const int8_t *dev, const uint16_t *prio
         n_loads += 1;
         load_start[h] = ls;
         s = max64(r, le);
+        /* reload of a copy this plan reclaimed from the device */
+        if ((reclaimed[d] >> m) & 1u) h_life += le - ls;
+        /* a prefetch is timely when its load is done by the release */
+        if (!ready && pf[h] && le <= r) timely += 1;
+        /* the delay a load adds to ready work */
+        if (ready) h_life += s - max64(r, free_before);
       } else {
         load_start[h] = -1;
         s = max64(r, free_t[d]);
@@ -285,6 +312,10 @@ int orc_score_plans(const orc_window *w, const int8_t *dev, const uint16_t *prio
       }
       free_t[d] = s;
       last[d * M + m] = pos;
+      if (ready && fits) {
+        admitted[wf_class ? wf_class[wf] : 0] += 1;
+        c_ready = max64(c_ready, s);
+      }
     }
 
     /* ---- reductions (Sec. 4 metrics) ---- */
@@ -314,7 +345,18 @@ int orc_score_plans(const orc_window *w, const int8_t *dev, const uint16_t *prio
     sc.min_headroom_mib = (int32_t)headroom;
     sc.n_loads = (uint16_t)(n_loads > 65535 ? 65535 : n_loads);
     sc.n_evicts = (uint16_t)(n_evicts > 65535 ? 65535 : n_evicts);
-    scores[p] = sc;
+    if (scores) scores[p] = sc;
+    if (keys) {
+      orc_phi k;
+      memset(&k, 0, sizeof k);
+      k.c_ready_us = c_ready;
+      k.h_life_us = h_life;
+      for (int c = 0; c < ORC_MAX_CLASSES; ++c)
+        k.admitted[c] = (uint16_t)(admitted[c] > 65535 ? 65535 : admitted[c]);
+      k.timely_prefetch = (uint16_t)(timely > 65535 ? 65535 : timely);
+      k.status = sc.status;
+      keys[p] = k;
+    }
 
     if (start_out) memcpy(start_out + p * N, start, (size_t)N * 8);
     if (finish_out) memcpy(finish_out + p * N, finish, (size_t)N * 8);
@@ -327,9 +369,22 @@ int orc_score_plans(const orc_window *w, const int8_t *dev, const uint16_t *prio
 done:
   free(fuse); free(pf); free(member); free(unit_Mx); free(order);
   free(start); free(finish); free(load_start); free(comp); free(free_t); free(used);
-  free(peak); free(res); free(remaining); free(last);
+  free(peak); free(res); free(reclaimed); free(remaining); free(last);
   free_struct(&st);
   return rc;
+}
+
+int orc_score_plans(const orc_window *w, const int8_t *dev, const uint16_t *prio,
+                    const uint8_t *flags, int64_t n_plans, orc_score *scores,
+                    int64_t *start_out, int64_t *finish_out, int64_t *load_out,
+                    int32_t *peak_out) {
+  return simulate(w, NULL, dev, prio, flags, n_plans, scores, start_out, finish_out, load_out,
+                  peak_out, NULL);
+}
+
+int orc_phi_keys(const orc_window *w, const uint8_t *wf_class, const int8_t *dev,
+                 const uint16_t *prio, const uint8_t *flags, int64_t n_plans, orc_phi *keys) {
+  return simulate(w, wf_class, dev, prio, flags, n_plans, NULL, NULL, NULL, NULL, NULL, keys);
 }
 
 /* ---------------------------------------------------------------------- */

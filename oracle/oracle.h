@@ -69,7 +69,8 @@ enum {
   ORC_ERR_ORDER = 3,      /* activations not numbered in level order           */
   ORC_ERR_INDEX = 4,      /* workflow / model id out of range                  */
   ORC_ERR_EMPTY_WF = 5,   /* a workflow without activations                    */
-  ORC_ERR_NOMEM = 6
+  ORC_ERR_NOMEM = 6,
+  ORC_ERR_CLASS = 7       /* a workflow class outside 0 .. ORC_MAX_CLASSES-1    */
 };
 
 /*
@@ -83,6 +84,45 @@ int orc_score_plans(const orc_window *w, const int8_t *dev, const uint16_t *prio
                     const uint8_t *flags, int64_t n_plans, orc_score *scores,
                     int64_t *start_us, int64_t *finish_us, int64_t *load_start_us,
                     int32_t *peak_mib);
+
+/*
+ * The lexicographic ranking key of Eq. 12 (Sec. 3.5),
+ *   Phi = (-A_1, ..., -A_K, C_F, -P_N, H_life),
+ * under these readings (K <= ORC_MAX_CLASSES):
+ *   - a unit is ready (in F_t) when its head has no predecessor and its
+ *     workflow has arrived by the window time t = 0; every other unit is
+ *     near-ready;
+ *   - the priority class of a ready unit is its workflow's class
+ *     (wf_class[w] in 0 .. K-1, class 0 ranked first; NULL puts every
+ *     workflow in class 0);
+ *   - A_k counts the ready units of class k that are admitted: their memory
+ *     check (Eq. 11) holds at their turn;
+ *   - C_F is the latest completion (absolute us) of an admitted ready unit,
+ *     0 when there is none;
+ *   - P_N counts timely prefetches: near-ready units with the prefetch bit
+ *     whose model is loaded for them and whose load ends no later than
+ *     their release;
+ *   - H_life is the loading delay of ready work -- for a ready unit that
+ *     loads, its start minus the later of its release and the time its
+ *     device became free -- plus the reload cost of reclamation -- the load
+ *     time of every load of a model that an earlier unit of the plan had
+ *     reclaimed from that device.
+ * The simulation is the one of orc_score_plans.  For a plan with status
+ * ORC_INELIGIBLE every other field is 0.
+ */
+enum { ORC_MAX_CLASSES = 4 };
+
+typedef struct {
+  int64_t c_ready_us;                  /* C_F                                  */
+  int64_t h_life_us;                   /* H_life                               */
+  uint16_t admitted[ORC_MAX_CLASSES];  /* A_1 .. A_K (unused classes 0)        */
+  uint16_t timely_prefetch;            /* P_N                                  */
+  uint16_t pad;
+  uint32_t status;                     /* as orc_score.status                  */
+} orc_phi;
+
+int orc_phi_keys(const orc_window *w, const uint8_t *wf_class, const int8_t *dev,
+                 const uint16_t *prio, const uint8_t *flags, int64_t n_plans, orc_phi *keys);
 
 /* Topological level of every activation (0 for sources).  Returns an error
  * code as above. */

@@ -61,6 +61,9 @@ class Window:
     w_makespan: float = 1.0
     w_p95: float = 0.5
     name: str = "window"
+    # uint8[W] priority class of each workflow for the ranking key of Eq. 12
+    # (0 ranked first, below 4); None puts every workflow in class 0
+    wf_class: Optional[np.ndarray] = None
 
     def arrays(self):
         return {f.name: getattr(self, f.name) for f in dataclasses.fields(self)}
@@ -526,7 +529,7 @@ def random_plans(win: Window, n_plans: int, rng: np.random.Generator,
 
 
 def save_npz(path: str, win: Window, plans: Optional[PlanBatch] = None) -> None:
-    arrs = {f"w_{k}": np.asarray(v) for k, v in win.arrays().items()}
+    arrs = {f"w_{k}": np.asarray(v) for k, v in win.arrays().items() if v is not None}
     if plans is not None:
         arrs.update(p_dev=plans.dev, p_prio=plans.prio, p_flags=plans.flags)
     np.savez(path, **arrs)
@@ -536,6 +539,8 @@ def load_npz(path: str):
     z = np.load(path, allow_pickle=False)
     kw = {}
     for f in dataclasses.fields(Window):
+        if f"w_{f.name}" not in z:  # an optional field that was None
+            continue
         v = z[f"w_{f.name}"]
         kw[f.name] = v.item() if v.ndim == 0 else v
     kw["name"] = str(kw["name"])

@@ -15,6 +15,7 @@ import test_oracle_independent as t_ind
 import test_oracle_paper_examples as t_pap
 import test_oracle_properties as t_prop
 import test_oracle_search as t_search
+import test_oracle_phi as t_phi
 
 # (name, original fragment, planted mistake)
 MUTANTS = [
@@ -47,8 +48,8 @@ MUTANTS = [
      "finish[v] = s + w->lat_us[(int64_t)v * D + (pdev[v] >= 0 && pdev[v] < D ? pdev[v] : d)];"),
     ("makespan from time zero", "sc.makespan_us = max_fin - min_arr;", "sc.makespan_us = max_fin;"),
     ("load table transposed", "w->load_us[m * D + d]", "w->load_us[(d * M + m) % (M * D)]"),
-    ("capacity check inclusive", "if (used[d] + need > w->dev_cap_mib[d]) sc.status |= ORC_CAPACITY;",
-     "if (used[d] + need >= w->dev_cap_mib[d]) sc.status |= ORC_CAPACITY;"),
+    ("capacity check inclusive", "const int fits = !(used[d] + need > w->dev_cap_mib[d]);",
+     "const int fits = !(used[d] + need >= w->dev_cap_mib[d]);"),
     ("eviction ignores activation memory",
      "int64_t need = (miss ? (int64_t)w->model_mib[m] : 0) + Mx;",
      "int64_t need = (miss ? (int64_t)w->model_mib[m] : 0);"),
@@ -65,6 +66,21 @@ MUTANTS = [
     ("load waits for release when prefetched", "int64_t ls = max64(pf[h] ? w->wf_arrival_us[wf] : r, free_t[d]);",
      "int64_t ls = max64(r, free_t[d]);"),
     ("pred finish ignored", "r = max64(r, finish[w->pred_idx[k]]);", "r = max64(r, start[w->pred_idx[k]]);"),
+    # ranking key (Eq. 12)
+    ("ready ignores arrival", "w->pred_off[h] == w->pred_off[h + 1] && w->wf_arrival_us[wf] <= 0",
+     "w->pred_off[h] == w->pred_off[h + 1]"),
+    ("admitted ignores capacity", "if (ready && fits) {", "if (ready) {"),
+    ("class ignored", "admitted[wf_class ? wf_class[wf] : 0] += 1;", "admitted[0] += 1;"),
+    ("ready completion at start", "c_ready = max64(c_ready, s);", "c_ready = max64(c_ready, start[h]);"),
+    ("timely prefetch strict", "if (!ready && pf[h] && le <= r) timely += 1;",
+     "if (!ready && pf[h] && le < r) timely += 1;"),
+    ("timely prefetch counts ready work", "if (!ready && pf[h] && le <= r) timely += 1;",
+     "if (pf[h] && le <= r) timely += 1;"),
+    ("every load a reload", "if ((reclaimed[d] >> m) & 1u) h_life += le - ls;", "h_life += le - ls;"),
+    ("loading delay from release", "if (ready) h_life += s - max64(r, free_before);",
+     "if (ready) h_life += s - r;"),
+    ("loading delay of all work", "if (ready) h_life += s - max64(r, free_before);",
+     "h_life += s - max64(r, free_before);"),
 ]
 
 
@@ -89,6 +105,9 @@ def _pin_checks():
     checks += [lambda k=k: t_search.test_philox_known_answers(*k) for k in t_search.KAT]
     checks += [t_search.test_one_mutation_decoded_site_by_site, t_search.test_ranges_are_independent_of_splitting]
     checks += [lambda n=n: t_search.test_candidate_structure(n) for n in (1, 4)]
+    checks += [lambda n=n: t_phi.test_worked_examples(n) for n in ("phi_reload", "phi_prefetch", "phi_ready_prefetch")]
+    checks += [lambda s=s: t_phi.test_phi_from_schedule(s) for s in range(6)]
+    checks += [lambda s=s: t_phi.test_phi_invariants(s) for s in range(3)]
     return checks
 
 
