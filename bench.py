@@ -45,7 +45,7 @@ def kernel_source_digest() -> str:
     on."""
     import hashlib
     h = hashlib.sha256()
-    for name in ("score.hip", "kernels.h", "host.hip"):
+    for name in ("score_kernel.h", "score.hip", "kernels.h", "host.hip"):
         with open(os.path.join(CSRC, name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()
@@ -129,6 +129,8 @@ def main():
                     help="plans checked against the oracle before timing (0 = none)")
     ap.add_argument("--search-mut", type=int, default=2,
                     help="mutations per generated candidate in the search leg (-1 = skip it)")
+    ap.add_argument("--no-keys", action="store_true",
+                    help="skip the ranking-key leg (Eq. 12 keys and their argmin)")
     ap.add_argument("--copy-probe", type=int, default=None, metavar="BYTES",
                     help="only run a plain copy kernel of BYTES bytes (counter calibration)")
     args = ap.parse_args()
@@ -270,6 +272,44 @@ def main():
                   "note": "candidates generated around one incumbent plan inside the scoring "
                           "kernel (no plan rows in HBM), same window and count"}
 
+    # the ranking keys of Eq. 12 for the same plans, and their lexicographic
+    # argmin
+    keys_leg = None
+    if not args.no_keys:
+        keys = scores  # 32 bytes per plan as well
+        if args.check:
+            import oracle
+            n_chk = min(P, args.check)
+            idx = np.unique(np.linspace(0, P - 1, n_chk).astype(np.int64))
+            ctx.wf_plan_score_keys(dev, prio, flags, P, keys, stream)
+            torch.cuda.synchronize()
+            got = pkg.keys_to_numpy(keys, P)[idx]
+            ref = oracle.phi_keys(win, plans.take(idx), threads=min(16, os.cpu_count() or 1))
+            if got.tobytes() != ref.tobytes():
+                print("[bench] ranking keys differ from the oracle", file=sys.stderr)
+                sys.exit(1)
+        out_k = torch.empty(1, dtype=torch.int64, device="cuda:0")
+        for _ in range(args.warmup):
+            ctx.wf_plan_score_keys(dev, prio, flags, P, keys, stream)
+            ctx.wf_plan_argmin_keys(keys, P, out_k, stream)
+        torch.cuda.synchronize()
+        kev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
+                torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+        for a, b, c in kev:
+            a.record(stream)
+            ctx.wf_plan_score_keys(dev, prio, flags, P, keys, stream)
+            b.record(stream)
+            ctx.wf_plan_argmin_keys(keys, P, out_k, stream)
+            c.record(stream)
+        torch.cuda.synchronize()
+        k_ms = float(np.mean([a.elapsed_time(b) for a, b, c in kev]))
+        ka_ms = float(np.mean([b.elapsed_time(c) for a, b, c in kev]))
+        keys_leg = {"value": round(P / ((k_ms + ka_ms) * 1e-3), 1), "unit": "plans/s",
+                    "kernel_ms": round(k_ms, 4), "argmin_ms": round(ka_ms, 4),
+                    "note": "ranking keys of Eq. 12 (admitted ready work, its latest completion, "
+                            "timely prefetches, lifecycle overhead) for the same plans, then "
+                            "their lexicographic argmin"}
+
     cpu = None
     if not args.no_cpu_baseline:
         import oracle
@@ -309,6 +349,7 @@ def main():
         "valu_roofline": valu_roofline(args.config, P, kernel_ms),
         "cpu_baseline": cpu,
         "search": search,
+        "keys": keys_leg,
     }
     print(json.dumps(line))
     ctx.close()

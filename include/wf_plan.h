@@ -83,6 +83,7 @@ typedef enum {
 #define WF_MAX_TIME_US (1LL << 52) /* arrivals and initial free times; every
                                       time then stays below 2^53 (exact in fp64) */
 #define WF_MAX_MUT 64              /* mutations per generated candidate        */
+#define WF_MAX_CLASSES 4           /* priority classes of the ranking key      */
 
 /* Plan status bits; a plan is feasible iff status == 0. */
 enum { WF_ST_INELIGIBLE = 1u, WF_ST_CAPACITY = 2u };
@@ -113,6 +114,9 @@ typedef struct {
   const uint64_t *init_resident;  /* [D] resident-model bitmask; must fit the capacity */
   const int64_t *dev_free0_us;    /* [D] busy-until time, or NULL for all 0    */
   float w_makespan, w_p95;        /* objective weights, finite and >= 0        */
+  const uint8_t *wf_class;        /* [W] priority class of each workflow for the ranking
+                                     key (Eq. 12), 0..WF_MAX_CLASSES-1, class 0 ranked
+                                     first; NULL = every workflow in class 0    */
 } wf_window_desc;
 
 /* Per-plan score, 32 bytes.  For a WF_ST_INELIGIBLE plan every other field
@@ -215,6 +219,59 @@ wf_status wf_plan_search_rows(wf_plan_ctx *ctx, const int8_t *dev, const uint16_
                               const uint8_t *flags, uint64_t seed, int32_t n_mut, int64_t first,
                               int64_t n_candidates, int8_t *out_dev, uint16_t *out_prio,
                               uint8_t *out_flags, void *hip_stream);
+
+/*
+ * Ranking keys.  The paper's scheduler ranks plans lexicographically by
+ * Eq. 12 (Sec. 3.5),  Phi = (-A_1, ..., -A_K, C_F, -P_N, H_life):  ready-work
+ * coverage per priority class first, then the latest completion of that
+ * work, then timely prefetching and lifecycle overhead.  This library
+ * computes the terms on the same simulation as wf_plan_score_batch, under
+ * these readings:
+ *   - a unit is ready (in F_t) when its head has no predecessor and its
+ *     workflow has arrived by the window time 0; every other unit is
+ *     near-ready (N_t);
+ *   - the class of a ready unit is its workflow's wf_class (K =
+ *     WF_MAX_CLASSES; classes the window does not use count 0);
+ *   - A_k = the ready units of class k that are admitted: the memory check
+ *     of step 3 holds at their turn;
+ *   - C_F = the latest finish (absolute us) of an admitted ready unit, 0 if
+ *     there is none;
+ *   - P_N = the near-ready units with the prefetch bit whose model is loaded
+ *     for them and whose load ends no later than their release;
+ *   - H_life = for each ready unit that loads, its start minus the later of
+ *     its release and the time its device became free (the delay the load
+ *     adds), plus the load time of every load of a model that an earlier
+ *     unit of the plan had reclaimed from that device (reload cost).
+ * For a WF_ST_INELIGIBLE plan every field other than status is 0.
+ */
+typedef struct {
+  int64_t c_ready_us;                  /* C_F                                   */
+  int64_t h_life_us;                   /* H_life                                */
+  uint16_t admitted[WF_MAX_CLASSES];   /* A_1 .. A_K                            */
+  uint16_t timely_prefetch;            /* P_N, saturates at 65535               */
+  uint16_t pad;                        /* 0                                     */
+  uint32_t status;                     /* as wf_plan_score.status               */
+} wf_plan_key;                         /* 32 bytes                              */
+
+/* Ranking keys of plans 0..n_plans-1 (rows as for wf_plan_score_batch) into
+ * keys [P] (device memory).  Asynchronous on hip_stream. */
+wf_status wf_plan_score_keys(wf_plan_ctx *ctx, const int8_t *dev, const uint16_t *prio,
+                             const uint8_t *flags, int64_t n_plans, wf_plan_key *keys,
+                             void *hip_stream);
+
+/* Ranking keys of generated candidates first .. first+n_candidates-1 around
+ * an incumbent (arguments and limits as for wf_plan_search_batch). */
+wf_status wf_plan_search_keys(wf_plan_ctx *ctx, const int8_t *dev, const uint16_t *prio,
+                              const uint8_t *flags, uint64_t seed, int32_t n_mut, int64_t first,
+                              int64_t n_candidates, wf_plan_key *keys, void *hip_stream);
+
+/* Among keys with status 0, the index of the lexicographically smallest Phi
+ * (lowest index on ties), or -1 if none is feasible, written to the device
+ * int64 *out_index.  0 <= n_plans <= 2^62; n_plans = 0 writes -1.  Uses a
+ * small work area owned by the context: calls on one context must not run
+ * concurrently on different streams.  Asynchronous on hip_stream. */
+wf_status wf_plan_argmin_keys(wf_plan_ctx *ctx, const wf_plan_key *keys, int64_t n_plans,
+                              int64_t *out_index, void *hip_stream);
 
 /* Time arithmetic the kernels use for the uploaded window: 32 when every
  * time of every plan provably stays below 2^32 us after the window origin

@@ -6,13 +6,14 @@ the HIP stream.
 """
 from __future__ import annotations
 
-from ._lib import (EXPORTS, SCORE_DTYPE, WF_EHIP, WF_EINVAL, WF_ENOMEM, WF_ENOWINDOW, WF_OK,
+from ._lib import (EXPORTS, KEY_DTYPE, SCORE_DTYPE, WF_EHIP, WF_EINVAL, WF_ENOMEM, WF_ENOWINDOW, WF_OK,
                    WF_EUNSUPPORTED, WF_ST_CAPACITY, WF_ST_INELIGIBLE, Context, WFError, load,
                    wf_plan_validate_window, wf_plan_version)
 
 __all__ = [
-    "Context", "WFError", "SCORE_DTYPE", "EXPORTS", "load", "wf_plan_validate_window",
+    "Context", "WFError", "SCORE_DTYPE", "KEY_DTYPE", "EXPORTS", "load", "wf_plan_validate_window",
     "wf_plan_version", "device_plans", "score_batch", "argmin", "scores_to_numpy",
+    "keys_to_numpy",
     "WF_OK", "WF_EINVAL", "WF_ENOWINDOW", "WF_ENOMEM", "WF_EHIP", "WF_EUNSUPPORTED",
     "WF_ST_INELIGIBLE", "WF_ST_CAPACITY",
 ]
@@ -61,3 +62,8 @@ def argmin(ctx: Context, scores, n_plans: int, stream=None):
 
 def scores_to_numpy(scores, n_plans: int):
     return scores[:n_plans].cpu().numpy().reshape(-1).view(SCORE_DTYPE)[:n_plans]
+
+
+def keys_to_numpy(keys, n_plans: int):
+    """Ranking keys (uint8 [P, 32] device buffer) as a KEY_DTYPE array."""
+    return keys[:n_plans].cpu().numpy().reshape(-1).view(KEY_DTYPE)[:n_plans]

@@ -21,6 +21,7 @@ STATUS_NAMES = {0: "WF_OK", 1: "WF_EINVAL", 2: "WF_ENOWINDOW", 3: "WF_ENOMEM", 4
 WF_ST_INELIGIBLE = 1
 WF_ST_CAPACITY = 2
 WF_MAX_ACT, WF_MAX_MODELS, WF_MAX_DEV, WF_MAX_MUT = 65535, 64, 64, 64
+WF_MAX_CLASSES = 4
 
 SCORE_DTYPE = np.dtype([
     ("makespan_us", "<i8"), ("p95_us", "<i8"), ("objective", "<f4"),
@@ -29,10 +30,18 @@ SCORE_DTYPE = np.dtype([
 ])
 assert SCORE_DTYPE.itemsize == 32
 
+# wf_plan_key: the ranking key of Eq. 12
+KEY_DTYPE = np.dtype([
+    ("c_ready_us", "<i8"), ("h_life_us", "<i8"), ("admitted", "<u2", (WF_MAX_CLASSES,)),
+    ("timely_prefetch", "<u2"), ("pad", "<u2"), ("status", "<u4"),
+])
+assert KEY_DTYPE.itemsize == 32
+
 # every symbol declared in include/wf_plan.h
 EXPORTS = ("wf_plan_ctx_create", "wf_plan_ctx_destroy", "wf_plan_last_error",
            "wf_plan_validate_window", "wf_plan_upload_window", "wf_plan_score_batch",
            "wf_plan_argmin", "wf_plan_search_batch", "wf_plan_search_rows",
+           "wf_plan_score_keys", "wf_plan_search_keys", "wf_plan_argmin_keys",
            "wf_plan_time_bits", "wf_plan_version")
 
 
@@ -54,6 +63,7 @@ class wf_window_desc(ctypes.Structure):
         ("model_mib", ctypes.c_void_p), ("load_us", ctypes.c_void_p),
         ("init_resident", ctypes.c_void_p), ("dev_free0_us", ctypes.c_void_p),
         ("w_makespan", ctypes.c_float), ("w_p95", ctypes.c_float),
+        ("wf_class", ctypes.c_void_p),
     ]
 
 
@@ -95,6 +105,12 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.wf_plan_search_batch.restype = i32
     lib.wf_plan_search_rows.argtypes = [vp, vp, vp, vp, u64, ctypes.c_int32, i64, i64, vp, vp, vp, vp]
     lib.wf_plan_search_rows.restype = i32
+    lib.wf_plan_score_keys.argtypes = [vp, vp, vp, vp, i64, vp, vp]
+    lib.wf_plan_score_keys.restype = ctypes.c_int
+    lib.wf_plan_search_keys.argtypes = [vp, vp, vp, vp, u64, ctypes.c_int32, i64, i64, vp, vp]
+    lib.wf_plan_search_keys.restype = ctypes.c_int
+    lib.wf_plan_argmin_keys.argtypes = [vp, vp, i64, vp, vp]
+    lib.wf_plan_argmin_keys.restype = ctypes.c_int
     lib.wf_plan_time_bits.argtypes = [vp]
     lib.wf_plan_time_bits.restype = i32
     lib.wf_plan_version.argtypes = []
@@ -120,6 +136,8 @@ class _Desc:
             init_resident=c(win.init_resident, np.uint64))
         free0 = getattr(win, "dev_free0_us", None)
         self.keep["dev_free0_us"] = None if free0 is None else c(free0, np.int64)
+        cls = getattr(win, "wf_class", None)
+        self.keep["wf_class"] = None if cls is None else c(cls, np.uint8)
         d = wf_window_desc()
         d.n_act, d.n_wf, d.n_models, d.n_dev = win.n_act, win.n_wf, win.n_models, win.n_dev
         for k, v in self.keep.items():
@@ -203,6 +221,22 @@ class Context:
             self.handle, _ptr(dev), _ptr(prio), _ptr(flags), int(seed) & ((1 << 64) - 1),
             int(n_mut), int(first), int(n_candidates), _ptr(out_dev), _ptr(out_prio),
             _ptr(out_flags), _stream(stream)))
+
+    def wf_plan_score_keys(self, dev, prio, flags, n_plans: int, keys, stream=None) -> None:
+        """Ranking keys (Eq. 12) of plans 0..n_plans-1 into keys (32 B each)."""
+        self._check(self.lib.wf_plan_score_keys(self.handle, _ptr(dev), _ptr(prio), _ptr(flags),
+                                                int(n_plans), _ptr(keys), _stream(stream)))
+
+    def wf_plan_search_keys(self, dev, prio, flags, seed: int, n_mut: int, first: int,
+                            n_candidates: int, keys, stream=None) -> None:
+        """Ranking keys of candidates generated around the incumbent rows."""
+        self._check(self.lib.wf_plan_search_keys(
+            self.handle, _ptr(dev), _ptr(prio), _ptr(flags), int(seed) & ((1 << 64) - 1),
+            int(n_mut), int(first), int(n_candidates), _ptr(keys), _stream(stream)))
+
+    def wf_plan_argmin_keys(self, keys, n_plans: int, out_index, stream=None) -> None:
+        self._check(self.lib.wf_plan_argmin_keys(self.handle, _ptr(keys), int(n_plans),
+                                                 _ptr(out_index), _stream(stream)))
 
     def wf_plan_time_bits(self) -> int:
         return int(self.lib.wf_plan_time_bits(self.handle))

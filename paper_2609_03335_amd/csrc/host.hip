@@ -29,6 +29,7 @@ struct HostWindow {
   std::vector<uint8_t> fusible;
   std::vector<int64_t> arrival, free0;
   std::vector<uint64_t> init_res;
+  std::vector<uint8_t> wf_class;  // [W] priority class of the ranking key
   float w_mk = 1.f, w_p95 = 0.f;
 };
 
@@ -123,9 +124,16 @@ wf_status validate(const wf_window_desc* w, std::string* err, HostWindow* out) {
       return fail(err, WF_EINVAL, "initial residency of device %lld (%lld MiB) exceeds its capacity %d MiB",
                   (long long)d, (long long)used, w->dev_cap_mib[d]);
   }
+  if (w->wf_class)
+    for (int64_t f = 0; f < W; ++f)
+      if (w->wf_class[f] >= WF_MAX_CLASSES)
+        return fail(err, WF_EINVAL, "wf_class[%lld] = %d outside [0, %d)", (long long)f,
+                    (int)w->wf_class[f], WF_MAX_CLASSES);
   if (!out) return WF_OK;
 
   HostWindow& h = *out;
+  h.wf_class.assign((size_t)W, 0);
+  if (w->wf_class) h.wf_class.assign(w->wf_class, w->wf_class + W);
   h.N = (int32_t)N;
   h.W = (int32_t)W;
   h.M = (int32_t)M;
@@ -201,6 +209,7 @@ struct wf_plan_ctx {
   bool has_window = false;
   HostWindow host;
   DeviceWindow dw;
+  void* key_work = nullptr;  // partial results of the ranking-key argmin
 };
 
 namespace {
@@ -305,7 +314,10 @@ wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, Image& img, wfp::Sc
   std::vector<uint32_t> act((size_t)std::max(N, 1), 0);
   std::vector<uint16_t> cnext((size_t)std::max(N, 1), 0xffff);
   for (int32_t i = 0; i < N; ++i) {
-    act[i] = (uint32_t)h.act_model[i] | ((uint32_t)h.fusible[i] << 6) | ((uint32_t)h.act_wf[i] << 16);
+    // ready work of the ranking key: no predecessor, arrived by time 0
+    const bool ready = h.pred_off[i] == h.pred_off[i + 1] && h.arrival[h.act_wf[i]] <= 0;
+    act[i] = (uint32_t)h.act_model[i] | ((uint32_t)h.fusible[i] << 6) | ((uint32_t)ready << 7) |
+             ((uint32_t)h.wf_class[h.act_wf[i]] << 8) | ((uint32_t)h.act_wf[i] << 16);
     cnext[i] = h.chain_next[i] >= 0 ? (uint16_t)h.chain_next[i] : (uint16_t)0xffff;
   }
   const int32_t E = N > 0 ? h.pred_off[N] : 0;
@@ -534,6 +546,14 @@ wf_status wf_plan_ctx_create(int hip_device, wf_plan_ctx** out) {
     return WF_EHIP;
   }
   if (ctx->lds_per_cu <= 0) ctx->lds_per_cu = ctx->lds_per_block;
+  (void)hipSetDevice(hip_device);
+  e = hipMalloc(&ctx->key_work, (size_t)wfp::kArgminKeyBlocks * wfp::ARGMIN_KEY_WORK_BYTES);
+  (void)hipSetDevice(prev);
+  if (e != hipSuccess) {
+    g_thread_err = std::string("work area allocation failed: ") + hipGetErrorString(e);
+    delete ctx;
+    return WF_ENOMEM;
+  }
   *out = ctx;
   return WF_OK;
 }
@@ -544,6 +564,7 @@ void wf_plan_ctx_destroy(wf_plan_ctx* ctx) {
   (void)hipGetDevice(&prev);
   (void)hipSetDevice(ctx->device);
   free_device_window(ctx->dw);
+  if (ctx->key_work) (void)hipFree(ctx->key_work);
   (void)hipSetDevice(prev);
   delete ctx;
 }
@@ -729,6 +750,79 @@ wf_status wf_plan_argmin(wf_plan_ctx* ctx, const wf_plan_score* scores, int64_t 
   e = wfp::launch_argmin(scores, n_plans, out_index, ctx->n_cu * 4, static_cast<hipStream_t>(hip_stream));
   (void)hipSetDevice(prev);
   if (e != hipSuccess) return hip_fail(ctx, e, "launching the argmin kernels");
+  return WF_OK;
+}
+
+wf_status wf_plan_score_keys(wf_plan_ctx* ctx, const int8_t* dev, const uint16_t* prio,
+                             const uint8_t* flags, int64_t n_plans, wf_plan_key* keys,
+                             void* hip_stream) {
+  if (!ctx) {
+    g_thread_err = "ctx is NULL";
+    return WF_EINVAL;
+  }
+  if (!ctx->has_window) return fail(&ctx->err, WF_ENOWINDOW, "no window uploaded");
+  if (n_plans < 0) return fail(&ctx->err, WF_EINVAL, "n_plans is negative");
+  if (n_plans == 0) return WF_OK;
+  if (!keys) return fail(&ctx->err, WF_EINVAL, "keys is NULL");
+  if (ctx->host.N > 0 && (!dev || !prio || !flags))
+    return fail(&ctx->err, WF_EINVAL, "a plan array (dev, prio, flags) is NULL");
+  int prev = 0;
+  (void)hipGetDevice(&prev);
+  hipError_t e = hipSetDevice(ctx->device);
+  if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
+  wfp::ScoreParams sp = ctx->dw.sp;
+  const int64_t groups = (n_plans + sp.G - 1) / sp.G;
+  const int64_t wgs = (groups + sp.waves - 1) / sp.waves;
+  if (wgs < sp.grid) sp.grid = (int)wgs;
+  e = wfp::launch_score_keys(sp, dev, prio, flags, n_plans, keys, nullptr,
+                             static_cast<hipStream_t>(hip_stream));
+  (void)hipSetDevice(prev);
+  if (e != hipSuccess) return hip_fail(ctx, e, "launching the ranking-key kernel");
+  return WF_OK;
+}
+
+wf_status wf_plan_search_keys(wf_plan_ctx* ctx, const int8_t* dev, const uint16_t* prio,
+                              const uint8_t* flags, uint64_t seed, int32_t n_mut, int64_t first,
+                              int64_t n_candidates, wf_plan_key* keys, void* hip_stream) {
+  wf_status st = search_args(ctx, dev, prio, flags, n_mut, first, n_candidates);
+  if (st != WF_OK) return st;
+  if (n_candidates == 0) return WF_OK;
+  if (!keys) return fail(&ctx->err, WF_EINVAL, "keys is NULL");
+  int prev = 0;
+  (void)hipGetDevice(&prev);
+  hipError_t e = hipSetDevice(ctx->device);
+  if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
+  wfp::ScoreParams sp = ctx->dw.sp_search;
+  const int64_t groups = (n_candidates + sp.G - 1) / sp.G;
+  const int64_t wgs = (groups + sp.waves - 1) / sp.waves;
+  if (wgs < sp.grid) sp.grid = (int)wgs;
+  const wfp::SearchArgs sa{seed, n_mut, first};
+  e = wfp::launch_score_keys(sp, dev, prio, flags, n_candidates, keys, &sa,
+                             static_cast<hipStream_t>(hip_stream));
+  (void)hipSetDevice(prev);
+  if (e != hipSuccess) return hip_fail(ctx, e, "launching the ranking-key kernel");
+  return WF_OK;
+}
+
+wf_status wf_plan_argmin_keys(wf_plan_ctx* ctx, const wf_plan_key* keys, int64_t n_plans,
+                              int64_t* out_index, void* hip_stream) {
+  if (!ctx) {
+    g_thread_err = "ctx is NULL";
+    return WF_EINVAL;
+  }
+  if (!ctx->has_window) return fail(&ctx->err, WF_ENOWINDOW, "no window uploaded");
+  if (n_plans < 0 || n_plans > (int64_t(1) << 62))
+    return fail(&ctx->err, WF_EINVAL, "n_plans must be in [0, 2^62]");
+  if (!out_index) return fail(&ctx->err, WF_EINVAL, "out_index is NULL");
+  if (n_plans > 0 && !keys) return fail(&ctx->err, WF_EINVAL, "keys is NULL");
+  int prev = 0;
+  (void)hipGetDevice(&prev);
+  hipError_t e = hipSetDevice(ctx->device);
+  if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
+  e = wfp::launch_argmin_keys(keys, n_plans, out_index, ctx->key_work,
+                              static_cast<hipStream_t>(hip_stream));
+  (void)hipSetDevice(prev);
+  if (e != hipSuccess) return hip_fail(ctx, e, "launching the ranking-key argmin kernels");
   return WF_OK;
 }
 

@@ -85,6 +85,12 @@ struct PlanAcc {
   uint32_t claimed;               // distinct slots they occupy
   uint32_t bad;                   // a head priority outside its level's index range
   uint32_t pad;
+  // ranking-key terms (Eq. 12)
+  unsigned long long ph_adm;      // admitted ready units per class, 16 bits each
+  unsigned long long ph_cf;       // latest admitted ready finish (time bits)
+  unsigned long long ph_h;        // lifecycle overhead (time units)
+  uint32_t ph_pn;                 // timely prefetches
+  uint32_t ph_pad;
 };
 
 // Candidates generated around an incumbent plan instead of read from HBM.
@@ -102,6 +108,11 @@ hipError_t launch_score(const ScoreParams& sp, const int8_t* dev, const uint16_t
                         const wf_plan_sched* sched, const SearchArgs* search,
                         hipStream_t stream);
 
+// Ranking keys (Eq. 12) of plans or generated candidates.
+hipError_t launch_score_keys(const ScoreParams& sp, const int8_t* dev, const uint16_t* prio,
+                             const uint8_t* flags, int64_t n_plans, wf_plan_key* keys,
+                             const SearchArgs* search, hipStream_t stream);
+
 // Rows of candidates first .. first+P-1 around the incumbent rows.
 hipError_t launch_search_rows(const ScoreParams& sp, const int8_t* dev, const uint16_t* prio,
                               const uint8_t* flags, const SearchArgs& search, int64_t n,
@@ -110,5 +121,12 @@ hipError_t launch_search_rows(const ScoreParams& sp, const int8_t* dev, const ui
 
 hipError_t launch_argmin(const wf_plan_score* scores, int64_t n_plans, int64_t* out_index,
                          int grid, hipStream_t stream);
+
+// Lexicographic argmin of ranking keys: `blocks` partial results in `work`
+// (ARGMIN_KEY_WORK_BYTES per block), then one block for the final result.
+constexpr int kArgminKeyBlocks = 512;
+constexpr size_t ARGMIN_KEY_WORK_BYTES = 64;
+hipError_t launch_argmin_keys(const wf_plan_key* keys, int64_t n_plans, int64_t* out_index,
+                              void* work, hipStream_t stream);
 
 }  // namespace wfp

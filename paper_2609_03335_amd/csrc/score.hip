@@ -1,1016 +1,10 @@
-// Batched scoring of candidate physical execution plans on gfx950.
-//
-// A persistent grid of waves loops over groups of G plans; lane (g, d) =
-// (lane / D, lane % D) owns device d of plan g.  The window's table image is
-// read from LDS (one copy per workgroup) or through the cache.  Per group:
-//   1. flag rows are staged into the wave's LDS region; device and priority
-//      rows are read four activations per lane (or built in LDS for
-//      candidates generated around an incumbent);
-//   2. resource order (Eq. 10): each unit head's slot is its priority when
-//      every level's head priorities are distinct values in the level's index
-//      range (checked by counting heads against distinct slots), else its rank
-//      by (priority, index) within the level; slot entries, per-device slot
-//      masks and each (device, model)'s last slot are recorded, and the last
-//      unit of each model on each device is marked;
-//   3. per topological level: releases r = max(arrival, latest predecessor
-//      finish) (Eq. 2) by LDS atomic max over the level's incoming edges,
-//      accumulated in the finish array itself; then each device lane walks its
-//      units of the level in slot order -- reuse / reclaim / load (Eq. 5,
-//      Eq. 11) and the max-plus timeline of Eq. 7 -- with everything that
-//      does not depend on the device's sequential state loaded a unit ahead;
-//   4. makespan, nearest-rank p95, objective, headroom and counts.
-// Residency, reclamation and memory depend only on each device's unit
-// sequence, never on times, so device lanes are independent within a level;
-// every predecessor sits at a lower level, so releases are final when a
-// level starts.
-//
-// Times are relative to the window origin (earliest arrival or free time):
-// uint32 when the host has proven no time of any plan can reach 2^32, else
-// fp64 (every time is an integer below 2^53, so fp64 max/add are exact).
-#include <type_traits>
-
-#include "kernels.h"
+// Batched scoring of candidate physical execution plans on gfx950: the
+// scalar objective of every plan, and the rows of generated candidates.  The
+// kernel itself is in score_kernel.h.
+#include "score_kernel.h"
 
 namespace wfp {
 namespace {
-
-template <typename TT>
-struct TimeOps;
-
-template <>
-struct TimeOps<uint32_t> {
-  using bits_t = uint32_t;
-  __device__ static uint32_t load(const bits_t* p) { return *p; }
-  __device__ static uint32_t words(uint32_t lo, uint32_t) { return lo; }
-  __device__ static bits_t bits(uint32_t t) { return t; }
-  __device__ static uint32_t tmax(uint32_t a, uint32_t b) { return a > b ? a : b; }
-  __device__ static uint32_t add(uint32_t a, uint32_t d) { return a + d; }
-  __device__ static uint32_t sub(uint32_t a, uint32_t b) { return a - b; }
-  __device__ static int64_t i64(uint32_t t) { return (int64_t)t; }
-};
-
-template <>
-struct TimeOps<double> {
-  using bits_t = unsigned long long;
-  __device__ static double load(const bits_t* p) { return __longlong_as_double((long long)*p); }
-  __device__ static double words(uint32_t lo, uint32_t hi) {
-    return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
-  }
-  __device__ static bits_t bits(double t) { return (bits_t)__double_as_longlong(t); }
-  __device__ static double tmax(double a, double b) { return fmax(a, b); }
-  __device__ static double add(double a, uint32_t d) { return a + (double)d; }
-  __device__ static double sub(double a, double b) { return a - b; }
-  __device__ static int64_t i64(double t) { return (int64_t)t; }
-};
-
-__device__ __forceinline__ void wave_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-}
-
-// Zero nbytes at a 16-byte aligned address: 16-byte stores, then the tail.
-__device__ __forceinline__ void zero_bytes(unsigned char* dst, int nbytes, int lane) {
-  uint4* d = reinterpret_cast<uint4*>(dst);
-  const int n16 = nbytes >> 4;
-  for (int i = lane; i < n16; i += 64) d[i] = make_uint4(0u, 0u, 0u, 0u);
-  for (int i = (n16 << 4) + lane; i < nbytes; i += 64) dst[i] = 0;
-}
-
-// Copy nbytes with 4-byte accesses when source, destination and size allow.
-__device__ __forceinline__ void copy_row(unsigned char* dst, const unsigned char* src, int nbytes,
-                                         int lane) {
-  if (((reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(dst) | (uintptr_t)nbytes) &
-       3) == 0) {
-    const uint32_t* s = reinterpret_cast<const uint32_t*>(src);
-    uint32_t* d = reinterpret_cast<uint32_t*>(dst);
-    for (int i = lane; i < (nbytes >> 2); i += 64) d[i] = s[i];
-  } else {
-    for (int i = lane; i < nbytes; i += 64) dst[i] = src[i];
-  }
-}
-
-// Copy nbytes from HBM with the widest aligned accesses.
-__device__ __forceinline__ void stage(unsigned char* dst, const unsigned char* src, int nbytes,
-                                      int lane) {
-  const uintptr_t a = reinterpret_cast<uintptr_t>(src);
-  if (((a | (uintptr_t)nbytes) & 15) == 0) {
-    const uint4* s = reinterpret_cast<const uint4*>(src);
-    uint4* d = reinterpret_cast<uint4*>(dst);
-    for (int i = lane; i < (nbytes >> 4); i += 64) d[i] = s[i];
-  } else if (((a | (uintptr_t)nbytes) & 3) == 0) {
-    const uint32_t* s = reinterpret_cast<const uint32_t*>(src);
-    uint32_t* d = reinterpret_cast<uint32_t*>(dst);
-    for (int i = lane; i < (nbytes >> 2); i += 64) d[i] = s[i];
-  } else {
-    for (int i = lane; i < nbytes; i += 64) dst[i] = src[i];
-  }
-}
-
-__device__ __forceinline__ int fuse_bit(const uint8_t* fl, int v) {
-  return (fl[v >> 2] >> ((v & 3) << 1)) & 1;
-}
-
-// Philox4x32-10 (Salmon, Moraes, Dror and Shaw, SC'11): ten rounds of the
-// Philox-4x32 bijection of the counter x, the key bumped by the Weyl
-// constants after every round.
-__device__ __forceinline__ void philox4x32_10(uint32_t x[4], uint32_t k0, uint32_t k1) {
-#pragma unroll
-  for (int round = 0; round < 10; ++round) {
-    const uint32_t a = x[0], c = x[2];
-    x[0] = __umulhi(0xCD9E8D57u, c) ^ x[1] ^ k0;
-    x[1] = 0xCD9E8D57u * c;
-    x[2] = __umulhi(0xD2511F53u, a) ^ x[3] ^ k1;
-    x[3] = 0xD2511F53u * a;
-    k0 += 0x9E3779B9u;
-    k1 += 0xBB67AE85u;
-  }
-}
-
-// Turns rows (dev, prio, flags) holding the incumbent into candidate c: the
-// n_mut mutations drawn from Philox4x32-10 with counter (c, t) and the
-// seed as key -- another eligible device for activation i, a swap of two
-// priorities inside i's level, or a toggled fuse / prefetch bit of i.
-__device__ __forceinline__ void mutate(uint64_t c, const SearchArgs& sa, int N,
-                                       const unsigned long long* elig, const uint32_t* alv,
-                                       int8_t* rd, uint16_t* rp, uint8_t* rf) {
-  if (N <= 0) return;
-  for (int t = 0; t < sa.n_mut; ++t) {
-    uint32_t x[4] = {(uint32_t)c, (uint32_t)(c >> 32), (uint32_t)t, 0u};
-    philox4x32_10(x, (uint32_t)sa.seed, (uint32_t)(sa.seed >> 32));
-    const int i = (int)__umulhi(x[1], (uint32_t)N);
-    const uint32_t kind = x[0] >> 30;
-    if (kind == 0u) {
-      unsigned long long e = elig[i];
-      const uint32_t n = (uint32_t)__popcll(e);
-      if (n) {
-        for (uint32_t k = __umulhi(x[2], n); k; --k) e &= e - 1ull;
-        rd[i] = (int8_t)__builtin_ctzll(e);
-      }
-    } else if (kind == 1u) {
-      const uint32_t lvw = alv[i];
-      const int j = (int)(lvw & 0xffffu) + (int)__umulhi(x[2], lvw >> 16);
-      const uint16_t pi = rp[i];
-      rp[i] = rp[j];
-      rp[j] = pi;
-    } else {
-      rf[i >> 2] ^= (uint8_t)(1u << (((i & 3) << 1) + (kind == 3u ? 1 : 0)));
-    }
-  }
-}
-
-// slot entry: activation | model << 16 | prefetch << 22 | has fused successor << 23 |
-// device << 24 | last unit of its model on the device << 30 | finish written by
-// the general path (a fused chain, or schedule output requested) << 31
-constexpr uint32_t kPf = 1u << 22;
-constexpr uint32_t kChain = 1u << 23;
-constexpr uint32_t kLast = 1u << 30;
-constexpr uint32_t kSlow = 1u << 31;
-
-// What the device walk needs about one unit that does not depend on the
-// device's sequential state; it is loaded one unit ahead of its use.
-template <typename TT>
-struct UnitPre {
-  uint32_t meta;  // slot entry
-  int slot;       // resource-order slot, -1 past the device's last unit
-  TT arrv;        // workflow arrival
-  TT rtv;         // latest predecessor finish (0 for a source)
-  int32_t lat;    // head run time on the device (-1: ineligible)
-  int32_t mem;    // head activation memory on the device
-  int2 lw;        // model load time on the device, model weights
-};
-
-// SEARCH: plans are candidates generated around the incumbent rows dev_all,
-// prio_all, flags_all ([N] each) rather than [P][N] rows read from HBM.
-template <typename TT, bool TAB_LDS, int QB, bool WAVE_GLOBAL, bool SEARCH>
-__global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
-                                                   const int8_t* __restrict__ dev_all,
-                                                   const uint16_t* __restrict__ prio_all,
-                                                   const uint8_t* __restrict__ flags_all, int64_t P,
-                                                   wf_plan_score* __restrict__ scores,
-                                                   wf_plan_sched sched, int has_sched,
-                                                   SearchArgs sa) {
-  using TO = TimeOps<TT>;
-  using TB = typename TO::bits_t;
-  // reclamation queue: QB bits of 4-bit model ids (QB = 0: no queue, the
-  // resident set is scanned instead)
-  constexpr bool NIBBLE = QB != 0;
-  using QT = std::conditional_t<QB == 32, uint32_t, uint64_t>;
-  constexpr QT kOnes = (QT)0x1111111111111111ull, kHigh = (QT)0x8888888888888888ull;
-  constexpr int kQBits = (int)sizeof(QT) * 8;
-  extern __shared__ __align__(16) unsigned char lds[];
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  const int N = sp.N, W = sp.W, M = sp.M, D = sp.D, NB = sp.NB, G = sp.G, NWA = sp.nwa;
-
-  // ---- window tables ----
-  const unsigned char* tb;
-  int wave_base;
-  if constexpr (TAB_LDS) {
-    const uint4* src = reinterpret_cast<const uint4*>(sp.tab);
-    uint4* dst = reinterpret_cast<uint4*>(lds);
-    for (int i = tid; i < (sp.t.bytes >> 4); i += blockDim.x) dst[i] = src[i];
-    __syncthreads();
-    tb = lds;
-    wave_base = sp.t.bytes;
-  } else {
-    tb = sp.tab;
-    wave_base = 0;
-  }
-  const uint32_t* t_act = reinterpret_cast<const uint32_t*>(tb + sp.t.act);
-  const uint32_t* t_alv = reinterpret_cast<const uint32_t*>(tb + sp.t.alv);
-  const uint16_t* t_cnext = reinterpret_cast<const uint16_t*>(tb + sp.t.cnext);
-  const uint32_t* t_edge = reinterpret_cast<const uint32_t*>(tb + sp.t.edge);
-  const int32_t* t_eoff = reinterpret_cast<const int32_t*>(tb + sp.t.eoff);
-  const int32_t* t_loff = reinterpret_cast<const int32_t*>(tb + sp.t.loff);
-  const uint4* t_ud = reinterpret_cast<const uint4*>(tb + sp.t.ud);
-  const int2* t_lw = reinterpret_cast<const int2*>(tb + sp.t.lw);
-  const int32_t* t_wmib = reinterpret_cast<const int32_t*>(tb + sp.t.wmib);
-  const int32_t* t_cap = reinterpret_cast<const int32_t*>(tb + sp.t.cap);
-  const TB* t_arr = reinterpret_cast<const TB*>(tb + sp.t.arr);
-  const unsigned long long* t_res0 = reinterpret_cast<const unsigned long long*>(tb + sp.t.res0);
-  const TB* t_free0 = reinterpret_cast<const TB*>(tb + sp.t.free0);
-  const uint32_t* t_sink = reinterpret_cast<const uint32_t*>(tb + sp.t.sink);
-  const unsigned long long* t_elig = reinterpret_cast<const unsigned long long*>(tb + sp.t.elig);
-
-  // ---- this wave's region (LDS, or HBM scratch for very large windows) ----
-  unsigned char* wl;
-  if constexpr (WAVE_GLOBAL)
-    wl = sp.scratch + ((int64_t)blockIdx.x * sp.waves + wid) * (int64_t)sp.wo.bytes;
-  else
-    wl = lds + wave_base + wid * sp.wo.bytes;
-  uint8_t* s_fl = reinterpret_cast<uint8_t*>(wl + sp.wo.flags);
-  uint32_t* s_rec = reinterpret_cast<uint32_t*>(wl + sp.wo.rec);
-  unsigned long long* s_mask = reinterpret_cast<unsigned long long*>(wl + sp.wo.mask);
-  uint32_t* s_last = reinterpret_cast<uint32_t*>(wl + sp.wo.last);
-  TB* s_fin = reinterpret_cast<TB*>(wl + sp.wo.fin);
-  PlanAcc* s_acc = reinterpret_cast<PlanAcc*>(wl + sp.wo.acc);
-  uint16_t* s_stamp = reinterpret_cast<uint16_t*>(wl + sp.wo.stamp);
-  TB* s_wfm = reinterpret_cast<TB*>(wl + sp.wo.wfm);
-  int8_t* s_rdev = reinterpret_cast<int8_t*>(wl + sp.wo.rows);         // generated candidates
-  uint16_t* s_rprio = reinterpret_cast<uint16_t*>(wl + sp.wo.rows_prio);
-
-  const int g_me = lane / D;
-  // every unit's finish goes through the general path when the schedule is
-  // written out
-  const uint32_t slow0 = has_sched ? kSlow : 0u;
-  const int d_me = lane - g_me * D;
-  const int64_t n_groups = (P + G - 1) / G;
-  const int64_t stride = (int64_t)gridDim.x * sp.waves;
-  // per-device table rows of this lane's device
-  const uint4* ud_d = t_ud + d_me;
-  const int2* lw_d = t_lw + d_me;
-
-  // rows read four activations per lane with 4- and 8-byte loads
-  const bool vec = (N & 3) == 0 && (SEARCH || ((reinterpret_cast<uintptr_t>(dev_all) & 3) == 0 &&
-                                               (reinterpret_cast<uintptr_t>(prio_all) & 7) == 0));
-  // one 256-activation chunk and at most eight plans per group: the next
-  // group's device and priority rows are loaded while this group is walked
-  constexpr int kB = 8;
-  const bool pre = !SEARCH && vec && N <= 256 && G <= kB;
-  uint32_t dvp[kB];
-  uint2 pvp[kB];
-  auto load_rows = [&](int64_t grp_, uint32_t* dv, uint2* pv) {
-    const int64_t q0 = grp_ * G;
-    const int gq = (int)((P - q0) < G ? (P - q0) : G);
-    const int uc = 4 * lane < N ? 4 * lane : 0;
-#pragma unroll
-    for (int k = 0; k < kB; ++k) {
-      const int g = k < gq ? k : gq - 1;
-      dv[k] = *reinterpret_cast<const uint32_t*>(dev_all + (q0 + g) * N + uc);
-      pv[k] = *reinterpret_cast<const uint2*>(prio_all + (q0 + g) * N + uc);
-    }
-  };
-  {
-    const int64_t g_first = (int64_t)blockIdx.x * sp.waves + wid;
-    if (pre && g_first < n_groups) load_rows(g_first, dvp, pvp);
-  }
-
-  for (int64_t grp = (int64_t)blockIdx.x * sp.waves + wid; grp < n_groups; grp += stride) {
-    const int64_t p0 = grp * G;
-    const int gc = (int)((P - p0) < G ? (P - p0) : G);
-
-    // ---- stage the group's flag rows, clear the ordering state ----
-    if constexpr (SEARCH) {
-      // every plan of the group starts as the incumbent, then takes its
-      // candidate's mutations (one lane per plan, in order)
-      for (int g = 0; g < gc; ++g) {
-        copy_row(reinterpret_cast<unsigned char*>(s_rdev + g * N),
-                 reinterpret_cast<const unsigned char*>(dev_all), N, lane);
-        copy_row(reinterpret_cast<unsigned char*>(s_rprio + g * N),
-                 reinterpret_cast<const unsigned char*>(prio_all), 2 * N, lane);
-        copy_row(s_fl + g * NB, flags_all, NB, lane);
-      }
-      wave_sync();
-      if (lane < gc)
-        mutate((uint64_t)(sa.first + p0 + lane), sa, N, t_elig, t_alv, s_rdev + lane * N,
-               s_rprio + lane * N, s_fl + lane * NB);
-    } else {
-      stage(s_fl, flags_all + p0 * NB, gc * NB, lane);
-    }
-    zero_bytes(reinterpret_cast<unsigned char*>(s_last), G * D * M * 4, lane);
-    zero_bytes(reinterpret_cast<unsigned char*>(s_mask), G * D * NWA * 8, lane);
-    if (lane < G) {
-      PlanAcc a0;
-      a0.status = 0u;
-      a0.headroom = 0x7fffffff;
-      a0.loads = 0u;
-      a0.evicts = 0u;
-      a0.max_finish = 0ull;
-      a0.p95 = 0;
-      a0.heads = 0u;
-      a0.claimed = 0u;
-      a0.bad = 0u;
-      a0.pad = 0u;
-      s_acc[lane] = a0;
-    }
-    wave_sync();
-
-    // ---- resource order (Eq. 10), first try: a unit head's slot is its
-    // priority, valid when each level's head priorities are distinct values
-    // in the level's index range (checked below by counting) ----
-    // one activation u of plan g with device d and priority pr; cbyte is the
-    // flag byte of u's chain successor
-    auto order_fast = [&](int g, int u, int d, int pr, uint32_t a, uint32_t lvw, uint32_t c,
-                          uint32_t fb, uint32_t cbyte, uint32_t& nh, uint32_t& nbad,
-                          uint32_t& ninel) {
-      const bool head = !((fb & 1u) && (a & 64u));  // not a fused chain member
-      const bool okd = (unsigned)d < (unsigned)D;
-      const bool inr = (unsigned)(pr - (int)(lvw & 0xffffu)) < (lvw >> 16);
-      const bool chain = c != 0xffffu && ((cbyte >> ((c & 3u) << 1)) & 1u);
-      ninel |= (uint32_t)(head && !okd);
-      nbad |= (uint32_t)(head && okd && !inr);
-      if (head && okd && inr) {
-        const uint32_t m = a & 63u;
-        s_rec[g * N + pr] = (uint32_t)u | (m << 16) | ((fb & 2u) << 21) |
-                            (chain ? kChain | kSlow : slow0) | ((uint32_t)d << 24);
-        atomicOr(&s_mask[(g * D + d) * NWA + (pr >> 6)], 1ull << (pr & 63));
-        atomicMax(&s_last[(g * D + d) * M + (int)m], (uint32_t)pr + 1u);
-        ++nh;
-      }
-    };
-    // per-plan totals from uniform control flow, at most 4 heads per lane:
-    // wave ballots instead of 64 conflicting LDS atomics
-    auto order_flush4 = [&](int g, uint32_t nh, uint32_t nbad, uint32_t ninel) {
-      const uint32_t tot = (uint32_t)__popcll(__ballot(nh & 1u)) +
-                           2u * (uint32_t)__popcll(__ballot(nh & 2u)) +
-                           4u * (uint32_t)__popcll(__ballot(nh & 4u));
-      const bool any_bad = __ballot(nbad != 0u) != 0ull;
-      const bool any_inel = __ballot(ninel != 0u) != 0ull;
-      if (lane == 0) {
-        if (any_inel) s_acc[g].status |= (uint32_t)WF_ST_INELIGIBLE;
-        if (any_bad) s_acc[g].bad = 1u;
-        s_acc[g].heads += tot;
-      }
-    };
-    // device and priority rows of plan g: HBM, or the generated candidate
-    auto row_dev = [&](int g) -> const int8_t* {
-      if constexpr (SEARCH) return s_rdev + g * N;
-      else return dev_all + (p0 + g) * N;
-    };
-    auto row_prio = [&](int g) -> const uint16_t* {
-      if constexpr (SEARCH) return s_rprio + g * N;
-      else return prio_all + (p0 + g) * N;
-    };
-    // the rows of plans g0 .. g0 + kB - 1 at activations uc .. uc + 3
-    auto rows4 = [&](int g0, int uc, uint32_t* dv, uint2* pv) {
-#pragma unroll
-      for (int k = 0; k < kB; ++k) {
-        const int g = (g0 + k < gc) ? g0 + k : gc - 1;
-        if (pre) {
-          dv[k] = dvp[k];
-          pv[k] = pvp[k];
-        } else {
-          dv[k] = *reinterpret_cast<const uint32_t*>(row_dev(g) + uc);
-          pv[k] = *reinterpret_cast<const uint2*>(row_prio(g) + uc);
-        }
-      }
-    };
-    if (vec) {
-      // four consecutive activations per lane: one 4-byte device load, one
-      // 8-byte priority load and one flag byte per plan; every load of a
-      // batch of plans is issued before any of it is used
-      for (int base = 0; base < N; base += 256) {
-        const int u0 = base + 4 * lane;
-        const bool live = u0 < N;
-        const int uc = live ? u0 : 0;
-        const uint4 act4 = *reinterpret_cast<const uint4*>(t_act + uc);
-        const uint4 alv4 = *reinterpret_cast<const uint4*>(t_alv + uc);
-        const uint2 cn4 = *reinterpret_cast<const uint2*>(t_cnext + uc);
-        const uint32_t cn[4] = {cn4.x & 0xffffu, cn4.x >> 16, cn4.y & 0xffffu, cn4.y >> 16};
-        for (int g0 = 0; g0 < gc; g0 += kB) {
-          uint32_t dv[kB], fl[kB], cb[kB][4];
-          uint2 pv[kB];
-          rows4(g0, uc, dv, pv);
-#pragma unroll
-          for (int k = 0; k < kB; ++k) {
-            const int g = (g0 + k < gc) ? g0 + k : gc - 1;
-            fl[k] = s_fl[g * NB + (uc >> 2)];
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-              cb[k][j] = sp.has_chains ? s_fl[g * NB + ((cn[j] != 0xffffu ? cn[j] : (uint32_t)uc) >> 2)]
-                                       : 0u;
-          }
-#pragma unroll
-          for (int k = 0; k < kB; ++k) {
-            const int g = g0 + k;
-            if (g >= gc) break;
-            uint32_t nh = 0, nbad = 0, ninel = 0;
-            if (live) {
-              order_fast(g, uc, (int)(int8_t)(dv[k] & 0xffu), (int)(pv[k].x & 0xffffu), act4.x,
-                         alv4.x, cn[0], fl[k], cb[k][0], nh, nbad, ninel);
-              order_fast(g, uc + 1, (int)(int8_t)((dv[k] >> 8) & 0xffu), (int)(pv[k].x >> 16),
-                         act4.y, alv4.y, cn[1], fl[k] >> 2, cb[k][1], nh, nbad, ninel);
-              order_fast(g, uc + 2, (int)(int8_t)((dv[k] >> 16) & 0xffu), (int)(pv[k].y & 0xffffu),
-                         act4.z, alv4.z, cn[2], fl[k] >> 4, cb[k][2], nh, nbad, ninel);
-              order_fast(g, uc + 3, (int)(int8_t)(dv[k] >> 24), (int)(pv[k].y >> 16), act4.w,
-                         alv4.w, cn[3], fl[k] >> 6, cb[k][3], nh, nbad, ninel);
-            }
-            order_flush4(g, nh, nbad, ninel);
-          }
-        }
-      }
-    } else {
-      for (int g = 0; g < gc; ++g) {
-        const int8_t* pdev = row_dev(g);
-        const uint16_t* pprio = row_prio(g);
-        const uint8_t* pfl = s_fl + g * NB;
-        uint32_t nh = 0, nbad = 0, ninel = 0;
-        for (int u = lane; u < N; u += 64) {
-          const uint32_t fb = (uint32_t)pfl[u >> 2] >> ((u & 3) << 1);
-          const uint32_t c = t_cnext[u];
-          const uint32_t cbyte = pfl[(c != 0xffffu ? c : (uint32_t)u) >> 2];
-          order_fast(g, u, pdev[u], pprio[u], t_act[u], t_alv[u], c, fb, cbyte, nh, nbad, ninel);
-        }
-        if (ninel) atomicOr(&s_acc[g].status, (uint32_t)WF_ST_INELIGIBLE);
-        if (nbad) atomicOr(&s_acc[g].bad, 1u);
-        if (nh) atomicAdd(&s_acc[g].heads, nh);
-      }
-    }
-    wave_sync();
-    // distinct slots claimed per plan: the union of its devices' masks
-    for (int i = lane; i < gc * NWA; i += 64) {
-      const int g = i / NWA, w = i - g * NWA;
-      unsigned long long x = 0ull;
-      for (int d = 0; d < D; ++d) x |= s_mask[(g * D + d) * NWA + w];
-      if (x) atomicAdd(&s_acc[g].claimed, (uint32_t)__popcll(x));
-    }
-    wave_sync();
-    // plans whose priorities are not a permutation of each level's heads'
-    // index range (one lane per plan)
-    uint64_t rankedm;
-    {
-      const PlanAcc& ag = s_acc[lane < gc ? lane : 0];  // G <= 64
-      const bool rk = lane < gc && (ag.bad != 0u || ag.heads != ag.claimed);
-      rankedm = __ballot(rk);
-    }
-    // general path: rank by (priority, index) within each level
-    for (uint64_t rm = rankedm; rm; rm &= rm - 1ull) {
-      const int g = __builtin_ctzll(rm);
-      const int8_t* pdev = row_dev(g);
-      const uint16_t* pprio = row_prio(g);
-      const uint8_t* pfl = s_fl + g * NB;
-      uint32_t* rec = s_rec + g * N;
-      unsigned long long* mk = s_mask + g * D * NWA;
-      uint32_t* lastp = s_last + g * D * M;
-      for (int i = lane; i < D * NWA; i += 64) mk[i] = 0ull;
-      for (int i = lane; i < D * M; i += 64) lastp[i] = 0u;
-      wave_sync();
-      for (int u = lane; u < N; u += 64) {
-        const uint32_t a = t_act[u];
-        const int fb = pfl[u >> 2] >> ((u & 3) << 1);
-        if ((fb & 1) && (a & 64u)) continue;
-        const int d = pdev[u];
-        if ((unsigned)d >= (unsigned)D) continue;
-        const uint32_t lvw = t_alv[u];
-        const int lo = (int)(lvw & 0xffffu), hi = lo + (int)(lvw >> 16);
-        const int pu = pprio[u];
-        int slot = lo;
-        for (int j = lo; j < hi; ++j) {
-          if (fuse_bit(pfl, j) && (t_act[j] & 64u)) continue;
-          if ((unsigned)pdev[j] >= (unsigned)D) continue;
-          const int pj = pprio[j];
-          slot += (pj < pu) || (pj == pu && j < u);
-        }
-        const int c = t_cnext[u];
-        const uint32_t chain = (c != 0xffff && fuse_bit(pfl, c)) ? kChain : 0u;
-        rec[slot] = (uint32_t)u | ((a & 63u) << 16) | ((uint32_t)((fb >> 1) & 1) << 22) | chain |
-                    (chain ? kSlow : slow0) | ((uint32_t)d << 24);
-        atomicOr(&mk[d * NWA + (slot >> 6)], 1ull << (slot & 63));
-        atomicMax(&lastp[d * M + (int)(a & 63u)], (uint32_t)slot + 1u);
-      }
-      wave_sync();
-    }
-    if constexpr (NIBBLE) {
-      // mark each (device, model)'s last unit in its slot entry: the
-      // reclamation queues need only that bit, and last[] dies here
-      if (vec) {
-        // plans ordered by priority: re-derive each head's (device, slot,
-        // model) from its row; all loads first, then the marks
-        for (int base = 0; base < N; base += 256) {
-          const int u0 = base + 4 * lane;
-          const bool live = u0 < N;
-          const int uc = live ? u0 : 0;
-          const uint4 act4 = *reinterpret_cast<const uint4*>(t_act + uc);
-          const uint4 alv4 = *reinterpret_cast<const uint4*>(t_alv + uc);
-          const uint32_t av[4] = {act4.x, act4.y, act4.z, act4.w};
-          const uint32_t lv[4] = {alv4.x, alv4.y, alv4.z, alv4.w};
-          for (int g0 = 0; g0 < gc; g0 += kB) {
-            uint32_t dv[kB];
-            uint2 pv[kB];
-            rows4(g0, uc, dv, pv);
-            uint32_t fl[kB];
-#pragma unroll
-            for (int k = 0; k < kB; ++k) {
-              const int g = (g0 + k < gc) ? g0 + k : gc - 1;
-              fl[k] = s_fl[g * NB + (uc >> 2)];
-            }
-            int idx[kB][4], prs[kB][4];
-            bool ok[kB][4];
-            uint32_t lst[kB][4];
-#pragma unroll
-            for (int k = 0; k < kB; ++k) {
-              const int g = g0 + k;
-              const bool plan_ok = live && g < gc && !((rankedm >> (g & 63)) & 1ull);
-#pragma unroll
-              for (int j = 0; j < 4; ++j) {
-                const int d = (int)(int8_t)((dv[k] >> (8 * j)) & 0xffu);
-                const int pr = (int)(((j < 2 ? pv[k].x : pv[k].y) >> (16 * (j & 1))) & 0xffffu);
-                const uint32_t fb = fl[k] >> (2 * j);
-                const bool head = !((fb & 1u) && (av[j] & 64u));
-                const bool okd = (unsigned)d < (unsigned)D;
-                const bool inr = (unsigned)(pr - (int)(lv[j] & 0xffffu)) < (lv[j] >> 16);
-                ok[k][j] = plan_ok && head && okd && inr;
-                prs[k][j] = pr;
-                idx[k][j] = ok[k][j] ? (g * D + d) * M + (int)(av[j] & 63u) : 0;
-              }
-            }
-#pragma unroll
-            for (int k = 0; k < kB; ++k)
-#pragma unroll
-              for (int j = 0; j < 4; ++j) lst[k][j] = s_last[idx[k][j]];
-#pragma unroll
-            for (int k = 0; k < kB; ++k)
-#pragma unroll
-              for (int j = 0; j < 4; ++j)
-                if (ok[k][j] && lst[k][j] == (uint32_t)prs[k][j] + 1u)
-                  atomicOr(&s_rec[(g0 + k) * N + prs[k][j]], kLast);
-          }
-        }
-      }
-      // ranked plans (and every plan without the vector path): by slot
-      for (int g = 0; g < gc; ++g) {
-        if (vec && !((rankedm >> g) & 1ull)) continue;
-        uint32_t* rec = s_rec + g * N;
-        const unsigned long long* mk = s_mask + g * D * NWA;
-        const uint32_t* lastp = s_last + g * D * M;
-        for (int sl = lane; sl < N; sl += 64) {
-          const uint32_t e = rec[sl];
-          const int d = (int)((e >> 24) & 63u);
-          const int m = (int)((e >> 16) & 63u);
-          // entries of empty slots are stale: d, m may be anything below 64
-          const bool occ = d < D && m < M && ((mk[d * NWA + (sl >> 6)] >> (sl & 63)) & 1ull);
-          if (occ && lastp[d * M + m] == (uint32_t)sl + 1u) rec[sl] = e | kLast;
-        }
-      }
-      wave_sync();
-    }
-
-    if (pre && grp + stride < n_groups) load_rows(grp + stride, dvp, pvp);
-
-    // ---- device-lane state ----
-    const bool act = g_me < gc;
-    const int gme = act ? g_me : 0;
-    const int64_t pw = p0 + gme;
-    const uint32_t* mylast = s_last + (gme * D + d_me) * M;
-    uint16_t* mystamp = s_stamp + (gme * D + d_me) * M;
-    const unsigned long long* mymask = s_mask + (gme * D + d_me) * NWA;
-    const uint32_t* myrec = s_rec + gme * N;
-    TB* myfin = s_fin + gme * N;
-    const uint8_t* myfl = s_fl + gme * NB;
-    const int d = d_me;
-    uint64_t res = 0;
-    int32_t used = 0, peak = 0, capd = 0;
-    TT freet = 0;
-    uint32_t nld = 0, nev = 0, capbad = 0, inel = 0;
-    uint32_t seq = 1;
-    // reclamation queue (at most 16 models), 4 bits per entry, next victim
-    // in the low bits: first the nd resident models with no remaining use on
-    // this device, then those still needed, each part in least-recently-used
-    // order (never used: by id); nq entries in all
-    QT Q = 0;
-    int nd = 0, nq = 0;
-    if (act) {
-      res = t_res0[d];
-      capd = t_cap[d];
-      freet = TO::load(t_free0 + d);
-      QT qa = 0;
-      int na = 0;
-      for (uint64_t r = res; r; r &= r - 1) {
-        const int m = __builtin_ctzll(r);
-        used += t_wmib[m];
-        if constexpr (NIBBLE) {
-          if (mylast[m] == 0u) {
-            Q |= (QT)m << (4 * nd);
-            ++nd;
-          } else {
-            qa |= (QT)m << (4 * na);
-            ++na;
-          }
-        } else {
-          mystamp[m] = 0;
-        }
-      }
-      if constexpr (NIBBLE) {
-        if (na) Q |= qa << (4 * nd);  // nd + na <= QB / 4, so 4 * nd < QB here
-        nq = nd + na;
-      }
-      peak = used;
-    }
-    if constexpr (NIBBLE) wave_sync();  // last[] (aliasing fin) is read above
-    // every finish starts at 0: it accumulates the latest predecessor finish
-    // before its level, then holds the activation's own finish
-    zero_bytes(reinterpret_cast<unsigned char*>(s_fin), G * N * (int)sizeof(TB), lane);
-    zero_bytes(reinterpret_cast<unsigned char*>(s_wfm), G * W * (int)sizeof(TB), lane);
-    wave_sync();
-
-    for (int lv = 0; lv < sp.n_levels; ++lv) {
-      const int lo = t_loff[lv], hi = t_loff[lv + 1];
-      const int e0 = t_eoff[lv], e1 = t_eoff[lv + 1];
-      // ---- latest predecessor finish of the level's activations (Eq. 2):
-      // one lane per incoming edge.  A fused chain member already holds its
-      // own finish, which is later than its only predecessor's ----
-      if (e1 > e0) {
-        for (int e = e0 + lane; e < e1; e += 64) {
-          const uint32_t ed = t_edge[e];
-          const int src = (int)(ed & 0xffffu), dst = (int)(ed >> 16);
-          for (int g0 = 0; g0 < gc; g0 += kB) {
-            TB f[kB];
-#pragma unroll
-            for (int k = 0; k < kB; ++k) {
-              const int g = (g0 + k < gc) ? g0 + k : gc - 1;
-              f[k] = s_fin[g * N + src];
-            }
-#pragma unroll
-            for (int k = 0; k < kB; ++k)
-              if (g0 + k < gc) atomicMax(&s_fin[(g0 + k) * N + dst], f[k]);
-          }
-        }
-        wave_sync();
-      }
-
-      // ---- device lanes walk their units of this level in slot order ----
-      if (act) {
-        const int j1 = (hi - 1) >> 6;
-        const unsigned long long hmask = (hi & 63) ? ((1ull << (hi & 63)) - 1ull) : ~0ull;
-        // a level of at most 64 slots: this device's slots of the level as
-        // one word, slot lo at bit 0
-        const int width = hi - lo;
-        const bool narrow = width <= 64;
-        int j = lo >> 6;
-        unsigned long long bits, wnext = 0ull;
-        if (narrow) {
-          const int sh = lo & 63;
-          bits = mymask[j] >> sh;
-          if (sh + width > 64) bits |= mymask[j + 1] << (64 - sh);  // then j + 1 <= j1
-          if (width < 64) bits &= (1ull << width) - 1ull;
-        } else {
-          // wider: the current word's remaining bits, and the next word
-          // already loaded
-          bits = mymask[j] & (~0ull << (lo & 63));
-          if (j < j1) wnext = mymask[j + 1] & ((j + 1 == j1) ? hmask : ~0ull);
-        }
-        // the device's next slot in the level; -1 when there is none, -2 for
-        // a trip with no unit (an exhausted word followed by an empty one)
-        auto next_narrow = [&]() -> int {
-          const int sl = lo + __builtin_ctzll(bits | (1ull << 63));
-          const bool have = bits != 0ull;
-          bits &= bits - 1ull;
-          return have ? sl : -1;
-        };
-        auto next_wide = [&]() -> int {
-          const bool adv = bits == 0ull && j < j1;
-          bits = adv ? wnext : bits;
-          j += adv ? 1 : 0;
-          const int jn = j + 1 <= j1 ? j + 1 : j1;
-          const unsigned long long wl2 = mymask[jn] & ((jn == j1) ? hmask : ~0ull);
-          wnext = adv ? (j < j1 ? wl2 : 0ull) : wnext;
-          const int sl = (j << 6) + __builtin_ctzll(bits | (1ull << 63));
-          const bool have = bits != 0ull;
-          bits &= bits - 1ull;
-          return have ? sl : (j < j1 ? -2 : -1);
-        };
-        // slot entry; without a slot a stand-in (activation lo, model 0)
-        // keeps every address below in range
-        auto entry = [&](int sl) -> uint32_t {
-          const uint32_t keep = (uint32_t)~(sl >> 31);  // all ones for a real slot
-          const uint32_t raw = myrec[(int)((uint32_t)sl & keep)];
-          return (raw & keep) | ((uint32_t)lo & ~keep);
-        };
-        auto fetch = [&](int sl, uint32_t meta, UnitPre<TT>& p) {
-          const uint32_t u = meta & 0xffffu, m = (meta >> 16) & 63u;
-          p.meta = meta;
-          p.slot = sl;
-          const uint4 r = ud_d[__umul24(u, (uint32_t)D)];
-          p.lat = (int32_t)r.x;
-          p.mem = (int32_t)r.y;
-          p.arrv = TO::words(r.z, r.w);
-          p.rtv = TO::load(myfin + u);
-          p.lw = lw_d[__umul24(m, (uint32_t)D)];
-        };
-        // one unit of the device's sequence: reuse / reclaim / load, then
-        // the timeline
-        auto process = [&](const UnitPre<TT>& X) {
-          if (X.slot >= 0) {
-            const int u = (int)(X.meta & 0xffffu);
-            const int m = (int)((X.meta >> 16) & 63u);
-            const uint64_t mbit = 1ull << m;
-            bool hit;
-            int32_t w0 = 0, w1 = 0;
-            if constexpr (!NIBBLE) hit = ((res >> m) & 1ull) != 0ull;
-            if constexpr (NIBBLE) {
-              // the queue holds exactly the resident models: m is resident
-              // when it is found among the first nq entries (in the
-              // still-needed part); it is taken out and re-enters as the most
-              // recent
-              const uint32_t m8 = (uint32_t)m * 0x11111111u;  // m in every nibble
-              QT mq = (QT)m8;
-              if constexpr (QB == 64) mq |= (QT)m8 << 32;
-              const QT x = Q ^ mq;
-              const QT z = (x - kOnes) & ~x & kHigh;  // lowest flag: first zero nibble
-              int s4;  // 4 * position
-              if constexpr (QB == 64)
-                s4 = __builtin_ctzll(z | (1ull << 63)) & ~3;
-              else
-                s4 = __builtin_ctz(z | (1u << 31)) & ~3;
-              hit = z != (QT)0 && (s4 >> 2) < nq;
-              const QT low = Q & (((QT)1 << s4) - (QT)1);
-              const QT high = (s4 >= kQBits - 4) ? (QT)0 : ((Q >> (s4 + 4)) << s4);
-              Q = hit ? (low | high) : Q;
-              nq -= hit ? 1 : 0;
-              // the first two victims' weights, looked up ahead of need
-              w0 = t_wmib[(int)(Q & (QT)15)];
-              w1 = t_wmib[(int)((Q >> 4) & (QT)15)];
-            }
-            const TT r = TO::tmax(X.rtv, X.arrv);
-            // run time (summed over a fused chain, Eq. 4) and memory (max)
-            int32_t mxu = X.mem;
-            inel |= (uint32_t)(X.lat < 0);
-            uint32_t T = (uint32_t)X.lat;
-            if (X.meta & kChain) {
-              for (int v = t_cnext[u];;) {
-                const int2 lm = *reinterpret_cast<const int2*>(ud_d + __umul24((uint32_t)v, (uint32_t)D));
-                const int32_t lv2 = lm.x, mv = lm.y;
-                inel |= (uint32_t)(lv2 < 0);
-                T += (uint32_t)lv2;
-                mxu = mv > mxu ? mv : mxu;
-                const int c = t_cnext[v];
-                if (c == 0xffff || !fuse_bit(myfl, c)) break;
-                v = c;
-              }
-            }
-            const int32_t need = (hit ? 0 : X.lw.y) + mxu;
-            // reclaim (Sec. 3.5): a copy with no remaining use first, else the
-            // least recently used, else the lower model id
-            if constexpr (NIBBLE) {
-              int t = 0;
-              while (used + need > capd && nq > 0) {
-                const int v = (int)(Q & (QT)15);
-                Q >>= 4;
-                --nq;
-                nd = nd > 0 ? nd - 1 : 0;
-                int32_t wv = t ? w1 : w0;
-                if (t >= 2) wv = t_wmib[v];
-                used -= wv;
-                ++nev;
-                ++t;
-              }
-              // m re-enters after the no-remaining-use part when this was its
-              // last unit on the device, else at the end
-              const bool last_use = (X.meta & kLast) != 0u;
-              const int pos = 4 * (last_use ? nd : nq);  // nq < QB / 4 here
-              const QT lowm = ((QT)1 << pos) - (QT)1;
-              Q = (Q & lowm) | ((QT)m << pos) | ((Q & ~lowm) << 4);
-              nd += last_use ? 1 : 0;
-              ++nq;
-            } else {
-              (void)w0;
-              (void)w1;
-              while (used + need > capd) {
-                uint64_t cand = res & ~mbit;
-                if (!cand) break;
-                int v = 0;
-                uint32_t best = 0xffffffffu;
-                while (cand) {
-                  const int m2 = __builtin_ctzll(cand);
-                  cand &= cand - 1;
-                  const uint32_t alive = mylast[m2] > (uint32_t)X.slot + 1u;
-                  const uint32_t key = (alive << 16) | mystamp[m2];
-                  if (key < best) {
-                    best = key;
-                    v = m2;
-                  }
-                }
-                res &= ~(1ull << v);
-                used -= t_wmib[v];
-                ++nev;
-              }
-              mystamp[m] = (uint16_t)seq++;
-            }
-            capbad |= (uint32_t)(used + need > capd);
-            // timeline (Eq. 7): a load waits for the device and starts at the
-            // release, or at the workflow arrival when prefetched
-            const TT ls = TO::tmax((X.meta & kPf) ? X.arrv : r, freet);
-            const TT le = TO::add(ls, (uint32_t)X.lw.x);
-            const TT s = TO::tmax(r, hit ? freet : le);
-            if constexpr (!NIBBLE) res |= mbit;
-            used += hit ? 0 : X.lw.y;
-            nld += hit ? 0u : 1u;
-            peak = (used + mxu) > peak ? (used + mxu) : peak;
-            const TT f = TO::add(s, T);
-            freet = f;
-            if (!(X.meta & kSlow)) {
-              myfin[u] = TO::bits(f);
-            } else {
-              TT t = s;
-              for (int v = u;;) {
-                const TT tv =
-                    TO::add(t, ud_d[__umul24((uint32_t)v, (uint32_t)D)].x);
-                myfin[v] = TO::bits(tv);
-                if (has_sched) {
-                  sched.start_us[pw * N + v] = sp.origin + TO::i64(t);
-                  sched.finish_us[pw * N + v] = sp.origin + TO::i64(tv);
-                  sched.load_start_us[pw * N + v] =
-                      (v == u && !hit) ? sp.origin + TO::i64(ls) : (int64_t)-1;
-                }
-                t = tv;
-                const int c = t_cnext[v];
-                if (c == 0xffff || !fuse_bit(myfl, c)) break;
-                v = c;
-              }
-            }
-          }
-        };
-        // two units per trip so that the prefetched unit needs no copy; one
-        // copy of the loop per kind of level
-        auto run = [&](auto&& next_slot) {
-          UnitPre<TT> A, B;
-          {
-            const int sa = next_slot();
-            fetch(sa, entry(sa), A);
-          }
-          int sb = A.slot != -1 ? next_slot() : -1;
-          uint32_t mb_next = entry(sb);
-          while (A.slot != -1) {
-            fetch(sb, mb_next, B);
-            const int sc = sb != -1 ? next_slot() : -1;
-            const uint32_t mc = entry(sc);
-            process(A);
-            if (B.slot == -1) break;
-            fetch(sc, mc, A);
-            sb = sc != -1 ? next_slot() : -1;
-            mb_next = entry(sb);
-            process(B);
-          }
-        };
-        if (narrow)
-          run(next_narrow);
-        else
-          run(next_wide);
-      }
-      wave_sync();
-    }
-
-    // ---- per-plan reductions (Sec. 4 metrics) ----
-    if (act) {
-      atomicMin(&s_acc[gme].headroom, capd - peak);
-      atomicAdd(&s_acc[gme].loads, nld);
-      atomicAdd(&s_acc[gme].evicts, nev);
-      if (capbad) atomicOr(&s_acc[gme].status, (uint32_t)WF_ST_CAPACITY);
-      if (inel) atomicOr(&s_acc[gme].status, (uint32_t)WF_ST_INELIGIBLE);
-      if (has_sched) sched.peak_mib[pw * D + d_me] = peak;
-    }
-    // a workflow's completion is the latest finish among its activations
-    // without a successor in the same workflow
-    for (int i = lane; i < sp.S; i += 64) {
-      const uint32_t sk = t_sink[i];
-      const int src = (int)(sk & 0xffffu), wf = (int)(sk >> 16);
-      for (int g0 = 0; g0 < gc; g0 += kB) {
-        TB f[kB];
-#pragma unroll
-        for (int k = 0; k < kB; ++k) {
-          const int g = (g0 + k < gc) ? g0 + k : gc - 1;
-          f[k] = s_fin[g * N + src];
-        }
-#pragma unroll
-        for (int k = 0; k < kB; ++k)
-          if (g0 + k < gc) atomicMax(&s_wfm[(g0 + k) * W + wf], f[k]);
-      }
-    }
-    wave_sync();
-    // completion latencies in place, and the latest finish
-    for (int it = lane; it < gc * W; it += 64) {
-      const int g = it / W, a = it - g * W;
-      const TB fb = s_wfm[it];
-      atomicMax(&s_acc[g].max_finish, (unsigned long long)fb);
-      s_wfm[it] = TO::bits(TO::sub(TO::load(&fb), TO::load(t_arr + a)));
-    }
-    wave_sync();
-    // nearest-rank p95: the ceil(0.95 W)-th smallest completion latency,
-    // lanes over (plan, workflow)
-    const int kk = (95 * W + 99) / 100;
-    for (int it = lane; it < gc * W; it += 64) {
-      const int g = it / W;
-      const TB* cw = s_wfm + g * W;
-      const TT ca = TO::load(cw + (it - g * W));
-      int lt = 0, le = 0;
-#pragma unroll 8
-      for (int b = 0; b < W; ++b) {
-        const TT cb = TO::load(cw + b);
-        lt += cb < ca;
-        le += cb <= ca;
-      }
-      if (lt < kk && kk <= le) s_acc[g].p95 = TO::i64(ca);
-    }
-    wave_sync();
-    if (lane < gc) {
-      const PlanAcc a = s_acc[lane];
-      wf_plan_score sc;
-      if (a.status & WF_ST_INELIGIBLE) {
-        sc.makespan_us = 0;
-        sc.p95_us = 0;
-        sc.objective = 0.0f;
-        sc.status = WF_ST_INELIGIBLE;
-        sc.min_headroom_mib = 0;
-        sc.n_loads = 0;
-        sc.n_evicts = 0;
-      } else {
-        const TT mf = TO::load(reinterpret_cast<const TB*>(&a.max_finish));
-        const int64_t mk = N > 0 ? sp.origin + TO::i64(mf) - sp.min_arrival : 0;
-        const int64_t p95 = W > 0 ? (int64_t)a.p95 : 0;
-        const float fa = (float)mk;
-        const float fb = (float)p95;
-        const float x = sp.w_mk * fa;
-        const float y = sp.w_p95 * fb;
-        sc.makespan_us = mk;
-        sc.p95_us = p95;
-        sc.objective = x + y;
-        sc.status = a.status;
-        sc.min_headroom_mib = a.headroom;
-        sc.n_loads = (uint16_t)(a.loads > 65535u ? 65535u : a.loads);
-        sc.n_evicts = (uint16_t)(a.evicts > 65535u ? 65535u : a.evicts);
-      }
-      scores[p0 + lane] = sc;
-    }
-    wave_sync();
-  }
-}
-
-template <typename TT, bool TAB_LDS, int QB, bool WAVE_GLOBAL, bool SEARCH>
-hipError_t launch_variant(const ScoreParams& sp, const int8_t* dev, const uint16_t* prio,
-                          const uint8_t* flags, int64_t n_plans, wf_plan_score* scores,
-                          const wf_plan_sched& s, int has, const SearchArgs& sa,
-                          hipStream_t stream) {
-  auto k = score_plans<TT, TAB_LDS, QB, WAVE_GLOBAL, SEARCH>;
-  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, sp.lds_bytes);
-  hipLaunchKernelGGL(k, dim3(sp.grid), dim3(64 * sp.waves), sp.lds_bytes, stream, sp, dev, prio,
-                     flags, n_plans, scores, s, has, sa);
-  return hipGetLastError();
-}
-
-template <typename TT, int QB, bool SEARCH>
-hipError_t launch_place(const ScoreParams& sp, const int8_t* dev, const uint16_t* prio,
-                        const uint8_t* flags, int64_t n_plans, wf_plan_score* scores,
-                        const wf_plan_sched& s, int has, const SearchArgs& sa, hipStream_t stream) {
-  if (sp.wave_global)
-    return launch_variant<TT, false, QB, true, SEARCH>(sp, dev, prio, flags, n_plans, scores,
-                                                           s, has, sa, stream);
-  if (sp.tab_in_lds)
-    return launch_variant<TT, true, QB, false, SEARCH>(sp, dev, prio, flags, n_plans, scores,
-                                                           s, has, sa, stream);
-  return launch_variant<TT, false, QB, false, SEARCH>(sp, dev, prio, flags, n_plans, scores,
-                                                          s, has, sa, stream);
-}
-
-template <typename TT, bool SEARCH>
-hipError_t launch_time(const ScoreParams& sp, const int8_t* dev, const uint16_t* prio,
-                       const uint8_t* flags, int64_t n_plans, wf_plan_score* scores,
-                       const wf_plan_sched& s, int has, const SearchArgs& sa, hipStream_t stream) {
-  if (sp.nibble == 32)
-    return launch_place<TT, 32, SEARCH>(sp, dev, prio, flags, n_plans, scores, s, has, sa, stream);
-  if (sp.nibble == 64)
-    return launch_place<TT, 64, SEARCH>(sp, dev, prio, flags, n_plans, scores, s, has, sa, stream);
-  return launch_place<TT, 0, SEARCH>(sp, dev, prio, flags, n_plans, scores, s, has, sa, stream);
-}
-
-template <typename TT>
-hipError_t launch_mode(const ScoreParams& sp, const int8_t* dev, const uint16_t* prio,
-                       const uint8_t* flags, int64_t n_plans, wf_plan_score* scores,
-                       const wf_plan_sched& s, int has, const SearchArgs* search,
-                       hipStream_t stream) {
-  if (search)
-    return launch_time<TT, true>(sp, dev, prio, flags, n_plans, scores, s, 0, *search, stream);
-  return launch_time<TT, false>(sp, dev, prio, flags, n_plans, scores, s, has, SearchArgs{}, stream);
-}
 
 // One workgroup per candidate: the incumbent's rows, then its mutations.
 __global__ __launch_bounds__(64) void search_rows(const int8_t* __restrict__ dev,
@@ -1039,12 +33,7 @@ hipError_t launch_score(const ScoreParams& sp, const int8_t* dev, const uint16_t
                         const uint8_t* flags, int64_t n_plans, wf_plan_score* scores,
                         const wf_plan_sched* sched, const SearchArgs* search,
                         hipStream_t stream) {
-  wf_plan_sched s{};
-  if (sched) s = *sched;
-  const int has = sched != nullptr;
-  if (sp.time64)
-    return launch_mode<double>(sp, dev, prio, flags, n_plans, scores, s, has, search, stream);
-  return launch_mode<uint32_t>(sp, dev, prio, flags, n_plans, scores, s, has, search, stream);
+  return launch_all<false>(sp, dev, prio, flags, n_plans, scores, sched, search, stream);
 }
 
 hipError_t launch_search_rows(const ScoreParams& sp, const int8_t* dev, const uint16_t* prio,
@@ -1058,6 +47,5 @@ hipError_t launch_search_rows(const ScoreParams& sp, const int8_t* dev, const ui
                      sp.N, elig, alv, out_dev, out_prio, out_flags);
   return hipGetLastError();
 }
-
 
 }  // namespace wfp

@@ -48,6 +48,19 @@ def test_score_record_layout():
     assert [pkg.SCORE_DTYPE.fields[k][1] for k in pkg.SCORE_DTYPE.names] == [0, 8, 16, 20, 24, 28, 30]
 
 
+def test_key_record_layout():
+    text = open(HEADER).read()
+    assert "uint16_t admitted[WF_MAX_CLASSES];" in text and "} wf_plan_key;" in text
+    assert pkg.KEY_DTYPE.itemsize == 32
+    assert [pkg.KEY_DTYPE.fields[k][1] for k in pkg.KEY_DTYPE.names] == [0, 8, 16, 24, 26, 28]
+
+
+def test_classes_in_range_pass():
+    w = _ok_window()
+    w.wf_class = np.arange(w.n_wf, dtype=np.uint8) % pkg._lib.WF_MAX_CLASSES
+    assert pkg.wf_plan_validate_window(w)[0] == pkg.WF_OK
+
+
 def test_no_gpu_context_fails_cleanly():
     import torch
     if torch.cuda.is_available():
@@ -100,6 +113,8 @@ BAD = {
     "nan_weight": lambda w: setattr(w, "w_makespan", float("nan")),
     "empty_workflow": lambda w: (setattr(w, "n_wf", 3), setattr(w, "wf_arrival_us", np.zeros(3, np.int64))),
     "negative_free0": lambda w: w.dev_free0_us.__setitem__(0, -3),
+    "class_out_of_range": lambda w: setattr(w, "wf_class",
+                                            np.full(w.n_wf, pkg._lib.WF_MAX_CLASSES, np.uint8)),
 }
 
 
