@@ -351,6 +351,7 @@ wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, Image& img, wfp::Sc
       r[0] = (uint32_t)h.lat[(size_t)i * D + d];
       r[1] = (uint32_t)h.mem[(size_t)i * D + d];
       std::memcpy(&r[2], &arr[(size_t)h.act_wf[i] * tsz], tsz);
+      if (!time64) r[3] = act[i];  // the ranking-key mode reads it from here
     }
   wfp::TabOffsets& t = sp.t;
   t.act = img.put(act.data(), act.size() * 4);

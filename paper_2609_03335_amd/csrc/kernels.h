@@ -13,7 +13,9 @@ namespace wfp {
 // the image once per window; the scoring kernel copies it into LDS (or reads
 // it from HBM when it is too large) and uses the same offsets either way.
 struct TabOffsets {
-  int act;     // u32 [N]    model | fusible << 6 | workflow << 16
+  int act;     // u32 [N]    model | fusible << 6 | ready << 7 | class << 8 | workflow << 16
+               //            (ready: no predecessor and arrived by time 0; class: the
+               //            workflow's priority class of the ranking key)
   int alv;     // u32 [N]    first index of the activation's level | level width << 16
   int cnext;   // u16 [N]    successor v of u when Eq. 3 holds for (u, v), else 0xffff
   int edge;    // u32 [E]    predecessor | activation << 16, grouped by activation (CSR order)
@@ -21,7 +23,8 @@ struct TabOffsets {
   int loff;    // i32 [L+1]  first activation of each level
   int ud;      // 16 B [N*D] per (activation, device): {run time (-1 ineligible), activation
                //            memory, arrival of the activation's workflow (relative time,
-               //            low word / high word for fp64)}
+               //            low word / high word for fp64); with uint32 times the last word
+               //            repeats the activation's act entry}
   int lw;      // i32x2 [M*D] {load time, model weights}
   int wmib;    // i32 [M]    model weights
   int cap;     // i32 [D]    device capacity

@@ -735,7 +735,12 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
           p.arrv = TO::words(r.z, r.w);
           p.rtv = TO::load(myfin + u);
           p.lw = lw_d[__umul24(m, (uint32_t)D)];
-          if constexpr (PHI) p.act = t_act[u];
+          if constexpr (PHI) {
+            if constexpr (std::is_same<TT, uint32_t>::value)
+              p.act = r.w;
+            else
+              p.act = t_act[u];
+          }
         };
         // one unit of the device's sequence: reuse / reclaim / load, then
         // the timeline
