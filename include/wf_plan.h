@@ -174,7 +174,9 @@ wf_status wf_plan_score_batch(wf_plan_ctx *ctx, const int8_t *dev, const uint16_
 
 /* Among plans with status 0, the index of the smallest objective (lowest
  * index on ties), or -1 if none is feasible, written to the device int64
- * *out_index.  n_plans must be < 2^32; n_plans = 0 writes -1. */
+ * *out_index.  n_plans must be < 2^32; n_plans = 0 writes -1.  Uses a small
+ * work area owned by the context (shared with wf_plan_argmin_keys): argmin
+ * calls on one context must not run concurrently on different streams. */
 wf_status wf_plan_argmin(wf_plan_ctx *ctx, const wf_plan_score *scores, int64_t n_plans,
                          int64_t *out_index, void *hip_stream);
 

@@ -4,11 +4,10 @@
 // the scalar objective in place of the lexicographic key of Eq. 12).
 //
 // Each plan maps to a 64-bit key (order-preserving objective bits << 32 |
-// plan index); infeasible plans map to ~0.  The minimum key is reduced in a
-// wave with cross-lane shuffles, then across the grid with one 64-bit atomic
-// min per wave into the caller's output slot, which a final single-lane
-// kernel turns into the plan index.  The output slot doubles as the
-// reduction cell, so the call needs no library-owned scratch.
+// plan index); infeasible plans map to ~0.  Each block reduces a strided
+// share of the plans (wave shuffles, then LDS across its waves) to one
+// partial minimum in a work area, and one final block reduces the partials
+// and writes the plan index: deterministic, and without a contended atomic.
 #include "kernels.h"
 
 namespace wfp {
@@ -29,37 +28,50 @@ __device__ __forceinline__ unsigned long long wave_min(unsigned long long k) {
   return k;
 }
 
-__global__ __launch_bounds__(64) void argmin_init(unsigned long long* cell) { *cell = ~0ull; }
+// The block's minimum of k over its 256 threads; valid in thread 0.
+__device__ unsigned long long block_min(unsigned long long k) {
+  k = wave_min(k);
+  __shared__ unsigned long long wmin[4];
+  if ((threadIdx.x & 63) == 0) wmin[threadIdx.x >> 6] = k;
+  __syncthreads();
+  if (threadIdx.x == 0)
+    for (int w = 1; w < (int)(blockDim.x >> 6); ++w) k = wmin[w] < k ? wmin[w] : k;
+  return k;
+}
 
-__global__ __launch_bounds__(256) void argmin_reduce(const wf_plan_score* __restrict__ s,
-                                                     int64_t n, unsigned long long* cell) {
+__global__ __launch_bounds__(256) void argmin_partial(const wf_plan_score* __restrict__ s,
+                                                      int64_t n, unsigned long long* part) {
   unsigned long long best = ~0ull;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
     const unsigned long long k = plan_key(s, i);
     best = k < best ? k : best;
   }
-  best = wave_min(best);
-  if ((threadIdx.x & 63) == 0 && best != ~0ull) atomicMin(cell, best);
+  best = block_min(best);
+  if (threadIdx.x == 0) part[blockIdx.x] = best;
 }
 
-__global__ __launch_bounds__(64) void argmin_finish(unsigned long long* cell) {
-  const unsigned long long k = *cell;
-  *reinterpret_cast<int64_t*>(cell) = (k == ~0ull) ? (int64_t)-1 : (int64_t)(k & 0xffffffffull);
+__global__ __launch_bounds__(256) void argmin_final(const unsigned long long* __restrict__ part,
+                                                    int nparts, int64_t* out_index) {
+  unsigned long long best = ~0ull;
+  for (int i = threadIdx.x; i < nparts; i += blockDim.x) best = part[i] < best ? part[i] : best;
+  best = block_min(best);
+  if (threadIdx.x == 0)
+    *out_index = (best == ~0ull) ? (int64_t)-1 : (int64_t)(best & 0xffffffffull);
 }
 
 }  // namespace
 
 hipError_t launch_argmin(const wf_plan_score* scores, int64_t n_plans, int64_t* out_index,
-                         int grid, hipStream_t stream) {
-  unsigned long long* cell = reinterpret_cast<unsigned long long*>(out_index);
-  hipLaunchKernelGGL(argmin_init, dim3(1), dim3(1), 0, stream, cell);
+                         void* work, hipStream_t stream) {
+  unsigned long long* part = reinterpret_cast<unsigned long long*>(work);
+  int blocks = 0;
   if (n_plans > 0) {
-    int64_t need = (n_plans + 255) / 256;
-    const int g = (int)(need < grid ? need : grid);
-    hipLaunchKernelGGL(argmin_reduce, dim3(g), dim3(256), 0, stream, scores, n_plans, cell);
+    const int64_t need = (n_plans + 255) / 256;
+    blocks = (int)(need < kArgminKeyBlocks ? need : kArgminKeyBlocks);
+    hipLaunchKernelGGL(argmin_partial, dim3(blocks), dim3(256), 0, stream, scores, n_plans, part);
   }
-  hipLaunchKernelGGL(argmin_finish, dim3(1), dim3(1), 0, stream, cell);
+  hipLaunchKernelGGL(argmin_final, dim3(1), dim3(256), 0, stream, part, blocks, out_index);
   return hipGetLastError();
 }
 

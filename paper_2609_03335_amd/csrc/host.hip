@@ -209,7 +209,7 @@ struct wf_plan_ctx {
   bool has_window = false;
   HostWindow host;
   DeviceWindow dw;
-  void* key_work = nullptr;  // partial results of the ranking-key argmin
+  void* key_work = nullptr;  // partial results of the argmins
 };
 
 namespace {
@@ -748,7 +748,8 @@ wf_status wf_plan_argmin(wf_plan_ctx* ctx, const wf_plan_score* scores, int64_t 
   (void)hipGetDevice(&prev);
   hipError_t e = hipSetDevice(ctx->device);
   if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
-  e = wfp::launch_argmin(scores, n_plans, out_index, ctx->n_cu * 4, static_cast<hipStream_t>(hip_stream));
+  e = wfp::launch_argmin(scores, n_plans, out_index, ctx->key_work,
+                         static_cast<hipStream_t>(hip_stream));
   (void)hipSetDevice(prev);
   if (e != hipSuccess) return hip_fail(ctx, e, "launching the argmin kernels");
   return WF_OK;

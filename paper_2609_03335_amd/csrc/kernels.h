@@ -122,13 +122,14 @@ hipError_t launch_search_rows(const ScoreParams& sp, const int8_t* dev, const ui
                               int8_t* out_dev, uint16_t* out_prio, uint8_t* out_flags,
                               hipStream_t stream);
 
-hipError_t launch_argmin(const wf_plan_score* scores, int64_t n_plans, int64_t* out_index,
-                         int grid, hipStream_t stream);
-
-// Lexicographic argmin of ranking keys: `blocks` partial results in `work`
-// (ARGMIN_KEY_WORK_BYTES per block), then one block for the final result.
+// Argmins: at most kArgminKeyBlocks partial results in `work`
+// (ARGMIN_KEY_WORK_BYTES per block, owned by the context), then one block for
+// the final result.
 constexpr int kArgminKeyBlocks = 512;
 constexpr size_t ARGMIN_KEY_WORK_BYTES = 64;
+
+hipError_t launch_argmin(const wf_plan_score* scores, int64_t n_plans, int64_t* out_index,
+                         void* work, hipStream_t stream);
 hipError_t launch_argmin_keys(const wf_plan_key* keys, int64_t n_plans, int64_t* out_index,
                               void* work, hipStream_t stream);
 
