@@ -21,6 +21,8 @@ SRC_PATH = os.path.join(_HERE, "oracle.c")
 
 INELIGIBLE = 1
 CAPACITY = 2
+VICTIM_REMAINING_LRU = 0
+VICTIM_PAPER = 1
 
 SCORE_DTYPE = np.dtype([
     ("makespan_us", "<i8"), ("p95_us", "<i8"), ("objective", "<f4"),
@@ -59,6 +61,7 @@ class _Win(ctypes.Structure):
         ("model_mib", ctypes.c_void_p), ("load_us", ctypes.c_void_p),
         ("init_resident", ctypes.c_void_p), ("dev_free0_us", ctypes.c_void_p),
         ("w_makespan", ctypes.c_float), ("w_p95", ctypes.c_float),
+        ("victim_order", ctypes.c_int32),
     ]
 
 
@@ -119,6 +122,7 @@ class _WinHolder:
         for k, v in self.keep.items():
             setattr(s, k, None if v is None else v.ctypes.data)
         s.w_makespan, s.w_p95 = win.w_makespan, win.w_p95
+        s.victim_order = int(getattr(win, "victim_order", 0))
         self.struct = s
 
 

@@ -122,6 +122,25 @@ static int cmp_i64(const void *a, const void *b) {
 
 static int64_t max64(int64_t a, int64_t b) { return a > b ? a : b; }
 
+#define ORC_NO_USE INT64_MAX
+
+/* The paper's reclamation preference (Sec. 3.5): 1 when copy x should be
+ * reclaimed before copy y.  red: resident on another device; dist: positions
+ * until the next use on this device (ORC_NO_USE: none); load: reload time;
+ * last: position of the last use on this device (-1: never used). */
+static int paper_victim_before(int redx, int64_t distx, int64_t loadx, int64_t lastx,
+                               int redy, int64_t disty, int64_t loady, int64_t lasty) {
+  if (redx != redy) return redx > redy;                       /* redundant copies first */
+  const int infx = distx == ORC_NO_USE || loadx == 0;         /* distance / reload cost */
+  const int infy = disty == ORC_NO_USE || loady == 0;
+  if (infx != infy) return infx > infy;
+  if (!infx) {
+    const int64_t a = distx * loady, b = disty * loadx;       /* distx/loadx vs disty/loady */
+    if (a != b) return a > b;
+  }
+  return lastx < lasty;                                       /* least recently used */
+}
+
 /* ---------------------------------------------------------------------- */
 /* scoring                                                                 */
 /* ---------------------------------------------------------------------- */
@@ -135,6 +154,9 @@ static int simulate(const orc_window *w, const uint8_t *wf_class, const int8_t *
   if (wf_class)
     for (int32_t f = 0; f < w->n_wf; ++f)
       if (wf_class[f] >= ORC_MAX_CLASSES) return ORC_ERR_CLASS;
+  if (w->victim_order != ORC_VICTIM_REMAINING_LRU && w->victim_order != ORC_VICTIM_PAPER)
+    return ORC_ERR_VICTIM;
+  const int paper = w->victim_order == ORC_VICTIM_PAPER;
   orc_struct st;
   int rc = build_struct(w, &st);
   if (rc) return rc;
@@ -151,10 +173,13 @@ static int simulate(const orc_window *w, const uint8_t *wf_class, const int8_t *
           *peak = (int64_t *)malloc((size_t)D * 8);
   uint64_t *res = (uint64_t *)malloc((size_t)D * 8);
   uint64_t *reclaimed = (uint64_t *)malloc((size_t)D * 8);
+  uint64_t *res_level = (uint64_t *)malloc((size_t)D * 8);
+  int64_t *next_after = (int64_t *)malloc(n * 8);
+  int64_t *next_use = (int64_t *)malloc((size_t)D * M * 8);
   int64_t *remaining = (int64_t *)malloc((size_t)D * M * 8), *last = (int64_t *)malloc((size_t)D * M * 8);
   if (!fuse || !pf || !member || !unit_Mx || !order || !start || !finish ||
       !load_start || !comp || !free_t || !used || !peak || !res || !reclaimed || !remaining ||
-      !last) {
+      !last || !res_level || !next_after || !next_use) {
     rc = ORC_ERR_NOMEM;
     goto done;
   }
@@ -212,6 +237,15 @@ static int simulate(const orc_window *w, const uint8_t *wf_class, const int8_t *
       int32_t h = order[k].idx;
       remaining[pdev[h] * M + w->act_model[h]] += 1;
     }
+    /* next use of the same model on the same device after each position,
+     * and the first use of every (device, model) */
+    for (int32_t i = 0; i < D * M; ++i) next_use[i] = ORC_NO_USE;
+    for (int32_t k = n_units - 1; k >= 0; --k) {
+      int32_t h = order[k].idx;
+      int64_t *nu = &next_use[pdev[h] * M + w->act_model[h]];
+      next_after[k] = *nu;
+      *nu = k;
+    }
 
     /* ---- pool snapshot ---- */
     for (int32_t d = 0; d < D; ++d) {
@@ -236,6 +270,9 @@ static int simulate(const orc_window *w, const uint8_t *wf_class, const int8_t *
       int32_t wf = w->act_wf[h];
       int64_t Mx = unit_Mx[h];
       remaining[d * M + m] -= 1;
+      /* pool residency as the unit's topological level starts */
+      if (pos == 0 || order[pos].level != order[pos - 1].level)
+        for (int32_t e = 0; e < D; ++e) res_level[e] = res[e];
 
       /* predicted release (Eq. 2): workflow arrival, or the latest
        * predecessor completion */
@@ -254,6 +291,24 @@ static int simulate(const orc_window *w, const uint8_t *wf_class, const int8_t *
           if (!((cand >> m2) & 1u)) continue;
           if (victim < 0) {
             victim = m2;
+            continue;
+          }
+          if (paper) {
+            int64_t key[2][4];
+            const int32_t mm[2] = {m2, victim};
+            for (int q = 0; q < 2; ++q) {
+              int red = 0;
+              for (int32_t e = 0; e < D; ++e)
+                if (e != d && ((res_level[e] >> mm[q]) & 1u)) red = 1;
+              const int64_t nu = next_use[d * M + mm[q]];
+              key[q][0] = red;
+              key[q][1] = nu == ORC_NO_USE ? ORC_NO_USE : nu - pos;
+              key[q][2] = w->load_us[mm[q] * D + d];
+              key[q][3] = last[d * M + mm[q]];
+            }
+            if (paper_victim_before((int)key[0][0], key[0][1], key[0][2], key[0][3],
+                                    (int)key[1][0], key[1][1], key[1][2], key[1][3]))
+              victim = m2; /* equal keys keep the lower id (scanned first) */
             continue;
           }
           int alive2 = remaining[d * M + m2] > 0, aliveV = remaining[d * M + victim] > 0;
@@ -312,6 +367,7 @@ static int simulate(const orc_window *w, const uint8_t *wf_class, const int8_t *
       }
       free_t[d] = s;
       last[d * M + m] = pos;
+      next_use[d * M + m] = next_after[pos];
       if (ready && fits) {
         admitted[wf_class ? wf_class[wf] : 0] += 1;
         c_ready = max64(c_ready, s);
@@ -370,6 +426,7 @@ done:
   free(fuse); free(pf); free(member); free(unit_Mx); free(order);
   free(start); free(finish); free(load_start); free(comp); free(free_t); free(used);
   free(peak); free(res); free(reclaimed); free(remaining); free(last);
+  free(res_level); free(next_after); free(next_use);
   free_struct(&st);
   return rc;
 }

@@ -48,7 +48,25 @@ typedef struct {
   const uint64_t *init_resident;/* [n_dev] resident-model bitmask             */
   const int64_t *dev_free0_us;  /* [n_dev] busy-until, or NULL for all 0      */
   float w_makespan, w_p95;
+  int32_t victim_order;         /* ORC_VICTIM_REMAINING_LRU or ORC_VICTIM_PAPER */
 } orc_window;
+
+/*
+ * Reclamation victim order (Sec. 3.5, reclamation), among the resident
+ * models of the device other than the unit's own:
+ *   ORC_VICTIM_REMAINING_LRU -- copies with no remaining use on the device
+ *     in the plan first, then least recently used (initial residents never
+ *     used count as oldest), then the lower model id;
+ *   ORC_VICTIM_PAPER -- redundant copies first (the model is resident on
+ *     another device when the current topological level starts), then the
+ *     largest next-use distance relative to reload cost -- distance = the
+ *     number of positions in the resource order until the next unit of the
+ *     device that uses the model, infinite without one; the ratio
+ *     distance / load time is infinite when either the distance is infinite
+ *     or the load time is 0; finite ratios compare by cross-multiplication --,
+ *     then least recently used, then the lower model id.
+ */
+enum { ORC_VICTIM_REMAINING_LRU = 0, ORC_VICTIM_PAPER = 1 };
 
 typedef struct {
   int64_t makespan_us;
@@ -70,7 +88,8 @@ enum {
   ORC_ERR_INDEX = 4,      /* workflow / model id out of range                  */
   ORC_ERR_EMPTY_WF = 5,   /* a workflow without activations                    */
   ORC_ERR_NOMEM = 6,
-  ORC_ERR_CLASS = 7       /* a workflow class outside 0 .. ORC_MAX_CLASSES-1    */
+  ORC_ERR_CLASS = 7,      /* a workflow class outside 0 .. ORC_MAX_CLASSES-1    */
+  ORC_ERR_VICTIM = 8      /* victim_order is not one of ORC_VICTIM_*           */
 };
 
 /*

@@ -64,6 +64,10 @@ class Window:
     # uint8[W] priority class of each workflow for the ranking key of Eq. 12
     # (0 ranked first, below 4); None puts every workflow in class 0
     wf_class: Optional[np.ndarray] = None
+    # reclamation victim order: 0 = no remaining use first, then least
+    # recently used; 1 = the paper's (redundant copies, then next use
+    # relative to reload cost, then least recently used)
+    victim_order: int = 0
 
     def arrays(self):
         return {f.name: getattr(self, f.name) for f in dataclasses.fields(self)}
@@ -548,6 +552,8 @@ def load_npz(path: str):
         kw[k] = int(kw[k])
     for k in ("w_makespan", "w_p95"):
         kw[k] = float(kw[k])
+    if "victim_order" in kw:
+        kw["victim_order"] = int(kw["victim_order"])
     win = Window(**kw)
     plans = PlanBatch(z["p_dev"], z["p_prio"], z["p_flags"]) if "p_dev" in z else None
     return win, plans

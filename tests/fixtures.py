@@ -42,6 +42,11 @@ def load_golden(name):
         load_us=np.array([m["load_us"] for m in spec["models"]], np.int32).reshape(-1),
         init_resident=np.zeros(D, np.uint64), dev_free0_us=np.zeros(D, np.int64),
         w_makespan=1.0, w_p95=0.5, name=name)
+    for dname, mnames in spec.get("init_resident", {}).items():
+        bits = 0
+        for mn in mnames:
+            bits |= 1 << models.index(mn)
+        win.init_resident[devs.index(dname)] = np.uint64(bits)
     plans = {}
     for pname, ps in spec["plans"].items():
         dev = np.array([[devs.index(ps["device"][nm]) for nm in names]], np.int8)

@@ -16,6 +16,7 @@ import test_oracle_paper_examples as t_pap
 import test_oracle_properties as t_prop
 import test_oracle_search as t_search
 import test_oracle_phi as t_phi
+import test_oracle_victim as t_vic
 
 # (name, original fragment, planted mistake)
 MUTANTS = [
@@ -81,6 +82,19 @@ MUTANTS = [
      "if (ready) h_life += s - r;"),
     ("loading delay of all work", "if (ready) h_life += s - max64(r, free_before);",
      "h_life += s - max64(r, free_before);"),
+    # paper victim order (Sec. 3.5, reclamation)
+    ("paper order ignores redundancy", "if (redx != redy) return redx > redy;", ""),
+    ("paper order prefers kept copies elsewhere", "if (redx != redy) return redx > redy;",
+     "if (redx != redy) return redx < redy;"),
+    ("paper ratio inverted", "if (a != b) return a > b;", "if (a != b) return a < b;"),
+    ("paper order ignores reload cost", "const int64_t a = distx * loady, b = disty * loadx;",
+     "const int64_t a = distx, b = disty;"),
+    ("paper order ignores next use", "key[q][1] = nu == ORC_NO_USE ? ORC_NO_USE : nu - pos;",
+     "key[q][1] = 1;"),
+    ("redundancy from live residency", "if (e != d && ((res_level[e] >> mm[q]) & 1u)) red = 1;",
+     "if (e != d && ((res[e] >> mm[q]) & 1u)) red = 1;"),
+    ("next use not advanced", "next_use[d * M + m] = next_after[pos];", ""),
+    ("paper order most recently used", "return lastx < lasty;", "return lastx > lasty;"),
 ]
 
 
@@ -108,6 +122,10 @@ def _pin_checks():
     checks += [lambda n=n: t_phi.test_worked_examples(n) for n in ("phi_reload", "phi_prefetch", "phi_ready_prefetch")]
     checks += [lambda s=s: t_phi.test_phi_from_schedule(s) for s in range(6)]
     checks += [lambda s=s: t_phi.test_phi_invariants(s) for s in range(3)]
+    checks += [lambda n=n: t_vic.test_worked_examples(n)
+               for n in ("victim_order", "victim_order_chain", "victim_order_snapshot",
+                         "victim_order_ties")]
+    checks += [lambda s=s: t_vic.test_paper_order_is_belady_optimal_on_one_device(s) for s in range(40)]
     return checks
 
 
