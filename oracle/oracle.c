@@ -174,12 +174,13 @@ static int simulate(const orc_window *w, const uint8_t *wf_class, const int8_t *
   uint64_t *res = (uint64_t *)malloc((size_t)D * 8);
   uint64_t *reclaimed = (uint64_t *)malloc((size_t)D * 8);
   uint64_t *res_level = (uint64_t *)malloc((size_t)D * 8);
-  int64_t *next_after = (int64_t *)malloc(n * 8);
+  int64_t *dev_units = (int64_t *)malloc((size_t)D * 8);
+  int64_t *next_after = (int64_t *)malloc(n * 8), *dev_index = (int64_t *)malloc(n * 8);
   int64_t *next_use = (int64_t *)malloc((size_t)D * M * 8);
   int64_t *remaining = (int64_t *)malloc((size_t)D * M * 8), *last = (int64_t *)malloc((size_t)D * M * 8);
   if (!fuse || !pf || !member || !unit_Mx || !order || !start || !finish ||
       !load_start || !comp || !free_t || !used || !peak || !res || !reclaimed || !remaining ||
-      !last || !res_level || !next_after || !next_use) {
+      !last || !res_level || !dev_units || !next_after || !dev_index || !next_use) {
     rc = ORC_ERR_NOMEM;
     goto done;
   }
@@ -237,14 +238,17 @@ static int simulate(const orc_window *w, const uint8_t *wf_class, const int8_t *
       int32_t h = order[k].idx;
       remaining[pdev[h] * M + w->act_model[h]] += 1;
     }
-    /* next use of the same model on the same device after each position,
-     * and the first use of every (device, model) */
+    /* each unit's index among its device's units, the next use of the same
+     * model on the same device after each unit (as such an index), and the
+     * first use of every (device, model) */
+    for (int32_t d = 0; d < D; ++d) dev_units[d] = 0;
+    for (int32_t k = 0; k < n_units; ++k) dev_index[k] = dev_units[pdev[order[k].idx]]++;
     for (int32_t i = 0; i < D * M; ++i) next_use[i] = ORC_NO_USE;
     for (int32_t k = n_units - 1; k >= 0; --k) {
       int32_t h = order[k].idx;
       int64_t *nu = &next_use[pdev[h] * M + w->act_model[h]];
       next_after[k] = *nu;
-      *nu = k;
+      *nu = dev_index[k];
     }
 
     /* ---- pool snapshot ---- */
@@ -302,7 +306,7 @@ static int simulate(const orc_window *w, const uint8_t *wf_class, const int8_t *
                 if (e != d && ((res_level[e] >> mm[q]) & 1u)) red = 1;
               const int64_t nu = next_use[d * M + mm[q]];
               key[q][0] = red;
-              key[q][1] = nu == ORC_NO_USE ? ORC_NO_USE : nu - pos;
+              key[q][1] = nu == ORC_NO_USE ? ORC_NO_USE : nu - dev_index[pos];
               key[q][2] = w->load_us[mm[q] * D + d];
               key[q][3] = last[d * M + mm[q]];
             }
@@ -426,7 +430,7 @@ done:
   free(fuse); free(pf); free(member); free(unit_Mx); free(order);
   free(start); free(finish); free(load_start); free(comp); free(free_t); free(used);
   free(peak); free(res); free(reclaimed); free(remaining); free(last);
-  free(res_level); free(next_after); free(next_use);
+  free(res_level); free(dev_units); free(next_after); free(dev_index); free(next_use);
   free_struct(&st);
   return rc;
 }

@@ -60,8 +60,8 @@ typedef struct {
  *   ORC_VICTIM_PAPER -- redundant copies first (the model is resident on
  *     another device when the current topological level starts), then the
  *     largest next-use distance relative to reload cost -- distance = the
- *     number of positions in the resource order until the next unit of the
- *     device that uses the model, infinite without one; the ratio
+ *     number of the device's units, in resource order, from the current one
+ *     to the next one that uses the model, infinite without one; the ratio
  *     distance / load time is infinite when either the distance is infinite
  *     or the load time is 0; finite ratios compare by cross-multiplication --,
  *     then least recently used, then the lower model id.

@@ -89,7 +89,7 @@ MUTANTS = [
     ("paper ratio inverted", "if (a != b) return a > b;", "if (a != b) return a < b;"),
     ("paper order ignores reload cost", "const int64_t a = distx * loady, b = disty * loadx;",
      "const int64_t a = distx, b = disty;"),
-    ("paper order ignores next use", "key[q][1] = nu == ORC_NO_USE ? ORC_NO_USE : nu - pos;",
+    ("paper order ignores next use", "key[q][1] = nu == ORC_NO_USE ? ORC_NO_USE : nu - dev_index[pos];",
      "key[q][1] = 1;"),
     ("redundancy from live residency", "if (e != d && ((res_level[e] >> mm[q]) & 1u)) red = 1;",
      "if (e != d && ((res[e] >> mm[q]) & 1u)) red = 1;"),
