@@ -129,6 +129,8 @@ def main():
                     help="plans checked against the oracle before timing (0 = none)")
     ap.add_argument("--search-mut", type=int, default=2,
                     help="mutations per generated candidate in the search leg (-1 = skip it)")
+    ap.add_argument("--no-paper-order", action="store_true",
+                    help="skip the leg that scores with the paper's reclamation order")
     ap.add_argument("--no-keys", action="store_true",
                     help="skip the ranking-key leg (Eq. 12 keys and their argmin)")
     ap.add_argument("--copy-probe", type=int, default=None, metavar="BYTES",
@@ -310,6 +312,40 @@ def main():
                             "timely prefetches, lifecycle overhead) for the same plans, then "
                             "their lexicographic argmin"}
 
+    # the same plans under the paper's reclamation order (redundant copies,
+    # next use relative to reload cost, least recently used)
+    paper_leg = None
+    if not args.no_paper_order:
+        import dataclasses
+        win_p = dataclasses.replace(win, victim_order=1)
+        ctx.wf_plan_upload_window(win_p)
+        if args.check:
+            import oracle
+            n_chk = min(P, args.check)
+            idx = np.unique(np.linspace(0, P - 1, n_chk).astype(np.int64))
+            ctx.wf_plan_score_batch(dev, prio, flags, P, scores, None, stream)
+            torch.cuda.synchronize()
+            ref = oracle.score(win_p, plans.take(idx), threads=min(16, os.cpu_count() or 1))
+            if pkg.scores_to_numpy(scores, P)[idx].tobytes() != ref.tobytes():
+                print("[bench] paper reclamation order differs from the oracle", file=sys.stderr)
+                sys.exit(1)
+        for _ in range(args.warmup):
+            ctx.wf_plan_score_batch(dev, prio, flags, P, scores, None, stream)
+        torch.cuda.synchronize()
+        pev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(args.steps)]
+        for a, b in pev:
+            a.record(stream)
+            ctx.wf_plan_score_batch(dev, prio, flags, P, scores, None, stream)
+            b.record(stream)
+        torch.cuda.synchronize()
+        p_ms = float(np.mean([a.elapsed_time(b) for a, b in pev]))
+        paper_leg = {"value": round(P / (p_ms * 1e-3), 1), "unit": "plans/s",
+                     "kernel_ms": round(p_ms, 4),
+                     "note": "the same plans scored with the paper's reclamation order "
+                             "(victim_order = 1: a scan over the resident set per reclamation)"}
+        ctx.wf_plan_upload_window(win)
+
     cpu = None
     if not args.no_cpu_baseline:
         import oracle
@@ -350,6 +386,7 @@ def main():
         "cpu_baseline": cpu,
         "search": search,
         "keys": keys_leg,
+        "paper_order": paper_leg,
     }
     print(json.dumps(line))
     ctx.close()

@@ -117,7 +117,22 @@ typedef struct {
   const uint8_t *wf_class;        /* [W] priority class of each workflow for the ranking
                                      key (Eq. 12), 0..WF_MAX_CLASSES-1, class 0 ranked
                                      first; NULL = every workflow in class 0    */
+  int32_t victim_order;           /* WF_VICTIM_REMAINING_LRU (0, step 3 above) or
+                                     WF_VICTIM_PAPER (1, below)                 */
 } wf_window_desc;
+
+/*
+ * Reclamation victim order.  WF_VICTIM_REMAINING_LRU is step 3 above.
+ * WF_VICTIM_PAPER follows Sec. 3.5 (reclamation): among the resident copies
+ * other than the unit's own, first those whose model is resident on another
+ * device as the unit's topological level starts (redundant copies), then the
+ * largest next-use distance relative to reload cost -- distance = the number
+ * of the device's units, in resource order, from the current one to the next
+ * one that uses the model; the ratio distance / load time is infinite when
+ * there is no next use or the load takes 0 us, and finite ratios compare by
+ * cross-multiplication -- then least recently used, then the lower model id.
+ */
+enum { WF_VICTIM_REMAINING_LRU = 0, WF_VICTIM_PAPER = 1 };
 
 /* Per-plan score, 32 bytes.  For a WF_ST_INELIGIBLE plan every other field
  * is 0. */

@@ -22,6 +22,7 @@ WF_ST_INELIGIBLE = 1
 WF_ST_CAPACITY = 2
 WF_MAX_ACT, WF_MAX_MODELS, WF_MAX_DEV, WF_MAX_MUT = 65535, 64, 64, 64
 WF_MAX_CLASSES = 4
+WF_VICTIM_REMAINING_LRU, WF_VICTIM_PAPER = 0, 1
 
 SCORE_DTYPE = np.dtype([
     ("makespan_us", "<i8"), ("p95_us", "<i8"), ("objective", "<f4"),
@@ -64,6 +65,7 @@ class wf_window_desc(ctypes.Structure):
         ("init_resident", ctypes.c_void_p), ("dev_free0_us", ctypes.c_void_p),
         ("w_makespan", ctypes.c_float), ("w_p95", ctypes.c_float),
         ("wf_class", ctypes.c_void_p),
+        ("victim_order", ctypes.c_int32),
     ]
 
 
@@ -143,6 +145,7 @@ class _Desc:
         for k, v in self.keep.items():
             setattr(d, k, None if v is None else v.ctypes.data)
         d.w_makespan, d.w_p95 = win.w_makespan, win.w_p95
+        d.victim_order = int(getattr(win, "victim_order", 0))
         self.desc = d
 
 

@@ -30,6 +30,7 @@ struct HostWindow {
   std::vector<int64_t> arrival, free0;
   std::vector<uint64_t> init_res;
   std::vector<uint8_t> wf_class;  // [W] priority class of the ranking key
+  int32_t victim_order = WF_VICTIM_REMAINING_LRU;
   float w_mk = 1.f, w_p95 = 0.f;
 };
 
@@ -129,9 +130,12 @@ wf_status validate(const wf_window_desc* w, std::string* err, HostWindow* out) {
       if (w->wf_class[f] >= WF_MAX_CLASSES)
         return fail(err, WF_EINVAL, "wf_class[%lld] = %d outside [0, %d)", (long long)f,
                     (int)w->wf_class[f], WF_MAX_CLASSES);
+  if (w->victim_order != WF_VICTIM_REMAINING_LRU && w->victim_order != WF_VICTIM_PAPER)
+    return fail(err, WF_EINVAL, "victim_order = %d is not a WF_VICTIM_* value", (int)w->victim_order);
   if (!out) return WF_OK;
 
   HostWindow& h = *out;
+  h.victim_order = w->victim_order;
   h.wf_class.assign((size_t)W, 0);
   if (w->wf_class) h.wf_class.assign(w->wf_class, w->wf_class + W);
   h.N = (int32_t)N;
@@ -239,8 +243,9 @@ struct Image {
 };
 
 // Per-wave LDS carve-up for G plans; returns the wave's byte size.
-int wave_layout(const HostWindow& h, int G, int tsz, int nwa, bool nibble, bool search,
+int wave_layout(const HostWindow& h, int G, int tsz, int nwa, int qmode, bool search,
                 wfp::WaveOffsets& o) {
+  const bool nibble = qmode > 0, paper = qmode < 0;
   size_t off = 0;
   auto take = [&](size_t n) {
     const size_t at = off;
@@ -269,6 +274,12 @@ int wave_layout(const HostWindow& h, int G, int tsz, int nwa, bool nibble, bool 
   o.rows = o.fin + (int)rows_at;
   o.rows_prio = o.rows + (int)align_up((size_t)G * h.N, 16);
   o.wfm = take((size_t)G * std::max(1, h.W) * tsz);
+  o.nx = o.nxu = o.snap = 0;
+  if (paper) {
+    o.nx = take((size_t)G * h.N * 2);
+    o.nxu = take((size_t)G * h.D * h.M * 2);
+    o.snap = take((size_t)G * h.D * 8);
+  }
   o.bytes = (int)off;
   return o.bytes;
 }
@@ -411,7 +422,9 @@ wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, Image& img, wfp::Sc
   // its initial set, or models whose weights sum to at most its capacity, or
   // (after a load that overflows) the one model just loaded
   sp.nibble = 0;
-  if (M <= 16) {
+  if (h.victim_order == WF_VICTIM_PAPER) {
+    sp.nibble = -1;
+  } else if (M <= 16) {
     std::vector<int32_t> w(h.wmib.begin(), h.wmib.begin() + M);
     std::sort(w.begin(), w.end());
     int qcap = 1;
@@ -442,7 +455,7 @@ wf_status plan_launch(wf_plan_ctx* ctx, const HostWindow& h, bool search, wfp::S
     const int tab_lds = tl ? sp.t.bytes : 0;
     for (int G = gmax; G >= 1; --G) {
       wfp::WaveOffsets o{};
-      const int wb = wave_layout(h, G, tsz, sp.nwa, sp.nibble != 0, search, o);
+      const int wb = wave_layout(h, G, tsz, sp.nwa, sp.nibble, search, o);
       int waves = std::min(8, (lds_blk - tab_lds) / std::max(wb, 1));
       if (waves < 1) continue;
       const int lds_wg = tab_lds + waves * wb;
@@ -469,7 +482,7 @@ wf_status plan_launch(wf_plan_ctx* ctx, const HostWindow& h, bool search, wfp::S
     // per-wave regions in HBM: one plan per device lane group, a bounded grid
     wfp::WaveOffsets o{};
     const int G = gmax;
-    const int64_t wb = wave_layout(h, G, tsz, sp.nwa, sp.nibble != 0, search, o);
+    const int64_t wb = wave_layout(h, G, tsz, sp.nwa, sp.nibble, search, o);
     const int64_t cap_bytes = int64_t(1) << 30;
     const int waves = 4;
     int64_t wgs = std::min<int64_t>((int64_t)ctx->n_cu * 2, cap_bytes / std::max<int64_t>(wb * waves, 1));
@@ -628,7 +641,7 @@ wf_status wf_plan_upload_window(wf_plan_ctx* ctx, const wf_window_desc* w) {
                  "grid=%d tables=%s(%d B) wave=%d B lds/wg=%d reclaim=%s\n",
                  sp.N, sp.W, sp.D, sp.M, sp.n_levels, h.wmax, sp.time64 ? "fp64" : "u32", sp.G,
                  sp.waves, sp.grid, sp.wave_global ? "hbm+scratch" : (sp.tab_in_lds ? "lds" : "hbm"),
-                 sp.t.bytes, sp.wo.bytes, sp.lds_bytes, sp.nibble == 32 ? "queue32" : sp.nibble == 64 ? "queue64" : "scan");
+                 sp.t.bytes, sp.wo.bytes, sp.lds_bytes, sp.nibble == 32 ? "queue32" : sp.nibble == 64 ? "queue64" : sp.nibble < 0 ? "paper-scan" : "scan");
   free_device_window(ctx->dw);
   ctx->dw = dw;
   ctx->host = std::move(h);

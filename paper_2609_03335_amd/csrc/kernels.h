@@ -53,6 +53,10 @@ struct WaveOffsets {
                //                  the order is built
   int rows_prio;
   int wfm;     // time [G][W]      latest finish per workflow
+  int nx;      // u16 [G][N]       paper reclamation order: per slot, the device index of
+               //                  the next unit of the device with the same model
+  int nxu;     // u16 [G*D][M]     paper order: next use of each model (device index)
+  int snap;    // u64 [G][D]       paper order: resident models as the level starts
   int bytes;
 };
 
@@ -72,7 +76,8 @@ struct ScoreParams {
   int lds_bytes;              // dynamic LDS per workgroup
   int grid;                   // workgroups (persistent)
   int time64;                 // 1: fp64 times, 0: uint32 times
-  int nibble;                 // reclamation queue width in bits (32 or 64), 0: scan
+  int nibble;                 // reclamation queue width in bits (32 or 64), 0: scan,
+                              // -1: scan in the paper's reclamation order
   int has_chains;             // 1: some activation satisfies Eq. 3 (fused units possible)
 };
 

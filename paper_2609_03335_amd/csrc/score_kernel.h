@@ -168,6 +168,27 @@ constexpr uint32_t kChain = 1u << 23;
 constexpr uint32_t kLast = 1u << 30;
 constexpr uint32_t kSlow = 1u << 31;
 
+// The paper's reclamation preference (Sec. 3.5): whether copy x is reclaimed
+// before copy y.  red: resident on another device as the level started;
+// nu: device index of the next use (0xffff: none); ld: reload time; lru:
+// last-use stamp (0: never used); k: the current unit's device index.
+// Ratios (nu - k) / ld compare by cross-multiplication; no next use or a
+// free reload is an infinite ratio.
+__device__ __forceinline__ bool paper_victim_before(uint32_t redx, uint32_t nux, uint32_t ldx,
+                                                    uint32_t lrux, uint32_t redy, uint32_t nuy,
+                                                    uint32_t ldy, uint32_t lruy, uint32_t k) {
+  if (redx != redy) return redx > redy;
+  const bool infx = nux == 0xffffu || ldx == 0u;
+  const bool infy = nuy == 0xffffu || ldy == 0u;
+  if (infx != infy) return infx;
+  if (!infx) {
+    const unsigned long long a = (unsigned long long)(nux - k) * ldy;
+    const unsigned long long b = (unsigned long long)(nuy - k) * ldx;
+    if (a != b) return a > b;
+  }
+  return lrux < lruy;
+}
+
 // What the device walk needs about one unit that does not depend on the
 // device's sequential state; it is loaded one unit ahead of its use.
 template <typename TT>
@@ -200,7 +221,11 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   using TB = typename TO::bits_t;
   // reclamation queue: QB bits of 4-bit model ids (QB = 0: no queue, the
   // resident set is scanned instead)
-  constexpr bool NIBBLE = QB != 0;
+  constexpr bool NIBBLE = QB > 0;
+  // QB < 0: the paper's reclamation order (redundant copies, then next use
+  // relative to reload cost, then least recently used) over the scanned
+  // resident set
+  constexpr bool PAPER = QB < 0;
   using QT = std::conditional_t<QB == 32, uint32_t, uint64_t>;
   constexpr QT kOnes = (QT)0x1111111111111111ull, kHigh = (QT)0x8888888888888888ull;
   constexpr int kQBits = (int)sizeof(QT) * 8;
@@ -251,6 +276,9 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   TB* s_fin = reinterpret_cast<TB*>(wl + sp.wo.fin);
   PlanAcc* s_acc = reinterpret_cast<PlanAcc*>(wl + sp.wo.acc);
   uint16_t* s_stamp = reinterpret_cast<uint16_t*>(wl + sp.wo.stamp);
+  uint16_t* s_nx = reinterpret_cast<uint16_t*>(wl + sp.wo.nx);      // paper order only
+  uint16_t* s_nxu = reinterpret_cast<uint16_t*>(wl + sp.wo.nxu);
+  unsigned long long* s_snap = reinterpret_cast<unsigned long long*>(wl + sp.wo.snap);
   TB* s_wfm = reinterpret_cast<TB*>(wl + sp.wo.wfm);
   int8_t* s_rdev = reinterpret_cast<int8_t*>(wl + sp.wo.rows);         // generated candidates
   uint16_t* s_rprio = reinterpret_cast<uint16_t*>(wl + sp.wo.rows_prio);
@@ -594,6 +622,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
     const int64_t pw = p0 + gme;
     const uint32_t* mylast = s_last + (gme * D + d_me) * M;
     uint16_t* mystamp = s_stamp + (gme * D + d_me) * M;
+    uint16_t* mynxu = s_nxu + (gme * D + d_me) * M;  // next use of each model (device index)
     const unsigned long long* mymask = s_mask + (gme * D + d_me) * NWA;
     const uint32_t* myrec = s_rec + gme * N;
     TB* myfin = s_fin + gme * N;
@@ -618,6 +647,30 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
     TT ph_cf = 0;
     HT ph_h = 0;
     uint32_t ph_pn = 0u;
+    // paper order: this unit's index among the device's units, and the
+    // models resident on the plan's other devices as the level starts
+    int kdev = 0;
+    unsigned long long others = 0ull;
+    if (PAPER && act) {
+      // one backward pass over the device's units: for each unit, the index
+      // of the next unit of the device with the same model (0xffff: none);
+      // what remains in mynxu is every model's first use
+      for (int m = 0; m < M; ++m) mynxu[m] = 0xffff;
+      int cnt = 0;
+      for (int j = 0; j < NWA; ++j) cnt += __popcll(mymask[j]);
+      uint16_t* mynx = s_nx + gme * N;
+      for (int j = NWA - 1; j >= 0; --j) {
+        for (unsigned long long bits = mymask[j]; bits;) {
+          const int b = 63 - __clzll(bits);
+          bits &= ~(1ull << b);
+          const int sl = (j << 6) + b;
+          const int m = (int)((myrec[sl] >> 16) & 63u);
+          --cnt;
+          mynx[sl] = mynxu[m];
+          mynxu[m] = (uint16_t)cnt;
+        }
+      }
+    }
     if (act) {
       res = t_res0[d];
       capd = t_cap[d];
@@ -675,6 +728,16 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
           }
         }
         wave_sync();
+      }
+
+      // ---- paper order: the pool's residency as the level starts ----
+      if constexpr (PAPER) {
+        if (act) s_snap[gme * D + d_me] = res;
+        wave_sync();
+        others = 0ull;
+        if (act)
+          for (int e = 0; e < D; ++e)
+            if (e != d_me) others |= s_snap[gme * D + e];
       }
 
       // ---- device lanes walk their units of this level in slot order ----
@@ -818,6 +881,42 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
               Q = (Q & lowm) | ((QT)m << pos) | ((Q & ~lowm) << 4);
               nd += last_use ? 1 : 0;
               ++nq;
+            } else if constexpr (PAPER) {
+              (void)w0;
+              (void)w1;
+              while (used + need > capd) {
+                uint64_t cand = res & ~mbit;
+                if (!cand) break;
+                // the first candidate, then any that the paper's order
+                // reclaims before the current choice (ascending ids: equal
+                // keys keep the lower id)
+                int v = __builtin_ctzll(cand);
+                uint32_t vred = (uint32_t)((others >> v) & 1ull);
+                uint32_t vnu = mynxu[v];
+                uint32_t vld = (uint32_t)lw_d[__umul24((uint32_t)v, (uint32_t)D)].x;
+                uint32_t vlru = mystamp[v];
+                for (cand &= cand - 1; cand; cand &= cand - 1) {
+                  const int m2 = __builtin_ctzll(cand);
+                  const uint32_t red = (uint32_t)((others >> m2) & 1ull);
+                  const uint32_t nu = mynxu[m2];
+                  const uint32_t ld = (uint32_t)lw_d[__umul24((uint32_t)m2, (uint32_t)D)].x;
+                  const uint32_t lru = mystamp[m2];
+                  if (paper_victim_before(red, nu, ld, lru, vred, vnu, vld, vlru, (uint32_t)kdev)) {
+                    v = m2;
+                    vred = red;
+                    vnu = nu;
+                    vld = ld;
+                    vlru = lru;
+                  }
+                }
+                res &= ~(1ull << v);
+                if constexpr (PHI) ph_rec |= 1ull << v;
+                used -= t_wmib[v];
+                ++nev;
+              }
+              mystamp[m] = (uint16_t)seq++;
+              mynxu[m] = s_nx[gme * N + X.slot];
+              ++kdev;
             } else {
               (void)w0;
               (void)w1;
@@ -1069,6 +1168,8 @@ template <typename TT, bool SEARCH, bool PHI>
 hipError_t launch_time(const ScoreParams& sp, const int8_t* dev, const uint16_t* prio,
                        const uint8_t* flags, int64_t n_plans, OutRec<PHI>* out,
                        const wf_plan_sched& s, int has, const SearchArgs& sa, hipStream_t stream) {
+  if (sp.nibble < 0)
+    return launch_place<TT, -1, SEARCH, PHI>(sp, dev, prio, flags, n_plans, out, s, has, sa, stream);
   if (sp.nibble == 32)
     return launch_place<TT, 32, SEARCH, PHI>(sp, dev, prio, flags, n_plans, out, s, has, sa, stream);
   if (sp.nibble == 64)

@@ -115,6 +115,7 @@ BAD = {
     "negative_free0": lambda w: w.dev_free0_us.__setitem__(0, -3),
     "class_out_of_range": lambda w: setattr(w, "wf_class",
                                             np.full(w.n_wf, pkg._lib.WF_MAX_CLASSES, np.uint8)),
+    "victim_order_unknown": lambda w: setattr(w, "victim_order", 2),
 }
 
 
