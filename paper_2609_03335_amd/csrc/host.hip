@@ -266,6 +266,11 @@ int wave_layout(const HostWindow& h, int G, int tsz, int nwa, int qmode, bool se
     o.fin = take(std::max(std::max(fin_bytes, last_bytes), rows_at + rows_bytes));
     o.last = o.fin;
     o.stamp = 0;
+  } else if (paper) {
+    // the paper order keeps no last[] (it is never written)
+    o.fin = take(std::max(fin_bytes, rows_bytes));
+    o.last = o.fin;
+    o.stamp = take((size_t)G * h.D * h.M * 2);
   } else {
     o.fin = take(std::max(fin_bytes, rows_bytes));
     o.last = take(last_bytes);
@@ -450,9 +455,11 @@ wf_status plan_launch(wf_plan_ctx* ctx, const HostWindow& h, bool search, wfp::S
   const int lds_cu = std::min(ctx->lds_per_cu, 160 * 1024);
   const int lds_blk = std::min(ctx->lds_per_block, lds_cu);
   const int gmax = std::max(1, 64 / D);
+  // the paper reclamation order keeps every load time in LDS
+  sp.wg_ld = sp.nibble < 0 ? (int)align_up((size_t)h.M * D * 4, 16) : 0;
   double best = -1.0;
   for (int tl = 1; tl >= 0; --tl) {
-    const int tab_lds = tl ? sp.t.bytes : 0;
+    const int tab_lds = (tl ? sp.t.bytes : 0) + sp.wg_ld;
     for (int G = gmax; G >= 1; --G) {
       wfp::WaveOffsets o{};
       const int wb = wave_layout(h, G, tsz, sp.nwa, sp.nibble, search, o);
@@ -493,7 +500,7 @@ wf_status plan_launch(wf_plan_ctx* ctx, const HostWindow& h, bool search, wfp::S
     sp.waves = waves;
     sp.tab_in_lds = 0;
     sp.wave_global = 1;
-    sp.lds_bytes = 0;
+    sp.lds_bytes = sp.wg_ld;
     sp.grid = (int)wgs;
     sp.wo = o;
   }

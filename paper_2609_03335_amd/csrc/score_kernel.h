@@ -177,16 +177,16 @@ constexpr uint32_t kSlow = 1u << 31;
 __device__ __forceinline__ bool paper_victim_before(uint32_t redx, uint32_t nux, uint32_t ldx,
                                                     uint32_t lrux, uint32_t redy, uint32_t nuy,
                                                     uint32_t ldy, uint32_t lruy, uint32_t k) {
-  if (redx != redy) return redx > redy;
+  // evaluated without branches: each level of the preference decides only
+  // where all earlier levels tie
   const bool infx = nux == 0xffffu || ldx == 0u;
   const bool infy = nuy == 0xffffu || ldy == 0u;
-  if (infx != infy) return infx;
-  if (!infx) {
-    const unsigned long long a = (unsigned long long)(nux - k) * ldy;
-    const unsigned long long b = (unsigned long long)(nuy - k) * ldx;
-    if (a != b) return a > b;
-  }
-  return lrux < lruy;
+  const unsigned long long a = (unsigned long long)(nux - k) * ldy;
+  const unsigned long long b = (unsigned long long)(nuy - k) * ldx;
+  const bool ratio_tie = infx || a == b;  // both infinite, or equal finite ratios
+  const bool by_ratio = infx != infy ? infx : (!ratio_tie && a > b);
+  const bool later = infx != infy || !ratio_tie ? by_ratio : lrux < lruy;
+  return redx != redy ? redx > redy : later;
 }
 
 // What the device walk needs about one unit that does not depend on the
@@ -256,6 +256,15 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   const uint4* t_ud = reinterpret_cast<const uint4*>(tb + sp.t.ud);
   const int2* t_lw = reinterpret_cast<const int2*>(tb + sp.t.lw);
   const int32_t* t_wmib = reinterpret_cast<const int32_t*>(tb + sp.t.wmib);
+  // paper reclamation order: the workgroup's copy of every (model, device)
+  // load time, read per candidate victim
+  uint32_t* wg_ld = reinterpret_cast<uint32_t*>(lds + wave_base);
+  if constexpr (PAPER) {
+    const int2* lw = reinterpret_cast<const int2*>(tb + sp.t.lw);
+    for (int i = tid; i < M * D; i += blockDim.x) wg_ld[i] = (uint32_t)lw[i].x;
+    __syncthreads();
+  }
+  wave_base += sp.wg_ld;
   const int32_t* t_cap = reinterpret_cast<const int32_t*>(tb + sp.t.cap);
   const TB* t_arr = reinterpret_cast<const TB*>(tb + sp.t.arr);
   const unsigned long long* t_res0 = reinterpret_cast<const unsigned long long*>(tb + sp.t.res0);
@@ -341,7 +350,9 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
     } else {
       stage(s_fl, flags_all + p0 * NB, gc * NB, lane);
     }
-    zero_bytes(reinterpret_cast<unsigned char*>(s_last), G * D * M * 4, lane);
+    // last[] (each (device, model)'s last slot) serves the other reclamation
+    // orders only
+    if constexpr (!PAPER) zero_bytes(reinterpret_cast<unsigned char*>(s_last), G * D * M * 4, lane);
     zero_bytes(reinterpret_cast<unsigned char*>(s_mask), G * D * NWA * 8, lane);
     if (lane < G) {
       PlanAcc a0;
@@ -383,7 +394,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
         s_rec[g * N + pr] = (uint32_t)u | (m << 16) | ((fb & 2u) << 21) |
                             (chain ? kChain | kSlow : slow0) | ((uint32_t)d << 24);
         atomicOr(&s_mask[(g * D + d) * NWA + (pr >> 6)], 1ull << (pr & 63));
-        atomicMax(&s_last[(g * D + d) * M + (int)m], (uint32_t)pr + 1u);
+        if constexpr (!PAPER) atomicMax(&s_last[(g * D + d) * M + (int)m], (uint32_t)pr + 1u);
         ++nh;
       }
     };
@@ -512,7 +523,8 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
       unsigned long long* mk = s_mask + g * D * NWA;
       uint32_t* lastp = s_last + g * D * M;
       for (int i = lane; i < D * NWA; i += 64) mk[i] = 0ull;
-      for (int i = lane; i < D * M; i += 64) lastp[i] = 0u;
+      if constexpr (!PAPER)
+        for (int i = lane; i < D * M; i += 64) lastp[i] = 0u;
       wave_sync();
       for (int u = lane; u < N; u += 64) {
         const uint32_t a = t_act[u];
@@ -535,7 +547,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
         rec[slot] = (uint32_t)u | ((a & 63u) << 16) | ((uint32_t)((fb >> 1) & 1) << 22) | chain |
                     (chain ? kSlow : slow0) | ((uint32_t)d << 24);
         atomicOr(&mk[d * NWA + (slot >> 6)], 1ull << (slot & 63));
-        atomicMax(&lastp[d * M + (int)(a & 63u)], (uint32_t)slot + 1u);
+        if constexpr (!PAPER) atomicMax(&lastp[d * M + (int)(a & 63u)], (uint32_t)slot + 1u);
       }
       wave_sync();
     }
@@ -893,13 +905,13 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
                 int v = __builtin_ctzll(cand);
                 uint32_t vred = (uint32_t)((others >> v) & 1ull);
                 uint32_t vnu = mynxu[v];
-                uint32_t vld = (uint32_t)lw_d[__umul24((uint32_t)v, (uint32_t)D)].x;
+                uint32_t vld = wg_ld[__umul24((uint32_t)v, (uint32_t)D) + (uint32_t)d];
                 uint32_t vlru = mystamp[v];
                 for (cand &= cand - 1; cand; cand &= cand - 1) {
                   const int m2 = __builtin_ctzll(cand);
                   const uint32_t red = (uint32_t)((others >> m2) & 1ull);
                   const uint32_t nu = mynxu[m2];
-                  const uint32_t ld = (uint32_t)lw_d[__umul24((uint32_t)m2, (uint32_t)D)].x;
+                  const uint32_t ld = wg_ld[__umul24((uint32_t)m2, (uint32_t)D) + (uint32_t)d];
                   const uint32_t lru = mystamp[m2];
                   if (paper_victim_before(red, nu, ld, lru, vred, vnu, vld, vlru, (uint32_t)kdev)) {
                     v = m2;
