@@ -23,6 +23,7 @@ INELIGIBLE = 1
 CAPACITY = 2
 VICTIM_REMAINING_LRU = 0
 VICTIM_PAPER = 1
+MAX_BATCH = 4
 
 SCORE_DTYPE = np.dtype([
     ("makespan_us", "<i8"), ("p95_us", "<i8"), ("objective", "<f4"),
@@ -62,6 +63,7 @@ class _Win(ctypes.Structure):
         ("init_resident", ctypes.c_void_p), ("dev_free0_us", ctypes.c_void_p),
         ("w_makespan", ctypes.c_float), ("w_p95", ctypes.c_float),
         ("victim_order", ctypes.c_int32),
+        ("dev_batch", ctypes.c_void_p),
     ]
 
 
@@ -114,6 +116,8 @@ class _WinHolder:
             "dev_cap_mib": _c(win.dev_cap_mib, np.int32), "model_mib": _c(win.model_mib, np.int32),
             "load_us": _c(win.load_us, np.int32), "init_resident": _c(win.init_resident, np.uint64),
             "dev_free0_us": None if win.dev_free0_us is None else _c(win.dev_free0_us, np.int64),
+            "dev_batch": (None if getattr(win, "dev_batch", None) is None
+                          else _c(win.dev_batch, np.int32)),
         }
         if self.keep["pred_idx"].size == 0:
             self.keep["pred_idx"] = np.zeros(1, dtype=np.int32)

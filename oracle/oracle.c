@@ -157,6 +157,9 @@ static int simulate(const orc_window *w, const uint8_t *wf_class, const int8_t *
   if (w->victim_order != ORC_VICTIM_REMAINING_LRU && w->victim_order != ORC_VICTIM_PAPER)
     return ORC_ERR_VICTIM;
   const int paper = w->victim_order == ORC_VICTIM_PAPER;
+  if (w->dev_batch)
+    for (int32_t d = 0; d < w->n_dev; ++d)
+      if (w->dev_batch[d] < 1 || w->dev_batch[d] > ORC_MAX_BATCH) return ORC_ERR_BATCH;
   orc_struct st;
   int rc = build_struct(w, &st);
   if (rc) return rc;
@@ -169,7 +172,13 @@ static int simulate(const orc_window *w, const uint8_t *wf_class, const int8_t *
   int64_t *start = (int64_t *)malloc(n * 8), *finish = (int64_t *)malloc(n * 8),
           *load_start = (int64_t *)malloc(n * 8);
   int64_t *comp = (int64_t *)malloc((size_t)(W > 0 ? W : 1) * 8);
-  int64_t *free_t = (int64_t *)malloc((size_t)D * 8), *used = (int64_t *)malloc((size_t)D * 8),
+  /* per device and batch slot: free time, and the running unit's finish,
+   * memory and model */
+  const size_t ns = (size_t)D * ORC_MAX_BATCH;
+  int64_t *slot_free = (int64_t *)malloc(ns * 8), *run_fin = (int64_t *)malloc(ns * 8),
+          *run_mem = (int64_t *)malloc(ns * 8), *run_model = (int64_t *)malloc(ns * 8);
+  int64_t *dispatched = (int64_t *)malloc((size_t)D * 8); /* last first-action time */
+  int64_t *used = (int64_t *)malloc((size_t)D * 8),
           *peak = (int64_t *)malloc((size_t)D * 8);
   uint64_t *res = (uint64_t *)malloc((size_t)D * 8);
   uint64_t *reclaimed = (uint64_t *)malloc((size_t)D * 8);
@@ -179,7 +188,7 @@ static int simulate(const orc_window *w, const uint8_t *wf_class, const int8_t *
   int64_t *next_use = (int64_t *)malloc((size_t)D * M * 8);
   int64_t *remaining = (int64_t *)malloc((size_t)D * M * 8), *last = (int64_t *)malloc((size_t)D * M * 8);
   if (!fuse || !pf || !member || !unit_Mx || !order || !start || !finish ||
-      !load_start || !comp || !free_t || !used || !peak || !res || !reclaimed || !remaining ||
+      !load_start || !comp || !slot_free || !run_fin || !run_mem || !run_model || !dispatched || !used || !peak || !res || !reclaimed || !remaining ||
       !last || !res_level || !dev_units || !next_after || !dev_index || !next_use) {
     rc = ORC_ERR_NOMEM;
     goto done;
@@ -253,7 +262,13 @@ static int simulate(const orc_window *w, const uint8_t *wf_class, const int8_t *
 
     /* ---- pool snapshot ---- */
     for (int32_t d = 0; d < D; ++d) {
-      free_t[d] = w->dev_free0_us ? w->dev_free0_us[d] : 0;
+      dispatched[d] = w->dev_free0_us ? w->dev_free0_us[d] : 0;
+      for (int32_t k = 0; k < ORC_MAX_BATCH; ++k) {
+        slot_free[d * ORC_MAX_BATCH + k] = w->dev_free0_us ? w->dev_free0_us[d] : 0;
+        run_fin[d * ORC_MAX_BATCH + k] = slot_free[d * ORC_MAX_BATCH + k];
+        run_mem[d * ORC_MAX_BATCH + k] = 0;
+        run_model[d * ORC_MAX_BATCH + k] = -1;
+      }
       res[d] = w->init_resident[d];
       used[d] = 0;
       for (int32_t m = 0; m < M; ++m)
@@ -284,11 +299,36 @@ static int simulate(const orc_window *w, const uint8_t *wf_class, const int8_t *
       for (int32_t k = w->pred_off[h]; k < w->pred_off[h + 1]; ++k)
         r = max64(r, finish[w->pred_idx[k]]);
 
-      /* lifecycle (Eq. 5) with reclamation and the cumulative check (Eq. 11) */
+      /* the device's slot that frees first (batch limit B; B = 1: the device) */
+      const int32_t B = w->dev_batch ? w->dev_batch[d] : 1;
+      int64_t *sf = &slot_free[d * ORC_MAX_BATCH];
+      int32_t ks = 0;
+      for (int32_t k = 1; k < B; ++k)
+        if (sf[k] < sf[ks]) ks = k;
+      const int64_t free_before = sf[ks];
+
+      /* lifecycle (Eq. 5) with reclamation and the cumulative check (Eq. 11)
+       * at the first action's time t: a load waits for the slot and starts
+       * at the unit's release, or at the workflow's arrival when prefetched;
+       * units still running at t hold their memory and lease their model */
       int miss = !((res[d] >> m) & 1u);
       int64_t need = (miss ? (int64_t)w->model_mib[m] : 0) + Mx;
-      while (used[d] + need > w->dev_cap_mib[d]) {
-        uint64_t cand = res[d] & ~(1ull << m);
+      int64_t t = max64(max64(miss && pf[h] ? w->wf_arrival_us[wf] : r, free_before), dispatched[d]);
+      int64_t run_act = 0;
+      uint64_t leased = 0;
+      for (;;) {
+        int64_t next_fin = INT64_MAX;
+        run_act = 0;
+        leased = 0;
+        for (int32_t k = 0; k < B; ++k) {
+          const int32_t q = d * ORC_MAX_BATCH + k;
+          if (run_fin[q] <= t) continue;
+          run_act += run_mem[q];
+          leased |= 1ull << run_model[q];
+          if (run_fin[q] < next_fin) next_fin = run_fin[q];
+        }
+      while (used[d] + run_act + need > w->dev_cap_mib[d]) {
+        uint64_t cand = res[d] & ~(1ull << m) & ~leased;
         if (!cand) break;
         int32_t victim = -1;
         for (int32_t m2 = 0; m2 < M; ++m2) {
@@ -327,19 +367,22 @@ static int simulate(const orc_window *w, const uint8_t *wf_class, const int8_t *
         n_evicts += 1;
         reclaimed[d] |= 1ull << victim;
       }
-      const int fits = !(used[d] + need > w->dev_cap_mib[d]);
+        /* fits, or nothing left to wait for */
+        if (!(used[d] + run_act + need > w->dev_cap_mib[d]) || next_fin == INT64_MAX) break;
+        t = next_fin;
+      }
+      const int fits = !(used[d] + run_act + need > w->dev_cap_mib[d]);
       if (!fits) sc.status |= ORC_CAPACITY;
 
       /* ready work (F_t): no predecessor, and the workflow has arrived by
        * the window time 0 */
       const int ready = w->pred_off[h] == w->pred_off[h + 1] && w->wf_arrival_us[wf] <= 0;
-      const int64_t free_before = free_t[d];
 
       /* timeline (Eq. 7): a load waits for the device; it starts at the
        * unit's release, or at the workflow's arrival when prefetched */
       int64_t s;
       if (miss) {
-        int64_t ls = max64(pf[h] ? w->wf_arrival_us[wf] : r, free_t[d]);
+        int64_t ls = t;
         int64_t le = ls + w->load_us[m * D + d];
         res[d] |= 1ull << m;
         used[d] += w->model_mib[m];
@@ -354,9 +397,9 @@ static int simulate(const orc_window *w, const uint8_t *wf_class, const int8_t *
         if (ready) h_life += s - max64(r, free_before);
       } else {
         load_start[h] = -1;
-        s = max64(r, free_t[d]);
+        s = t;
       }
-      if (used[d] + Mx > peak[d]) peak[d] = used[d] + Mx;
+      if (used[d] + run_act + Mx > peak[d]) peak[d] = used[d] + run_act + Mx;
 
       /* the unit's activations run back-to-back under one grant (Eq. 4) */
       int32_t v = h;
@@ -369,7 +412,11 @@ static int simulate(const orc_window *w, const uint8_t *wf_class, const int8_t *
         if (c >= 0 && member[c]) v = c;
         else break;
       }
-      free_t[d] = s;
+      sf[ks] = s;
+      dispatched[d] = t;
+      run_fin[d * ORC_MAX_BATCH + ks] = s;
+      run_mem[d * ORC_MAX_BATCH + ks] = Mx;
+      run_model[d * ORC_MAX_BATCH + ks] = m;
       last[d * M + m] = pos;
       next_use[d * M + m] = next_after[pos];
       if (ready && fits) {
@@ -428,7 +475,8 @@ static int simulate(const orc_window *w, const uint8_t *wf_class, const int8_t *
 
 done:
   free(fuse); free(pf); free(member); free(unit_Mx); free(order);
-  free(start); free(finish); free(load_start); free(comp); free(free_t); free(used);
+  free(start); free(finish); free(load_start); free(comp); free(slot_free); free(run_fin);
+  free(run_mem); free(run_model); free(dispatched); free(used);
   free(peak); free(res); free(reclaimed); free(remaining); free(last);
   free(res_level); free(dev_units); free(next_after); free(dev_index); free(next_use);
   free_struct(&st);

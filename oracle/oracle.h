@@ -49,7 +49,28 @@ typedef struct {
   const int64_t *dev_free0_us;  /* [n_dev] busy-until, or NULL for all 0      */
   float w_makespan, w_p95;
   int32_t victim_order;         /* ORC_VICTIM_REMAINING_LRU or ORC_VICTIM_PAPER */
+  const int32_t *dev_batch;     /* [n_dev] batch limit 1..ORC_MAX_BATCH, NULL = all 1 */
 } orc_window;
+
+/*
+ * Batch limit (Eq. 11 and the replica batch limit B_q after it; Sec. 4,
+ * continuous batching).  A device with batch limit B runs up to B units at
+ * once, dispatched from its queue in resource order.  A unit takes the
+ * device's slot that frees first (lowest slot on ties); its first action --
+ * the load when its model is not resident, else the unit itself -- begins at
+ *   t = max(release, or the workflow arrival for a prefetched load; the
+ *           slot's free time; the previous unit's first action).
+ * At t the device must hold its resident weights, the memory of every unit
+ * still running at t (finish > t), the load and the unit's own memory.  Only
+ * copies whose model no running unit uses (lease-free) may be reclaimed, in
+ * the window's victim order.  If it still does not fit, t moves to the next
+ * finish of a running unit and the check repeats; with no unit running the
+ * plan is flagged ORC_CAPACITY and the unit proceeds.  A load ends L later
+ * and the unit starts at max(release, load end); otherwise it starts at t.
+ * Peak memory is taken at t.  With B = 1 this is exactly the one-unit device
+ * of the semantics above.
+ */
+enum { ORC_MAX_BATCH = 4 };
 
 /*
  * Reclamation victim order (Sec. 3.5, reclamation), among the resident
@@ -89,7 +110,8 @@ enum {
   ORC_ERR_EMPTY_WF = 5,   /* a workflow without activations                    */
   ORC_ERR_NOMEM = 6,
   ORC_ERR_CLASS = 7,      /* a workflow class outside 0 .. ORC_MAX_CLASSES-1    */
-  ORC_ERR_VICTIM = 8      /* victim_order is not one of ORC_VICTIM_*           */
+  ORC_ERR_VICTIM = 8,     /* victim_order is not one of ORC_VICTIM_*           */
+  ORC_ERR_BATCH = 9       /* a batch limit outside 1 .. ORC_MAX_BATCH          */
 };
 
 /*

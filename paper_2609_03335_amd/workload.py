@@ -68,6 +68,9 @@ class Window:
     # recently used; 1 = the paper's (redundant copies, then next use
     # relative to reload cost, then least recently used)
     victim_order: int = 0
+    # int32[D] batch limit of each device (units it runs at once, 1..4);
+    # None = 1 everywhere
+    dev_batch: Optional[np.ndarray] = None
 
     def arrays(self):
         return {f.name: getattr(self, f.name) for f in dataclasses.fields(self)}

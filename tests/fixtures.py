@@ -42,6 +42,9 @@ def load_golden(name):
         load_us=np.array([m["load_us"] for m in spec["models"]], np.int32).reshape(-1),
         init_resident=np.zeros(D, np.uint64), dev_free0_us=np.zeros(D, np.int64),
         w_makespan=1.0, w_p95=0.5, name=name)
+    batch = [d.get("batch", 1) for d in spec["devices"]]
+    if any(b != 1 for b in batch):
+        win.dev_batch = np.array(batch, np.int32)
     for dname, mnames in spec.get("init_resident", {}).items():
         bits = 0
         for mn in mnames:

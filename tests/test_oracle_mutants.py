@@ -17,6 +17,7 @@ import test_oracle_properties as t_prop
 import test_oracle_search as t_search
 import test_oracle_phi as t_phi
 import test_oracle_victim as t_vic
+import test_oracle_batch as t_batch
 
 # (name, original fragment, planted mistake)
 MUTANTS = [
@@ -36,9 +37,12 @@ MUTANTS = [
     ("victim prefers live copies", "if (alive2 < aliveV) victim = m2;", "if (alive2 > aliveV) victim = m2;"),
     ("victim most recently used", "} else if (last[d * M + m2] < last[d * M + victim]) {",
      "} else if (last[d * M + m2] > last[d * M + victim]) {"),
-    ("prefetch ignored", "pf[h] ? w->wf_arrival_us[wf] : r", "r"),
-    ("peak without activation memory", "if (used[d] + Mx > peak[d]) peak[d] = used[d] + Mx;",
-     "if (used[d] > peak[d]) peak[d] = used[d];"),
+    ("prefetch ignored",
+     "int64_t t = max64(max64(miss && pf[h] ? w->wf_arrival_us[wf] : r, free_before), dispatched[d]);",
+     "int64_t t = max64(max64(r, free_before), dispatched[d]);"),
+    ("peak without activation memory",
+     "if (used[d] + run_act + Mx > peak[d]) peak[d] = used[d] + run_act + Mx;",
+     "if (used[d] + run_act > peak[d]) peak[d] = used[d] + run_act;"),
     ("start ignores release after load", "s = max64(r, le);", "s = le;"),
     ("p95 rank rounded", "(95 * W + 99) / 100", "(95 * W + 50) / 100"),
     ("priority ignored", "if (x->prio != y->prio) return x->prio < y->prio ? -1 : 1;", ""),
@@ -49,23 +53,24 @@ MUTANTS = [
      "finish[v] = s + w->lat_us[(int64_t)v * D + (pdev[v] >= 0 && pdev[v] < D ? pdev[v] : d)];"),
     ("makespan from time zero", "sc.makespan_us = max_fin - min_arr;", "sc.makespan_us = max_fin;"),
     ("load table transposed", "w->load_us[m * D + d]", "w->load_us[(d * M + m) % (M * D)]"),
-    ("capacity check inclusive", "const int fits = !(used[d] + need > w->dev_cap_mib[d]);",
-     "const int fits = !(used[d] + need >= w->dev_cap_mib[d]);"),
+    ("capacity check inclusive", "const int fits = !(used[d] + run_act + need > w->dev_cap_mib[d]);",
+     "const int fits = !(used[d] + run_act + need >= w->dev_cap_mib[d]);"),
     ("eviction ignores activation memory",
      "int64_t need = (miss ? (int64_t)w->model_mib[m] : 0) + Mx;",
      "int64_t need = (miss ? (int64_t)w->model_mib[m] : 0);"),
     ("objective weight swapped", "float y = w->w_p95 * b;", "float y = w->w_makespan * b;"),
-    ("hit ignores busy device", "s = max64(r, free_t[d]);", "s = r;"),
+    ("hit ignores busy device",
+     "int64_t t = max64(max64(miss && pf[h] ? w->wf_arrival_us[wf] : r, free_before), dispatched[d]);",
+     "int64_t t = miss ? max64(max64(pf[h] ? w->wf_arrival_us[wf] : r, free_before), dispatched[d]) : r;"),
     ("loads double counted", "n_loads += 1;", "n_loads += 2;"),
-    ("evicts one too many", "while (used[d] + need > w->dev_cap_mib[d]) {",
-     "while (used[d] + need + 1 > w->dev_cap_mib[d]) {"),
+    ("evicts one too many", "while (used[d] + run_act + need > w->dev_cap_mib[d]) {",
+     "while (used[d] + run_act + need + 1 > w->dev_cap_mib[d]) {"),
     ("snapshot memory ignored", "if ((res[d] >> m) & 1u) used[d] += w->model_mib[m];",
      "if ((res[d] >> m) & 1u) used[d] += 0;"),
-    ("device free after head only", "free_t[d] = s;", "free_t[d] = finish[h];"),
+    ("device free after head only", "sf[ks] = s;", "sf[ks] = finish[h];"),
     ("completion from first arrival", "comp[wf] -= w->wf_arrival_us[wf];", "comp[wf] -= min_arr;"),
     ("headroom maximum", "< headroom) headroom", "> headroom) headroom"),
-    ("load waits for release when prefetched", "int64_t ls = max64(pf[h] ? w->wf_arrival_us[wf] : r, free_t[d]);",
-     "int64_t ls = max64(r, free_t[d]);"),
+    ("load ignores the slot", "int64_t ls = t;", "int64_t ls = miss && pf[h] ? w->wf_arrival_us[wf] : r;"),
     ("pred finish ignored", "r = max64(r, finish[w->pred_idx[k]]);", "r = max64(r, start[w->pred_idx[k]]);"),
     # ranking key (Eq. 12)
     ("ready ignores arrival", "w->pred_off[h] == w->pred_off[h + 1] && w->wf_arrival_us[wf] <= 0",
@@ -95,6 +100,12 @@ MUTANTS = [
      "if (e != d && ((res[e] >> mm[q]) & 1u)) red = 1;"),
     ("next use not advanced", "next_use[d * M + m] = next_after[pos];", ""),
     ("paper order most recently used", "return lastx < lasty;", "return lastx > lasty;"),
+    # batch limit (Eq. 11, replica batch limit)
+    ("running units hold no memory", "run_act += run_mem[q];", ""),
+    ("running units lease nothing", "leased |= 1ull << run_model[q];", ""),
+    ("no wait for running units", "|| next_fin == INT64_MAX) break;", "|| 1) break;"),
+    ("slot that frees last", "if (sf[k] < sf[ks]) ks = k;", "if (sf[k] > sf[ks]) ks = k;"),
+    ("queue overtaking", "dispatched[d] = t;", ""),
 ]
 
 
@@ -126,6 +137,9 @@ def _pin_checks():
                for n in ("victim_order", "victim_order_chain", "victim_order_snapshot",
                          "victim_order_ties")]
     checks += [lambda s=s: t_vic.test_paper_order_is_belady_optimal_on_one_device(s) for s in range(40)]
+    checks += [lambda n=n: t_batch.test_worked_examples(n) for n in ("batch_memory", "batch_lease")]
+    checks += [lambda s=s: t_batch.test_contention_free_longest_path(s) for s in (0, 1, 2, 3, 5, 6)]
+    checks += [lambda s=s: t_batch.test_schedule_invariants(s) for s in range(8)]
     return checks
 
 
