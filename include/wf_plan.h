@@ -84,6 +84,7 @@ typedef enum {
                                       time then stays below 2^53 (exact in fp64) */
 #define WF_MAX_MUT 64              /* mutations per generated candidate        */
 #define WF_MAX_CLASSES 4           /* priority classes of the ranking key      */
+#define WF_MAX_BATCH 4             /* batch limit of a device                  */
 
 /* Plan status bits; a plan is feasible iff status == 0. */
 enum { WF_ST_INELIGIBLE = 1u, WF_ST_CAPACITY = 2u };
@@ -119,7 +120,27 @@ typedef struct {
                                      first; NULL = every workflow in class 0    */
   int32_t victim_order;           /* WF_VICTIM_REMAINING_LRU (0, step 3 above) or
                                      WF_VICTIM_PAPER (1, below)                 */
+  const int32_t *dev_batch;       /* [D] batch limit 1..WF_MAX_BATCH (below), or NULL
+                                     for 1 everywhere                           */
 } wf_window_desc;
+
+/*
+ * Batch limits (Eq. 11 and the replica batch limit B_q after it; Sec. 4,
+ * continuous batching).  A device with batch limit B runs up to B units at
+ * once, dispatched from its queue in resource order.  A unit takes the
+ * device's slot that frees first (lowest slot on ties); its first action --
+ * the load when its model is not resident, else the unit itself -- begins at
+ *   t = max(release, or the workflow arrival for a prefetched load; the
+ *           slot's free time; the previous unit's first action).
+ * At t the device must hold its resident weights, the memory of every unit
+ * still running at t (finish > t), the load and the unit's own memory.  Only
+ * copies whose model no running unit uses (lease-free) may be reclaimed, in
+ * the window's victim order.  If it still does not fit, t moves to the next
+ * finish of a running unit and the check repeats; with no unit running the
+ * plan is flagged WF_ST_CAPACITY and the unit proceeds.  A load ends L later
+ * and the unit starts at max(release, load end); otherwise it starts at t.
+ * Peak memory is taken at t.  B = 1 is the one-unit device of step 4.
+ */
 
 /*
  * Reclamation victim order.  WF_VICTIM_REMAINING_LRU is step 3 above.

@@ -23,6 +23,7 @@ WF_ST_CAPACITY = 2
 WF_MAX_ACT, WF_MAX_MODELS, WF_MAX_DEV, WF_MAX_MUT = 65535, 64, 64, 64
 WF_MAX_CLASSES = 4
 WF_VICTIM_REMAINING_LRU, WF_VICTIM_PAPER = 0, 1
+WF_MAX_BATCH = 4
 
 SCORE_DTYPE = np.dtype([
     ("makespan_us", "<i8"), ("p95_us", "<i8"), ("objective", "<f4"),
@@ -66,6 +67,7 @@ class wf_window_desc(ctypes.Structure):
         ("w_makespan", ctypes.c_float), ("w_p95", ctypes.c_float),
         ("wf_class", ctypes.c_void_p),
         ("victim_order", ctypes.c_int32),
+        ("dev_batch", ctypes.c_void_p),
     ]
 
 
@@ -140,6 +142,8 @@ class _Desc:
         self.keep["dev_free0_us"] = None if free0 is None else c(free0, np.int64)
         cls = getattr(win, "wf_class", None)
         self.keep["wf_class"] = None if cls is None else c(cls, np.uint8)
+        bat = getattr(win, "dev_batch", None)
+        self.keep["dev_batch"] = None if bat is None else c(bat, np.int32)
         d = wf_window_desc()
         d.n_act, d.n_wf, d.n_models, d.n_dev = win.n_act, win.n_wf, win.n_models, win.n_dev
         for k, v in self.keep.items():

@@ -31,6 +31,7 @@ struct HostWindow {
   std::vector<uint64_t> init_res;
   std::vector<uint8_t> wf_class;  // [W] priority class of the ranking key
   int32_t victim_order = WF_VICTIM_REMAINING_LRU;
+  std::vector<int32_t> batch;  // [D] batch limit
   float w_mk = 1.f, w_p95 = 0.f;
 };
 
@@ -132,10 +133,17 @@ wf_status validate(const wf_window_desc* w, std::string* err, HostWindow* out) {
                     (int)w->wf_class[f], WF_MAX_CLASSES);
   if (w->victim_order != WF_VICTIM_REMAINING_LRU && w->victim_order != WF_VICTIM_PAPER)
     return fail(err, WF_EINVAL, "victim_order = %d is not a WF_VICTIM_* value", (int)w->victim_order);
+  if (w->dev_batch)
+    for (int64_t d = 0; d < D; ++d)
+      if (w->dev_batch[d] < 1 || w->dev_batch[d] > WF_MAX_BATCH)
+        return fail(err, WF_EINVAL, "dev_batch[%lld] = %d outside [1, %d]", (long long)d,
+                    (int)w->dev_batch[d], WF_MAX_BATCH);
   if (!out) return WF_OK;
 
   HostWindow& h = *out;
   h.victim_order = w->victim_order;
+  h.batch.assign((size_t)D, 1);
+  if (w->dev_batch) h.batch.assign(w->dev_batch, w->dev_batch + D);
   h.wf_class.assign((size_t)W, 0);
   if (w->wf_class) h.wf_class.assign(w->wf_class, w->wf_class + W);
   h.N = (int32_t)N;
@@ -245,7 +253,7 @@ struct Image {
 // Per-wave LDS carve-up for G plans; returns the wave's byte size.
 int wave_layout(const HostWindow& h, int G, int tsz, int nwa, int qmode, bool search,
                 wfp::WaveOffsets& o) {
-  const bool nibble = qmode > 0, paper = qmode < 0;
+  const bool nibble = qmode > 0, paper = qmode == -1 || qmode == -3;
   size_t off = 0;
   auto take = [&](size_t n) {
     const size_t at = off;
@@ -390,6 +398,7 @@ wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, Image& img, wfp::Sc
     for (int32_t d = 0; d < D; ++d)
       if (h.lat[(size_t)i * D + d] >= 0) elig[i] |= uint64_t(1) << d;
   t.elig = img.put(elig.data(), elig.size() * 8);
+  t.batch = img.put(h.batch.data(), h.batch.size() * 4);
   t.cap = img.put(h.cap.data(), h.cap.size() * 4);
   t.arr = img.put(arr.data(), arr.size());
   t.res0 = img.put(h.init_res.data(), h.init_res.size() * 8);
@@ -427,7 +436,10 @@ wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, Image& img, wfp::Sc
   // its initial set, or models whose weights sum to at most its capacity, or
   // (after a load that overflows) the one model just loaded
   sp.nibble = 0;
-  if (h.victim_order == WF_VICTIM_PAPER) {
+  const bool batched = std::any_of(h.batch.begin(), h.batch.end(), [](int32_t b) { return b > 1; });
+  if (batched) {
+    sp.nibble = h.victim_order == WF_VICTIM_PAPER ? -3 : -2;
+  } else if (h.victim_order == WF_VICTIM_PAPER) {
     sp.nibble = -1;
   } else if (M <= 16) {
     std::vector<int32_t> w(h.wmib.begin(), h.wmib.begin() + M);
@@ -456,7 +468,7 @@ wf_status plan_launch(wf_plan_ctx* ctx, const HostWindow& h, bool search, wfp::S
   const int lds_blk = std::min(ctx->lds_per_block, lds_cu);
   const int gmax = std::max(1, 64 / D);
   // the paper reclamation order keeps every load time in LDS
-  sp.wg_ld = sp.nibble < 0 ? (int)align_up((size_t)h.M * D * 4, 16) : 0;
+  sp.wg_ld = (sp.nibble == -1 || sp.nibble == -3) ? (int)align_up((size_t)h.M * D * 4, 16) : 0;
   double best = -1.0;
   for (int tl = 1; tl >= 0; --tl) {
     const int tab_lds = (tl ? sp.t.bytes : 0) + sp.wg_ld;
@@ -648,7 +660,8 @@ wf_status wf_plan_upload_window(wf_plan_ctx* ctx, const wf_window_desc* w) {
                  "grid=%d tables=%s(%d B) wave=%d B lds/wg=%d reclaim=%s\n",
                  sp.N, sp.W, sp.D, sp.M, sp.n_levels, h.wmax, sp.time64 ? "fp64" : "u32", sp.G,
                  sp.waves, sp.grid, sp.wave_global ? "hbm+scratch" : (sp.tab_in_lds ? "lds" : "hbm"),
-                 sp.t.bytes, sp.wo.bytes, sp.lds_bytes, sp.nibble == 32 ? "queue32" : sp.nibble == 64 ? "queue64" : sp.nibble < 0 ? "paper-scan" : "scan");
+                 sp.t.bytes, sp.wo.bytes, sp.lds_bytes, sp.nibble == 32 ? "queue32" : sp.nibble == 64 ? "queue64" : sp.nibble == -1 ? "paper-scan" :
+                 sp.nibble == -2 ? "batch-scan" : sp.nibble == -3 ? "batch-paper-scan" : "scan");
   free_device_window(ctx->dw);
   ctx->dw = dw;
   ctx->host = std::move(h);

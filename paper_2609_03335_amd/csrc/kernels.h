@@ -9,6 +9,8 @@
 
 namespace wfp {
 
+constexpr int kMaxBatch = WF_MAX_BATCH;  // slots per device in the batch-limit modes
+
 // Byte offsets of the window tables inside the table image.  The host builds
 // the image once per window; the scoring kernel copies it into LDS (or reads
 // it from HBM when it is too large) and uses the same offsets either way.
@@ -33,6 +35,7 @@ struct TabOffsets {
   int free0;   // time [D]   initial busy-until relative to the window origin
   int sink;    // u32 [S]    activations without successor in their workflow: index | workflow << 16
   int elig;    // u64 [N]    devices d with lat[i][d] >= 0
+  int batch;   // i32 [D]    batch limit (units a device runs at once)
   int bytes;
 };
 
@@ -80,7 +83,8 @@ struct ScoreParams {
   int grid;                   // workgroups (persistent)
   int time64;                 // 1: fp64 times, 0: uint32 times
   int nibble;                 // reclamation queue width in bits (32 or 64), 0: scan,
-                              // -1: scan in the paper's reclamation order
+                              // -1: scan in the paper's reclamation order; -2 / -3: the
+                              // same two scans with per-device batch limits
   int has_chains;             // 1: some activation satisfies Eq. 3 (fused units possible)
 };
 

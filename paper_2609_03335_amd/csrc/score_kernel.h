@@ -222,10 +222,12 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   // reclamation queue: QB bits of 4-bit model ids (QB = 0: no queue, the
   // resident set is scanned instead)
   constexpr bool NIBBLE = QB > 0;
-  // QB < 0: the paper's reclamation order (redundant copies, then next use
-  // relative to reload cost, then least recently used) over the scanned
-  // resident set
-  constexpr bool PAPER = QB < 0;
+  // QB = -1, -3: the paper's reclamation order (redundant copies, then next
+  // use relative to reload cost, then least recently used) over the scanned
+  // resident set; QB = -2, -3: devices with batch limits (several units at
+  // once, each in one of up to kMaxBatch slots)
+  constexpr bool PAPER = QB == -1 || QB == -3;
+  constexpr bool BATCH = QB <= -2;
   using QT = std::conditional_t<QB == 32, uint32_t, uint64_t>;
   constexpr QT kOnes = (QT)0x1111111111111111ull, kHigh = (QT)0x8888888888888888ull;
   constexpr int kQBits = (int)sizeof(QT) * 8;
@@ -271,6 +273,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   const TB* t_free0 = reinterpret_cast<const TB*>(tb + sp.t.free0);
   const uint32_t* t_sink = reinterpret_cast<const uint32_t*>(tb + sp.t.sink);
   const unsigned long long* t_elig = reinterpret_cast<const unsigned long long*>(tb + sp.t.elig);
+  const int32_t* t_batch = reinterpret_cast<const int32_t*>(tb + sp.t.batch);
 
   // ---- this wave's region (LDS, or HBM scratch for very large windows) ----
   unsigned char* wl;
@@ -663,6 +666,18 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
     // models resident on the plan's other devices as the level starts
     int kdev = 0;
     unsigned long long others = 0ull;
+    // batch limits: per slot the free time, and the running unit's finish,
+    // memory and model; the last first-action time (dispatch is in order)
+    int nbatch = 1;
+    TT bs_free[kMaxBatch], bs_fin[kMaxBatch], bdisp = 0;
+    int32_t bs_mem[kMaxBatch], bs_model[kMaxBatch];
+#pragma unroll
+    for (int k = 0; k < kMaxBatch; ++k) {
+      bs_free[k] = 0;
+      bs_fin[k] = 0;
+      bs_mem[k] = 0;
+      bs_model[k] = 0;
+    }
     if (PAPER && act) {
       // one backward pass over the device's units: for each unit, the index
       // of the next unit of the device with the same model (0xffff: none);
@@ -687,6 +702,15 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
       res = t_res0[d];
       capd = t_cap[d];
       freet = TO::load(t_free0 + d);
+      if constexpr (BATCH) {
+        nbatch = t_batch[d];
+        bdisp = freet;
+#pragma unroll
+        for (int k = 0; k < kMaxBatch; ++k) {
+          bs_free[k] = freet;
+          bs_fin[k] = freet;
+        }
+      }
       QT qa = 0;
       int na = 0;
       for (uint64_t r = res; r; r &= r - 1) {
@@ -819,6 +843,46 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
         };
         // one unit of the device's sequence: reuse / reclaim / load, then
         // the timeline
+        // one victim among the candidate copies `cand` (not empty): the
+        // paper's order, or no remaining use first, then least recently used
+        // (ascending ids: equal keys keep the lower id)
+        auto victim_paper = [&](uint64_t cand) -> int {
+          int v = __builtin_ctzll(cand);
+          uint32_t vred = (uint32_t)((others >> v) & 1ull);
+          uint32_t vnu = mynxu[v];
+          uint32_t vld = wg_ld[__umul24((uint32_t)v, (uint32_t)D) + (uint32_t)d];
+          uint32_t vlru = mystamp[v];
+          for (cand &= cand - 1; cand; cand &= cand - 1) {
+            const int m2 = __builtin_ctzll(cand);
+            const uint32_t red = (uint32_t)((others >> m2) & 1ull);
+            const uint32_t nu = mynxu[m2];
+            const uint32_t ld = wg_ld[__umul24((uint32_t)m2, (uint32_t)D) + (uint32_t)d];
+            const uint32_t lru = mystamp[m2];
+            if (paper_victim_before(red, nu, ld, lru, vred, vnu, vld, vlru, (uint32_t)kdev)) {
+              v = m2;
+              vred = red;
+              vnu = nu;
+              vld = ld;
+              vlru = lru;
+            }
+          }
+          return v;
+        };
+        auto victim_lru = [&](uint64_t cand, int slot) -> int {
+          int v = 0;
+          uint32_t best = 0xffffffffu;
+          while (cand) {
+            const int m2 = __builtin_ctzll(cand);
+            cand &= cand - 1;
+            const uint32_t alive = mylast[m2] > (uint32_t)slot + 1u;
+            const uint32_t key = (alive << 16) | mystamp[m2];
+            if (key < best) {
+              best = key;
+              v = m2;
+            }
+          }
+          return v;
+        };
         auto process = [&](const UnitPre<TT>& X) {
           if (X.slot >= 0) {
             const int u = (int)(X.meta & 0xffffu);
@@ -869,9 +933,58 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
               }
             }
             const int32_t need = (hit ? 0 : X.lw.y) + mxu;
-            // reclaim (Sec. 3.5): a copy with no remaining use first, else the
-            // least recently used, else the lower model id
-            if constexpr (NIBBLE) {
+            // batch limits: the slot that frees first, the first action's
+            // time t, and the memory and leases of the units running at t
+            int ks = 0;
+            TT sft = bs_free[0], t0 = 0;
+            int32_t run_act = 0;
+            if constexpr (BATCH) {
+#pragma unroll
+              for (int k = 1; k < kMaxBatch; ++k)
+                if (k < nbatch && bs_free[k] < sft) {
+                  ks = k;
+                  sft = bs_free[k];
+                }
+              t0 = TO::tmax(TO::tmax((!hit && (X.meta & kPf)) ? X.arrv : r, sft), bdisp);
+              for (;;) {
+                uint64_t leased = 0ull;
+                TT nf = 0;
+                bool any = false;
+                run_act = 0;
+#pragma unroll
+                for (int k = 0; k < kMaxBatch; ++k) {
+                  const bool running = k < nbatch && bs_fin[k] > t0;
+                  run_act += running ? bs_mem[k] : 0;
+                  leased |= running ? (1ull << bs_model[k]) : 0ull;
+                  nf = running && (!any || bs_fin[k] < nf) ? bs_fin[k] : nf;
+                  any |= running;
+                }
+                // reclaim lease-free copies (Sec. 3.5) in the window's order
+                while (used + run_act + need > capd) {
+                  const uint64_t cand = res & ~mbit & ~leased;
+                  if (!cand) break;
+                  int v;
+                  if constexpr (PAPER)
+                    v = victim_paper(cand);
+                  else
+                    v = victim_lru(cand, X.slot);
+                  res &= ~(1ull << v);
+                  if constexpr (PHI) ph_rec |= 1ull << v;
+                  used -= t_wmib[v];
+                  ++nev;
+                }
+                // fits, or no running unit left to wait for
+                if (!(used + run_act + need > capd) || !any) break;
+                t0 = nf;
+              }
+              mystamp[m] = (uint16_t)seq++;
+              if constexpr (PAPER) {
+                mynxu[m] = s_nx[gme * N + X.slot];
+                ++kdev;
+              }
+            } else if constexpr (NIBBLE) {
+              // reclaim (Sec. 3.5): a copy with no remaining use first, else
+              // the least recently used, else the lower model id
               int t = 0;
               while (used + need > capd && nq > 0) {
                 const int v = (int)(Q & (QT)15);
@@ -897,30 +1010,9 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
               (void)w0;
               (void)w1;
               while (used + need > capd) {
-                uint64_t cand = res & ~mbit;
+                const uint64_t cand = res & ~mbit;
                 if (!cand) break;
-                // the first candidate, then any that the paper's order
-                // reclaims before the current choice (ascending ids: equal
-                // keys keep the lower id)
-                int v = __builtin_ctzll(cand);
-                uint32_t vred = (uint32_t)((others >> v) & 1ull);
-                uint32_t vnu = mynxu[v];
-                uint32_t vld = wg_ld[__umul24((uint32_t)v, (uint32_t)D) + (uint32_t)d];
-                uint32_t vlru = mystamp[v];
-                for (cand &= cand - 1; cand; cand &= cand - 1) {
-                  const int m2 = __builtin_ctzll(cand);
-                  const uint32_t red = (uint32_t)((others >> m2) & 1ull);
-                  const uint32_t nu = mynxu[m2];
-                  const uint32_t ld = wg_ld[__umul24((uint32_t)m2, (uint32_t)D) + (uint32_t)d];
-                  const uint32_t lru = mystamp[m2];
-                  if (paper_victim_before(red, nu, ld, lru, vred, vnu, vld, vlru, (uint32_t)kdev)) {
-                    v = m2;
-                    vred = red;
-                    vnu = nu;
-                    vld = ld;
-                    vlru = lru;
-                  }
-                }
+                const int v = victim_paper(cand);
                 res &= ~(1ull << v);
                 if constexpr (PHI) ph_rec |= 1ull << v;
                 used -= t_wmib[v];
@@ -933,20 +1025,9 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
               (void)w0;
               (void)w1;
               while (used + need > capd) {
-                uint64_t cand = res & ~mbit;
+                const uint64_t cand = res & ~mbit;
                 if (!cand) break;
-                int v = 0;
-                uint32_t best = 0xffffffffu;
-                while (cand) {
-                  const int m2 = __builtin_ctzll(cand);
-                  cand &= cand - 1;
-                  const uint32_t alive = mylast[m2] > (uint32_t)X.slot + 1u;
-                  const uint32_t key = (alive << 16) | mystamp[m2];
-                  if (key < best) {
-                    best = key;
-                    v = m2;
-                  }
-                }
+                const int v = victim_lru(cand, X.slot);
                 res &= ~(1ull << v);
                 if constexpr (PHI) ph_rec |= 1ull << v;
                 used -= t_wmib[v];
@@ -954,13 +1035,15 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
               }
               mystamp[m] = (uint16_t)seq++;
             }
-            const bool over = used + need > capd;
+            const bool over = used + run_act + need > capd;
             capbad |= (uint32_t)over;
-            // timeline (Eq. 7): a load waits for the device and starts at the
-            // release, or at the workflow arrival when prefetched
-            const TT ls = TO::tmax((X.meta & kPf) ? X.arrv : r, freet);
+            // timeline (Eq. 7): a load waits for the device (a slot) and
+            // starts at the release, or at the workflow arrival when
+            // prefetched
+            const TT dev_free = BATCH ? sft : freet;
+            const TT ls = BATCH ? t0 : TO::tmax((X.meta & kPf) ? X.arrv : r, freet);
             const TT le = TO::add(ls, (uint32_t)X.lw.x);
-            const TT s = TO::tmax(r, hit ? freet : le);
+            const TT s = BATCH ? (hit ? t0 : TO::tmax(r, le)) : TO::tmax(r, hit ? freet : le);
             // ready work: no predecessor, arrived by the window time
             const bool ready = PHI && ((X.act >> 7) & 1u);
             if constexpr (PHI) {
@@ -970,14 +1053,25 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
                 // a prefetch is timely when its load is done by the release
                 if (!ready && (X.meta & kPf) && le <= r) ++ph_pn;
                 // the delay a load adds to ready work
-                if (ready) ph_h += (HT)TO::sub(s, TO::tmax(r, freet));
+                if (ready) ph_h += (HT)TO::sub(s, TO::tmax(r, dev_free));
               }
             }
             if constexpr (!NIBBLE) res |= mbit;
             used += hit ? 0 : X.lw.y;
             nld += hit ? 0u : 1u;
-            peak = (used + mxu) > peak ? (used + mxu) : peak;
+            peak = (used + run_act + mxu) > peak ? (used + run_act + mxu) : peak;
             const TT f = TO::add(s, T);
+            if constexpr (BATCH) {
+#pragma unroll
+              for (int k = 0; k < kMaxBatch; ++k) {
+                const bool mine = k == ks;
+                bs_free[k] = mine ? f : bs_free[k];
+                bs_fin[k] = mine ? f : bs_fin[k];
+                bs_mem[k] = mine ? mxu : bs_mem[k];
+                bs_model[k] = mine ? m : bs_model[k];
+              }
+              bdisp = t0;
+            }
             if constexpr (PHI) {
               if (ready && !over) {
                 ph_adm += 1ull << (16u * ((X.act >> 8) & 3u));
@@ -1180,8 +1274,12 @@ template <typename TT, bool SEARCH, bool PHI>
 hipError_t launch_time(const ScoreParams& sp, const int8_t* dev, const uint16_t* prio,
                        const uint8_t* flags, int64_t n_plans, OutRec<PHI>* out,
                        const wf_plan_sched& s, int has, const SearchArgs& sa, hipStream_t stream) {
-  if (sp.nibble < 0)
+  if (sp.nibble == -1)
     return launch_place<TT, -1, SEARCH, PHI>(sp, dev, prio, flags, n_plans, out, s, has, sa, stream);
+  if (sp.nibble == -2)
+    return launch_place<TT, -2, SEARCH, PHI>(sp, dev, prio, flags, n_plans, out, s, has, sa, stream);
+  if (sp.nibble == -3)
+    return launch_place<TT, -3, SEARCH, PHI>(sp, dev, prio, flags, n_plans, out, s, has, sa, stream);
   if (sp.nibble == 32)
     return launch_place<TT, 32, SEARCH, PHI>(sp, dev, prio, flags, n_plans, out, s, has, sa, stream);
   if (sp.nibble == 64)

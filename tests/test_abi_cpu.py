@@ -116,6 +116,8 @@ BAD = {
     "class_out_of_range": lambda w: setattr(w, "wf_class",
                                             np.full(w.n_wf, pkg._lib.WF_MAX_CLASSES, np.uint8)),
     "victim_order_unknown": lambda w: setattr(w, "victim_order", 2),
+    "batch_zero": lambda w: setattr(w, "dev_batch", np.zeros(w.n_dev, np.int32)),
+    "batch_too_big": lambda w: setattr(w, "dev_batch", np.full(w.n_dev, pkg._lib.WF_MAX_BATCH + 1, np.int32)),
 }
 
 
