@@ -133,6 +133,8 @@ def main():
                     help="skip the leg that scores with the paper's reclamation order")
     ap.add_argument("--no-keys", action="store_true",
                     help="skip the ranking-key leg (Eq. 12 keys and their argmin)")
+    ap.add_argument("--batch-limit", type=int, default=4,
+                    help="units per device at once in the batch-limit leg (1 = skip it)")
     ap.add_argument("--copy-probe", type=int, default=None, metavar="BYTES",
                     help="only run a plain copy kernel of BYTES bytes (counter calibration)")
     args = ap.parse_args()
@@ -312,22 +314,19 @@ def main():
                             "timely prefetches, lifecycle overhead) for the same plans, then "
                             "their lexicographic argmin"}
 
-    # the same plans under the paper's reclamation order (redundant copies,
-    # next use relative to reload cost, least recently used)
-    paper_leg = None
-    if not args.no_paper_order:
-        import dataclasses
-        win_p = dataclasses.replace(win, victim_order=1)
-        ctx.wf_plan_upload_window(win_p)
+    def window_leg(win_v, what):
+        """The same plans scored under a variant of the window: checked against
+        the oracle on a sample, then timed like the main leg."""
+        ctx.wf_plan_upload_window(win_v)
         if args.check:
             import oracle
             n_chk = min(P, args.check)
             idx = np.unique(np.linspace(0, P - 1, n_chk).astype(np.int64))
             ctx.wf_plan_score_batch(dev, prio, flags, P, scores, None, stream)
             torch.cuda.synchronize()
-            ref = oracle.score(win_p, plans.take(idx), threads=min(16, os.cpu_count() or 1))
+            ref = oracle.score(win_v, plans.take(idx), threads=min(16, os.cpu_count() or 1))
             if pkg.scores_to_numpy(scores, P)[idx].tobytes() != ref.tobytes():
-                print("[bench] paper reclamation order differs from the oracle", file=sys.stderr)
+                print(f"[bench] {what}: scores differ from the oracle", file=sys.stderr)
                 sys.exit(1)
         for _ in range(args.warmup):
             ctx.wf_plan_score_batch(dev, prio, flags, P, scores, None, stream)
@@ -339,12 +338,29 @@ def main():
             ctx.wf_plan_score_batch(dev, prio, flags, P, scores, None, stream)
             b.record(stream)
         torch.cuda.synchronize()
-        p_ms = float(np.mean([a.elapsed_time(b) for a, b in pev]))
+        ctx.wf_plan_upload_window(win)
+        return float(np.mean([a.elapsed_time(b) for a, b in pev]))
+
+    import dataclasses
+    # the same plans under the paper's reclamation order (redundant copies,
+    # next use relative to reload cost, least recently used)
+    paper_leg = None
+    if not args.no_paper_order:
+        p_ms = window_leg(dataclasses.replace(win, victim_order=1), "paper reclamation order")
         paper_leg = {"value": round(P / (p_ms * 1e-3), 1), "unit": "plans/s",
                      "kernel_ms": round(p_ms, 4),
                      "note": "the same plans scored with the paper's reclamation order "
                              "(victim_order = 1: a scan over the resident set per reclamation)"}
-        ctx.wf_plan_upload_window(win)
+    # the same plans with a batch limit on every device (several units run
+    # at once; memory is checked against the running units)
+    batch_leg = None
+    if args.batch_limit > 1:
+        bl = np.full(D, args.batch_limit, np.int32)
+        b_ms = window_leg(dataclasses.replace(win, dev_batch=bl), "batch limits")
+        batch_leg = {"value": round(P / (b_ms * 1e-3), 1), "unit": "plans/s",
+                     "kernel_ms": round(b_ms, 4), "batch_limit": args.batch_limit,
+                     "note": "the same plans with up to batch_limit units per device at once "
+                             "(slots, memory of running units, leases on their models)"}
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -387,6 +403,7 @@ def main():
         "search": search,
         "keys": keys_leg,
         "paper_order": paper_leg,
+        "batch_limit": batch_leg,
     }
     print(json.dumps(line))
     ctx.close()
