@@ -497,14 +497,20 @@ wf_status plan_launch(wf_plan_ctx* ctx, const HostWindow& h, bool search, wfp::S
   }
   sp.wave_global = 0;
   sp.scratch = nullptr;
-  if (best < 0) {
-    // per-wave regions in HBM: one plan per device lane group, a bounded grid
+  // per-wave regions in HBM: every lane of a wave busy and eight waves per
+  // CU, but each region access goes through the cache instead of LDS.  Taken
+  // when no LDS layout fits, or when the LDS layout keeps at most an eighth
+  // as many walk lanes in flight (deep windows, whose per-plan state fills
+  // LDS with one or two plans per CU)
+  const double hbm_lanes = (double)std::min(gmax * D, 64) * 8;
+  if (best < 0 || best * 8.0 <= hbm_lanes) {
     wfp::WaveOffsets o{};
     const int G = gmax;
     const int64_t wb = wave_layout(h, G, tsz, sp.nwa, sp.nibble, search, o);
     const int64_t cap_bytes = int64_t(1) << 30;
     const int waves = 4;
     int64_t wgs = std::min<int64_t>((int64_t)ctx->n_cu * 2, cap_bytes / std::max<int64_t>(wb * waves, 1));
+    if (wgs < 1 && best >= 0) return WF_OK;  // keep the LDS layout
     if (wgs < 1)
       return fail(&ctx->err, WF_EUNSUPPORTED, "window too large (N=%d, widest level %d, D=%d, M=%d)",
                   h.N, h.wmax, D, h.M);
