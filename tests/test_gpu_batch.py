@@ -90,6 +90,23 @@ def test_random_windows_with_batch_limits(ctx, seed):
     check(ctx, win, plans, f"seed {seed}")
 
 
+@pytest.mark.parametrize("fit", [8, 9, 16])
+def test_sixteen_models_with_batch_limits(ctx, fit):
+    """Sixteen equal-weight models, capacity for exactly `fit` of them plus a
+    little activation memory, batch limits 2 and 4: the resident set runs
+    full and most units reclaim a copy, often with others leased by running
+    units."""
+    rng = np.random.default_rng(700 + fit)
+    win = W.random_window(rng, n_wf=6, nodes=(6, 14), n_dev=2, n_models=16,
+                          cap_range=(fit * 1000 + 600, fit * 1000 + 600), w_range=(1000, 1000),
+                          mem_range=(0, 200), q_inel=0.0, same_model_bias=0.0)
+    win.dev_batch = np.array([2, 4], np.int32)
+    plans = W.random_plans(win, 300, rng, prio_mode="perm")
+    check(ctx, win, plans, f"fit {fit}")
+    if fit < 16:
+        assert (oracle.score(win, plans)["n_evicts"] > 0).mean() > 0.5
+
+
 def test_worked_examples_with_batch_limits(ctx):
     from fixtures import load_golden
     for name in ("batch_memory", "batch_lease"):
