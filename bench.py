@@ -342,8 +342,8 @@ def main():
         return float(np.mean([a.elapsed_time(b) for a, b in pev]))
 
     import dataclasses
-    # the same plans under the paper's reclamation order (redundant copies,
-    # next use relative to reload cost, least recently used)
+    # the same plans under the paper's reclamation order (copies held on
+    # another device, then next-use distance per reload time, then recency)
     paper_leg = None
     if not args.no_paper_order:
         p_ms = window_leg(dataclasses.replace(win, victim_order=1), "paper reclamation order")

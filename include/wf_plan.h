@@ -29,7 +29,8 @@
  *      id.  If it still does not fit the plan is flagged WF_ST_CAPACITY
  *      (memory equal to capacity fits).
  *   4. Timeline (Eq. 2, Eq. 7).  Release r = max(workflow arrival, latest
- *      predecessor finish).  A device runs one unit or one load at a time.
+ *      predecessor finish).  A device runs one unit or one load at a time
+ *      (unless the window sets batch limits, below).
  *      A load starts at max(r, device free) -- or max(arrival, device free)
  *      when the prefetch bit is set (Eq. 5, alpha_N = Prefetch) -- and the
  *      unit starts at max(r, load end); without a load at max(r, device
@@ -147,7 +148,7 @@ typedef struct {
  * WF_VICTIM_PAPER follows Sec. 3.5 (reclamation): among the resident copies
  * other than the unit's own, first those whose model is resident on another
  * device as the unit's topological level starts (redundant copies), then the
- * largest next-use distance relative to reload cost -- distance = the number
+ * largest ratio of next-use distance to reload time -- distance = the number
  * of the device's units, in resource order, from the current one to the next
  * one that uses the model; the ratio distance / load time is infinite when
  * there is no next use or the load takes 0 us, and finite ratios compare by

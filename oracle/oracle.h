@@ -80,7 +80,7 @@ enum { ORC_MAX_BATCH = 4 };
  *     used count as oldest), then the lower model id;
  *   ORC_VICTIM_PAPER -- redundant copies first (the model is resident on
  *     another device when the current topological level starts), then the
- *     largest next-use distance relative to reload cost -- distance = the
+ *     largest ratio of next-use distance to reload time -- distance = the
  *     number of the device's units, in resource order, from the current one
  *     to the next one that uses the model, infinite without one; the ratio
  *     distance / load time is infinite when either the distance is infinite

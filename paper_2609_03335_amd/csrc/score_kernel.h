@@ -222,8 +222,8 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   // reclamation queue: QB bits of 4-bit model ids (QB = 0: no queue, the
   // resident set is scanned instead)
   constexpr bool NIBBLE = QB > 0;
-  // QB = -1, -3: the paper's reclamation order (redundant copies, then next
-  // use relative to reload cost, then least recently used) over the scanned
+  // QB = -1, -3: the paper's reclamation order (copies held on another
+  // device, then next-use distance per reload time, then recency) over the scanned
   // resident set; QB = -2, -3: devices with batch limits (several units at
   // once, each in one of up to kMaxBatch slots)
   constexpr bool PAPER = QB == -1 || QB == -3;

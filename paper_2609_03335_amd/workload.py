@@ -65,8 +65,8 @@ class Window:
     # (0 ranked first, below 4); None puts every workflow in class 0
     wf_class: Optional[np.ndarray] = None
     # reclamation victim order: 0 = no remaining use first, then least
-    # recently used; 1 = the paper's (redundant copies, then next use
-    # relative to reload cost, then least recently used)
+    # recently used; 1 = the paper's (copies held on another device, then
+    # next-use distance per reload time, then least recently used)
     victim_order: int = 0
     # int32[D] batch limit of each device (units it runs at once, 1..4);
     # None = 1 everywhere

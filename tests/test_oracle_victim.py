@@ -1,6 +1,6 @@
-"""Pins of the oracle's paper victim order (Sec. 3.5, reclamation: redundant
-copies first, then distant next use relative to reload cost, then least
-recently used).
+"""Pins of the oracle's paper victim order (Sec. 3.5, reclamation: copies
+held on another device first, then the largest ratio of next-use distance to
+reload time, then least recently used).
 
 * Worked examples (tests/golden/victim_order*.json), each derived by hand in
   the fixture: a choice decided by redundancy, one decided by the ratio of
