@@ -312,10 +312,15 @@ wf_status wf_plan_search_keys(wf_plan_ctx *ctx, const int8_t *dev, const uint16_
 wf_status wf_plan_argmin_keys(wf_plan_ctx *ctx, const wf_plan_key *keys, int64_t n_plans,
                               int64_t *out_index, void *hip_stream);
 
-/* Time arithmetic the kernels use for the uploaded window: 32 when every
- * time of every plan provably stays below 2^32 us after the window origin
- * (uint32 offsets), 64 otherwise (fp64, exact for integers below 2^53); 0
- * when ctx is NULL or has no window.  Results are identical either way. */
+/* Time arithmetic the kernels use for the uploaded window: 32 when they
+ * carry times as uint32 offsets from the window origin, 64 when they use
+ * fp64 (exact for integers below 2^53); 0 when ctx is NULL or has no window.
+ * uint32 is used when every time of every plan provably stays below 2^32 us
+ * (a static bound: latest arrival or busy-until plus every activation's
+ * longest run and load), and also when that bound is below 8 x 2^32 us: then
+ * uint32 additions saturate, and every scoring call runs a second, fp64 pass
+ * over the groups of plans whose times saturated.  Results are identical in
+ * every case. */
 int wf_plan_time_bits(const wf_plan_ctx *ctx);
 
 /* Library version string. */

@@ -205,9 +205,14 @@ wf_status validate(const wf_window_desc* w, std::string* err, HostWindow* out) {
 
 struct DeviceWindow {
   void* tab = nullptr;          // table image in HBM
+  void* tab64 = nullptr;        // fp64-time table image of the rescoring pass
   void* scratch = nullptr;      // per-wave regions for windows too big for LDS
   wfp::ScoreParams sp{};        // scoring plans read from HBM
   wfp::ScoreParams sp_search{}; // scoring candidates generated around an incumbent
+  // uint32 times without a proof that none reaches 2^32: plans whose times
+  // saturate are rescored with fp64 times
+  bool checked = false;
+  wfp::ScoreParams sp64{}, sp64_search{};
 };
 
 }  // namespace
@@ -233,6 +238,7 @@ wf_status hip_fail(wf_plan_ctx* ctx, hipError_t e, const char* what) {
 
 void free_device_window(DeviceWindow& dw) {
   if (dw.tab) (void)hipFree(dw.tab);
+  if (dw.tab64) (void)hipFree(dw.tab64);
   if (dw.scratch) (void)hipFree(dw.scratch);
   dw = DeviceWindow{};
 }
@@ -297,9 +303,18 @@ int wave_layout(const HostWindow& h, int G, int tsz, int nwa, int qmode, bool se
   return o.bytes;
 }
 
-// Build the table image and choose time width, LDS placement, plans per
-// wave and waves per workgroup for this window.
-wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, Image& img, wfp::ScoreParams& sp) {
+// How a window's times are carried: uint32 when no time of any plan can reach
+// 2^32 (proven by the static bound below), uint32 with an fp64 rescoring of
+// the plans that saturate when the bound is within kCheckedSpan of 2^32 (few
+// plans get there), else fp64.
+enum TimeMode { kTimeU32 = 0, kTimeF64 = 1, kTimeChecked = 2 };
+constexpr int64_t kCheckedSpan = 8;
+
+// Build the table image and choose LDS placement, plans per wave and waves per
+// workgroup for this window, with uint32 (time64 = false) or fp64 times;
+// *mode reports which time arithmetic the window needs.
+wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, bool time64_req, Image& img,
+                      wfp::ScoreParams& sp, TimeMode* mode) {
   const int N = h.N, D = h.D, M = h.M, W = h.W;
   // time origin: earliest arrival or device free time
   int64_t origin = INT64_MAX;
@@ -331,7 +346,10 @@ wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, Image& img, wfp::Sc
   }
   if (chain_max >= (int64_t(1) << 32))
     return fail(&ctx->err, WF_EUNSUPPORTED, "a fusible chain may run for 2^32 us or more");
-  const bool time64 = bound >= (int64_t(1) << 32);
+  const int64_t two32 = int64_t(1) << 32;
+  *mode = bound < two32 ? kTimeU32
+          : (t0 < two32 / 2 && bound < kCheckedSpan * two32) ? kTimeChecked : kTimeF64;
+  const bool time64 = *mode == kTimeF64 || time64_req;
   const int tsz = time64 ? 8 : 4;
 
   // ---- table image ----
@@ -525,6 +543,25 @@ wf_status plan_launch(wf_plan_ctx* ctx, const HostWindow& h, bool search, wfp::S
   return WF_OK;
 }
 
+// Launch parameters of one pass over n plans: the grid never exceeds the
+// groups there are.
+wfp::ScoreParams fit_grid(wfp::ScoreParams sp, int64_t n) {
+  const int64_t groups = (n + sp.G - 1) / sp.G;
+  const int64_t wgs = (groups + sp.waves - 1) / sp.waves;
+  if (wgs < sp.grid) sp.grid = (int)wgs;
+  return sp;
+}
+
+// Run a scoring launch with the window's parameters, then, for a window
+// whose uint32 times are not proven safe, the fp64 pass over the groups it
+// flagged (same stream, so in order).
+template <typename F>
+hipError_t two_pass(const DeviceWindow& dw, bool search, int64_t n, F&& launch) {
+  hipError_t e = launch(fit_grid(search ? dw.sp_search : dw.sp, n));
+  if (e == hipSuccess && dw.checked) e = launch(fit_grid(search ? dw.sp64_search : dw.sp64, n));
+  return e;
+}
+
 }  // namespace
 
 extern "C" {
@@ -616,15 +653,29 @@ wf_status wf_plan_upload_window(wf_plan_ctx* ctx, const wf_window_desc* w) {
   HostWindow h;
   wf_status st = validate(w, &ctx->err, &h);
   if (st != WF_OK) return st;
-  Image img;
-  wfp::ScoreParams sp{};
-  st = plan_window(ctx, h, img, sp);
+  Image img, img64;
+  wfp::ScoreParams sp{}, sp64{};
+  TimeMode mode;
+  st = plan_window(ctx, h, false, img, sp, &mode);
   if (st != WF_OK) return st;
   wfp::ScoreParams sps = sp;
   st = plan_launch(ctx, h, false, sp);
   if (st != WF_OK) return st;
   st = plan_launch(ctx, h, true, sps);
   if (st != WF_OK) return st;
+  const bool checked = mode == kTimeChecked;
+  wfp::ScoreParams sps64{};
+  if (checked) {
+    st = plan_window(ctx, h, true, img64, sp64, &mode);
+    if (st != WF_OK) return st;
+    sps64 = sp64;
+    st = plan_launch(ctx, h, false, sp64);
+    if (st != WF_OK) return st;
+    st = plan_launch(ctx, h, true, sps64);
+    if (st != WF_OK) return st;
+    sp64.rescore = 1;
+    sps64.rescore = 1;
+  }
 
   int prev = 0;
   (void)hipGetDevice(&prev);
@@ -643,9 +694,28 @@ wf_status wf_plan_upload_window(wf_plan_ctx* ctx, const wf_window_desc* w) {
     (void)hipSetDevice(prev);
     return hip_fail(ctx, e, "copying the window to the device");
   }
-  if (sp.wave_global || sps.wave_global) {
-    const size_t need = std::max(sp.wave_global ? (size_t)sp.grid * sp.waves * (size_t)sp.wo.bytes : 0,
-                                 sps.wave_global ? (size_t)sps.grid * sps.waves * (size_t)sps.wo.bytes : 0);
+  if (checked) {
+    e = hipMalloc(&dw.tab64, img64.bytes.size());
+    if (e != hipSuccess) {
+      free_device_window(dw);
+      (void)hipSetDevice(prev);
+      ctx->err = "device allocation of the window failed";
+      return WF_ENOMEM;
+    }
+    e = hipMemcpy(dw.tab64, img64.bytes.data(), img64.bytes.size(), hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+      free_device_window(dw);
+      (void)hipSetDevice(prev);
+      return hip_fail(ctx, e, "copying the window to the device");
+    }
+  }
+  // one scratch area serves every pass (they run in order on a stream)
+  wfp::ScoreParams* all[4] = {&sp, &sps, &sp64, &sps64};
+  size_t need = 0;
+  for (int i = 0; i < (checked ? 4 : 2); ++i)
+    if (all[i]->wave_global)
+      need = std::max(need, (size_t)all[i]->grid * all[i]->waves * (size_t)all[i]->wo.bytes);
+  if (need) {
     e = hipMalloc(&dw.scratch, need);
     if (e != hipSuccess) {
       free_device_window(dw);
@@ -653,18 +723,26 @@ wf_status wf_plan_upload_window(wf_plan_ctx* ctx, const wf_window_desc* w) {
       ctx->err = "device allocation of the scoring scratch failed";
       return WF_ENOMEM;
     }
-    if (sp.wave_global) sp.scratch = static_cast<unsigned char*>(dw.scratch);
-    if (sps.wave_global) sps.scratch = static_cast<unsigned char*>(dw.scratch);
+    for (int i = 0; i < 4; ++i)
+      if (all[i]->wave_global) all[i]->scratch = static_cast<unsigned char*>(dw.scratch);
   }
   sp.tab = static_cast<const unsigned char*>(dw.tab);
   sps.tab = static_cast<const unsigned char*>(dw.tab);
   dw.sp = sp;
   dw.sp_search = sps;
+  dw.checked = checked;
+  if (checked) {
+    sp64.tab = static_cast<const unsigned char*>(dw.tab64);
+    sps64.tab = static_cast<const unsigned char*>(dw.tab64);
+    dw.sp64 = sp64;
+    dw.sp64_search = sps64;
+  }
   if (std::getenv("WF_PLAN_VERBOSE"))
     std::fprintf(stderr,
                  "[wf_plan] N=%d W=%d D=%d M=%d levels=%d wmax=%d time=%s G=%d waves/wg=%d "
                  "grid=%d tables=%s(%d B) wave=%d B lds/wg=%d reclaim=%s\n",
-                 sp.N, sp.W, sp.D, sp.M, sp.n_levels, h.wmax, sp.time64 ? "fp64" : "u32", sp.G,
+                 sp.N, sp.W, sp.D, sp.M, sp.n_levels, h.wmax,
+                 sp.time64 ? "fp64" : checked ? "u32+fp64" : "u32", sp.G,
                  sp.waves, sp.grid, sp.wave_global ? "hbm+scratch" : (sp.tab_in_lds ? "lds" : "hbm"),
                  sp.t.bytes, sp.wo.bytes, sp.lds_bytes, sp.nibble == 32 ? "queue32" : sp.nibble == 64 ? "queue64" : sp.nibble == -1 ? "paper-scan" :
                  sp.nibble == -2 ? "batch-scan" : sp.nibble == -3 ? "batch-paper-scan" : "scan");
@@ -696,12 +774,10 @@ wf_status wf_plan_score_batch(wf_plan_ctx* ctx, const int8_t* dev, const uint16_
   (void)hipGetDevice(&prev);
   hipError_t e = hipSetDevice(ctx->device);
   if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
-  wfp::ScoreParams sp = ctx->dw.sp;
-  const int64_t groups = (n_plans + sp.G - 1) / sp.G;
-  const int64_t wgs = (groups + sp.waves - 1) / sp.waves;
-  if (wgs < sp.grid) sp.grid = (int)wgs;
-  e = wfp::launch_score(sp, dev, prio, flags, n_plans, scores, sched, nullptr,
-                        static_cast<hipStream_t>(hip_stream));
+  e = two_pass(ctx->dw, false, n_plans, [&](const wfp::ScoreParams& sp) {
+    return wfp::launch_score(sp, dev, prio, flags, n_plans, scores, sched, nullptr,
+                             static_cast<hipStream_t>(hip_stream));
+  });
   (void)hipSetDevice(prev);
   if (e != hipSuccess) return hip_fail(ctx, e, "launching the scoring kernel");
   return WF_OK;
@@ -737,13 +813,11 @@ wf_status wf_plan_search_batch(wf_plan_ctx* ctx, const int8_t* dev, const uint16
   (void)hipGetDevice(&prev);
   hipError_t e = hipSetDevice(ctx->device);
   if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
-  wfp::ScoreParams sp = ctx->dw.sp_search;
-  const int64_t groups = (n_candidates + sp.G - 1) / sp.G;
-  const int64_t wgs = (groups + sp.waves - 1) / sp.waves;
-  if (wgs < sp.grid) sp.grid = (int)wgs;
   const wfp::SearchArgs sa{seed, n_mut, first};
-  e = wfp::launch_score(sp, dev, prio, flags, n_candidates, scores, nullptr, &sa,
-                        static_cast<hipStream_t>(hip_stream));
+  e = two_pass(ctx->dw, true, n_candidates, [&](const wfp::ScoreParams& sp) {
+    return wfp::launch_score(sp, dev, prio, flags, n_candidates, scores, nullptr, &sa,
+                             static_cast<hipStream_t>(hip_stream));
+  });
   (void)hipSetDevice(prev);
   if (e != hipSuccess) return hip_fail(ctx, e, "launching the scoring kernel");
   return WF_OK;
@@ -811,12 +885,10 @@ wf_status wf_plan_score_keys(wf_plan_ctx* ctx, const int8_t* dev, const uint16_t
   (void)hipGetDevice(&prev);
   hipError_t e = hipSetDevice(ctx->device);
   if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
-  wfp::ScoreParams sp = ctx->dw.sp;
-  const int64_t groups = (n_plans + sp.G - 1) / sp.G;
-  const int64_t wgs = (groups + sp.waves - 1) / sp.waves;
-  if (wgs < sp.grid) sp.grid = (int)wgs;
-  e = wfp::launch_score_keys(sp, dev, prio, flags, n_plans, keys, nullptr,
-                             static_cast<hipStream_t>(hip_stream));
+  e = two_pass(ctx->dw, false, n_plans, [&](const wfp::ScoreParams& sp) {
+    return wfp::launch_score_keys(sp, dev, prio, flags, n_plans, keys, nullptr,
+                                  static_cast<hipStream_t>(hip_stream));
+  });
   (void)hipSetDevice(prev);
   if (e != hipSuccess) return hip_fail(ctx, e, "launching the ranking-key kernel");
   return WF_OK;
@@ -833,13 +905,11 @@ wf_status wf_plan_search_keys(wf_plan_ctx* ctx, const int8_t* dev, const uint16_
   (void)hipGetDevice(&prev);
   hipError_t e = hipSetDevice(ctx->device);
   if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
-  wfp::ScoreParams sp = ctx->dw.sp_search;
-  const int64_t groups = (n_candidates + sp.G - 1) / sp.G;
-  const int64_t wgs = (groups + sp.waves - 1) / sp.waves;
-  if (wgs < sp.grid) sp.grid = (int)wgs;
   const wfp::SearchArgs sa{seed, n_mut, first};
-  e = wfp::launch_score_keys(sp, dev, prio, flags, n_candidates, keys, &sa,
-                             static_cast<hipStream_t>(hip_stream));
+  e = two_pass(ctx->dw, true, n_candidates, [&](const wfp::ScoreParams& sp) {
+    return wfp::launch_score_keys(sp, dev, prio, flags, n_candidates, keys, &sa,
+                                  static_cast<hipStream_t>(hip_stream));
+  });
   (void)hipSetDevice(prev);
   if (e != hipSuccess) return hip_fail(ctx, e, "launching the ranking-key kernel");
   return WF_OK;

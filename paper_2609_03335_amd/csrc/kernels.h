@@ -86,7 +86,14 @@ struct ScoreParams {
                               // -1: scan in the paper's reclamation order; -2 / -3: the
                               // same two scans with per-device batch limits
   int has_chains;             // 1: some activation satisfies Eq. 3 (fused units possible)
+  int rescore;                // 1: fp64 pass over the groups holding a plan whose uint32
+                              // times saturated (status bit kRescore of the first pass)
 };
+
+// Internal status bit of a uint32-time pass: some time of the plan reached
+// 2^32 - 1 (saturated), so an fp64 pass rescores it.  Never left in a record
+// a call returns.
+constexpr uint32_t kRescore = 1u << 31;
 
 // Per-plan accumulators kept in LDS by the scoring kernel.
 struct PlanAcc {

@@ -25,8 +25,10 @@
 // level starts.
 //
 // Times are relative to the window origin (earliest arrival or free time):
-// uint32 when the host has proven no time of any plan can reach 2^32, else
-// fp64 (every time is an integer below 2^53, so fp64 max/add are exact).
+// uint32 or fp64 (every time is an integer below 2^53, so fp64 max/add are
+// exact).  uint32 additions saturate; a plan with a saturated time is flagged
+// (kRescore) and the host rescores its group in fp64 unless it has proven
+// that no time can reach 2^32.
 #pragma once
 
 #include <type_traits>
@@ -46,7 +48,9 @@ struct TimeOps<uint32_t> {
   __device__ static uint32_t words(uint32_t lo, uint32_t) { return lo; }
   __device__ static bits_t bits(uint32_t t) { return t; }
   __device__ static uint32_t tmax(uint32_t a, uint32_t b) { return a > b ? a : b; }
-  __device__ static uint32_t add(uint32_t a, uint32_t d) { return a + d; }
+  // saturating: a time that would pass 2^32 - 1 stays there, and every max
+  // and sum that takes it does too, up to the device's last finish
+  __device__ static uint32_t add(uint32_t a, uint32_t d) { return __builtin_elementwise_add_sat(a, d); }
   __device__ static uint32_t sub(uint32_t a, uint32_t b) { return a - b; }
   __device__ static int64_t i64(uint32_t t) { return (int64_t)t; }
 };
@@ -312,7 +316,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   // one 256-activation chunk and at most eight plans per group: the next
   // group's device and priority rows are loaded while this group is walked
   constexpr int kB = 8;
-  const bool pre = !SEARCH && vec && N <= 256 && G <= kB;
+  const bool pre = !SEARCH && vec && N <= 256 && G <= kB && !sp.rescore;
   uint32_t dvp[kB];
   uint2 pvp[kB];
   auto load_rows = [&](int64_t grp_, uint32_t* dv, uint2* pv) {
@@ -334,6 +338,11 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   for (int64_t grp = (int64_t)blockIdx.x * sp.waves + wid; grp < n_groups; grp += stride) {
     const int64_t p0 = grp * G;
     const int gc = (int)((P - p0) < G ? (P - p0) : G);
+    if (sp.rescore) {
+      // second pass: only groups holding a plan the uint32 pass flagged
+      const bool flagged = lane < gc && (scores[p0 + lane].status & kRescore) != 0u;
+      if (__ballot(flagged) == 0ull) continue;
+    }
 
     // ---- stage the group's flag rows, clear the ordering state ----
     if constexpr (SEARCH) {
@@ -1137,6 +1146,15 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
       atomicAdd(&s_acc[gme].loads, nld);
       atomicAdd(&s_acc[gme].evicts, nev);
       if (capbad) atomicOr(&s_acc[gme].status, (uint32_t)WF_ST_CAPACITY);
+      if constexpr (std::is_same<TT, uint32_t>::value) {
+        // a saturated time ends in the device's last finish
+        TT last = freet;
+        if constexpr (BATCH) {
+#pragma unroll
+          for (int k = 0; k < kMaxBatch; ++k) last = TO::tmax(last, bs_free[k]);
+        }
+        if (last == 0xffffffffu) atomicOr(&s_acc[gme].status, kRescore);
+      }
       if (inel) atomicOr(&s_acc[gme].status, (uint32_t)WF_ST_INELIGIBLE);
       if (has_sched) sched.peak_mib[pw * D + d_me] = peak;
       if constexpr (PHI) {

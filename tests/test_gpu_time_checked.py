@@ -1,0 +1,131 @@
+"""Windows whose static time bound passes 2^32 us but stays below 8 x 2^32:
+the kernels carry uint32 times with saturating additions, and the plans
+whose times saturate are rescored with fp64 times in a second pass over
+their groups.  Every record against the oracle, from windows where no plan,
+a few, about half, or nearly every plan passes 2^32 us."""
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_03335_amd as pkg
+from paper_2609_03335_amd import workload as W
+from enumerate_plans import best_plan
+
+pytestmark = pytest.mark.gpu
+THREADS = max(1, min(16, os.cpu_count() or 1))
+TWO32 = 1 << 32
+
+
+def log(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def ctx():
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+    c = pkg.Context(0)
+    yield c
+    c.close()
+
+
+def long_window(scale, seed, n_dev=2):
+    """Loads of 0.4-1.2 s x scale x 1000 and runs of 0.04-0.2 s x scale x 1000
+    on few devices with no initial residency: times near 2^32 us."""
+    rng = np.random.default_rng(5150 + seed)
+    win = W.random_window(rng, n_wf=4, nodes=(4, 8), n_dev=n_dev, n_models=5, resident=False,
+                          lat_range=(int(4e7 * scale), int(2e8 * scale)),
+                          load_range=(int(4e8 * scale), int(12e8 * scale)),
+                          cap_range=(9000, 14000), w_range=(4000, 7000))
+    plans = W.random_plans(win, 400, rng, prio_mode=["any", "perm"][seed % 2])
+    return win, plans
+
+
+def overflow_fraction(win, plans):
+    sc, (st, fi, ls, pk) = oracle.score(win, plans, schedule=True, threads=THREADS)
+    origin = min(int(win.wf_arrival_us.min()), int(win.dev_free0_us.min()))
+    ok = sc["status"] & oracle.INELIGIBLE == 0
+    return float(((fi.max(axis=1) - origin)[ok] >= TWO32 - 1).mean())
+
+
+def check_scores(ctx, win, plans, where):
+    ctx.wf_plan_upload_window(win)
+    assert ctx.wf_plan_time_bits() == 32
+    P, N, D = plans.n_plans, win.n_act, win.n_dev
+    dev, prio, flags = pkg.device_plans(plans, "cuda:0")
+    scores, sched = pkg.score_batch(ctx, dev, prio, flags, P, schedule=True, n_act=N, n_dev=D)
+    best = pkg.argmin(ctx, scores, P)
+    torch.cuda.synchronize()
+    got = pkg.scores_to_numpy(scores, P)
+    ref, rs = oracle.score(win, plans, schedule=True, threads=THREADS)
+    assert got.tobytes() == ref.tobytes(), where
+    ok = ref["status"] & oracle.INELIGIBLE == 0
+    for name, a, b in zip(("start", "finish", "load_start", "peak"), sched, rs):
+        assert np.array_equal(a.cpu().numpy()[ok][:, :b.shape[1]], b[ok]), (where, name)
+    assert int(best.item()) == best_plan(ref)
+
+
+CASES = [(0.25, 0), (0.35, 3), (0.35, 1), (0.35, 0), (0.5, 3), (0.5, 0)]
+
+
+@pytest.mark.parametrize("scale,seed", CASES)
+def test_scores_and_schedules(ctx, scale, seed, capfd, monkeypatch):
+    win, plans = long_window(scale, seed)
+    frac = overflow_fraction(win, plans)
+    log(f"[checked] scale {scale} seed {seed}: N={win.n_act} overflow fraction {frac:.2f}")
+    monkeypatch.setenv("WF_PLAN_VERBOSE", "1")
+    check_scores(ctx, win, plans, (scale, seed))
+    assert "time=u32+fp64" in capfd.readouterr().err
+
+
+def test_cases_span_none_to_most():
+    fr = [overflow_fraction(*long_window(s, k)) for s, k in CASES]
+    assert min(fr) == 0.0 and max(fr) > 0.9
+    assert any(0.0 < f < 0.15 for f in fr)  # a few flagged groups among many skipped ones
+    assert any(0.3 < f < 0.7 for f in fr)
+
+
+def test_every_plan_passes_2_32(ctx):
+    win, plans = long_window(0.5, 0, n_dev=1)
+    assert overflow_fraction(win, plans) == 1.0
+    check_scores(ctx, win, plans, "all")
+
+
+@pytest.mark.parametrize("option", ["paper_order", "batch_limit"])
+def test_window_options(ctx, option):
+    win, plans = long_window(0.35, 0)
+    if option == "paper_order":
+        win.victim_order = 1
+    else:
+        win.dev_batch = np.array([2, 3], np.int32)
+    log(f"[checked] {option}: overflow fraction {overflow_fraction(win, plans):.2f}")
+    check_scores(ctx, win, plans, option)
+
+
+def test_keys_and_candidates(ctx):
+    win, plans = long_window(0.35, 0)
+    win.wf_class = (np.arange(win.n_wf) % 3).astype(np.uint8)
+    ctx.wf_plan_upload_window(win)
+    P = plans.n_plans
+    dev, prio, flags = pkg.device_plans(plans, "cuda:0")
+    keys = torch.empty((P, 32), dtype=torch.uint8, device="cuda:0")
+    ctx.wf_plan_score_keys(dev, prio, flags, P, keys)
+    torch.cuda.synchronize()
+    assert pkg.keys_to_numpy(keys, P).tobytes() == oracle.phi_keys(win, plans).tobytes()
+    inc = (plans.dev[7].copy(), plans.prio[7].copy(), plans.flags[7].copy())
+    rows = (torch.from_numpy(inc[0]).cuda(), torch.from_numpy(inc[1].view("<i2")).cuda(),
+            torch.from_numpy(inc[2]).cuda())
+    n = 3000
+    cand = W.PlanBatch(*oracle.search_candidates(win, *inc, 77, 3, 0, n))
+    log(f"[checked] candidates: overflow fraction {overflow_fraction(win, cand):.2f}")
+    scores = torch.empty((n, 32), dtype=torch.uint8, device="cuda:0")
+    ctx.wf_plan_search_batch(rows[0], rows[1], rows[2], 77, 3, 0, n, scores)
+    kk = torch.empty((n, 32), dtype=torch.uint8, device="cuda:0")
+    ctx.wf_plan_search_keys(rows[0], rows[1], rows[2], 77, 3, 0, n, kk)
+    torch.cuda.synchronize()
+    assert pkg.scores_to_numpy(scores, n).tobytes() == oracle.score(win, cand).tobytes()
+    assert pkg.keys_to_numpy(kk, n).tobytes() == oracle.phi_keys(win, cand).tobytes()
