@@ -40,14 +40,16 @@ def algorithmic_bytes_per_plan(n_act: int) -> int:
 
 
 def kernel_source_digest() -> str:
-    """sha256 over the scoring kernel's sources and its launch planner: a
-    stored HBM-traffic measurement is only valid for the code it was taken
-    on."""
+    """sha256 over the scoring kernel's sources, its launch planner and the
+    compiler flags: a stored counter measurement is only valid for the code
+    it was taken on."""
     import hashlib
+    from paper_2609_03335_amd import build
     h = hashlib.sha256()
     for name in ("score_kernel.h", "score.hip", "kernels.h", "host.hip"):
         with open(os.path.join(CSRC, name), "rb") as f:
             h.update(f.read())
+    h.update(" ".join(build.HIP_FLAGS).encode())
     return h.hexdigest()
 
 
