@@ -129,3 +129,20 @@ def test_keys_and_candidates(ctx):
     torch.cuda.synchronize()
     assert pkg.scores_to_numpy(scores, n).tobytes() == oracle.score(win, cand).tobytes()
     assert pkg.keys_to_numpy(kk, n).tobytes() == oracle.phi_keys(win, cand).tobytes()
+
+
+@pytest.mark.parametrize("scale,expect", [(0.65, 0.0), (0.8, 1.0)])
+def test_large_window_hbm_regions(ctx, scale, expect, capfd, monkeypatch):
+    """A 19,784-activation window on two devices: too large for LDS, so both
+    passes keep their per-wave regions in the shared HBM scratch area; no
+    plan passes 2^32 us at the smaller scale, every plan at the larger."""
+    rng = np.random.default_rng(5)
+    win = W.random_window(rng, n_wf=400, nodes=(40, 60), n_dev=2, n_models=8, p_edge=0.1,
+                          q_inel=0.0, resident=False, lat_range=(int(1e5 * scale), int(6e5 * scale)),
+                          load_range=(int(1e5 * scale), int(6e5 * scale)))
+    plans = W.random_plans(win, 24, rng, prio_mode="perm")
+    assert overflow_fraction(win, plans) == expect
+    monkeypatch.setenv("WF_PLAN_VERBOSE", "1")
+    check_scores(ctx, win, plans, f"large {scale}")
+    err = capfd.readouterr().err
+    assert "time=u32+fp64" in err and "hbm+scratch" in err
