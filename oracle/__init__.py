@@ -81,7 +81,9 @@ def _load(path: Optional[str] = None):
                 build(force=True)
             lib = ctypes.CDLL(path)
             lib.orc_score_plans.restype = ctypes.c_int
-            lib.orc_score_plans.argtypes = [ctypes.c_void_p] * 4 + [ctypes.c_int64] + [ctypes.c_void_p] * 5
+            lib.orc_score_plans.argtypes = [ctypes.c_void_p] * 4 + [ctypes.c_int64] + [ctypes.c_void_p] * 6
+            lib.orc_prefix.restype = ctypes.c_int
+            lib.orc_prefix.argtypes = [ctypes.c_void_p] * 9
             lib.orc_phi_keys.restype = ctypes.c_int
             lib.orc_phi_keys.argtypes = [ctypes.c_void_p] * 5 + [ctypes.c_int64, ctypes.c_void_p]
             lib.orc_levels.restype = ctypes.c_int
@@ -173,9 +175,11 @@ def _run_split(run, P, threads):
 
 
 def score(win, plans, begin: int = 0, end: Optional[int] = None, schedule: bool = False,
-          threads: int = 1, lib_path: Optional[str] = None):
+          threads: int = 1, lib_path: Optional[str] = None, reclaims: bool = False):
     """Score plans [begin, end) of ``plans``.  Returns a structured score
-    array, and with ``schedule=True`` also (start, finish, load_start, peak)."""
+    array, and with ``schedule=True`` also (start, finish, load_start, peak),
+    with ``reclaims=True`` as well followed by the [P][N] uint64 masks of the
+    copies reclaimed before each unit."""
     lib = _load(lib_path)
     h = _WinHolder(win)
     end = plans.n_plans if end is None else end
@@ -187,6 +191,8 @@ def score(win, plans, begin: int = 0, end: Optional[int] = None, schedule: bool 
     if schedule:
         sched = (np.zeros((P, N), np.int64), np.zeros((P, N), np.int64),
                  np.zeros((P, N), np.int64), np.zeros((P, D), np.int32))
+        if reclaims:
+            sched = sched + (np.zeros((P, N), np.uint64),)
 
     def run(a, b):
         if b <= a:
@@ -195,14 +201,36 @@ def score(win, plans, begin: int = 0, end: Optional[int] = None, schedule: bool 
         def ptr(arr):
             return None if arr is None else arr.ctypes.data + a * arr.strides[0]
 
-        s0, s1, s2, s3 = sched if sched is not None else (None, None, None, None)
+        s0, s1, s2, s3 = sched[:4] if sched is not None else (None, None, None, None)
+        s4 = sched[4] if sched is not None and len(sched) > 4 else None
         return lib.orc_score_plans(ctypes.byref(h.struct), ptr(dev), ptr(prio), ptr(flags),
-                                   b - a, ptr(scores), ptr(s0), ptr(s1), ptr(s2), ptr(s3))
+                                   b - a, ptr(scores), ptr(s0), ptr(s1), ptr(s2), ptr(s3), ptr(s4))
 
     _run_split(run, P, threads)
     if schedule:
         return scores, sched
     return scores
+
+
+def prefix(win, dev_row, start, finish, load_start, reclaimed, lib_path: Optional[str] = None):
+    """Prefix commit of Algorithm 1 for one plan (its device row and
+    schedule rows): (commit uint8[N], commit_reclaimed uint64[N], t_next)."""
+    lib = _load(lib_path)
+    h = _WinHolder(win)
+    N = win.n_act
+    arrs = [np.ascontiguousarray(x, dt) for x, dt in ((dev_row, np.int8), (start, np.int64),
+                                                      (finish, np.int64), (load_start, np.int64),
+                                                      (reclaimed, np.uint64))]
+    for x in arrs:
+        assert x.shape == (N,)
+    commit = np.zeros(N, np.uint8)
+    crec = np.zeros(N, np.uint64)
+    t_next = np.zeros(1, np.int64)
+    rc = lib.orc_prefix(ctypes.byref(h.struct), *[x.ctypes.data for x in arrs], commit.ctypes.data,
+                        crec.ctypes.data, t_next.ctypes.data)
+    if rc:
+        raise OracleError(rc)
+    return commit, crec, int(t_next[0])
 
 
 def phi_keys(win, plans, begin: int = 0, end: Optional[int] = None, threads: int = 1,

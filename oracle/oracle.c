@@ -150,7 +150,8 @@ static int paper_victim_before(int redx, int64_t distx, int64_t loadx, int64_t l
 static int simulate(const orc_window *w, const uint8_t *wf_class, const int8_t *dev,
                     const uint16_t *prio, const uint8_t *flags, int64_t n_plans,
                     orc_score *scores, int64_t *start_out, int64_t *finish_out,
-                    int64_t *load_out, int32_t *peak_out, orc_phi *keys) {
+                    int64_t *load_out, int32_t *peak_out, uint64_t *reclaim_out,
+                    orc_phi *keys) {
   if (wf_class)
     for (int32_t f = 0; f < w->n_wf; ++f)
       if (wf_class[f] >= ORC_MAX_CLASSES) return ORC_ERR_CLASS;
@@ -281,6 +282,11 @@ static int simulate(const orc_window *w, const uint8_t *wf_class, const int8_t *
     /* ranking-key terms (Eq. 12) */
     int64_t admitted[ORC_MAX_CLASSES] = {0, 0, 0, 0}, c_ready = 0, h_life = 0, timely = 0;
 
+    /* copies reclaimed before each unit's first action (0 for members) */
+    uint64_t *rec_row = reclaim_out ? reclaim_out + p * N : NULL;
+    if (rec_row)
+      for (int32_t i = 0; i < N; ++i) rec_row[i] = 0;
+
     /* ---- propagate units in resource order ---- */
     for (int32_t pos = 0; pos < n_units; ++pos) {
       int32_t h = order[pos].idx;
@@ -366,6 +372,7 @@ static int simulate(const orc_window *w, const uint8_t *wf_class, const int8_t *
         used[d] -= w->model_mib[victim];
         n_evicts += 1;
         reclaimed[d] |= 1ull << victim;
+        if (rec_row) rec_row[h] |= 1ull << victim;
       }
         /* fits, or nothing left to wait for */
         if (!(used[d] + run_act + need > w->dev_cap_mib[d]) || next_fin == INT64_MAX) break;
@@ -486,14 +493,45 @@ done:
 int orc_score_plans(const orc_window *w, const int8_t *dev, const uint16_t *prio,
                     const uint8_t *flags, int64_t n_plans, orc_score *scores,
                     int64_t *start_out, int64_t *finish_out, int64_t *load_out,
-                    int32_t *peak_out) {
+                    int32_t *peak_out, uint64_t *reclaim_out) {
   return simulate(w, NULL, dev, prio, flags, n_plans, scores, start_out, finish_out, load_out,
-                  peak_out, NULL);
+                  peak_out, reclaim_out, NULL);
+}
+
+int orc_prefix(const orc_window *w, const int8_t *dev, const int64_t *start_us,
+               const int64_t *finish_us, const int64_t *load_start_us,
+               const uint64_t *reclaimed, uint8_t *commit, uint64_t *commit_reclaimed,
+               int64_t *t_next_us) {
+  const int32_t N = w->n_act, D = w->n_dev;
+  for (int32_t i = 0; i < N; ++i)
+    if (dev[i] < 0 || dev[i] >= D) return ORC_ERR_INDEX;
+  /* the next predicted event after the window time 0: a unit's finish, a
+   * load's end, a workflow's arrival */
+  int64_t t = INT64_MAX;
+  for (int32_t i = 0; i < N; ++i) {
+    if (finish_us[i] > 0 && finish_us[i] < t) t = finish_us[i];
+    if (load_start_us[i] >= 0) {
+      const int64_t le = load_start_us[i] + w->load_us[(int64_t)w->act_model[i] * D + dev[i]];
+      if (le > 0 && le < t) t = le;
+    }
+  }
+  for (int32_t f = 0; f < w->n_wf; ++f)
+    if (w->wf_arrival_us[f] > 0 && w->wf_arrival_us[f] < t) t = w->wf_arrival_us[f];
+  *t_next_us = t;
+  /* every action that begins before that event is committed now */
+  for (int32_t i = 0; i < N; ++i) {
+    const int grant = start_us[i] < t;
+    const int load = load_start_us[i] >= 0 && load_start_us[i] < t;
+    const int64_t first = load_start_us[i] >= 0 ? load_start_us[i] : start_us[i];
+    commit[i] = (uint8_t)(grant | (load << 1));
+    commit_reclaimed[i] = first < t ? reclaimed[i] : 0;
+  }
+  return ORC_OK;
 }
 
 int orc_phi_keys(const orc_window *w, const uint8_t *wf_class, const int8_t *dev,
                  const uint16_t *prio, const uint8_t *flags, int64_t n_plans, orc_phi *keys) {
-  return simulate(w, wf_class, dev, prio, flags, n_plans, NULL, NULL, NULL, NULL, NULL, keys);
+  return simulate(w, wf_class, dev, prio, flags, n_plans, NULL, NULL, NULL, NULL, NULL, NULL, keys);
 }
 
 /* ---------------------------------------------------------------------- */

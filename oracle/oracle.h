@@ -118,13 +118,36 @@ enum {
  * Score plans [0, n_plans) of the row-major batch that starts at dev/prio/
  * flags (dev[p*N+i], prio[p*N+i], flags[p*ceil(N/4)+i/4]).  For a plan with
  * status ORC_INELIGIBLE every other score field is 0 and its schedule rows
- * are left untouched.  start/finish/load_start ([P][N]) and peak ([P][D])
- * may be NULL.  Thread-safe: no global state.
+ * are left untouched.  start/finish/load_start ([P][N]), peak ([P][D]) and
+ * reclaimed ([P][N]: the mask of models whose copies were reclaimed from the
+ * unit's device before the unit's first action, at the unit's head; 0 for
+ * chain members) may each be NULL.  Thread-safe: no global state.
  */
 int orc_score_plans(const orc_window *w, const int8_t *dev, const uint16_t *prio,
                     const uint8_t *flags, int64_t n_plans, orc_score *scores,
                     int64_t *start_us, int64_t *finish_us, int64_t *load_start_us,
-                    int32_t *peak_mib);
+                    int32_t *peak_mib, uint64_t *reclaimed);
+
+/*
+ * The prefix commit of Algorithm 1 (Prefix_t: of the selected plan, the
+ * actions executable before the window is planned again), for one plan's
+ * device row and schedule (as orc_score_plans writes them), read thus:
+ *   - the window is planned again at the next predicted event after the
+ *     window time 0: the earliest activation finish, load end (load start
+ *     + the model's load time on the unit's device) or workflow arrival that
+ *     is later than 0; INT64_MAX when there is none;
+ *   - every action that begins before that event is committed: commit[i]
+ *     bit 0 when activation i starts before it (the unit's grant), bit 1
+ *     when i's load starts before it;
+ *   - the reclamations of a unit whose first action (its load, else its
+ *     start) begins before the event are committed with it:
+ *     commit_reclaimed[i] = reclaimed[i] then, else 0.
+ * Returns ORC_ERR_INDEX for a device entry outside 0 .. n_dev-1.
+ */
+int orc_prefix(const orc_window *w, const int8_t *dev, const int64_t *start_us,
+               const int64_t *finish_us, const int64_t *load_start_us,
+               const uint64_t *reclaimed, uint8_t *commit, uint64_t *commit_reclaimed,
+               int64_t *t_next_us);
 
 /*
  * The lexicographic ranking key of Eq. 12 (Sec. 3.5),

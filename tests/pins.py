@@ -97,7 +97,8 @@ def form_units(win, dev_row, prio_row, fuse_row):
 
 
 def replay_lifecycle(win, units):
-    """Per unit: (miss, n_evicted, used_after, peak_candidate, over_capacity).
+    """Per unit: (miss, n_evicted, used_after, peak_candidate, over_capacity,
+    mask of the evicted models).
 
     Each unit's state is recomputed from the snapshot by replaying its
     device's prefix."""
@@ -116,7 +117,7 @@ def replay_lifecycle(win, units):
         used = sum(int(W[m]) for m in resident)
         miss = u.model not in resident
         need = (int(W[u.model]) if miss else 0) + mx
-        evicted = 0
+        evicted, gone = 0, 0
         while used + need > cap[d]:
             cands = [m for m in resident if m != u.model]
             if not cands:
@@ -130,11 +131,12 @@ def replay_lifecycle(win, units):
             resident.discard(victim)
             used -= int(W[victim])
             evicted += 1
+            gone |= 1 << victim
         over = used + need > cap[d]
         if miss:
             resident.add(u.model)
             used += int(W[u.model])
-        return miss, evicted, used, used + mx, over
+        return miss, evicted, used, used + mx, over, gone
 
     out = {}
     for d, seq in seqs.items():
@@ -254,11 +256,15 @@ def independent_score(win, dev_row, prio_row, fuse_row, pf_row):
         makespan, p95 = 0, 0
     obj = np.float32(np.float32(win.w_makespan) * np.float32(makespan)) + \
         np.float32(np.float32(win.w_p95) * np.float32(p95))
+    reclaimed = np.zeros(win.n_act, np.uint64)
+    for h in life:
+        reclaimed[h] = life[h][5]
     return dict(status=status, makespan_us=makespan, p95_us=p95, objective=np.float32(obj),
                 min_headroom_mib=int((cap - peak).min()),
                 n_loads=min(65535, sum(1 for h in life if life[h][0])),
                 n_evicts=min(65535, sum(life[h][1] for h in life)),
-                start=start, finish=finish, load_start=load_start, peak=peak, units=units)
+                start=start, finish=finish, load_start=load_start, peak=peak, units=units,
+                reclaimed=reclaimed)
 
 
 def plan_rows(win, plans, p):
@@ -281,7 +287,9 @@ def compare_plan(win, plans, p, oracle_scores, oracle_sched) -> List[str]:
     if np.float32(sc["objective"]).view(np.uint32) != np.float32(ref["objective"]).view(np.uint32):
         errs.append(f"plan {p}: objective {sc['objective']} != {ref['objective']}")
     if oracle_sched is not None:
-        st, fi, ls, pk = (x[p] for x in oracle_sched)
+        st, fi, ls, pk = (x[p] for x in oracle_sched[:4])
+        if len(oracle_sched) > 4 and not np.array_equal(oracle_sched[4][p], ref["reclaimed"]):
+            errs.append(f"plan {p}: reclaimed copies differ")
         for name, a, b in (("start", st, ref["start"]), ("finish", fi, ref["finish"]),
                            ("load_start", ls, ref["load_start"]), ("peak", pk, ref["peak"])):
             if not np.array_equal(np.asarray(a, np.int64), np.asarray(b, np.int64)):

@@ -1,7 +1,9 @@
 """The oracle against an independent second formulation (tests/pins.py) on
 random windows with every feature switched on: arrivals, device free times,
 initial residency, ineligible entries, fused chains, prefetch bits, priority
-ties, and capacities tight enough to force evictions and over-capacity."""
+ties, and capacities tight enough to force evictions and over-capacity.
+Also the copies each unit reclaims (schedule output), from the replayed
+resident sets."""
 import numpy as np
 import pytest
 
@@ -11,7 +13,7 @@ import pins
 
 
 def _check(win, plans):
-    sc, sched = oracle.score(win, plans, schedule=True)
+    sc, sched = oracle.score(win, plans, schedule=True, reclaims=True)
     errs = []
     for p in range(plans.n_plans):
         errs += pins.compare_plan(win, plans, p, sc, sched)

@@ -18,6 +18,7 @@ import test_oracle_search as t_search
 import test_oracle_phi as t_phi
 import test_oracle_victim as t_vic
 import test_oracle_batch as t_batch
+import test_oracle_prefix as t_prefix
 
 # (name, original fragment, planted mistake)
 MUTANTS = [
@@ -106,6 +107,17 @@ MUTANTS = [
     ("no wait for running units", "|| next_fin == INT64_MAX) break;", "|| 1) break;"),
     ("slot that frees last", "if (sf[k] < sf[ks]) ks = k;", "if (sf[k] > sf[ks]) ks = k;"),
     ("queue overtaking", "dispatched[d] = t;", ""),
+    # reclaimed copies per unit, prefix commit (Algorithm 1, Prefix_t)
+    ("reclaims not reported", "if (rec_row) rec_row[h] |= 1ull << victim;", ""),
+    ("prefix counts events at time 0", "if (finish_us[i] > 0 && finish_us[i] < t)",
+     "if (finish_us[i] >= 0 && finish_us[i] < t)"),
+    ("prefix ignores load ends", "if (le > 0 && le < t) t = le;", ""),
+    ("prefix load end without the load", "const int64_t le = load_start_us[i] + w->load_us[(int64_t)w->act_model[i] * D + dev[i]];",
+     "const int64_t le = load_start_us[i];"),
+    ("prefix ignores arrivals", "if (w->wf_arrival_us[f] > 0 && w->wf_arrival_us[f] < t) t = w->wf_arrival_us[f];", ""),
+    ("prefix commits at the event", "const int grant = start_us[i] < t;", "const int grant = start_us[i] <= t;"),
+    ("prefix reclaims follow the start", "const int64_t first = load_start_us[i] >= 0 ? load_start_us[i] : start_us[i];",
+     "const int64_t first = start_us[i];"),
 ]
 
 
@@ -140,6 +152,9 @@ def _pin_checks():
     checks += [lambda n=n: t_batch.test_worked_examples(n) for n in ("batch_memory", "batch_lease")]
     checks += [lambda s=s: t_batch.test_contention_free_longest_path(s) for s in (0, 1, 2, 3, 5, 6)]
     checks += [lambda s=s: t_batch.test_schedule_invariants(s) for s in range(8)]
+    checks += [t_prefix.test_worked_example]
+    checks += [lambda s=s: t_prefix.test_single_device_chain(s) for s in range(4)]
+    checks += [lambda s=s: t_prefix.test_invariants(s) for s in range(4)]
     return checks
 
 
