@@ -169,12 +169,17 @@ typedef struct {
 } wf_plan_score;
 
 /* Optional schedule output (device pointers, row-major per plan).  Rows of
- * WF_ST_INELIGIBLE plans are unspecified. */
+ * WF_ST_INELIGIBLE plans are unspecified.  The first four arrays are
+ * required when a schedule is requested; reclaimed_models may be NULL. */
 typedef struct {
   int64_t *start_us;       /* [P][N] start of each activation                 */
   int64_t *finish_us;      /* [P][N] finish of each activation                */
   int64_t *load_start_us;  /* [P][N] load start of a unit head, -1 otherwise  */
   int32_t *peak_mib;       /* [P][D] peak memory of each device               */
+  uint64_t *reclaimed_models; /* [P][N] at a unit head: bit m set when the copy
+                                 of model m was reclaimed from the unit's device
+                                 before the unit's first action (Eq. 5, Sec. 3.5
+                                 reclamation); 0 for chain members          */
 } wf_plan_sched;
 
 /* Create a context on HIP device `hip_device`.  On failure *out is NULL and
@@ -311,6 +316,30 @@ wf_status wf_plan_search_keys(wf_plan_ctx *ctx, const int8_t *dev, const uint16_
  * concurrently on different streams.  Asynchronous on hip_stream. */
 wf_status wf_plan_argmin_keys(wf_plan_ctx *ctx, const wf_plan_key *keys, int64_t n_plans,
                               int64_t *out_index, void *hip_stream);
+
+/* The prefix commit of Algorithm 1 (Prefix_t): of one selected plan, the
+ * actions to commit before the window is planned again.  Inputs are the
+ * plan's device row dev [N] and its schedule rows start_us, finish_us,
+ * load_start_us, reclaimed [N] (as wf_plan_score_batch writes them for that
+ * plan; all device memory).  Readings:
+ *   - the window is planned again at the next predicted event after the
+ *     window time 0: the earliest activation finish, load end (load start
+ *     plus the model's load time on the unit's device) or workflow arrival
+ *     that is later than 0; INT64_MAX when there is none -> *t_next_us;
+ *   - every action that begins before that event is committed: commit[i]
+ *     bit 0 when activation i starts before it (the unit's grant), bit 1
+ *     when i's load starts before it;
+ *   - the reclamations before a unit's first action (its load, else its
+ *     start) are committed with it: commit_reclaimed[i] = reclaimed[i] when
+ *     that action begins before the event, else 0.
+ * Outputs commit [N] uint8, commit_reclaimed [N] uint64 and *t_next_us are
+ * device memory.  A device entry outside 0..n_dev-1 (an ineligible plan)
+ * gives unspecified results without touching memory outside the arrays.
+ * N = 0 writes only *t_next_us.  Asynchronous on hip_stream. */
+wf_status wf_plan_prefix(wf_plan_ctx *ctx, const int8_t *dev, const int64_t *start_us,
+                         const int64_t *finish_us, const int64_t *load_start_us,
+                         const uint64_t *reclaimed, uint8_t *commit,
+                         uint64_t *commit_reclaimed, int64_t *t_next_us, void *hip_stream);
 
 /* Time arithmetic the kernels use for the uploaded window: 32 when they
  * carry times as uint32 offsets from the window origin, 64 when they use

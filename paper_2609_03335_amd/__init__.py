@@ -36,10 +36,11 @@ def device_plans(plans, device="cuda"):
 
 
 def score_batch(ctx: Context, dev, prio, flags, n_plans: int, schedule: bool = False,
-                n_act: int = 0, n_dev: int = 0, stream=None):
+                n_act: int = 0, n_dev: int = 0, stream=None, reclaims: bool = False):
     """Allocate outputs on the plans' device and enqueue scoring.  Returns
     the raw score buffer (uint8 [P, 32]) and, with ``schedule``, the
-    (start, finish, load_start, peak) tensors."""
+    (start, finish, load_start, peak) tensors, followed with ``reclaims`` by
+    the [P, N] int64 tensor of reclaimed-model masks (uint64 bits)."""
     import torch
     device = dev.device
     scores = torch.empty((max(1, n_plans), 32), dtype=torch.uint8, device=device)
@@ -49,6 +50,8 @@ def score_batch(ctx: Context, dev, prio, flags, n_plans: int, schedule: bool = F
                  torch.empty((n_plans, max(1, n_act)), dtype=torch.int64, device=device),
                  torch.empty((n_plans, max(1, n_act)), dtype=torch.int64, device=device),
                  torch.empty((n_plans, n_dev), dtype=torch.int32, device=device))
+        if reclaims:
+            sched = sched + (torch.empty((n_plans, max(1, n_act)), dtype=torch.int64, device=device),)
     ctx.wf_plan_score_batch(dev, prio, flags, n_plans, scores, sched, stream)
     return (scores, sched) if schedule else scores
 

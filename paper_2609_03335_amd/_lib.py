@@ -44,7 +44,7 @@ EXPORTS = ("wf_plan_ctx_create", "wf_plan_ctx_destroy", "wf_plan_last_error",
            "wf_plan_validate_window", "wf_plan_upload_window", "wf_plan_score_batch",
            "wf_plan_argmin", "wf_plan_search_batch", "wf_plan_search_rows",
            "wf_plan_score_keys", "wf_plan_search_keys", "wf_plan_argmin_keys",
-           "wf_plan_time_bits", "wf_plan_version")
+           "wf_plan_prefix", "wf_plan_time_bits", "wf_plan_version")
 
 
 class WFError(RuntimeError):
@@ -73,7 +73,8 @@ class wf_window_desc(ctypes.Structure):
 
 class wf_plan_sched(ctypes.Structure):
     _fields_ = [("start_us", ctypes.c_void_p), ("finish_us", ctypes.c_void_p),
-                ("load_start_us", ctypes.c_void_p), ("peak_mib", ctypes.c_void_p)]
+                ("load_start_us", ctypes.c_void_p), ("peak_mib", ctypes.c_void_p),
+                ("reclaimed_models", ctypes.c_void_p)]
 
 
 _lib = None
@@ -115,10 +116,17 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.wf_plan_search_keys.restype = ctypes.c_int
     lib.wf_plan_argmin_keys.argtypes = [vp, vp, i64, vp, vp]
     lib.wf_plan_argmin_keys.restype = ctypes.c_int
+    lib.wf_plan_prefix.argtypes = [vp] * 10
+    lib.wf_plan_prefix.restype = i32
     lib.wf_plan_time_bits.argtypes = [vp]
     lib.wf_plan_time_bits.restype = i32
     lib.wf_plan_version.argtypes = []
     lib.wf_plan_version.restype = ctypes.c_char_p
+    # an entry point without a declared signature would take Python ints as
+    # 32-bit C ints and cut device addresses short
+    for name in EXPORTS:
+        if getattr(lib, name).argtypes is None:
+            raise RuntimeError(f"{name}: no ctypes signature declared")
     if path is None:
         _lib = lib
     return lib
@@ -200,14 +208,24 @@ class Context:
 
     def wf_plan_score_batch(self, dev, prio, flags, n_plans: int, scores, sched=None,
                             stream=None) -> None:
-        """dev/prio/flags/scores (and the four schedule arrays) are device
-        buffers: torch tensors or raw device addresses."""
+        """dev/prio/flags/scores (and the schedule arrays: start, finish,
+        load_start, peak and optionally reclaimed) are device buffers: torch
+        tensors or raw device addresses."""
         s = None
         if sched is not None:
             s = wf_plan_sched(*(_ptr(x) for x in sched))
         self._check(self.lib.wf_plan_score_batch(
             self.handle, _ptr(dev), _ptr(prio), _ptr(flags), int(n_plans), _ptr(scores),
             None if s is None else ctypes.byref(s), _stream(stream)))
+
+    def wf_plan_prefix(self, dev, start, finish, load_start, reclaimed, commit,
+                       commit_reclaimed, t_next, stream=None) -> None:
+        """One plan's device row and schedule rows in; commit flags, committed
+        reclamations and the next event time out (all device buffers)."""
+        self._check(self.lib.wf_plan_prefix(
+            self.handle, _ptr(dev), _ptr(start), _ptr(finish), _ptr(load_start),
+            _ptr(reclaimed), _ptr(commit), _ptr(commit_reclaimed), _ptr(t_next),
+            _stream(stream)))
 
     def wf_plan_argmin(self, scores, n_plans: int, out_index, stream=None) -> None:
         self._check(self.lib.wf_plan_argmin(self.handle, _ptr(scores), int(n_plans),

@@ -915,6 +915,34 @@ wf_status wf_plan_search_keys(wf_plan_ctx* ctx, const int8_t* dev, const uint16_
   return WF_OK;
 }
 
+wf_status wf_plan_prefix(wf_plan_ctx* ctx, const int8_t* dev, const int64_t* start_us,
+                         const int64_t* finish_us, const int64_t* load_start_us,
+                         const uint64_t* reclaimed, uint8_t* commit, uint64_t* commit_reclaimed,
+                         int64_t* t_next_us, void* hip_stream) {
+  if (!ctx) {
+    g_thread_err = "ctx is NULL";
+    return WF_EINVAL;
+  }
+  if (!ctx->has_window) return fail(&ctx->err, WF_ENOWINDOW, "no window uploaded");
+  if (!t_next_us) return fail(&ctx->err, WF_EINVAL, "t_next_us is NULL");
+  if (ctx->host.N > 0 && (!dev || !start_us || !finish_us || !load_start_us || !reclaimed ||
+                          !commit || !commit_reclaimed))
+    return fail(&ctx->err, WF_EINVAL, "a plan, schedule or output array is NULL");
+  // the earliest workflow arrival after the window time 0
+  int64_t next_arrival = INT64_MAX;
+  for (int32_t f = 0; f < ctx->host.W; ++f)
+    if (ctx->host.arrival[f] > 0 && ctx->host.arrival[f] < next_arrival) next_arrival = ctx->host.arrival[f];
+  int prev = 0;
+  (void)hipGetDevice(&prev);
+  hipError_t e = hipSetDevice(ctx->device);
+  if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
+  e = wfp::launch_prefix(ctx->dw.sp, next_arrival, dev, start_us, finish_us, load_start_us, reclaimed,
+                         commit, commit_reclaimed, t_next_us, static_cast<hipStream_t>(hip_stream));
+  (void)hipSetDevice(prev);
+  if (e != hipSuccess) return hip_fail(ctx, e, "launching the prefix kernel");
+  return WF_OK;
+}
+
 wf_status wf_plan_argmin_keys(wf_plan_ctx* ctx, const wf_plan_key* keys, int64_t n_plans,
                               int64_t* out_index, void* hip_stream) {
   if (!ctx) {

@@ -152,4 +152,11 @@ hipError_t launch_argmin(const wf_plan_score* scores, int64_t n_plans, int64_t* 
 hipError_t launch_argmin_keys(const wf_plan_key* keys, int64_t n_plans, int64_t* out_index,
                               void* work, hipStream_t stream);
 
+// Prefix commit of one plan (prefix.hip): next_arrival is the earliest
+// workflow arrival later than 0 (INT64_MAX when none).
+hipError_t launch_prefix(const ScoreParams& sp, int64_t next_arrival, const int8_t* dev,
+                         const int64_t* start, const int64_t* finish, const int64_t* load_start,
+                         const uint64_t* reclaimed, uint8_t* commit, uint64_t* commit_rec,
+                         int64_t* t_next, hipStream_t stream);
+
 }  // namespace wfp

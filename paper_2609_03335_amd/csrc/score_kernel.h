@@ -897,6 +897,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
             const int u = (int)(X.meta & 0xffffu);
             const int m = (int)((X.meta >> 16) & 63u);
             const uint64_t mbit = 1ull << m;
+            uint64_t urec = 0ull;  // copies reclaimed for this unit (schedule output)
             bool hit;
             int32_t w0 = 0, w1 = 0;
             if constexpr (!NIBBLE) hit = ((res >> m) & 1ull) != 0ull;
@@ -979,6 +980,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
                     v = victim_lru(cand, X.slot);
                   res &= ~(1ull << v);
                   if constexpr (PHI) ph_rec |= 1ull << v;
+                  urec |= 1ull << v;
                   used -= t_wmib[v];
                   ++nev;
                 }
@@ -998,6 +1000,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
               while (used + need > capd && nq > 0) {
                 const int v = (int)(Q & (QT)15);
                 if constexpr (PHI) ph_rec |= 1ull << v;
+                urec |= 1ull << v;
                 Q >>= 4;
                 --nq;
                 nd = nd > 0 ? nd - 1 : 0;
@@ -1024,6 +1027,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
                 const int v = victim_paper(cand);
                 res &= ~(1ull << v);
                 if constexpr (PHI) ph_rec |= 1ull << v;
+                urec |= 1ull << v;
                 used -= t_wmib[v];
                 ++nev;
               }
@@ -1039,6 +1043,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
                 const int v = victim_lru(cand, X.slot);
                 res &= ~(1ull << v);
                 if constexpr (PHI) ph_rec |= 1ull << v;
+                urec |= 1ull << v;
                 used -= t_wmib[v];
                 ++nev;
               }
@@ -1101,6 +1106,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
                   sched.finish_us[pw * N + v] = sp.origin + TO::i64(tv);
                   sched.load_start_us[pw * N + v] =
                       (v == u && !hit) ? sp.origin + TO::i64(ls) : (int64_t)-1;
+                  if (sched.reclaimed_models) sched.reclaimed_models[pw * N + v] = v == u ? urec : 0ull;
                 }
                 t = tv;
                 const int c = t_cnext[v];

@@ -37,6 +37,24 @@ def test_exports_every_declared_symbol():
     assert pkg.wf_plan_version().startswith("wf_plan")
 
 
+def test_every_entry_point_has_a_full_signature():
+    """Each binding declares the C signature, with one ctypes type per
+    parameter of the header's prototype: an undeclared pointer argument
+    would reach the library cut to 32 bits."""
+    lib = _lib.load()
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    for name in _lib.EXPORTS:
+        m = re.search(r"\b" + name + r"\s*\(([^)]*)\)\s*;", text)
+        assert m, name
+        params = [x for x in m.group(1).split(",") if x.strip() and x.strip() != "void"]
+        argtypes = getattr(lib, name).argtypes
+        assert argtypes is not None, name
+        assert len(argtypes) == len(params), (name, len(argtypes), len(params))
+        for ctype, decl in zip(argtypes, params):
+            if "*" in decl:  # every pointer travels as a full address
+                assert ctype in (ctypes.c_void_p, ctypes.c_char_p) or hasattr(ctype, "contents"), (name, decl)
+
+
 def test_time_bits_without_window():
     assert _lib.load().wf_plan_time_bits(None) == 0
 
