@@ -135,6 +135,8 @@ def main():
                     help="skip the leg that scores with the paper's reclamation order")
     ap.add_argument("--no-keys", action="store_true",
                     help="skip the ranking-key leg (Eq. 12 keys and their argmin)")
+    ap.add_argument("--no-prefix", action="store_true",
+                    help="skip the prefix-commit leg (Algorithm 1's last step, one plan)")
     ap.add_argument("--batch-limit", type=int, default=4,
                     help="units per device at once in the batch-limit leg (1 = skip it)")
     ap.add_argument("--copy-probe", type=int, default=None, metavar="BYTES",
@@ -244,6 +246,45 @@ def main():
                 "kernel": "score_plans", "kernel_ms": round(kernel_ms, 4),
                 "bytes_per_plan": bpp, "copy_gbs_measured": round(copy_gbs, 1),
                 "frac_of_copy": round(achieved / copy_gbs, 4), "argmin_ms": round(argmin_ms, 4)}
+
+    # the prefix commit of the selected plan (Algorithm 1's last step): the
+    # plan scored again with its schedule, then the actions to commit before
+    # the next predicted event
+    prefix_leg = None
+    b_idx = int(best.item())
+    if b_idx >= 0 and not args.no_prefix:
+        rows = (dev[b_idx:b_idx + 1], prio[b_idx:b_idx + 1], flags[b_idx:b_idx + 1])
+        _, sch = pkg.score_batch(ctx, *rows, 1, schedule=True, n_act=N, n_dev=D, reclaims=True,
+                                 stream=stream)
+        commit = torch.empty(max(N, 1), dtype=torch.uint8, device="cuda:0")
+        crec = torch.empty(max(N, 1), dtype=torch.int64, device="cuda:0")
+        t_next = torch.empty(1, dtype=torch.int64, device="cuda:0")
+        pargs = (rows[0][0], sch[0][0], sch[1][0], sch[2][0], sch[4][0], commit, crec, t_next)
+        ctx.wf_plan_prefix(*pargs, stream)
+        torch.cuda.synchronize()
+        if args.check:
+            import oracle
+            one = plans.take(np.array([b_idx]))
+            _, rs = oracle.score(win, one, schedule=True, reclaims=True)
+            c, cr, t = oracle.prefix(win, one.dev[0], rs[0][0], rs[1][0], rs[2][0], rs[4][0])
+            if (int(t_next.item()) != t or not np.array_equal(commit.cpu().numpy()[:N], c)
+                    or not np.array_equal(crec.cpu().numpy()[:N].view(np.uint64), cr)):
+                print("[bench] prefix commit differs from the oracle", file=sys.stderr)
+                sys.exit(1)
+        pev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(args.steps)]
+        for a, b in pev:
+            a.record(stream)
+            ctx.wf_plan_prefix(*pargs, stream)
+            b.record(stream)
+        torch.cuda.synchronize()
+        cm = commit.cpu().numpy()[:N]
+        prefix_leg = {"us": round(float(np.mean([a.elapsed_time(b) for a, b in pev])) * 1e3, 2),
+                      "plan": b_idx, "t_next_us": int(t_next.item()),
+                      "grants": int((cm & 1).astype(bool).sum()),
+                      "loads": int((cm & 2).astype(bool).sum()),
+                      "note": "prefix commit of the selected plan (Algorithm 1): the grants, loads "
+                              "and reclamations that begin before its next predicted event"}
 
     # candidates generated around plan 0 on the GPU and scored (no plan rows
     # in HBM): the same number of plans, same window
@@ -406,6 +447,7 @@ def main():
         "keys": keys_leg,
         "paper_order": paper_leg,
         "batch_limit": batch_leg,
+        "prefix": prefix_leg,
     }
     print(json.dumps(line))
     ctx.close()
