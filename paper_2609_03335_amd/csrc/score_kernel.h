@@ -213,13 +213,13 @@ struct UnitPre {
 template <bool PHI>
 using OutRec = std::conditional_t<PHI, wf_plan_key, wf_plan_score>;
 
-template <typename TT, bool TAB_LDS, int QB, bool WAVE_GLOBAL, bool SEARCH, bool PHI>
+template <typename TT, bool TAB_LDS, int QB, bool WAVE_GLOBAL, bool SEARCH, bool PHI, bool SCHED>
 __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
                                                    const int8_t* __restrict__ dev_all,
                                                    const uint16_t* __restrict__ prio_all,
                                                    const uint8_t* __restrict__ flags_all, int64_t P,
                                                    OutRec<PHI>* __restrict__ scores,
-                                                   wf_plan_sched sched, int has_sched,
+                                                   wf_plan_sched sched, int has_sched_arg,
                                                    SearchArgs sa) {
   using TO = TimeOps<TT>;
   using TB = typename TO::bits_t;
@@ -302,6 +302,9 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   const int g_me = lane / D;
   // every unit's finish goes through the general path when the schedule is
   // written out
+  // SCHED: the schedule is written (known at compile time, so that the
+  // instantiations without one carry none of its code or registers)
+  const bool has_sched = SCHED && has_sched_arg != 0;
   const uint32_t slow0 = has_sched ? kSlow : 0u;
   const int d_me = lane - g_me * D;
   const int64_t n_groups = (P + G - 1) / G;
@@ -897,7 +900,10 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
             const int u = (int)(X.meta & 0xffffu);
             const int m = (int)((X.meta >> 16) & 63u);
             const uint64_t mbit = 1ull << m;
-            uint64_t urec = 0ull;  // copies reclaimed for this unit (schedule output)
+            // copies reclaimed for this unit (schedule output), accumulated
+            // in place so that nothing stays live in registers without one
+            const bool rec_on = has_sched && sched.reclaimed_models != nullptr;
+            if (rec_on) sched.reclaimed_models[pw * N + u] = 0ull;
             bool hit;
             int32_t w0 = 0, w1 = 0;
             if constexpr (!NIBBLE) hit = ((res >> m) & 1ull) != 0ull;
@@ -980,7 +986,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
                     v = victim_lru(cand, X.slot);
                   res &= ~(1ull << v);
                   if constexpr (PHI) ph_rec |= 1ull << v;
-                  urec |= 1ull << v;
+                  if (rec_on) sched.reclaimed_models[pw * N + u] |= 1ull << v;
                   used -= t_wmib[v];
                   ++nev;
                 }
@@ -1000,7 +1006,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
               while (used + need > capd && nq > 0) {
                 const int v = (int)(Q & (QT)15);
                 if constexpr (PHI) ph_rec |= 1ull << v;
-                urec |= 1ull << v;
+                if (rec_on) sched.reclaimed_models[pw * N + u] |= 1ull << v;
                 Q >>= 4;
                 --nq;
                 nd = nd > 0 ? nd - 1 : 0;
@@ -1027,7 +1033,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
                 const int v = victim_paper(cand);
                 res &= ~(1ull << v);
                 if constexpr (PHI) ph_rec |= 1ull << v;
-                urec |= 1ull << v;
+                if (rec_on) sched.reclaimed_models[pw * N + u] |= 1ull << v;
                 used -= t_wmib[v];
                 ++nev;
               }
@@ -1043,7 +1049,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
                 const int v = victim_lru(cand, X.slot);
                 res &= ~(1ull << v);
                 if constexpr (PHI) ph_rec |= 1ull << v;
-                urec |= 1ull << v;
+                if (rec_on) sched.reclaimed_models[pw * N + u] |= 1ull << v;
                 used -= t_wmib[v];
                 ++nev;
               }
@@ -1106,7 +1112,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
                   sched.finish_us[pw * N + v] = sp.origin + TO::i64(tv);
                   sched.load_start_us[pw * N + v] =
                       (v == u && !hit) ? sp.origin + TO::i64(ls) : (int64_t)-1;
-                  if (sched.reclaimed_models) sched.reclaimed_models[pw * N + v] = v == u ? urec : 0ull;
+                  if (rec_on && v != u) sched.reclaimed_models[pw * N + v] = 0ull;
                 }
                 t = tv;
                 const int c = t_cnext[v];
@@ -1267,12 +1273,12 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   }
 }
 
-template <typename TT, bool TAB_LDS, int QB, bool WAVE_GLOBAL, bool SEARCH, bool PHI>
+template <typename TT, bool TAB_LDS, int QB, bool WAVE_GLOBAL, bool SEARCH, bool PHI, bool SCHED>
 hipError_t launch_variant(const ScoreParams& sp, const int8_t* dev, const uint16_t* prio,
                           const uint8_t* flags, int64_t n_plans, OutRec<PHI>* out,
                           const wf_plan_sched& s, int has, const SearchArgs& sa,
                           hipStream_t stream) {
-  auto k = score_plans<TT, TAB_LDS, QB, WAVE_GLOBAL, SEARCH, PHI>;
+  auto k = score_plans<TT, TAB_LDS, QB, WAVE_GLOBAL, SEARCH, PHI, SCHED>;
   (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k),
                             hipFuncAttributeMaxDynamicSharedMemorySize, sp.lds_bytes);
   hipLaunchKernelGGL(k, dim3(sp.grid), dim3(64 * sp.waves), sp.lds_bytes, stream, sp, dev, prio,
@@ -1280,53 +1286,62 @@ hipError_t launch_variant(const ScoreParams& sp, const int8_t* dev, const uint16
   return hipGetLastError();
 }
 
-template <typename TT, int QB, bool SEARCH, bool PHI>
+template <typename TT, int QB, bool SEARCH, bool PHI, bool SCHED>
 hipError_t launch_place(const ScoreParams& sp, const int8_t* dev, const uint16_t* prio,
                         const uint8_t* flags, int64_t n_plans, OutRec<PHI>* out,
                         const wf_plan_sched& s, int has, const SearchArgs& sa, hipStream_t stream) {
   if (sp.wave_global)
-    return launch_variant<TT, false, QB, true, SEARCH, PHI>(sp, dev, prio, flags, n_plans, out, s,
-                                                            has, sa, stream);
+    return launch_variant<TT, false, QB, true, SEARCH, PHI, SCHED>(sp, dev, prio, flags, n_plans,
+                                                                   out, s, has, sa, stream);
   if (sp.tab_in_lds)
-    return launch_variant<TT, true, QB, false, SEARCH, PHI>(sp, dev, prio, flags, n_plans, out, s,
-                                                            has, sa, stream);
-  return launch_variant<TT, false, QB, false, SEARCH, PHI>(sp, dev, prio, flags, n_plans, out, s,
-                                                           has, sa, stream);
+    return launch_variant<TT, true, QB, false, SEARCH, PHI, SCHED>(sp, dev, prio, flags, n_plans,
+                                                                   out, s, has, sa, stream);
+  return launch_variant<TT, false, QB, false, SEARCH, PHI, SCHED>(sp, dev, prio, flags, n_plans,
+                                                                  out, s, has, sa, stream);
 }
 
-template <typename TT, bool SEARCH, bool PHI>
+template <typename TT, bool SEARCH, bool PHI, bool SCHED>
 hipError_t launch_time(const ScoreParams& sp, const int8_t* dev, const uint16_t* prio,
                        const uint8_t* flags, int64_t n_plans, OutRec<PHI>* out,
                        const wf_plan_sched& s, int has, const SearchArgs& sa, hipStream_t stream) {
-  if (sp.nibble == -1)
-    return launch_place<TT, -1, SEARCH, PHI>(sp, dev, prio, flags, n_plans, out, s, has, sa, stream);
-  if (sp.nibble == -2)
-    return launch_place<TT, -2, SEARCH, PHI>(sp, dev, prio, flags, n_plans, out, s, has, sa, stream);
-  if (sp.nibble == -3)
-    return launch_place<TT, -3, SEARCH, PHI>(sp, dev, prio, flags, n_plans, out, s, has, sa, stream);
-  if (sp.nibble == 32)
-    return launch_place<TT, 32, SEARCH, PHI>(sp, dev, prio, flags, n_plans, out, s, has, sa, stream);
-  if (sp.nibble == 64)
-    return launch_place<TT, 64, SEARCH, PHI>(sp, dev, prio, flags, n_plans, out, s, has, sa, stream);
-  return launch_place<TT, 0, SEARCH, PHI>(sp, dev, prio, flags, n_plans, out, s, has, sa, stream);
+  switch (sp.nibble) {
+    case -1:
+      return launch_place<TT, -1, SEARCH, PHI, SCHED>(sp, dev, prio, flags, n_plans, out, s, has, sa, stream);
+    case -2:
+      return launch_place<TT, -2, SEARCH, PHI, SCHED>(sp, dev, prio, flags, n_plans, out, s, has, sa, stream);
+    case -3:
+      return launch_place<TT, -3, SEARCH, PHI, SCHED>(sp, dev, prio, flags, n_plans, out, s, has, sa, stream);
+    case 32:
+      return launch_place<TT, 32, SEARCH, PHI, SCHED>(sp, dev, prio, flags, n_plans, out, s, has, sa, stream);
+    case 64:
+      return launch_place<TT, 64, SEARCH, PHI, SCHED>(sp, dev, prio, flags, n_plans, out, s, has, sa, stream);
+    default:
+      return launch_place<TT, 0, SEARCH, PHI, SCHED>(sp, dev, prio, flags, n_plans, out, s, has, sa, stream);
+  }
 }
 
 // Plans from HBM rows, or candidates generated around an incumbent; fp64 or
-// uint32 times.
+// uint32 times; with or without the schedule output (rows from HBM only).
 template <bool PHI>
 hipError_t launch_all(const ScoreParams& sp, const int8_t* dev, const uint16_t* prio,
                       const uint8_t* flags, int64_t n_plans, OutRec<PHI>* out,
                       const wf_plan_sched* sched, const SearchArgs* search, hipStream_t stream) {
   wf_plan_sched s{};
   if (sched) s = *sched;
-  const int has = sched != nullptr && !search;
   const SearchArgs sa = search ? *search : SearchArgs{};
-  if (sp.time64) {
-    if (search) return launch_time<double, true, PHI>(sp, dev, prio, flags, n_plans, out, s, 0, sa, stream);
-    return launch_time<double, false, PHI>(sp, dev, prio, flags, n_plans, out, s, has, sa, stream);
+  if constexpr (!PHI) {
+    if (sched && !search) {
+      if (sp.time64)
+        return launch_time<double, false, false, true>(sp, dev, prio, flags, n_plans, out, s, 1, sa, stream);
+      return launch_time<uint32_t, false, false, true>(sp, dev, prio, flags, n_plans, out, s, 1, sa, stream);
+    }
   }
-  if (search) return launch_time<uint32_t, true, PHI>(sp, dev, prio, flags, n_plans, out, s, 0, sa, stream);
-  return launch_time<uint32_t, false, PHI>(sp, dev, prio, flags, n_plans, out, s, has, sa, stream);
+  if (sp.time64) {
+    if (search) return launch_time<double, true, PHI, false>(sp, dev, prio, flags, n_plans, out, s, 0, sa, stream);
+    return launch_time<double, false, PHI, false>(sp, dev, prio, flags, n_plans, out, s, 0, sa, stream);
+  }
+  if (search) return launch_time<uint32_t, true, PHI, false>(sp, dev, prio, flags, n_plans, out, s, 0, sa, stream);
+  return launch_time<uint32_t, false, PHI, false>(sp, dev, prio, flags, n_plans, out, s, 0, sa, stream);
 }
 
 }  // namespace
