@@ -144,9 +144,9 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py scores plans on one GPU only; multi-GPU runs are not part of this "
-              "build (plans are independent: see DESIGN.md for how the batch would shard)",
-              file=sys.stderr)
+        print("bench.py scores plans on one GPU only; runs on several GPUs are not supported "
+              "(plans are independent: a batch would split into one range per GPU, with one "
+              "exchange of the per-GPU argmin keys)", file=sys.stderr)
         sys.exit(2)
 
     import torch

@@ -72,10 +72,10 @@ typedef enum {
   WF_ENOWINDOW = 2,     /* score/argmin before a successful upload          */
   WF_ENOMEM = 3,        /* host or device allocation failed                 */
   WF_EHIP = 4,          /* HIP runtime error (message has the HIP string)   */
-  WF_EUNSUPPORTED = 5   /* valid but outside this build's limits            */
+  WF_EUNSUPPORTED = 5   /* valid but outside the library's limits           */
 } wf_status;
 
-/* Limits of this build. */
+/* Limits of the library. */
 #define WF_MAX_ACT 65535    /* activations per window                     */
 #define WF_MAX_MODELS 64    /* models (resident sets are 64-bit masks)    */
 #define WF_MAX_DEV 64       /* devices in the pool                        */
