@@ -128,7 +128,7 @@ def main():
                     help="plans in the CPU-baseline sample (default: about 10 s of CPU work)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--check", type=int, default=4096,
-                    help="plans checked against the oracle before timing (0 = none)")
+                    help="plans per leg checked against the oracle in the CPU-baseline leg (0 = none)")
     ap.add_argument("--search-mut", type=int, default=2,
                     help="mutations per generated candidate in the search leg (-1 = skip it)")
     ap.add_argument("--no-paper-order", action="store_true",
@@ -176,18 +176,18 @@ def main():
         ctx.wf_plan_score_batch(dev, prio, flags, P, scores, None, stream)
         ctx.wf_plan_argmin(scores, P, best, stream)
 
-    # correctness gate on a sample before timing
+    # samples of every leg's GPU records, checked against the oracle in the
+    # CPU-baseline leg (the one part of this script that runs the oracle):
+    # (what, GPU bytes, function of the oracle module giving its bytes)
+    checks = []
+    T = min(16, os.cpu_count() or 1)
     if args.check:
-        import oracle
         step()
         torch.cuda.synchronize()
         idx = np.unique(np.linspace(0, P - 1, min(P, args.check)).astype(np.int64))
         got = pkg.scores_to_numpy(scores, P)[idx]
-        ref = oracle.score(win, plans.take(idx), threads=min(16, os.cpu_count() or 1))
-        if got.tobytes() != ref.tobytes():
-            print("[bench] GPU scores differ from the oracle", file=sys.stderr)
-            sys.exit(1)
-        print(f"[bench] {len(idx)} sampled plans bit-exact vs oracle", file=sys.stderr, flush=True)
+        checks.append(("scores", got.tobytes(),
+                       lambda o, idx=idx: o.score(win, plans.take(idx), threads=T).tobytes()))
 
     for _ in range(args.warmup):
         step()
@@ -263,14 +263,15 @@ def main():
         ctx.wf_plan_prefix(*pargs, stream)
         torch.cuda.synchronize()
         if args.check:
-            import oracle
-            one = plans.take(np.array([b_idx]))
-            _, rs = oracle.score(win, one, schedule=True, reclaims=True)
-            c, cr, t = oracle.prefix(win, one.dev[0], rs[0][0], rs[1][0], rs[2][0], rs[4][0])
-            if (int(t_next.item()) != t or not np.array_equal(commit.cpu().numpy()[:N], c)
-                    or not np.array_equal(crec.cpu().numpy()[:N].view(np.uint64), cr)):
-                print("[bench] prefix commit differs from the oracle", file=sys.stderr)
-                sys.exit(1)
+            got = (np.array([t_next.item()], np.int64).tobytes() + commit.cpu().numpy()[:N].tobytes()
+                   + crec.cpu().numpy()[:N].tobytes())
+
+            def prefix_ref(o, b_idx=b_idx):
+                one = plans.take(np.array([b_idx]))
+                _, rs = o.score(win, one, schedule=True, reclaims=True)
+                c, cr, t = o.prefix(win, one.dev[0], rs[0][0], rs[1][0], rs[2][0], rs[4][0])
+                return np.array([t], np.int64).tobytes() + c.tobytes() + cr.tobytes()
+            checks.append(("prefix commit", got, prefix_ref))
         pev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
                for _ in range(args.steps)]
         for a, b in pev:
@@ -293,16 +294,16 @@ def main():
         sd, sp_, sf = dev[0].contiguous(), prio[0].contiguous(), flags[0].contiguous()
         seed = 0x5EED
         if args.check:
-            import oracle
             n_chk = min(P, args.check)
             ctx.wf_plan_search_batch(sd, sp_, sf, seed, args.search_mut, 0, n_chk, scores, stream)
             torch.cuda.synchronize()
-            inc = (plans.dev[0], plans.prio[0], plans.flags[0])
-            cand = workload.PlanBatch(*oracle.search_candidates(win, *inc, seed, args.search_mut, 0, n_chk))
-            ref = oracle.score(win, cand, threads=min(16, os.cpu_count() or 1))
-            if pkg.scores_to_numpy(scores, n_chk).tobytes() != ref.tobytes():
-                print("[bench] generated candidates differ from the oracle", file=sys.stderr)
-                sys.exit(1)
+
+            def search_ref(o, n_chk=n_chk, seed=seed):
+                inc = (plans.dev[0], plans.prio[0], plans.flags[0])
+                cand = workload.PlanBatch(*o.search_candidates(win, *inc, seed, args.search_mut, 0, n_chk))
+                return o.score(win, cand, threads=T).tobytes()
+            checks.append(("generated candidates", pkg.scores_to_numpy(scores, n_chk).tobytes(),
+                           search_ref))
         for _ in range(args.warmup):
             ctx.wf_plan_search_batch(sd, sp_, sf, seed, args.search_mut, 0, P, scores, stream)
         torch.cuda.synchronize()
@@ -325,16 +326,12 @@ def main():
     if not args.no_keys:
         keys = scores  # 32 bytes per plan as well
         if args.check:
-            import oracle
             n_chk = min(P, args.check)
             idx = np.unique(np.linspace(0, P - 1, n_chk).astype(np.int64))
             ctx.wf_plan_score_keys(dev, prio, flags, P, keys, stream)
             torch.cuda.synchronize()
-            got = pkg.keys_to_numpy(keys, P)[idx]
-            ref = oracle.phi_keys(win, plans.take(idx), threads=min(16, os.cpu_count() or 1))
-            if got.tobytes() != ref.tobytes():
-                print("[bench] ranking keys differ from the oracle", file=sys.stderr)
-                sys.exit(1)
+            checks.append(("ranking keys", pkg.keys_to_numpy(keys, P)[idx].tobytes(),
+                           lambda o, idx=idx: o.phi_keys(win, plans.take(idx), threads=T).tobytes()))
         out_k = torch.empty(1, dtype=torch.int64, device="cuda:0")
         for _ in range(args.warmup):
             ctx.wf_plan_score_keys(dev, prio, flags, P, keys, stream)
@@ -358,19 +355,16 @@ def main():
                             "their lexicographic argmin"}
 
     def window_leg(win_v, what):
-        """The same plans scored under a variant of the window: checked against
-        the oracle on a sample, then timed like the main leg."""
+        """The same plans scored under a variant of the window: a sample kept
+        for the oracle check, then timed like the main leg."""
         ctx.wf_plan_upload_window(win_v)
         if args.check:
-            import oracle
             n_chk = min(P, args.check)
             idx = np.unique(np.linspace(0, P - 1, n_chk).astype(np.int64))
             ctx.wf_plan_score_batch(dev, prio, flags, P, scores, None, stream)
             torch.cuda.synchronize()
-            ref = oracle.score(win_v, plans.take(idx), threads=min(16, os.cpu_count() or 1))
-            if pkg.scores_to_numpy(scores, P)[idx].tobytes() != ref.tobytes():
-                print(f"[bench] {what}: scores differ from the oracle", file=sys.stderr)
-                sys.exit(1)
+            checks.append((what, pkg.scores_to_numpy(scores, P)[idx].tobytes(),
+                           lambda o, idx=idx: o.score(win_v, plans.take(idx), threads=T).tobytes()))
         for _ in range(args.warmup):
             ctx.wf_plan_score_batch(dev, prio, flags, P, scores, None, stream)
         torch.cuda.synchronize()
@@ -428,6 +422,17 @@ def main():
                "sample": f"{what}, {threads} threads, {dt:.2f} s wall, {dc:.1f} s CPU "
                          f"({cpu_model()}, {os.cpu_count()} logical CPUs visible)",
                "value_1_thread": round(n1 / d1, 1)}
+        # every leg's sampled records against the oracle
+        for name, got, ref_fn in checks:
+            if got != ref_fn(oracle):
+                print(f"[bench] {name}: GPU records differ from the oracle", file=sys.stderr)
+                sys.exit(1)
+        if checks:
+            print(f"[bench] {len(checks)} legs' sampled records bit-exact vs the oracle",
+                  file=sys.stderr, flush=True)
+    elif checks:
+        print("[bench] no CPU-baseline leg: the sampled records were not checked against the oracle",
+              file=sys.stderr, flush=True)
 
     line = {
         "metric": "candidate plans scored/sec at 1 GPU; achieved HBM GB/s vs peak",
