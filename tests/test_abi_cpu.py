@@ -202,3 +202,27 @@ def test_device_buffers_are_row_major():
         assert t.numpy().tobytes() == np.ascontiguousarray(a).tobytes()
     with pytest.raises(ValueError):
         _lib._ptr(torch.zeros((4, 3), dtype=torch.int16).t())
+
+
+def _struct_fields(name):
+    """Member names of `typedef struct { ... } name;` in the header, in order."""
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    m = re.search(r"typedef struct\s*\{([^}]*)\}\s*" + name + r"\s*;", text)
+    assert m, name
+    out = []
+    for decl in m.group(1).split(";"):
+        decl = decl.strip()
+        if not decl:
+            continue
+        # "const int32_t *a, *b" or "float w_makespan, w_p95" or "uint16_t admitted[4]"
+        head, *rest = decl.split(",")
+        names = [head.split()[-1]] + [r.strip() for r in rest]
+        out += [re.sub(r"[\*\s]|\[.*\]", "", n) for n in names]
+    return out
+
+
+@pytest.mark.parametrize("name", ["wf_window_desc", "wf_plan_sched"])
+def test_binding_structs_follow_the_header(name):
+    """The ctypes mirrors list the header's members in the header's order."""
+    py = [f[0] for f in getattr(_lib, name)._fields_]
+    assert py == _struct_fields(name)
