@@ -133,3 +133,22 @@ def test_prefix_arguments(ctx):
         assert e.value.status == pkg.WF_ENOWINDOW
     finally:
         c2.close()
+
+
+def test_empty_window(ctx):
+    """No activations: only the next event is written (none: INT64_MAX), and
+    the plan and schedule arrays may be NULL."""
+    win = W.Window(n_act=0, n_wf=0, n_models=2, n_dev=3, act_wf=np.zeros(0, np.int32),
+                   act_model=np.zeros(0, np.int32), pred_off=np.zeros(1, np.int32),
+                   pred_idx=np.zeros(0, np.int32), lat_us=np.zeros(0, np.int32),
+                   mem_mib=np.zeros(0, np.int32), wf_arrival_us=np.zeros(0, np.int64),
+                   dev_cap_mib=np.array([100, 50, 70], np.int32), model_mib=np.array([30, 20], np.int32),
+                   load_us=np.zeros(6, np.int32), init_resident=np.array([3, 0, 2], np.uint64),
+                   dev_free0_us=np.zeros(3, np.int64))
+    ctx.wf_plan_upload_window(win)
+    t_next = torch.zeros(1, dtype=torch.int64, device="cuda:0")
+    ctx.wf_plan_prefix(None, None, None, None, None, None, None, t_next)
+    torch.cuda.synchronize()
+    c, cr, t = oracle.prefix(win, np.zeros(0, np.int8), np.zeros(0, np.int64), np.zeros(0, np.int64),
+                             np.zeros(0, np.int64), np.zeros(0, np.uint64))
+    assert int(t_next.item()) == t == np.iinfo(np.int64).max
