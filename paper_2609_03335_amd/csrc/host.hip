@@ -256,9 +256,12 @@ struct Image {
   }
 };
 
-// Per-wave LDS carve-up for G plans; returns the wave's byte size.
+// Per-wave region for G plans; returns the wave's byte size.  In LDS
+// (global = false) it is one block.  With regions in HBM (global = true) the
+// small per-(device, model) arrays come first, [0, o.split), and stay in LDS;
+// the per-activation arrays follow in HBM.
 int wave_layout(const HostWindow& h, int G, int tsz, int nwa, int qmode, bool search,
-                wfp::WaveOffsets& o) {
+                wfp::WaveOffsets& o, bool global) {
   const bool nibble = qmode > 0, paper = qmode == -1 || qmode == -3;
   size_t off = 0;
   auto take = [&](size_t n) {
@@ -268,36 +271,55 @@ int wave_layout(const HostWindow& h, int G, int tsz, int nwa, int qmode, bool se
   };
   const int NB = (h.N + 3) / 4;
   const size_t fin_bytes = (size_t)G * h.N * tsz, last_bytes = (size_t)G * h.D * h.M * 4;
-  o.flags = take((size_t)G * NB);
-  o.rec = take((size_t)G * h.N * 4);
-  o.mask = take((size_t)G * h.D * nwa * 8);
-  o.acc = take((size_t)G * sizeof(wfp::PlanAcc));
+  const size_t dm2 = (size_t)G * h.D * h.M * 2;
   // generated candidates keep their device and priority rows in fin's
   // storage (after last[] when that shares it) while the order is built
   const size_t rows_at = nibble ? align_up(last_bytes, 16) : 0;
   const size_t rows_bytes = search ? align_up((size_t)G * h.N, 16) + (size_t)G * h.N * 2 : 0;
+  o = wfp::WaveOffsets{};
+  if (global) {
+    // LDS part: the arrays read per reclamation candidate and the totals
+    o.acc = take((size_t)G * sizeof(wfp::PlanAcc));
+    if (!nibble) {
+      if (!paper) o.last = take(last_bytes);
+      o.stamp = take(dm2);
+    }
+    if (paper) {
+      o.nxu = take(dm2);
+      o.snap = take((size_t)G * h.D * 8);
+    }
+    o.split = (int)off;
+  }
+  o.flags = take((size_t)G * NB);
+  o.rec = take((size_t)G * h.N * 4);
+  o.mask = take((size_t)G * h.D * nwa * 8);
+  if (!global) o.acc = take((size_t)G * sizeof(wfp::PlanAcc));
   if (nibble) {
     o.fin = take(std::max(std::max(fin_bytes, last_bytes), rows_at + rows_bytes));
     o.last = o.fin;
-    o.stamp = 0;
   } else if (paper) {
     // the paper order keeps no last[] (it is never written)
     o.fin = take(std::max(fin_bytes, rows_bytes));
     o.last = o.fin;
-    o.stamp = take((size_t)G * h.D * h.M * 2);
+    if (!global) o.stamp = take(dm2);
   } else {
     o.fin = take(std::max(fin_bytes, rows_bytes));
-    o.last = take(last_bytes);
-    o.stamp = take((size_t)G * h.D * h.M * 2);
+    if (!global) {
+      o.last = take(last_bytes);
+      o.stamp = take(dm2);
+    }
   }
   o.rows = o.fin + (int)rows_at;
   o.rows_prio = o.rows + (int)align_up((size_t)G * h.N, 16);
   o.wfm = take((size_t)G * std::max(1, h.W) * tsz);
-  o.nx = o.nxu = o.snap = 0;
+  // unused arrays point at the start of their part
+  o.nx = global ? o.split : 0;
   if (paper) {
     o.nx = take((size_t)G * h.N * 2);
-    o.nxu = take((size_t)G * h.D * h.M * 2);
-    o.snap = take((size_t)G * h.D * 8);
+    if (!global) {
+      o.nxu = take(dm2);
+      o.snap = take((size_t)G * h.D * 8);
+    }
   }
   o.bytes = (int)off;
   return o.bytes;
@@ -492,7 +514,7 @@ wf_status plan_launch(wf_plan_ctx* ctx, const HostWindow& h, bool search, wfp::S
     const int tab_lds = (tl ? sp.t.bytes : 0) + sp.wg_ld;
     for (int G = gmax; G >= 1; --G) {
       wfp::WaveOffsets o{};
-      const int wb = wave_layout(h, G, tsz, sp.nwa, sp.nibble, search, o);
+      const int wb = wave_layout(h, G, tsz, sp.nwa, sp.nibble, search, o, false);
       int waves = std::min(8, (lds_blk - tab_lds) / std::max(wb, 1));
       if (waves < 1) continue;
       const int lds_wg = tab_lds + waves * wb;
@@ -515,19 +537,27 @@ wf_status plan_launch(wf_plan_ctx* ctx, const HostWindow& h, bool search, wfp::S
   }
   sp.wave_global = 0;
   sp.scratch = nullptr;
-  // per-wave regions in HBM: every lane of a wave busy and eight waves per
-  // CU, but each region access goes through the cache instead of LDS.  Taken
+  // per-wave regions in HBM (the small per-(device, model) arrays stay in
+  // LDS): every lane of a wave busy and up to eight waves per CU, but each
+  // per-activation access goes through the cache instead of LDS.  Taken
   // when no LDS layout fits, or when the LDS layout keeps at most an eighth
   // as many walk lanes in flight (deep windows, whose per-plan state fills
   // LDS with one or two plans per CU)
-  const double hbm_lanes = (double)std::min(gmax * D, 64) * 8;
-  if (best < 0 || best * 8.0 <= hbm_lanes) {
-    wfp::WaveOffsets o{};
-    const int G = gmax;
-    const int64_t wb = wave_layout(h, G, tsz, sp.nwa, sp.nibble, search, o);
+  wfp::WaveOffsets og{};
+  const int Gg = gmax, waves_g = 4;
+  const int64_t wb_g = wave_layout(h, Gg, tsz, sp.nwa, sp.nibble, search, og, true);
+  const int64_t hbm_wave = wb_g - og.split;  // HBM bytes per wave
+  const int lds_wg_g = sp.wg_ld + waves_g * og.split;
+  const int wgs_per_cu = lds_wg_g <= lds_blk ? std::max(1, std::min(2, lds_cu / std::max(lds_wg_g, 1))) : 0;
+  const double hbm_lanes = (double)std::min(Gg * D, 64) * waves_g * wgs_per_cu;
+  if (best < 0 && wgs_per_cu == 0)
+    return fail(&ctx->err, WF_EUNSUPPORTED, "window too large for LDS (N=%d, D=%d, M=%d)", h.N, D, h.M);
+  if (wgs_per_cu > 0 && (best < 0 || best * 8.0 <= hbm_lanes)) {
     const int64_t cap_bytes = int64_t(1) << 30;
-    const int waves = 4;
-    int64_t wgs = std::min<int64_t>((int64_t)ctx->n_cu * 2, cap_bytes / std::max<int64_t>(wb * waves, 1));
+    const int G = Gg, waves = waves_g;
+    const wfp::WaveOffsets o = og;
+    int64_t wgs = std::min<int64_t>((int64_t)ctx->n_cu * wgs_per_cu,
+                                    cap_bytes / std::max<int64_t>(hbm_wave * waves, 1));
     if (wgs < 1 && best >= 0) return WF_OK;  // keep the LDS layout
     if (wgs < 1)
       return fail(&ctx->err, WF_EUNSUPPORTED, "window too large (N=%d, widest level %d, D=%d, M=%d)",
@@ -536,7 +566,7 @@ wf_status plan_launch(wf_plan_ctx* ctx, const HostWindow& h, bool search, wfp::S
     sp.waves = waves;
     sp.tab_in_lds = 0;
     sp.wave_global = 1;
-    sp.lds_bytes = sp.wg_ld;
+    sp.lds_bytes = lds_wg_g;
     sp.grid = (int)wgs;
     sp.wo = o;
   }
@@ -714,7 +744,8 @@ wf_status wf_plan_upload_window(wf_plan_ctx* ctx, const wf_window_desc* w) {
   size_t need = 0;
   for (int i = 0; i < (checked ? 4 : 2); ++i)
     if (all[i]->wave_global)
-      need = std::max(need, (size_t)all[i]->grid * all[i]->waves * (size_t)all[i]->wo.bytes);
+      need = std::max(need, (size_t)all[i]->grid * all[i]->waves *
+                                (size_t)(all[i]->wo.bytes - all[i]->wo.split));
   if (need) {
     e = hipMalloc(&dw.scratch, need);
     if (e != hipSuccess) {

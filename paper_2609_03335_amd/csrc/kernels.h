@@ -61,6 +61,11 @@ struct WaveOffsets {
   int nxu;     // u16 [G*D][M]     paper order: next use of each model (device index)
   int snap;    // u64 [G][D]       paper order: resident models as the level starts
   int bytes;
+  // per-wave regions in HBM: the arrays at offsets below `split` (acc, and
+  // outside the queue modes last, stamp, nxu, snap: O(G D M) bytes) stay in
+  // LDS, `split` bytes per wave; the others live in HBM, `bytes - split` per
+  // wave, at their offset minus split.  0 when the whole region is in LDS.
+  int split;
 };
 
 struct ScoreParams {

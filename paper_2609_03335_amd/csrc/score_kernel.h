@@ -280,24 +280,34 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   const int32_t* t_batch = reinterpret_cast<const int32_t*>(tb + sp.t.batch);
 
   // ---- this wave's region (LDS, or HBM scratch for very large windows) ----
+  // (with regions in HBM, the small per-(device, model) arrays stay in LDS:
+  // big() addresses the HBM part, small() the LDS part)
   unsigned char* wl;
-  if constexpr (WAVE_GLOBAL)
-    wl = sp.scratch + ((int64_t)blockIdx.x * sp.waves + wid) * (int64_t)sp.wo.bytes;
-  else
+  unsigned char* wls;
+  if constexpr (WAVE_GLOBAL) {
+    wl = sp.scratch + ((int64_t)blockIdx.x * sp.waves + wid) * (int64_t)(sp.wo.bytes - sp.wo.split);
+    wls = lds + wave_base + wid * sp.wo.split;
+  } else {
     wl = lds + wave_base + wid * sp.wo.bytes;
-  uint8_t* s_fl = reinterpret_cast<uint8_t*>(wl + sp.wo.flags);
-  uint32_t* s_rec = reinterpret_cast<uint32_t*>(wl + sp.wo.rec);
-  unsigned long long* s_mask = reinterpret_cast<unsigned long long*>(wl + sp.wo.mask);
-  uint32_t* s_last = reinterpret_cast<uint32_t*>(wl + sp.wo.last);
-  TB* s_fin = reinterpret_cast<TB*>(wl + sp.wo.fin);
-  PlanAcc* s_acc = reinterpret_cast<PlanAcc*>(wl + sp.wo.acc);
-  uint16_t* s_stamp = reinterpret_cast<uint16_t*>(wl + sp.wo.stamp);
-  uint16_t* s_nx = reinterpret_cast<uint16_t*>(wl + sp.wo.nx);      // paper order only
-  uint16_t* s_nxu = reinterpret_cast<uint16_t*>(wl + sp.wo.nxu);
-  unsigned long long* s_snap = reinterpret_cast<unsigned long long*>(wl + sp.wo.snap);
-  TB* s_wfm = reinterpret_cast<TB*>(wl + sp.wo.wfm);
-  int8_t* s_rdev = reinterpret_cast<int8_t*>(wl + sp.wo.rows);         // generated candidates
-  uint16_t* s_rprio = reinterpret_cast<uint16_t*>(wl + sp.wo.rows_prio);
+    wls = wl;
+  }
+  auto big = [&](int off) -> unsigned char* { return wl + (WAVE_GLOBAL ? off - sp.wo.split : off); };
+  auto small = [&](int off) -> unsigned char* { return wls + off; };
+  uint8_t* s_fl = reinterpret_cast<uint8_t*>(big(sp.wo.flags));
+  uint32_t* s_rec = reinterpret_cast<uint32_t*>(big(sp.wo.rec));
+  unsigned long long* s_mask = reinterpret_cast<unsigned long long*>(big(sp.wo.mask));
+  // last[] shares fin's storage in the queue modes, else it is a small array
+  // (the paper order keeps no last[]; its offset is fin's)
+  uint32_t* s_last = reinterpret_cast<uint32_t*>((NIBBLE || PAPER) ? big(sp.wo.last) : small(sp.wo.last));
+  TB* s_fin = reinterpret_cast<TB*>(big(sp.wo.fin));
+  PlanAcc* s_acc = reinterpret_cast<PlanAcc*>(small(sp.wo.acc));
+  uint16_t* s_stamp = reinterpret_cast<uint16_t*>(small(sp.wo.stamp));
+  uint16_t* s_nx = reinterpret_cast<uint16_t*>(big(sp.wo.nx));      // paper order only
+  uint16_t* s_nxu = reinterpret_cast<uint16_t*>(small(sp.wo.nxu));
+  unsigned long long* s_snap = reinterpret_cast<unsigned long long*>(small(sp.wo.snap));
+  TB* s_wfm = reinterpret_cast<TB*>(big(sp.wo.wfm));
+  int8_t* s_rdev = reinterpret_cast<int8_t*>(big(sp.wo.rows));         // generated candidates
+  uint16_t* s_rprio = reinterpret_cast<uint16_t*>(big(sp.wo.rows_prio));
 
   const int g_me = lane / D;
   // every unit's finish goes through the general path when the schedule is
