@@ -771,11 +771,11 @@ wf_status wf_plan_upload_window(wf_plan_ctx* ctx, const wf_window_desc* w) {
   if (std::getenv("WF_PLAN_VERBOSE"))
     std::fprintf(stderr,
                  "[wf_plan] N=%d W=%d D=%d M=%d levels=%d wmax=%d time=%s G=%d waves/wg=%d "
-                 "grid=%d tables=%s(%d B) wave=%d B lds/wg=%d reclaim=%s\n",
+                 "grid=%d tables=%s(%d B) wave=%d B (lds part %d B) lds/wg=%d reclaim=%s\n",
                  sp.N, sp.W, sp.D, sp.M, sp.n_levels, h.wmax,
                  sp.time64 ? "fp64" : checked ? "u32+fp64" : "u32", sp.G,
                  sp.waves, sp.grid, sp.wave_global ? "hbm+scratch" : (sp.tab_in_lds ? "lds" : "hbm"),
-                 sp.t.bytes, sp.wo.bytes, sp.lds_bytes, sp.nibble == 32 ? "queue32" : sp.nibble == 64 ? "queue64" : sp.nibble == -1 ? "paper-scan" :
+                 sp.t.bytes, sp.wo.bytes, sp.wave_global ? sp.wo.split : sp.wo.bytes, sp.lds_bytes, sp.nibble == 32 ? "queue32" : sp.nibble == 64 ? "queue64" : sp.nibble == -1 ? "paper-scan" :
                  sp.nibble == -2 ? "batch-scan" : sp.nibble == -3 ? "batch-paper-scan" : "scan");
   free_device_window(ctx->dw);
   ctx->dw = dw;
