@@ -540,9 +540,12 @@ wf_status plan_launch(wf_plan_ctx* ctx, const HostWindow& h, bool search, wfp::S
   // per-wave regions in HBM (the small per-(device, model) arrays stay in
   // LDS): every lane of a wave busy and up to eight waves per CU, but each
   // per-activation access goes through the cache instead of LDS.  Taken
-  // when no LDS layout fits, or when the LDS layout keeps at most an eighth
-  // as many walk lanes in flight (deep windows, whose per-plan state fills
-  // LDS with one or two plans per CU)
+  // when no LDS layout fits, or when the LDS layout keeps too few walk lanes
+  // in flight: at most 1/8 as many with a reclamation queue (its last-slot
+  // table then lives in HBM too), at most 1/2.1 as many with a scan (deep or
+  // wide windows, whose per-plan state fills LDS with a few plans per CU).
+  // Measured on MI355X: scans at ratios 2.15-4 run 1.4-2.4x faster in HBM,
+  // a scan at 2.0 and a queue at 1.6 run 1.3x and 2.4x slower there.
   wfp::WaveOffsets og{};
   const int Gg = gmax, waves_g = 4;
   const int64_t wb_g = wave_layout(h, Gg, tsz, sp.nwa, sp.nibble, search, og, true);
@@ -552,7 +555,8 @@ wf_status plan_launch(wf_plan_ctx* ctx, const HostWindow& h, bool search, wfp::S
   const double hbm_lanes = (double)std::min(Gg * D, 64) * waves_g * wgs_per_cu;
   if (best < 0 && wgs_per_cu == 0)
     return fail(&ctx->err, WF_EUNSUPPORTED, "window too large for LDS (N=%d, D=%d, M=%d)", h.N, D, h.M);
-  if (wgs_per_cu > 0 && (best < 0 || best * 8.0 <= hbm_lanes)) {
+  const double min_ratio = sp.nibble > 0 ? 8.0 : 2.1;
+  if (wgs_per_cu > 0 && (best < 0 || best * min_ratio <= hbm_lanes)) {
     const int64_t cap_bytes = int64_t(1) << 30;
     const int G = Gg, waves = waves_g;
     const wfp::WaveOffsets o = og;
