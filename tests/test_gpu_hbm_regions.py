@@ -107,3 +107,35 @@ def test_keys_and_candidates(ctx, name):
     ctx.wf_plan_search_batch(dev[0], prio[0], flags[0], 5, 2, 3, n, scores)
     torch.cuda.synchronize()
     assert pkg.scores_to_numpy(scores, n).tobytes() == oracle.score(win, cand, threads=THREADS).tobytes()
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_random_mid_windows(ctx, seed, capfd, monkeypatch):
+    """Windows of 400-3,000 activations with more than 16 models, under the
+    three scanning modes: the host picks either layout by the lanes each
+    keeps in flight, and both must agree with the oracle bytewise."""
+    rng = np.random.default_rng(31_000 + seed)
+    D = int(rng.integers(2, 17))
+    win = W.random_window(rng, n_wf=int(rng.integers(20, 120)), nodes=(10, 40), n_dev=D,
+                          n_models=int(rng.integers(17, 48)), p_edge=0.2, q_inel=0.0,
+                          cap_range=(16000, 40000))
+    mode = seed % 3
+    if mode == 1:
+        win.victim_order = 1
+    elif mode == 2:
+        win.dev_batch = rng.integers(1, 5, size=D).astype(np.int32)
+    plans = W.random_plans(win, 40, rng, prio_mode="perm")
+    monkeypatch.setenv("WF_PLAN_VERBOSE", "1")
+    ctx.wf_plan_upload_window(win)
+    where, wave, lds_part, lds_wg, rmode = layout_line(capfd.readouterr().err)
+    log(f"[hbm] random {seed}: N={win.n_act} D={D} M={win.n_models} mode={rmode} layout={where}")
+    P, N = plans.n_plans, win.n_act
+    dev, prio, flags = pkg.device_plans(plans, "cuda:0")
+    scores, sched = pkg.score_batch(ctx, dev, prio, flags, P, schedule=True, n_act=N, n_dev=D)
+    torch.cuda.synchronize()
+    got = pkg.scores_to_numpy(scores, P)
+    ref, rs = oracle.score(win, plans, schedule=True, threads=THREADS)
+    assert got.tobytes() == ref.tobytes(), seed
+    ok = ref["status"] & oracle.INELIGIBLE == 0
+    for label, a, b in zip(("start", "finish", "load_start", "peak"), sched, rs):
+        assert np.array_equal(a.cpu().numpy()[ok][:, :b.shape[1]], b[ok]), (seed, label)
