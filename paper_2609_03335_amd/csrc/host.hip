@@ -541,11 +541,14 @@ wf_status plan_launch(wf_plan_ctx* ctx, const HostWindow& h, bool search, wfp::S
   // LDS): every lane of a wave busy and up to eight waves per CU, but each
   // per-activation access goes through the cache instead of LDS.  Taken
   // when no LDS layout fits, or when the LDS layout keeps too few walk lanes
-  // in flight: at most 1/8 as many with a reclamation queue (its last-slot
-  // table then lives in HBM too), at most 1/2.1 as many with a scan (deep or
-  // wide windows, whose per-plan state fills LDS with a few plans per CU).
-  // Measured on MI355X: scans at ratios 2.15-4 run 1.4-2.4x faster in HBM,
-  // a scan at 2.0 and a queue at 1.6 run 1.3x and 2.4x slower there.
+  // in flight (deep or wide windows, whose per-plan state fills LDS with a
+  // few plans per CU).  The cheaper a walk trip, the more the cache latency
+  // of the HBM part shows, so the ratio needed depends on the reclamation
+  // mode: 8 with a queue (whose last-slot table then lives in HBM too), 3
+  // with a plain or batch-limited scan, 2.1 with the paper's order.
+  // Measured on MI355X: paper-order scans at ratios 2.15-6.4 run 1.3-2.4x
+  // faster in HBM; other scans at 3.3-6.4 run 1.2-1.7x faster, at 2.0-2.24
+  // 1.3-1.5x slower; a queue at 1.6 runs 2.4x slower.
   wfp::WaveOffsets og{};
   const int Gg = gmax, waves_g = 4;
   const int64_t wb_g = wave_layout(h, Gg, tsz, sp.nwa, sp.nibble, search, og, true);
@@ -555,7 +558,8 @@ wf_status plan_launch(wf_plan_ctx* ctx, const HostWindow& h, bool search, wfp::S
   const double hbm_lanes = (double)std::min(Gg * D, 64) * waves_g * wgs_per_cu;
   if (best < 0 && wgs_per_cu == 0)
     return fail(&ctx->err, WF_EUNSUPPORTED, "window too large for LDS (N=%d, D=%d, M=%d)", h.N, D, h.M);
-  const double min_ratio = sp.nibble > 0 ? 8.0 : 2.1;
+  const bool paper_scan = sp.nibble == -1 || sp.nibble == -3;
+  const double min_ratio = sp.nibble > 0 ? 8.0 : paper_scan ? 2.1 : 3.0;
   if (wgs_per_cu > 0 && (best < 0 || best * min_ratio <= hbm_lanes)) {
     const int64_t cap_bytes = int64_t(1) << 30;
     const int G = Gg, waves = waves_g;
