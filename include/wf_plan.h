@@ -52,9 +52,13 @@
  *     queued on the given stream has completed.  score_batch and argmin are
  *     asynchronous on that stream (NULL = the default stream); launch errors
  *     are reported on return as WF_EHIP.
- *   - A context is not thread-safe; use one per host thread.  Work queued on
- *     different streams of one context may run concurrently, but a new
- *     upload must not race with queued scoring (synchronise first).
+ *   - A context is not thread-safe; use one per host thread.  Calls on one
+ *     context must not run concurrently on different streams: the scoring
+ *     calls may share the context's scratch area (per-wave regions of
+ *     windows too large for LDS, allocated at upload, at most 1 GiB) and
+ *     the argmins its work area.  A new upload must not race with queued
+ *     work either (synchronise first).  Use one context per stream for
+ *     concurrent scoring.
  */
 #ifndef WF_PLAN_H
 #define WF_PLAN_H
