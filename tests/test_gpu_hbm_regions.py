@@ -139,3 +139,31 @@ def test_random_mid_windows(ctx, seed, capfd, monkeypatch):
     ok = ref["status"] & oracle.INELIGIBLE == 0
     for label, a, b in zip(("start", "finish", "load_start", "peak"), sched, rs):
         assert np.array_equal(a.cpu().numpy()[ok][:, :b.shape[1]], b[ok]), (seed, label)
+
+
+def test_two_contexts_two_streams():
+    """Concurrent scoring takes one context per stream: each context owns its
+    scratch area, so two HBM-layout launches in flight at once both match
+    the oracle."""
+    win, plans = big_window("scan")
+    P = plans.n_plans
+    ref = oracle.score(win, plans, threads=THREADS)
+    log(f"[hbm] two contexts on two streams: N={win.n_act} P={P}")
+    ctxs = [pkg.Context(0), pkg.Context(0)]
+    try:
+        streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+        dev, prio, flags = pkg.device_plans(plans, "cuda:0")
+        outs = []
+        for c in ctxs:
+            c.wf_plan_upload_window(win)
+        torch.cuda.synchronize()
+        for c, s in zip(ctxs, streams):
+            sc = torch.empty((P, 32), dtype=torch.uint8, device="cuda:0")
+            c.wf_plan_score_batch(dev, prio, flags, P, sc, None, s)
+            outs.append(sc)
+        torch.cuda.synchronize()
+        for sc in outs:
+            assert pkg.scores_to_numpy(sc, P).tobytes() == ref.tobytes()
+    finally:
+        for c in ctxs:
+            c.close()
