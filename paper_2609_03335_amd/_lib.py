@@ -163,13 +163,36 @@ class _Desc:
 
 def _ptr(x) -> Optional[int]:
     """Device address of a buffer; tensors must be dense row-major (the ABI
-    takes flat row-major arrays)."""
+    takes flat row-major arrays).  No placement or size check: the Context
+    methods check tensors with _buf before calling the library."""
     if x is None:
         return None
     if isinstance(x, int):
         return x
     if hasattr(x, "is_contiguous") and not x.is_contiguous():
         raise ValueError("device buffers must be contiguous row-major tensors")
+    return int(x.data_ptr())
+
+
+def _buf(x, need: int, device: int, name: str) -> Optional[int]:
+    """Device address of a buffer argument after the checks the library
+    cannot make on a bare pointer: a torch tensor must be contiguous, live on
+    GPU `device` and hold at least `need` bytes.  A raw int is taken as a
+    device address the caller vouches for; None passes through (the library
+    rejects a missing required array)."""
+    if x is None or isinstance(x, int):
+        return x
+    if not hasattr(x, "data_ptr"):
+        raise TypeError(f"{name}: expected a torch tensor or a device address")
+    if not x.is_contiguous():
+        raise ValueError(f"{name}: device buffers must be contiguous row-major tensors")
+    if not x.is_cuda:
+        raise ValueError(f"{name}: a host tensor cannot be passed to the GPU library")
+    if x.device.index != device:
+        raise ValueError(f"{name}: tensor on cuda:{x.device.index}, context on cuda:{device}")
+    nbytes = x.numel() * x.element_size()
+    if nbytes < need:
+        raise ValueError(f"{name}: {nbytes} bytes, at least {need} needed")
     return int(x.data_ptr())
 
 
@@ -187,7 +210,9 @@ def wf_plan_validate_window(win) -> tuple:
 
 
 class Context:
-    """A wf_plan_ctx on one HIP device."""
+    """A wf_plan_ctx on one HIP device.  Tensor arguments are checked before
+    any call reaches the library (GPU tensor, the context's device, enough
+    bytes for the uploaded window's sizes)."""
 
     def __init__(self, device: int = 0):
         self.lib = load()
@@ -197,71 +222,108 @@ class Context:
             raise WFError(st, self.lib.wf_plan_last_error(None).decode())
         self.handle = h
         self.device = device
+        self._nd = (0, 0)  # (N, D) of the uploaded window
 
     def _check(self, st):
         if st != WF_OK:
             raise WFError(st, self.lib.wf_plan_last_error(self.handle).decode())
 
+    @staticmethod
+    def _cnt(n, limit=1 << 62) -> int:
+        """A plan count for sizing buffers; a count the library will refuse
+        (negative or above its limit) sizes nothing, so that the library's
+        WF_EINVAL reaches the caller."""
+        n = int(n)
+        return n if 0 <= n <= limit else 0
+
+    def _b(self, x, need: int, name: str) -> Optional[int]:
+        return _buf(x, max(int(need), 0), self.device, name)
+
+    def _rows(self, dev, prio, flags, n: int):
+        """Addresses of n plan rows (dev [n][N], prio [n][N], flags [n][ceil(N/4)])."""
+        N = self._nd[0]
+        return (self._b(dev, n * N, "dev"), self._b(prio, 2 * n * N, "prio"),
+                self._b(flags, n * ((N + 3) // 4), "flags"))
+
     def wf_plan_upload_window(self, win) -> None:
         d = _Desc(win)
         self._check(self.lib.wf_plan_upload_window(self.handle, ctypes.byref(d.desc)))
+        self._nd = (int(win.n_act), int(win.n_dev))
 
     def wf_plan_score_batch(self, dev, prio, flags, n_plans: int, scores, sched=None,
                             stream=None) -> None:
         """dev/prio/flags/scores (and the schedule arrays: start, finish,
         load_start, peak and optionally reclaimed) are device buffers: torch
         tensors or raw device addresses."""
+        P = self._cnt(n_plans)
+        N, D = self._nd
         s = None
         if sched is not None:
-            s = wf_plan_sched(*(_ptr(x) for x in sched))
+            sched = tuple(sched) + (None,) * (5 - len(sched))
+            needs = (8 * P * N, 8 * P * N, 8 * P * N, 4 * P * D, 8 * P * N)
+            names = ("start_us", "finish_us", "load_start_us", "peak_mib", "reclaimed_models")
+            s = wf_plan_sched(*(self._b(x, k, nm) for x, k, nm in zip(sched, needs, names)))
         self._check(self.lib.wf_plan_score_batch(
-            self.handle, _ptr(dev), _ptr(prio), _ptr(flags), int(n_plans), _ptr(scores),
-            None if s is None else ctypes.byref(s), _stream(stream)))
+            self.handle, *self._rows(dev, prio, flags, P), int(n_plans),
+            self._b(scores, 32 * P, "scores"), None if s is None else ctypes.byref(s),
+            _stream(stream)))
 
     def wf_plan_prefix(self, dev, start, finish, load_start, reclaimed, commit,
                        commit_reclaimed, t_next, stream=None) -> None:
         """One plan's device row and schedule rows in; commit flags, committed
         reclamations and the next event time out (all device buffers)."""
+        N = self._nd[0]
         self._check(self.lib.wf_plan_prefix(
-            self.handle, _ptr(dev), _ptr(start), _ptr(finish), _ptr(load_start),
-            _ptr(reclaimed), _ptr(commit), _ptr(commit_reclaimed), _ptr(t_next),
+            self.handle, self._b(dev, N, "dev"), self._b(start, 8 * N, "start_us"),
+            self._b(finish, 8 * N, "finish_us"), self._b(load_start, 8 * N, "load_start_us"),
+            self._b(reclaimed, 8 * N, "reclaimed"), self._b(commit, N, "commit"),
+            self._b(commit_reclaimed, 8 * N, "commit_reclaimed"), self._b(t_next, 8, "t_next_us"),
             _stream(stream)))
 
     def wf_plan_argmin(self, scores, n_plans: int, out_index, stream=None) -> None:
-        self._check(self.lib.wf_plan_argmin(self.handle, _ptr(scores), int(n_plans),
-                                            _ptr(out_index), _stream(stream)))
+        self._check(self.lib.wf_plan_argmin(
+            self.handle, self._b(scores, 32 * self._cnt(n_plans, (1 << 32) - 1), "scores"), int(n_plans),
+            self._b(out_index, 8, "out_index"), _stream(stream)))
 
     def wf_plan_search_batch(self, dev, prio, flags, seed: int, n_mut: int, first: int,
                              n_candidates: int, scores, stream=None) -> None:
         """Score candidates first .. first+n_candidates-1 generated around the
         incumbent rows dev/prio/flags (device buffers of one plan)."""
         self._check(self.lib.wf_plan_search_batch(
-            self.handle, _ptr(dev), _ptr(prio), _ptr(flags), int(seed) & ((1 << 64) - 1),
-            int(n_mut), int(first), int(n_candidates), _ptr(scores), _stream(stream)))
+            self.handle, *self._rows(dev, prio, flags, 1), int(seed) & ((1 << 64) - 1),
+            int(n_mut), int(first), int(n_candidates),
+            self._b(scores, 32 * self._cnt(n_candidates), "scores"), _stream(stream)))
 
     def wf_plan_search_rows(self, dev, prio, flags, seed: int, n_mut: int, first: int,
                             n_candidates: int, out_dev, out_prio, out_flags, stream=None) -> None:
         """Write the rows of candidates first .. first+n_candidates-1."""
+        n = self._cnt(n_candidates)
+        N = self._nd[0]
         self._check(self.lib.wf_plan_search_rows(
-            self.handle, _ptr(dev), _ptr(prio), _ptr(flags), int(seed) & ((1 << 64) - 1),
-            int(n_mut), int(first), int(n_candidates), _ptr(out_dev), _ptr(out_prio),
-            _ptr(out_flags), _stream(stream)))
+            self.handle, *self._rows(dev, prio, flags, 1), int(seed) & ((1 << 64) - 1),
+            int(n_mut), int(first), int(n_candidates), self._b(out_dev, n * N, "out_dev"),
+            self._b(out_prio, 2 * n * N, "out_prio"),
+            self._b(out_flags, n * ((N + 3) // 4), "out_flags"), _stream(stream)))
 
     def wf_plan_score_keys(self, dev, prio, flags, n_plans: int, keys, stream=None) -> None:
         """Ranking keys (Eq. 12) of plans 0..n_plans-1 into keys (32 B each)."""
-        self._check(self.lib.wf_plan_score_keys(self.handle, _ptr(dev), _ptr(prio), _ptr(flags),
-                                                int(n_plans), _ptr(keys), _stream(stream)))
+        P = self._cnt(n_plans)
+        self._check(self.lib.wf_plan_score_keys(
+            self.handle, *self._rows(dev, prio, flags, P), int(n_plans),
+            self._b(keys, 32 * P, "keys"), _stream(stream)))
 
     def wf_plan_search_keys(self, dev, prio, flags, seed: int, n_mut: int, first: int,
                             n_candidates: int, keys, stream=None) -> None:
         """Ranking keys of candidates generated around the incumbent rows."""
         self._check(self.lib.wf_plan_search_keys(
-            self.handle, _ptr(dev), _ptr(prio), _ptr(flags), int(seed) & ((1 << 64) - 1),
-            int(n_mut), int(first), int(n_candidates), _ptr(keys), _stream(stream)))
+            self.handle, *self._rows(dev, prio, flags, 1), int(seed) & ((1 << 64) - 1),
+            int(n_mut), int(first), int(n_candidates),
+            self._b(keys, 32 * self._cnt(n_candidates), "keys"), _stream(stream)))
 
     def wf_plan_argmin_keys(self, keys, n_plans: int, out_index, stream=None) -> None:
-        self._check(self.lib.wf_plan_argmin_keys(self.handle, _ptr(keys), int(n_plans),
-                                                 _ptr(out_index), _stream(stream)))
+        self._check(self.lib.wf_plan_argmin_keys(
+            self.handle, self._b(keys, 32 * self._cnt(n_plans), "keys"), int(n_plans),
+            self._b(out_index, 8, "out_index"), _stream(stream)))
 
     def wf_plan_time_bits(self) -> int:
         return int(self.lib.wf_plan_time_bits(self.handle))

@@ -226,3 +226,76 @@ def test_binding_structs_follow_the_header(name):
     """The ctypes mirrors list the header's members in the header's order."""
     py = [f[0] for f in getattr(_lib, name)._fields_]
     assert py == _struct_fields(name)
+
+
+class _FakeGpuTensor:
+    """Stands in for a torch CUDA tensor on a machine without a GPU: the
+    binding's checks read only these attributes."""
+
+    class _Dev:
+        def __init__(self, index):
+            self.index = index
+
+    def __init__(self, nbytes, index=0, cuda=True, contiguous=True):
+        self._n, self.is_cuda, self._c = nbytes, cuda, contiguous
+        self.device = self._Dev(index)
+
+    def is_contiguous(self):
+        return self._c
+
+    def numel(self):
+        return self._n
+
+    def element_size(self):
+        return 1
+
+    def data_ptr(self):
+        return 0x7f0000000000
+
+
+def test_buffer_checks_before_the_library():
+    """A host tensor, a tensor on another GPU, a strided tensor or one too
+    small for the call never reach the kernels as an address."""
+    import torch
+    with pytest.raises(ValueError, match="host tensor"):
+        _lib._buf(torch.zeros(64, dtype=torch.uint8), 32, 0, "scores")
+    with pytest.raises(ValueError, match="cuda:1"):
+        _lib._buf(_FakeGpuTensor(64, index=1), 32, 0, "scores")
+    with pytest.raises(ValueError, match="contiguous"):
+        _lib._buf(_FakeGpuTensor(64, contiguous=False), 32, 0, "scores")
+    with pytest.raises(ValueError, match="at least 64"):
+        _lib._buf(_FakeGpuTensor(63), 64, 0, "scores")
+    assert _lib._buf(_FakeGpuTensor(64), 64, 0, "scores") == 0x7f0000000000
+    assert _lib._buf(None, 64, 0, "scores") is None
+    assert _lib._buf(0x1000, 64, 0, "scores") == 0x1000  # a raw address is the caller's
+
+
+def test_context_methods_size_buffers_from_the_window(monkeypatch):
+    """Each Context method asks for the bytes the uploaded window implies:
+    a [P][N] schedule array one row short is refused before the call."""
+    class _NoLib:  # any call reaching the library fails the test
+        def __getattr__(self, name):
+            def call(*a):
+                raise AssertionError(f"{name} reached the library")
+            return call
+    ctx = _lib.Context.__new__(_lib.Context)
+    ctx.lib, ctx.handle, ctx.device, ctx._nd = _NoLib(), None, 0, (10, 3)
+    P = 4
+    rows = (_FakeGpuTensor(P * 10), _FakeGpuTensor(2 * P * 10), _FakeGpuTensor(P * 3))
+    ok_sched = [_FakeGpuTensor(8 * P * 10)] * 3 + [_FakeGpuTensor(4 * P * 3)]
+    short = list(ok_sched)
+    short[1] = _FakeGpuTensor(8 * (P - 1) * 10)
+    with pytest.raises(ValueError, match="finish_us"):
+        ctx.wf_plan_score_batch(*rows, P, _FakeGpuTensor(32 * P), short)
+    with pytest.raises(ValueError, match="scores"):
+        ctx.wf_plan_score_batch(*rows, P, _FakeGpuTensor(32 * P - 1))
+    with pytest.raises(ValueError, match="prio"):
+        ctx.wf_plan_score_keys(rows[0], _FakeGpuTensor(2 * P * 10 - 2), rows[2], P,
+                               _FakeGpuTensor(32 * P))
+    with pytest.raises(ValueError, match="peak_mib"):
+        ctx.wf_plan_score_batch(*rows, P, _FakeGpuTensor(32 * P),
+                                ok_sched[:3] + [_FakeGpuTensor(4 * P * 3 - 4)])
+    with pytest.raises(ValueError, match="out_dev"):
+        ctx.wf_plan_search_rows(_FakeGpuTensor(10), _FakeGpuTensor(20), _FakeGpuTensor(3), 1, 1, 0,
+                                5, _FakeGpuTensor(49), _FakeGpuTensor(100), _FakeGpuTensor(15))
+
