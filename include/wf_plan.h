@@ -226,6 +226,20 @@ wf_status wf_plan_score_batch(wf_plan_ctx *ctx, const int8_t *dev, const uint16_
 wf_status wf_plan_argmin(wf_plan_ctx *ctx, const wf_plan_score *scores, int64_t n_plans,
                          int64_t *out_index, void *hip_stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the
+ * result of wf_plan_argmin without a context.  Runs on the calling thread's
+ * current HIP device and allocates nothing: its partial minima (512 of 8
+ * bytes, 4 KiB) live in a static array of the library that each GPU holds
+ * for the life of the process.  Every call on one GPU shares that array, so
+ * calls that overlap on one GPU (different streams or host threads) race;
+ * each call writes every entry it reads, so nothing needs clearing.
+ * n_plans must be < 2^32 (WF_EINVAL otherwise); n_plans = 0 writes -1.
+ * Errors are reported by wf_plan_last_error(NULL).  Asynchronous on
+ * hip_stream. */
+wf_status wf_plan_argmin_noalloc(const wf_plan_score *scores, int64_t n_plans,
+                                 int64_t *out_index, void *hip_stream);
+
 /*
  * Candidate generation fused with scoring.  Algorithm 1 weighs alternatives
  * before Propagate checks one: another eligible device for a unit (the

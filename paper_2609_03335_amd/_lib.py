@@ -42,7 +42,7 @@ assert KEY_DTYPE.itemsize == 32
 # every symbol declared in include/wf_plan.h
 EXPORTS = ("wf_plan_ctx_create", "wf_plan_ctx_destroy", "wf_plan_last_error",
            "wf_plan_validate_window", "wf_plan_upload_window", "wf_plan_score_batch",
-           "wf_plan_argmin", "wf_plan_search_batch", "wf_plan_search_rows",
+           "wf_plan_argmin", "wf_plan_argmin_noalloc", "wf_plan_search_batch", "wf_plan_search_rows",
            "wf_plan_score_keys", "wf_plan_search_keys", "wf_plan_argmin_keys",
            "wf_plan_prefix", "wf_plan_time_bits", "wf_plan_version")
 
@@ -105,6 +105,8 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.wf_plan_score_batch.restype = i32
     lib.wf_plan_argmin.argtypes = [vp, vp, i64, vp, vp]
     lib.wf_plan_argmin.restype = i32
+    lib.wf_plan_argmin_noalloc.argtypes = [vp, i64, vp, vp]
+    lib.wf_plan_argmin_noalloc.restype = i32
     u64 = ctypes.c_uint64
     lib.wf_plan_search_batch.argtypes = [vp, vp, vp, vp, u64, ctypes.c_int32, i64, i64, vp, vp]
     lib.wf_plan_search_batch.restype = i32
@@ -207,6 +209,23 @@ def wf_plan_validate_window(win) -> tuple:
     buf = ctypes.create_string_buffer(512)
     st = lib.wf_plan_validate_window(ctypes.byref(d.desc), buf, len(buf))
     return st, buf.value.decode()
+
+
+def wf_plan_argmin_noalloc(scores, n_plans: int, out_index, stream=None) -> None:
+    """wf_plan_argmin without a context or any allocation, on the current
+    HIP device (its work area is the library's static array).  Tensors must
+    live on the current device."""
+    lib = load()
+    n = int(n_plans)
+    sized = n if 0 <= n < (1 << 32) else 0
+    cur = 0
+    if any(x is not None and not isinstance(x, int) for x in (scores, out_index)):
+        import torch
+        cur = torch.cuda.current_device()
+    st = lib.wf_plan_argmin_noalloc(_buf(scores, 32 * sized, cur, "scores"), n,
+                                    _buf(out_index, 8, cur, "out_index"), _stream(stream))
+    if st != WF_OK:
+        raise WFError(st, lib.wf_plan_last_error(None).decode())
 
 
 class Context:

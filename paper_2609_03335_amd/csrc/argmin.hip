@@ -8,7 +8,15 @@
 // share of the plans (wave shuffles, then LDS across its waves) to one
 // partial minimum in a work area, and one final block reduces the partials
 // and writes the plan index: deterministic, and without a contended atomic.
+#include <mutex>
+
 #include "kernels.h"
+
+// Partial minima of wf_plan_argmin_noalloc: one 64-bit key per block of the
+// first pass (4 KiB).  Each GPU holds its own copy for the life of the
+// process; host code reaches it only through the address that
+// hipGetSymbolAddress returns for that GPU (static_scratch below).
+static __device__ __align__(256) unsigned long long scratch[wfp::kArgminKeyBlocks];
 
 namespace wfp {
 namespace {
@@ -61,6 +69,26 @@ __global__ __launch_bounds__(256) void argmin_final(const unsigned long long* __
 }
 
 }  // namespace
+
+hipError_t static_scratch(int device, void** out) {
+  // looked up once per device, with that device current (the caller's
+  // thread has it selected), and kept: every GPU's copy of the array has its
+  // own address, and the array's name in host code is no device address
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  if (device < 0 || device >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[device]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    addr[device] = p;
+  }
+  *out = addr[device];
+  return hipSuccess;
+}
 
 hipError_t launch_argmin(const wf_plan_score* scores, int64_t n_plans, int64_t* out_index,
                          void* work, hipStream_t stream) {

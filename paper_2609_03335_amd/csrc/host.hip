@@ -907,6 +907,37 @@ wf_status wf_plan_argmin(wf_plan_ctx* ctx, const wf_plan_score* scores, int64_t 
   return WF_OK;
 }
 
+wf_status wf_plan_argmin_noalloc(const wf_plan_score* scores, int64_t n_plans,
+                                 int64_t* out_index, void* hip_stream) {
+  if (n_plans < 0 || n_plans >= (int64_t(1) << 32)) {
+    g_thread_err = "n_plans must be in [0, 2^32)";
+    return WF_EINVAL;
+  }
+  if (!out_index) {
+    g_thread_err = "out_index is NULL";
+    return WF_EINVAL;
+  }
+  if (n_plans > 0 && !scores) {
+    g_thread_err = "scores is NULL";
+    return WF_EINVAL;
+  }
+  int device = 0;
+  hipError_t e = hipGetDevice(&device);
+  void* work = nullptr;
+  if (e == hipSuccess) e = wfp::static_scratch(device, &work);
+  if (e != hipSuccess) {
+    g_thread_err = std::string("static work area of the current device: ") + hipGetErrorString(e);
+    return WF_EHIP;
+  }
+  e = wfp::launch_argmin(scores, n_plans, out_index, work, static_cast<hipStream_t>(hip_stream));
+  if (e != hipSuccess) {
+    g_thread_err = std::string("launching the argmin kernels: ") + hipGetErrorString(e);
+    return WF_EHIP;
+  }
+  g_thread_err.clear();
+  return WF_OK;
+}
+
 wf_status wf_plan_score_keys(wf_plan_ctx* ctx, const int8_t* dev, const uint16_t* prio,
                              const uint8_t* flags, int64_t n_plans, wf_plan_key* keys,
                              void* hip_stream) {

@@ -154,6 +154,12 @@ constexpr size_t ARGMIN_KEY_WORK_BYTES = 64;
 
 hipError_t launch_argmin(const wf_plan_score* scores, int64_t n_plans, int64_t* out_index,
                          void* work, hipStream_t stream);
+
+// Device address of the current device's static array of kArgminKeyBlocks
+// partial minima (argmin.hip), looked up on the first call for `device` (the
+// current device) and kept; the argmin that allocates nothing uses it as its
+// work area.
+hipError_t static_scratch(int device, void** out);
 hipError_t launch_argmin_keys(const wf_plan_key* keys, int64_t n_plans, int64_t* out_index,
                               void* work, hipStream_t stream);
 

@@ -299,3 +299,13 @@ def test_context_methods_size_buffers_from_the_window(monkeypatch):
         ctx.wf_plan_search_rows(_FakeGpuTensor(10), _FakeGpuTensor(20), _FakeGpuTensor(3), 1, 1, 0,
                                 5, _FakeGpuTensor(49), _FakeGpuTensor(100), _FakeGpuTensor(15))
 
+
+def test_noalloc_argmin_argument_errors_without_gpu():
+    """Argument errors of the allocation-free argmin are found on the host,
+    before any HIP call."""
+    lib = _lib.load()
+    assert lib.wf_plan_argmin_noalloc(None, -1, 0x1000, None) == _lib.WF_EINVAL
+    assert lib.wf_plan_argmin_noalloc(0x1000, 1 << 32, 0x1000, None) == _lib.WF_EINVAL
+    assert b"2^32" in lib.wf_plan_last_error(None)
+    assert lib.wf_plan_argmin_noalloc(0x1000, 5, None, None) == _lib.WF_EINVAL
+    assert lib.wf_plan_argmin_noalloc(None, 5, 0x1000, None) == _lib.WF_EINVAL
