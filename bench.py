@@ -46,7 +46,7 @@ def kernel_source_digest() -> str:
     import hashlib
     from paper_2609_03335_amd import build
     h = hashlib.sha256()
-    for name in ("score_kernel.h", "score.hip", "kernels.h", "host.hip"):
+    for name in ("score_kernel.h", "score.hip", "lean.hip", "kernels.h", "host.hip"):
         with open(os.path.join(CSRC, name), "rb") as f:
             h.update(f.read())
     h.update(" ".join(build.HIP_FLAGS).encode())
@@ -243,7 +243,7 @@ def main():
     traffic = measured_traffic(args.config, P)
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-                "kernel": "score_plans", "kernel_ms": round(kernel_ms, 4),
+                "kernel": ctx.wf_plan_score_kernel(), "kernel_ms": round(kernel_ms, 4),
                 "bytes_per_plan": bpp, "copy_gbs_measured": round(copy_gbs, 1),
                 "frac_of_copy": round(achieved / copy_gbs, 4), "argmin_ms": round(argmin_ms, 4)}
 

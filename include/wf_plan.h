@@ -370,6 +370,13 @@ wf_status wf_plan_prefix(wf_plan_ctx *ctx, const int8_t *dev, const int64_t *sta
  * every case. */
 int wf_plan_time_bits(const wf_plan_ctx *ctx);
 
+/* Name of the kernel that scores plans read from HBM for the uploaded
+ * window without a schedule: "score_lean" when the window qualifies for the
+ * lean kernel (uint32 times, at most 16 models, at most 512 activations, no
+ * batch limits, the default reclamation order), else "score_plans"; "" when
+ * ctx is NULL or has no window.  Both give identical results. */
+const char *wf_plan_score_kernel(const wf_plan_ctx *ctx);
+
 /* Library version string. */
 const char *wf_plan_version(void);
 

@@ -44,7 +44,7 @@ EXPORTS = ("wf_plan_ctx_create", "wf_plan_ctx_destroy", "wf_plan_last_error",
            "wf_plan_validate_window", "wf_plan_upload_window", "wf_plan_score_batch",
            "wf_plan_argmin", "wf_plan_argmin_noalloc", "wf_plan_search_batch", "wf_plan_search_rows",
            "wf_plan_score_keys", "wf_plan_search_keys", "wf_plan_argmin_keys",
-           "wf_plan_prefix", "wf_plan_time_bits", "wf_plan_version")
+           "wf_plan_prefix", "wf_plan_time_bits", "wf_plan_score_kernel", "wf_plan_version")
 
 
 class WFError(RuntimeError):
@@ -122,6 +122,8 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.wf_plan_prefix.restype = i32
     lib.wf_plan_time_bits.argtypes = [vp]
     lib.wf_plan_time_bits.restype = i32
+    lib.wf_plan_score_kernel.argtypes = [vp]
+    lib.wf_plan_score_kernel.restype = ctypes.c_char_p
     lib.wf_plan_version.argtypes = []
     lib.wf_plan_version.restype = ctypes.c_char_p
     # an entry point without a declared signature would take Python ints as
@@ -346,6 +348,9 @@ class Context:
 
     def wf_plan_time_bits(self) -> int:
         return int(self.lib.wf_plan_time_bits(self.handle))
+
+    def wf_plan_score_kernel(self) -> str:
+        return self.lib.wf_plan_score_kernel(self.handle).decode()
 
     def close(self):
         if getattr(self, "handle", None):

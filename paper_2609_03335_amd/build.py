@@ -12,7 +12,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB_NAME = "libwfplan.so"
 LIB_PATH = os.path.join(PKG, LIB_NAME)
-SOURCES = ["host.hip", "score.hip", "score_keys.hip", "argmin.hip", "prefix.hip"]
+SOURCES = ["host.hip", "score.hip", "score_keys.hip", "argmin.hip", "prefix.hip", "lean.hip"]
 ARCH = "gfx950"
 
 HIP_FLAGS = [

@@ -207,12 +207,16 @@ struct DeviceWindow {
   void* tab = nullptr;          // table image in HBM
   void* tab64 = nullptr;        // fp64-time table image of the rescoring pass
   void* scratch = nullptr;      // per-wave regions for windows too big for LDS
+  void* tab_lean = nullptr;     // the lean kernel's table image
   wfp::ScoreParams sp{};        // scoring plans read from HBM
   wfp::ScoreParams sp_search{}; // scoring candidates generated around an incumbent
   // uint32 times without a proof that none reaches 2^32: plans whose times
   // saturate are rescored with fp64 times
   bool checked = false;
   wfp::ScoreParams sp64{}, sp64_search{};
+  // the lean kernel for scores of plans read from HBM, when the window
+  // qualifies (lean.ok)
+  wfp::LeanParams lean{};
 };
 
 }  // namespace
@@ -240,6 +244,7 @@ void free_device_window(DeviceWindow& dw) {
   if (dw.tab) (void)hipFree(dw.tab);
   if (dw.tab64) (void)hipFree(dw.tab64);
   if (dw.scratch) (void)hipFree(dw.scratch);
+  if (dw.tab_lean) (void)hipFree(dw.tab_lean);
   dw = DeviceWindow{};
 }
 
@@ -581,6 +586,135 @@ wf_status plan_launch(wf_plan_ctx* ctx, const HostWindow& h, bool search, wfp::S
   return WF_OK;
 }
 
+// Per-wave LDS region of the lean kernel for G plans; returns its size.
+int lean_layout(const HostWindow& h, int G, int nwa, wfp::LeanOffsets& o) {
+  size_t off = 0;
+  auto take = [&](size_t n) {
+    const size_t at = off;
+    off = align_up(off + std::max<size_t>(n, 1), 16);
+    return (int)at;
+  };
+  const int NB = (h.N + 3) / 4;
+  o = wfp::LeanOffsets{};
+  o.flags = take((size_t)G * NB);
+  o.rec = take((size_t)G * h.N * 2);
+  o.mask = take((size_t)G * h.D * nwa * 8);
+  o.last = take((size_t)G * h.D * h.M * 4);
+  o.fin = take((size_t)G * h.N * 4);
+  o.wfm = take((size_t)G * std::max(1, h.W) * 4);
+  o.acc = take((size_t)G * 48);
+  o.bytes = (int)off;
+  return o.bytes;
+}
+
+// waves per workgroup of the lean kernel: two per SIMD
+constexpr int kLeanMaxWaves = 8;
+
+// Whether the lean kernel serves this window's plan scores, and its table
+// image and launch plan: uint32 times (proven or checked), the 4-bit
+// reclamation queue (at most 16 models, the default order, one unit per
+// device), at most 512 activations (9-bit slot entries), and the tables
+// plus the waves' regions in LDS.  Plans per wave: 64 / D; as many waves as
+// LDS holds, at most 8 per workgroup (two per SIMD at the kernel's register
+// use).
+void plan_lean(wf_plan_ctx* ctx, const HostWindow& h, const wfp::ScoreParams& sp, bool checked,
+               Image& img, wfp::LeanParams& lp) {
+  lp = wfp::LeanParams{};
+  const char* force = std::getenv("WF_PLAN_KERNEL");
+  if (force && std::strcmp(force, "general") == 0) return;
+  if (sp.time64 || (sp.nibble != 32 && sp.nibble != 64) || h.N < 1 || h.N > 512 || h.M > 16 ||
+      h.D > 64)
+    return;
+  const int N = h.N, D = h.D, M = h.M, W = h.W;
+  // ---- table image (same words as the general image where they coincide) ----
+  int64_t origin = INT64_MAX;
+  for (int32_t f = 0; f < W; ++f) origin = std::min(origin, h.arrival[f]);
+  for (int32_t d = 0; d < D; ++d) origin = std::min(origin, h.free0[d]);
+  if (origin == INT64_MAX) origin = 0;
+  if (origin != sp.origin) return;
+  std::vector<uint32_t> act((size_t)N), alv((size_t)N), aarr((size_t)N), arr((size_t)std::max(W, 1), 0);
+  std::vector<uint16_t> cnext((size_t)N);
+  for (int32_t f = 0; f < W; ++f) arr[f] = (uint32_t)(h.arrival[f] - origin);
+  for (int32_t i = 0; i < N; ++i) {
+    const bool ready = h.pred_off[i] == h.pred_off[i + 1] && h.arrival[h.act_wf[i]] <= 0;
+    act[i] = (uint32_t)h.act_model[i] | ((uint32_t)h.fusible[i] << 6) | ((uint32_t)ready << 7) |
+             ((uint32_t)h.wf_class[h.act_wf[i]] << 8) | ((uint32_t)h.act_wf[i] << 16);
+    cnext[i] = h.chain_next[i] >= 0 ? (uint16_t)h.chain_next[i] : (uint16_t)0xffff;
+    aarr[i] = arr[h.act_wf[i]];
+  }
+  for (int32_t l = 0; l < h.n_levels; ++l)
+    for (int32_t i = h.level_off[l]; i < h.level_off[l + 1]; ++i)
+      alv[i] = (uint32_t)h.level_off[l] | ((uint32_t)(h.level_off[l + 1] - h.level_off[l]) << 16);
+  const int32_t E = h.pred_off[N];
+  std::vector<uint32_t> edge((size_t)std::max(E, 1), 0);
+  for (int32_t v = 0; v < N; ++v)
+    for (int32_t k = h.pred_off[v]; k < h.pred_off[v + 1]; ++k)
+      edge[k] = (uint32_t)h.pred_idx[k] | ((uint32_t)v << 16);
+  std::vector<int32_t> eoff((size_t)h.n_levels + 1);
+  for (int32_t l = 0; l <= h.n_levels; ++l) eoff[l] = h.pred_off[h.level_off[l]];
+  // device-major: a device lane's rows are contiguous
+  std::vector<int32_t> um((size_t)N * D * 2), lw((size_t)M * D * 4, 0);
+  for (int32_t i = 0; i < N; ++i)
+    for (int32_t d = 0; d < D; ++d) {
+      um[((size_t)d * N + i) * 2] = h.lat[(size_t)i * D + d];
+      um[((size_t)d * N + i) * 2 + 1] = h.mem[(size_t)i * D + d];
+    }
+  for (int32_t m = 0; m < M; ++m)
+    for (int32_t d = 0; d < D; ++d) {
+      int32_t* r = &lw[((size_t)d * M + m) * 4];
+      r[0] = h.load[(size_t)m * D + d];
+      r[1] = h.wmib[m];
+      r[2] = (int32_t)((uint32_t)m * 0x11111111u);
+    }
+  std::vector<uint32_t> fr((size_t)D);
+  for (int32_t d = 0; d < D; ++d) fr[d] = (uint32_t)(h.free0[d] - origin);
+  std::vector<uint8_t> has_wf_succ((size_t)N, 0);
+  for (int32_t v = 0; v < N; ++v)
+    for (int32_t k = h.pred_off[v]; k < h.pred_off[v + 1]; ++k)
+      if (h.act_wf[h.pred_idx[k]] == h.act_wf[v]) has_wf_succ[h.pred_idx[k]] = 1;
+  std::vector<uint32_t> sink;
+  for (int32_t i = 0; i < N; ++i)
+    if (!has_wf_succ[i]) sink.push_back((uint32_t)i | ((uint32_t)h.act_wf[i] << 16));
+  if ((int)sink.size() != sp.S) return;
+  if (sink.empty()) sink.push_back(0);
+  wfp::LeanTab& t = lp.t;
+  t.lw = img.put(lw.data(), lw.size() * 4);
+  t.wmib = img.put(h.wmib.data(), h.wmib.size() * 4);
+  t.aarr = img.put(aarr.data(), aarr.size() * 4);
+  img.bytes.resize(align_up(img.bytes.size(), 16), 0);
+  t.lds_bytes = (int)img.bytes.size();
+  t.um = img.put(um.data(), um.size() * 4);
+  t.act = img.put(act.data(), act.size() * 4);
+  t.alv = img.put(alv.data(), alv.size() * 4);
+  t.cnext = img.put(cnext.data(), cnext.size() * 2);
+  t.edge = img.put(edge.data(), edge.size() * 4);
+  t.eoff = img.put(eoff.data(), eoff.size() * 4);
+  t.loff = img.put(h.level_off.data(), h.level_off.size() * 4);
+  t.cap = img.put(h.cap.data(), h.cap.size() * 4);
+  t.arr = img.put(arr.data(), arr.size() * 4);
+  t.res0 = img.put(h.init_res.data(), h.init_res.size() * 8);
+  t.free0 = img.put(fr.data(), fr.size() * 4);
+  t.sink = img.put(sink.data(), sink.size() * 4);
+  img.bytes.resize(align_up(img.bytes.size(), 16), 0);
+  t.bytes = (int)img.bytes.size();
+  // ---- launch plan ----
+  const int lds_cu = std::min(ctx->lds_per_cu, 160 * 1024);
+  const int lds_blk = std::min(ctx->lds_per_block, lds_cu);
+  const int G = std::max(1, 64 / D);
+  wfp::LeanOffsets o{};
+  const int wb = lean_layout(h, G, sp.nwa, o);
+  const int waves = std::min(kLeanMaxWaves, (lds_blk - t.lds_bytes) / std::max(wb, 1));
+  if (waves < 2) return;
+  lp.G = G;
+  lp.waves = waves;
+  lp.lds_bytes = t.lds_bytes + waves * wb;
+  lp.grid = ctx->n_cu * std::max(1, lds_cu / lp.lds_bytes);
+  lp.wo = o;
+  lp.checked = checked ? 1 : 0;
+  lp.qbits = sp.nibble;
+  lp.ok = 1;
+}
+
 // Launch parameters of one pass over n plans: the grid never exceeds the
 // groups there are.
 wfp::ScoreParams fit_grid(wfp::ScoreParams sp, int64_t n) {
@@ -609,6 +743,11 @@ const char* wf_plan_version(void) { return "wf_plan 0.2 (gfx950)"; }
 int wf_plan_time_bits(const wf_plan_ctx* ctx) {
   if (!ctx || !ctx->has_window) return 0;
   return ctx->dw.sp.time64 ? 64 : 32;
+}
+
+const char* wf_plan_score_kernel(const wf_plan_ctx* ctx) {
+  if (!ctx || !ctx->has_window) return "";
+  return ctx->dw.lean.ok ? "score_lean" : "score_plans";
 }
 
 const char* wf_plan_last_error(const wf_plan_ctx* ctx) {
@@ -767,6 +906,19 @@ wf_status wf_plan_upload_window(wf_plan_ctx* ctx, const wf_window_desc* w) {
   }
   sp.tab = static_cast<const unsigned char*>(dw.tab);
   sps.tab = static_cast<const unsigned char*>(dw.tab);
+  Image limg;
+  plan_lean(ctx, h, sp, checked, limg, dw.lean);
+  if (dw.lean.ok) {
+    e = hipMalloc(&dw.tab_lean, limg.bytes.size());
+    if (e == hipSuccess)
+      e = hipMemcpy(dw.tab_lean, limg.bytes.data(), limg.bytes.size(), hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+      free_device_window(dw);
+      (void)hipSetDevice(prev);
+      return hip_fail(ctx, e, "copying the lean kernel's tables to the device");
+    }
+    dw.lean.tab = static_cast<const unsigned char*>(dw.tab_lean);
+  }
   dw.sp = sp;
   dw.sp_search = sps;
   dw.checked = checked;
@@ -785,6 +937,10 @@ wf_status wf_plan_upload_window(wf_plan_ctx* ctx, const wf_window_desc* w) {
                  sp.waves, sp.grid, sp.wave_global ? "hbm+scratch" : (sp.tab_in_lds ? "lds" : "hbm"),
                  sp.t.bytes, sp.wo.bytes, sp.wave_global ? sp.wo.split : sp.wo.bytes, sp.lds_bytes, sp.nibble == 32 ? "queue32" : sp.nibble == 64 ? "queue64" : sp.nibble == -1 ? "paper-scan" :
                  sp.nibble == -2 ? "batch-scan" : sp.nibble == -3 ? "batch-paper-scan" : "scan");
+  if (std::getenv("WF_PLAN_VERBOSE") && dw.lean.ok)
+    std::fprintf(stderr, "[wf_plan] lean kernel: G=%d waves/wg=%d grid=%d tables=%d B wave=%d B lds/wg=%d\n",
+                 dw.lean.G, dw.lean.waves, dw.lean.grid, dw.lean.t.bytes, dw.lean.wo.bytes,
+                 dw.lean.lds_bytes);
   free_device_window(ctx->dw);
   ctx->dw = dw;
   ctx->host = std::move(h);
@@ -813,10 +969,25 @@ wf_status wf_plan_score_batch(wf_plan_ctx* ctx, const int8_t* dev, const uint16_
   (void)hipGetDevice(&prev);
   hipError_t e = hipSetDevice(ctx->device);
   if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
-  e = two_pass(ctx->dw, false, n_plans, [&](const wfp::ScoreParams& sp) {
-    return wfp::launch_score(sp, dev, prio, flags, n_plans, scores, sched, nullptr,
-                             static_cast<hipStream_t>(hip_stream));
-  });
+  const DeviceWindow& dw = ctx->dw;
+  if (!sched && dw.lean.ok) {
+    // the lean kernel, then (times not proven below 2^32) the general fp64
+    // pass over the groups holding a plan whose times saturated
+    wfp::LeanParams lp = dw.lean;
+    const int64_t groups = (n_plans + lp.G - 1) / lp.G;
+    const int64_t wgs = (groups + lp.waves - 1) / lp.waves;
+    if (wgs < lp.grid) lp.grid = (int)wgs;
+    e = wfp::launch_score_lean(dw.sp, lp, dev, prio, flags, n_plans, scores,
+                               static_cast<hipStream_t>(hip_stream));
+    if (e == hipSuccess && dw.checked)
+      e = wfp::launch_score(fit_grid(dw.sp64, n_plans), dev, prio, flags, n_plans, scores, nullptr,
+                            nullptr, static_cast<hipStream_t>(hip_stream));
+  } else {
+    e = two_pass(dw, false, n_plans, [&](const wfp::ScoreParams& sp) {
+      return wfp::launch_score(sp, dev, prio, flags, n_plans, scores, sched, nullptr,
+                               static_cast<hipStream_t>(hip_stream));
+    });
+  }
   (void)hipSetDevice(prev);
   if (e != hipSuccess) return hip_fail(ctx, e, "launching the scoring kernel");
   return WF_OK;

@@ -95,6 +95,63 @@ struct ScoreParams {
                               // times saturated (status bit kRescore of the first pass)
 };
 
+// Byte offsets inside one wave's LDS region of the lean kernel (lean.hip):
+// G plans, lane (g, d) = (lane / D, lane % D).
+struct LeanOffsets {
+  int flags;   // u8 [G][NB]       staged fuse/prefetch rows
+  int rec;     // u16 [G][N]       per resource-order slot: activation | model << 9 |
+               //                  prefetch << 13 | fused successor << 14
+  int mask;    // u64 [G][D][NWA]  slots of each device's units
+  int last;    // u32 [G][D][M]    1 + slot of the last unit of each (device, model), 0 = none
+  int fin;     // u32 [G][N]       latest predecessor finish, then the activation's own finish
+  int wfm;     // u32 [G][W]       latest finish per workflow, then its completion latency
+  int acc;     // LeanAcc [G]
+  int bytes;
+};
+
+// The lean kernel's window tables: one image in HBM whose first part (the
+// tables the walk reads per unit, lds_bytes) every workgroup copies into
+// LDS; the rest is read through the cache.
+struct LeanTab {
+  // LDS part
+  int lw;      // i32x4 [D][M] {load time, model weights, model id in every nibble, 0}
+  int wmib;    // i32 [M]
+  int aarr;    // u32 [N]    arrival of the activation's workflow (relative time)
+  int lds_bytes;
+  // through the cache
+  int um;      // i32x2 [D][N] {run time (-1 ineligible), activation memory} of each
+               //            activation on each device
+  int act;     // u32 [N]    as TabOffsets::act
+  int alv;     // u32 [N]    as TabOffsets::alv
+  int cnext;   // u16 [N]    as TabOffsets::cnext
+  int edge;    // u32 [E]    as TabOffsets::edge
+  int eoff;    // i32 [L+1]
+  int loff;    // i32 [L+1]
+  int cap;     // i32 [D]
+  int arr;     // u32 [W]    workflow arrival (relative time)
+  int res0;    // u64 [D]
+  int free0;   // u32 [D]
+  int sink;    // u32 [S]    as TabOffsets::sink
+  int bytes;
+};
+
+// Launch plan of the lean kernel (the scalar objective of plans read from
+// HBM, uint32 times, at most 16 models in a 4-bit queue, one unit per
+// device, the default reclamation order, at most 512 activations).
+struct LeanParams {
+  int ok;          // 1: the window qualifies and a layout fits in LDS
+  int checked;     // 1: uint32 additions saturate and flag the plan for the fp64 pass
+  int qbits;       // reclamation queue width: 32 or 64
+  int G, waves, grid, lds_bytes;
+  const unsigned char* tab;  // the lean table image in HBM
+  LeanTab t;
+  LeanOffsets wo;  // wave regions follow the image's LDS part
+};
+
+hipError_t launch_score_lean(const ScoreParams& sp, const LeanParams& lp, const int8_t* dev,
+                             const uint16_t* prio, const uint8_t* flags, int64_t n_plans,
+                             wf_plan_score* scores, hipStream_t stream);
+
 // Internal status bit of a uint32-time pass: some time of the plan reached
 // 2^32 - 1 (saturated), so an fp64 pass rescores it.  Never left in a record
 // a call returns.

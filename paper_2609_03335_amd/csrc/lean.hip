@@ -1,0 +1,716 @@
+// The lean scoring kernel: the scalar objective of plans read from HBM for
+// windows whose times fit uint32 offsets and whose resident sets fit a queue
+// of 4-bit model ids (at most 16 models), with one unit per device, the
+// default reclamation order and at most 512 activations -- the configuration
+// the throughput workload (256 activations x 1,048,576 plans) runs in.  Same
+// results as the general kernel of score_kernel.h, with only the code this
+// configuration needs: 16-bit slot entries, no schedule, key, search,
+// batch-limit or fp64 paths, and the per-unit tables of the walk in LDS.
+//
+// A persistent grid of waves loops over groups of G plans; lane (g, d) =
+// (lane / D, lane % D) owns device d of plan g.  Per group:
+//   1. flag rows are staged into LDS; the resource order (Eq. 10) puts each
+//      unit head at slot = its priority when each level's head priorities
+//      are distinct values of the level's index range (checked by counting),
+//      else at its rank by (priority, index) within the level; a 16-bit slot
+//      entry, the device's slot mask and each (device, model)'s last slot are
+//      recorded;
+//   2. per topological level, releases (Eq. 2) by LDS atomic max over the
+//      level's incoming edges, then each device lane walks its units of the
+//      level in slot order: reuse / reclaim / load (Eq. 5, Eq. 11) on a
+//      4-bit queue of the resident models and the max-plus timeline of Eq. 7;
+//   3. makespan, nearest-rank p95, objective, headroom and counts.
+// Memory is tracked as the excess of a unit's need over the device's free
+// memory: a unit fits when its excess after reclamation is <= 0, the device's
+// peak is its capacity plus the largest such excess, so the peak, the
+// CAPACITY test and the headroom need one max per unit.
+#include <type_traits>
+
+#include "kernels.h"
+
+namespace wfp {
+namespace {
+
+struct LeanAcc {
+  uint32_t status;
+  int32_t headroom;
+  uint32_t loads;
+  uint32_t evicts;
+  uint32_t max_finish;  // relative time
+  uint32_t p95;         // selected completion latency
+  uint32_t heads;       // unit heads given a slot by the first ordering try
+  uint32_t claimed;     // distinct slots they occupy
+  uint32_t bad;         // a head priority outside its level's index range
+  uint32_t pad[3];
+};
+static_assert(sizeof(LeanAcc) == 48, "LeanAcc layout");
+
+// slot entry
+constexpr uint32_t kEAct = 0x1ffu;
+constexpr uint32_t kEPf = 1u << 13;
+constexpr uint32_t kEChain = 1u << 14;
+
+__device__ __forceinline__ void lsync() {
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+}
+
+__device__ __forceinline__ void zero16(unsigned char* dst, int nbytes, int lane) {
+  uint4* d = reinterpret_cast<uint4*>(dst);
+  const int n16 = nbytes >> 4;
+  for (int i = lane; i < n16; i += 64) d[i] = make_uint4(0u, 0u, 0u, 0u);
+  for (int i = (n16 << 4) + lane; i < nbytes; i += 64) dst[i] = 0;
+}
+
+__device__ __forceinline__ void stage_rows(unsigned char* dst, const unsigned char* src, int nbytes,
+                                           int lane) {
+  const uintptr_t a = reinterpret_cast<uintptr_t>(src);
+  if (((a | (uintptr_t)nbytes) & 15) == 0) {
+    const uint4* s = reinterpret_cast<const uint4*>(src);
+    uint4* d = reinterpret_cast<uint4*>(dst);
+    for (int i = lane; i < (nbytes >> 4); i += 64) d[i] = s[i];
+  } else if (((a | (uintptr_t)nbytes) & 3) == 0) {
+    const uint32_t* s = reinterpret_cast<const uint32_t*>(src);
+    uint32_t* d = reinterpret_cast<uint32_t*>(dst);
+    for (int i = lane; i < (nbytes >> 2); i += 64) d[i] = s[i];
+  } else {
+    for (int i = lane; i < nbytes; i += 64) dst[i] = src[i];
+  }
+}
+
+__device__ __forceinline__ uint32_t fuse_of(const uint8_t* fl, int v) {
+  return ((uint32_t)fl[v >> 2] >> ((v & 3) << 1)) & 1u;
+}
+
+// uint32 time addition: saturating when the window's bound is not proven
+// below 2^32 (a saturated time only grows through the max-plus steps, so it
+// ends in its device's last finish, where it is detected)
+template <bool CHECKED>
+__device__ __forceinline__ uint32_t tadd(uint32_t a, uint32_t b) {
+  if constexpr (CHECKED)
+    return __builtin_elementwise_add_sat(a, b);
+  else
+    return a + b;
+}
+
+__device__ __forceinline__ uint32_t umax(uint32_t a, uint32_t b) { return a > b ? a : b; }
+
+template <bool CHECKED, int QB>
+__global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
+                                                  const int8_t* __restrict__ dev_all,
+                                                  const uint16_t* __restrict__ prio_all,
+                                                  const uint8_t* __restrict__ flags_all, int64_t P,
+                                                  wf_plan_score* __restrict__ scores) {
+  using QT = std::conditional_t<QB == 32, uint32_t, uint64_t>;
+  constexpr QT kOnes = (QT)0x1111111111111111ull, kHigh = (QT)0x8888888888888888ull;
+  extern __shared__ __align__(16) unsigned char lds[];
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int N = sp.N, W = sp.W, M = sp.M, D = sp.D, NB = sp.NB, G = lp.G, NWA = sp.nwa;
+
+  // ---- window tables: the per-unit ones in LDS, the rest through the cache ----
+  {
+    const uint4* src = reinterpret_cast<const uint4*>(lp.tab);
+    uint4* dst = reinterpret_cast<uint4*>(lds);
+    for (int i = tid; i < (lp.t.lds_bytes >> 4); i += blockDim.x) dst[i] = src[i];
+  }
+  __syncthreads();
+  const unsigned char* tg = lp.tab;
+  const int4* t_lw = reinterpret_cast<const int4*>(lds + lp.t.lw);
+  const int32_t* t_wmib = reinterpret_cast<const int32_t*>(lds + lp.t.wmib);
+  const uint32_t* t_aarr = reinterpret_cast<const uint32_t*>(lds + lp.t.aarr);
+  const int2* t_um = reinterpret_cast<const int2*>(tg + lp.t.um);
+  const uint32_t* t_act = reinterpret_cast<const uint32_t*>(tg + lp.t.act);
+  const uint32_t* t_alv = reinterpret_cast<const uint32_t*>(tg + lp.t.alv);
+  const uint16_t* t_cnext = reinterpret_cast<const uint16_t*>(tg + lp.t.cnext);
+  const uint32_t* t_edge = reinterpret_cast<const uint32_t*>(tg + lp.t.edge);
+  const int32_t* t_eoff = reinterpret_cast<const int32_t*>(tg + lp.t.eoff);
+  const int32_t* t_loff = reinterpret_cast<const int32_t*>(tg + lp.t.loff);
+  const int32_t* t_cap = reinterpret_cast<const int32_t*>(tg + lp.t.cap);
+  const uint32_t* t_arr = reinterpret_cast<const uint32_t*>(tg + lp.t.arr);
+  const unsigned long long* t_res0 = reinterpret_cast<const unsigned long long*>(tg + lp.t.res0);
+  const uint32_t* t_free0 = reinterpret_cast<const uint32_t*>(tg + lp.t.free0);
+  const uint32_t* t_sink = reinterpret_cast<const uint32_t*>(tg + lp.t.sink);
+
+  // ---- this wave's LDS region ----
+  unsigned char* wl = lds + lp.t.lds_bytes + lp.wo.bytes * wid;
+  uint8_t* s_fl = wl + lp.wo.flags;
+  uint16_t* s_rec = reinterpret_cast<uint16_t*>(wl + lp.wo.rec);
+  unsigned long long* s_mask = reinterpret_cast<unsigned long long*>(wl + lp.wo.mask);
+  uint32_t* s_last = reinterpret_cast<uint32_t*>(wl + lp.wo.last);
+  uint32_t* s_fin = reinterpret_cast<uint32_t*>(wl + lp.wo.fin);
+  uint32_t* s_wfm = reinterpret_cast<uint32_t*>(wl + lp.wo.wfm);
+  LeanAcc* s_acc = reinterpret_cast<LeanAcc*>(wl + lp.wo.acc);
+
+  const int g_me = lane / D;
+  const int d_me = lane - g_me * D;
+  const int64_t n_groups = (P + G - 1) / G;
+  const int64_t stride = (int64_t)gridDim.x * lp.waves;
+  // this lane's device rows
+  const int2* um_d = t_um + d_me * N;
+  const int4* lw_d = t_lw + d_me * M;
+
+  // rows read four activations per lane with 4- and 8-byte loads
+  const bool vec = (N & 3) == 0 && (reinterpret_cast<uintptr_t>(dev_all) & 3) == 0 &&
+                   (reinterpret_cast<uintptr_t>(prio_all) & 7) == 0;
+  // the order sweep takes four plans at a time (all their row loads issued
+  // before any is used)
+  constexpr int kB = 4;
+  const bool pre = false;
+  uint32_t dvp[kB];
+  uint2 pvp[kB];
+  auto load_rows = [&](int64_t grp_, uint32_t* dv, uint2* pv) {
+    const int64_t q0 = grp_ * G;
+    const int gq = (int)((P - q0) < G ? (P - q0) : G);
+    const int uc = 4 * lane < N ? 4 * lane : 0;
+#pragma unroll
+    for (int k = 0; k < kB; ++k) {
+      const int g = k < gq ? k : gq - 1;
+      dv[k] = *reinterpret_cast<const uint32_t*>(dev_all + (q0 + g) * N + uc);
+      pv[k] = *reinterpret_cast<const uint2*>(prio_all + (q0 + g) * N + uc);
+    }
+  };
+  {
+    const int64_t g_first = (int64_t)blockIdx.x * lp.waves + wid;
+    if (pre && g_first < n_groups) load_rows(g_first, dvp, pvp);
+  }
+
+  for (int64_t grp = (int64_t)blockIdx.x * lp.waves + wid; grp < n_groups; grp += stride) {
+    const int64_t p0 = grp * G;
+    const int gc = (int)((P - p0) < G ? (P - p0) : G);
+
+    stage_rows(s_fl, flags_all + p0 * NB, gc * NB, lane);
+    zero16(reinterpret_cast<unsigned char*>(s_last), G * D * M * 4, lane);
+    zero16(reinterpret_cast<unsigned char*>(s_mask), G * D * NWA * 8, lane);
+    if (lane < G) {
+      LeanAcc a0{};
+      a0.headroom = 0x7fffffff;
+      s_acc[lane] = a0;
+    }
+    lsync();
+
+    // ---- resource order (Eq. 10), first try: slot = priority ----
+    auto order_one = [&](int g, int u, int d, int pr, uint32_t a, uint32_t lvw, uint32_t c,
+                         uint32_t fb, uint32_t cbyte, uint32_t& nh, uint32_t& nbad,
+                         uint32_t& ninel) {
+      const bool head = !((fb & 1u) && (a & 64u));  // not a fused chain member
+      const bool okd = (unsigned)d < (unsigned)D;
+      const bool inr = (unsigned)(pr - (int)(lvw & 0xffffu)) < (lvw >> 16);
+      const bool chain = c != 0xffffu && ((cbyte >> ((c & 3u) << 1)) & 1u);
+      ninel |= (uint32_t)(head && !okd);
+      nbad |= (uint32_t)(head && okd && !inr);
+      if (head && okd && inr) {
+        const uint32_t m = a & 63u;
+        s_rec[g * N + pr] =
+            (uint16_t)((uint32_t)u | (m << 9) | ((fb & 2u) << 12) | (chain ? kEChain : 0u));
+        atomicOr(&s_mask[(g * D + d) * NWA + (pr >> 6)], 1ull << (pr & 63));
+        atomicMax(&s_last[(g * D + d) * M + (int)m], (uint32_t)pr + 1u);
+        ++nh;
+      }
+    };
+    auto flush4 = [&](int g, uint32_t nh, uint32_t nbad, uint32_t ninel) {
+      const uint32_t tot = (uint32_t)__popcll(__ballot(nh & 1u)) +
+                           2u * (uint32_t)__popcll(__ballot(nh & 2u)) +
+                           4u * (uint32_t)__popcll(__ballot(nh & 4u));
+      const bool any_bad = __ballot(nbad != 0u) != 0ull;
+      const bool any_inel = __ballot(ninel != 0u) != 0ull;
+      if (lane == 0) {
+        if (any_inel) s_acc[g].status |= (uint32_t)WF_ST_INELIGIBLE;
+        if (any_bad) s_acc[g].bad = 1u;
+        s_acc[g].heads += tot;
+      }
+    };
+    if (vec) {
+      for (int base = 0; base < N; base += 256) {
+        const int u0 = base + 4 * lane;
+        const bool live = u0 < N;
+        const int uc = live ? u0 : 0;
+        const uint4 act4 = *reinterpret_cast<const uint4*>(t_act + uc);
+        const uint4 alv4 = *reinterpret_cast<const uint4*>(t_alv + uc);
+        const uint2 cn4 = *reinterpret_cast<const uint2*>(t_cnext + uc);
+        const uint32_t cn[4] = {cn4.x & 0xffffu, cn4.x >> 16, cn4.y & 0xffffu, cn4.y >> 16};
+        for (int g0 = 0; g0 < gc; g0 += kB) {
+          uint32_t dv[kB], fl[kB], cb[kB][4];
+          uint2 pv[kB];
+#pragma unroll
+          for (int k = 0; k < kB; ++k) {
+            const int g = (g0 + k < gc) ? g0 + k : gc - 1;
+            if (pre) {
+              dv[k] = dvp[k];
+              pv[k] = pvp[k];
+            } else {
+              dv[k] = *reinterpret_cast<const uint32_t*>(dev_all + (p0 + g) * N + uc);
+              pv[k] = *reinterpret_cast<const uint2*>(prio_all + (p0 + g) * N + uc);
+            }
+          }
+#pragma unroll
+          for (int k = 0; k < kB; ++k) {
+            const int g = (g0 + k < gc) ? g0 + k : gc - 1;
+            fl[k] = s_fl[g * NB + (uc >> 2)];
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+              cb[k][j] = sp.has_chains
+                             ? s_fl[g * NB + ((cn[j] != 0xffffu ? cn[j] : (uint32_t)uc) >> 2)]
+                             : 0u;
+          }
+#pragma unroll
+          for (int k = 0; k < kB; ++k) {
+            const int g = g0 + k;
+            if (g >= gc) break;
+            uint32_t nh = 0, nbad = 0, ninel = 0;
+            if (live) {
+              order_one(g, uc, (int)(int8_t)(dv[k] & 0xffu), (int)(pv[k].x & 0xffffu), act4.x,
+                        alv4.x, cn[0], fl[k], cb[k][0], nh, nbad, ninel);
+              order_one(g, uc + 1, (int)(int8_t)((dv[k] >> 8) & 0xffu), (int)(pv[k].x >> 16),
+                        act4.y, alv4.y, cn[1], fl[k] >> 2, cb[k][1], nh, nbad, ninel);
+              order_one(g, uc + 2, (int)(int8_t)((dv[k] >> 16) & 0xffu), (int)(pv[k].y & 0xffffu),
+                        act4.z, alv4.z, cn[2], fl[k] >> 4, cb[k][2], nh, nbad, ninel);
+              order_one(g, uc + 3, (int)(int8_t)(dv[k] >> 24), (int)(pv[k].y >> 16), act4.w,
+                        alv4.w, cn[3], fl[k] >> 6, cb[k][3], nh, nbad, ninel);
+            }
+            flush4(g, nh, nbad, ninel);
+          }
+        }
+      }
+    } else {
+      for (int g = 0; g < gc; ++g) {
+        const int8_t* pdev = dev_all + (p0 + g) * N;
+        const uint16_t* pprio = prio_all + (p0 + g) * N;
+        const uint8_t* pfl = s_fl + g * NB;
+        uint32_t nh = 0, nbad = 0, ninel = 0;
+        for (int u = lane; u < N; u += 64) {
+          const uint32_t fb = (uint32_t)pfl[u >> 2] >> ((u & 3) << 1);
+          const uint32_t c = t_cnext[u];
+          const uint32_t cbyte = pfl[(c != 0xffffu ? c : (uint32_t)u) >> 2];
+          order_one(g, u, pdev[u], pprio[u], t_act[u], t_alv[u], c, fb, cbyte, nh, nbad, ninel);
+        }
+        if (ninel) atomicOr(&s_acc[g].status, (uint32_t)WF_ST_INELIGIBLE);
+        if (nbad) atomicOr(&s_acc[g].bad, 1u);
+        if (nh) atomicAdd(&s_acc[g].heads, nh);
+      }
+    }
+    lsync();
+    // distinct slots claimed per plan: the union of its devices' masks
+    for (int i = lane; i < gc * NWA; i += 64) {
+      const int g = i / NWA, w = i - g * NWA;
+      unsigned long long x = 0ull;
+      for (int d = 0; d < D; ++d) x |= s_mask[(g * D + d) * NWA + w];
+      if (x) atomicAdd(&s_acc[g].claimed, (uint32_t)__popcll(x));
+    }
+    lsync();
+    uint64_t rankedm;
+    {
+      const LeanAcc& ag = s_acc[lane < gc ? lane : 0];  // G <= 64
+      rankedm = __ballot(lane < gc && (ag.bad != 0u || ag.heads != ag.claimed));
+    }
+    // plans whose priorities are not a permutation of each level's heads'
+    // index range: rank by (priority, index) within each level
+    for (uint64_t rm = rankedm; rm; rm &= rm - 1ull) {
+      const int g = __builtin_ctzll(rm);
+      const int8_t* pdev = dev_all + (p0 + g) * N;
+      const uint16_t* pprio = prio_all + (p0 + g) * N;
+      const uint8_t* pfl = s_fl + g * NB;
+      uint16_t* rec = s_rec + g * N;
+      unsigned long long* mk = s_mask + g * D * NWA;
+      uint32_t* lastp = s_last + g * D * M;
+      for (int i = lane; i < D * NWA; i += 64) mk[i] = 0ull;
+      for (int i = lane; i < D * M; i += 64) lastp[i] = 0u;
+      lsync();
+      for (int u = lane; u < N; u += 64) {
+        const uint32_t a = t_act[u];
+        const uint32_t fb = (uint32_t)pfl[u >> 2] >> ((u & 3) << 1);
+        if ((fb & 1u) && (a & 64u)) continue;
+        const int d = pdev[u];
+        if ((unsigned)d >= (unsigned)D) continue;
+        const uint32_t lvw = t_alv[u];
+        const int lo = (int)(lvw & 0xffffu), hi = lo + (int)(lvw >> 16);
+        const int pu = pprio[u];
+        int slot = lo;
+        for (int j = lo; j < hi; ++j) {
+          if (fuse_of(pfl, j) && (t_act[j] & 64u)) continue;
+          if ((unsigned)pdev[j] >= (unsigned)D) continue;
+          const int pj = pprio[j];
+          slot += (pj < pu) || (pj == pu && j < u);
+        }
+        const int c = t_cnext[u];
+        const bool chain = c != 0xffff && fuse_of(pfl, c);
+        rec[slot] = (uint16_t)((uint32_t)u | ((a & 63u) << 9) | ((fb & 2u) << 12) |
+                               (chain ? kEChain : 0u));
+        atomicOr(&mk[d * NWA + (slot >> 6)], 1ull << (slot & 63));
+        atomicMax(&lastp[d * M + (int)(a & 63u)], (uint32_t)slot + 1u);
+      }
+      lsync();
+    }
+    if (pre && grp + stride < n_groups) load_rows(grp + stride, dvp, pvp);
+
+    // ---- device-lane state ----
+    const bool act = g_me < gc;
+    const int gme = act ? g_me : 0;
+    const int d = d_me;
+    const uint32_t* mylast = s_last + (gme * D + d) * M;
+    const unsigned long long* mymask64 = s_mask + (gme * D + d) * NWA;
+    uint16_t* myrec = s_rec + gme * N;
+    uint32_t* myfin = s_fin + gme * N;
+    const uint8_t* myfl = s_fl + gme * NB;
+    // reclamation queue of the resident models, 4 bits each, next victim in
+    // the low bits: first the nd4 / 4 models with no remaining use on this
+    // device, then those still needed, each part least recently used first
+    // (never used: by id); nq4 / 4 entries in all
+    QT Q = 0;
+    uint32_t nq4 = 0, nd4 = 0;
+    int32_t fm = 0;   // free memory: capacity - resident weights
+    int32_t pe = 0;   // largest excess of a unit's need over the free memory
+    uint32_t freet = 0, nld = 0, nev4 = 0, inel = 0;
+    if (act) {
+      const uint64_t res = t_res0[d];
+      const int32_t capd = t_cap[d];
+      freet = t_free0[d];
+      int32_t used = 0;
+      QT qa = 0;
+      uint32_t na = 0;
+      for (uint64_t r = res; r; r &= r - 1) {
+        const int m = __builtin_ctzll(r);
+        used += t_wmib[m];
+        if (mylast[m] == 0u) {
+          Q |= (QT)m << nd4;
+          nd4 += 4;
+        } else {
+          qa |= (QT)m << na;
+          na += 4;
+        }
+      }
+      if (na) Q |= qa << nd4;  // nd4 + na <= QB here
+      nq4 = nd4 + na;
+      fm = capd - used;
+      pe = used - capd;
+    }
+
+    // every finish starts at 0: it accumulates the latest predecessor finish
+    // before its level, then holds the activation's own finish
+    zero16(reinterpret_cast<unsigned char*>(s_fin), G * N * 4, lane);
+    zero16(reinterpret_cast<unsigned char*>(s_wfm), G * W * 4, lane);
+    lsync();
+
+    for (int lv = 0; lv < sp.n_levels; ++lv) {
+      const int lo = t_loff[lv], hi = t_loff[lv + 1];
+      const int eb = t_eoff[lv], ee = t_eoff[lv + 1];
+      // ---- latest predecessor finish of the level's activations (Eq. 2):
+      // one lane per incoming edge; a fused chain member already holds its
+      // own, later, finish ----
+      if (ee > eb) {
+        for (int e = eb + lane; e < ee; e += 64) {
+          const uint32_t ed = t_edge[e];
+          const int src = (int)(ed & 0xffffu), dst = (int)(ed >> 16);
+          for (int g0 = 0; g0 < gc; g0 += kB) {
+            uint32_t f[kB];
+#pragma unroll
+            for (int k = 0; k < kB; ++k) {
+              const int g = (g0 + k < gc) ? g0 + k : gc - 1;
+              f[k] = s_fin[g * N + src];
+            }
+#pragma unroll
+            for (int k = 0; k < kB; ++k)
+              if (g0 + k < gc) atomicMax(&s_fin[(g0 + k) * N + dst], f[k]);
+          }
+        }
+        lsync();
+      }
+
+      // ---- device lanes walk their units of the level in slot order ----
+      if (act) {
+        const int j1 = (hi - 1) >> 6;
+        const unsigned long long hmask = (hi & 63) ? ((1ull << (hi & 63)) - 1ull) : ~0ull;
+        const int width = hi - lo;
+        const bool narrow = width <= 64;
+        int j = lo >> 6;
+        unsigned long long bits, wnext = 0ull;
+        if (narrow) {
+          const int sh = lo & 63;
+          bits = mymask64[j] >> sh;
+          if (sh + width > 64) bits |= mymask64[j + 1] << (64 - sh);
+          if (width < 64) bits &= (1ull << width) - 1ull;
+        } else {
+          bits = mymask64[j] & (~0ull << (lo & 63));
+          if (j < j1) wnext = mymask64[j + 1] & ((j + 1 == j1) ? hmask : ~0ull);
+        }
+        // the device's next slot of the level; -1 when there is none, -2
+        // for a trip without a unit (a finished word followed by an empty one)
+        auto next_narrow = [&]() -> int {
+          const int sl = lo + __builtin_ctzll(bits | (1ull << 63));
+          const bool have = bits != 0ull;
+          bits &= bits - 1ull;
+          return have ? sl : -1;
+        };
+        auto next_wide = [&]() -> int {
+          const bool adv = bits == 0ull && j < j1;
+          bits = adv ? wnext : bits;
+          j += adv ? 1 : 0;
+          const int jn = j + 1 <= j1 ? j + 1 : j1;
+          const unsigned long long wl2 = mymask64[jn] & ((jn == j1) ? hmask : ~0ull);
+          wnext = adv ? (j < j1 ? wl2 : 0ull) : wnext;
+          const int sl = (j << 6) + __builtin_ctzll(bits | (1ull << 63));
+          const bool have = bits != 0ull;
+          bits &= bits - 1ull;
+          return have ? sl : (j < j1 ? -2 : -1);
+        };
+        // everything of a unit that does not depend on the device's
+        // sequential state; without a slot, activation 0 and model 0 keep
+        // every address in range
+        struct U { int slot; uint32_t e, lst, arr, r; int32_t lat, mem; int4 lw; };
+        auto fetch = [&](int sl, U& X) {
+          X.slot = sl;
+          const uint32_t e = sl >= 0 ? (uint32_t)myrec[sl] : 0u;
+          X.e = e;
+          const uint32_t u = e & kEAct, m = (e >> 9) & 15u;
+          X.lst = mylast[m] == (uint32_t)sl + 1u ? 1u : 0u;
+          const int2 r = um_d[u];
+          X.lat = r.x;
+          X.mem = r.y;
+          X.arr = t_aarr[u];
+          X.r = umax(myfin[u], X.arr);
+          X.lw = lw_d[m];
+        };
+        auto process = [&](const U& X) {
+          if (X.slot < 0) return;
+          const uint32_t u = X.e & kEAct;
+          const uint32_t m = (X.e >> 9) & 15u;
+          // run time (summed over a fused chain, Eq. 4) and memory (max)
+          uint32_t T = (uint32_t)X.lat;
+          int32_t mx = X.mem;
+          inel |= (uint32_t)X.lat >> 31;
+          if (X.e & kEChain) {
+            for (int v = t_cnext[u];;) {
+              const int2 lm = um_d[v];
+              inel |= (uint32_t)lm.x >> 31;
+              T += (uint32_t)lm.x;
+              mx = lm.y > mx ? lm.y : mx;
+              const int c = t_cnext[v];
+              if (c == 0xffff || !fuse_of(myfl, c)) break;
+              v = c;
+            }
+          }
+          // residency: m is resident when its nibble is among the first
+          // nq4 / 4 entries; a hit takes it out of the queue (it re-enters
+          // below as the most recent)
+          QT mq = (QT)(uint32_t)X.lw.z;
+          if constexpr (QB == 64) mq |= mq << 32;
+          const QT x = Q ^ mq;
+          QT z = (x - kOnes) & ~x & kHigh;  // lowest flag: first zero nibble
+          const QT valid = nq4 >= (uint32_t)QB ? ~(QT)0 : (((QT)1 << nq4) - (QT)1);
+          z &= valid;
+          const bool hit = z != (QT)0;
+          uint32_t s4;
+          if constexpr (QB == 64)
+            s4 = (uint32_t)__builtin_ctzll(z | (1ull << 63)) & ~3u;
+          else
+            s4 = (uint32_t)__builtin_ctz(z | (1u << 31)) & ~3u;
+          {
+            const QT lowm = ((QT)1 << s4) - (QT)1;
+            const QT rem = (Q & lowm) | ((Q >> 4) & ~lowm);
+            Q = hit ? rem : Q;
+          }
+          nq4 -= hit ? 4u : 0u;
+          const int32_t need = mx + (hit ? 0 : X.lw.y);
+          int32_t ex = need - fm;  // > 0: the unit does not fit yet
+          // reclaim (Sec. 3.5) from the queue's front: no remaining use
+          // first, then least recently used, then the lower model id; the
+          // first two victims branch-free, any further ones in a loop
+          {
+            const int32_t w0 = t_wmib[(int)(Q & (QT)15)];
+            const int32_t w1 = t_wmib[(int)((Q >> 4) & (QT)15)];
+            const bool c0 = ex > 0 && nq4 >= 4u;
+            const int32_t ex0 = ex - w0;
+            const bool c1 = c0 && ex0 > 0 && nq4 >= 8u;
+            const uint32_t k4 = (c0 ? 4u : 0u) + (c1 ? 4u : 0u);
+            ex = c1 ? ex0 - w1 : (c0 ? ex0 : ex);
+            Q >>= k4;
+            nq4 -= k4;
+            nd4 = nd4 > k4 ? nd4 - k4 : 0u;
+            nev4 += k4;
+            while (ex > 0 && nq4 >= 4u && c1) {
+              const int v = (int)(Q & (QT)15);
+              Q >>= 4;
+              nq4 -= 4u;
+              nd4 = nd4 > 4u ? nd4 - 4u : 0u;
+              ex -= t_wmib[v];
+              nev4 += 4u;
+            }
+          }
+          // peak memory = capacity + the largest excess after reclamation;
+          // free memory after the load: mx - ex
+          pe = ex > pe ? ex : pe;
+          fm = mx - ex;
+          // m re-enters after the no-remaining-use part when this was its
+          // last unit on the device, else at the end
+          {
+            const uint32_t pos = X.lst ? nd4 : nq4;
+            const QT lowm = ((QT)1 << pos) - (QT)1;
+            Q = (Q & lowm) | ((QT)m << pos) | ((Q & ~lowm) << 4);
+            nd4 += X.lst ? 4u : 0u;
+            nq4 += 4u;
+          }
+          nld += hit ? 0u : 1u;
+          // timeline (Eq. 7): a load waits for the device and starts at the
+          // release, or at the workflow arrival when prefetched; the unit
+          // starts at max(release, load end), or at max(release, device
+          // free) when its model was resident
+          const uint32_t a0 = (X.e & kEPf) ? X.arr : X.r;
+          const uint32_t ls = umax(a0, freet);
+          const uint32_t le = tadd<CHECKED>(ls, (uint32_t)X.lw.x);
+          const uint32_t s = umax(X.r, hit ? freet : le);
+          if (!(X.e & kEChain)) {
+            const uint32_t f = tadd<CHECKED>(s, T);
+            myfin[u] = f;
+            freet = f;
+          } else {
+            // members back to back on the head's device
+            uint32_t t = s;
+            for (int v = (int)u;;) {
+              const uint32_t tv = tadd<CHECKED>(t, (uint32_t)um_d[v].x);
+              myfin[v] = tv;
+              t = tv;
+              const int c = t_cnext[v];
+              if (c == 0xffff || !fuse_of(myfl, c)) break;
+              v = c;
+            }
+            freet = t;
+          }
+        };
+        // two units per trip so that the prefetched unit needs no copy; one
+        // copy of the loop per kind of level
+        auto run = [&](auto&& next_slot) {
+          U A, B;
+          fetch(next_slot(), A);
+          while (A.slot != -1) {
+            fetch(next_slot(), B);
+            process(A);
+            if (B.slot == -1) break;
+            fetch(next_slot(), A);
+            process(B);
+          }
+        };
+        if (narrow)
+          run(next_narrow);
+        else
+          run(next_wide);
+      }
+      lsync();
+    }
+
+    // ---- per-plan reductions (Sec. 4 metrics) ----
+    if (act) {
+      atomicMin(&s_acc[gme].headroom, -pe);
+      atomicAdd(&s_acc[gme].loads, nld);
+      atomicAdd(&s_acc[gme].evicts, nev4 >> 2);
+      uint32_t st = pe > 0 ? (uint32_t)WF_ST_CAPACITY : 0u;
+      if (inel) st |= (uint32_t)WF_ST_INELIGIBLE;
+      // a saturated time ends in the device's last finish
+      if (CHECKED && freet == 0xffffffffu) st |= kRescore;
+      if (st) atomicOr(&s_acc[gme].status, st);
+    }
+    // a workflow's completion is the latest finish among its activations
+    // without a successor in the same workflow
+    for (int i = lane; i < sp.S; i += 64) {
+      const uint32_t sk = t_sink[i];
+      const int src = (int)(sk & 0xffffu), wf = (int)(sk >> 16);
+      for (int g0 = 0; g0 < gc; g0 += kB) {
+        uint32_t f[kB];
+#pragma unroll
+        for (int k = 0; k < kB; ++k) {
+          const int g = (g0 + k < gc) ? g0 + k : gc - 1;
+          f[k] = s_fin[g * N + src];
+        }
+#pragma unroll
+        for (int k = 0; k < kB; ++k)
+          if (g0 + k < gc) atomicMax(&s_wfm[(g0 + k) * W + wf], f[k]);
+      }
+    }
+    lsync();
+    // completion latencies in place, and the latest finish
+    for (int it = lane; it < gc * W; it += 64) {
+      const int g = it / W, a = it - g * W;
+      const uint32_t fb = s_wfm[it];
+      atomicMax(&s_acc[g].max_finish, fb);
+      s_wfm[it] = fb - t_arr[a];
+    }
+    lsync();
+    // nearest-rank p95: the ceil(0.95 W)-th smallest completion latency,
+    // lanes over (plan, workflow)
+    const int kk = (95 * W + 99) / 100;
+    for (int it = lane; it < gc * W; it += 64) {
+      const int g = it / W;
+      const uint32_t* cw = s_wfm + g * W;
+      const uint32_t ca = cw[it - g * W];
+      int lt = 0, le = 0;
+#pragma unroll 8
+      for (int b = 0; b < W; ++b) {
+        const uint32_t cb = cw[b];
+        lt += cb < ca;
+        le += cb <= ca;
+      }
+      if (lt < kk && kk <= le) s_acc[g].p95 = ca;
+    }
+    lsync();
+    if (lane < gc) {
+      const LeanAcc a = s_acc[lane];
+      wf_plan_score sc;
+      if (a.status & WF_ST_INELIGIBLE) {
+        sc.makespan_us = 0;
+        sc.p95_us = 0;
+        sc.objective = 0.0f;
+        sc.status = WF_ST_INELIGIBLE;
+        sc.min_headroom_mib = 0;
+        sc.n_loads = 0;
+        sc.n_evicts = 0;
+      } else {
+        const int64_t mk = N > 0 ? sp.origin + (int64_t)a.max_finish - sp.min_arrival : 0;
+        const int64_t p95 = W > 0 ? (int64_t)a.p95 : 0;
+        const float fa = (float)mk;
+        const float fb = (float)p95;
+        const float x = sp.w_mk * fa;
+        const float y = sp.w_p95 * fb;
+        sc.makespan_us = mk;
+        sc.p95_us = p95;
+        sc.objective = x + y;
+        sc.status = a.status;
+        sc.min_headroom_mib = a.headroom;
+        sc.n_loads = (uint16_t)(a.loads > 65535u ? 65535u : a.loads);
+        sc.n_evicts = (uint16_t)(a.evicts > 65535u ? 65535u : a.evicts);
+      }
+      scores[p0 + lane] = sc;
+    }
+    lsync();
+  }
+}
+
+template <bool CHECKED, int QB>
+hipError_t launch_lean_variant(const ScoreParams& sp, const LeanParams& lp, const int8_t* dev,
+                               const uint16_t* prio, const uint8_t* flags, int64_t n_plans,
+                               wf_plan_score* scores, hipStream_t stream) {
+  auto k = score_lean<CHECKED, QB>;
+  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, lp.lds_bytes);
+  hipLaunchKernelGGL(k, dim3(lp.grid), dim3(64 * lp.waves), lp.lds_bytes, stream, sp, lp, dev, prio,
+                     flags, n_plans, scores);
+  return hipGetLastError();
+}
+
+template <bool CHECKED>
+hipError_t launch_lean_q(const ScoreParams& sp, const LeanParams& lp, const int8_t* dev,
+                         const uint16_t* prio, const uint8_t* flags, int64_t n_plans,
+                         wf_plan_score* scores, hipStream_t stream) {
+  if (lp.qbits == 32)
+    return launch_lean_variant<CHECKED, 32>(sp, lp, dev, prio, flags, n_plans, scores, stream);
+  return launch_lean_variant<CHECKED, 64>(sp, lp, dev, prio, flags, n_plans, scores, stream);
+}
+
+}  // namespace
+
+hipError_t launch_score_lean(const ScoreParams& sp, const LeanParams& lp, const int8_t* dev,
+                             const uint16_t* prio, const uint8_t* flags, int64_t n_plans,
+                             wf_plan_score* scores, hipStream_t stream) {
+  if (lp.checked)
+    return launch_lean_q<true>(sp, lp, dev, prio, flags, n_plans, scores, stream);
+  return launch_lean_q<false>(sp, lp, dev, prio, flags, n_plans, scores, stream);
+}
+
+}  // namespace wfp

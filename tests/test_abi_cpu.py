@@ -309,3 +309,7 @@ def test_noalloc_argmin_argument_errors_without_gpu():
     assert b"2^32" in lib.wf_plan_last_error(None)
     assert lib.wf_plan_argmin_noalloc(0x1000, 5, None, None) == _lib.WF_EINVAL
     assert lib.wf_plan_argmin_noalloc(None, 5, 0x1000, None) == _lib.WF_EINVAL
+
+
+def test_score_kernel_without_window():
+    assert _lib.load().wf_plan_score_kernel(None) == b""

@@ -1,0 +1,88 @@
+"""The lean scoring kernel (lean.hip) against the oracle and against the
+general kernel on the same plans: which windows it serves, and bytewise
+equal records on the workloads it serves and on random windows that stress
+its paths (tied and out-of-range priorities, invalid devices, fused chains,
+initial residency, busy devices, tight memory, saturating uint32 times)."""
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_03335_amd as pkg
+from paper_2609_03335_amd import workload as W
+
+pytestmark = pytest.mark.gpu
+THREADS = max(1, min(16, os.cpu_count() or 1))
+
+
+def log(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def score(win, plans, general=False):
+    """Records of every plan, and the kernel that scored them."""
+    old = os.environ.get("WF_PLAN_KERNEL")
+    if general:
+        os.environ["WF_PLAN_KERNEL"] = "general"
+    try:
+        with pkg.Context(0) as ctx:
+            ctx.wf_plan_upload_window(win)
+            kern = (ctx.wf_plan_score_kernel(), ctx.wf_plan_time_bits())
+            P = plans.n_plans
+            dev, prio, flags = pkg.device_plans(plans, "cuda:0")
+            s = pkg.score_batch(ctx, dev, prio, flags, P)
+            torch.cuda.synchronize()
+            return pkg.scores_to_numpy(s, P), kern
+    finally:
+        if general:
+            if old is None:
+                del os.environ["WF_PLAN_KERNEL"]
+            else:
+                os.environ["WF_PLAN_KERNEL"] = old
+
+
+@pytest.mark.parametrize("cfg,n", [(0, 512), (1, 16384), (4, 65536)])
+def test_workloads_served_by_the_lean_kernel(cfg, n):
+    win, plans = W.make_config(cfg, n_plans=n)
+    log(f"[lean] config {cfg}: {n} plans")
+    got, kern = score(win, plans)
+    assert kern[0] == "score_lean"
+    gen, kern_g = score(win, plans, general=True)
+    assert kern_g[0] == "score_plans"
+    assert got.tobytes() == gen.tobytes()
+    assert got.tobytes() == oracle.score(win, plans, threads=THREADS).tobytes()
+
+
+@pytest.mark.parametrize("cfg", [2, 3])
+def test_workloads_outside_the_lean_kernel(cfg):
+    win, _ = W.make_config(cfg, n_plans=1)
+    with pkg.Context(0) as ctx:
+        ctx.wf_plan_upload_window(win)
+        assert ctx.wf_plan_score_kernel() == "score_plans"
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_random_windows(seed):
+    rng = np.random.default_rng(9000 + seed)
+    kw = dict(n_wf=int(rng.integers(1, 7)), nodes=(1, 12), n_dev=int(rng.integers(1, 13)),
+              n_models=int(rng.integers(1, 17)), same_model_bias=0.6)
+    if seed % 4 == 1:  # tight memory: frequent reclamation and CAPACITY plans
+        kw.update(cap_range=(3000, 12000), w_range=(1000, 9000))
+    if seed % 4 == 2:  # long loads and run times: uint32 times checked, some saturate
+        kw.update(lat_range=(1, 1 << 29), load_range=(0, 1 << 30))
+    win = W.random_window(rng, **kw)
+    mode = ("any", "perm", "globalperm")[seed % 3]
+    plans = W.random_plans(win, 700, rng, p_bad_dev=0.02 if seed % 5 == 0 else 0.0,
+                           prio_mode=mode)
+    got, kern = score(win, plans)
+    ref = oracle.score(win, plans, threads=THREADS)
+    log(f"[lean] seed {seed}: N={win.n_act} D={win.n_dev} M={win.n_models} kernel={kern}")
+    if win.n_act <= 512 and win.n_models <= 16 and kern[1] == 32:
+        assert kern[0] == "score_lean"
+    assert got.tobytes() == ref.tobytes()
+    gen, _ = score(win, plans, general=True)
+    assert got.tobytes() == gen.tobytes()
