@@ -82,7 +82,7 @@ typedef enum {
 /* Limits of the library. */
 #define WF_MAX_ACT 65535    /* activations per window                     */
 #define WF_MAX_MODELS 64    /* models (resident sets are 64-bit masks)    */
-#define WF_MAX_DEV 64       /* devices in the pool                        */
+#define WF_MAX_DEV 127      /* devices in the pool (plans carry int8 device ids) */
 #define WF_MAX_MEM_MIB (1 << 28)   /* per weight / activation memory entry */
 #define WF_MAX_CAP_MIB (1 << 30)   /* per device capacity                   */
 #define WF_MAX_TIME_US (1LL << 52) /* arrivals and initial free times; every

@@ -20,7 +20,7 @@ STATUS_NAMES = {0: "WF_OK", 1: "WF_EINVAL", 2: "WF_ENOWINDOW", 3: "WF_ENOMEM", 4
                 5: "WF_EUNSUPPORTED"}
 WF_ST_INELIGIBLE = 1
 WF_ST_CAPACITY = 2
-WF_MAX_ACT, WF_MAX_MODELS, WF_MAX_DEV, WF_MAX_MUT = 65535, 64, 64, 64
+WF_MAX_ACT, WF_MAX_MODELS, WF_MAX_DEV, WF_MAX_MUT = 65535, 64, 127, 64
 WF_MAX_CLASSES = 4
 WF_VICTIM_REMAINING_LRU, WF_VICTIM_PAPER = 0, 1
 WF_MAX_BATCH = 4

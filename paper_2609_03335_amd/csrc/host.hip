@@ -293,6 +293,7 @@ int wave_layout(const HostWindow& h, int G, int tsz, int nwa, int qmode, bool se
       o.nxu = take(dm2);
       o.snap = take((size_t)G * h.D * 8);
     }
+    o.hstate = take(h.D > 64 ? 2 * 64 * sizeof(wfp::HState) : 0);
     o.split = (int)off;
   }
   o.flags = take((size_t)G * NB);
@@ -326,6 +327,7 @@ int wave_layout(const HostWindow& h, int G, int tsz, int nwa, int qmode, bool se
       o.snap = take((size_t)G * h.D * 8);
     }
   }
+  if (!global) o.hstate = take(h.D > 64 ? 2 * 64 * sizeof(wfp::HState) : 0);
   o.bytes = (int)off;
   return o.bytes;
 }
@@ -438,10 +440,10 @@ wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, bool time64_req, Im
       lw[((size_t)m * D + d) * 2 + 1] = h.wmib[m];
     }
   t.lw = img.put(lw.data(), lw.size() * 4);
-  std::vector<uint64_t> elig((size_t)std::max(N, 1), 0);
+  std::vector<uint64_t> elig((size_t)std::max(N, 1) * 2, 0);
   for (int32_t i = 0; i < N; ++i)
     for (int32_t d = 0; d < D; ++d)
-      if (h.lat[(size_t)i * D + d] >= 0) elig[i] |= uint64_t(1) << d;
+      if (h.lat[(size_t)i * D + d] >= 0) elig[(size_t)i * 2 + d / 64] |= uint64_t(1) << (d % 64);
   t.elig = img.put(elig.data(), elig.size() * 8);
   t.batch = img.put(h.batch.data(), h.batch.size() * 4);
   t.cap = img.put(h.cap.data(), h.cap.size() * 4);

@@ -34,7 +34,7 @@ struct TabOffsets {
   int res0;    // u64 [D]    initial resident-model mask
   int free0;   // time [D]   initial busy-until relative to the window origin
   int sink;    // u32 [S]    activations without successor in their workflow: index | workflow << 16
-  int elig;    // u64 [N]    devices d with lat[i][d] >= 0
+  int elig;    // u64 [N][2] devices d with lat[i][d] >= 0 (bit d % 64 of word d / 64)
   int batch;   // i32 [D]    batch limit (units a device runs at once)
   int bytes;
 };
@@ -60,12 +60,26 @@ struct WaveOffsets {
                //                  the next unit of the device with the same model
   int nxu;     // u16 [G*D][M]     paper order: next use of each model (device index)
   int snap;    // u64 [G][D]       paper order: resident models as the level starts
+  int hstate;  // HState [2][64]   more than 64 devices: the state of each lane's idle device
   int bytes;
   // per-wave regions in HBM: the arrays at offsets below `split` (acc, and
   // outside the queue modes last, stamp, nxu, snap: O(G D M) bytes) stay in
   // LDS, `split` bytes per wave; the others live in HBM, `bytes - split` per
   // wave, at their offset minus split.  0 when the whole region is in LDS.
   int split;
+};
+
+// With more than 64 devices each lane owns two; the state of the one not in
+// registers waits in LDS (times as their bit patterns).
+struct HState {
+  unsigned long long res, freet, q, ph_adm, ph_rec, ph_cf, ph_h, bdisp;
+  unsigned long long bs_free[kMaxBatch], bs_fin[kMaxBatch];
+  int32_t bs_mem[kMaxBatch], bs_model[kMaxBatch];
+  int32_t used, peak, capd;
+  uint32_t nld, nev, capbad, inel, seq;
+  int32_t nd, nq;
+  uint32_t ph_pn;
+  int32_t kdev, nbatch, pad;
 };
 
 struct ScoreParams {
@@ -76,7 +90,8 @@ struct ScoreParams {
   const unsigned char* tab;   // table image in HBM
   TabOffsets t;
   WaveOffsets wo;
-  int G;                      // plans per wave (G * D <= 64)
+  int G;                      // plans per wave (G * D <= 64; 1 when D > 64, each lane
+                              // then owning devices lane and lane + 64)
   int waves;                  // waves per workgroup
   int tab_in_lds;             // 1: the table image is staged in LDS
   int wave_global;            // 1: per-wave regions live in HBM scratch (windows too big for LDS)

@@ -146,11 +146,18 @@ __device__ __forceinline__ void mutate(uint64_t c, const SearchArgs& sa, int N,
     const int i = (int)__umulhi(x[1], (uint32_t)N);
     const uint32_t kind = x[0] >> 30;
     if (kind == 0u) {
-      unsigned long long e = elig[i];
-      const uint32_t n = (uint32_t)__popcll(e);
+      unsigned long long e = elig[2 * i], e1 = elig[2 * i + 1];
+      const uint32_t n0 = (uint32_t)__popcll(e), n = n0 + (uint32_t)__popcll(e1);
       if (n) {
-        for (uint32_t k = __umulhi(x[2], n); k; --k) e &= e - 1ull;
-        rd[i] = (int8_t)__builtin_ctzll(e);
+        uint32_t k = __umulhi(x[2], n);
+        int base = 0;
+        if (k >= n0) {
+          k -= n0;
+          e = e1;
+          base = 64;
+        }
+        for (; k; --k) e &= e - 1ull;
+        rd[i] = (int8_t)(base + __builtin_ctzll(e));
       }
     } else if (kind == 1u) {
       const uint32_t lvw = alv[i];
@@ -165,8 +172,8 @@ __device__ __forceinline__ void mutate(uint64_t c, const SearchArgs& sa, int N,
 }
 
 // slot entry: activation | model << 16 | prefetch << 22 | has fused successor << 23 |
-// device << 24 | last unit of its model on the device << 30 | finish written by
-// the general path (a fused chain, or schedule output requested) << 31
+// last unit of its model on the device << 30 | finish written by the general
+// path (a fused chain, or schedule output requested) << 31
 constexpr uint32_t kPf = 1u << 22;
 constexpr uint32_t kChain = 1u << 23;
 constexpr uint32_t kLast = 1u << 30;
@@ -305,6 +312,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   uint16_t* s_nx = reinterpret_cast<uint16_t*>(big(sp.wo.nx));      // paper order only
   uint16_t* s_nxu = reinterpret_cast<uint16_t*>(small(sp.wo.nxu));
   unsigned long long* s_snap = reinterpret_cast<unsigned long long*>(small(sp.wo.snap));
+  HState* s_hst = reinterpret_cast<HState*>(small(sp.wo.hstate));  // more than 64 devices only
   TB* s_wfm = reinterpret_cast<TB*>(big(sp.wo.wfm));
   int8_t* s_rdev = reinterpret_cast<int8_t*>(big(sp.wo.rows));         // generated candidates
   uint16_t* s_rprio = reinterpret_cast<uint16_t*>(big(sp.wo.rows_prio));
@@ -319,7 +327,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   const int d_me = lane - g_me * D;
   const int64_t n_groups = (P + G - 1) / G;
   const int64_t stride = (int64_t)gridDim.x * sp.waves;
-  // per-device table rows of this lane's device
+  // per-device table rows of this lane's device (bound per device below)
   const uint4* ud_d = t_ud + d_me;
   const int2* lw_d = t_lw + d_me;
 
@@ -417,7 +425,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
       if (head && okd && inr) {
         const uint32_t m = a & 63u;
         s_rec[g * N + pr] = (uint32_t)u | (m << 16) | ((fb & 2u) << 21) |
-                            (chain ? kChain | kSlow : slow0) | ((uint32_t)d << 24);
+                            (chain ? kChain | kSlow : slow0);
         atomicOr(&s_mask[(g * D + d) * NWA + (pr >> 6)], 1ull << (pr & 63));
         if constexpr (!PAPER) atomicMax(&s_last[(g * D + d) * M + (int)m], (uint32_t)pr + 1u);
         ++nh;
@@ -570,7 +578,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
         const int c = t_cnext[u];
         const uint32_t chain = (c != 0xffff && fuse_bit(pfl, c)) ? kChain : 0u;
         rec[slot] = (uint32_t)u | ((a & 63u) << 16) | ((uint32_t)((fb >> 1) & 1) << 22) | chain |
-                    (chain ? kSlow : slow0) | ((uint32_t)d << 24);
+                    (chain ? kSlow : slow0);
         atomicOr(&mk[d * NWA + (slot >> 6)], 1ull << (slot & 63));
         if constexpr (!PAPER) atomicMax(&lastp[d * M + (int)(a & 63u)], (uint32_t)slot + 1u);
       }
@@ -639,12 +647,16 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
         uint32_t* rec = s_rec + g * N;
         const unsigned long long* mk = s_mask + g * D * NWA;
         const uint32_t* lastp = s_last + g * D * M;
+        const int8_t* pdev = row_dev(g);
         for (int sl = lane; sl < N; sl += 64) {
           const uint32_t e = rec[sl];
-          const int d = (int)((e >> 24) & 63u);
+          // entries of empty slots are stale: the activation, its device and
+          // the model may be anything; only an occupied slot counts
+          const int u = (int)(e & 0xffffu);
+          const int d = u < N ? (int)pdev[u] : -1;
           const int m = (int)((e >> 16) & 63u);
-          // entries of empty slots are stale: d, m may be anything below 64
-          const bool occ = d < D && m < M && ((mk[d * NWA + (sl >> 6)] >> (sl & 63)) & 1ull);
+          const bool occ = (unsigned)d < (unsigned)D && m < M &&
+                           ((mk[d * NWA + (sl >> 6)] >> (sl & 63)) & 1ull);
           if (occ && lastp[d * M + m] == (uint32_t)sl + 1u) rec[sl] = e | kLast;
         }
       }
@@ -654,9 +666,17 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
     if (pre && grp + stride < n_groups) load_rows(grp + stride, dvp, pvp);
 
     // ---- device-lane state ----
-    const bool act = g_me < gc;
-    const int gme = act ? g_me : 0;
+    // With more than 64 devices (one plan per wave) a lane owns two devices,
+    // d_me and d_me + 64: their states take turns in registers, the other
+    // one waiting in the wave's LDS region, and each level walks the first
+    // device's units, then the second's (devices are independent within a
+    // level).
+    const int NH = D > 64 ? 2 : 1;
+    const bool act_plan = g_me < gc;
+    const int gme = act_plan ? g_me : 0;
     const int64_t pw = p0 + gme;
+    bool act = act_plan;
+    int d = d_me;
     const uint32_t* mylast = s_last + (gme * D + d_me) * M;
     uint16_t* mystamp = s_stamp + (gme * D + d_me) * M;
     uint16_t* mynxu = s_nxu + (gme * D + d_me) * M;  // next use of each model (device index)
@@ -664,7 +684,19 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
     const uint32_t* myrec = s_rec + gme * N;
     TB* myfin = s_fin + gme * N;
     const uint8_t* myfl = s_fl + gme * NB;
-    const int d = d_me;
+    // the lane's h-th device (h = 0, 1) and its table rows; a lane without
+    // a second device keeps in-range pointers and stays inactive
+    auto bind = [&](int h) {
+      d = d_me + 64 * h;
+      act = act_plan && d < D;
+      const int dd = d < D ? d : d_me;
+      mylast = s_last + (gme * D + dd) * M;
+      mystamp = s_stamp + (gme * D + dd) * M;
+      mynxu = s_nxu + (gme * D + dd) * M;
+      mymask = s_mask + (gme * D + dd) * NWA;
+      ud_d = t_ud + dd;
+      lw_d = t_lw + dd;
+    };
     uint64_t res = 0;
     int32_t used = 0, peak = 0, capd = 0;
     TT freet = 0;
@@ -693,6 +725,92 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
     int nbatch = 1;
     TT bs_free[kMaxBatch], bs_fin[kMaxBatch], bdisp = 0;
     int32_t bs_mem[kMaxBatch], bs_model[kMaxBatch];
+    // the idle device's state in LDS, and back
+    using HT2 = HT;
+    auto save = [&](int h) {
+      HState& x = s_hst[h * 64 + lane];
+      x.res = res;
+      x.freet = (unsigned long long)TO::bits(freet);
+      x.q = (unsigned long long)Q;
+      x.ph_adm = ph_adm;
+      x.ph_rec = ph_rec;
+      x.ph_cf = (unsigned long long)TO::bits(ph_cf);
+      if constexpr (std::is_same<HT2, double>::value)
+        x.ph_h = (unsigned long long)__double_as_longlong(ph_h);
+      else
+        x.ph_h = (unsigned long long)ph_h;
+      x.bdisp = (unsigned long long)TO::bits(bdisp);
+#pragma unroll
+      for (int k = 0; k < kMaxBatch; ++k) {
+        x.bs_free[k] = (unsigned long long)TO::bits(bs_free[k]);
+        x.bs_fin[k] = (unsigned long long)TO::bits(bs_fin[k]);
+        x.bs_mem[k] = bs_mem[k];
+        x.bs_model[k] = bs_model[k];
+      }
+      x.used = used;
+      x.peak = peak;
+      x.capd = capd;
+      x.nld = nld;
+      x.nev = nev;
+      x.capbad = capbad;
+      x.inel = inel;
+      x.seq = seq;
+      x.nd = nd;
+      x.nq = nq;
+      x.ph_pn = ph_pn;
+      x.kdev = kdev;
+      x.nbatch = nbatch;
+    };
+    auto load = [&](int h) {
+      const HState& x = s_hst[h * 64 + lane];
+      res = x.res;
+      freet = TO::load(reinterpret_cast<const TB*>(&x.freet));
+      Q = (QT)x.q;
+      ph_adm = x.ph_adm;
+      ph_rec = x.ph_rec;
+      ph_cf = TO::load(reinterpret_cast<const TB*>(&x.ph_cf));
+      if constexpr (std::is_same<HT2, double>::value)
+        ph_h = __longlong_as_double((long long)x.ph_h);
+      else
+        ph_h = (HT2)x.ph_h;
+      bdisp = TO::load(reinterpret_cast<const TB*>(&x.bdisp));
+#pragma unroll
+      for (int k = 0; k < kMaxBatch; ++k) {
+        bs_free[k] = TO::load(reinterpret_cast<const TB*>(&x.bs_free[k]));
+        bs_fin[k] = TO::load(reinterpret_cast<const TB*>(&x.bs_fin[k]));
+        bs_mem[k] = x.bs_mem[k];
+        bs_model[k] = x.bs_model[k];
+      }
+      used = x.used;
+      peak = x.peak;
+      capd = x.capd;
+      nld = x.nld;
+      nev = x.nev;
+      capbad = x.capbad;
+      inel = x.inel;
+      seq = x.seq;
+      nd = x.nd;
+      nq = x.nq;
+      ph_pn = x.ph_pn;
+      kdev = x.kdev;
+      nbatch = x.nbatch;
+    };
+    for (int h = 0; h < NH; ++h) {
+    if (NH > 1) bind(h);
+    res = 0;
+    used = peak = capd = 0;
+    freet = 0;
+    nld = nev = capbad = inel = 0u;
+    seq = 1;
+    Q = 0;
+    nd = nq = 0;
+    ph_adm = ph_rec = 0ull;
+    ph_cf = 0;
+    ph_h = 0;
+    ph_pn = 0u;
+    kdev = 0;
+    nbatch = 1;
+    bdisp = 0;
 #pragma unroll
     for (int k = 0; k < kMaxBatch; ++k) {
       bs_free[k] = 0;
@@ -756,6 +874,8 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
       }
       peak = used;
     }
+    if (NH > 1) save(h);
+    }
     if constexpr (NIBBLE) wave_sync();  // last[] (aliasing fin) is read above
     // every finish starts at 0: it accumulates the latest predecessor finish
     // before its level, then holds the activation's own finish
@@ -790,15 +910,28 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
 
       // ---- paper order: the pool's residency as the level starts ----
       if constexpr (PAPER) {
-        if (act) s_snap[gme * D + d_me] = res;
+        for (int h = 0; h < NH; ++h) {
+          if (NH > 1) {
+            bind(h);
+            res = s_hst[h * 64 + lane].res;
+          }
+          if (act) s_snap[gme * D + d] = res;
+        }
         wave_sync();
-        others = 0ull;
-        if (act)
-          for (int e = 0; e < D; ++e)
-            if (e != d_me) others |= s_snap[gme * D + e];
       }
 
       // ---- device lanes walk their units of this level in slot order ----
+      for (int h = 0; h < NH; ++h) {
+      if (NH > 1) {
+        bind(h);
+        load(h);
+      }
+      if constexpr (PAPER) {
+        others = 0ull;
+        if (act)
+          for (int e = 0; e < D; ++e)
+            if (e != d) others |= s_snap[gme * D + e];
+      }
       if (act) {
         const int j1 = (hi - 1) >> 6;
         const unsigned long long hmask = (hi & 63) ? ((1ull << (hi & 63)) - 1ull) : ~0ull;
@@ -1159,10 +1292,17 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
         else
           run(next_wide);
       }
+      if (NH > 1) save(h);
+      }
       wave_sync();
     }
 
     // ---- per-plan reductions (Sec. 4 metrics) ----
+    for (int h = 0; h < NH; ++h) {
+    if (NH > 1) {
+      bind(h);
+      load(h);
+    }
     if (act) {
       atomicMin(&s_acc[gme].headroom, capd - peak);
       atomicAdd(&s_acc[gme].loads, nld);
@@ -1178,7 +1318,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
         if (last == 0xffffffffu) atomicOr(&s_acc[gme].status, kRescore);
       }
       if (inel) atomicOr(&s_acc[gme].status, (uint32_t)WF_ST_INELIGIBLE);
-      if (has_sched) sched.peak_mib[pw * D + d_me] = peak;
+      if (has_sched) sched.peak_mib[pw * D + d] = peak;
       if constexpr (PHI) {
         if (ph_adm) {
           atomicAdd(&s_acc[gme].ph_adm, ph_adm);
@@ -1188,6 +1328,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
         // exact: an integer below 2^53 with fp64 times
         if (ph_h) atomicAdd(&s_acc[gme].ph_h, (unsigned long long)ph_h);
       }
+    }
     }
     // a workflow's completion is the latest finish among its activations
     // without a successor in the same workflow (not part of the ranking key)

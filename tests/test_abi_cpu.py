@@ -112,7 +112,7 @@ def _mutate(fn):
 BAD = {
     "n_models_zero": lambda w: setattr(w, "n_models", 0),
     "n_models_65": lambda w: setattr(w, "n_models", 65),
-    "n_dev_65": lambda w: setattr(w, "n_dev", 65),
+    "n_dev_128": lambda w: setattr(w, "n_dev", 128),
     "n_wf_zero": lambda w: setattr(w, "n_wf", 0),
     "pred_self_loop": lambda w: w.pred_idx.__setitem__(0, int(np.nonzero(np.diff(w.pred_off))[0][0])),
     "pred_off_nonzero_start": lambda w: w.pred_off.__setitem__(0, 1),
@@ -313,3 +313,11 @@ def test_noalloc_argmin_argument_errors_without_gpu():
 
 def test_score_kernel_without_window():
     assert _lib.load().wf_plan_score_kernel(None) == b""
+
+
+@pytest.mark.parametrize("D", [65, 96, 127])
+def test_pools_up_to_127_devices_validate(D):
+    """Plans carry int8 device ids: pools of up to 127 devices are valid."""
+    rng = np.random.default_rng(D)
+    st, msg = pkg.wf_plan_validate_window(W.random_window(rng, n_dev=D, n_models=20))
+    assert st == pkg.WF_OK, msg
