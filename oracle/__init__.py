@@ -21,6 +21,7 @@ SRC_PATH = os.path.join(_HERE, "oracle.c")
 
 INELIGIBLE = 1
 CAPACITY = 2
+REPLICA = 4
 VICTIM_REMAINING_LRU = 0
 VICTIM_PAPER = 1
 MAX_BATCH = 4
@@ -64,6 +65,7 @@ class _Win(ctypes.Structure):
         ("w_makespan", ctypes.c_float), ("w_p95", ctypes.c_float),
         ("victim_order", ctypes.c_int32),
         ("dev_batch", ctypes.c_void_p),
+        ("replica_cap", ctypes.c_void_p),
     ]
 
 
@@ -120,6 +122,8 @@ class _WinHolder:
             "dev_free0_us": None if win.dev_free0_us is None else _c(win.dev_free0_us, np.int64),
             "dev_batch": (None if getattr(win, "dev_batch", None) is None
                           else _c(win.dev_batch, np.int32)),
+            "replica_cap": (None if getattr(win, "model_replica_cap", None) is None
+                            else _c(win.model_replica_cap, np.int32)),
         }
         if self.keep["pred_idx"].size == 0:
             self.keep["pred_idx"] = np.zeros(1, dtype=np.int32)

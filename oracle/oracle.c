@@ -147,6 +147,18 @@ static int paper_victim_before(int redx, int64_t distx, int64_t loadx, int64_t l
 
 /* The propagation of every plan; scores, the schedule rows and the ranking
  * keys (Eq. 12) are each written when their pointer is not NULL. */
+/* Replica cap of one level: whether some model is held, as the level starts
+ * (held) or by a load during it (loaded), on more devices than its cap. */
+static int replica_over(const orc_window *w, const uint64_t *held, const uint64_t *loaded) {
+  if (!w->replica_cap) return 0;
+  for (int32_t m = 0; m < w->n_models; ++m) {
+    int32_t copies = 0;
+    for (int32_t d = 0; d < w->n_dev; ++d) copies += (int32_t)(((held[d] | loaded[d]) >> m) & 1u);
+    if (copies > w->replica_cap[m]) return 1;
+  }
+  return 0;
+}
+
 static int simulate(const orc_window *w, const uint8_t *wf_class, const int8_t *dev,
                     const uint16_t *prio, const uint8_t *flags, int64_t n_plans,
                     orc_score *scores, int64_t *start_out, int64_t *finish_out,
@@ -161,6 +173,14 @@ static int simulate(const orc_window *w, const uint8_t *wf_class, const int8_t *
   if (w->dev_batch)
     for (int32_t d = 0; d < w->n_dev; ++d)
       if (w->dev_batch[d] < 1 || w->dev_batch[d] > ORC_MAX_BATCH) return ORC_ERR_BATCH;
+  if (w->replica_cap && w->n_models >= 1 && w->n_models <= 64) {
+    for (int32_t m = 0; m < w->n_models; ++m) {
+      if (w->replica_cap[m] < 1) return ORC_ERR_REPLICA;
+      int32_t copies = 0;
+      for (int32_t d = 0; d < w->n_dev; ++d) copies += (int32_t)((w->init_resident[d] >> m) & 1u);
+      if (copies > w->replica_cap[m]) return ORC_ERR_REPLICA;
+    }
+  }
   orc_struct st;
   int rc = build_struct(w, &st);
   if (rc) return rc;
@@ -184,13 +204,14 @@ static int simulate(const orc_window *w, const uint8_t *wf_class, const int8_t *
   uint64_t *res = (uint64_t *)malloc((size_t)D * 8);
   uint64_t *reclaimed = (uint64_t *)malloc((size_t)D * 8);
   uint64_t *res_level = (uint64_t *)malloc((size_t)D * 8);
+  uint64_t *loaded_level = (uint64_t *)malloc((size_t)D * 8);
   int64_t *dev_units = (int64_t *)malloc((size_t)D * 8);
   int64_t *next_after = (int64_t *)malloc(n * 8), *dev_index = (int64_t *)malloc(n * 8);
   int64_t *next_use = (int64_t *)malloc((size_t)D * M * 8);
   int64_t *remaining = (int64_t *)malloc((size_t)D * M * 8), *last = (int64_t *)malloc((size_t)D * M * 8);
   if (!fuse || !pf || !member || !unit_Mx || !order || !start || !finish ||
       !load_start || !comp || !slot_free || !run_fin || !run_mem || !run_model || !dispatched || !used || !peak || !res || !reclaimed || !remaining ||
-      !last || !res_level || !dev_units || !next_after || !dev_index || !next_use) {
+      !last || !res_level || !loaded_level || !dev_units || !next_after || !dev_index || !next_use) {
     rc = ORC_ERR_NOMEM;
     goto done;
   }
@@ -295,9 +316,15 @@ static int simulate(const orc_window *w, const uint8_t *wf_class, const int8_t *
       int32_t wf = w->act_wf[h];
       int64_t Mx = unit_Mx[h];
       remaining[d * M + m] -= 1;
-      /* pool residency as the unit's topological level starts */
-      if (pos == 0 || order[pos].level != order[pos - 1].level)
-        for (int32_t e = 0; e < D; ++e) res_level[e] = res[e];
+      /* pool residency as the unit's topological level starts; the replica
+       * cap of the level that ends */
+      if (pos == 0 || order[pos].level != order[pos - 1].level) {
+        if (pos > 0 && replica_over(w, res_level, loaded_level)) sc.status |= ORC_REPLICA;
+        for (int32_t e = 0; e < D; ++e) {
+          res_level[e] = res[e];
+          loaded_level[e] = 0;
+        }
+      }
 
       /* predicted release (Eq. 2): workflow arrival, or the latest
        * predecessor completion */
@@ -392,6 +419,7 @@ static int simulate(const orc_window *w, const uint8_t *wf_class, const int8_t *
         int64_t ls = t;
         int64_t le = ls + w->load_us[m * D + d];
         res[d] |= 1ull << m;
+        loaded_level[d] |= 1ull << m;
         used[d] += w->model_mib[m];
         n_loads += 1;
         load_start[h] = ls;
@@ -431,6 +459,9 @@ static int simulate(const orc_window *w, const uint8_t *wf_class, const int8_t *
         c_ready = max64(c_ready, s);
       }
     }
+
+    /* the replica cap of the last level */
+    if (n_units > 0 && replica_over(w, res_level, loaded_level)) sc.status |= ORC_REPLICA;
 
     /* ---- reductions (Sec. 4 metrics) ---- */
     if (N > 0) {
@@ -485,7 +516,7 @@ done:
   free(start); free(finish); free(load_start); free(comp); free(slot_free); free(run_fin);
   free(run_mem); free(run_model); free(dispatched); free(used);
   free(peak); free(res); free(reclaimed); free(remaining); free(last);
-  free(res_level); free(dev_units); free(next_after); free(dev_index); free(next_use);
+  free(res_level); free(loaded_level); free(dev_units); free(next_after); free(dev_index); free(next_use);
   free_struct(&st);
   return rc;
 }

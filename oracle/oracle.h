@@ -50,7 +50,18 @@ typedef struct {
   float w_makespan, w_p95;
   int32_t victim_order;         /* ORC_VICTIM_REMAINING_LRU or ORC_VICTIM_PAPER */
   const int32_t *dev_batch;     /* [n_dev] batch limit 1..ORC_MAX_BATCH, NULL = all 1 */
+  const int32_t *replica_cap;   /* [n_models] replica cap >= 1, NULL = no cap (below) */
 } orc_window;
+
+/*
+ * Replica cap (Sec. 3.5: scale-out, a new replica of a deployment on another
+ * device, is subject to the replica cap).  With replica_cap set, a plan is
+ * flagged ORC_REPLICA when, for some model m and some topological level L,
+ * the devices that hold a copy of m as the units of L start (in resource
+ * order) or load one for a unit of L outnumber replica_cap[m].  The flag is
+ * a check only: no time, memory or count of the plan changes.  The initial
+ * residency must respect the caps (ORC_ERR_REPLICA otherwise).
+ */
 
 /*
  * Batch limit (Eq. 11 and the replica batch limit B_q after it; Sec. 4,
@@ -93,12 +104,12 @@ typedef struct {
   int64_t makespan_us;
   int64_t p95_us;
   float objective;
-  uint32_t status;            /* ORC_INELIGIBLE | ORC_CAPACITY, 0 = feasible */
+  uint32_t status;            /* ORC_INELIGIBLE | ORC_CAPACITY | ORC_REPLICA, 0 = feasible */
   int32_t min_headroom_mib;
   uint16_t n_loads, n_evicts; /* saturate at 65535                            */
 } orc_score;
 
-enum { ORC_INELIGIBLE = 1u, ORC_CAPACITY = 2u };
+enum { ORC_INELIGIBLE = 1u, ORC_CAPACITY = 2u, ORC_REPLICA = 4u };
 
 /* Error codes of orc_score_plans. */
 enum {
@@ -111,7 +122,8 @@ enum {
   ORC_ERR_NOMEM = 6,
   ORC_ERR_CLASS = 7,      /* a workflow class outside 0 .. ORC_MAX_CLASSES-1    */
   ORC_ERR_VICTIM = 8,     /* victim_order is not one of ORC_VICTIM_*           */
-  ORC_ERR_BATCH = 9       /* a batch limit outside 1 .. ORC_MAX_BATCH          */
+  ORC_ERR_BATCH = 9,      /* a batch limit outside 1 .. ORC_MAX_BATCH          */
+  ORC_ERR_REPLICA = 10    /* a replica cap below 1, or initial copies above it */
 };
 
 /*

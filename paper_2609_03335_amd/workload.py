@@ -71,6 +71,9 @@ class Window:
     # int32[D] batch limit of each device (units it runs at once, 1..4);
     # None = 1 everywhere
     dev_batch: Optional[np.ndarray] = None
+    # int32[M] replica cap of each model (copies held across the pool in one
+    # topological level, Sec. 3.5 scale-out), >= 1; None = no cap
+    model_replica_cap: Optional[np.ndarray] = None
 
     def arrays(self):
         return {f.name: getattr(self, f.name) for f in dataclasses.fields(self)}

@@ -45,6 +45,8 @@ def load_golden(name):
     batch = [d.get("batch", 1) for d in spec["devices"]]
     if any(b != 1 for b in batch):
         win.dev_batch = np.array(batch, np.int32)
+    if any("replica_cap" in m for m in spec["models"]):
+        win.model_replica_cap = np.array([m.get("replica_cap", D) for m in spec["models"]], np.int32)
     for dname, mnames in spec.get("init_resident", {}).items():
         bits = 0
         for mn in mnames:

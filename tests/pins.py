@@ -295,3 +295,51 @@ def compare_plan(win, plans, p, oracle_scores, oracle_sched) -> List[str]:
             if not np.array_equal(np.asarray(a, np.int64), np.asarray(b, np.int64)):
                 errs.append(f"plan {p}: {name} differs")
     return errs
+
+
+def replica_over(win, units) -> bool:
+    """Second formulation of the replica cap: replay every device's units in
+    order to obtain, per device and topological level, the resident set as
+    the level starts and the models the device loads during the level; a
+    model held that way on more devices than its cap puts the plan over."""
+    if getattr(win, "model_replica_cap", None) is None or not units:
+        return False
+    M, D = win.n_models, win.n_dev
+    W = np.asarray(win.model_mib, dtype=np.int64)
+    cap = np.asarray(win.dev_cap_mib, dtype=np.int64)
+    mem = np.asarray(win.mem_mib, dtype=np.int64).reshape(win.n_act, D)
+    rcap = np.asarray(win.model_replica_cap, dtype=np.int64)
+    levels = sorted({u.key[0] for u in units})
+    # holders[L][m] = set of devices
+    holders = {L: [set() for _ in range(M)] for L in levels}
+    seqs: Dict[int, List[Unit]] = {}
+    for u in units:
+        seqs.setdefault(u.device, []).append(u)
+    for d in range(D):
+        seq = seqs.get(d, [])
+        resident = {m for m in range(M) if (int(win.init_resident[d]) >> m) & 1}
+        last_use = {m: -1 for m in range(M)}
+        k = 0
+        for L in levels:
+            for m in resident:
+                holders[L][m].add(d)
+            while k < len(seq) and seq[k].key[0] == L:
+                u = seq[k]
+                mx = max(int(mem[v, d]) for v in u.chain)
+                used = sum(int(W[m]) for m in resident)
+                miss = u.model not in resident
+                need = (int(W[u.model]) if miss else 0) + mx
+                while used + need > cap[d]:
+                    cands = [m for m in resident if m != u.model]
+                    if not cands:
+                        break
+                    later = {s.model for s in seq[k + 1:]}
+                    victim = min(cands, key=lambda m: (m in later, last_use[m], m))
+                    resident.discard(victim)
+                    used -= int(W[victim])
+                if miss:
+                    resident.add(u.model)
+                    holders[L][u.model].add(d)
+                last_use[u.model] = k
+                k += 1
+    return any(len(holders[L][m]) > rcap[m] for L in levels for m in range(M))

@@ -19,9 +19,18 @@ import test_oracle_phi as t_phi
 import test_oracle_victim as t_vic
 import test_oracle_batch as t_batch
 import test_oracle_prefix as t_prefix
+import test_oracle_replica as t_rep
 
 # (name, original fragment, planted mistake)
 MUTANTS = [
+    # replica cap
+    ("replica cap inclusive", "if (copies > w->replica_cap[m]) return 1;", "if (copies >= w->replica_cap[m]) return 1;"),
+    ("replica cap counts only loads", "(((held[d] | loaded[d]) >> m) & 1u)", "((loaded[d] >> m) & 1u)"),
+    ("replica cap counts only holders", "(((held[d] | loaded[d]) >> m) & 1u)", "((held[d] >> m) & 1u)"),
+    ("replica cap skips the last level",
+     "if (n_units > 0 && replica_over(w, res_level, loaded_level)) sc.status |= ORC_REPLICA;", ""),
+    ("replica loads accumulate across levels", "          loaded_level[e] = 0;\n", ""),
+    ("replica flag clears other bits", "sc.status |= ORC_REPLICA;\n        for", "sc.status = ORC_REPLICA;\n        for"),
     # candidate generator
     ("philox multiplier swapped", "(uint64_t)0xD2511F53u * x0", "(uint64_t)0xCD9E8D57u * x0"),
     ("philox key not bumped", "k1 += 0xBB67AE85u;", ""),
@@ -152,6 +161,8 @@ def _pin_checks():
     checks += [lambda n=n: t_batch.test_worked_examples(n) for n in ("batch_memory", "batch_lease")]
     checks += [lambda s=s: t_batch.test_contention_free_longest_path(s) for s in (0, 1, 2, 3, 5, 6)]
     checks += [lambda s=s: t_batch.test_schedule_invariants(s) for s in range(8)]
+    checks += [t_rep.test_worked_example, t_rep.test_both_outcomes_occur]
+    checks += [lambda s=s: t_rep.test_cap_is_a_check_only(s) for s in range(3)]
     checks += [t_prefix.test_worked_example]
     checks += [lambda s=s: t_prefix.test_single_device_chain(s) for s in range(4)]
     checks += [lambda s=s: t_prefix.test_invariants(s) for s in range(4)]
