@@ -139,6 +139,8 @@ def main():
                     help="skip the prefix-commit leg (Algorithm 1's last step, one plan)")
     ap.add_argument("--batch-limit", type=int, default=4,
                     help="units per device at once in the batch-limit leg (1 = skip it)")
+    ap.add_argument("--replica-cap", type=int, default=6,
+                    help="copies per model in the replica-cap leg (0 = skip it)")
     ap.add_argument("--copy-probe", type=int, default=None, metavar="BYTES",
                     help="only run a plain copy kernel of BYTES bytes (counter calibration)")
     args = ap.parse_args()
@@ -399,6 +401,17 @@ def main():
                      "note": "the same plans with up to batch_limit units per device at once "
                              "(slots, memory of running units, leases on their models)"}
 
+    # the same plans with a replica cap on every model (Sec. 3.5 scale-out):
+    # the window moves to the scanned-residency kernel with a per-level check
+    replica_leg = None
+    if args.replica_cap > 0:
+        rc = np.full(win.n_models, args.replica_cap, np.int32)
+        r_ms = window_leg(dataclasses.replace(win, model_replica_cap=rc), "replica caps")
+        replica_leg = {"value": round(P / (r_ms * 1e-3), 1), "unit": "plans/s",
+                       "kernel_ms": round(r_ms, 4), "replica_cap": args.replica_cap,
+                       "note": "the same plans with every model capped at replica_cap copies "
+                               "held per topological level (status bit 4 beyond it)"}
+
     cpu = None
     if not args.no_cpu_baseline:
         import oracle
@@ -452,6 +465,7 @@ def main():
         "keys": keys_leg,
         "paper_order": paper_leg,
         "batch_limit": batch_leg,
+        "replica_cap": replica_leg,
         "prefix": prefix_leg,
     }
     print(json.dumps(line))

@@ -92,7 +92,7 @@ typedef enum {
 #define WF_MAX_BATCH 4             /* batch limit of a device                  */
 
 /* Plan status bits; a plan is feasible iff status == 0. */
-enum { WF_ST_INELIGIBLE = 1u, WF_ST_CAPACITY = 2u };
+enum { WF_ST_INELIGIBLE = 1u, WF_ST_CAPACITY = 2u, WF_ST_REPLICA = 4u };
 
 typedef struct wf_plan_ctx wf_plan_ctx; /* opaque; owns the device copy of a window */
 
@@ -127,7 +127,19 @@ typedef struct {
                                      WF_VICTIM_PAPER (1, below)                 */
   const int32_t *dev_batch;       /* [D] batch limit 1..WF_MAX_BATCH (below), or NULL
                                      for 1 everywhere                           */
+  const int32_t *model_replica_cap; /* [M] replica cap of each model >= 1 (below), or
+                                     NULL for none; the initial residency must
+                                     hold at most cap[m] copies of model m      */
 } wf_window_desc;
+
+/*
+ * Replica cap (Sec. 3.5: scale-out -- a new replica of a deployment on
+ * another device -- is subject to the replica cap).  A plan is flagged
+ * WF_ST_REPLICA when, for some model m and some topological level L, the
+ * devices that hold a copy of m as the units of L start (in resource order)
+ * or load one for a unit of L outnumber model_replica_cap[m].  The flag is a
+ * check only: no time, memory or count of the plan changes.
+ */
 
 /*
  * Batch limits (Eq. 11 and the replica batch limit B_q after it; Sec. 4,

@@ -20,6 +20,7 @@ STATUS_NAMES = {0: "WF_OK", 1: "WF_EINVAL", 2: "WF_ENOWINDOW", 3: "WF_ENOMEM", 4
                 5: "WF_EUNSUPPORTED"}
 WF_ST_INELIGIBLE = 1
 WF_ST_CAPACITY = 2
+WF_ST_REPLICA = 4
 WF_MAX_ACT, WF_MAX_MODELS, WF_MAX_DEV, WF_MAX_MUT = 65535, 64, 127, 64
 WF_MAX_CLASSES = 4
 WF_VICTIM_REMAINING_LRU, WF_VICTIM_PAPER = 0, 1
@@ -68,6 +69,7 @@ class wf_window_desc(ctypes.Structure):
         ("wf_class", ctypes.c_void_p),
         ("victim_order", ctypes.c_int32),
         ("dev_batch", ctypes.c_void_p),
+        ("model_replica_cap", ctypes.c_void_p),
     ]
 
 
@@ -156,6 +158,8 @@ class _Desc:
         self.keep["wf_class"] = None if cls is None else c(cls, np.uint8)
         bat = getattr(win, "dev_batch", None)
         self.keep["dev_batch"] = None if bat is None else c(bat, np.int32)
+        rc = getattr(win, "model_replica_cap", None)
+        self.keep["model_replica_cap"] = None if rc is None else c(rc, np.int32)
         d = wf_window_desc()
         d.n_act, d.n_wf, d.n_models, d.n_dev = win.n_act, win.n_wf, win.n_models, win.n_dev
         for k, v in self.keep.items():

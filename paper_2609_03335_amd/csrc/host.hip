@@ -32,6 +32,7 @@ struct HostWindow {
   std::vector<uint8_t> wf_class;  // [W] priority class of the ranking key
   int32_t victim_order = WF_VICTIM_REMAINING_LRU;
   std::vector<int32_t> batch;  // [D] batch limit
+  std::vector<int32_t> rcap;   // [M] replica cap, empty = none
   float w_mk = 1.f, w_p95 = 0.f;
 };
 
@@ -138,12 +139,24 @@ wf_status validate(const wf_window_desc* w, std::string* err, HostWindow* out) {
       if (w->dev_batch[d] < 1 || w->dev_batch[d] > WF_MAX_BATCH)
         return fail(err, WF_EINVAL, "dev_batch[%lld] = %d outside [1, %d]", (long long)d,
                     (int)w->dev_batch[d], WF_MAX_BATCH);
+  if (w->model_replica_cap)
+    for (int64_t m = 0; m < M; ++m) {
+      if (w->model_replica_cap[m] < 1)
+        return fail(err, WF_EINVAL, "model_replica_cap[%lld] = %d is below 1", (long long)m,
+                    (int)w->model_replica_cap[m]);
+      int64_t copies = 0;
+      for (int64_t d = 0; d < D; ++d) copies += (int64_t)((w->init_resident[d] >> m) & 1ull);
+      if (copies > w->model_replica_cap[m])
+        return fail(err, WF_EINVAL, "initial residency holds %lld copies of model %lld, above its replica cap %d",
+                    (long long)copies, (long long)m, (int)w->model_replica_cap[m]);
+    }
   if (!out) return WF_OK;
 
   HostWindow& h = *out;
   h.victim_order = w->victim_order;
   h.batch.assign((size_t)D, 1);
   if (w->dev_batch) h.batch.assign(w->dev_batch, w->dev_batch + D);
+  if (w->model_replica_cap) h.rcap.assign(w->model_replica_cap, w->model_replica_cap + M);
   h.wf_class.assign((size_t)W, 0);
   if (w->wf_class) h.wf_class.assign(w->wf_class, w->wf_class + W);
   h.N = (int32_t)N;
@@ -294,6 +307,7 @@ int wave_layout(const HostWindow& h, int G, int tsz, int nwa, int qmode, bool se
       o.snap = take((size_t)G * h.D * 8);
     }
     o.hstate = take(h.D > 64 ? 2 * 64 * sizeof(wfp::HState) : 0);
+    o.hold = take(h.rcap.empty() ? 0 : (size_t)G * h.D * 8);
     o.split = (int)off;
   }
   o.flags = take((size_t)G * NB);
@@ -327,7 +341,10 @@ int wave_layout(const HostWindow& h, int G, int tsz, int nwa, int qmode, bool se
       o.snap = take((size_t)G * h.D * 8);
     }
   }
-  if (!global) o.hstate = take(h.D > 64 ? 2 * 64 * sizeof(wfp::HState) : 0);
+  if (!global) {
+    o.hstate = take(h.D > 64 ? 2 * 64 * sizeof(wfp::HState) : 0);
+    o.hold = take(h.rcap.empty() ? 0 : (size_t)G * h.D * 8);
+  }
   o.bytes = (int)off;
   return o.bytes;
 }
@@ -446,6 +463,7 @@ wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, bool time64_req, Im
       if (h.lat[(size_t)i * D + d] >= 0) elig[(size_t)i * 2 + d / 64] |= uint64_t(1) << (d % 64);
   t.elig = img.put(elig.data(), elig.size() * 8);
   t.batch = img.put(h.batch.data(), h.batch.size() * 4);
+  t.rcap = img.put(h.rcap.data(), h.rcap.size() * 4);
   t.cap = img.put(h.cap.data(), h.cap.size() * 4);
   t.arr = img.put(arr.data(), arr.size());
   t.res0 = img.put(h.init_res.data(), h.init_res.size() * 8);
@@ -483,12 +501,15 @@ wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, bool time64_req, Im
   // its initial set, or models whose weights sum to at most its capacity, or
   // (after a load that overflows) the one model just loaded
   sp.nibble = 0;
+  sp.rcap = h.rcap.empty() ? 0 : 1;
   const bool batched = std::any_of(h.batch.begin(), h.batch.end(), [](int32_t b) { return b > 1; });
   if (batched) {
     sp.nibble = h.victim_order == WF_VICTIM_PAPER ? -3 : -2;
   } else if (h.victim_order == WF_VICTIM_PAPER) {
     sp.nibble = -1;
-  } else if (M <= 16) {
+  } else if (M <= 16 && !sp.rcap) {
+    // (with replica caps the resident set stays a mask: the per-level check
+    // reads it)
     std::vector<int32_t> w(h.wmib.begin(), h.wmib.begin() + M);
     std::sort(w.begin(), w.end());
     int qcap = 1;

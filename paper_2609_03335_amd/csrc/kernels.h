@@ -36,6 +36,7 @@ struct TabOffsets {
   int sink;    // u32 [S]    activations without successor in their workflow: index | workflow << 16
   int elig;    // u64 [N][2] devices d with lat[i][d] >= 0 (bit d % 64 of word d / 64)
   int batch;   // i32 [D]    batch limit (units a device runs at once)
+  int rcap;    // i32 [M]    replica cap of each model (windows with caps)
   int bytes;
 };
 
@@ -61,6 +62,7 @@ struct WaveOffsets {
   int nxu;     // u16 [G*D][M]     paper order: next use of each model (device index)
   int snap;    // u64 [G][D]       paper order: resident models as the level starts
   int hstate;  // HState [2][64]   more than 64 devices: the state of each lane's idle device
+  int hold;    // u64 [G][D]       replica caps: models each device held or loaded in the level
   int bytes;
   // per-wave regions in HBM: the arrays at offsets below `split` (acc, and
   // outside the queue modes last, stamp, nxu, snap: O(G D M) bytes) stay in
@@ -106,6 +108,7 @@ struct ScoreParams {
                               // -1: scan in the paper's reclamation order; -2 / -3: the
                               // same two scans with per-device batch limits
   int has_chains;             // 1: some activation satisfies Eq. 3 (fused units possible)
+  int rcap;                   // 1: the window caps replicas (checked per level; scan modes only)
   int rescore;                // 1: fp64 pass over the groups holding a plan whose uint32
                               // times saturated (status bit kRescore of the first pass)
 };

@@ -313,6 +313,8 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   uint16_t* s_nxu = reinterpret_cast<uint16_t*>(small(sp.wo.nxu));
   unsigned long long* s_snap = reinterpret_cast<unsigned long long*>(small(sp.wo.snap));
   HState* s_hst = reinterpret_cast<HState*>(small(sp.wo.hstate));  // more than 64 devices only
+  unsigned long long* s_hold = reinterpret_cast<unsigned long long*>(small(sp.wo.hold));  // replica caps
+  const int32_t* t_rcap = reinterpret_cast<const int32_t*>(tb + sp.t.rcap);
   TB* s_wfm = reinterpret_cast<TB*>(big(sp.wo.wfm));
   int8_t* s_rdev = reinterpret_cast<int8_t*>(big(sp.wo.rows));         // generated candidates
   uint16_t* s_rprio = reinterpret_cast<uint16_t*>(big(sp.wo.rows_prio));
@@ -720,6 +722,9 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
     // models resident on the plan's other devices as the level starts
     int kdev = 0;
     unsigned long long others = 0ull;
+    // replica caps: the models the device holds as the level starts or loads
+    // during it (scanned resident sets only)
+    unsigned long long lv_hold = 0ull;
     // batch limits: per slot the free time, and the running unit's finish,
     // memory and model; the last first-action time (dispatch is in order)
     int nbatch = 1;
@@ -932,6 +937,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
           for (int e = 0; e < D; ++e)
             if (e != d) others |= s_snap[gme * D + e];
       }
+      if constexpr (!NIBBLE) lv_hold = res;
       if (act) {
         const int j1 = (hi - 1) >> 6;
         const unsigned long long hmask = (hi & 63) ? ((1ull << (hi & 63)) - 1ull) : ~0ull;
@@ -1219,7 +1225,10 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
                 if (ready) ph_h += (HT)TO::sub(s, TO::tmax(r, dev_free));
               }
             }
-            if constexpr (!NIBBLE) res |= mbit;
+            if constexpr (!NIBBLE) {
+              res |= mbit;
+              lv_hold |= mbit;
+            }
             used += hit ? 0 : X.lw.y;
             nld += hit ? 0u : 1u;
             peak = (used + run_act + mxu) > peak ? (used + run_act + mxu) : peak;
@@ -1292,9 +1301,25 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
         else
           run(next_wide);
       }
+      if constexpr (!NIBBLE) {
+        if (sp.rcap && act) s_hold[gme * D + d] = lv_hold;
+      }
       if (NH > 1) save(h);
       }
       wave_sync();
+      // ---- replica caps (Sec. 3.5 scale-out): a model held or loaded in
+      // this level on more devices than its cap; lanes over (plan, model) ----
+      if constexpr (!NIBBLE) {
+        if (sp.rcap) {
+          for (int it = lane; it < gc * M; it += 64) {
+            const int g = it / M, m = it - g * M;
+            int copies = 0;
+            for (int e = 0; e < D; ++e) copies += (int)((s_hold[g * D + e] >> m) & 1ull);
+            if (copies > t_rcap[m]) atomicOr(&s_acc[g].status, (uint32_t)WF_ST_REPLICA);
+          }
+          wave_sync();
+        }
+      }
     }
 
     // ---- per-plan reductions (Sec. 4 metrics) ----

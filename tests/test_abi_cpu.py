@@ -136,6 +136,11 @@ BAD = {
     "victim_order_unknown": lambda w: setattr(w, "victim_order", 2),
     "batch_zero": lambda w: setattr(w, "dev_batch", np.zeros(w.n_dev, np.int32)),
     "batch_too_big": lambda w: setattr(w, "dev_batch", np.full(w.n_dev, pkg._lib.WF_MAX_BATCH + 1, np.int32)),
+    "replica_cap_zero": lambda w: setattr(w, "model_replica_cap", np.zeros(w.n_models, np.int32)),
+    "replica_cap_below_initial_copies": lambda w: (
+        w.init_resident.__setitem__(slice(None), np.uint64(1)),
+        w.dev_cap_mib.__setitem__(slice(None), 1 << 29),
+        setattr(w, "model_replica_cap", np.ones(w.n_models, np.int32))),
 }
 
 

@@ -1,0 +1,136 @@
+"""Replica caps (Sec. 3.5: scale-out subject to the replica cap) on the GPU,
+bytewise against the oracle: the worked example, random windows under every
+reclamation mode (the default order over a scanned resident set, the
+paper's order, batch limits), both time arithmetics, more than 64 devices,
+schedules, ranking keys and generated candidates."""
+import dataclasses
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_03335_amd as pkg
+from fixtures import load_golden
+from paper_2609_03335_amd import workload as W
+
+pytestmark = pytest.mark.gpu
+THREADS = max(1, min(16, os.cpu_count() or 1))
+
+
+def log(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def ctx():
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+    c = pkg.Context(0)
+    yield c
+    c.close()
+
+
+def gpu(ctx, win, plans, schedule=False):
+    ctx.wf_plan_upload_window(win)
+    P, N, D = plans.n_plans, win.n_act, win.n_dev
+    dev, prio, flags = pkg.device_plans(plans, "cuda:0")
+    out = pkg.score_batch(ctx, dev, prio, flags, P, schedule=schedule, n_act=N, n_dev=D,
+                          reclaims=schedule)
+    keys = torch.empty((max(P, 1), 32), dtype=torch.uint8, device="cuda:0")
+    ctx.wf_plan_score_keys(dev, prio, flags, P, keys)
+    torch.cuda.synchronize()
+    s, sched = out if schedule else (out, None)
+    return pkg.scores_to_numpy(s, P), sched, pkg.keys_to_numpy(keys, P)
+
+
+def test_worked_example(ctx):
+    win, plans, ix, spec = load_golden("replica_cap")
+    for name, pl in plans.items():
+        got, _, _ = gpu(ctx, win, pl)
+        assert int(got["status"][0]) == spec["expect_status"][name], name
+        assert got.tobytes() == oracle.score(win, pl).tobytes(), name
+
+
+def capped_window(seed, mode):
+    rng = np.random.default_rng(4400 + seed)
+    D = {"manydev": 80}.get(mode, int(rng.integers(2, 9)))
+    M = int(rng.integers(2, 7)) if mode != "scan64" else 30
+    kw = dict(n_wf=int(rng.integers(2, 7)), nodes=(2, 10), n_dev=D, n_models=M,
+              cap_range=(8000, 30000), same_model_bias=0.5)
+    if mode == "fp64":
+        kw.update(lat_range=(1, 1 << 30), load_range=(0, 1 << 31))
+    if mode == "checked":
+        kw.update(lat_range=(1, 1 << 26), load_range=(0, 1 << 28))
+    win = W.random_window(rng, **kw)
+    init = np.array([sum(((int(win.init_resident[d]) >> m) & 1) for d in range(D)) for m in range(M)])
+    # caps near the number of devices: some plans spread a model that far
+    near = D - rng.integers(0, 3, M) if D <= 16 else rng.integers(6, 14, M)
+    win.model_replica_cap = np.maximum(init, near).clip(1).astype(np.int32)
+    if mode == "paper":
+        win.victim_order = 1
+    if mode == "batch":
+        win.dev_batch = rng.integers(1, 5, D).astype(np.int32)
+    plans = W.random_plans(win, 400, rng, prio_mode=("any", "perm")[seed % 2])
+    return win, plans
+
+
+MODES = ["scan", "scan64", "paper", "batch", "fp64", "checked", "manydev"]
+
+
+@pytest.mark.parametrize("mode", MODES)
+@pytest.mark.parametrize("seed", range(3))
+def test_random_capped_windows(ctx, mode, seed):
+    win, plans = capped_window(seed, mode)
+    log(f"[replica] mode={mode} seed={seed} N={win.n_act} D={win.n_dev} M={win.n_models}")
+    got, sched, keys = gpu(ctx, win, plans, schedule=True)
+    ref, rs = oracle.score(win, plans, schedule=True, reclaims=True, threads=THREADS)
+    assert got.tobytes() == ref.tobytes()
+    assert keys.tobytes() == oracle.phi_keys(win, plans, threads=THREADS).tobytes()
+    ok = (ref["status"] & pkg.WF_ST_INELIGIBLE) == 0
+    for name, g, r in zip(("start", "finish", "load_start", "peak", "reclaimed"), sched, rs):
+        a = g.cpu().numpy()
+        if name == "reclaimed":
+            a = a.view(np.uint64)
+        assert np.array_equal(a[:, :r.shape[1]][ok], r[ok]), name
+
+
+def test_some_plans_flagged_some_not(ctx):
+    flagged = total = 0
+    for seed in range(3):
+        win, plans = capped_window(seed, "scan")
+        got, _, _ = gpu(ctx, win, plans)
+        ok = (got["status"] & pkg.WF_ST_INELIGIBLE) == 0
+        flagged += int(((got["status"] & pkg.WF_ST_REPLICA) != 0).sum())
+        total += int(ok.sum())
+    assert 0 < flagged < total
+
+
+def test_generated_candidates_under_caps(ctx):
+    win, plans = capped_window(5, "scan")
+    ctx.wf_plan_upload_window(win)
+    inc = (plans.dev[0], plans.prio[0], plans.flags[0])
+    td = torch.from_numpy(np.ascontiguousarray(inc[0])).to("cuda:0")
+    tp = torch.from_numpy(np.ascontiguousarray(inc[1]).view(np.int16)).to("cuda:0")
+    tf = torch.from_numpy(np.ascontiguousarray(inc[2])).to("cuda:0")
+    n = 3000
+    scores = torch.empty((n, 32), dtype=torch.uint8, device="cuda:0")
+    ctx.wf_plan_search_batch(td, tp, tf, 99, 3, 0, n, scores)
+    torch.cuda.synchronize()
+    cand = W.PlanBatch(*oracle.search_candidates(win, *inc, 99, 3, 0, n))
+    assert pkg.scores_to_numpy(scores, n).tobytes() == oracle.score(win, cand, threads=THREADS).tobytes()
+
+
+def test_throughput_window_with_caps(ctx):
+    """The 256-activation window with every model capped at six copies (a
+    fifth of the plans spread some model further): the cap moves the window
+    to the scanned-residency kernel; records of 65,536 plans bytewise."""
+    win, plans = W.make_config(4, n_plans=65536)
+    win = dataclasses.replace(win, model_replica_cap=np.full(win.n_models, 6, np.int32))
+    got, _, _ = gpu(ctx, win, plans)
+    assert ctx.wf_plan_score_kernel() == "score_plans"
+    ref = oracle.score(win, plans, threads=THREADS)
+    assert got.tobytes() == ref.tobytes()
+    assert (ref["status"] & pkg.WF_ST_REPLICA).any() and not (ref["status"] & pkg.WF_ST_REPLICA).all()
