@@ -66,6 +66,7 @@ class _Win(ctypes.Structure):
         ("victim_order", ctypes.c_int32),
         ("dev_batch", ctypes.c_void_p),
         ("replica_cap", ctypes.c_void_p),
+        ("prefetch_slack_us", ctypes.c_int64),
     ]
 
 
@@ -94,7 +95,8 @@ def _load(path: Optional[str] = None):
             lib.orc_philox4x32_10.argtypes = [ctypes.c_void_p] * 3
             lib.orc_search_candidates.restype = ctypes.c_int
             lib.orc_search_candidates.argtypes = ([ctypes.c_void_p] * 4 + [ctypes.c_uint64, ctypes.c_int32,
-                                                  ctypes.c_int64, ctypes.c_int64] + [ctypes.c_void_p] * 3)
+                                                  ctypes.c_int64, ctypes.c_int64, ctypes.c_int32]
+                                                 + [ctypes.c_void_p] * 3)
             _libs[path] = lib
     return _libs[path]
 
@@ -133,6 +135,7 @@ class _WinHolder:
             setattr(s, k, None if v is None else v.ctypes.data)
         s.w_makespan, s.w_p95 = win.w_makespan, win.w_p95
         s.victim_order = int(getattr(win, "victim_order", 0))
+        s.prefetch_slack_us = int(getattr(win, "prefetch_slack_us", 0))
         self.struct = s
 
 
@@ -280,10 +283,14 @@ def philox4x32_10(ctr, key, lib_path: Optional[str] = None) -> np.ndarray:
     return out
 
 
+SEARCH_UNIFORM, SEARCH_RULES = 0, 1
+
+
 def search_candidates(win, dev, prio, flags, seed: int, n_mut: int, first: int, count: int,
-                      lib_path: Optional[str] = None):
+                      lib_path: Optional[str] = None, mode: int = SEARCH_UNIFORM):
     """Rows (dev, prio, flags) of candidates first .. first+count-1 around the
-    incumbent rows (one plan each)."""
+    incumbent rows (one plan each); mode SEARCH_RULES takes the device and
+    prefetch alternatives from the rules of Algorithm 1 (oracle.h)."""
     lib = _load(lib_path)
     h = _WinHolder(win)
     N = win.n_act
@@ -300,8 +307,8 @@ def search_candidates(win, dev, prio, flags, seed: int, n_mut: int, first: int, 
     ff = f if nb else np.zeros(1, np.uint8)
     rc = lib.orc_search_candidates(ctypes.byref(h.struct), dd.ctypes.data, pp.ctypes.data,
                                    ff.ctypes.data, int(seed) & ((1 << 64) - 1), int(n_mut),
-                                   int(first), int(count), od.ctypes.data, op.ctypes.data,
-                                   of.ctypes.data)
+                                   int(first), int(count), int(mode), od.ctypes.data,
+                                   op.ctypes.data, of.ctypes.data)
     if rc:
         raise OracleError(f"oracle rejected window (code {rc})")
     return od[:, :N].copy(), op[:, :N].copy(), of[:, :nb].copy()

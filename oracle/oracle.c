@@ -595,14 +595,103 @@ void orc_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t ou
 /* floor(r * n / 2^32): a draw r scaled to [0, n) */
 static uint32_t scale32(uint32_t r, uint32_t n) { return (uint32_t)(((uint64_t)r * n) >> 32); }
 
+/* The rule tables of the candidate generator: each activation's best
+ * binding (-1: none eligible), its earliest release, whether it is ready. */
+static int rule_tables(const orc_window *w, int8_t *best, int64_t *rel_lb, uint8_t *ready) {
+  const int32_t N = w->n_act, D = w->n_dev, M = w->n_models;
+  int64_t *unlock = (int64_t *)calloc((size_t)M * D, 8);
+  if (!unlock) return ORC_ERR_NOMEM;
+  for (int32_t i = 0; i < N; ++i)
+    ready[i] = w->pred_off[i] == w->pred_off[i + 1] && w->wf_arrival_us[w->act_wf[i]] <= 0;
+  /* ready work a load of model m on device d would unlock */
+  for (int32_t i = 0; i < N; ++i) {
+    if (!ready[i]) continue;
+    for (int32_t d = 0; d < D; ++d) {
+      const int32_t l = w->lat_us[(int64_t)i * D + d];
+      if (l >= 0) unlock[(int64_t)w->act_model[i] * D + d] += l;
+    }
+  }
+  for (int32_t i = 0; i < N; ++i) {
+    const int32_t m = w->act_model[i];
+    int32_t b = -1, resident = 0;
+    /* a resident accepting replica first: the fastest, then the lower id */
+    for (int32_t d = 0; d < D; ++d) {
+      const int32_t l = w->lat_us[(int64_t)i * D + d];
+      if (l < 0 || !((w->init_resident[d] >> m) & 1u)) continue;
+      if (!resident || l < w->lat_us[(int64_t)i * D + b]) b = d;
+      resident = 1;
+    }
+    if (!resident) {
+      /* otherwise the load worth the most: unlocked ready work per load time */
+      for (int32_t d = 0; d < D; ++d) {
+        const int32_t l = w->lat_us[(int64_t)i * D + d];
+        if (l < 0) continue;
+        if (b < 0) {
+          b = d;
+          continue;
+        }
+        const int64_t ld = w->load_us[(int64_t)m * D + d], lb = w->load_us[(int64_t)m * D + b];
+        const int64_t ud = unlock[(int64_t)m * D + d], ub = unlock[(int64_t)m * D + b];
+        int cmp; /* > 0: d is worth more than b */
+        if ((ld == 0) != (lb == 0)) cmp = ld == 0 ? 1 : -1;
+        else if (ld == 0) cmp = 0;
+        else {
+          const __int128 x = (__int128)ud * lb, y = (__int128)ub * ld;
+          cmp = x > y ? 1 : (x < y ? -1 : 0);
+        }
+        if (cmp > 0 || (cmp == 0 && l < w->lat_us[(int64_t)i * D + b])) b = d;
+      }
+    }
+    best[i] = (int8_t)b;
+  }
+  /* earliest release: predecessors on their fastest eligible devices */
+  for (int32_t i = 0; i < N; ++i) {
+    int64_t r = w->wf_arrival_us[w->act_wf[i]];
+    for (int32_t k = w->pred_off[i]; k < w->pred_off[i + 1]; ++k) {
+      const int32_t p = w->pred_idx[k];
+      int64_t fast = -1;
+      for (int32_t d = 0; d < D; ++d) {
+        const int32_t l = w->lat_us[(int64_t)p * D + d];
+        if (l >= 0 && (fast < 0 || l < fast)) fast = l;
+      }
+      if (rel_lb[p] + (fast < 0 ? 0 : fast) > r) r = rel_lb[p] + (fast < 0 ? 0 : fast);
+    }
+    rel_lb[i] = r;
+  }
+  free(unlock);
+  return ORC_OK;
+}
+
 int orc_search_candidates(const orc_window *w, const int8_t *dev, const uint16_t *prio,
                           const uint8_t *flags, uint64_t seed, int32_t n_mut, int64_t first,
-                          int64_t count, int8_t *out_dev, uint16_t *out_prio,
+                          int64_t count, int32_t mode, int8_t *out_dev, uint16_t *out_prio,
                           uint8_t *out_flags) {
+  if (mode != ORC_SEARCH_UNIFORM && mode != ORC_SEARCH_RULES) return ORC_ERR_SIZE;
   orc_struct st;
   int rc = build_struct(w, &st);
   if (rc) return rc;
   const int32_t N = w->n_act, D = w->n_dev, NB = (N + 3) / 4;
+  const size_t n = (size_t)(N > 0 ? N : 1);
+  int8_t *best = (int8_t *)malloc(n);
+  int64_t *rel_lb = (int64_t *)malloc(n * 8);
+  uint8_t *ready = (uint8_t *)malloc(n);
+  if (!best || !rel_lb || !ready) {
+    free(best);
+    free(rel_lb);
+    free(ready);
+    free_struct(&st);
+    return ORC_ERR_NOMEM;
+  }
+  if (mode == ORC_SEARCH_RULES) {
+    rc = rule_tables(w, best, rel_lb, ready);
+    if (rc) {
+      free(best);
+      free(rel_lb);
+      free(ready);
+      free_struct(&st);
+      return rc;
+    }
+  }
   const uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
   for (int64_t k = 0; k < count; ++k) {
     int8_t *cd = out_dev + k * N;
@@ -619,7 +708,10 @@ int orc_search_candidates(const orc_window *w, const int8_t *dev, const uint16_t
       orc_philox4x32_10(ctr, key, r);
       const int32_t i = (int32_t)scale32(r[1], (uint32_t)N);
       const uint32_t kind = r[0] >> 30;
-      if (kind == 0) {
+      if (kind == 0 && mode == ORC_SEARCH_RULES) {
+        /* BestFeasibleBinding */
+        if (best[i] >= 0) cd[i] = best[i];
+      } else if (kind == 0) {
         /* another eligible device (Eq. 8) */
         int32_t n_elig = 0;
         for (int32_t d = 0; d < D; ++d) n_elig += w->lat_us[(int64_t)i * D + d] >= 0;
@@ -644,11 +736,23 @@ int orc_search_candidates(const orc_window *w, const int8_t *dev, const uint16_t
         cp[j] = tmp;
       } else if (kind == 2) {
         cf[i / 4] ^= (uint8_t)(1u << (2 * (i % 4)));     /* fuse bit (Eq. 3) */
+      } else if (mode == ORC_SEARCH_RULES) {
+        /* PlanPrefetch: near-ready work whose earliest release is within
+         * the load time plus the dispatch slack */
+        const int32_t d = cd[i];
+        if (d < 0 || d >= D) continue;
+        const int64_t ld = w->load_us[(int64_t)w->act_model[i] * D + d];
+        const int on = !ready[i] && rel_lb[i] <= ld + w->prefetch_slack_us;
+        const uint8_t bit = (uint8_t)(1u << (2 * (i % 4) + 1));
+        cf[i / 4] = on ? (uint8_t)(cf[i / 4] | bit) : (uint8_t)(cf[i / 4] & ~bit);
       } else {
         cf[i / 4] ^= (uint8_t)(1u << (2 * (i % 4) + 1)); /* prefetch bit (Eq. 5) */
       }
     }
   }
+  free(best);
+  free(rel_lb);
+  free(ready);
   free_struct(&st);
   return ORC_OK;
 }

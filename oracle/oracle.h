@@ -51,6 +51,7 @@ typedef struct {
   int32_t victim_order;         /* ORC_VICTIM_REMAINING_LRU or ORC_VICTIM_PAPER */
   const int32_t *dev_batch;     /* [n_dev] batch limit 1..ORC_MAX_BATCH, NULL = all 1 */
   const int32_t *replica_cap;   /* [n_models] replica cap >= 1, NULL = no cap (below) */
+  int64_t prefetch_slack_us;    /* dispatch slack of the prefetch rule (below), >= 0 */
 } orc_window;
 
 /*
@@ -231,11 +232,37 @@ void orc_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t ou
 
 /* Rows of candidates first .. first+count-1 (out_dev [count][N], out_prio
  * [count][N], out_flags [count][ceil(N/4)]) around the incumbent rows dev,
- * prio, flags of one plan.  Returns an error code as above. */
+ * prio, flags of one plan.  mode ORC_SEARCH_UNIFORM draws the alternatives
+ * uniformly; ORC_SEARCH_RULES takes them from the rules below.  Returns an
+ * error code as above (ORC_ERR_SIZE for an unknown mode). */
+enum { ORC_SEARCH_UNIFORM = 0, ORC_SEARCH_RULES = 1 };
 int orc_search_candidates(const orc_window *w, const int8_t *dev, const uint16_t *prio,
                           const uint8_t *flags, uint64_t seed, int32_t n_mut, int64_t first,
-                          int64_t count, int8_t *out_dev, uint16_t *out_prio,
+                          int64_t count, int32_t mode, int8_t *out_dev, uint16_t *out_prio,
                           uint8_t *out_flags);
+
+/*
+ * Rule-guided alternatives (Algorithm 1, Sec. 3.5).  A unit is ready when
+ * its activation has no predecessor and its workflow has arrived by the
+ * window time 0; every other one is near-ready.
+ *   BestFeasibleBinding of activation i (mutation kind 0): among its
+ *   eligible devices (Eq. 8), one that holds i's model in the snapshot is
+ *   reused first -- the fastest for i, then the lower id; with no resident
+ *   copy, the load whose value is largest: the ready work it unlocks (the
+ *   summed run times on that device of the ready activations of the same
+ *   model eligible there) per load time of the model there (a free load is
+ *   worth the most; equal values: the faster device for i, then the lower
+ *   id).  An activation without an eligible device keeps its device.
+ *   PlanPrefetch of activation i (kind 3): the prefetch bit is set when i
+ *   is near-ready and its earliest release -- the longest path to it from
+ *   the workflow's arrival over predecessors on their fastest eligible
+ *   devices -- is at most the load time of its model on its current device
+ *   plus the window's dispatch slack; otherwise it is cleared (ready units
+ *   load at their release anyway).  A current device outside 0..n_dev-1
+ *   leaves the bit unchanged.
+ * Kinds 1 (a priority swap in the level) and 2 (the fuse bit) are drawn as
+ * in the uniform mode.
+ */
 
 #ifdef __cplusplus
 }

@@ -74,6 +74,8 @@ class Window:
     # int32[M] replica cap of each model (copies held across the pool in one
     # topological level, Sec. 3.5 scale-out), >= 1; None = no cap
     model_replica_cap: Optional[np.ndarray] = None
+    # dispatch slack of the rule-guided prefetch alternative (us, >= 0)
+    prefetch_slack_us: int = 0
 
     def arrays(self):
         return {f.name: getattr(self, f.name) for f in dataclasses.fields(self)}

@@ -47,6 +47,8 @@ def load_golden(name):
         win.dev_batch = np.array(batch, np.int32)
     if any("replica_cap" in m for m in spec["models"]):
         win.model_replica_cap = np.array([m.get("replica_cap", D) for m in spec["models"]], np.int32)
+    if "slack_us" in spec:
+        win.prefetch_slack_us = int(spec["slack_us"])
     for dname, mnames in spec.get("init_resident", {}).items():
         bits = 0
         for mn in mnames:

@@ -20,6 +20,7 @@ import test_oracle_victim as t_vic
 import test_oracle_batch as t_batch
 import test_oracle_prefix as t_prefix
 import test_oracle_replica as t_rep
+import test_oracle_search_rules as t_rules
 
 # (name, original fragment, planted mistake)
 MUTANTS = [
@@ -31,6 +32,31 @@ MUTANTS = [
      "if (n_units > 0 && replica_over(w, res_level, loaded_level)) sc.status |= ORC_REPLICA;", ""),
     ("replica loads accumulate across levels", "          loaded_level[e] = 0;\n", ""),
     ("replica flag clears other bits", "sc.status |= ORC_REPLICA;\n        for", "sc.status = ORC_REPLICA;\n        for"),
+    # rule-guided candidates (BestFeasibleBinding, PlanPrefetch)
+    ("rules: residency ignored", "if (l < 0 || !((w->init_resident[d] >> m) & 1u)) continue;", "if (l < 0 || 1) continue;"),
+    ("rules: slowest resident replica", "if (!resident || l < w->lat_us[(int64_t)i * D + b]) b = d;",
+     "if (!resident || l > w->lat_us[(int64_t)i * D + b]) b = d;"),
+    ("rules: value ratio inverted", "const __int128 x = (__int128)ud * lb, y = (__int128)ub * ld;",
+     "const __int128 x = (__int128)ud * ld, y = (__int128)ub * lb;"),
+    ("rules: free load not preferred", "if ((ld == 0) != (lb == 0)) cmp = ld == 0 ? 1 : -1;",
+     "if ((ld == 0) != (lb == 0)) cmp = ld == 0 ? -1 : 1;"),
+    ("rules: equal values keep the first", "if (cmp > 0 || (cmp == 0 && l < w->lat_us[(int64_t)i * D + b])) b = d;",
+     "if (cmp > 0) b = d;"),
+    ("rules: unlock counts waiting work", "    if (!ready[i]) continue;\n    for (int32_t d = 0; d < D; ++d) {",
+     "    for (int32_t d = 0; d < D; ++d) {"),
+    ("rules: readiness ignores arrival", "w->pred_off[i] == w->pred_off[i + 1] && w->wf_arrival_us[w->act_wf[i]] <= 0;",
+     "w->pred_off[i] == w->pred_off[i + 1];"),
+    ("rules: release ignores run times", "if (rel_lb[p] + (fast < 0 ? 0 : fast) > r) r = rel_lb[p] + (fast < 0 ? 0 : fast);",
+     "if (rel_lb[p] > r) r = rel_lb[p];"),
+    ("rules: release from the slowest device", "if (l >= 0 && (fast < 0 || l < fast)) fast = l;",
+     "if (l >= 0 && (fast < 0 || l > fast)) fast = l;"),
+    ("rules: prefetch without slack", "rel_lb[i] <= ld + w->prefetch_slack_us;", "rel_lb[i] <= ld;"),
+    ("rules: prefetch of ready work", "const int on = !ready[i] && rel_lb[i]", "const int on = rel_lb[i]"),
+    ("rules: prefetch on the incumbent's device", "const int32_t d = cd[i];\n        if (d < 0 || d >= D) continue;",
+     "const int32_t d = dev[i];\n        if (d < 0 || d >= D) continue;"),
+    ("rules: prefetch toggles", "cf[i / 4] = on ? (uint8_t)(cf[i / 4] | bit) : (uint8_t)(cf[i / 4] & ~bit);",
+     "cf[i / 4] ^= bit;"),
+    ("rules: binding falls back to uniform", "if (kind == 0 && mode == ORC_SEARCH_RULES) {", "if (kind == 0 && mode == 99) {"),
     # candidate generator
     ("philox multiplier swapped", "(uint64_t)0xD2511F53u * x0", "(uint64_t)0xCD9E8D57u * x0"),
     ("philox key not bumped", "k1 += 0xBB67AE85u;", ""),
@@ -164,6 +190,8 @@ def _pin_checks():
     checks += [t_rep.test_worked_example, t_rep.test_both_outcomes_occur]
     checks += [lambda s=s: t_rep.test_cap_is_a_check_only(s) for s in range(3)]
     checks += [t_prefix.test_worked_example]
+    checks += [t_rules.test_worked_example, t_rules.test_config_windows]
+    checks += [lambda s=s: t_rules.test_against_second_formulation(s) for s in range(4)]
     checks += [lambda s=s: t_prefix.test_single_device_chain(s) for s in range(4)]
     checks += [lambda s=s: t_prefix.test_invariants(s) for s in range(4)]
     return checks
