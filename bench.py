@@ -131,6 +131,8 @@ def main():
                     help="plans per leg checked against the oracle in the CPU-baseline leg (0 = none)")
     ap.add_argument("--search-mut", type=int, default=2,
                     help="mutations per generated candidate in the search leg (-1 = skip it)")
+    ap.add_argument("--prefetch-slack-us", type=int, default=None,
+                    help="dispatch slack of the rule-guided search leg (default: median load time)")
     ap.add_argument("--no-paper-order", action="store_true",
                     help="skip the leg that scores with the paper's reclamation order")
     ap.add_argument("--no-keys", action="store_true",
@@ -161,6 +163,10 @@ def main():
         return
     t0 = time.time()
     win, plans = workload.make_config(args.config, n_plans=args.plans)
+    # dispatch slack of the rule-guided prefetch alternative: the median load
+    # time of the window (used only by the rule-guided search leg)
+    win.prefetch_slack_us = int(np.median(win.load_us)) if args.prefetch_slack_us is None \
+        else args.prefetch_slack_us
     P, N, D = plans.n_plans, win.n_act, win.n_dev
     print(f"[bench] config {args.config}: N={N} W={win.n_wf} D={D} M={win.n_models} P={P} "
           f"generated in {time.time() - t0:.1f}s", file=sys.stderr, flush=True)
@@ -290,37 +296,47 @@ def main():
                               "and reclamations that begin before its next predicted event"}
 
     # candidates generated around plan 0 on the GPU and scored (no plan rows
-    # in HBM): the same number of plans, same window
-    search = None
+    # in HBM): the same number of plans, same window; uniform alternatives
+    # and the rule-guided ones of Algorithm 1
+    search, search_rules = None, None
     if args.search_mut >= 0:
         sd, sp_, sf = dev[0].contiguous(), prio[0].contiguous(), flags[0].contiguous()
         seed = 0x5EED
-        if args.check:
-            n_chk = min(P, args.check)
-            ctx.wf_plan_search_batch(sd, sp_, sf, seed, args.search_mut, 0, n_chk, scores, stream)
-            torch.cuda.synchronize()
+        legs = {}
+        for mname, mode in (("uniform", pkg.WF_SEARCH_UNIFORM), ("rules", pkg.WF_SEARCH_RULES)):
+            if args.check:
+                n_chk = min(P, args.check)
+                ctx.wf_plan_search_batch(sd, sp_, sf, seed, args.search_mut, 0, n_chk, scores, stream,
+                                         mode=mode)
+                torch.cuda.synchronize()
 
-            def search_ref(o, n_chk=n_chk, seed=seed):
-                inc = (plans.dev[0], plans.prio[0], plans.flags[0])
-                cand = workload.PlanBatch(*o.search_candidates(win, *inc, seed, args.search_mut, 0, n_chk))
-                return o.score(win, cand, threads=T).tobytes()
-            checks.append(("generated candidates", pkg.scores_to_numpy(scores, n_chk).tobytes(),
-                           search_ref))
-        for _ in range(args.warmup):
-            ctx.wf_plan_search_batch(sd, sp_, sf, seed, args.search_mut, 0, P, scores, stream)
-        torch.cuda.synchronize()
-        sev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-               for _ in range(args.steps)]
-        for i in range(args.steps):
-            sev[i][0].record(stream)
-            ctx.wf_plan_search_batch(sd, sp_, sf, seed, args.search_mut, i * P, P, scores, stream)
-            sev[i][1].record(stream)
-        torch.cuda.synchronize()
-        s_ms = float(np.mean([a.elapsed_time(b) for a, b in sev]))
-        search = {"value": round(P / (s_ms * 1e-3), 1), "unit": "candidates/s",
-                  "kernel_ms": round(s_ms, 4), "n_mut": args.search_mut,
-                  "note": "candidates generated around one incumbent plan inside the scoring "
-                          "kernel (no plan rows in HBM), same window and count"}
+                def search_ref(o, n_chk=n_chk, seed=seed, mode=mode):
+                    inc = (plans.dev[0], plans.prio[0], plans.flags[0])
+                    cand = workload.PlanBatch(*o.search_candidates(win, *inc, seed, args.search_mut, 0,
+                                                                   n_chk, mode=mode))
+                    return o.score(win, cand, threads=T).tobytes()
+                checks.append((f"generated candidates ({mname})",
+                               pkg.scores_to_numpy(scores, n_chk).tobytes(), search_ref))
+            for _ in range(args.warmup):
+                ctx.wf_plan_search_batch(sd, sp_, sf, seed, args.search_mut, 0, P, scores, stream,
+                                         mode=mode)
+            torch.cuda.synchronize()
+            sev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                   for _ in range(args.steps)]
+            for i in range(args.steps):
+                sev[i][0].record(stream)
+                ctx.wf_plan_search_batch(sd, sp_, sf, seed, args.search_mut, i * P, P, scores, stream,
+                                         mode=mode)
+                sev[i][1].record(stream)
+            torch.cuda.synchronize()
+            s_ms = float(np.mean([a.elapsed_time(b) for a, b in sev]))
+            legs[mname] = {"value": round(P / (s_ms * 1e-3), 1), "unit": "candidates/s",
+                           "kernel_ms": round(s_ms, 4), "n_mut": args.search_mut}
+        search = dict(legs["uniform"], note="candidates generated around one incumbent plan inside "
+                      "the scoring kernel (no plan rows in HBM), same window and count")
+        search_rules = dict(legs["rules"], prefetch_slack_us=int(win.prefetch_slack_us),
+                            note="the same with Algorithm 1's rules for re-placed devices "
+                                 "(BestFeasibleBinding) and prefetch bits (PlanPrefetch)")
 
     # the ranking keys of Eq. 12 for the same plans, and their lexicographic
     # argmin
@@ -462,6 +478,7 @@ def main():
         "valu_roofline": valu_roofline(args.config, P, kernel_ms),
         "cpu_baseline": cpu,
         "search": search,
+        "search_rules": search_rules,
         "keys": keys_leg,
         "paper_order": paper_leg,
         "batch_limit": batch_leg,

@@ -91,6 +91,9 @@ typedef enum {
 #define WF_MAX_CLASSES 4           /* priority classes of the ranking key      */
 #define WF_MAX_BATCH 4             /* batch limit of a device                  */
 
+/* How generated candidates choose a re-placed device and a prefetch bit. */
+enum { WF_SEARCH_UNIFORM = 0, WF_SEARCH_RULES = 1 };
+
 /* Plan status bits; a plan is feasible iff status == 0. */
 enum { WF_ST_INELIGIBLE = 1u, WF_ST_CAPACITY = 2u, WF_ST_REPLICA = 4u };
 
@@ -130,6 +133,9 @@ typedef struct {
   const int32_t *model_replica_cap; /* [M] replica cap of each model >= 1 (below), or
                                      NULL for none; the initial residency must
                                      hold at most cap[m] copies of model m      */
+  int64_t prefetch_slack_us;      /* dispatch slack of the rule-guided prefetch
+                                     alternative (WF_SEARCH_RULES, below),
+                                     0..WF_MAX_TIME_US                          */
 } wf_window_desc;
 
 /*
@@ -272,7 +278,26 @@ wf_status wf_plan_argmin_noalloc(const wf_plan_score *scores, int64_t n_plans,
  *           j = lo + (r2 * w) div 2^32; prio[i] and prio[j] are swapped;
  *   kind 2: the fuse bit of i is toggled;
  *   kind 3: the prefetch bit of i is toggled.
- * r3 is not used.  With N = 0 a candidate is the incumbent.
+ * r3 is not used.  With N = 0 a candidate is the incumbent.  This is mode
+ * WF_SEARCH_UNIFORM.  Mode WF_SEARCH_RULES draws the same (kind, i) and
+ * takes kinds 0 and 3 from the rules Algorithm 1 names (Sec. 3.5) instead,
+ * under these readings:
+ *   - a unit is ready when activation i has no predecessor and its workflow
+ *     has arrived by the window time 0; every other unit is near-ready;
+ *   - kind 0, BestFeasibleBinding: among E, a device whose initial resident
+ *     set holds i's model is reused first (the one with the smallest
+ *     lat_us[i][d], then the lower id); with none, the load of largest value
+ *     -- the summed lat_us[j][d] of the ready activations j of i's model
+ *     eligible on d (the ready work the load unlocks) over load_us[m][d],
+ *     a load time of 0 worth more than any ratio -- then the smallest
+ *     lat_us[i][d], then the lower id.  With E empty dev[i] is unchanged;
+ *   - kind 3, PlanPrefetch: with d = dev[i] as the earlier mutations left it
+ *     (unchanged when d is outside 0..n_dev-1), the prefetch bit of i is set
+ *     iff i is near-ready and its earliest release -- the longest path to it
+ *     from its workflow's arrival over its predecessors, each on its fastest
+ *     eligible device (0 with none) -- is at most load_us[m][d] +
+ *     prefetch_slack_us; otherwise it is cleared.
+ * Kinds 1 and 2 are as in the uniform mode.  Any other mode is WF_EINVAL.
  *
  * dev [N], prio [N], flags [ceil(N/4)] are the incumbent's rows (device
  * memory, layout of wf_plan_score_batch).  Candidates first ..
@@ -283,16 +308,17 @@ wf_status wf_plan_argmin_noalloc(const wf_plan_score *scores, int64_t n_plans,
 /* Score the candidates: scores[k] is candidate first+k scored exactly as
  * wf_plan_score_batch would score its rows.  Asynchronous on hip_stream. */
 wf_status wf_plan_search_batch(wf_plan_ctx *ctx, const int8_t *dev, const uint16_t *prio,
-                               const uint8_t *flags, uint64_t seed, int32_t n_mut, int64_t first,
-                               int64_t n_candidates, wf_plan_score *scores, void *hip_stream);
+                               const uint8_t *flags, int32_t mode, uint64_t seed, int32_t n_mut,
+                               int64_t first, int64_t n_candidates, wf_plan_score *scores,
+                               void *hip_stream);
 
 /* Write the candidates' rows (out_dev [n][N], out_prio [n][N], out_flags
  * [n][ceil(N/4)], device memory) -- to adopt a winner found by
  * wf_plan_search_batch and wf_plan_argmin.  Asynchronous on hip_stream. */
 wf_status wf_plan_search_rows(wf_plan_ctx *ctx, const int8_t *dev, const uint16_t *prio,
-                              const uint8_t *flags, uint64_t seed, int32_t n_mut, int64_t first,
-                              int64_t n_candidates, int8_t *out_dev, uint16_t *out_prio,
-                              uint8_t *out_flags, void *hip_stream);
+                              const uint8_t *flags, int32_t mode, uint64_t seed, int32_t n_mut,
+                              int64_t first, int64_t n_candidates, int8_t *out_dev,
+                              uint16_t *out_prio, uint8_t *out_flags, void *hip_stream);
 
 /*
  * Ranking keys.  The paper's scheduler ranks plans lexicographically by
@@ -336,8 +362,9 @@ wf_status wf_plan_score_keys(wf_plan_ctx *ctx, const int8_t *dev, const uint16_t
 /* Ranking keys of generated candidates first .. first+n_candidates-1 around
  * an incumbent (arguments and limits as for wf_plan_search_batch). */
 wf_status wf_plan_search_keys(wf_plan_ctx *ctx, const int8_t *dev, const uint16_t *prio,
-                              const uint8_t *flags, uint64_t seed, int32_t n_mut, int64_t first,
-                              int64_t n_candidates, wf_plan_key *keys, void *hip_stream);
+                              const uint8_t *flags, int32_t mode, uint64_t seed, int32_t n_mut,
+                              int64_t first, int64_t n_candidates, wf_plan_key *keys,
+                              void *hip_stream);
 
 /* Among keys with status 0, the index of the lexicographically smallest Phi
  * (lowest index on ties), or -1 if none is feasible, written to the device

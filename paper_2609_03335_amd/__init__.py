@@ -7,15 +7,16 @@ the HIP stream.
 from __future__ import annotations
 
 from ._lib import (EXPORTS, KEY_DTYPE, SCORE_DTYPE, WF_EHIP, WF_EINVAL, WF_ENOMEM, WF_ENOWINDOW, WF_OK,
-                   WF_EUNSUPPORTED, WF_ST_CAPACITY, WF_ST_INELIGIBLE, WF_ST_REPLICA, Context, WFError, load,
-                   wf_plan_argmin_noalloc, wf_plan_validate_window, wf_plan_version)
+                   WF_EUNSUPPORTED, WF_SEARCH_RULES, WF_SEARCH_UNIFORM, WF_ST_CAPACITY, WF_ST_INELIGIBLE,
+                   WF_ST_REPLICA, Context, WFError, load, wf_plan_argmin_noalloc, wf_plan_validate_window,
+                   wf_plan_version)
 
 __all__ = [
     "Context", "WFError", "wf_plan_argmin_noalloc", "SCORE_DTYPE", "KEY_DTYPE", "EXPORTS", "load", "wf_plan_validate_window",
     "wf_plan_version", "device_plans", "score_batch", "argmin", "scores_to_numpy",
     "keys_to_numpy",
     "WF_OK", "WF_EINVAL", "WF_ENOWINDOW", "WF_ENOMEM", "WF_EHIP", "WF_EUNSUPPORTED",
-    "WF_ST_INELIGIBLE", "WF_ST_CAPACITY", "WF_ST_REPLICA",
+    "WF_ST_INELIGIBLE", "WF_ST_CAPACITY", "WF_ST_REPLICA", "WF_SEARCH_UNIFORM", "WF_SEARCH_RULES",
 ]
 
 

@@ -25,6 +25,7 @@ WF_MAX_ACT, WF_MAX_MODELS, WF_MAX_DEV, WF_MAX_MUT = 65535, 64, 127, 64
 WF_MAX_CLASSES = 4
 WF_VICTIM_REMAINING_LRU, WF_VICTIM_PAPER = 0, 1
 WF_MAX_BATCH = 4
+WF_SEARCH_UNIFORM, WF_SEARCH_RULES = 0, 1
 
 SCORE_DTYPE = np.dtype([
     ("makespan_us", "<i8"), ("p95_us", "<i8"), ("objective", "<f4"),
@@ -70,6 +71,7 @@ class wf_window_desc(ctypes.Structure):
         ("victim_order", ctypes.c_int32),
         ("dev_batch", ctypes.c_void_p),
         ("model_replica_cap", ctypes.c_void_p),
+        ("prefetch_slack_us", ctypes.c_int64),
     ]
 
 
@@ -110,13 +112,13 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.wf_plan_argmin_noalloc.argtypes = [vp, i64, vp, vp]
     lib.wf_plan_argmin_noalloc.restype = i32
     u64 = ctypes.c_uint64
-    lib.wf_plan_search_batch.argtypes = [vp, vp, vp, vp, u64, ctypes.c_int32, i64, i64, vp, vp]
+    lib.wf_plan_search_batch.argtypes = [vp, vp, vp, vp, i32, u64, i32, i64, i64, vp, vp]
     lib.wf_plan_search_batch.restype = i32
-    lib.wf_plan_search_rows.argtypes = [vp, vp, vp, vp, u64, ctypes.c_int32, i64, i64, vp, vp, vp, vp]
+    lib.wf_plan_search_rows.argtypes = [vp, vp, vp, vp, i32, u64, i32, i64, i64, vp, vp, vp, vp]
     lib.wf_plan_search_rows.restype = i32
     lib.wf_plan_score_keys.argtypes = [vp, vp, vp, vp, i64, vp, vp]
     lib.wf_plan_score_keys.restype = ctypes.c_int
-    lib.wf_plan_search_keys.argtypes = [vp, vp, vp, vp, u64, ctypes.c_int32, i64, i64, vp, vp]
+    lib.wf_plan_search_keys.argtypes = [vp, vp, vp, vp, i32, u64, i32, i64, i64, vp, vp]
     lib.wf_plan_search_keys.restype = ctypes.c_int
     lib.wf_plan_argmin_keys.argtypes = [vp, vp, i64, vp, vp]
     lib.wf_plan_argmin_keys.restype = ctypes.c_int
@@ -166,6 +168,7 @@ class _Desc:
             setattr(d, k, None if v is None else v.ctypes.data)
         d.w_makespan, d.w_p95 = win.w_makespan, win.w_p95
         d.victim_order = int(getattr(win, "victim_order", 0))
+        d.prefetch_slack_us = int(getattr(win, "prefetch_slack_us", 0))
         self.desc = d
 
 
@@ -311,21 +314,24 @@ class Context:
             self._b(out_index, 8, "out_index"), _stream(stream)))
 
     def wf_plan_search_batch(self, dev, prio, flags, seed: int, n_mut: int, first: int,
-                             n_candidates: int, scores, stream=None) -> None:
+                             n_candidates: int, scores, stream=None,
+                             mode: int = WF_SEARCH_UNIFORM) -> None:
         """Score candidates first .. first+n_candidates-1 generated around the
-        incumbent rows dev/prio/flags (device buffers of one plan)."""
+        incumbent rows dev/prio/flags (device buffers of one plan); mode is
+        WF_SEARCH_UNIFORM or WF_SEARCH_RULES."""
         self._check(self.lib.wf_plan_search_batch(
-            self.handle, *self._rows(dev, prio, flags, 1), int(seed) & ((1 << 64) - 1),
+            self.handle, *self._rows(dev, prio, flags, 1), int(mode), int(seed) & ((1 << 64) - 1),
             int(n_mut), int(first), int(n_candidates),
             self._b(scores, 32 * self._cnt(n_candidates), "scores"), _stream(stream)))
 
     def wf_plan_search_rows(self, dev, prio, flags, seed: int, n_mut: int, first: int,
-                            n_candidates: int, out_dev, out_prio, out_flags, stream=None) -> None:
+                            n_candidates: int, out_dev, out_prio, out_flags, stream=None,
+                            mode: int = WF_SEARCH_UNIFORM) -> None:
         """Write the rows of candidates first .. first+n_candidates-1."""
         n = self._cnt(n_candidates)
         N = self._nd[0]
         self._check(self.lib.wf_plan_search_rows(
-            self.handle, *self._rows(dev, prio, flags, 1), int(seed) & ((1 << 64) - 1),
+            self.handle, *self._rows(dev, prio, flags, 1), int(mode), int(seed) & ((1 << 64) - 1),
             int(n_mut), int(first), int(n_candidates), self._b(out_dev, n * N, "out_dev"),
             self._b(out_prio, 2 * n * N, "out_prio"),
             self._b(out_flags, n * ((N + 3) // 4), "out_flags"), _stream(stream)))
@@ -338,10 +344,11 @@ class Context:
             self._b(keys, 32 * P, "keys"), _stream(stream)))
 
     def wf_plan_search_keys(self, dev, prio, flags, seed: int, n_mut: int, first: int,
-                            n_candidates: int, keys, stream=None) -> None:
+                            n_candidates: int, keys, stream=None,
+                            mode: int = WF_SEARCH_UNIFORM) -> None:
         """Ranking keys of candidates generated around the incumbent rows."""
         self._check(self.lib.wf_plan_search_keys(
-            self.handle, *self._rows(dev, prio, flags, 1), int(seed) & ((1 << 64) - 1),
+            self.handle, *self._rows(dev, prio, flags, 1), int(mode), int(seed) & ((1 << 64) - 1),
             int(n_mut), int(first), int(n_candidates),
             self._b(keys, 32 * self._cnt(n_candidates), "keys"), _stream(stream)))
 

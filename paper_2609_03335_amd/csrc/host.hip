@@ -34,6 +34,7 @@ struct HostWindow {
   std::vector<int32_t> batch;  // [D] batch limit
   std::vector<int32_t> rcap;   // [M] replica cap, empty = none
   float w_mk = 1.f, w_p95 = 0.f;
+  int64_t pf_slack = 0;        // dispatch slack of the prefetch rule
 };
 
 wf_status fail(std::string* err, wf_status st, const char* fmt, ...) __attribute__((format(printf, 3, 4)));
@@ -150,9 +151,13 @@ wf_status validate(const wf_window_desc* w, std::string* err, HostWindow* out) {
         return fail(err, WF_EINVAL, "initial residency holds %lld copies of model %lld, above its replica cap %d",
                     (long long)copies, (long long)m, (int)w->model_replica_cap[m]);
     }
+  if (w->prefetch_slack_us < 0 || w->prefetch_slack_us > WF_MAX_TIME_US)
+    return fail(err, WF_EINVAL, "prefetch_slack_us = %lld outside [0, 2^52]",
+                (long long)w->prefetch_slack_us);
   if (!out) return WF_OK;
 
   HostWindow& h = *out;
+  h.pf_slack = w->prefetch_slack_us;
   h.victim_order = w->victim_order;
   h.batch.assign((size_t)D, 1);
   if (w->dev_batch) h.batch.assign(w->dev_batch, w->dev_batch + D);
@@ -218,6 +223,9 @@ wf_status validate(const wf_window_desc* w, std::string* err, HostWindow* out) {
 
 struct DeviceWindow {
   void* tab = nullptr;          // table image in HBM
+  void* rules = nullptr;        // rule tables of the candidate generator
+  const unsigned long long* rule_pf = nullptr;
+  const int8_t* rule_best = nullptr;
   void* tab64 = nullptr;        // fp64-time table image of the rescoring pass
   void* scratch = nullptr;      // per-wave regions for windows too big for LDS
   void* tab_lean = nullptr;     // the lean kernel's table image
@@ -258,7 +266,79 @@ void free_device_window(DeviceWindow& dw) {
   if (dw.tab64) (void)hipFree(dw.tab64);
   if (dw.scratch) (void)hipFree(dw.scratch);
   if (dw.tab_lean) (void)hipFree(dw.tab_lean);
+  if (dw.rules) (void)hipFree(dw.rules);
   dw = DeviceWindow{};
+}
+
+// The rule tables of the candidate generator (Algorithm 1, Sec. 3.5), as a
+// byte image: [N][2] 64-bit masks of the devices on which PlanPrefetch sets
+// activation i's prefetch bit, then [N] best feasible bindings (-1: no
+// eligible device).  A unit is ready when it has no predecessor and its
+// workflow has arrived by time 0.
+std::vector<unsigned char> rule_image(const HostWindow& h, size_t* best_at) {
+  const int32_t N = h.N, D = h.D, M = h.M;
+  const size_t n = (size_t)std::max(N, 1);
+  std::vector<unsigned char> img(n * 16 + n, 0);
+  *best_at = n * 16;
+  uint64_t* pf = reinterpret_cast<uint64_t*>(img.data());
+  int8_t* best = reinterpret_cast<int8_t*>(img.data() + n * 16);
+  std::vector<uint8_t> ready((size_t)N);
+  std::vector<int64_t> work((size_t)M * D, 0);  // ready work a load of (m, d) unlocks
+  std::vector<int64_t> rel((size_t)N), fastest((size_t)N);
+  for (int32_t i = 0; i < N; ++i) {
+    const int32_t* li = &h.lat[(size_t)i * D];
+    ready[i] = h.pred_off[i] == h.pred_off[i + 1] && h.arrival[h.act_wf[i]] <= 0;
+    int64_t f = -1;
+    for (int32_t d = 0; d < D; ++d) {
+      if (li[d] < 0) continue;
+      if (f < 0 || li[d] < f) f = li[d];
+      if (ready[i]) work[(size_t)h.act_model[i] * D + d] += li[d];
+    }
+    fastest[i] = f < 0 ? 0 : f;
+    // activations are in topological order: predecessors are final here
+    int64_t r = h.arrival[h.act_wf[i]];
+    for (int32_t k = h.pred_off[i]; k < h.pred_off[i + 1]; ++k)
+      r = std::max(r, rel[h.pred_idx[k]] + fastest[h.pred_idx[k]]);
+    rel[i] = r;
+  }
+  for (int32_t i = 0; i < N; ++i) {
+    const int32_t m = h.act_model[i];
+    const int32_t* li = &h.lat[(size_t)i * D];
+    const int32_t* lm = &h.load[(size_t)m * D];
+    const int64_t* wm = &work[(size_t)m * D];
+    int b = -1;
+    bool b_res = false;
+    for (int32_t d = 0; d < D; ++d) {
+      if (li[d] < 0) continue;
+      const bool res = (h.init_res[d] >> m) & 1ull;
+      bool take;
+      if (b < 0 || res != b_res) {
+        take = b < 0 || res;  // a resident replica beats any load
+      } else if (res) {
+        take = li[d] < li[b];
+      } else {
+        // value = work / load, a free load above every ratio
+        int v;
+        if (lm[d] == 0 || lm[b] == 0) {
+          v = (lm[d] == 0) - (lm[b] == 0);
+        } else {
+          const unsigned __int128 x = (unsigned __int128)(uint64_t)wm[d] * (uint32_t)lm[b];
+          const unsigned __int128 y = (unsigned __int128)(uint64_t)wm[b] * (uint32_t)lm[d];
+          v = (x > y) - (x < y);
+        }
+        take = v > 0 || (v == 0 && li[d] < li[b]);
+      }
+      if (take) {
+        b = d;
+        b_res = res;
+      }
+    }
+    best[i] = (int8_t)b;
+    if (ready[i]) continue;
+    for (int32_t d = 0; d < D; ++d)
+      if (rel[i] <= (int64_t)lm[d] + h.pf_slack) pf[(size_t)i * 2 + d / 64] |= 1ull << (d % 64);
+  }
+  return img;
 }
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
@@ -909,6 +989,17 @@ wf_status wf_plan_upload_window(wf_plan_ctx* ctx, const wf_window_desc* w) {
       return hip_fail(ctx, e, "copying the window to the device");
     }
   }
+  size_t rule_best_at = 0;
+  const std::vector<unsigned char> rimg = rule_image(h, &rule_best_at);
+  e = hipMalloc(&dw.rules, rimg.size());
+  if (e == hipSuccess) e = hipMemcpy(dw.rules, rimg.data(), rimg.size(), hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    free_device_window(dw);
+    (void)hipSetDevice(prev);
+    return hip_fail(ctx, e, "copying the rule tables to the device");
+  }
+  dw.rule_pf = static_cast<const unsigned long long*>(dw.rules);
+  dw.rule_best = static_cast<const int8_t*>(dw.rules) + rule_best_at;
   // one scratch area serves every pass (they run in order on a stream)
   wfp::ScoreParams* all[4] = {&sp, &sps, &sp64, &sps64};
   size_t need = 0;
@@ -1018,13 +1109,15 @@ wf_status wf_plan_score_batch(wf_plan_ctx* ctx, const int8_t* dev, const uint16_
 
 // Shared argument checks of the candidate-generation calls.
 static wf_status search_args(wf_plan_ctx* ctx, const int8_t* dev, const uint16_t* prio,
-                             const uint8_t* flags, int32_t n_mut, int64_t first,
+                             const uint8_t* flags, int32_t mode, int32_t n_mut, int64_t first,
                              int64_t n_candidates) {
   if (!ctx) {
     g_thread_err = "ctx is NULL";
     return WF_EINVAL;
   }
   if (!ctx->has_window) return fail(&ctx->err, WF_ENOWINDOW, "no window uploaded");
+  if (mode != WF_SEARCH_UNIFORM && mode != WF_SEARCH_RULES)
+    return fail(&ctx->err, WF_EINVAL, "mode = %d is not a WF_SEARCH_* value", (int)mode);
   if (n_mut < 0 || n_mut > WF_MAX_MUT)
     return fail(&ctx->err, WF_EINVAL, "n_mut must be in [0, %d]", WF_MAX_MUT);
   if (n_candidates < 0) return fail(&ctx->err, WF_EINVAL, "n_candidates is negative");
@@ -1035,10 +1128,17 @@ static wf_status search_args(wf_plan_ctx* ctx, const int8_t* dev, const uint16_t
   return WF_OK;
 }
 
+static wfp::SearchArgs search_params(const wf_plan_ctx* ctx, int32_t mode, uint64_t seed,
+                                     int32_t n_mut, int64_t first) {
+  return wfp::SearchArgs{seed, n_mut, mode, first, ctx->host.D, ctx->dw.rule_best,
+                         ctx->dw.rule_pf};
+}
+
 wf_status wf_plan_search_batch(wf_plan_ctx* ctx, const int8_t* dev, const uint16_t* prio,
-                               const uint8_t* flags, uint64_t seed, int32_t n_mut, int64_t first,
-                               int64_t n_candidates, wf_plan_score* scores, void* hip_stream) {
-  wf_status st = search_args(ctx, dev, prio, flags, n_mut, first, n_candidates);
+                               const uint8_t* flags, int32_t mode, uint64_t seed, int32_t n_mut,
+                               int64_t first, int64_t n_candidates, wf_plan_score* scores,
+                               void* hip_stream) {
+  wf_status st = search_args(ctx, dev, prio, flags, mode, n_mut, first, n_candidates);
   if (st != WF_OK) return st;
   if (n_candidates == 0) return WF_OK;
   if (!scores) return fail(&ctx->err, WF_EINVAL, "scores is NULL");
@@ -1046,7 +1146,7 @@ wf_status wf_plan_search_batch(wf_plan_ctx* ctx, const int8_t* dev, const uint16
   (void)hipGetDevice(&prev);
   hipError_t e = hipSetDevice(ctx->device);
   if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
-  const wfp::SearchArgs sa{seed, n_mut, first};
+  const wfp::SearchArgs sa = search_params(ctx, mode, seed, n_mut, first);
   e = two_pass(ctx->dw, true, n_candidates, [&](const wfp::ScoreParams& sp) {
     return wfp::launch_score(sp, dev, prio, flags, n_candidates, scores, nullptr, &sa,
                              static_cast<hipStream_t>(hip_stream));
@@ -1057,10 +1157,10 @@ wf_status wf_plan_search_batch(wf_plan_ctx* ctx, const int8_t* dev, const uint16
 }
 
 wf_status wf_plan_search_rows(wf_plan_ctx* ctx, const int8_t* dev, const uint16_t* prio,
-                              const uint8_t* flags, uint64_t seed, int32_t n_mut, int64_t first,
-                              int64_t n_candidates, int8_t* out_dev, uint16_t* out_prio,
-                              uint8_t* out_flags, void* hip_stream) {
-  wf_status st = search_args(ctx, dev, prio, flags, n_mut, first, n_candidates);
+                              const uint8_t* flags, int32_t mode, uint64_t seed, int32_t n_mut,
+                              int64_t first, int64_t n_candidates, int8_t* out_dev,
+                              uint16_t* out_prio, uint8_t* out_flags, void* hip_stream) {
+  wf_status st = search_args(ctx, dev, prio, flags, mode, n_mut, first, n_candidates);
   if (st != WF_OK) return st;
   if (n_candidates == 0 || ctx->host.N == 0) return WF_OK;
   if (!out_dev || !out_prio || !out_flags)
@@ -1071,7 +1171,7 @@ wf_status wf_plan_search_rows(wf_plan_ctx* ctx, const int8_t* dev, const uint16_
   (void)hipGetDevice(&prev);
   hipError_t e = hipSetDevice(ctx->device);
   if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
-  const wfp::SearchArgs sa{seed, n_mut, first};
+  const wfp::SearchArgs sa = search_params(ctx, mode, seed, n_mut, first);
   e = wfp::launch_search_rows(ctx->dw.sp_search, dev, prio, flags, sa, n_candidates, out_dev,
                               out_prio, out_flags, static_cast<hipStream_t>(hip_stream));
   (void)hipSetDevice(prev);
@@ -1159,9 +1259,10 @@ wf_status wf_plan_score_keys(wf_plan_ctx* ctx, const int8_t* dev, const uint16_t
 }
 
 wf_status wf_plan_search_keys(wf_plan_ctx* ctx, const int8_t* dev, const uint16_t* prio,
-                              const uint8_t* flags, uint64_t seed, int32_t n_mut, int64_t first,
-                              int64_t n_candidates, wf_plan_key* keys, void* hip_stream) {
-  wf_status st = search_args(ctx, dev, prio, flags, n_mut, first, n_candidates);
+                              const uint8_t* flags, int32_t mode, uint64_t seed, int32_t n_mut,
+                              int64_t first, int64_t n_candidates, wf_plan_key* keys,
+                              void* hip_stream) {
+  wf_status st = search_args(ctx, dev, prio, flags, mode, n_mut, first, n_candidates);
   if (st != WF_OK) return st;
   if (n_candidates == 0) return WF_OK;
   if (!keys) return fail(&ctx->err, WF_EINVAL, "keys is NULL");
@@ -1169,7 +1270,7 @@ wf_status wf_plan_search_keys(wf_plan_ctx* ctx, const int8_t* dev, const uint16_
   (void)hipGetDevice(&prev);
   hipError_t e = hipSetDevice(ctx->device);
   if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
-  const wfp::SearchArgs sa{seed, n_mut, first};
+  const wfp::SearchArgs sa = search_params(ctx, mode, seed, n_mut, first);
   e = two_pass(ctx->dw, true, n_candidates, [&](const wfp::ScoreParams& sp) {
     return wfp::launch_score_keys(sp, dev, prio, flags, n_candidates, keys, &sa,
                                   static_cast<hipStream_t>(hip_stream));

@@ -199,7 +199,14 @@ struct PlanAcc {
 struct SearchArgs {
   uint64_t seed;
   int32_t n_mut;
+  int32_t mode;   // WF_SEARCH_UNIFORM or WF_SEARCH_RULES
   int64_t first;  // index of the first candidate
+  int32_t D;
+  // rule tables of the window (WF_SEARCH_RULES): each activation's best
+  // binding (-1: none eligible) and the devices on which PlanPrefetch sets
+  // its prefetch bit ([N][2] 64-bit masks)
+  const int8_t* rule_best;
+  const unsigned long long* rule_pf;
 };
 
 // Scores plans read from dev/prio/flags ([P][N] rows), or -- with search --

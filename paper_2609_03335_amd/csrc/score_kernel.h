@@ -135,7 +135,9 @@ __device__ __forceinline__ void philox4x32_10(uint32_t x[4], uint32_t k0, uint32
 // Turns rows (dev, prio, flags) holding the incumbent into candidate c: the
 // n_mut mutations drawn from Philox4x32-10 with counter (c, t) and the
 // seed as key -- another eligible device for activation i, a swap of two
-// priorities inside i's level, or a toggled fuse / prefetch bit of i.
+// priorities inside i's level, or a toggled fuse / prefetch bit of i.  With
+// the rules (Algorithm 1, Sec. 3.5) the device is i's best feasible binding
+// and the prefetch bit is what PlanPrefetch decides on i's current device.
 __device__ __forceinline__ void mutate(uint64_t c, const SearchArgs& sa, int N,
                                        const unsigned long long* elig, const uint32_t* alv,
                                        int8_t* rd, uint16_t* rp, uint8_t* rf) {
@@ -145,7 +147,19 @@ __device__ __forceinline__ void mutate(uint64_t c, const SearchArgs& sa, int N,
     philox4x32_10(x, (uint32_t)sa.seed, (uint32_t)(sa.seed >> 32));
     const int i = (int)__umulhi(x[1], (uint32_t)N);
     const uint32_t kind = x[0] >> 30;
-    if (kind == 0u) {
+    if (sa.mode == WF_SEARCH_RULES && (kind == 0u || kind == 3u)) {
+      if (kind == 0u) {
+        const int b = sa.rule_best[i];
+        if (b >= 0) rd[i] = (int8_t)b;
+      } else {
+        const int d = rd[i];
+        if (d >= 0 && d < sa.D) {
+          const uint8_t bit = (uint8_t)(2u << ((i & 3) << 1));
+          if ((sa.rule_pf[2 * i + (d >> 6)] >> (d & 63)) & 1ull) rf[i >> 2] |= bit;
+          else rf[i >> 2] &= (uint8_t)~bit;
+        }
+      }
+    } else if (kind == 0u) {
       unsigned long long e = elig[2 * i], e1 = elig[2 * i + 1];
       const uint32_t n0 = (uint32_t)__popcll(e), n = n0 + (uint32_t)__popcll(e1);
       if (n) {

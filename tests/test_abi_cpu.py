@@ -141,6 +141,8 @@ BAD = {
         w.init_resident.__setitem__(slice(None), np.uint64(1)),
         w.dev_cap_mib.__setitem__(slice(None), 1 << 29),
         setattr(w, "model_replica_cap", np.ones(w.n_models, np.int32))),
+    "prefetch_slack_negative": lambda w: setattr(w, "prefetch_slack_us", -1),
+    "prefetch_slack_too_big": lambda w: setattr(w, "prefetch_slack_us", (1 << 52) + 1),
 }
 
 
@@ -149,6 +151,12 @@ def test_invalid_windows_rejected(name):
     w = _mutate(BAD[name])
     st, msg = pkg.wf_plan_validate_window(w)
     assert st == pkg.WF_EINVAL and msg, (name, st, msg)
+
+
+def test_prefetch_slack_limits_accepted():
+    for slack in (0, 1, 1 << 52):
+        w = _mutate(lambda w: setattr(w, "prefetch_slack_us", slack))
+        assert pkg.wf_plan_validate_window(w)[0] == pkg.WF_OK
 
 
 def test_not_level_sorted_rejected():
