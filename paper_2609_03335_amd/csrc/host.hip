@@ -429,6 +429,32 @@ int wave_layout(const HostWindow& h, int G, int tsz, int nwa, int qmode, bool se
   return o.bytes;
 }
 
+// Per-wave LDS region of the ring layout for G plans (kernel PLACE 2): the
+// per-plan arrays of the current level and of the ring's levels only.
+int ring_layout(const HostWindow& h, const wfp::ScoreParams& sp, int G, int tsz, int nwl,
+                wfp::WaveOffsets& o) {
+  size_t off = 0;
+  auto take = [&](size_t n) {
+    const size_t at = off;
+    off = align_up(off + std::max<size_t>(n, 1), 16);
+    return (int)at;
+  };
+  const size_t dm = (size_t)G * h.D * h.M;
+  o = wfp::WaveOffsets{};
+  o.flags = take((size_t)G * ((h.N + 3) / 4));
+  o.rec = take((size_t)G * sp.ring_w * 4);
+  o.mask = take((size_t)G * h.D * nwl * 8);
+  o.acc = take((size_t)G * sizeof(wfp::PlanAcc));
+  o.last = take(dm * 4);
+  o.stamp = take(dm * 2);
+  o.fin = take((size_t)G * sp.ring_levels * sp.ring_w * tsz);
+  o.wfm = take((size_t)G * std::max(1, h.W) * tsz);
+  o.hstate = take(h.D > 64 ? 2 * 64 * sizeof(wfp::HState) : 0);
+  o.hold = take(h.rcap.empty() ? 0 : (size_t)G * h.D * 8);
+  o.bytes = (int)off;
+  return o.bytes;
+}
+
 // How a window's times are carried: uint32 when no time of any plan can reach
 // 2^32 (proven by the static bound below), uint32 with an fp64 rescoring of
 // the plans that saturate when the bound is within kCheckedSpan of 2^32 (few
@@ -560,6 +586,45 @@ wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, bool time64_req, Im
   const int32_t S = (int32_t)sink.size();
   if (sink.empty()) sink.push_back(0);
   t.sink = img.put(sink.data(), sink.size() * 4);
+  // ring of recent levels (scan reclamation in the default order): a
+  // finish must stay from the level where it is written -- a fused chain's
+  // members with the chain head, up to ring_a levels early -- to the last
+  // level an edge reads it, ring_b levels later
+  const bool batched_w = std::any_of(h.batch.begin(), h.batch.end(), [](int32_t b) { return b > 1; });
+  const bool scan_lru = h.victim_order != WF_VICTIM_PAPER && (batched_w || M > 16 || !h.rcap.empty());
+  sp.ring_ok = 0;
+  if (scan_lru && N > 0) {
+    std::vector<int32_t> lvl((size_t)N), wmin((size_t)N);
+    for (int32_t l = 0; l < h.n_levels; ++l)
+      for (int32_t i = h.level_off[l]; i < h.level_off[l + 1]; ++i) lvl[i] = l;
+    int32_t ra = 0, rb = 0;
+    for (int32_t v = 0; v < N; ++v) {
+      wmin[v] = h.fusible[v] ? wmin[h.pred_idx[h.pred_off[v]]] : lvl[v];
+      ra = std::max(ra, lvl[v] - wmin[v]);
+      for (int32_t k = h.pred_off[v]; k < h.pred_off[v + 1]; ++k)
+        rb = std::max(rb, lvl[v] - lvl[h.pred_idx[k]]);
+    }
+    const int64_t levels = (int64_t)ra + rb + 1;
+    if (levels * h.wmax <= 65535) {
+      sp.ring_ok = 1;
+      sp.ring_levels = (int)levels;
+      sp.ring_w = h.wmax;
+      sp.ring_a = ra;
+      sp.ring_b = rb;
+      std::vector<uint16_t> rpos((size_t)N), rsnk((size_t)N);
+      for (int32_t i = 0; i < N; ++i) {
+        rpos[i] = (uint16_t)((lvl[i] % levels) * h.wmax + (i - h.level_off[lvl[i]]));
+        rsnk[i] = has_wf_succ[i] ? (uint16_t)0xffff : (uint16_t)h.act_wf[i];
+      }
+      std::vector<uint32_t> redge((size_t)std::max(E, 1), 0);
+      for (int32_t v = 0; v < N; ++v)
+        for (int32_t k = h.pred_off[v]; k < h.pred_off[v + 1]; ++k)
+          redge[k] = (uint32_t)rpos[h.pred_idx[k]] | ((uint32_t)rpos[v] << 16);
+      t.rpos = img.put(rpos.data(), rpos.size() * 2);
+      t.rsnk = img.put(rsnk.data(), rsnk.size() * 2);
+      t.redge = img.put(redge.data(), redge.size() * 4);
+    }
+  }
   img.bytes.resize(align_up(img.bytes.size(), 16), 0);
   t.bytes = (int)img.bytes.size();
 
@@ -685,6 +750,48 @@ wf_status plan_launch(wf_plan_ctx* ctx, const HostWindow& h, bool search, wfp::S
     sp.lds_bytes = lds_wg_g;
     sp.grid = (int)wgs;
     sp.wo = o;
+  }
+  // the ring of recent levels: per-plan state of the current level and the
+  // levels a unit can still reach, all in LDS.  Taken over the LDS layout
+  // when it keeps more walk lanes in flight, and over the HBM layout when
+  // it keeps as many.
+  sp.ring = 0;
+  const char* ring_env = std::getenv("WF_PLAN_RING");
+  const bool ring_off = ring_env && std::strcmp(ring_env, "off") == 0;
+  if (!search && !ring_off && sp.ring_ok && (sp.nibble == 0 || sp.nibble == -2)) {
+    const int nwl = (sp.ring_w + 63) / 64 + 1;
+    const double cur = sp.wave_global ? hbm_lanes : best;
+    double rbest = -1.0;
+    int rG = 0, rwaves = 0, rlds = 0, rwgs = 0;
+    wfp::WaveOffsets ro{};
+    for (int G = gmax; G >= 1; --G) {
+      wfp::WaveOffsets o{};
+      const int wb = ring_layout(h, sp, G, tsz, nwl, o);
+      const int waves = std::min(8, lds_blk / std::max(wb, 1));
+      if (waves < 1) continue;
+      const int lds_wg = waves * wb;
+      const int wg_per_cu = std::max(1, lds_cu / lds_wg);
+      const double score = (double)std::min(G * D, 64) * std::min(std::min(32, wg_per_cu * waves), 8);
+      if (score > rbest) {
+        rbest = score;
+        rG = G;
+        rwaves = waves;
+        rlds = lds_wg;
+        rwgs = wg_per_cu;
+        ro = o;
+      }
+    }
+    if (rbest > 0 && (rbest > cur || (sp.wave_global && rbest >= cur))) {
+      sp.ring = 1;
+      sp.wave_global = 0;
+      sp.tab_in_lds = 0;
+      sp.G = rG;
+      sp.waves = rwaves;
+      sp.lds_bytes = rlds;
+      sp.grid = ctx->n_cu * rwgs;
+      sp.wo = ro;
+      sp.nwa = nwl;
+    }
   }
   return WF_OK;
 }
@@ -1051,6 +1158,10 @@ wf_status wf_plan_upload_window(wf_plan_ctx* ctx, const wf_window_desc* w) {
                  sp.waves, sp.grid, sp.wave_global ? "hbm+scratch" : (sp.tab_in_lds ? "lds" : "hbm"),
                  sp.t.bytes, sp.wo.bytes, sp.wave_global ? sp.wo.split : sp.wo.bytes, sp.lds_bytes, sp.nibble == 32 ? "queue32" : sp.nibble == 64 ? "queue64" : sp.nibble == -1 ? "paper-scan" :
                  sp.nibble == -2 ? "batch-scan" : sp.nibble == -3 ? "batch-paper-scan" : "scan");
+  if (std::getenv("WF_PLAN_VERBOSE") && sp.ring)
+    std::fprintf(stderr, "[wf_plan] ring of recent levels: %d levels (%d ahead, %d behind) x %d "
+                 "activations, %d mask words per device\n", sp.ring_levels, sp.ring_a, sp.ring_b,
+                 sp.ring_w, sp.nwa);
   if (std::getenv("WF_PLAN_VERBOSE") && dw.lean.ok)
     std::fprintf(stderr, "[wf_plan] lean kernel: G=%d waves/wg=%d grid=%d tables=%d B wave=%d B lds/wg=%d\n",
                  dw.lean.G, dw.lean.waves, dw.lean.grid, dw.lean.t.bytes, dw.lean.wo.bytes,

@@ -37,6 +37,13 @@ struct TabOffsets {
   int elig;    // u64 [N][2] devices d with lat[i][d] >= 0 (bit d % 64 of word d / 64)
   int batch;   // i32 [D]    batch limit (units a device runs at once)
   int rcap;    // i32 [M]    replica cap of each model (windows with caps)
+  // ring of recent levels (ScoreParams::ring): finishes are kept only for
+  // the levels a unit can still reach, at ring positions
+  int rpos;    // u16 [N]    ring position: (level mod ring levels) * widest level +
+               //            index inside the level
+  int redge;   // u32 [E]    as edge, with ring positions instead of activation ids
+  int rsnk;    // u16 [N]    workflow of an activation without successor in its
+               //            workflow, else 0xffff
   int bytes;
 };
 
@@ -51,6 +58,9 @@ struct WaveOffsets {
   int fin;     // time [G][N]      latest predecessor finish, then the activation's own finish
   int acc;     // PlanAcc [G]
   int stamp;   // u16 [G*D][M]     last use of each model (general reclamation only)
+               // (ring layout: rec holds [G][widest level] entries of the current
+               // level, mask [G][D][NWA] its words, last the count of each
+               // (device, model)'s units not yet walked, fin [G][ring size])
   int rows;    // generated candidates only: int8 [G][N] devices, then u16 [G][N]
                //                  priorities at rows + rows_prio; they live in fin's
                //                  storage (after last[] when that shares it) until
@@ -111,6 +121,14 @@ struct ScoreParams {
   int rcap;                   // 1: the window caps replicas (checked per level; scan modes only)
   int rescore;                // 1: fp64 pass over the groups holding a plan whose uint32
                               // times saturated (status bit kRescore of the first pass)
+  // ring of recent levels (deep or wide windows, scan reclamation, plan rows
+  // from HBM): the slot entries and device masks of the current level only,
+  // and the finishes of ring_levels consecutive levels; ring_a levels ahead
+  // (a fused chain's members get their finish with the chain head) and
+  // ring_b behind (the longest edge, in levels)
+  int ring;                   // 1: this launch uses the ring layout
+  int ring_ok;                // 1: the window admits it (tables rpos, redge, rsnk built)
+  int ring_levels, ring_w, ring_a, ring_b;
 };
 
 // Byte offsets inside one wave's LDS region of the lean kernel (lean.hip):

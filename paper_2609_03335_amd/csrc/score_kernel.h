@@ -234,7 +234,10 @@ struct UnitPre {
 template <bool PHI>
 using OutRec = std::conditional_t<PHI, wf_plan_key, wf_plan_score>;
 
-template <typename TT, bool TAB_LDS, int QB, bool WAVE_GLOBAL, bool SEARCH, bool PHI, bool SCHED>
+// PLACE: 0 = per-wave regions in LDS, 1 = their per-activation arrays in HBM
+// scratch, 2 = the ring of recent levels in LDS (scan reclamation, rows from
+// HBM).
+template <typename TT, bool TAB_LDS, int QB, int PLACE, bool SEARCH, bool PHI, bool SCHED>
 __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
                                                    const int8_t* __restrict__ dev_all,
                                                    const uint16_t* __restrict__ prio_all,
@@ -253,6 +256,9 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   // once, each in one of up to kMaxBatch slots)
   constexpr bool PAPER = QB == -1 || QB == -3;
   constexpr bool BATCH = QB <= -2;
+  constexpr bool WAVE_GLOBAL = PLACE == 1;
+  constexpr bool RING = PLACE == 2;
+  static_assert(!RING || ((QB == 0 || QB == -2) && !SEARCH), "ring layout: scans, rows from HBM");
   using QT = std::conditional_t<QB == 32, uint32_t, uint64_t>;
   constexpr QT kOnes = (QT)0x1111111111111111ull, kHigh = (QT)0x8888888888888888ull;
   constexpr int kQBits = (int)sizeof(QT) * 8;
@@ -299,6 +305,16 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   const uint32_t* t_sink = reinterpret_cast<const uint32_t*>(tb + sp.t.sink);
   const unsigned long long* t_elig = reinterpret_cast<const unsigned long long*>(tb + sp.t.elig);
   const int32_t* t_batch = reinterpret_cast<const int32_t*>(tb + sp.t.batch);
+  const uint16_t* t_rpos = reinterpret_cast<const uint16_t*>(tb + sp.t.rpos);
+  const uint16_t* t_rsnk = reinterpret_cast<const uint16_t*>(tb + sp.t.rsnk);
+  // ring layout: slot entries per plan (the widest level), finishes per plan
+  // (the ring), a finish's position
+  const int RW = RING ? sp.ring_w : N;
+  const int FS = RING ? sp.ring_levels * sp.ring_w : N;
+  auto fpos = [&](int u) -> int {
+    if constexpr (RING) return (int)t_rpos[u];
+    else return u;
+  };
 
   // ---- this wave's region (LDS, or HBM scratch for very large windows) ----
   // (with regions in HBM, the small per-(device, model) arrays stay in LDS:
@@ -353,7 +369,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   // one 256-activation chunk and at most eight plans per group: the next
   // group's device and priority rows are loaded while this group is walked
   constexpr int kB = 8;
-  const bool pre = !SEARCH && vec && N <= 256 && G <= kB && !sp.rescore;
+  const bool pre = !SEARCH && !RING && vec && N <= 256 && G <= kB && !sp.rescore;
   uint32_t dvp[kB];
   uint2 pvp[kB];
   auto load_rows = [&](int64_t grp_, uint32_t* dv, uint2* pv) {
@@ -424,257 +440,276 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
     }
     wave_sync();
 
-    // ---- resource order (Eq. 10), first try: a unit head's slot is its
-    // priority, valid when each level's head priorities are distinct values
-    // in the level's index range (checked below by counting) ----
-    // one activation u of plan g with device d and priority pr; cbyte is the
-    // flag byte of u's chain successor
-    auto order_fast = [&](int g, int u, int d, int pr, uint32_t a, uint32_t lvw, uint32_t c,
-                          uint32_t fb, uint32_t cbyte, uint32_t& nh, uint32_t& nbad,
-                          uint32_t& ninel) {
-      const bool head = !((fb & 1u) && (a & 64u));  // not a fused chain member
-      const bool okd = (unsigned)d < (unsigned)D;
-      const bool inr = (unsigned)(pr - (int)(lvw & 0xffffu)) < (lvw >> 16);
-      const bool chain = c != 0xffffu && ((cbyte >> ((c & 3u) << 1)) & 1u);
-      ninel |= (uint32_t)(head && !okd);
-      nbad |= (uint32_t)(head && okd && !inr);
-      if (head && okd && inr) {
-        const uint32_t m = a & 63u;
-        s_rec[g * N + pr] = (uint32_t)u | (m << 16) | ((fb & 2u) << 21) |
-                            (chain ? kChain | kSlow : slow0);
-        atomicOr(&s_mask[(g * D + d) * NWA + (pr >> 6)], 1ull << (pr & 63));
-        if constexpr (!PAPER) atomicMax(&s_last[(g * D + d) * M + (int)m], (uint32_t)pr + 1u);
-        ++nh;
-      }
-    };
-    // per-plan totals from uniform control flow, at most 4 heads per lane:
-    // wave ballots instead of 64 conflicting LDS atomics
-    auto order_flush4 = [&](int g, uint32_t nh, uint32_t nbad, uint32_t ninel) {
-      const uint32_t tot = (uint32_t)__popcll(__ballot(nh & 1u)) +
-                           2u * (uint32_t)__popcll(__ballot(nh & 2u)) +
-                           4u * (uint32_t)__popcll(__ballot(nh & 4u));
-      const bool any_bad = __ballot(nbad != 0u) != 0ull;
-      const bool any_inel = __ballot(ninel != 0u) != 0ull;
-      if (lane == 0) {
-        if (any_inel) s_acc[g].status |= (uint32_t)WF_ST_INELIGIBLE;
-        if (any_bad) s_acc[g].bad = 1u;
-        s_acc[g].heads += tot;
-      }
-    };
-    // device and priority rows of plan g: HBM, or the generated candidate
-    auto row_dev = [&](int g) -> const int8_t* {
-      if constexpr (SEARCH) return s_rdev + g * N;
-      else return dev_all + (p0 + g) * N;
-    };
-    auto row_prio = [&](int g) -> const uint16_t* {
-      if constexpr (SEARCH) return s_rprio + g * N;
-      else return prio_all + (p0 + g) * N;
-    };
-    // the rows of plans g0 .. g0 + kB - 1 at activations uc .. uc + 3
-    auto rows4 = [&](int g0, int uc, uint32_t* dv, uint2* pv) {
-#pragma unroll
-      for (int k = 0; k < kB; ++k) {
-        const int g = (g0 + k < gc) ? g0 + k : gc - 1;
-        if (pre) {
-          dv[k] = dvp[k];
-          pv[k] = pvp[k];
-        } else {
-          dv[k] = *reinterpret_cast<const uint32_t*>(row_dev(g) + uc);
-          pv[k] = *reinterpret_cast<const uint2*>(row_prio(g) + uc);
+    if constexpr (!RING) {
+      // ---- resource order (Eq. 10), first try: a unit head's slot is its
+      // priority, valid when each level's head priorities are distinct values
+      // in the level's index range (checked below by counting) ----
+      // one activation u of plan g with device d and priority pr; cbyte is the
+      // flag byte of u's chain successor
+      auto order_fast = [&](int g, int u, int d, int pr, uint32_t a, uint32_t lvw, uint32_t c,
+                            uint32_t fb, uint32_t cbyte, uint32_t& nh, uint32_t& nbad,
+                            uint32_t& ninel) {
+        const bool head = !((fb & 1u) && (a & 64u));  // not a fused chain member
+        const bool okd = (unsigned)d < (unsigned)D;
+        const bool inr = (unsigned)(pr - (int)(lvw & 0xffffu)) < (lvw >> 16);
+        const bool chain = c != 0xffffu && ((cbyte >> ((c & 3u) << 1)) & 1u);
+        ninel |= (uint32_t)(head && !okd);
+        nbad |= (uint32_t)(head && okd && !inr);
+        if (head && okd && inr) {
+          const uint32_t m = a & 63u;
+          s_rec[g * N + pr] = (uint32_t)u | (m << 16) | ((fb & 2u) << 21) |
+                              (chain ? kChain | kSlow : slow0);
+          atomicOr(&s_mask[(g * D + d) * NWA + (pr >> 6)], 1ull << (pr & 63));
+          if constexpr (!PAPER) atomicMax(&s_last[(g * D + d) * M + (int)m], (uint32_t)pr + 1u);
+          ++nh;
         }
-      }
-    };
-    if (vec) {
-      // four consecutive activations per lane: one 4-byte device load, one
-      // 8-byte priority load and one flag byte per plan; every load of a
-      // batch of plans is issued before any of it is used
-      for (int base = 0; base < N; base += 256) {
-        const int u0 = base + 4 * lane;
-        const bool live = u0 < N;
-        const int uc = live ? u0 : 0;
-        const uint4 act4 = *reinterpret_cast<const uint4*>(t_act + uc);
-        const uint4 alv4 = *reinterpret_cast<const uint4*>(t_alv + uc);
-        const uint2 cn4 = *reinterpret_cast<const uint2*>(t_cnext + uc);
-        const uint32_t cn[4] = {cn4.x & 0xffffu, cn4.x >> 16, cn4.y & 0xffffu, cn4.y >> 16};
-        for (int g0 = 0; g0 < gc; g0 += kB) {
-          uint32_t dv[kB], fl[kB], cb[kB][4];
-          uint2 pv[kB];
-          rows4(g0, uc, dv, pv);
-#pragma unroll
-          for (int k = 0; k < kB; ++k) {
-            const int g = (g0 + k < gc) ? g0 + k : gc - 1;
-            fl[k] = s_fl[g * NB + (uc >> 2)];
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-              cb[k][j] = sp.has_chains ? s_fl[g * NB + ((cn[j] != 0xffffu ? cn[j] : (uint32_t)uc) >> 2)]
-                                       : 0u;
-          }
-#pragma unroll
-          for (int k = 0; k < kB; ++k) {
-            const int g = g0 + k;
-            if (g >= gc) break;
-            uint32_t nh = 0, nbad = 0, ninel = 0;
-            if (live) {
-              order_fast(g, uc, (int)(int8_t)(dv[k] & 0xffu), (int)(pv[k].x & 0xffffu), act4.x,
-                         alv4.x, cn[0], fl[k], cb[k][0], nh, nbad, ninel);
-              order_fast(g, uc + 1, (int)(int8_t)((dv[k] >> 8) & 0xffu), (int)(pv[k].x >> 16),
-                         act4.y, alv4.y, cn[1], fl[k] >> 2, cb[k][1], nh, nbad, ninel);
-              order_fast(g, uc + 2, (int)(int8_t)((dv[k] >> 16) & 0xffu), (int)(pv[k].y & 0xffffu),
-                         act4.z, alv4.z, cn[2], fl[k] >> 4, cb[k][2], nh, nbad, ninel);
-              order_fast(g, uc + 3, (int)(int8_t)(dv[k] >> 24), (int)(pv[k].y >> 16), act4.w,
-                         alv4.w, cn[3], fl[k] >> 6, cb[k][3], nh, nbad, ninel);
-            }
-            order_flush4(g, nh, nbad, ninel);
+      };
+      // per-plan totals from uniform control flow, at most 4 heads per lane:
+      // wave ballots instead of 64 conflicting LDS atomics
+      auto order_flush4 = [&](int g, uint32_t nh, uint32_t nbad, uint32_t ninel) {
+        const uint32_t tot = (uint32_t)__popcll(__ballot(nh & 1u)) +
+                             2u * (uint32_t)__popcll(__ballot(nh & 2u)) +
+                             4u * (uint32_t)__popcll(__ballot(nh & 4u));
+        const bool any_bad = __ballot(nbad != 0u) != 0ull;
+        const bool any_inel = __ballot(ninel != 0u) != 0ull;
+        if (lane == 0) {
+          if (any_inel) s_acc[g].status |= (uint32_t)WF_ST_INELIGIBLE;
+          if (any_bad) s_acc[g].bad = 1u;
+          s_acc[g].heads += tot;
+        }
+      };
+      // device and priority rows of plan g: HBM, or the generated candidate
+      auto row_dev = [&](int g) -> const int8_t* {
+        if constexpr (SEARCH) return s_rdev + g * N;
+        else return dev_all + (p0 + g) * N;
+      };
+      auto row_prio = [&](int g) -> const uint16_t* {
+        if constexpr (SEARCH) return s_rprio + g * N;
+        else return prio_all + (p0 + g) * N;
+      };
+      // the rows of plans g0 .. g0 + kB - 1 at activations uc .. uc + 3
+      auto rows4 = [&](int g0, int uc, uint32_t* dv, uint2* pv) {
+  #pragma unroll
+        for (int k = 0; k < kB; ++k) {
+          const int g = (g0 + k < gc) ? g0 + k : gc - 1;
+          if (pre) {
+            dv[k] = dvp[k];
+            pv[k] = pvp[k];
+          } else {
+            dv[k] = *reinterpret_cast<const uint32_t*>(row_dev(g) + uc);
+            pv[k] = *reinterpret_cast<const uint2*>(row_prio(g) + uc);
           }
         }
-      }
-    } else {
-      for (int g = 0; g < gc; ++g) {
-        const int8_t* pdev = row_dev(g);
-        const uint16_t* pprio = row_prio(g);
-        const uint8_t* pfl = s_fl + g * NB;
-        uint32_t nh = 0, nbad = 0, ninel = 0;
-        for (int u = lane; u < N; u += 64) {
-          const uint32_t fb = (uint32_t)pfl[u >> 2] >> ((u & 3) << 1);
-          const uint32_t c = t_cnext[u];
-          const uint32_t cbyte = pfl[(c != 0xffffu ? c : (uint32_t)u) >> 2];
-          order_fast(g, u, pdev[u], pprio[u], t_act[u], t_alv[u], c, fb, cbyte, nh, nbad, ninel);
-        }
-        if (ninel) atomicOr(&s_acc[g].status, (uint32_t)WF_ST_INELIGIBLE);
-        if (nbad) atomicOr(&s_acc[g].bad, 1u);
-        if (nh) atomicAdd(&s_acc[g].heads, nh);
-      }
-    }
-    wave_sync();
-    // distinct slots claimed per plan: the union of its devices' masks
-    for (int i = lane; i < gc * NWA; i += 64) {
-      const int g = i / NWA, w = i - g * NWA;
-      unsigned long long x = 0ull;
-      for (int d = 0; d < D; ++d) x |= s_mask[(g * D + d) * NWA + w];
-      if (x) atomicAdd(&s_acc[g].claimed, (uint32_t)__popcll(x));
-    }
-    wave_sync();
-    // plans whose priorities are not a permutation of each level's heads'
-    // index range (one lane per plan)
-    uint64_t rankedm;
-    {
-      const PlanAcc& ag = s_acc[lane < gc ? lane : 0];  // G <= 64
-      const bool rk = lane < gc && (ag.bad != 0u || ag.heads != ag.claimed);
-      rankedm = __ballot(rk);
-    }
-    // general path: rank by (priority, index) within each level
-    for (uint64_t rm = rankedm; rm; rm &= rm - 1ull) {
-      const int g = __builtin_ctzll(rm);
-      const int8_t* pdev = row_dev(g);
-      const uint16_t* pprio = row_prio(g);
-      const uint8_t* pfl = s_fl + g * NB;
-      uint32_t* rec = s_rec + g * N;
-      unsigned long long* mk = s_mask + g * D * NWA;
-      uint32_t* lastp = s_last + g * D * M;
-      for (int i = lane; i < D * NWA; i += 64) mk[i] = 0ull;
-      if constexpr (!PAPER)
-        for (int i = lane; i < D * M; i += 64) lastp[i] = 0u;
-      wave_sync();
-      for (int u = lane; u < N; u += 64) {
-        const uint32_t a = t_act[u];
-        const int fb = pfl[u >> 2] >> ((u & 3) << 1);
-        if ((fb & 1) && (a & 64u)) continue;
-        const int d = pdev[u];
-        if ((unsigned)d >= (unsigned)D) continue;
-        const uint32_t lvw = t_alv[u];
-        const int lo = (int)(lvw & 0xffffu), hi = lo + (int)(lvw >> 16);
-        const int pu = pprio[u];
-        int slot = lo;
-        for (int j = lo; j < hi; ++j) {
-          if (fuse_bit(pfl, j) && (t_act[j] & 64u)) continue;
-          if ((unsigned)pdev[j] >= (unsigned)D) continue;
-          const int pj = pprio[j];
-          slot += (pj < pu) || (pj == pu && j < u);
-        }
-        const int c = t_cnext[u];
-        const uint32_t chain = (c != 0xffff && fuse_bit(pfl, c)) ? kChain : 0u;
-        rec[slot] = (uint32_t)u | ((a & 63u) << 16) | ((uint32_t)((fb >> 1) & 1) << 22) | chain |
-                    (chain ? kSlow : slow0);
-        atomicOr(&mk[d * NWA + (slot >> 6)], 1ull << (slot & 63));
-        if constexpr (!PAPER) atomicMax(&lastp[d * M + (int)(a & 63u)], (uint32_t)slot + 1u);
-      }
-      wave_sync();
-    }
-    if constexpr (NIBBLE) {
-      // mark each (device, model)'s last unit in its slot entry: the
-      // reclamation queues need only that bit, and last[] dies here
+      };
       if (vec) {
-        // plans ordered by priority: re-derive each head's (device, slot,
-        // model) from its row; all loads first, then the marks
+        // four consecutive activations per lane: one 4-byte device load, one
+        // 8-byte priority load and one flag byte per plan; every load of a
+        // batch of plans is issued before any of it is used
         for (int base = 0; base < N; base += 256) {
           const int u0 = base + 4 * lane;
           const bool live = u0 < N;
           const int uc = live ? u0 : 0;
           const uint4 act4 = *reinterpret_cast<const uint4*>(t_act + uc);
           const uint4 alv4 = *reinterpret_cast<const uint4*>(t_alv + uc);
-          const uint32_t av[4] = {act4.x, act4.y, act4.z, act4.w};
-          const uint32_t lv[4] = {alv4.x, alv4.y, alv4.z, alv4.w};
+          const uint2 cn4 = *reinterpret_cast<const uint2*>(t_cnext + uc);
+          const uint32_t cn[4] = {cn4.x & 0xffffu, cn4.x >> 16, cn4.y & 0xffffu, cn4.y >> 16};
           for (int g0 = 0; g0 < gc; g0 += kB) {
-            uint32_t dv[kB];
+            uint32_t dv[kB], fl[kB], cb[kB][4];
             uint2 pv[kB];
             rows4(g0, uc, dv, pv);
-            uint32_t fl[kB];
-#pragma unroll
+  #pragma unroll
             for (int k = 0; k < kB; ++k) {
               const int g = (g0 + k < gc) ? g0 + k : gc - 1;
               fl[k] = s_fl[g * NB + (uc >> 2)];
+  #pragma unroll
+              for (int j = 0; j < 4; ++j)
+                cb[k][j] = sp.has_chains ? s_fl[g * NB + ((cn[j] != 0xffffu ? cn[j] : (uint32_t)uc) >> 2)]
+                                         : 0u;
             }
-            int idx[kB][4], prs[kB][4];
-            bool ok[kB][4];
-            uint32_t lst[kB][4];
-#pragma unroll
+  #pragma unroll
             for (int k = 0; k < kB; ++k) {
               const int g = g0 + k;
-              const bool plan_ok = live && g < gc && !((rankedm >> (g & 63)) & 1ull);
-#pragma unroll
-              for (int j = 0; j < 4; ++j) {
-                const int d = (int)(int8_t)((dv[k] >> (8 * j)) & 0xffu);
-                const int pr = (int)(((j < 2 ? pv[k].x : pv[k].y) >> (16 * (j & 1))) & 0xffffu);
-                const uint32_t fb = fl[k] >> (2 * j);
-                const bool head = !((fb & 1u) && (av[j] & 64u));
-                const bool okd = (unsigned)d < (unsigned)D;
-                const bool inr = (unsigned)(pr - (int)(lv[j] & 0xffffu)) < (lv[j] >> 16);
-                ok[k][j] = plan_ok && head && okd && inr;
-                prs[k][j] = pr;
-                idx[k][j] = ok[k][j] ? (g * D + d) * M + (int)(av[j] & 63u) : 0;
+              if (g >= gc) break;
+              uint32_t nh = 0, nbad = 0, ninel = 0;
+              if (live) {
+                order_fast(g, uc, (int)(int8_t)(dv[k] & 0xffu), (int)(pv[k].x & 0xffffu), act4.x,
+                           alv4.x, cn[0], fl[k], cb[k][0], nh, nbad, ninel);
+                order_fast(g, uc + 1, (int)(int8_t)((dv[k] >> 8) & 0xffu), (int)(pv[k].x >> 16),
+                           act4.y, alv4.y, cn[1], fl[k] >> 2, cb[k][1], nh, nbad, ninel);
+                order_fast(g, uc + 2, (int)(int8_t)((dv[k] >> 16) & 0xffu), (int)(pv[k].y & 0xffffu),
+                           act4.z, alv4.z, cn[2], fl[k] >> 4, cb[k][2], nh, nbad, ninel);
+                order_fast(g, uc + 3, (int)(int8_t)(dv[k] >> 24), (int)(pv[k].y >> 16), act4.w,
+                           alv4.w, cn[3], fl[k] >> 6, cb[k][3], nh, nbad, ninel);
               }
+              order_flush4(g, nh, nbad, ninel);
             }
-#pragma unroll
-            for (int k = 0; k < kB; ++k)
-#pragma unroll
-              for (int j = 0; j < 4; ++j) lst[k][j] = s_last[idx[k][j]];
-#pragma unroll
-            for (int k = 0; k < kB; ++k)
-#pragma unroll
-              for (int j = 0; j < 4; ++j)
-                if (ok[k][j] && lst[k][j] == (uint32_t)prs[k][j] + 1u)
-                  atomicOr(&s_rec[(g0 + k) * N + prs[k][j]], kLast);
           }
         }
-      }
-      // ranked plans (and every plan without the vector path): by slot
-      for (int g = 0; g < gc; ++g) {
-        if (vec && !((rankedm >> g) & 1ull)) continue;
-        uint32_t* rec = s_rec + g * N;
-        const unsigned long long* mk = s_mask + g * D * NWA;
-        const uint32_t* lastp = s_last + g * D * M;
-        const int8_t* pdev = row_dev(g);
-        for (int sl = lane; sl < N; sl += 64) {
-          const uint32_t e = rec[sl];
-          // entries of empty slots are stale: the activation, its device and
-          // the model may be anything; only an occupied slot counts
-          const int u = (int)(e & 0xffffu);
-          const int d = u < N ? (int)pdev[u] : -1;
-          const int m = (int)((e >> 16) & 63u);
-          const bool occ = (unsigned)d < (unsigned)D && m < M &&
-                           ((mk[d * NWA + (sl >> 6)] >> (sl & 63)) & 1ull);
-          if (occ && lastp[d * M + m] == (uint32_t)sl + 1u) rec[sl] = e | kLast;
+      } else {
+        for (int g = 0; g < gc; ++g) {
+          const int8_t* pdev = row_dev(g);
+          const uint16_t* pprio = row_prio(g);
+          const uint8_t* pfl = s_fl + g * NB;
+          uint32_t nh = 0, nbad = 0, ninel = 0;
+          for (int u = lane; u < N; u += 64) {
+            const uint32_t fb = (uint32_t)pfl[u >> 2] >> ((u & 3) << 1);
+            const uint32_t c = t_cnext[u];
+            const uint32_t cbyte = pfl[(c != 0xffffu ? c : (uint32_t)u) >> 2];
+            order_fast(g, u, pdev[u], pprio[u], t_act[u], t_alv[u], c, fb, cbyte, nh, nbad, ninel);
+          }
+          if (ninel) atomicOr(&s_acc[g].status, (uint32_t)WF_ST_INELIGIBLE);
+          if (nbad) atomicOr(&s_acc[g].bad, 1u);
+          if (nh) atomicAdd(&s_acc[g].heads, nh);
         }
+      }
+      wave_sync();
+      // distinct slots claimed per plan: the union of its devices' masks
+      for (int i = lane; i < gc * NWA; i += 64) {
+        const int g = i / NWA, w = i - g * NWA;
+        unsigned long long x = 0ull;
+        for (int d = 0; d < D; ++d) x |= s_mask[(g * D + d) * NWA + w];
+        if (x) atomicAdd(&s_acc[g].claimed, (uint32_t)__popcll(x));
+      }
+      wave_sync();
+      // plans whose priorities are not a permutation of each level's heads'
+      // index range (one lane per plan)
+      uint64_t rankedm;
+      {
+        const PlanAcc& ag = s_acc[lane < gc ? lane : 0];  // G <= 64
+        const bool rk = lane < gc && (ag.bad != 0u || ag.heads != ag.claimed);
+        rankedm = __ballot(rk);
+      }
+      // general path: rank by (priority, index) within each level
+      for (uint64_t rm = rankedm; rm; rm &= rm - 1ull) {
+        const int g = __builtin_ctzll(rm);
+        const int8_t* pdev = row_dev(g);
+        const uint16_t* pprio = row_prio(g);
+        const uint8_t* pfl = s_fl + g * NB;
+        uint32_t* rec = s_rec + g * N;
+        unsigned long long* mk = s_mask + g * D * NWA;
+        uint32_t* lastp = s_last + g * D * M;
+        for (int i = lane; i < D * NWA; i += 64) mk[i] = 0ull;
+        if constexpr (!PAPER)
+          for (int i = lane; i < D * M; i += 64) lastp[i] = 0u;
+        wave_sync();
+        for (int u = lane; u < N; u += 64) {
+          const uint32_t a = t_act[u];
+          const int fb = pfl[u >> 2] >> ((u & 3) << 1);
+          if ((fb & 1) && (a & 64u)) continue;
+          const int d = pdev[u];
+          if ((unsigned)d >= (unsigned)D) continue;
+          const uint32_t lvw = t_alv[u];
+          const int lo = (int)(lvw & 0xffffu), hi = lo + (int)(lvw >> 16);
+          const int pu = pprio[u];
+          int slot = lo;
+          for (int j = lo; j < hi; ++j) {
+            if (fuse_bit(pfl, j) && (t_act[j] & 64u)) continue;
+            if ((unsigned)pdev[j] >= (unsigned)D) continue;
+            const int pj = pprio[j];
+            slot += (pj < pu) || (pj == pu && j < u);
+          }
+          const int c = t_cnext[u];
+          const uint32_t chain = (c != 0xffff && fuse_bit(pfl, c)) ? kChain : 0u;
+          rec[slot] = (uint32_t)u | ((a & 63u) << 16) | ((uint32_t)((fb >> 1) & 1) << 22) | chain |
+                      (chain ? kSlow : slow0);
+          atomicOr(&mk[d * NWA + (slot >> 6)], 1ull << (slot & 63));
+          if constexpr (!PAPER) atomicMax(&lastp[d * M + (int)(a & 63u)], (uint32_t)slot + 1u);
+        }
+        wave_sync();
+      }
+      if constexpr (NIBBLE) {
+        // mark each (device, model)'s last unit in its slot entry: the
+        // reclamation queues need only that bit, and last[] dies here
+        if (vec) {
+          // plans ordered by priority: re-derive each head's (device, slot,
+          // model) from its row; all loads first, then the marks
+          for (int base = 0; base < N; base += 256) {
+            const int u0 = base + 4 * lane;
+            const bool live = u0 < N;
+            const int uc = live ? u0 : 0;
+            const uint4 act4 = *reinterpret_cast<const uint4*>(t_act + uc);
+            const uint4 alv4 = *reinterpret_cast<const uint4*>(t_alv + uc);
+            const uint32_t av[4] = {act4.x, act4.y, act4.z, act4.w};
+            const uint32_t lv[4] = {alv4.x, alv4.y, alv4.z, alv4.w};
+            for (int g0 = 0; g0 < gc; g0 += kB) {
+              uint32_t dv[kB];
+              uint2 pv[kB];
+              rows4(g0, uc, dv, pv);
+              uint32_t fl[kB];
+  #pragma unroll
+              for (int k = 0; k < kB; ++k) {
+                const int g = (g0 + k < gc) ? g0 + k : gc - 1;
+                fl[k] = s_fl[g * NB + (uc >> 2)];
+              }
+              int idx[kB][4], prs[kB][4];
+              bool ok[kB][4];
+              uint32_t lst[kB][4];
+  #pragma unroll
+              for (int k = 0; k < kB; ++k) {
+                const int g = g0 + k;
+                const bool plan_ok = live && g < gc && !((rankedm >> (g & 63)) & 1ull);
+  #pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                  const int d = (int)(int8_t)((dv[k] >> (8 * j)) & 0xffu);
+                  const int pr = (int)(((j < 2 ? pv[k].x : pv[k].y) >> (16 * (j & 1))) & 0xffffu);
+                  const uint32_t fb = fl[k] >> (2 * j);
+                  const bool head = !((fb & 1u) && (av[j] & 64u));
+                  const bool okd = (unsigned)d < (unsigned)D;
+                  const bool inr = (unsigned)(pr - (int)(lv[j] & 0xffffu)) < (lv[j] >> 16);
+                  ok[k][j] = plan_ok && head && okd && inr;
+                  prs[k][j] = pr;
+                  idx[k][j] = ok[k][j] ? (g * D + d) * M + (int)(av[j] & 63u) : 0;
+                }
+              }
+  #pragma unroll
+              for (int k = 0; k < kB; ++k)
+  #pragma unroll
+                for (int j = 0; j < 4; ++j) lst[k][j] = s_last[idx[k][j]];
+  #pragma unroll
+              for (int k = 0; k < kB; ++k)
+  #pragma unroll
+                for (int j = 0; j < 4; ++j)
+                  if (ok[k][j] && lst[k][j] == (uint32_t)prs[k][j] + 1u)
+                    atomicOr(&s_rec[(g0 + k) * N + prs[k][j]], kLast);
+            }
+          }
+        }
+        // ranked plans (and every plan without the vector path): by slot
+        for (int g = 0; g < gc; ++g) {
+          if (vec && !((rankedm >> g) & 1ull)) continue;
+          uint32_t* rec = s_rec + g * N;
+          const unsigned long long* mk = s_mask + g * D * NWA;
+          const uint32_t* lastp = s_last + g * D * M;
+          const int8_t* pdev = row_dev(g);
+          for (int sl = lane; sl < N; sl += 64) {
+            const uint32_t e = rec[sl];
+            // entries of empty slots are stale: the activation, its device and
+            // the model may be anything; only an occupied slot counts
+            const int u = (int)(e & 0xffffu);
+            const int d = u < N ? (int)pdev[u] : -1;
+            const int m = (int)((e >> 16) & 63u);
+            const bool occ = (unsigned)d < (unsigned)D && m < M &&
+                             ((mk[d * NWA + (sl >> 6)] >> (sl & 63)) & 1ull);
+            if (occ && lastp[d * M + m] == (uint32_t)sl + 1u) rec[sl] = e | kLast;
+          }
+        }
+        wave_sync();
+      }
+    } else {
+      // ring layout: the order is built level by level during the walk; here
+      // only each (device, model)'s number of units (the reclamation order
+      // asks whether a copy has a remaining use on its device) and the
+      // plans with a unit head on no valid device
+      for (int it = lane; it < gc * N; it += 64) {
+        const int g = it / N, u = it - g * N;
+        const uint32_t a = t_act[u];
+        const uint32_t fb = (uint32_t)s_fl[g * NB + (u >> 2)] >> ((u & 3) << 1);
+        if ((fb & 1u) && (a & 64u)) continue;  // a fused chain member
+        const int dv = dev_all[(p0 + g) * N + u];
+        if ((unsigned)dv < (unsigned)D)
+          atomicAdd(&s_last[(g * D + dv) * M + (int)(a & 63u)], 1u);
+        else
+          atomicOr(&s_acc[g].status, (uint32_t)WF_ST_INELIGIBLE);
       }
       wave_sync();
     }
@@ -693,12 +728,12 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
     const int64_t pw = p0 + gme;
     bool act = act_plan;
     int d = d_me;
-    const uint32_t* mylast = s_last + (gme * D + d_me) * M;
+    uint32_t* mylast = s_last + (gme * D + d_me) * M;
     uint16_t* mystamp = s_stamp + (gme * D + d_me) * M;
     uint16_t* mynxu = s_nxu + (gme * D + d_me) * M;  // next use of each model (device index)
     const unsigned long long* mymask = s_mask + (gme * D + d_me) * NWA;
-    const uint32_t* myrec = s_rec + gme * N;
-    TB* myfin = s_fin + gme * N;
+    const uint32_t* myrec = s_rec + gme * RW;
+    TB* myfin = s_fin + gme * FS;
     const uint8_t* myfl = s_fl + gme * NB;
     // the lane's h-th device (h = 0, 1) and its table rows; a lane without
     // a second device keeps in-range pointers and stays inactive
@@ -898,30 +933,122 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
     if constexpr (NIBBLE) wave_sync();  // last[] (aliasing fin) is read above
     // every finish starts at 0: it accumulates the latest predecessor finish
     // before its level, then holds the activation's own finish
-    zero_bytes(reinterpret_cast<unsigned char*>(s_fin), G * N * (int)sizeof(TB), lane);
+    zero_bytes(reinterpret_cast<unsigned char*>(s_fin), G * FS * (int)sizeof(TB), lane);
     zero_bytes(reinterpret_cast<unsigned char*>(s_wfm), G * W * (int)sizeof(TB), lane);
     wave_sync();
 
+    // ring layout: fold the sinks of level L into their workflows' latest
+    // finish, and clear L's finishes when `clear` (its ring positions pass
+    // to level L + ring levels)
+    auto ring_fold = [&](int L, bool clear) {
+      const int base = (L % sp.ring_levels) * RW;
+      const int loL = t_loff[L], wL = t_loff[L + 1] - loL;
+      for (int it = lane; it < gc * RW; it += 64) {
+        const int g = it / RW, k = it - g * RW;
+        TB* f = s_fin + g * FS + base + k;
+        if (!PHI && k < wL) {
+          const uint32_t wf = t_rsnk[loL + k];
+          if (wf != 0xffffu) atomicMax(&s_wfm[g * W + (int)wf], *f);
+        }
+        if (clear) *f = (TB)0;
+      }
+    };
     for (int lv = 0; lv < sp.n_levels; ++lv) {
       const int lo = t_loff[lv], hi = t_loff[lv + 1];
       const int e0 = t_eoff[lv], e1 = t_eoff[lv + 1];
+      if constexpr (RING) {
+        // ---- the level leaving the ring, then this level's resource order
+        // (Eq. 10): a head's slot is its priority when the level's head
+        // priorities are distinct values in its index range, else its rank
+        // by (priority, index) ----
+        const int lold = lv - sp.ring_b - 1;
+        if (lold >= 0) ring_fold(lold, true);
+        const int width = hi - lo, jb = lo >> 6;
+        for (int i = lane; i < gc * D * NWA; i += 64) s_mask[i] = 0ull;
+        if (lane < gc) s_acc[lane].bad = 0u;
+        wave_sync();
+        auto head_entry = [&](int g, int u, uint32_t a, uint32_t fb) -> uint32_t {
+          const int c = t_cnext[u];
+          const bool chain = c != 0xffff && fuse_bit(s_fl + g * NB, c);
+          return (uint32_t)u | ((a & 63u) << 16) | ((fb & 2u) << 21) | (chain ? kChain | kSlow : slow0);
+        };
+        for (int it = lane; it < gc * width; it += 64) {
+          const int g = it / width, u = lo + (it - g * width);
+          const uint32_t a = t_act[u];
+          const uint32_t fb = (uint32_t)s_fl[g * NB + (u >> 2)] >> ((u & 3) << 1);
+          if ((fb & 1u) && (a & 64u)) continue;
+          const int dv = dev_all[(p0 + g) * N + u];
+          if ((unsigned)dv >= (unsigned)D) continue;
+          const int pr = prio_all[(p0 + g) * N + u];
+          if ((unsigned)(pr - lo) >= (unsigned)width) {
+            s_acc[g].bad = 1u;
+            continue;
+          }
+          s_rec[g * RW + (pr - lo)] = head_entry(g, u, a, fb);
+          const unsigned long long bit = 1ull << (pr & 63);
+          // a slot taken twice: the priorities are not distinct
+          if (atomicOr(&s_mask[(g * D + dv) * NWA + ((pr >> 6) - jb)], bit) & bit) s_acc[g].bad = 1u;
+        }
+        wave_sync();
+        // a slot claimed on two devices is a repeated priority as well
+        for (int i = lane; i < gc * NWA; i += 64) {
+          const int g = i / NWA, w = i - g * NWA;
+          unsigned long long x = 0ull;
+          bool dup = false;
+          for (int e = 0; e < D; ++e) {
+            const unsigned long long y = s_mask[(g * D + e) * NWA + w];
+            dup |= (x & y) != 0ull;
+            x |= y;
+          }
+          if (dup) s_acc[g].bad = 1u;
+        }
+        wave_sync();
+        const uint64_t rankedm = __ballot(lane < gc && s_acc[lane < gc ? lane : 0].bad != 0u);
+        for (uint64_t rm = rankedm; rm; rm &= rm - 1ull) {
+          const int g = __builtin_ctzll(rm);
+          const int8_t* pdev = dev_all + (p0 + g) * N;
+          const uint16_t* pprio = prio_all + (p0 + g) * N;
+          const uint8_t* pfl = s_fl + g * NB;
+          for (int i = lane; i < D * NWA; i += 64) s_mask[g * D * NWA + i] = 0ull;
+          wave_sync();
+          for (int u = lo + lane; u < hi; u += 64) {
+            const uint32_t a = t_act[u];
+            const uint32_t fb = (uint32_t)pfl[u >> 2] >> ((u & 3) << 1);
+            if ((fb & 1u) && (a & 64u)) continue;
+            const int dv = pdev[u];
+            if ((unsigned)dv >= (unsigned)D) continue;
+            const int pu = pprio[u];
+            int slot = lo;
+            for (int j = lo; j < hi; ++j) {
+              if (fuse_bit(pfl, j) && (t_act[j] & 64u)) continue;
+              if ((unsigned)pdev[j] >= (unsigned)D) continue;
+              const int pj = pprio[j];
+              slot += (pj < pu) || (pj == pu && j < u);
+            }
+            s_rec[g * RW + (slot - lo)] = head_entry(g, u, a, fb);
+            atomicOr(&s_mask[(g * D + dv) * NWA + ((slot >> 6) - jb)], 1ull << (slot & 63));
+          }
+          wave_sync();
+        }
+      }
       // ---- latest predecessor finish of the level's activations (Eq. 2):
       // one lane per incoming edge.  A fused chain member already holds its
       // own finish, which is later than its only predecessor's ----
       if (e1 > e0) {
+        const uint32_t* t_ed = RING ? reinterpret_cast<const uint32_t*>(tb + sp.t.redge) : t_edge;
         for (int e = e0 + lane; e < e1; e += 64) {
-          const uint32_t ed = t_edge[e];
+          const uint32_t ed = t_ed[e];
           const int src = (int)(ed & 0xffffu), dst = (int)(ed >> 16);
           for (int g0 = 0; g0 < gc; g0 += kB) {
             TB f[kB];
 #pragma unroll
             for (int k = 0; k < kB; ++k) {
               const int g = (g0 + k < gc) ? g0 + k : gc - 1;
-              f[k] = s_fin[g * N + src];
+              f[k] = s_fin[g * FS + src];
             }
 #pragma unroll
             for (int k = 0; k < kB; ++k)
-              if (g0 + k < gc) atomicMax(&s_fin[(g0 + k) * N + dst], f[k]);
+              if (g0 + k < gc) atomicMax(&s_fin[(g0 + k) * FS + dst], f[k]);
           }
         }
         wave_sync();
@@ -960,17 +1087,19 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
         const int width = hi - lo;
         const bool narrow = width <= 64;
         int j = lo >> 6;
+        // ring layout: the level's mask words and slot entries start at 0
+        const int jo = RING ? (lo >> 6) : 0, ro = RING ? lo : 0;
         unsigned long long bits, wnext = 0ull;
         if (narrow) {
           const int sh = lo & 63;
-          bits = mymask[j] >> sh;
-          if (sh + width > 64) bits |= mymask[j + 1] << (64 - sh);  // then j + 1 <= j1
+          bits = mymask[j - jo] >> sh;
+          if (sh + width > 64) bits |= mymask[j + 1 - jo] << (64 - sh);  // then j + 1 <= j1
           if (width < 64) bits &= (1ull << width) - 1ull;
         } else {
           // wider: the current word's remaining bits, and the next word
           // already loaded
-          bits = mymask[j] & (~0ull << (lo & 63));
-          if (j < j1) wnext = mymask[j + 1] & ((j + 1 == j1) ? hmask : ~0ull);
+          bits = mymask[j - jo] & (~0ull << (lo & 63));
+          if (j < j1) wnext = mymask[j + 1 - jo] & ((j + 1 == j1) ? hmask : ~0ull);
         }
         // the device's next slot in the level; -1 when there is none, -2 for
         // a trip with no unit (an exhausted word followed by an empty one)
@@ -985,7 +1114,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
           bits = adv ? wnext : bits;
           j += adv ? 1 : 0;
           const int jn = j + 1 <= j1 ? j + 1 : j1;
-          const unsigned long long wl2 = mymask[jn] & ((jn == j1) ? hmask : ~0ull);
+          const unsigned long long wl2 = mymask[jn - jo] & ((jn == j1) ? hmask : ~0ull);
           wnext = adv ? (j < j1 ? wl2 : 0ull) : wnext;
           const int sl = (j << 6) + __builtin_ctzll(bits | (1ull << 63));
           const bool have = bits != 0ull;
@@ -996,7 +1125,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
         // keeps every address below in range
         auto entry = [&](int sl) -> uint32_t {
           const uint32_t keep = (uint32_t)~(sl >> 31);  // all ones for a real slot
-          const uint32_t raw = myrec[(int)((uint32_t)sl & keep)];
+          const uint32_t raw = myrec[(int)((uint32_t)(sl - ro) & keep)];
           return (raw & keep) | ((uint32_t)lo & ~keep);
         };
         auto fetch = [&](int sl, uint32_t meta, UnitPre<TT>& p) {
@@ -1007,7 +1136,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
           p.lat = (int32_t)r.x;
           p.mem = (int32_t)r.y;
           p.arrv = TO::words(r.z, r.w);
-          p.rtv = TO::load(myfin + u);
+          p.rtv = TO::load(myfin + fpos((int)u));
           p.lw = lw_d[__umul24(m, (uint32_t)D)];
           if constexpr (PHI) {
             if constexpr (std::is_same<TT, uint32_t>::value)
@@ -1049,7 +1178,9 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
           while (cand) {
             const int m2 = __builtin_ctzll(cand);
             cand &= cand - 1;
-            const uint32_t alive = mylast[m2] > (uint32_t)slot + 1u;
+            // a remaining use on the device: a later slot (ring layout: a
+            // unit not yet walked)
+            const uint32_t alive = RING ? (uint32_t)(mylast[m2] != 0u) : (uint32_t)(mylast[m2] > (uint32_t)slot + 1u);
             const uint32_t key = (alive << 16) | mystamp[m2];
             if (key < best) {
               best = key;
@@ -1063,6 +1194,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
             const int u = (int)(X.meta & 0xffffu);
             const int m = (int)((X.meta >> 16) & 63u);
             const uint64_t mbit = 1ull << m;
+            if constexpr (RING) --mylast[m];  // units of m on the device still to walk
             // copies reclaimed for this unit (schedule output), accumulated
             // in place so that nothing stays live in registers without one
             const bool rec_on = has_sched && sched.reclaimed_models != nullptr;
@@ -1266,13 +1398,13 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
             }
             freet = f;
             if (!(X.meta & kSlow)) {
-              myfin[u] = TO::bits(f);
+              myfin[fpos(u)] = TO::bits(f);
             } else {
               TT t = s;
               for (int v = u;;) {
                 const TT tv =
                     TO::add(t, ud_d[__umul24((uint32_t)v, (uint32_t)D)].x);
-                myfin[v] = TO::bits(tv);
+                myfin[fpos(v)] = TO::bits(tv);
                 if (has_sched) {
                   sched.start_us[pw * N + v] = sp.origin + TO::i64(t);
                   sched.finish_us[pw * N + v] = sp.origin + TO::i64(tv);
@@ -1370,8 +1502,15 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
     }
     }
     // a workflow's completion is the latest finish among its activations
-    // without a successor in the same workflow (not part of the ranking key)
-    for (int i = lane; i < (PHI ? 0 : sp.S); i += 64) {
+    // without a successor in the same workflow (not part of the ranking key);
+    // the ring layout folded every level but its last ring_b + 1 during the
+    // walk
+    if constexpr (RING) {
+      if (!PHI)
+        for (int L = sp.n_levels - sp.ring_b - 1 > 0 ? sp.n_levels - sp.ring_b - 1 : 0; L < sp.n_levels; ++L)
+          ring_fold(L, false);
+    }
+    for (int i = lane; i < ((PHI || RING) ? 0 : sp.S); i += 64) {
       const uint32_t sk = t_sink[i];
       const int src = (int)(sk & 0xffffu), wf = (int)(sk >> 16);
       for (int g0 = 0; g0 < gc; g0 += kB) {
@@ -1463,12 +1602,12 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   }
 }
 
-template <typename TT, bool TAB_LDS, int QB, bool WAVE_GLOBAL, bool SEARCH, bool PHI, bool SCHED>
+template <typename TT, bool TAB_LDS, int QB, int PLACE, bool SEARCH, bool PHI, bool SCHED>
 hipError_t launch_variant(const ScoreParams& sp, const int8_t* dev, const uint16_t* prio,
                           const uint8_t* flags, int64_t n_plans, OutRec<PHI>* out,
                           const wf_plan_sched& s, int has, const SearchArgs& sa,
                           hipStream_t stream) {
-  auto k = score_plans<TT, TAB_LDS, QB, WAVE_GLOBAL, SEARCH, PHI, SCHED>;
+  auto k = score_plans<TT, TAB_LDS, QB, PLACE, SEARCH, PHI, SCHED>;
   (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k),
                             hipFuncAttributeMaxDynamicSharedMemorySize, sp.lds_bytes);
   hipLaunchKernelGGL(k, dim3(sp.grid), dim3(64 * sp.waves), sp.lds_bytes, stream, sp, dev, prio,
@@ -1480,14 +1619,19 @@ template <typename TT, int QB, bool SEARCH, bool PHI, bool SCHED>
 hipError_t launch_place(const ScoreParams& sp, const int8_t* dev, const uint16_t* prio,
                         const uint8_t* flags, int64_t n_plans, OutRec<PHI>* out,
                         const wf_plan_sched& s, int has, const SearchArgs& sa, hipStream_t stream) {
-  if (sp.wave_global)
-    return launch_variant<TT, false, QB, true, SEARCH, PHI, SCHED>(sp, dev, prio, flags, n_plans,
-                                                                   out, s, has, sa, stream);
-  if (sp.tab_in_lds)
-    return launch_variant<TT, true, QB, false, SEARCH, PHI, SCHED>(sp, dev, prio, flags, n_plans,
-                                                                   out, s, has, sa, stream);
-  return launch_variant<TT, false, QB, false, SEARCH, PHI, SCHED>(sp, dev, prio, flags, n_plans,
+  if constexpr ((QB == 0 || QB == -2) && !SEARCH) {
+    if (sp.ring)
+      return launch_variant<TT, false, QB, 2, SEARCH, PHI, SCHED>(sp, dev, prio, flags, n_plans,
                                                                   out, s, has, sa, stream);
+  }
+  if (sp.wave_global)
+    return launch_variant<TT, false, QB, 1, SEARCH, PHI, SCHED>(sp, dev, prio, flags, n_plans,
+                                                                out, s, has, sa, stream);
+  if (sp.tab_in_lds)
+    return launch_variant<TT, true, QB, 0, SEARCH, PHI, SCHED>(sp, dev, prio, flags, n_plans,
+                                                               out, s, has, sa, stream);
+  return launch_variant<TT, false, QB, 0, SEARCH, PHI, SCHED>(sp, dev, prio, flags, n_plans,
+                                                              out, s, has, sa, stream);
 }
 
 template <typename TT, bool SEARCH, bool PHI, bool SCHED>

@@ -29,7 +29,7 @@ import numpy as np
 
 __all__ = [
     "Window", "PlanBatch", "CONFIGS", "make_config", "make_window",
-    "make_plans", "random_window", "random_plans", "pack_flags",
+    "make_plans", "random_window", "random_deep_window", "random_plans", "pack_flags",
     "unpack_flags", "save_npz", "load_npz",
 ]
 
@@ -465,6 +465,37 @@ def random_window(rng: np.random.Generator, n_wf: int = 2, nodes=(1, 6), n_dev: 
             if len(ps) == 1 and rng.random() < same_model_bias:
                 models[j] = models[ps[0]]
         b.add_workflow(par, models)
+    return _random_tables(b, rng, n_dev, n_models, q_inel, cap_range, w_range, mem_range, lat_range,
+                          load_range, arrivals, free0, resident, name)
+
+
+def random_deep_window(rng: np.random.Generator, n_wf: int = 1, n_levels=(20, 60), width=(1, 12),
+                       span: int = 2, p_edge: float = 0.3, n_dev: int = 8, n_models: int = 20,
+                       same_model_bias: float = 0.5, **kw) -> Window:
+    """Deep layered workflows (many topological levels, edges reaching back
+    up to ``span`` levels, a parent in the previous level for every node
+    past the first, same-model parent->child chains), with the tables of
+    random_window (its keyword arguments)."""
+    b = _Builder()
+    for _ in range(n_wf):
+        L = int(rng.integers(n_levels[0], n_levels[1] + 1))
+        sizes = [int(rng.integers(width[0], width[1] + 1)) for _ in range(L)]
+        par = _layered_parents(rng, sizes, p_edge, span=span, force_parent=True)
+        k = sum(sizes)
+        models = rng.integers(0, n_models, size=k)
+        for j, ps in enumerate(par):
+            if len(ps) == 1 and rng.random() < same_model_bias:
+                models[j] = models[ps[0]]
+        b.add_workflow(par, models)
+    args = dict(q_inel=0.1, cap_range=(8000, 40000), w_range=(1000, 12000), mem_range=(100, 4000),
+                lat_range=(1, 1000), load_range=(0, 5000), arrivals=True, free0=True, resident=True,
+                name="random-deep")
+    args.update(kw)
+    return _random_tables(b, rng, n_dev, n_models, **args)
+
+
+def _random_tables(b, rng, n_dev, n_models, q_inel, cap_range, w_range, mem_range, lat_range,
+                   load_range, arrivals, free0, resident, name) -> Window:
     act_wf, act_model, off, idx, W = b.finish()
     n, D, M = len(act_wf), n_dev, n_models
     cap = rng.integers(cap_range[0], cap_range[1], size=D, endpoint=True).astype(np.int32)

@@ -1,7 +1,7 @@
 """Windows too large for LDS: each wave's per-activation arrays live in the
 HBM scratch area and its per-(device, model) arrays stay in LDS.  Every
 reclamation mode (4-bit queue, scan, the paper's order, batch limits) on
-such a window against the oracle: score records, schedules, reclaimed copies,
+such a window (the scans with the ring layout switched off) against the oracle: score records, schedules, reclaimed copies,
 ranking keys and generated candidates, bytewise."""
 import os
 import re
@@ -67,6 +67,7 @@ def test_scores_schedules_reclaims(ctx, name, capfd, monkeypatch):
     P, N, D = plans.n_plans, win.n_act, win.n_dev
     log(f"[hbm] {name}: N={N} D={D} M={win.n_models} P={P}")
     monkeypatch.setenv("WF_PLAN_VERBOSE", "1")
+    monkeypatch.setenv("WF_PLAN_RING", "off")  # the scan modes would take the ring layout
     ctx.wf_plan_upload_window(win)
     where, wave, lds_part, lds_wg, mode = layout_line(capfd.readouterr().err)
     assert where == "hbm+scratch" and mode == CASES[name][4], (where, mode)
@@ -141,10 +142,11 @@ def test_random_mid_windows(ctx, seed, capfd, monkeypatch):
         assert np.array_equal(a.cpu().numpy()[ok][:, :b.shape[1]], b[ok]), (seed, label)
 
 
-def test_two_contexts_two_streams():
+def test_two_contexts_two_streams(monkeypatch):
     """Concurrent scoring takes one context per stream: each context owns its
     scratch area, so two HBM-layout launches in flight at once both match
     the oracle."""
+    monkeypatch.setenv("WF_PLAN_RING", "off")
     win, plans = big_window("scan")
     P = plans.n_plans
     ref = oracle.score(win, plans, threads=THREADS)
