@@ -445,9 +445,9 @@ int ring_layout(const HostWindow& h, const wfp::ScoreParams& sp, int G, int tsz,
   o.rec = take((size_t)G * sp.ring_w * 4);
   o.mask = take((size_t)G * h.D * nwl * 8);
   o.acc = take((size_t)G * sizeof(wfp::PlanAcc));
-  o.last = take(dm * 4);
+  o.last = take(dm * 2);
   o.stamp = take(dm * 2);
-  o.fin = take((size_t)G * sp.ring_levels * sp.ring_w * tsz);
+  o.fin = take((size_t)G * sp.ring_size * tsz);
   o.wfm = take((size_t)G * std::max(1, h.W) * tsz);
   o.hstate = take(h.D > 64 ? 2 * 64 * sizeof(wfp::HState) : 0);
   o.hold = take(h.rcap.empty() ? 0 : (size_t)G * h.D * 8);
@@ -604,16 +604,22 @@ wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, bool time64_req, Im
       for (int32_t k = h.pred_off[v]; k < h.pred_off[v + 1]; ++k)
         rb = std::max(rb, lvl[v] - lvl[h.pred_idx[k]]);
     }
-    const int64_t levels = (int64_t)ra + rb + 1;
-    if (levels * h.wmax <= 65535) {
+    // positions are activation indices mod the ring size: the most
+    // activations held by levels lv - ring_b .. lv + ring_a for any lv
+    int64_t size = 1;
+    for (int32_t l = 0; l < h.n_levels; ++l) {
+      const int32_t a0 = std::max(0, l - rb), a1 = std::min(h.n_levels, l + ra + 1);
+      size = std::max<int64_t>(size, h.level_off[a1] - h.level_off[a0]);
+    }
+    if (size <= 65535) {
       sp.ring_ok = 1;
-      sp.ring_levels = (int)levels;
+      sp.ring_size = (int)size;
       sp.ring_w = h.wmax;
       sp.ring_a = ra;
       sp.ring_b = rb;
       std::vector<uint16_t> rpos((size_t)N), rsnk((size_t)N);
       for (int32_t i = 0; i < N; ++i) {
-        rpos[i] = (uint16_t)((lvl[i] % levels) * h.wmax + (i - h.level_off[lvl[i]]));
+        rpos[i] = (uint16_t)(i % size);
         rsnk[i] = has_wf_succ[i] ? (uint16_t)0xffff : (uint16_t)h.act_wf[i];
       }
       std::vector<uint32_t> redge((size_t)std::max(E, 1), 0);
@@ -758,6 +764,7 @@ wf_status plan_launch(wf_plan_ctx* ctx, const HostWindow& h, bool search, wfp::S
   sp.ring = 0;
   const char* ring_env = std::getenv("WF_PLAN_RING");
   const bool ring_off = ring_env && std::strcmp(ring_env, "off") == 0;
+  const bool ring_force = ring_env && std::strcmp(ring_env, "on") == 0;
   if (!search && !ring_off && sp.ring_ok && (sp.nibble == 0 || sp.nibble == -2)) {
     const int nwl = (sp.ring_w + 63) / 64 + 1;
     const double cur = sp.wave_global ? hbm_lanes : best;
@@ -781,7 +788,7 @@ wf_status plan_launch(wf_plan_ctx* ctx, const HostWindow& h, bool search, wfp::S
         ro = o;
       }
     }
-    if (rbest > 0 && (rbest > cur || (sp.wave_global && rbest >= cur))) {
+    if (rbest > 0 && (ring_force || rbest > cur || (sp.wave_global && rbest >= cur))) {
       sp.ring = 1;
       sp.wave_global = 0;
       sp.tab_in_lds = 0;
@@ -1159,9 +1166,9 @@ wf_status wf_plan_upload_window(wf_plan_ctx* ctx, const wf_window_desc* w) {
                  sp.t.bytes, sp.wo.bytes, sp.wave_global ? sp.wo.split : sp.wo.bytes, sp.lds_bytes, sp.nibble == 32 ? "queue32" : sp.nibble == 64 ? "queue64" : sp.nibble == -1 ? "paper-scan" :
                  sp.nibble == -2 ? "batch-scan" : sp.nibble == -3 ? "batch-paper-scan" : "scan");
   if (std::getenv("WF_PLAN_VERBOSE") && sp.ring)
-    std::fprintf(stderr, "[wf_plan] ring of recent levels: %d levels (%d ahead, %d behind) x %d "
-                 "activations, %d mask words per device\n", sp.ring_levels, sp.ring_a, sp.ring_b,
-                 sp.ring_w, sp.nwa);
+    std::fprintf(stderr, "[wf_plan] ring of recent levels: %d positions (%d levels ahead, %d "
+                 "behind), widest level %d, %d mask words per device\n", sp.ring_size, sp.ring_a,
+                 sp.ring_b, sp.ring_w, sp.nwa);
   if (std::getenv("WF_PLAN_VERBOSE") && dw.lean.ok)
     std::fprintf(stderr, "[wf_plan] lean kernel: G=%d waves/wg=%d grid=%d tables=%d B wave=%d B lds/wg=%d\n",
                  dw.lean.G, dw.lean.waves, dw.lean.grid, dw.lean.t.bytes, dw.lean.wo.bytes,

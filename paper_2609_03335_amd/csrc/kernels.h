@@ -39,8 +39,7 @@ struct TabOffsets {
   int rcap;    // i32 [M]    replica cap of each model (windows with caps)
   // ring of recent levels (ScoreParams::ring): finishes are kept only for
   // the levels a unit can still reach, at ring positions
-  int rpos;    // u16 [N]    ring position: (level mod ring levels) * widest level +
-               //            index inside the level
+  int rpos;    // u16 [N]    ring position: activation index mod ring size
   int redge;   // u32 [E]    as edge, with ring positions instead of activation ids
   int rsnk;    // u16 [N]    workflow of an activation without successor in its
                //            workflow, else 0xffff
@@ -59,7 +58,7 @@ struct WaveOffsets {
   int acc;     // PlanAcc [G]
   int stamp;   // u16 [G*D][M]     last use of each model (general reclamation only)
                // (ring layout: rec holds [G][widest level] entries of the current
-               // level, mask [G][D][NWA] its words, last the count of each
+               // level, mask [G][D][NWA] its words, last the u16 count of each
                // (device, model)'s units not yet walked, fin [G][ring size])
   int rows;    // generated candidates only: int8 [G][N] devices, then u16 [G][N]
                //                  priorities at rows + rows_prio; they live in fin's
@@ -123,12 +122,14 @@ struct ScoreParams {
                               // times saturated (status bit kRescore of the first pass)
   // ring of recent levels (deep or wide windows, scan reclamation, plan rows
   // from HBM): the slot entries and device masks of the current level only,
-  // and the finishes of ring_levels consecutive levels; ring_a levels ahead
-  // (a fused chain's members get their finish with the chain head) and
-  // ring_b behind (the longest edge, in levels)
+  // and the finishes of the levels from ring_b behind the current one (the
+  // longest edge, in levels) to ring_a ahead (a fused chain's members get
+  // their finish with the chain head), at positions index mod ring_size:
+  // ring_size is the most activations any such span of levels holds, so
+  // the live finishes never share a position
   int ring;                   // 1: this launch uses the ring layout
   int ring_ok;                // 1: the window admits it (tables rpos, redge, rsnk built)
-  int ring_levels, ring_w, ring_a, ring_b;
+  int ring_size, ring_w, ring_a, ring_b;  // ring_w: the widest level
 };
 
 // Byte offsets inside one wave's LDS region of the lean kernel (lean.hip):

@@ -310,7 +310,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   // ring layout: slot entries per plan (the widest level), finishes per plan
   // (the ring), a finish's position
   const int RW = RING ? sp.ring_w : N;
-  const int FS = RING ? sp.ring_levels * sp.ring_w : N;
+  const int FS = RING ? sp.ring_size : N;
   auto fpos = [&](int u) -> int {
     if constexpr (RING) return (int)t_rpos[u];
     else return u;
@@ -417,7 +417,8 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
     }
     // last[] (each (device, model)'s last slot) serves the other reclamation
     // orders only
-    if constexpr (!PAPER) zero_bytes(reinterpret_cast<unsigned char*>(s_last), G * D * M * 4, lane);
+    if constexpr (!PAPER)
+      zero_bytes(reinterpret_cast<unsigned char*>(s_last), G * D * M * (RING ? 2 : 4), lane);
     zero_bytes(reinterpret_cast<unsigned char*>(s_mask), G * D * NWA * 8, lane);
     if (lane < G) {
       PlanAcc a0;
@@ -706,10 +707,13 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
         const uint32_t fb = (uint32_t)s_fl[g * NB + (u >> 2)] >> ((u & 3) << 1);
         if ((fb & 1u) && (a & 64u)) continue;  // a fused chain member
         const int dv = dev_all[(p0 + g) * N + u];
-        if ((unsigned)dv < (unsigned)D)
-          atomicAdd(&s_last[(g * D + dv) * M + (int)(a & 63u)], 1u);
-        else
+        if ((unsigned)dv < (unsigned)D) {
+          // 16-bit counts, two to a word (a count stays below 2^16)
+          const int ci = (g * D + dv) * M + (int)(a & 63u);
+          atomicAdd(&s_last[ci >> 1], 1u << ((ci & 1) << 4));
+        } else {
           atomicOr(&s_acc[g].status, (uint32_t)WF_ST_INELIGIBLE);
+        }
       }
       wave_sync();
     }
@@ -729,6 +733,8 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
     bool act = act_plan;
     int d = d_me;
     uint32_t* mylast = s_last + (gme * D + d_me) * M;
+    // ring layout: the lane's 16-bit counts of units still to walk per model
+    uint16_t* mycnt = reinterpret_cast<uint16_t*>(s_last) + (gme * D + d_me) * M;
     uint16_t* mystamp = s_stamp + (gme * D + d_me) * M;
     uint16_t* mynxu = s_nxu + (gme * D + d_me) * M;  // next use of each model (device index)
     const unsigned long long* mymask = s_mask + (gme * D + d_me) * NWA;
@@ -742,6 +748,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
       act = act_plan && d < D;
       const int dd = d < D ? d : d_me;
       mylast = s_last + (gme * D + dd) * M;
+      mycnt = reinterpret_cast<uint16_t*>(s_last) + (gme * D + dd) * M;
       mystamp = s_stamp + (gme * D + dd) * M;
       mynxu = s_nxu + (gme * D + dd) * M;
       mymask = s_mask + (gme * D + dd) * NWA;
@@ -937,20 +944,20 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
     zero_bytes(reinterpret_cast<unsigned char*>(s_wfm), G * W * (int)sizeof(TB), lane);
     wave_sync();
 
-    // ring layout: fold the sinks of level L into their workflows' latest
-    // finish, and clear L's finishes when `clear` (its ring positions pass
-    // to level L + ring levels)
-    auto ring_fold = [&](int L, bool clear) {
-      const int base = (L % sp.ring_levels) * RW;
+    // ring layout: fold the finishes of level L's activations without a
+    // successor in their workflow into the workflow's latest finish (L
+    // leaves the ring), or clear L's positions (L enters it)
+    auto ring_level = [&](int L, bool clear) {
       const int loL = t_loff[L], wL = t_loff[L + 1] - loL;
-      for (int it = lane; it < gc * RW; it += 64) {
-        const int g = it / RW, k = it - g * RW;
-        TB* f = s_fin + g * FS + base + k;
-        if (!PHI && k < wL) {
-          const uint32_t wf = t_rsnk[loL + k];
+      for (int it = lane; it < gc * wL; it += 64) {
+        const int g = it / wL, u = loL + (it - g * wL);
+        TB* f = s_fin + g * FS + (int)t_rpos[u];
+        if (clear) {
+          *f = (TB)0;
+        } else {
+          const uint32_t wf = t_rsnk[u];
           if (wf != 0xffffu) atomicMax(&s_wfm[g * W + (int)wf], *f);
         }
-        if (clear) *f = (TB)0;
       }
     };
     for (int lv = 0; lv < sp.n_levels; ++lv) {
@@ -961,8 +968,14 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
         // (Eq. 10): a head's slot is its priority when the level's head
         // priorities are distinct values in its index range, else its rank
         // by (priority, index) ----
-        const int lold = lv - sp.ring_b - 1;
-        if (lold >= 0) ring_fold(lold, true);
+        const int lold = lv - sp.ring_b - 1, lnew = lv + sp.ring_a;
+        if (lold >= 0) {
+          if (!PHI) ring_level(lold, false);
+          if (lnew < sp.n_levels) {
+            wave_sync();  // the positions may be shared
+            ring_level(lnew, true);
+          }
+        }
         const int width = hi - lo, jb = lo >> 6;
         for (int i = lane; i < gc * D * NWA; i += 64) s_mask[i] = 0ull;
         if (lane < gc) s_acc[lane].bad = 0u;
@@ -1180,7 +1193,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
             cand &= cand - 1;
             // a remaining use on the device: a later slot (ring layout: a
             // unit not yet walked)
-            const uint32_t alive = RING ? (uint32_t)(mylast[m2] != 0u) : (uint32_t)(mylast[m2] > (uint32_t)slot + 1u);
+            const uint32_t alive = RING ? (uint32_t)(mycnt[m2] != 0u) : (uint32_t)(mylast[m2] > (uint32_t)slot + 1u);
             const uint32_t key = (alive << 16) | mystamp[m2];
             if (key < best) {
               best = key;
@@ -1194,7 +1207,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
             const int u = (int)(X.meta & 0xffffu);
             const int m = (int)((X.meta >> 16) & 63u);
             const uint64_t mbit = 1ull << m;
-            if constexpr (RING) --mylast[m];  // units of m on the device still to walk
+            if constexpr (RING) --mycnt[m];  // units of m on the device still to walk
             // copies reclaimed for this unit (schedule output), accumulated
             // in place so that nothing stays live in registers without one
             const bool rec_on = has_sched && sched.reclaimed_models != nullptr;
@@ -1508,7 +1521,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
     if constexpr (RING) {
       if (!PHI)
         for (int L = sp.n_levels - sp.ring_b - 1 > 0 ? sp.n_levels - sp.ring_b - 1 : 0; L < sp.n_levels; ++L)
-          ring_fold(L, false);
+          ring_level(L, false);
     }
     for (int i = lane; i < ((PHI || RING) ? 0 : sp.S); i += 64) {
       const uint32_t sk = t_sink[i];
