@@ -686,8 +686,10 @@ wf_status plan_launch(wf_plan_ctx* ctx, const HostWindow& h, bool search, wfp::S
   const int lds_cu = std::min(ctx->lds_per_cu, 160 * 1024);
   const int lds_blk = std::min(ctx->lds_per_block, lds_cu);
   const int gmax = std::max(1, 64 / D);
-  // the paper reclamation order keeps every load time in LDS
-  sp.wg_ld = (sp.nibble == -1 || sp.nibble == -3) ? (int)align_up((size_t)h.M * D * 4, 16) : 0;
+  // the workgroup's copies in LDS: every (model, device) load time (the
+  // paper reclamation order) and every model's weights
+  sp.wg_ld = ((sp.nibble == -1 || sp.nibble == -3) ? (int)align_up((size_t)h.M * D * 4, 16) : 0) +
+             (int)align_up((size_t)h.M * 4, 16);
   double best = -1.0;
   for (int tl = 1; tl >= 0; --tl) {
     const int tab_lds = (tl ? sp.t.bytes : 0) + sp.wg_ld;
@@ -758,9 +760,14 @@ wf_status plan_launch(wf_plan_ctx* ctx, const HostWindow& h, bool search, wfp::S
     sp.wo = o;
   }
   // the ring of recent levels: per-plan state of the current level and the
-  // levels a unit can still reach, all in LDS.  Taken over the LDS layout
-  // when it keeps more walk lanes in flight, and over the HBM layout when
-  // it keeps as many.
+  // levels a unit can still reach, all in LDS.  Taken over the HBM layout
+  // when it keeps as many walk lanes in flight, and over the LDS layout
+  // only when that keeps fewer than half as many: building the order level
+  // by level costs more per plan than the LDS layout's one sweep.
+  // Measured on MI355X: 4,096 activations in 128 levels 12.5 -> 2.55 ms
+  // (against the HBM layout); 256 activations with batch limits or replica
+  // caps 11.2 -> 13.0 and 8.4 -> 10.9 ms with the ring at 1.3x the LDS
+  // layout's lanes.
   sp.ring = 0;
   const char* ring_env = std::getenv("WF_PLAN_RING");
   const bool ring_off = ring_env && std::strcmp(ring_env, "off") == 0;
@@ -774,9 +781,9 @@ wf_status plan_launch(wf_plan_ctx* ctx, const HostWindow& h, bool search, wfp::S
     for (int G = gmax; G >= 1; --G) {
       wfp::WaveOffsets o{};
       const int wb = ring_layout(h, sp, G, tsz, nwl, o);
-      const int waves = std::min(8, lds_blk / std::max(wb, 1));
+      const int waves = std::min(8, (lds_blk - sp.wg_ld) / std::max(wb, 1));
       if (waves < 1) continue;
-      const int lds_wg = waves * wb;
+      const int lds_wg = sp.wg_ld + waves * wb;
       const int wg_per_cu = std::max(1, lds_cu / lds_wg);
       const double score = (double)std::min(G * D, 64) * std::min(std::min(32, wg_per_cu * waves), 8);
       if (score > rbest) {
@@ -788,7 +795,7 @@ wf_status plan_launch(wf_plan_ctx* ctx, const HostWindow& h, bool search, wfp::S
         ro = o;
       }
     }
-    if (rbest > 0 && (ring_force || rbest > cur || (sp.wave_global && rbest >= cur))) {
+    if (rbest > 0 && (ring_force || (sp.wave_global ? rbest >= cur : rbest >= 2.0 * cur))) {
       sp.ring = 1;
       sp.wave_global = 0;
       sp.tab_in_lds = 0;

@@ -108,9 +108,10 @@ struct ScoreParams {
   int wave_global;            // 1: per-wave regions live in HBM scratch (windows too big for LDS)
   unsigned char* scratch;     // per-wave regions when wave_global
   int lds_bytes;              // dynamic LDS per workgroup
-  int wg_ld;                  // paper reclamation order: bytes of the workgroup's copy of
-                              // every (model, device) load time, after the table image
-                              // when that is in LDS and before the waves' regions
+  int wg_ld;                  // bytes of the workgroup's copies of every (model, device)
+                              // load time (paper reclamation order only) and of every
+                              // model's weights, after the table image when that is in
+                              // LDS and before the waves' regions
   int grid;                   // workgroups (persistent)
   int time64;                 // 1: fp64 times, 0: uint32 times
   int nibble;                 // reclamation queue width in bits (32 or 64), 0: scan,

@@ -288,7 +288,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   const int32_t* t_loff = reinterpret_cast<const int32_t*>(tb + sp.t.loff);
   const uint4* t_ud = reinterpret_cast<const uint4*>(tb + sp.t.ud);
   const int2* t_lw = reinterpret_cast<const int2*>(tb + sp.t.lw);
-  const int32_t* t_wmib = reinterpret_cast<const int32_t*>(tb + sp.t.wmib);
+  const int32_t* t_wmib = reinterpret_cast<const int32_t*>(tb + sp.t.wmib);  // (LDS below)
   // paper reclamation order: the workgroup's copy of every (model, device)
   // load time, read per candidate victim
   uint32_t* wg_ld = reinterpret_cast<uint32_t*>(lds + wave_base);
@@ -296,6 +296,14 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
     const int2* lw = reinterpret_cast<const int2*>(tb + sp.t.lw);
     for (int i = tid; i < M * D; i += blockDim.x) wg_ld[i] = (uint32_t)lw[i].x;
     __syncthreads();
+  }
+  // every model's weights, read per reclamation: the workgroup's copy in LDS
+  // (after the paper order's load times) when the tables stay in HBM
+  if constexpr (!TAB_LDS) {
+    int32_t* wg_wm = reinterpret_cast<int32_t*>(lds + wave_base + (PAPER ? ((M * D * 4 + 15) & ~15) : 0));
+    for (int i = tid; i < M; i += blockDim.x) wg_wm[i] = t_wmib[i];
+    __syncthreads();
+    t_wmib = wg_wm;
   }
   wave_base += sp.wg_ld;
   const int32_t* t_cap = reinterpret_cast<const int32_t*>(tb + sp.t.cap);

@@ -105,7 +105,7 @@ def test_deep_workload(ctx, capfd):
 def deep_case(seed):
     rng = np.random.default_rng(77_000 + seed)
     D = [4, 8, 16, 6][seed % 4]
-    win = W.random_deep_window(rng, n_wf=1 + seed % 3, n_levels=(30, 70), width=(3, 12 + 3 * (seed % 3)),
+    win = W.random_deep_window(rng, n_wf=1 + seed % 3, n_levels=(40, 90), width=(4, 14 + 3 * (seed % 3)),
                                span=1 + seed % 3, p_edge=[0.3, 0.08][seed % 2], n_dev=D,
                                n_models=[20, 24, 40][seed % 3])
     if seed % 4 == 1:
@@ -147,7 +147,7 @@ def test_ring_time_modes(ctx, capfd, kind):
     """fp64 times, and uint32 times with the fp64 rescoring pass."""
     rng = np.random.default_rng(5 if kind == "fp64" else 6)
     lat = (1, 1 << 30) if kind == "fp64" else (1 << 22, 1 << 23)
-    win = W.random_deep_window(rng, n_levels=(30, 40), width=(2, 8), n_dev=8, n_models=20,
+    win = W.random_deep_window(rng, n_levels=(60, 90), width=(6, 16), n_dev=8, n_models=20,
                                lat_range=lat, load_range=(0, 1 << 20))
     plans = W.random_plans(win, 2000, rng, prio_mode="perm")
     assert upload(ctx, win, capfd)
