@@ -30,7 +30,7 @@ HBM_PEAK_GBS = 8000.0  # MI355X published HBM3E bandwidth
 # packed fp32 as two more)
 VALU_PEAK_TLANE = 256 * 64 * 2.4e9 / 1e12
 CSRC = os.path.join(ROOT, "paper_2609_03335_amd", "csrc")
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "score_plans_traffic.json")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "score_lean_traffic.json")
 
 
 def algorithmic_bytes_per_plan(n_act: int) -> int:
