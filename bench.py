@@ -46,7 +46,7 @@ def kernel_source_digest() -> str:
     import hashlib
     from paper_2609_03335_amd import build
     h = hashlib.sha256()
-    for name in ("score_kernel.h", "score.hip", "lean.hip", "kernels.h", "host.hip"):
+    for name in ("score_kernel.h", "mutation.h", "score.hip", "lean.hip", "kernels.h", "host.hip"):
         with open(os.path.join(CSRC, name), "rb") as f:
             h.update(f.read())
     h.update(" ".join(build.HIP_FLAGS).encode())

@@ -937,6 +937,9 @@ void plan_lean(wf_plan_ctx* ctx, const HostWindow& h, const wfp::ScoreParams& sp
   lp.checked = checked ? 1 : 0;
   lp.qbits = sp.nibble;
   lp.ok = 1;
+  // generated candidates: each plan's changed sites live in its finish
+  // entries until the walk
+  lp.search_ok = N >= 1 + 4 * wfp::kLeanMaxMut ? 1 : 0;
 }
 
 // Launch parameters of one pass over n plans: the grid never exceeds the
@@ -1216,7 +1219,7 @@ wf_status wf_plan_score_batch(wf_plan_ctx* ctx, const int8_t* dev, const uint16_
     const int64_t groups = (n_plans + lp.G - 1) / lp.G;
     const int64_t wgs = (groups + lp.waves - 1) / lp.waves;
     if (wgs < lp.grid) lp.grid = (int)wgs;
-    e = wfp::launch_score_lean(dw.sp, lp, dev, prio, flags, n_plans, scores,
+    e = wfp::launch_score_lean(dw.sp, lp, dev, prio, flags, n_plans, scores, nullptr,
                                static_cast<hipStream_t>(hip_stream));
     if (e == hipSuccess && dw.checked)
       e = wfp::launch_score(fit_grid(dw.sp64, n_plans), dev, prio, flags, n_plans, scores, nullptr,
@@ -1256,7 +1259,8 @@ static wf_status search_args(wf_plan_ctx* ctx, const int8_t* dev, const uint16_t
 static wfp::SearchArgs search_params(const wf_plan_ctx* ctx, int32_t mode, uint64_t seed,
                                      int32_t n_mut, int64_t first) {
   return wfp::SearchArgs{seed, n_mut, mode, first, ctx->host.D, ctx->dw.rule_best,
-                         ctx->dw.rule_pf};
+                         ctx->dw.rule_pf,
+                         reinterpret_cast<const unsigned long long*>(ctx->dw.sp.tab + ctx->dw.sp.t.elig)};
 }
 
 wf_status wf_plan_search_batch(wf_plan_ctx* ctx, const int8_t* dev, const uint16_t* prio,
@@ -1272,10 +1276,28 @@ wf_status wf_plan_search_batch(wf_plan_ctx* ctx, const int8_t* dev, const uint16
   hipError_t e = hipSetDevice(ctx->device);
   if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
   const wfp::SearchArgs sa = search_params(ctx, mode, seed, n_mut, first);
-  e = two_pass(ctx->dw, true, n_candidates, [&](const wfp::ScoreParams& sp) {
-    return wfp::launch_score(sp, dev, prio, flags, n_candidates, scores, nullptr, &sa,
-                             static_cast<hipStream_t>(hip_stream));
-  });
+  const DeviceWindow& dw = ctx->dw;
+  const char* force = std::getenv("WF_PLAN_KERNEL");
+  const bool general = force && std::strcmp(force, "general") == 0;
+  if (dw.lean.ok && dw.lean.search_ok && n_mut <= wfp::kLeanMaxMut && !general) {
+    // the lean kernel generates the candidates as the incumbent plus their
+    // changed sites; then (times not proven below 2^32) the general fp64
+    // pass over the groups holding a candidate whose times saturated
+    wfp::LeanParams lp = dw.lean;
+    const int64_t groups = (n_candidates + lp.G - 1) / lp.G;
+    const int64_t wgs = (groups + lp.waves - 1) / lp.waves;
+    if (wgs < lp.grid) lp.grid = (int)wgs;
+    e = wfp::launch_score_lean(dw.sp, lp, dev, prio, flags, n_candidates, scores, &sa,
+                               static_cast<hipStream_t>(hip_stream));
+    if (e == hipSuccess && dw.checked)
+      e = wfp::launch_score(fit_grid(dw.sp64_search, n_candidates), dev, prio, flags, n_candidates,
+                            scores, nullptr, &sa, static_cast<hipStream_t>(hip_stream));
+  } else {
+    e = two_pass(dw, true, n_candidates, [&](const wfp::ScoreParams& sp) {
+      return wfp::launch_score(sp, dev, prio, flags, n_candidates, scores, nullptr, &sa,
+                               static_cast<hipStream_t>(hip_stream));
+    });
+  }
   (void)hipSetDevice(prev);
   if (e != hipSuccess) return hip_fail(ctx, e, "launching the scoring kernel");
   return WF_OK;

@@ -184,11 +184,22 @@ struct LeanParams {
   const unsigned char* tab;  // the lean table image in HBM
   LeanTab t;
   LeanOffsets wo;  // wave regions follow the image's LDS part
+  int search_ok;   // 1: it also generates candidates (their changed sites fit the
+                   // finish array's storage)
 };
 
+// Generated candidates served by the lean kernel: at most this many
+// mutations each (a candidate is the incumbent plus at most 2 changed sites
+// per mutation).
+constexpr int kLeanMaxMut = 8;
+
+struct SearchArgs;
+
+// Scores of plans read from HBM, or (search) of candidates generated around
+// the incumbent rows dev/prio/flags.
 hipError_t launch_score_lean(const ScoreParams& sp, const LeanParams& lp, const int8_t* dev,
                              const uint16_t* prio, const uint8_t* flags, int64_t n_plans,
-                             wf_plan_score* scores, hipStream_t stream);
+                             wf_plan_score* scores, const SearchArgs* search, hipStream_t stream);
 
 // Internal status bit of a uint32-time pass: some time of the plan reached
 // 2^32 - 1 (saturated), so an fp64 pass rescores it.  Never left in a record
@@ -227,6 +238,9 @@ struct SearchArgs {
   // its prefetch bit ([N][2] 64-bit masks)
   const int8_t* rule_best;
   const unsigned long long* rule_pf;
+  // each activation's eligible devices ([N][2] 64-bit masks; the general
+  // kernel reads its own table image's copy)
+  const unsigned long long* elig;
 };
 
 // Scores plans read from dev/prio/flags ([P][N] rows), or -- with search --

@@ -6,6 +6,11 @@
 // results as the general kernel of score_kernel.h, with only the code this
 // configuration needs: 16-bit slot entries, no schedule, key, search,
 // batch-limit or fp64 paths, and the per-unit tables of the walk in LDS.
+// With SEARCH the plans are candidates generated around an incumbent (at
+// most kLeanMaxMut mutations each): a candidate is kept as the incumbent's
+// rows plus the sites its mutations changed (in the finish array's storage,
+// dead until the walk), and the order sweep patches the incumbent's row
+// words with them, so no candidate row exists in HBM or LDS.
 //
 // A persistent grid of waves loops over groups of G plans; lane (g, d) =
 // (lane / D, lane % D) owns device d of plan g.  Per group:
@@ -27,9 +32,55 @@
 #include <type_traits>
 
 #include "kernels.h"
+#include "mutation.h"
 
 namespace wfp {
 namespace {
+
+// A candidate as the incumbent's rows plus the changed sites: per plan a
+// count, then 2 words per site (activation | priority << 16, device).
+constexpr int kPatchWords = 1 + 4 * kLeanMaxMut;
+
+struct PatchRows {
+  uint32_t* p;             // this plan's count and sites
+  const int8_t* idev;      // incumbent rows
+  const uint16_t* iprio;
+  uint8_t* rf;             // this plan's flag row (staged)
+  __device__ __forceinline__ int find(int i) const {
+    const int n = (int)p[0];
+    for (int k = 0; k < n; ++k)
+      if ((int)(p[1 + 2 * k] & 0xffffu) == i) return k;
+    return -1;
+  }
+  __device__ __forceinline__ int site(int i) {
+    int k = find(i);
+    if (k < 0) {
+      k = (int)p[0];
+      p[1 + 2 * k] = (uint32_t)i | ((uint32_t)iprio[i] << 16);
+      p[2 + 2 * k] = (uint32_t)(int32_t)idev[i];
+      p[0] = (uint32_t)(k + 1);
+    }
+    return k;
+  }
+  __device__ __forceinline__ int dev(int i) const {
+    const int k = find(i);
+    return k >= 0 ? (int)(int32_t)p[2 + 2 * k] : (int)idev[i];
+  }
+  __device__ __forceinline__ void set_dev(int i, int d) { p[2 + 2 * site(i)] = (uint32_t)d; }
+  __device__ __forceinline__ void swap_prio(int i, int j) {
+    const int ki = site(i), kj = site(j);
+    const uint32_t pi = p[1 + 2 * ki] >> 16, pj = p[1 + 2 * kj] >> 16;
+    p[1 + 2 * ki] = (uint32_t)i | (pj << 16);
+    p[1 + 2 * kj] = (uint32_t)j | (pi << 16);
+  }
+  __device__ __forceinline__ void toggle_flag(int i, int bit) {
+    rf[i >> 2] ^= (uint8_t)(1u << (((i & 3) << 1) + bit));
+  }
+  __device__ __forceinline__ void set_prefetch(int i, bool on) {
+    const uint8_t b = (uint8_t)(2u << ((i & 3) << 1));
+    rf[i >> 2] = on ? (uint8_t)(rf[i >> 2] | b) : (uint8_t)(rf[i >> 2] & ~b);
+  }
+};
 
 struct LeanAcc {
   uint32_t status;
@@ -95,12 +146,12 @@ __device__ __forceinline__ uint32_t tadd(uint32_t a, uint32_t b) {
 
 __device__ __forceinline__ uint32_t umax(uint32_t a, uint32_t b) { return a > b ? a : b; }
 
-template <bool CHECKED, int QB>
+template <bool CHECKED, int QB, bool SEARCH>
 __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
                                                   const int8_t* __restrict__ dev_all,
                                                   const uint16_t* __restrict__ prio_all,
                                                   const uint8_t* __restrict__ flags_all, int64_t P,
-                                                  wf_plan_score* __restrict__ scores) {
+                                                  wf_plan_score* __restrict__ scores, SearchArgs sa) {
   using QT = std::conditional_t<QB == 32, uint32_t, uint64_t>;
   constexpr QT kOnes = (QT)0x1111111111111111ull, kHigh = (QT)0x8888888888888888ull;
   extern __shared__ __align__(16) unsigned char lds[];
@@ -140,6 +191,7 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
   uint32_t* s_fin = reinterpret_cast<uint32_t*>(wl + lp.wo.fin);
   uint32_t* s_wfm = reinterpret_cast<uint32_t*>(wl + lp.wo.wfm);
   LeanAcc* s_acc = reinterpret_cast<LeanAcc*>(wl + lp.wo.acc);
+  uint32_t* s_pat = s_fin;  // generated candidates' changed sites (until the walk)
 
   const int g_me = lane / D;
   const int d_me = lane - g_me * D;
@@ -178,7 +230,19 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
     const int64_t p0 = grp * G;
     const int gc = (int)((P - p0) < G ? (P - p0) : G);
 
-    stage_rows(s_fl, flags_all + p0 * NB, gc * NB, lane);
+    if constexpr (SEARCH) {
+      // every plan starts as the incumbent; lane g then applies candidate
+      // g's mutations to its changed sites and flag row
+      for (int i = lane; i < gc * NB; i += 64) s_fl[i] = flags_all[i - (i / NB) * NB];
+      lsync();
+      if (lane < gc) {
+        PatchRows rows{s_pat + lane * kPatchWords, dev_all, prio_all, s_fl + lane * NB};
+        rows.p[0] = 0u;
+        mutate_rows((uint64_t)(sa.first + p0 + lane), sa, N, sa.elig, t_alv, rows);
+      }
+    } else {
+      stage_rows(s_fl, flags_all + p0 * NB, gc * NB, lane);
+    }
     zero16(reinterpret_cast<unsigned char*>(s_last), G * D * M * 4, lane);
     zero16(reinterpret_cast<unsigned char*>(s_mask), G * D * NWA * 8, lane);
     if (lane < G) {
@@ -187,6 +251,43 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
       s_acc[lane] = a0;
     }
     lsync();
+
+    // device and priority of activation u in plan g
+    auto rdev = [&](int g, int u) -> int {
+      if constexpr (SEARCH) {
+        const PatchRows rows{s_pat + g * kPatchWords, dev_all, prio_all, nullptr};
+        return rows.dev(u);
+      } else {
+        return dev_all[(p0 + g) * N + u];
+      }
+    };
+    auto rprio = [&](int g, int u) -> int {
+      if constexpr (SEARCH) {
+        const PatchRows rows{s_pat + g * kPatchWords, dev_all, prio_all, nullptr};
+        const int k = rows.find(u);
+        return k >= 0 ? (int)(rows.p[1 + 2 * k] >> 16) : (int)prio_all[u];
+      } else {
+        return prio_all[(p0 + g) * N + u];
+      }
+    };
+    // the incumbent's row words at activations uc .. uc + 3 with candidate
+    // g's changed sites written in
+    auto patch4 = [&](int g, int uc, uint32_t& dv, uint2& pv) {
+      const uint32_t* pp = s_pat + g * kPatchWords;
+      const int n = (int)pp[0];
+      for (int k = 0; k < n; ++k) {
+        const uint32_t e0 = pp[1 + 2 * k];
+        const uint32_t o = (e0 & 0xffffu) - (uint32_t)uc;
+        if (o < 4u) {
+          const uint32_t sh = o << 3, ph = (o & 1u) << 4, pr = e0 >> 16;
+          dv = (dv & ~(0xffu << sh)) | ((pp[2 + 2 * k] & 0xffu) << sh);
+          if (o < 2u)
+            pv.x = (pv.x & ~(0xffffu << ph)) | (pr << ph);
+          else
+            pv.y = (pv.y & ~(0xffffu << ph)) | (pr << ph);
+        }
+      }
+    };
 
     // ---- resource order (Eq. 10), first try: slot = priority ----
     auto order_one = [&](int g, int u, int d, int pr, uint32_t a, uint32_t lvw, uint32_t c,
@@ -227,6 +328,9 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
         const uint4 act4 = *reinterpret_cast<const uint4*>(t_act + uc);
         const uint4 alv4 = *reinterpret_cast<const uint4*>(t_alv + uc);
         const uint2 cn4 = *reinterpret_cast<const uint2*>(t_cnext + uc);
+        // (generated candidates: the incumbent's words, the same for every plan)
+        const uint32_t idv = SEARCH ? *reinterpret_cast<const uint32_t*>(dev_all + uc) : 0u;
+        const uint2 ipv = SEARCH ? *reinterpret_cast<const uint2*>(prio_all + uc) : make_uint2(0u, 0u);
         const uint32_t cn[4] = {cn4.x & 0xffffu, cn4.x >> 16, cn4.y & 0xffffu, cn4.y >> 16};
         for (int g0 = 0; g0 < gc; g0 += kB) {
           uint32_t dv[kB], fl[kB], cb[kB][4];
@@ -234,7 +338,11 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
 #pragma unroll
           for (int k = 0; k < kB; ++k) {
             const int g = (g0 + k < gc) ? g0 + k : gc - 1;
-            if (pre) {
+            if constexpr (SEARCH) {
+              dv[k] = idv;
+              pv[k] = ipv;
+              patch4(g, uc, dv[k], pv[k]);
+            } else if (pre) {
               dv[k] = dvp[k];
               pv[k] = pvp[k];
             } else {
@@ -273,15 +381,14 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
       }
     } else {
       for (int g = 0; g < gc; ++g) {
-        const int8_t* pdev = dev_all + (p0 + g) * N;
-        const uint16_t* pprio = prio_all + (p0 + g) * N;
         const uint8_t* pfl = s_fl + g * NB;
         uint32_t nh = 0, nbad = 0, ninel = 0;
         for (int u = lane; u < N; u += 64) {
           const uint32_t fb = (uint32_t)pfl[u >> 2] >> ((u & 3) << 1);
           const uint32_t c = t_cnext[u];
           const uint32_t cbyte = pfl[(c != 0xffffu ? c : (uint32_t)u) >> 2];
-          order_one(g, u, pdev[u], pprio[u], t_act[u], t_alv[u], c, fb, cbyte, nh, nbad, ninel);
+          order_one(g, u, rdev(g, u), rprio(g, u), t_act[u], t_alv[u], c, fb, cbyte, nh, nbad,
+                    ninel);
         }
         if (ninel) atomicOr(&s_acc[g].status, (uint32_t)WF_ST_INELIGIBLE);
         if (nbad) atomicOr(&s_acc[g].bad, 1u);
@@ -306,8 +413,6 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
     // index range: rank by (priority, index) within each level
     for (uint64_t rm = rankedm; rm; rm &= rm - 1ull) {
       const int g = __builtin_ctzll(rm);
-      const int8_t* pdev = dev_all + (p0 + g) * N;
-      const uint16_t* pprio = prio_all + (p0 + g) * N;
       const uint8_t* pfl = s_fl + g * NB;
       uint16_t* rec = s_rec + g * N;
       unsigned long long* mk = s_mask + g * D * NWA;
@@ -319,16 +424,16 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
         const uint32_t a = t_act[u];
         const uint32_t fb = (uint32_t)pfl[u >> 2] >> ((u & 3) << 1);
         if ((fb & 1u) && (a & 64u)) continue;
-        const int d = pdev[u];
+        const int d = rdev(g, u);
         if ((unsigned)d >= (unsigned)D) continue;
         const uint32_t lvw = t_alv[u];
         const int lo = (int)(lvw & 0xffffu), hi = lo + (int)(lvw >> 16);
-        const int pu = pprio[u];
+        const int pu = rprio(g, u);
         int slot = lo;
         for (int j = lo; j < hi; ++j) {
           if (fuse_of(pfl, j) && (t_act[j] & 64u)) continue;
-          if ((unsigned)pdev[j] >= (unsigned)D) continue;
-          const int pj = pprio[j];
+          if ((unsigned)rdev(g, j) >= (unsigned)D) continue;
+          const int pj = rprio(g, j);
           slot += (pj < pu) || (pj == pu && j < u);
         }
         const int c = t_cnext[u];
@@ -682,35 +787,43 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
   }
 }
 
-template <bool CHECKED, int QB>
+template <bool CHECKED, int QB, bool SEARCH>
 hipError_t launch_lean_variant(const ScoreParams& sp, const LeanParams& lp, const int8_t* dev,
                                const uint16_t* prio, const uint8_t* flags, int64_t n_plans,
-                               wf_plan_score* scores, hipStream_t stream) {
-  auto k = score_lean<CHECKED, QB>;
+                               wf_plan_score* scores, const SearchArgs& sa, hipStream_t stream) {
+  auto k = score_lean<CHECKED, QB, SEARCH>;
   (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k),
                             hipFuncAttributeMaxDynamicSharedMemorySize, lp.lds_bytes);
   hipLaunchKernelGGL(k, dim3(lp.grid), dim3(64 * lp.waves), lp.lds_bytes, stream, sp, lp, dev, prio,
-                     flags, n_plans, scores);
+                     flags, n_plans, scores, sa);
   return hipGetLastError();
 }
 
-template <bool CHECKED>
+template <bool CHECKED, bool SEARCH>
 hipError_t launch_lean_q(const ScoreParams& sp, const LeanParams& lp, const int8_t* dev,
                          const uint16_t* prio, const uint8_t* flags, int64_t n_plans,
-                         wf_plan_score* scores, hipStream_t stream) {
+                         wf_plan_score* scores, const SearchArgs& sa, hipStream_t stream) {
   if (lp.qbits == 32)
-    return launch_lean_variant<CHECKED, 32>(sp, lp, dev, prio, flags, n_plans, scores, stream);
-  return launch_lean_variant<CHECKED, 64>(sp, lp, dev, prio, flags, n_plans, scores, stream);
+    return launch_lean_variant<CHECKED, 32, SEARCH>(sp, lp, dev, prio, flags, n_plans, scores, sa,
+                                                     stream);
+  return launch_lean_variant<CHECKED, 64, SEARCH>(sp, lp, dev, prio, flags, n_plans, scores, sa,
+                                                   stream);
 }
 
 }  // namespace
 
 hipError_t launch_score_lean(const ScoreParams& sp, const LeanParams& lp, const int8_t* dev,
                              const uint16_t* prio, const uint8_t* flags, int64_t n_plans,
-                             wf_plan_score* scores, hipStream_t stream) {
+                             wf_plan_score* scores, const SearchArgs* search, hipStream_t stream) {
+  const SearchArgs sa = search ? *search : SearchArgs{};
+  if (search) {
+    if (lp.checked)
+      return launch_lean_q<true, true>(sp, lp, dev, prio, flags, n_plans, scores, sa, stream);
+    return launch_lean_q<false, true>(sp, lp, dev, prio, flags, n_plans, scores, sa, stream);
+  }
   if (lp.checked)
-    return launch_lean_q<true>(sp, lp, dev, prio, flags, n_plans, scores, stream);
-  return launch_lean_q<false>(sp, lp, dev, prio, flags, n_plans, scores, stream);
+    return launch_lean_q<true, false>(sp, lp, dev, prio, flags, n_plans, scores, sa, stream);
+  return launch_lean_q<false, false>(sp, lp, dev, prio, flags, n_plans, scores, sa, stream);
 }
 
 }  // namespace wfp

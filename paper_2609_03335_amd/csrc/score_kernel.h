@@ -34,6 +34,7 @@
 #include <type_traits>
 
 #include "kernels.h"
+#include "mutation.h"
 
 namespace wfp {
 namespace {
@@ -116,73 +117,12 @@ __device__ __forceinline__ int fuse_bit(const uint8_t* fl, int v) {
   return (fl[v >> 2] >> ((v & 3) << 1)) & 1;
 }
 
-// Philox4x32-10 (Salmon, Moraes, Dror and Shaw, SC'11): ten rounds of the
-// Philox-4x32 bijection of the counter x, the key bumped by the Weyl
-// constants after every round.
-__device__ __forceinline__ void philox4x32_10(uint32_t x[4], uint32_t k0, uint32_t k1) {
-#pragma unroll
-  for (int round = 0; round < 10; ++round) {
-    const uint32_t a = x[0], c = x[2];
-    x[0] = __umulhi(0xCD9E8D57u, c) ^ x[1] ^ k0;
-    x[1] = 0xCD9E8D57u * c;
-    x[2] = __umulhi(0xD2511F53u, a) ^ x[3] ^ k1;
-    x[3] = 0xD2511F53u * a;
-    k0 += 0x9E3779B9u;
-    k1 += 0xBB67AE85u;
-  }
-}
-
-// Turns rows (dev, prio, flags) holding the incumbent into candidate c: the
-// n_mut mutations drawn from Philox4x32-10 with counter (c, t) and the
-// seed as key -- another eligible device for activation i, a swap of two
-// priorities inside i's level, or a toggled fuse / prefetch bit of i.  With
-// the rules (Algorithm 1, Sec. 3.5) the device is i's best feasible binding
-// and the prefetch bit is what PlanPrefetch decides on i's current device.
+// Candidate c from the incumbent's rows held whole.
 __device__ __forceinline__ void mutate(uint64_t c, const SearchArgs& sa, int N,
                                        const unsigned long long* elig, const uint32_t* alv,
                                        int8_t* rd, uint16_t* rp, uint8_t* rf) {
-  if (N <= 0) return;
-  for (int t = 0; t < sa.n_mut; ++t) {
-    uint32_t x[4] = {(uint32_t)c, (uint32_t)(c >> 32), (uint32_t)t, 0u};
-    philox4x32_10(x, (uint32_t)sa.seed, (uint32_t)(sa.seed >> 32));
-    const int i = (int)__umulhi(x[1], (uint32_t)N);
-    const uint32_t kind = x[0] >> 30;
-    if (sa.mode == WF_SEARCH_RULES && (kind == 0u || kind == 3u)) {
-      if (kind == 0u) {
-        const int b = sa.rule_best[i];
-        if (b >= 0) rd[i] = (int8_t)b;
-      } else {
-        const int d = rd[i];
-        if (d >= 0 && d < sa.D) {
-          const uint8_t bit = (uint8_t)(2u << ((i & 3) << 1));
-          if ((sa.rule_pf[2 * i + (d >> 6)] >> (d & 63)) & 1ull) rf[i >> 2] |= bit;
-          else rf[i >> 2] &= (uint8_t)~bit;
-        }
-      }
-    } else if (kind == 0u) {
-      unsigned long long e = elig[2 * i], e1 = elig[2 * i + 1];
-      const uint32_t n0 = (uint32_t)__popcll(e), n = n0 + (uint32_t)__popcll(e1);
-      if (n) {
-        uint32_t k = __umulhi(x[2], n);
-        int base = 0;
-        if (k >= n0) {
-          k -= n0;
-          e = e1;
-          base = 64;
-        }
-        for (; k; --k) e &= e - 1ull;
-        rd[i] = (int8_t)(base + __builtin_ctzll(e));
-      }
-    } else if (kind == 1u) {
-      const uint32_t lvw = alv[i];
-      const int j = (int)(lvw & 0xffffu) + (int)__umulhi(x[2], lvw >> 16);
-      const uint16_t pi = rp[i];
-      rp[i] = rp[j];
-      rp[j] = pi;
-    } else {
-      rf[i >> 2] ^= (uint8_t)(1u << (((i & 3) << 1) + (kind == 3u ? 1 : 0)));
-    }
-  }
+  FullRows rows{rd, rp, rf};
+  mutate_rows(c, sa, N, elig, alv, rows);
 }
 
 // slot entry: activation | model << 16 | prefetch << 22 | has fused successor << 23 |
