@@ -942,6 +942,15 @@ void plan_lean(wf_plan_ctx* ctx, const HostWindow& h, const wfp::ScoreParams& sp
   lp.search_ok = N >= 1 + 4 * wfp::kLeanMaxMut ? 1 : 0;
 }
 
+// The lean kernel's launch over n plans: the grid never exceeds the groups
+// there are.
+wfp::LeanParams lean_grid(wfp::LeanParams lp, int64_t n) {
+  const int64_t groups = (n + lp.G - 1) / lp.G;
+  const int64_t wgs = (groups + lp.waves - 1) / lp.waves;
+  if (wgs < lp.grid) lp.grid = (int)wgs;
+  return lp;
+}
+
 // Launch parameters of one pass over n plans: the grid never exceeds the
 // groups there are.
 wfp::ScoreParams fit_grid(wfp::ScoreParams sp, int64_t n) {
@@ -1219,7 +1228,7 @@ wf_status wf_plan_score_batch(wf_plan_ctx* ctx, const int8_t* dev, const uint16_
     const int64_t groups = (n_plans + lp.G - 1) / lp.G;
     const int64_t wgs = (groups + lp.waves - 1) / lp.waves;
     if (wgs < lp.grid) lp.grid = (int)wgs;
-    e = wfp::launch_score_lean(dw.sp, lp, dev, prio, flags, n_plans, scores, nullptr,
+    e = wfp::launch_score_lean(dw.sp, lp, dev, prio, flags, n_plans, scores, nullptr, false,
                                static_cast<hipStream_t>(hip_stream));
     if (e == hipSuccess && dw.checked)
       e = wfp::launch_score(fit_grid(dw.sp64, n_plans), dev, prio, flags, n_plans, scores, nullptr,
@@ -1277,9 +1286,7 @@ wf_status wf_plan_search_batch(wf_plan_ctx* ctx, const int8_t* dev, const uint16
   if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
   const wfp::SearchArgs sa = search_params(ctx, mode, seed, n_mut, first);
   const DeviceWindow& dw = ctx->dw;
-  const char* force = std::getenv("WF_PLAN_KERNEL");
-  const bool general = force && std::strcmp(force, "general") == 0;
-  if (dw.lean.ok && dw.lean.search_ok && n_mut <= wfp::kLeanMaxMut && !general) {
+  if (dw.lean.ok && dw.lean.search_ok && n_mut <= wfp::kLeanMaxMut) {
     // the lean kernel generates the candidates as the incumbent plus their
     // changed sites; then (times not proven below 2^32) the general fp64
     // pass over the groups holding a candidate whose times saturated
@@ -1287,7 +1294,7 @@ wf_status wf_plan_search_batch(wf_plan_ctx* ctx, const int8_t* dev, const uint16
     const int64_t groups = (n_candidates + lp.G - 1) / lp.G;
     const int64_t wgs = (groups + lp.waves - 1) / lp.waves;
     if (wgs < lp.grid) lp.grid = (int)wgs;
-    e = wfp::launch_score_lean(dw.sp, lp, dev, prio, flags, n_candidates, scores, &sa,
+    e = wfp::launch_score_lean(dw.sp, lp, dev, prio, flags, n_candidates, scores, &sa, false,
                                static_cast<hipStream_t>(hip_stream));
     if (e == hipSuccess && dw.checked)
       e = wfp::launch_score(fit_grid(dw.sp64_search, n_candidates), dev, prio, flags, n_candidates,
@@ -1396,10 +1403,22 @@ wf_status wf_plan_score_keys(wf_plan_ctx* ctx, const int8_t* dev, const uint16_t
   (void)hipGetDevice(&prev);
   hipError_t e = hipSetDevice(ctx->device);
   if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
-  e = two_pass(ctx->dw, false, n_plans, [&](const wfp::ScoreParams& sp) {
-    return wfp::launch_score_keys(sp, dev, prio, flags, n_plans, keys, nullptr,
-                                  static_cast<hipStream_t>(hip_stream));
-  });
+  const DeviceWindow& dw = ctx->dw;
+  if (dw.lean.ok) {
+    // the lean kernel's key mode, then the general fp64 pass over the groups
+    // holding a plan whose uint32 times saturated
+    const wfp::LeanParams lp = lean_grid(dw.lean, n_plans);
+    e = wfp::launch_score_lean(dw.sp, lp, dev, prio, flags, n_plans, keys, nullptr, true,
+                               static_cast<hipStream_t>(hip_stream));
+    if (e == hipSuccess && dw.checked)
+      e = wfp::launch_score_keys(fit_grid(dw.sp64, n_plans), dev, prio, flags, n_plans, keys,
+                                 nullptr, static_cast<hipStream_t>(hip_stream));
+  } else {
+    e = two_pass(dw, false, n_plans, [&](const wfp::ScoreParams& sp) {
+      return wfp::launch_score_keys(sp, dev, prio, flags, n_plans, keys, nullptr,
+                                    static_cast<hipStream_t>(hip_stream));
+    });
+  }
   (void)hipSetDevice(prev);
   if (e != hipSuccess) return hip_fail(ctx, e, "launching the ranking-key kernel");
   return WF_OK;
@@ -1418,10 +1437,20 @@ wf_status wf_plan_search_keys(wf_plan_ctx* ctx, const int8_t* dev, const uint16_
   hipError_t e = hipSetDevice(ctx->device);
   if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
   const wfp::SearchArgs sa = search_params(ctx, mode, seed, n_mut, first);
-  e = two_pass(ctx->dw, true, n_candidates, [&](const wfp::ScoreParams& sp) {
-    return wfp::launch_score_keys(sp, dev, prio, flags, n_candidates, keys, &sa,
-                                  static_cast<hipStream_t>(hip_stream));
-  });
+  const DeviceWindow& dw = ctx->dw;
+  if (dw.lean.ok && dw.lean.search_ok && n_mut <= wfp::kLeanMaxMut) {
+    const wfp::LeanParams lp = lean_grid(dw.lean, n_candidates);
+    e = wfp::launch_score_lean(dw.sp, lp, dev, prio, flags, n_candidates, keys, &sa, true,
+                               static_cast<hipStream_t>(hip_stream));
+    if (e == hipSuccess && dw.checked)
+      e = wfp::launch_score_keys(fit_grid(dw.sp64_search, n_candidates), dev, prio, flags,
+                                 n_candidates, keys, &sa, static_cast<hipStream_t>(hip_stream));
+  } else {
+    e = two_pass(dw, true, n_candidates, [&](const wfp::ScoreParams& sp) {
+      return wfp::launch_score_keys(sp, dev, prio, flags, n_candidates, keys, &sa,
+                                    static_cast<hipStream_t>(hip_stream));
+    });
+  }
   (void)hipSetDevice(prev);
   if (e != hipSuccess) return hip_fail(ctx, e, "launching the ranking-key kernel");
   return WF_OK;

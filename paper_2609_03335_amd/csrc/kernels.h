@@ -195,11 +195,12 @@ constexpr int kLeanMaxMut = 8;
 
 struct SearchArgs;
 
-// Scores of plans read from HBM, or (search) of candidates generated around
-// the incumbent rows dev/prio/flags.
+// Scores (wf_plan_score [n]) or, with keys, ranking keys (wf_plan_key [n])
+// of plans read from HBM, or (search) of candidates generated around the
+// incumbent rows dev/prio/flags.
 hipError_t launch_score_lean(const ScoreParams& sp, const LeanParams& lp, const int8_t* dev,
                              const uint16_t* prio, const uint8_t* flags, int64_t n_plans,
-                             wf_plan_score* scores, const SearchArgs* search, hipStream_t stream);
+                             void* out, const SearchArgs* search, bool keys, hipStream_t stream);
 
 // Internal status bit of a uint32-time pass: some time of the plan reached
 // 2^32 - 1 (saturated), so an fp64 pass rescores it.  Never left in a record

@@ -82,6 +82,8 @@ struct PatchRows {
   }
 };
 
+// (ranking keys: loads holds the timely prefetches P_N, max_finish and p95
+// together the 64-bit count of admitted ready units per class)
 struct LeanAcc {
   uint32_t status;
   int32_t headroom;
@@ -92,7 +94,8 @@ struct LeanAcc {
   uint32_t heads;       // unit heads given a slot by the first ordering try
   uint32_t claimed;     // distinct slots they occupy
   uint32_t bad;         // a head priority outside its level's index range
-  uint32_t pad[3];
+  uint32_t cf;          // ranking keys: latest admitted ready finish
+  unsigned long long h_life;  // ranking keys: lifecycle overhead
 };
 static_assert(sizeof(LeanAcc) == 48, "LeanAcc layout");
 
@@ -146,7 +149,8 @@ __device__ __forceinline__ uint32_t tadd(uint32_t a, uint32_t b) {
 
 __device__ __forceinline__ uint32_t umax(uint32_t a, uint32_t b) { return a > b ? a : b; }
 
-template <bool CHECKED, int QB, bool SEARCH>
+// PHI: each plan's ranking key (Eq. 12) is written instead of its score.
+template <bool CHECKED, int QB, bool SEARCH, bool PHI>
 __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
                                                   const int8_t* __restrict__ dev_all,
                                                   const uint16_t* __restrict__ prio_all,
@@ -465,6 +469,11 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
     int32_t fm = 0;   // free memory: capacity - resident weights
     int32_t pe = 0;   // largest excess of a unit's need over the free memory
     uint32_t freet = 0, nld = 0, nev4 = 0, inel = 0;
+    // ranking-key terms (Eq. 12) of this device lane: models reclaimed from
+    // the device so far, admitted ready units per class (16 bits each), their
+    // latest finish, lifecycle overhead, timely prefetches
+    uint32_t ph_rec = 0u, ph_cf = 0u, ph_pn = 0u;
+    unsigned long long ph_adm = 0ull, ph_h = 0ull;
     if (act) {
       const uint64_t res = t_res0[d];
       const int32_t capd = t_cap[d];
@@ -560,7 +569,7 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
         // everything of a unit that does not depend on the device's
         // sequential state; without a slot, activation 0 and model 0 keep
         // every address in range
-        struct U { int slot; uint32_t e, lst, arr, r; int32_t lat, mem; int4 lw; };
+        struct U { int slot; uint32_t e, lst, arr, r, act; int32_t lat, mem; int4 lw; };
         auto fetch = [&](int sl, U& X) {
           X.slot = sl;
           const uint32_t e = sl >= 0 ? (uint32_t)myrec[sl] : 0u;
@@ -573,6 +582,7 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
           X.arr = t_aarr[u];
           X.r = umax(myfin[u], X.arr);
           X.lw = lw_d[m];
+          if constexpr (PHI) X.act = t_act[u];
         };
         auto process = [&](const U& X) {
           if (X.slot < 0) return;
@@ -620,13 +630,15 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
           // first, then least recently used, then the lower model id; the
           // first two victims branch-free, any further ones in a loop
           {
-            const int32_t w0 = t_wmib[(int)(Q & (QT)15)];
-            const int32_t w1 = t_wmib[(int)((Q >> 4) & (QT)15)];
+            const uint32_t q0 = (uint32_t)(Q & (QT)15), q1 = (uint32_t)((Q >> 4) & (QT)15);
+            const int32_t w0 = t_wmib[q0];
+            const int32_t w1 = t_wmib[q1];
             const bool c0 = ex > 0 && nq4 >= 4u;
             const int32_t ex0 = ex - w0;
             const bool c1 = c0 && ex0 > 0 && nq4 >= 8u;
             const uint32_t k4 = (c0 ? 4u : 0u) + (c1 ? 4u : 0u);
             ex = c1 ? ex0 - w1 : (c0 ? ex0 : ex);
+            if constexpr (PHI) ph_rec |= (c0 ? 1u << q0 : 0u) | (c1 ? 1u << q1 : 0u);
             Q >>= k4;
             nq4 -= k4;
             nd4 = nd4 > k4 ? nd4 - k4 : 0u;
@@ -638,6 +650,7 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
               nd4 = nd4 > 4u ? nd4 - 4u : 0u;
               ex -= t_wmib[v];
               nev4 += 4u;
+              if constexpr (PHI) ph_rec |= 1u << v;
             }
           }
           // peak memory = capacity + the largest excess after reclamation;
@@ -662,6 +675,7 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
           const uint32_t ls = umax(a0, freet);
           const uint32_t le = tadd<CHECKED>(ls, (uint32_t)X.lw.x);
           const uint32_t s = umax(X.r, hit ? freet : le);
+          const uint32_t fr0 = freet;
           if (!(X.e & kEChain)) {
             const uint32_t f = tadd<CHECKED>(s, T);
             myfin[u] = f;
@@ -678,6 +692,22 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
               v = c;
             }
             freet = t;
+          }
+          if constexpr (PHI) {
+            // ready work: no predecessor, arrived by the window time
+            const bool ready = ((X.act >> 7) & 1u) != 0u;
+            if (!hit) {
+              // a reload of a copy this plan reclaimed from the device
+              if ((ph_rec >> m) & 1u) ph_h += (uint32_t)X.lw.x;
+              // a prefetch is timely when its load is done by the release
+              if (!ready && (X.e & kEPf) && le <= X.r) ++ph_pn;
+              // the delay a load adds to ready work
+              if (ready) ph_h += s - umax(X.r, fr0);
+            }
+            if (ready && ex <= 0) {
+              ph_adm += 1ull << (16u * ((X.act >> 8) & 3u));
+              ph_cf = umax(ph_cf, freet);
+            }
           }
         };
         // two units per trip so that the prefetched unit needs no copy; one
@@ -703,9 +733,18 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
 
     // ---- per-plan reductions (Sec. 4 metrics) ----
     if (act) {
-      atomicMin(&s_acc[gme].headroom, -pe);
-      atomicAdd(&s_acc[gme].loads, nld);
-      atomicAdd(&s_acc[gme].evicts, nev4 >> 2);
+      if constexpr (PHI) {
+        if (ph_adm) {
+          atomicAdd(reinterpret_cast<unsigned long long*>(&s_acc[gme].max_finish), ph_adm);
+          atomicMax(&s_acc[gme].cf, ph_cf);
+        }
+        if (ph_pn) atomicAdd(&s_acc[gme].loads, ph_pn);
+        if (ph_h) atomicAdd(&s_acc[gme].h_life, ph_h);
+      } else {
+        atomicMin(&s_acc[gme].headroom, -pe);
+        atomicAdd(&s_acc[gme].loads, nld);
+        atomicAdd(&s_acc[gme].evicts, nev4 >> 2);
+      }
       uint32_t st = pe > 0 ? (uint32_t)WF_ST_CAPACITY : 0u;
       if (inel) st |= (uint32_t)WF_ST_INELIGIBLE;
       // a saturated time ends in the device's last finish
@@ -713,8 +752,8 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
       if (st) atomicOr(&s_acc[gme].status, st);
     }
     // a workflow's completion is the latest finish among its activations
-    // without a successor in the same workflow
-    for (int i = lane; i < sp.S; i += 64) {
+    // without a successor in the same workflow (not part of the ranking key)
+    for (int i = lane; i < (PHI ? 0 : sp.S); i += 64) {
       const uint32_t sk = t_sink[i];
       const int src = (int)(sk & 0xffffu), wf = (int)(sk >> 16);
       for (int g0 = 0; g0 < gc; g0 += kB) {
@@ -731,7 +770,7 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
     }
     lsync();
     // completion latencies in place, and the latest finish
-    for (int it = lane; it < gc * W; it += 64) {
+    for (int it = lane; it < (PHI ? 0 : gc * W); it += 64) {
       const int g = it / W, a = it - g * W;
       const uint32_t fb = s_wfm[it];
       atomicMax(&s_acc[g].max_finish, fb);
@@ -741,7 +780,7 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
     // nearest-rank p95: the ceil(0.95 W)-th smallest completion latency,
     // lanes over (plan, workflow)
     const int kk = (95 * W + 99) / 100;
-    for (int it = lane; it < gc * W; it += 64) {
+    for (int it = lane; it < (PHI ? 0 : gc * W); it += 64) {
       const int g = it / W;
       const uint32_t* cw = s_wfm + g * W;
       const uint32_t ca = cw[it - g * W];
@@ -755,7 +794,24 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
       if (lt < kk && kk <= le) s_acc[g].p95 = ca;
     }
     lsync();
-    if (lane < gc) {
+    if (PHI && lane < gc) {
+      const LeanAcc a = s_acc[lane];
+      const unsigned long long adm = *reinterpret_cast<const unsigned long long*>(&a.max_finish);
+      wf_plan_key k;
+      k.c_ready_us = 0;
+      k.h_life_us = 0;
+      for (int c = 0; c < WF_MAX_CLASSES; ++c) k.admitted[c] = 0;
+      k.timely_prefetch = 0;
+      k.pad = 0;
+      k.status = (a.status & WF_ST_INELIGIBLE) ? (uint32_t)WF_ST_INELIGIBLE : a.status;
+      if (!(a.status & WF_ST_INELIGIBLE)) {
+        if (adm) k.c_ready_us = sp.origin + (int64_t)a.cf;
+        k.h_life_us = (int64_t)a.h_life;
+        for (int c = 0; c < WF_MAX_CLASSES; ++c) k.admitted[c] = (uint16_t)((adm >> (16 * c)) & 0xffffull);
+        k.timely_prefetch = (uint16_t)(a.loads > 65535u ? 65535u : a.loads);
+      }
+      reinterpret_cast<wf_plan_key*>(scores)[p0 + lane] = k;
+    } else if (lane < gc) {
       const LeanAcc a = s_acc[lane];
       wf_plan_score sc;
       if (a.status & WF_ST_INELIGIBLE) {
@@ -787,11 +843,11 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
   }
 }
 
-template <bool CHECKED, int QB, bool SEARCH>
+template <bool CHECKED, int QB, bool SEARCH, bool PHI>
 hipError_t launch_lean_variant(const ScoreParams& sp, const LeanParams& lp, const int8_t* dev,
                                const uint16_t* prio, const uint8_t* flags, int64_t n_plans,
                                wf_plan_score* scores, const SearchArgs& sa, hipStream_t stream) {
-  auto k = score_lean<CHECKED, QB, SEARCH>;
+  auto k = score_lean<CHECKED, QB, SEARCH, PHI>;
   (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k),
                             hipFuncAttributeMaxDynamicSharedMemorySize, lp.lds_bytes);
   hipLaunchKernelGGL(k, dim3(lp.grid), dim3(64 * lp.waves), lp.lds_bytes, stream, sp, lp, dev, prio,
@@ -799,31 +855,38 @@ hipError_t launch_lean_variant(const ScoreParams& sp, const LeanParams& lp, cons
   return hipGetLastError();
 }
 
-template <bool CHECKED, bool SEARCH>
+template <bool CHECKED, bool SEARCH, bool PHI>
 hipError_t launch_lean_q(const ScoreParams& sp, const LeanParams& lp, const int8_t* dev,
                          const uint16_t* prio, const uint8_t* flags, int64_t n_plans,
                          wf_plan_score* scores, const SearchArgs& sa, hipStream_t stream) {
   if (lp.qbits == 32)
-    return launch_lean_variant<CHECKED, 32, SEARCH>(sp, lp, dev, prio, flags, n_plans, scores, sa,
-                                                     stream);
-  return launch_lean_variant<CHECKED, 64, SEARCH>(sp, lp, dev, prio, flags, n_plans, scores, sa,
-                                                   stream);
+    return launch_lean_variant<CHECKED, 32, SEARCH, PHI>(sp, lp, dev, prio, flags, n_plans, scores,
+                                                          sa, stream);
+  return launch_lean_variant<CHECKED, 64, SEARCH, PHI>(sp, lp, dev, prio, flags, n_plans, scores,
+                                                        sa, stream);
+}
+
+template <bool SEARCH, bool PHI>
+hipError_t launch_lean_c(const ScoreParams& sp, const LeanParams& lp, const int8_t* dev,
+                         const uint16_t* prio, const uint8_t* flags, int64_t n_plans,
+                         wf_plan_score* scores, const SearchArgs& sa, hipStream_t stream) {
+  if (lp.checked)
+    return launch_lean_q<true, SEARCH, PHI>(sp, lp, dev, prio, flags, n_plans, scores, sa, stream);
+  return launch_lean_q<false, SEARCH, PHI>(sp, lp, dev, prio, flags, n_plans, scores, sa, stream);
 }
 
 }  // namespace
 
 hipError_t launch_score_lean(const ScoreParams& sp, const LeanParams& lp, const int8_t* dev,
                              const uint16_t* prio, const uint8_t* flags, int64_t n_plans,
-                             wf_plan_score* scores, const SearchArgs* search, hipStream_t stream) {
+                             void* out, const SearchArgs* search, bool keys, hipStream_t stream) {
   const SearchArgs sa = search ? *search : SearchArgs{};
-  if (search) {
-    if (lp.checked)
-      return launch_lean_q<true, true>(sp, lp, dev, prio, flags, n_plans, scores, sa, stream);
-    return launch_lean_q<false, true>(sp, lp, dev, prio, flags, n_plans, scores, sa, stream);
-  }
-  if (lp.checked)
-    return launch_lean_q<true, false>(sp, lp, dev, prio, flags, n_plans, scores, sa, stream);
-  return launch_lean_q<false, false>(sp, lp, dev, prio, flags, n_plans, scores, sa, stream);
+  wf_plan_score* o = static_cast<wf_plan_score*>(out);
+  if (search)
+    return keys ? launch_lean_c<true, true>(sp, lp, dev, prio, flags, n_plans, o, sa, stream)
+                : launch_lean_c<true, false>(sp, lp, dev, prio, flags, n_plans, o, sa, stream);
+  return keys ? launch_lean_c<false, true>(sp, lp, dev, prio, flags, n_plans, o, sa, stream)
+              : launch_lean_c<false, false>(sp, lp, dev, prio, flags, n_plans, o, sa, stream);
 }
 
 }  // namespace wfp

@@ -86,3 +86,57 @@ def test_random_windows(seed):
     assert got.tobytes() == ref.tobytes()
     gen, _ = score(win, plans, general=True)
     assert got.tobytes() == gen.tobytes()
+
+
+def keys(win, plans, general=False):
+    old = os.environ.get("WF_PLAN_KERNEL")
+    if general:
+        os.environ["WF_PLAN_KERNEL"] = "general"
+    try:
+        with pkg.Context(0) as ctx:
+            ctx.wf_plan_upload_window(win)
+            P = plans.n_plans
+            dev, prio, flags = pkg.device_plans(plans, "cuda:0")
+            out = torch.empty((P, 32), dtype=torch.uint8, device="cuda:0")
+            ctx.wf_plan_score_keys(dev, prio, flags, P, out)
+            torch.cuda.synchronize()
+            return pkg.keys_to_numpy(out, P), ctx.wf_plan_score_kernel()
+    finally:
+        if general:
+            if old is None:
+                del os.environ["WF_PLAN_KERNEL"]
+            else:
+                os.environ["WF_PLAN_KERNEL"] = old
+
+
+@pytest.mark.parametrize("cfg,n", [(1, 16384), (4, 65536)])
+def test_ranking_keys_of_the_lean_kernel(cfg, n):
+    """Eq. 12 keys from the lean kernel's key mode, with priority classes."""
+    win, plans = W.make_config(cfg, n_plans=n)
+    win.wf_class = (np.arange(win.n_wf) % 4).astype(np.uint8)
+    log(f"[lean keys] config {cfg}: {n} plans")
+    got, kern = keys(win, plans)
+    assert kern == "score_lean"
+    assert got.tobytes() == oracle.phi_keys(win, plans, threads=THREADS).tobytes()
+    gen, _ = keys(win, plans, general=True)
+    assert got.tobytes() == gen.tobytes()
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_ranking_keys_random_windows(seed):
+    rng = np.random.default_rng(19_000 + seed)
+    kw = dict(n_wf=int(rng.integers(1, 7)), nodes=(1, 12), n_dev=int(rng.integers(1, 13)),
+              n_models=int(rng.integers(1, 17)), same_model_bias=0.6)
+    if seed % 3 == 1:
+        kw.update(cap_range=(3000, 12000), w_range=(1000, 9000))
+    if seed % 3 == 2:
+        kw.update(lat_range=(1, 1 << 29), load_range=(0, 1 << 30))
+    win = W.random_window(rng, **kw)
+    win.wf_class = rng.integers(0, 4, win.n_wf).astype(np.uint8)
+    # half the workflows arrive at time 0 (ready work)
+    win.wf_arrival_us = np.where(rng.random(win.n_wf) < 0.5, 0, win.wf_arrival_us).astype(np.int64)
+    plans = W.random_plans(win, 600, rng, prio_mode=("any", "perm", "globalperm")[seed % 3],
+                           p_bad_dev=0.02 if seed % 4 == 0 else 0.0)
+    got, kern = keys(win, plans)
+    log(f"[lean keys] seed {seed}: N={win.n_act} M={win.n_models} kernel={kern}")
+    assert got.tobytes() == oracle.phi_keys(win, plans, threads=THREADS).tobytes()
