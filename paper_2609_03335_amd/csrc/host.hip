@@ -658,9 +658,9 @@ wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, bool time64_req, Im
     sp.nibble = h.victim_order == WF_VICTIM_PAPER ? -3 : -2;
   } else if (h.victim_order == WF_VICTIM_PAPER) {
     sp.nibble = -1;
-  } else if (M <= 16 && !sp.rcap) {
-    // (with replica caps the resident set stays a mask: the per-level check
-    // reads it)
+  } else if (M <= 16) {
+    // (with replica caps the queue modes keep the resident mask as well: the
+    // per-level check reads it)
     std::vector<int32_t> w(h.wmib.begin(), h.wmib.begin() + M);
     std::sort(w.begin(), w.end());
     int qcap = 1;
@@ -827,6 +827,7 @@ int lean_layout(const HostWindow& h, int G, int nwa, wfp::LeanOffsets& o) {
   o.fin = take((size_t)G * h.N * 4);
   o.wfm = take((size_t)G * std::max(1, h.W) * 4);
   o.acc = take((size_t)G * 48);
+  o.hold = take(h.rcap.empty() ? 0 : (size_t)G * h.D * 2);
   o.bytes = (int)off;
   return o.bytes;
 }
@@ -905,6 +906,7 @@ void plan_lean(wf_plan_ctx* ctx, const HostWindow& h, const wfp::ScoreParams& sp
   t.lw = img.put(lw.data(), lw.size() * 4);
   t.wmib = img.put(h.wmib.data(), h.wmib.size() * 4);
   t.aarr = img.put(aarr.data(), aarr.size() * 4);
+  t.rcap = img.put(h.rcap.data(), h.rcap.size() * 4);
   img.bytes.resize(align_up(img.bytes.size(), 16), 0);
   t.lds_bytes = (int)img.bytes.size();
   t.um = img.put(um.data(), um.size() * 4);
@@ -936,6 +938,7 @@ void plan_lean(wf_plan_ctx* ctx, const HostWindow& h, const wfp::ScoreParams& sp
   lp.wo = o;
   lp.checked = checked ? 1 : 0;
   lp.qbits = sp.nibble;
+  lp.rcap = h.rcap.empty() ? 0 : 1;
   lp.ok = 1;
   // generated candidates: each plan's changed sites live in its finish
   // entries until the walk

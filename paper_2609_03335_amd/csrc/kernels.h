@@ -118,7 +118,7 @@ struct ScoreParams {
                               // -1: scan in the paper's reclamation order; -2 / -3: the
                               // same two scans with per-device batch limits
   int has_chains;             // 1: some activation satisfies Eq. 3 (fused units possible)
-  int rcap;                   // 1: the window caps replicas (checked per level; scan modes only)
+  int rcap;                   // 1: the window caps replicas (checked per level)
   int rescore;                // 1: fp64 pass over the groups holding a plan whose uint32
                               // times saturated (status bit kRescore of the first pass)
   // ring of recent levels (deep or wide windows, scan reclamation, plan rows
@@ -144,6 +144,7 @@ struct LeanOffsets {
   int fin;     // u32 [G][N]       latest predecessor finish, then the activation's own finish
   int wfm;     // u32 [G][W]       latest finish per workflow, then its completion latency
   int acc;     // LeanAcc [G]
+  int hold;    // u16 [G][D]       replica caps: models each device held or loaded in the level
   int bytes;
 };
 
@@ -155,6 +156,7 @@ struct LeanTab {
   int lw;      // i32x4 [D][M] {load time, model weights, model id in every nibble, 0}
   int wmib;    // i32 [M]
   int aarr;    // u32 [N]    arrival of the activation's workflow (relative time)
+  int rcap;    // i32 [M]    replica cap of each model (windows with caps)
   int lds_bytes;
   // through the cache
   int um;      // i32x2 [D][N] {run time (-1 ineligible), activation memory} of each
@@ -186,6 +188,7 @@ struct LeanParams {
   LeanOffsets wo;  // wave regions follow the image's LDS part
   int search_ok;   // 1: it also generates candidates (their changed sites fit the
                    // finish array's storage)
+  int rcap;        // 1: the window caps replicas (checked per level)
 };
 
 // Generated candidates served by the lean kernel: at most this many

@@ -150,7 +150,8 @@ __device__ __forceinline__ uint32_t tadd(uint32_t a, uint32_t b) {
 __device__ __forceinline__ uint32_t umax(uint32_t a, uint32_t b) { return a > b ? a : b; }
 
 // PHI: each plan's ranking key (Eq. 12) is written instead of its score.
-template <bool CHECKED, int QB, bool SEARCH, bool PHI>
+// RCAP: the window caps replicas (a resident mask beside the queue).
+template <bool CHECKED, int QB, bool SEARCH, bool PHI, bool RCAP>
 __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
                                                   const int8_t* __restrict__ dev_all,
                                                   const uint16_t* __restrict__ prio_all,
@@ -173,6 +174,7 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
   const int4* t_lw = reinterpret_cast<const int4*>(lds + lp.t.lw);
   const int32_t* t_wmib = reinterpret_cast<const int32_t*>(lds + lp.t.wmib);
   const uint32_t* t_aarr = reinterpret_cast<const uint32_t*>(lds + lp.t.aarr);
+  const int32_t* t_rcap = reinterpret_cast<const int32_t*>(lds + lp.t.rcap);
   const int2* t_um = reinterpret_cast<const int2*>(tg + lp.t.um);
   const uint32_t* t_act = reinterpret_cast<const uint32_t*>(tg + lp.t.act);
   const uint32_t* t_alv = reinterpret_cast<const uint32_t*>(tg + lp.t.alv);
@@ -196,6 +198,7 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
   uint32_t* s_wfm = reinterpret_cast<uint32_t*>(wl + lp.wo.wfm);
   LeanAcc* s_acc = reinterpret_cast<LeanAcc*>(wl + lp.wo.acc);
   uint32_t* s_pat = s_fin;  // generated candidates' changed sites (until the walk)
+  uint16_t* s_hold = reinterpret_cast<uint16_t*>(wl + lp.wo.hold);  // replica caps
 
   const int g_me = lane / D;
   const int d_me = lane - g_me * D;
@@ -473,9 +476,13 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
     // the device so far, admitted ready units per class (16 bits each), their
     // latest finish, lifecycle overhead, timely prefetches
     uint32_t ph_rec = 0u, ph_cf = 0u, ph_pn = 0u;
+    // replica caps: the resident models, and those held as the level starts
+    // or loaded during it (the queue holds the order, this mask the set)
+    uint32_t rmask = 0u, lv_hold = 0u;
     unsigned long long ph_adm = 0ull, ph_h = 0ull;
     if (act) {
       const uint64_t res = t_res0[d];
+      rmask = (uint32_t)res;
       const int32_t capd = t_cap[d];
       freet = t_free0[d];
       int32_t used = 0;
@@ -530,6 +537,7 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
       }
 
       // ---- device lanes walk their units of the level in slot order ----
+      lv_hold = rmask;
       if (act) {
         const int j1 = (hi - 1) >> 6;
         const unsigned long long hmask = (hi & 63) ? ((1ull << (hi & 63)) - 1ull) : ~0ull;
@@ -639,6 +647,7 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
             const uint32_t k4 = (c0 ? 4u : 0u) + (c1 ? 4u : 0u);
             ex = c1 ? ex0 - w1 : (c0 ? ex0 : ex);
             if constexpr (PHI) ph_rec |= (c0 ? 1u << q0 : 0u) | (c1 ? 1u << q1 : 0u);
+            if constexpr (RCAP) rmask &= ~((c0 ? 1u << q0 : 0u) | (c1 ? 1u << q1 : 0u));
             Q >>= k4;
             nq4 -= k4;
             nd4 = nd4 > k4 ? nd4 - k4 : 0u;
@@ -651,6 +660,7 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
               ex -= t_wmib[v];
               nev4 += 4u;
               if constexpr (PHI) ph_rec |= 1u << v;
+              if constexpr (RCAP) rmask &= ~(1u << v);
             }
           }
           // peak memory = capacity + the largest excess after reclamation;
@@ -667,6 +677,10 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
             nq4 += 4u;
           }
           nld += hit ? 0u : 1u;
+          if constexpr (RCAP) {
+            rmask |= 1u << m;
+            lv_hold |= 1u << m;
+          }
           // timeline (Eq. 7): a load waits for the device and starts at the
           // release, or at the workflow arrival when prefetched; the unit
           // starts at max(release, load end), or at max(release, device
@@ -728,7 +742,19 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
         else
           run(next_wide);
       }
+      if (RCAP && act) s_hold[gme * D + d] = (uint16_t)lv_hold;
       lsync();
+      // ---- replica caps (Sec. 3.5 scale-out): a model held or loaded in
+      // this level on more devices than its cap; lanes over (plan, model) ----
+      if constexpr (RCAP) {
+        for (int it = lane; it < gc * M; it += 64) {
+          const int g = it / M, m = it - g * M;
+          int copies = 0;
+          for (int e = 0; e < D; ++e) copies += (int)((s_hold[g * D + e] >> m) & 1u);
+          if (copies > t_rcap[m]) atomicOr(&s_acc[g].status, (uint32_t)WF_ST_REPLICA);
+        }
+        lsync();
+      }
     }
 
     // ---- per-plan reductions (Sec. 4 metrics) ----
@@ -843,11 +869,11 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
   }
 }
 
-template <bool CHECKED, int QB, bool SEARCH, bool PHI>
+template <bool CHECKED, int QB, bool SEARCH, bool PHI, bool RCAP>
 hipError_t launch_lean_variant(const ScoreParams& sp, const LeanParams& lp, const int8_t* dev,
                                const uint16_t* prio, const uint8_t* flags, int64_t n_plans,
                                wf_plan_score* scores, const SearchArgs& sa, hipStream_t stream) {
-  auto k = score_lean<CHECKED, QB, SEARCH, PHI>;
+  auto k = score_lean<CHECKED, QB, SEARCH, PHI, RCAP>;
   (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k),
                             hipFuncAttributeMaxDynamicSharedMemorySize, lp.lds_bytes);
   hipLaunchKernelGGL(k, dim3(lp.grid), dim3(64 * lp.waves), lp.lds_bytes, stream, sp, lp, dev, prio,
@@ -855,15 +881,26 @@ hipError_t launch_lean_variant(const ScoreParams& sp, const LeanParams& lp, cons
   return hipGetLastError();
 }
 
-template <bool CHECKED, bool SEARCH, bool PHI>
+template <bool CHECKED, bool SEARCH, bool PHI, bool RCAP>
 hipError_t launch_lean_q(const ScoreParams& sp, const LeanParams& lp, const int8_t* dev,
                          const uint16_t* prio, const uint8_t* flags, int64_t n_plans,
                          wf_plan_score* scores, const SearchArgs& sa, hipStream_t stream) {
   if (lp.qbits == 32)
-    return launch_lean_variant<CHECKED, 32, SEARCH, PHI>(sp, lp, dev, prio, flags, n_plans, scores,
-                                                          sa, stream);
-  return launch_lean_variant<CHECKED, 64, SEARCH, PHI>(sp, lp, dev, prio, flags, n_plans, scores,
-                                                        sa, stream);
+    return launch_lean_variant<CHECKED, 32, SEARCH, PHI, RCAP>(sp, lp, dev, prio, flags, n_plans,
+                                                                scores, sa, stream);
+  return launch_lean_variant<CHECKED, 64, SEARCH, PHI, RCAP>(sp, lp, dev, prio, flags, n_plans,
+                                                              scores, sa, stream);
+}
+
+template <bool CHECKED, bool SEARCH, bool PHI>
+hipError_t launch_lean_r(const ScoreParams& sp, const LeanParams& lp, const int8_t* dev,
+                         const uint16_t* prio, const uint8_t* flags, int64_t n_plans,
+                         wf_plan_score* scores, const SearchArgs& sa, hipStream_t stream) {
+  if (lp.rcap)
+    return launch_lean_q<CHECKED, SEARCH, PHI, true>(sp, lp, dev, prio, flags, n_plans, scores, sa,
+                                                     stream);
+  return launch_lean_q<CHECKED, SEARCH, PHI, false>(sp, lp, dev, prio, flags, n_plans, scores, sa,
+                                                    stream);
 }
 
 template <bool SEARCH, bool PHI>
@@ -871,8 +908,8 @@ hipError_t launch_lean_c(const ScoreParams& sp, const LeanParams& lp, const int8
                          const uint16_t* prio, const uint8_t* flags, int64_t n_plans,
                          wf_plan_score* scores, const SearchArgs& sa, hipStream_t stream) {
   if (lp.checked)
-    return launch_lean_q<true, SEARCH, PHI>(sp, lp, dev, prio, flags, n_plans, scores, sa, stream);
-  return launch_lean_q<false, SEARCH, PHI>(sp, lp, dev, prio, flags, n_plans, scores, sa, stream);
+    return launch_lean_r<true, SEARCH, PHI>(sp, lp, dev, prio, flags, n_plans, scores, sa, stream);
+  return launch_lean_r<false, SEARCH, PHI>(sp, lp, dev, prio, flags, n_plans, scores, sa, stream);
 }
 
 }  // namespace

@@ -727,7 +727,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
     int kdev = 0;
     unsigned long long others = 0ull;
     // replica caps: the models the device holds as the level starts or loads
-    // during it (scanned resident sets only)
+    // during it
     unsigned long long lv_hold = 0ull;
     // batch limits: per slot the free time, and the running unit's finish,
     // memory and model; the last first-action time (dispatch is in order)
@@ -1039,7 +1039,8 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
           for (int e = 0; e < D; ++e)
             if (e != d) others |= s_snap[gme * D + e];
       }
-      if constexpr (!NIBBLE) lv_hold = res;
+      // (the queue modes keep the resident mask only for the replica check)
+      if (!NIBBLE || sp.rcap) lv_hold = res;
       if (act) {
         const int j1 = (hi - 1) >> 6;
         const unsigned long long hmask = (hi & 63) ? ((1ull << (hi & 63)) - 1ull) : ~0ull;
@@ -1263,6 +1264,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
                 const int v = (int)(Q & (QT)15);
                 if constexpr (PHI) ph_rec |= 1ull << v;
                 if (rec_on) sched.reclaimed_models[pw * N + u] |= 1ull << v;
+                if (sp.rcap) res &= ~(1ull << v);
                 Q >>= 4;
                 --nq;
                 nd = nd > 0 ? nd - 1 : 0;
@@ -1332,7 +1334,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
                 if (ready) ph_h += (HT)TO::sub(s, TO::tmax(r, dev_free));
               }
             }
-            if constexpr (!NIBBLE) {
+            if (!NIBBLE || sp.rcap) {
               res |= mbit;
               lv_hold |= mbit;
             }
@@ -1408,24 +1410,20 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
         else
           run(next_wide);
       }
-      if constexpr (!NIBBLE) {
-        if (sp.rcap && act) s_hold[gme * D + d] = lv_hold;
-      }
+      if (sp.rcap && act) s_hold[gme * D + d] = lv_hold;
       if (NH > 1) save(h);
       }
       wave_sync();
       // ---- replica caps (Sec. 3.5 scale-out): a model held or loaded in
       // this level on more devices than its cap; lanes over (plan, model) ----
-      if constexpr (!NIBBLE) {
-        if (sp.rcap) {
-          for (int it = lane; it < gc * M; it += 64) {
-            const int g = it / M, m = it - g * M;
-            int copies = 0;
-            for (int e = 0; e < D; ++e) copies += (int)((s_hold[g * D + e] >> m) & 1ull);
-            if (copies > t_rcap[m]) atomicOr(&s_acc[g].status, (uint32_t)WF_ST_REPLICA);
-          }
-          wave_sync();
+      if (sp.rcap) {
+        for (int it = lane; it < gc * M; it += 64) {
+          const int g = it / M, m = it - g * M;
+          int copies = 0;
+          for (int e = 0; e < D; ++e) copies += (int)((s_hold[g * D + e] >> m) & 1ull);
+          if (copies > t_rcap[m]) atomicOr(&s_acc[g].status, (uint32_t)WF_ST_REPLICA);
         }
+        wave_sync();
       }
     }
 

@@ -123,14 +123,19 @@ def test_generated_candidates_under_caps(ctx):
     assert pkg.scores_to_numpy(scores, n).tobytes() == oracle.score(win, cand, threads=THREADS).tobytes()
 
 
-def test_throughput_window_with_caps(ctx):
+def test_throughput_window_with_caps(ctx, monkeypatch):
     """The 256-activation window with every model capped at six copies (a
-    fifth of the plans spread some model further): the cap moves the window
-    to the scanned-residency kernel; records of 65,536 plans bytewise."""
+    fifth of the plans spread some model further): the lean kernel keeps its
+    reclamation queue and a resident mask beside it for the check; records
+    of 65,536 plans bytewise, from it and from the general kernel."""
     win, plans = W.make_config(4, n_plans=65536)
     win = dataclasses.replace(win, model_replica_cap=np.full(win.n_models, 6, np.int32))
     got, _, _ = gpu(ctx, win, plans)
-    assert ctx.wf_plan_score_kernel() == "score_plans"
+    assert ctx.wf_plan_score_kernel() == "score_lean"
     ref = oracle.score(win, plans, threads=THREADS)
     assert got.tobytes() == ref.tobytes()
+    monkeypatch.setenv("WF_PLAN_KERNEL", "general")
+    gen, _, _ = gpu(ctx, win, plans)
+    assert ctx.wf_plan_score_kernel() == "score_plans"
+    assert gen.tobytes() == ref.tobytes()
     assert (ref["status"] & pkg.WF_ST_REPLICA).any() and not (ref["status"] & pkg.WF_ST_REPLICA).all()
