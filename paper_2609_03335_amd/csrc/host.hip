@@ -651,16 +651,12 @@ wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, bool time64_req, Im
   // 32 bits when no device can ever hold more than 8 models: a device holds
   // its initial set, or models whose weights sum to at most its capacity, or
   // (after a load that overflows) the one model just loaded
+  // (with batch limits too: a load reclaims until the models, plus the
+  // running units' memory, fit, or until nothing is left to reclaim)
   sp.nibble = 0;
+  sp.queue = 0;
   sp.rcap = h.rcap.empty() ? 0 : 1;
-  const bool batched = std::any_of(h.batch.begin(), h.batch.end(), [](int32_t b) { return b > 1; });
-  if (batched) {
-    sp.nibble = h.victim_order == WF_VICTIM_PAPER ? -3 : -2;
-  } else if (h.victim_order == WF_VICTIM_PAPER) {
-    sp.nibble = -1;
-  } else if (M <= 16) {
-    // (with replica caps the queue modes keep the resident mask as well: the
-    // per-level check reads it)
+  if (M <= 16) {
     std::vector<int32_t> w(h.wmib.begin(), h.wmib.begin() + M);
     std::sort(w.begin(), w.end());
     int qcap = 1;
@@ -670,7 +666,17 @@ wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, bool time64_req, Im
       while (k < M && sum + w[k] <= h.cap[d]) sum += w[k++];
       qcap = std::max(qcap, std::max(k, __builtin_popcountll(h.init_res[d])));
     }
-    sp.nibble = qcap <= 8 ? 32 : 64;
+    sp.queue = qcap <= 8 ? 32 : 64;
+  }
+  const bool batched = std::any_of(h.batch.begin(), h.batch.end(), [](int32_t b) { return b > 1; });
+  if (batched) {
+    sp.nibble = h.victim_order == WF_VICTIM_PAPER ? -3 : -2;
+  } else if (h.victim_order == WF_VICTIM_PAPER) {
+    sp.nibble = -1;
+  } else {
+    // (with replica caps the queue modes keep the resident mask as well: the
+    // per-level check reads it)
+    sp.nibble = sp.queue;
   }
   sp.has_chains = 0;
   for (int32_t i = 0; i < N; ++i) sp.has_chains |= h.chain_next[i] >= 0 ? 1 : 0;
@@ -847,8 +853,11 @@ void plan_lean(wf_plan_ctx* ctx, const HostWindow& h, const wfp::ScoreParams& sp
   lp = wfp::LeanParams{};
   const char* force = std::getenv("WF_PLAN_KERNEL");
   if (force && std::strcmp(force, "general") == 0) return;
-  if (sp.time64 || (sp.nibble != 32 && sp.nibble != 64) || h.N < 1 || h.N > 512 || h.M > 16 ||
-      h.D > 64)
+  // (batch limits with the default order: the queue's order, passing over
+  // leased copies; not with replica caps)
+  const bool batch = sp.nibble == -2 && h.rcap.empty();
+  if (sp.time64 || (sp.nibble != 32 && sp.nibble != 64 && !batch) || h.N < 1 || h.N > 512 ||
+      h.M > 16 || h.D > 64)
     return;
   const int N = h.N, D = h.D, M = h.M, W = h.W;
   // ---- table image (same words as the general image where they coincide) ----
@@ -921,6 +930,7 @@ void plan_lean(wf_plan_ctx* ctx, const HostWindow& h, const wfp::ScoreParams& sp
   t.res0 = img.put(h.init_res.data(), h.init_res.size() * 8);
   t.free0 = img.put(fr.data(), fr.size() * 4);
   t.sink = img.put(sink.data(), sink.size() * 4);
+  t.batch = img.put(h.batch.data(), h.batch.size() * 4);
   img.bytes.resize(align_up(img.bytes.size(), 16), 0);
   t.bytes = (int)img.bytes.size();
   // ---- launch plan ----
@@ -937,8 +947,9 @@ void plan_lean(wf_plan_ctx* ctx, const HostWindow& h, const wfp::ScoreParams& sp
   lp.grid = ctx->n_cu * std::max(1, lds_cu / lp.lds_bytes);
   lp.wo = o;
   lp.checked = checked ? 1 : 0;
-  lp.qbits = sp.nibble;
+  lp.qbits = sp.queue;
   lp.rcap = h.rcap.empty() ? 0 : 1;
+  lp.batch = batch ? 1 : 0;
   lp.ok = 1;
   // generated candidates: each plan's changed sites live in its finish
   // entries until the walk
@@ -1289,7 +1300,7 @@ wf_status wf_plan_search_batch(wf_plan_ctx* ctx, const int8_t* dev, const uint16
   if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
   const wfp::SearchArgs sa = search_params(ctx, mode, seed, n_mut, first);
   const DeviceWindow& dw = ctx->dw;
-  if (dw.lean.ok && dw.lean.search_ok && n_mut <= wfp::kLeanMaxMut) {
+  if (dw.lean.ok && !dw.lean.batch && dw.lean.search_ok && n_mut <= wfp::kLeanMaxMut) {
     // the lean kernel generates the candidates as the incumbent plus their
     // changed sites; then (times not proven below 2^32) the general fp64
     // pass over the groups holding a candidate whose times saturated
@@ -1407,7 +1418,7 @@ wf_status wf_plan_score_keys(wf_plan_ctx* ctx, const int8_t* dev, const uint16_t
   hipError_t e = hipSetDevice(ctx->device);
   if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
   const DeviceWindow& dw = ctx->dw;
-  if (dw.lean.ok) {
+  if (dw.lean.ok && !dw.lean.batch) {
     // the lean kernel's key mode, then the general fp64 pass over the groups
     // holding a plan whose uint32 times saturated
     const wfp::LeanParams lp = lean_grid(dw.lean, n_plans);
@@ -1441,7 +1452,7 @@ wf_status wf_plan_search_keys(wf_plan_ctx* ctx, const int8_t* dev, const uint16_
   if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
   const wfp::SearchArgs sa = search_params(ctx, mode, seed, n_mut, first);
   const DeviceWindow& dw = ctx->dw;
-  if (dw.lean.ok && dw.lean.search_ok && n_mut <= wfp::kLeanMaxMut) {
+  if (dw.lean.ok && !dw.lean.batch && dw.lean.search_ok && n_mut <= wfp::kLeanMaxMut) {
     const wfp::LeanParams lp = lean_grid(dw.lean, n_candidates);
     e = wfp::launch_score_lean(dw.sp, lp, dev, prio, flags, n_candidates, keys, &sa, true,
                                static_cast<hipStream_t>(hip_stream));

@@ -117,6 +117,7 @@ struct ScoreParams {
   int nibble;                 // reclamation queue width in bits (32 or 64), 0: scan,
                               // -1: scan in the paper's reclamation order; -2 / -3: the
                               // same two scans with per-device batch limits
+  int queue;                  // width a queue would take (32 or 64; 0: over 16 models)
   int has_chains;             // 1: some activation satisfies Eq. 3 (fused units possible)
   int rcap;                   // 1: the window caps replicas (checked per level)
   int rescore;                // 1: fp64 pass over the groups holding a plan whose uint32
@@ -172,12 +173,14 @@ struct LeanTab {
   int res0;    // u64 [D]
   int free0;   // u32 [D]
   int sink;    // u32 [S]    as TabOffsets::sink
+  int batch;   // i32 [D]    batch limit of each device
   int bytes;
 };
 
-// Launch plan of the lean kernel (the scalar objective of plans read from
-// HBM, uint32 times, at most 16 models in a 4-bit queue, one unit per
-// device, the default reclamation order, at most 512 activations).
+// Launch plan of the lean kernel (scores or ranking keys of plans read from
+// HBM or generated around an incumbent; uint32 times, at most 16 models in a
+// 4-bit queue, the default reclamation order, at most 512 activations;
+// devices with batch limits for plan scores only).
 struct LeanParams {
   int ok;          // 1: the window qualifies and a layout fits in LDS
   int checked;     // 1: uint32 additions saturate and flag the plan for the fp64 pass
@@ -189,6 +192,7 @@ struct LeanParams {
   int search_ok;   // 1: it also generates candidates (their changed sites fit the
                    // finish array's storage)
   int rcap;        // 1: the window caps replicas (checked per level)
+  int batch;       // 1: devices with batch limits (plan scores only)
 };
 
 // Generated candidates served by the lean kernel: at most this many

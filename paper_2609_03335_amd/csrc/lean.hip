@@ -148,10 +148,13 @@ __device__ __forceinline__ uint32_t tadd(uint32_t a, uint32_t b) {
 }
 
 __device__ __forceinline__ uint32_t umax(uint32_t a, uint32_t b) { return a > b ? a : b; }
+__device__ __forceinline__ uint32_t umin(uint32_t a, uint32_t b) { return a < b ? a : b; }
 
 // PHI: each plan's ranking key (Eq. 12) is written instead of its score.
 // RCAP: the window caps replicas (a resident mask beside the queue).
-template <bool CHECKED, int QB, bool SEARCH, bool PHI, bool RCAP>
+// BATCH: devices run up to their batch limit of units at once (plan scores
+// only).
+template <bool CHECKED, int QB, bool SEARCH, bool PHI, bool RCAP, bool BATCH>
 __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
                                                   const int8_t* __restrict__ dev_all,
                                                   const uint16_t* __restrict__ prio_all,
@@ -159,6 +162,7 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
                                                   wf_plan_score* __restrict__ scores, SearchArgs sa) {
   using QT = std::conditional_t<QB == 32, uint32_t, uint64_t>;
   constexpr QT kOnes = (QT)0x1111111111111111ull, kHigh = (QT)0x8888888888888888ull;
+  static_assert(!BATCH || (!SEARCH && !PHI && !RCAP), "batch limits: plan scores only");
   extern __shared__ __align__(16) unsigned char lds[];
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int N = sp.N, W = sp.W, M = sp.M, D = sp.D, NB = sp.NB, G = lp.G, NWA = sp.nwa;
@@ -187,6 +191,7 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
   const unsigned long long* t_res0 = reinterpret_cast<const unsigned long long*>(tg + lp.t.res0);
   const uint32_t* t_free0 = reinterpret_cast<const uint32_t*>(tg + lp.t.free0);
   const uint32_t* t_sink = reinterpret_cast<const uint32_t*>(tg + lp.t.sink);
+  const int32_t* t_batch = reinterpret_cast<const int32_t*>(tg + lp.t.batch);
 
   // ---- this wave's LDS region ----
   unsigned char* wl = lds + lp.t.lds_bytes + lp.wo.bytes * wid;
@@ -480,11 +485,33 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
     // or loaded during it (the queue holds the order, this mask the set)
     uint32_t rmask = 0u, lv_hold = 0u;
     unsigned long long ph_adm = 0ull, ph_h = 0ull;
+    // batch limits: per slot the time it frees (the running unit's finish),
+    // the unit's memory, and its model's bit (a lease while it runs); the
+    // last dispatch time (units dispatch in order).  Slots beyond the
+    // device's limit never free and hold bit 16, outside every model.
+    uint32_t bs_fin[kMaxBatch], bs_lb[kMaxBatch], bdisp = 0u;
+    int32_t bs_mem[kMaxBatch];
+    int nbatch = 1;
+#pragma unroll
+    for (int k = 0; k < kMaxBatch; ++k) {
+      bs_fin[k] = 0u;
+      bs_lb[k] = 0u;
+      bs_mem[k] = 0;
+    }
     if (act) {
       const uint64_t res = t_res0[d];
       rmask = (uint32_t)res;
       const int32_t capd = t_cap[d];
       freet = t_free0[d];
+      if constexpr (BATCH) {
+        nbatch = t_batch[d];
+        bdisp = freet;
+#pragma unroll
+        for (int k = 0; k < kMaxBatch; ++k) {
+          bs_fin[k] = k < nbatch ? freet : 0xffffffffu;
+          bs_lb[k] = k < nbatch ? 0u : 1u << 16;
+        }
+      }
       int32_t used = 0;
       QT qa = 0;
       uint32_t na = 0;
@@ -633,40 +660,98 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
           }
           nq4 -= hit ? 4u : 0u;
           const int32_t need = mx + (hit ? 0 : X.lw.y);
-          int32_t ex = need - fm;  // > 0: the unit does not fit yet
-          // reclaim (Sec. 3.5) from the queue's front: no remaining use
-          // first, then least recently used, then the lower model id; the
-          // first two victims branch-free, any further ones in a loop
-          {
-            const uint32_t q0 = (uint32_t)(Q & (QT)15), q1 = (uint32_t)((Q >> 4) & (QT)15);
-            const int32_t w0 = t_wmib[q0];
-            const int32_t w1 = t_wmib[q1];
-            const bool c0 = ex > 0 && nq4 >= 4u;
-            const int32_t ex0 = ex - w0;
-            const bool c1 = c0 && ex0 > 0 && nq4 >= 8u;
-            const uint32_t k4 = (c0 ? 4u : 0u) + (c1 ? 4u : 0u);
-            ex = c1 ? ex0 - w1 : (c0 ? ex0 : ex);
-            if constexpr (PHI) ph_rec |= (c0 ? 1u << q0 : 0u) | (c1 ? 1u << q1 : 0u);
-            if constexpr (RCAP) rmask &= ~((c0 ? 1u << q0 : 0u) | (c1 ? 1u << q1 : 0u));
-            Q >>= k4;
-            nq4 -= k4;
-            nd4 = nd4 > k4 ? nd4 - k4 : 0u;
-            nev4 += k4;
-            while (ex > 0 && nq4 >= 4u && c1) {
-              const int v = (int)(Q & (QT)15);
-              Q >>= 4;
-              nq4 -= 4u;
-              nd4 = nd4 > 4u ? nd4 - 4u : 0u;
-              ex -= t_wmib[v];
-              nev4 += 4u;
-              if constexpr (PHI) ph_rec |= 1u << v;
-              if constexpr (RCAP) rmask &= ~(1u << v);
+          int32_t ex;       // > 0: the unit does not fit yet
+          int32_t run = 0;  // memory of the units still running (batch limits)
+          int ks = 0;       // batch limits: the unit's slot, and its dispatch time
+          uint32_t t0 = 0u;
+          if constexpr (BATCH) {
+            // the slot that frees first; units dispatch in order, at the
+            // release (the arrival for a prefetched load) at the earliest
+            uint32_t sft = bs_fin[0];
+#pragma unroll
+            for (int k = 1; k < kMaxBatch; ++k)
+              if (bs_fin[k] < sft) {
+                ks = k;
+                sft = bs_fin[k];
+              }
+            t0 = umax(umax((!hit && (X.e & kEPf)) ? X.arr : X.r, sft), bdisp);
+            // the units running at t0: their memory, leases on their
+            // models, and the first of their finishes
+            uint32_t leased, nf;
+            auto running_at = [&]() {
+              leased = 0u;
+              nf = 0xffffffffu;
+              run = 0;
+#pragma unroll
+              for (int k = 0; k < kMaxBatch; ++k) {
+                const bool r = bs_fin[k] > t0;
+                run += r ? bs_mem[k] : 0;
+                leased |= r ? bs_lb[k] : 0u;
+                nf = r ? umin(nf, bs_fin[k]) : nf;
+              }
+            };
+            // reclaim (Sec. 3.5) in the queue's order, passing over the
+            // copies whose model holds a lease; when the unit still does not
+            // fit, wait for the next running unit to finish (its lease and
+            // memory end) and look again
+            int32_t ex0 = need - fm;  // excess without the running units
+            for (;;) {
+              running_at();
+              for (uint32_t p = 0u; ex0 + run > 0 && p < nq4;) {
+                const uint32_t v = (uint32_t)(Q >> p) & 15u;
+                const int32_t wv = t_wmib[v];
+                if ((leased >> v) & 1u) {
+                  p += 4u;
+                  continue;
+                }
+                const QT lowm = ((QT)1 << p) - (QT)1;
+                Q = (Q & lowm) | ((Q >> 4) & ~lowm);
+                nq4 -= 4u;
+                nd4 -= p < nd4 ? 4u : 0u;
+                ex0 -= wv;
+                nev4 += 4u;
+              }
+              // fits, or no running unit left to wait for
+              if (ex0 + run <= 0 || (leased & 0xffffu) == 0u) break;
+              t0 = nf;
+            }
+            ex = ex0 + run;
+          } else {
+            ex = need - fm;
+            // reclaim (Sec. 3.5) from the queue's front: no remaining use
+            // first, then least recently used, then the lower model id; the
+            // first two victims branch-free, any further ones in a loop
+            {
+              const uint32_t q0 = (uint32_t)(Q & (QT)15), q1 = (uint32_t)((Q >> 4) & (QT)15);
+              const int32_t w0 = t_wmib[q0];
+              const int32_t w1 = t_wmib[q1];
+              const bool c0 = ex > 0 && nq4 >= 4u;
+              const int32_t ex0 = ex - w0;
+              const bool c1 = c0 && ex0 > 0 && nq4 >= 8u;
+              const uint32_t k4 = (c0 ? 4u : 0u) + (c1 ? 4u : 0u);
+              ex = c1 ? ex0 - w1 : (c0 ? ex0 : ex);
+              if constexpr (PHI) ph_rec |= (c0 ? 1u << q0 : 0u) | (c1 ? 1u << q1 : 0u);
+              if constexpr (RCAP) rmask &= ~((c0 ? 1u << q0 : 0u) | (c1 ? 1u << q1 : 0u));
+              Q >>= k4;
+              nq4 -= k4;
+              nd4 = nd4 > k4 ? nd4 - k4 : 0u;
+              nev4 += k4;
+              while (ex > 0 && nq4 >= 4u && c1) {
+                const int v = (int)(Q & (QT)15);
+                Q >>= 4;
+                nq4 -= 4u;
+                nd4 = nd4 > 4u ? nd4 - 4u : 0u;
+                ex -= t_wmib[v];
+                nev4 += 4u;
+                if constexpr (PHI) ph_rec |= 1u << v;
+                if constexpr (RCAP) rmask &= ~(1u << v);
+              }
             }
           }
           // peak memory = capacity + the largest excess after reclamation;
-          // free memory after the load: mx - ex
+          // free memory after the load: mx + run - ex
           pe = ex > pe ? ex : pe;
-          fm = mx - ex;
+          fm = mx + run - ex;
           // m re-enters after the no-remaining-use part when this was its
           // last unit on the device, else at the end
           {
@@ -685,10 +770,12 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
           // release, or at the workflow arrival when prefetched; the unit
           // starts at max(release, load end), or at max(release, device
           // free) when its model was resident
+          // (batch limits: the load starts at the dispatch, a resident
+          // model's unit runs at once)
           const uint32_t a0 = (X.e & kEPf) ? X.arr : X.r;
-          const uint32_t ls = umax(a0, freet);
+          const uint32_t ls = BATCH ? t0 : umax(a0, freet);
           const uint32_t le = tadd<CHECKED>(ls, (uint32_t)X.lw.x);
-          const uint32_t s = umax(X.r, hit ? freet : le);
+          const uint32_t s = BATCH ? (hit ? t0 : umax(X.r, le)) : umax(X.r, hit ? freet : le);
           const uint32_t fr0 = freet;
           if (!(X.e & kEChain)) {
             const uint32_t f = tadd<CHECKED>(s, T);
@@ -706,6 +793,15 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
               v = c;
             }
             freet = t;
+          }
+          if constexpr (BATCH) {
+#pragma unroll
+            for (int k = 0; k < kMaxBatch; ++k) {
+              bs_fin[k] = k == ks ? freet : bs_fin[k];
+              bs_mem[k] = k == ks ? mx : bs_mem[k];
+              bs_lb[k] = k == ks ? 1u << m : bs_lb[k];
+            }
+            bdisp = t0;
           }
           if constexpr (PHI) {
             // ready work: no predecessor, arrived by the window time
@@ -774,7 +870,12 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
       uint32_t st = pe > 0 ? (uint32_t)WF_ST_CAPACITY : 0u;
       if (inel) st |= (uint32_t)WF_ST_INELIGIBLE;
       // a saturated time ends in the device's last finish
-      if (CHECKED && freet == 0xffffffffu) st |= kRescore;
+      uint32_t last = freet;
+      if constexpr (BATCH) {
+#pragma unroll
+        for (int k = 0; k < kMaxBatch; ++k) last = k < nbatch ? umax(last, bs_fin[k]) : last;
+      }
+      if (CHECKED && last == 0xffffffffu) st |= kRescore;
       if (st) atomicOr(&s_acc[gme].status, st);
     }
     // a workflow's completion is the latest finish among its activations
@@ -869,11 +970,11 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
   }
 }
 
-template <bool CHECKED, int QB, bool SEARCH, bool PHI, bool RCAP>
+template <bool CHECKED, int QB, bool SEARCH, bool PHI, bool RCAP, bool BATCH>
 hipError_t launch_lean_variant(const ScoreParams& sp, const LeanParams& lp, const int8_t* dev,
                                const uint16_t* prio, const uint8_t* flags, int64_t n_plans,
                                wf_plan_score* scores, const SearchArgs& sa, hipStream_t stream) {
-  auto k = score_lean<CHECKED, QB, SEARCH, PHI, RCAP>;
+  auto k = score_lean<CHECKED, QB, SEARCH, PHI, RCAP, BATCH>;
   (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k),
                             hipFuncAttributeMaxDynamicSharedMemorySize, lp.lds_bytes);
   hipLaunchKernelGGL(k, dim3(lp.grid), dim3(64 * lp.waves), lp.lds_bytes, stream, sp, lp, dev, prio,
@@ -881,15 +982,15 @@ hipError_t launch_lean_variant(const ScoreParams& sp, const LeanParams& lp, cons
   return hipGetLastError();
 }
 
-template <bool CHECKED, bool SEARCH, bool PHI, bool RCAP>
+template <bool CHECKED, bool SEARCH, bool PHI, bool RCAP, bool BATCH>
 hipError_t launch_lean_q(const ScoreParams& sp, const LeanParams& lp, const int8_t* dev,
                          const uint16_t* prio, const uint8_t* flags, int64_t n_plans,
                          wf_plan_score* scores, const SearchArgs& sa, hipStream_t stream) {
   if (lp.qbits == 32)
-    return launch_lean_variant<CHECKED, 32, SEARCH, PHI, RCAP>(sp, lp, dev, prio, flags, n_plans,
-                                                                scores, sa, stream);
-  return launch_lean_variant<CHECKED, 64, SEARCH, PHI, RCAP>(sp, lp, dev, prio, flags, n_plans,
-                                                              scores, sa, stream);
+    return launch_lean_variant<CHECKED, 32, SEARCH, PHI, RCAP, BATCH>(sp, lp, dev, prio, flags,
+                                                                       n_plans, scores, sa, stream);
+  return launch_lean_variant<CHECKED, 64, SEARCH, PHI, RCAP, BATCH>(sp, lp, dev, prio, flags,
+                                                                     n_plans, scores, sa, stream);
 }
 
 template <bool CHECKED, bool SEARCH, bool PHI>
@@ -897,10 +998,10 @@ hipError_t launch_lean_r(const ScoreParams& sp, const LeanParams& lp, const int8
                          const uint16_t* prio, const uint8_t* flags, int64_t n_plans,
                          wf_plan_score* scores, const SearchArgs& sa, hipStream_t stream) {
   if (lp.rcap)
-    return launch_lean_q<CHECKED, SEARCH, PHI, true>(sp, lp, dev, prio, flags, n_plans, scores, sa,
-                                                     stream);
-  return launch_lean_q<CHECKED, SEARCH, PHI, false>(sp, lp, dev, prio, flags, n_plans, scores, sa,
-                                                    stream);
+    return launch_lean_q<CHECKED, SEARCH, PHI, true, false>(sp, lp, dev, prio, flags, n_plans,
+                                                            scores, sa, stream);
+  return launch_lean_q<CHECKED, SEARCH, PHI, false, false>(sp, lp, dev, prio, flags, n_plans,
+                                                           scores, sa, stream);
 }
 
 template <bool SEARCH, bool PHI>
@@ -919,6 +1020,15 @@ hipError_t launch_score_lean(const ScoreParams& sp, const LeanParams& lp, const 
                              void* out, const SearchArgs* search, bool keys, hipStream_t stream) {
   const SearchArgs sa = search ? *search : SearchArgs{};
   wf_plan_score* o = static_cast<wf_plan_score*>(out);
+  if (lp.batch) {
+    // windows with batch limits: plan scores only
+    if (search || keys || lp.rcap) return hipErrorInvalidValue;
+    if (lp.checked)
+      return launch_lean_q<true, false, false, false, true>(sp, lp, dev, prio, flags, n_plans, o,
+                                                            sa, stream);
+    return launch_lean_q<false, false, false, false, true>(sp, lp, dev, prio, flags, n_plans, o, sa,
+                                                           stream);
+  }
   if (search)
     return keys ? launch_lean_c<true, true>(sp, lp, dev, prio, flags, n_plans, o, sa, stream)
                 : launch_lean_c<true, false>(sp, lp, dev, prio, flags, n_plans, o, sa, stream);

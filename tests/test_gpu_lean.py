@@ -140,3 +140,70 @@ def test_ranking_keys_random_windows(seed):
     got, kern = keys(win, plans)
     log(f"[lean keys] seed {seed}: N={win.n_act} M={win.n_models} kernel={kern}")
     assert got.tobytes() == oracle.phi_keys(win, plans, threads=THREADS).tobytes()
+
+
+@pytest.mark.parametrize("cfg,n,limit", [(0, 512, 2), (1, 16384, 4), (4, 65536, 2), (4, 8192, 3)])
+def test_batch_limits_in_the_lean_kernel(cfg, n, limit):
+    """Devices with batch limits (several units at once, memory checked
+    against the running units, leases on their models): the lean kernel's
+    batch mode against the oracle and the general kernel."""
+    win, plans = W.make_config(cfg, n_plans=n)
+    win.dev_batch = np.full(win.n_dev, limit, np.int32)
+    win.dev_batch[0] = 1
+    log(f"[lean batch] config {cfg}: {n} plans, limit {limit}")
+    got, kern = score(win, plans)
+    assert kern[0] == "score_lean"
+    assert got.tobytes() == oracle.score(win, plans, threads=THREADS).tobytes()
+    gen, kern_g = score(win, plans, general=True)
+    assert kern_g[0] == "score_plans"
+    assert got.tobytes() == gen.tobytes()
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_batch_limits_random_windows(seed):
+    rng = np.random.default_rng(29_000 + seed)
+    kind = seed % 4
+    D = int(rng.integers(1, 9))
+    if kind == 0:  # weightless models: the running units' memory decides
+        win = W.random_window(rng, n_wf=4, nodes=(2, 9), n_dev=D, n_models=4, w_range=(0, 0),
+                              cap_range=(3000, 9000), mem_range=(500, 4000))
+    elif kind == 1:  # tight weights: leases hold copies back from reclamation
+        win = W.random_window(rng, n_wf=5, nodes=(2, 10), n_dev=D, n_models=int(rng.integers(4, 17)),
+                              cap_range=(8000, 16000), w_range=(2000, 6000), mem_range=(0, 2000))
+    elif kind == 2:  # long run and load times: uint32 times checked, some saturate
+        win = W.random_window(rng, n_wf=int(rng.integers(2, 8)), nodes=(2, 10), n_dev=D,
+                              n_models=int(rng.integers(2, 17)), lat_range=(1, 1 << 29),
+                              load_range=(0, 1 << 30))
+    else:  # fused chains, prefetch, busy devices
+        win = W.random_window(rng, n_wf=4, nodes=(4, 12), n_dev=D, n_models=6, same_model_bias=0.8,
+                              cap_range=(9000, 20000), w_range=(2000, 5000))
+    win.dev_batch = rng.integers(1, pkg._lib.WF_MAX_BATCH + 1, D).astype(np.int32)
+    if (win.dev_batch == 1).all():
+        win.dev_batch[0] = 2
+    plans = W.random_plans(win, int(rng.integers(64, 700)), rng,
+                           prio_mode=("any", "perm", "globalperm")[seed % 3],
+                           p_bad_dev=0.02 if seed % 5 == 0 else 0.0)
+    got, kern = score(win, plans)
+    log(f"[lean batch] seed {seed}: N={win.n_act} D={D} M={win.n_models} "
+        f"batch={list(win.dev_batch)} kernel={kern}")
+    if win.n_act <= 512 and kern[1] == 32:
+        assert kern[0] == "score_lean"
+    assert got.tobytes() == oracle.score(win, plans, threads=THREADS).tobytes()
+    gen, _ = score(win, plans, general=True)
+    assert got.tobytes() == gen.tobytes()
+
+
+def test_batch_limits_keys_and_replica_caps():
+    """With batch limits the lean kernel scores plans only: ranking keys come
+    from the general kernel, and so does everything once replicas are capped
+    as well."""
+    win, plans = W.make_config(1, n_plans=2048)
+    win.dev_batch = np.full(win.n_dev, 2, np.int32)
+    win.wf_class = (np.arange(win.n_wf) % 4).astype(np.uint8)
+    got, kern = keys(win, plans)
+    assert kern == "score_lean"
+    assert got.tobytes() == oracle.phi_keys(win, plans, threads=THREADS).tobytes()
+    win.model_replica_cap = np.full(win.n_models, win.n_dev, np.int32)
+    got, kern = score(win, plans)
+    assert kern[0] == "score_plans"
+    assert got.tobytes() == oracle.score(win, plans, threads=THREADS).tobytes()
