@@ -833,7 +833,9 @@ int lean_layout(const HostWindow& h, int G, int nwa, wfp::LeanOffsets& o) {
   o.fin = take((size_t)G * h.N * 4);
   o.wfm = take((size_t)G * std::max(1, h.W) * 4);
   o.acc = take((size_t)G * 48);
-  o.hold = take(h.rcap.empty() ? 0 : (size_t)G * h.D * 2);
+  const bool paper = h.victim_order == WF_VICTIM_PAPER;
+  o.hold = take(h.rcap.empty() && !paper ? 0 : (size_t)G * h.D * 2);
+  o.nx = take(paper ? (size_t)G * h.N * 2 : 0);
   o.bytes = (int)off;
   return o.bytes;
 }
@@ -854,10 +856,12 @@ void plan_lean(wf_plan_ctx* ctx, const HostWindow& h, const wfp::ScoreParams& sp
   const char* force = std::getenv("WF_PLAN_KERNEL");
   if (force && std::strcmp(force, "general") == 0) return;
   // (batch limits with the default order: the queue's order, passing over
-  // leased copies; not with replica caps)
+  // leased copies; the paper's order over a resident mask; neither with
+  // replica caps)
   const bool batch = sp.nibble == -2 && h.rcap.empty();
-  if (sp.time64 || (sp.nibble != 32 && sp.nibble != 64 && !batch) || h.N < 1 || h.N > 512 ||
-      h.M > 16 || h.D > 64)
+  const bool paper = sp.nibble == -1 && h.rcap.empty();
+  if (sp.time64 || (sp.nibble != 32 && sp.nibble != 64 && !batch && !paper) || h.N < 1 ||
+      h.N > 512 || h.M > 16 || h.D > 64)
     return;
   const int N = h.N, D = h.D, M = h.M, W = h.W;
   // ---- table image (same words as the general image where they coincide) ----
@@ -947,9 +951,10 @@ void plan_lean(wf_plan_ctx* ctx, const HostWindow& h, const wfp::ScoreParams& sp
   lp.grid = ctx->n_cu * std::max(1, lds_cu / lp.lds_bytes);
   lp.wo = o;
   lp.checked = checked ? 1 : 0;
-  lp.qbits = sp.queue;
+  lp.qbits = paper ? -1 : sp.queue;
   lp.rcap = h.rcap.empty() ? 0 : 1;
   lp.batch = batch ? 1 : 0;
+  lp.paper = paper ? 1 : 0;
   lp.ok = 1;
   // generated candidates: each plan's changed sites live in its finish
   // entries until the walk
@@ -1300,7 +1305,8 @@ wf_status wf_plan_search_batch(wf_plan_ctx* ctx, const int8_t* dev, const uint16
   if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
   const wfp::SearchArgs sa = search_params(ctx, mode, seed, n_mut, first);
   const DeviceWindow& dw = ctx->dw;
-  if (dw.lean.ok && !dw.lean.batch && dw.lean.search_ok && n_mut <= wfp::kLeanMaxMut) {
+  if (dw.lean.ok && !dw.lean.batch && !dw.lean.paper && dw.lean.search_ok &&
+      n_mut <= wfp::kLeanMaxMut) {
     // the lean kernel generates the candidates as the incumbent plus their
     // changed sites; then (times not proven below 2^32) the general fp64
     // pass over the groups holding a candidate whose times saturated
@@ -1418,7 +1424,7 @@ wf_status wf_plan_score_keys(wf_plan_ctx* ctx, const int8_t* dev, const uint16_t
   hipError_t e = hipSetDevice(ctx->device);
   if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
   const DeviceWindow& dw = ctx->dw;
-  if (dw.lean.ok && !dw.lean.batch) {
+  if (dw.lean.ok && !dw.lean.batch && !dw.lean.paper) {
     // the lean kernel's key mode, then the general fp64 pass over the groups
     // holding a plan whose uint32 times saturated
     const wfp::LeanParams lp = lean_grid(dw.lean, n_plans);
@@ -1452,7 +1458,8 @@ wf_status wf_plan_search_keys(wf_plan_ctx* ctx, const int8_t* dev, const uint16_
   if (e != hipSuccess) return hip_fail(ctx, e, "hipSetDevice");
   const wfp::SearchArgs sa = search_params(ctx, mode, seed, n_mut, first);
   const DeviceWindow& dw = ctx->dw;
-  if (dw.lean.ok && !dw.lean.batch && dw.lean.search_ok && n_mut <= wfp::kLeanMaxMut) {
+  if (dw.lean.ok && !dw.lean.batch && !dw.lean.paper && dw.lean.search_ok &&
+      n_mut <= wfp::kLeanMaxMut) {
     const wfp::LeanParams lp = lean_grid(dw.lean, n_candidates);
     e = wfp::launch_score_lean(dw.sp, lp, dev, prio, flags, n_candidates, keys, &sa, true,
                                static_cast<hipStream_t>(hip_stream));

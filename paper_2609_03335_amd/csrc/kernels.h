@@ -11,6 +11,27 @@ namespace wfp {
 
 constexpr int kMaxBatch = WF_MAX_BATCH;  // slots per device in the batch-limit modes
 
+// The paper's reclamation preference (Sec. 3.5): whether copy x is reclaimed
+// before copy y.  red: resident on another device as the level started;
+// nu: device index of the next use (0xffff: none); ld: reload time; lru:
+// last-use stamp (0: never used); k: the current unit's device index.
+// Ratios (nu - k) / ld compare by cross-multiplication; no next use or a
+// free reload is an infinite ratio.
+__device__ __forceinline__ bool paper_victim_before(uint32_t redx, uint32_t nux, uint32_t ldx,
+                                                    uint32_t lrux, uint32_t redy, uint32_t nuy,
+                                                    uint32_t ldy, uint32_t lruy, uint32_t k) {
+  // evaluated without branches: each level of the preference decides only
+  // where all earlier levels tie
+  const bool infx = nux == 0xffffu || ldx == 0u;
+  const bool infy = nuy == 0xffffu || ldy == 0u;
+  const unsigned long long a = (unsigned long long)(nux - k) * ldy;
+  const unsigned long long b = (unsigned long long)(nuy - k) * ldx;
+  const bool ratio_tie = infx || a == b;  // both infinite, or equal finite ratios
+  const bool by_ratio = infx != infy ? infx : (!ratio_tie && a > b);
+  const bool later = infx != infy || !ratio_tie ? by_ratio : lrux < lruy;
+  return redx != redy ? redx > redy : later;
+}
+
 // Byte offsets of the window tables inside the table image.  The host builds
 // the image once per window; the scoring kernel copies it into LDS (or reads
 // it from HBM when it is too large) and uses the same offsets either way.
@@ -145,7 +166,10 @@ struct LeanOffsets {
   int fin;     // u32 [G][N]       latest predecessor finish, then the activation's own finish
   int wfm;     // u32 [G][W]       latest finish per workflow, then its completion latency
   int acc;     // LeanAcc [G]
-  int hold;    // u16 [G][D]       replica caps: models each device held or loaded in the level
+  int hold;    // u16 [G][D]       replica caps: models each device held or loaded in the
+               //                  level; the paper's order: resident models as the level starts
+  int nx;      // u16 [G][N]       the paper's order: per slot, the device index of the next
+               //                  unit of the same model on the device (0xffff: none)
   int bytes;
 };
 
@@ -178,13 +202,14 @@ struct LeanTab {
 };
 
 // Launch plan of the lean kernel (scores or ranking keys of plans read from
-// HBM or generated around an incumbent; uint32 times, at most 16 models in a
-// 4-bit queue, the default reclamation order, at most 512 activations;
-// devices with batch limits for plan scores only).
+// HBM or generated around an incumbent; uint32 times, at most 16 models, at
+// most 512 activations; the default reclamation order in a 4-bit queue, or,
+// for plan scores only, the paper's order over a resident mask; devices with
+// batch limits for plan scores only).
 struct LeanParams {
   int ok;          // 1: the window qualifies and a layout fits in LDS
   int checked;     // 1: uint32 additions saturate and flag the plan for the fp64 pass
-  int qbits;       // reclamation queue width: 32 or 64
+  int qbits;       // reclamation queue width: 32 or 64; -1: no queue (the paper's order)
   int G, waves, grid, lds_bytes;
   const unsigned char* tab;  // the lean table image in HBM
   LeanTab t;
@@ -193,6 +218,7 @@ struct LeanParams {
                    // finish array's storage)
   int rcap;        // 1: the window caps replicas (checked per level)
   int batch;       // 1: devices with batch limits (plan scores only)
+  int paper;       // 1: the paper's reclamation order (plan scores only; qbits -1)
 };
 
 // Generated candidates served by the lean kernel: at most this many

@@ -153,7 +153,8 @@ __device__ __forceinline__ uint32_t umin(uint32_t a, uint32_t b) { return a < b 
 // PHI: each plan's ranking key (Eq. 12) is written instead of its score.
 // RCAP: the window caps replicas (a resident mask beside the queue).
 // BATCH: devices run up to their batch limit of units at once (plan scores
-// only).
+// only).  QB = -1: the paper's reclamation order over a resident mask, no
+// queue (plan scores only).
 template <bool CHECKED, int QB, bool SEARCH, bool PHI, bool RCAP, bool BATCH>
 __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
                                                   const int8_t* __restrict__ dev_all,
@@ -163,6 +164,8 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
   using QT = std::conditional_t<QB == 32, uint32_t, uint64_t>;
   constexpr QT kOnes = (QT)0x1111111111111111ull, kHigh = (QT)0x8888888888888888ull;
   static_assert(!BATCH || (!SEARCH && !PHI && !RCAP), "batch limits: plan scores only");
+  constexpr bool PAPER = QB < 0;
+  static_assert(!PAPER || (!SEARCH && !PHI && !RCAP && !BATCH), "the paper's order: plan scores only");
   extern __shared__ __align__(16) unsigned char lds[];
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
   const int N = sp.N, W = sp.W, M = sp.M, D = sp.D, NB = sp.NB, G = lp.G, NWA = sp.nwa;
@@ -204,6 +207,10 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
   LeanAcc* s_acc = reinterpret_cast<LeanAcc*>(wl + lp.wo.acc);
   uint32_t* s_pat = s_fin;  // generated candidates' changed sites (until the walk)
   uint16_t* s_hold = reinterpret_cast<uint16_t*>(wl + lp.wo.hold);  // replica caps
+  // the paper's order: resident models of each device as the level starts
+  // (in the replica caps' region), next use per slot
+  uint16_t* s_snap = s_hold;
+  uint16_t* s_nx = reinterpret_cast<uint16_t*>(wl + lp.wo.nx);
 
   const int g_me = lane / D;
   const int d_me = lane - g_me * D;
@@ -518,18 +525,43 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
       for (uint64_t r = res; r; r &= r - 1) {
         const int m = __builtin_ctzll(r);
         used += t_wmib[m];
-        if (mylast[m] == 0u) {
-          Q |= (QT)m << nd4;
-          nd4 += 4;
-        } else {
-          qa |= (QT)m << na;
-          na += 4;
+        if constexpr (!PAPER) {
+          if (mylast[m] == 0u) {
+            Q |= (QT)m << nd4;
+            nd4 += 4;
+          } else {
+            qa |= (QT)m << na;
+            na += 4;
+          }
         }
       }
       if (na) Q |= qa << nd4;  // nd4 + na <= QB here
       nq4 = nd4 + na;
       fm = capd - used;
       pe = used - capd;
+    }
+    // the paper's order: per model the device index of its next use (low 16
+    // bits, 0xffff: none) and its last-use stamp (high 16 bits, 0: not used
+    // yet), in the last-slot region; one backward pass over the device's
+    // units gives every slot the next use of its model after it
+    uint32_t* mypk = s_last + (gme * D + d) * M;
+    uint32_t kdev = 0u, seq = 1u, others = 0u;
+    if (PAPER && act) {
+      for (int m = 0; m < M; ++m) mypk[m] = 0xffffu;
+      int cnt = 0;
+      for (int j = 0; j < NWA; ++j) cnt += __popcll(mymask64[j]);
+      uint16_t* mynx = s_nx + gme * N;
+      for (int j = NWA - 1; j >= 0; --j)
+        for (unsigned long long bits = mymask64[j]; bits;) {
+          const int b = 63 - __clzll(bits);
+          bits &= ~(1ull << b);
+          const int sl = (j << 6) + b;
+          const uint32_t m = ((uint32_t)myrec[sl] >> 9) & 15u;
+          --cnt;
+          mynx[sl] = (uint16_t)mypk[m];
+          mypk[m] = (uint32_t)cnt;
+        }
+      s_snap[gme * D + d] = (uint16_t)rmask;
     }
 
     // every finish starts at 0: it accumulates the latest predecessor finish
@@ -565,6 +597,11 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
 
       // ---- device lanes walk their units of the level in slot order ----
       lv_hold = rmask;
+      if (PAPER && act) {
+        // models resident on the plan's other devices as the level starts
+        others = 0u;
+        for (int e = 0; e < D; ++e) others |= e != d ? (uint32_t)s_snap[gme * D + e] : 0u;
+      }
       if (act) {
         const int j1 = (hi - 1) >> 6;
         const unsigned long long hmask = (hi & 63) ? ((1ull << (hi & 63)) - 1ull) : ~0ull;
@@ -610,7 +647,7 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
           const uint32_t e = sl >= 0 ? (uint32_t)myrec[sl] : 0u;
           X.e = e;
           const uint32_t u = e & kEAct, m = (e >> 9) & 15u;
-          X.lst = mylast[m] == (uint32_t)sl + 1u ? 1u : 0u;
+          X.lst = !PAPER && mylast[m] == (uint32_t)sl + 1u ? 1u : 0u;
           const int2 r = um_d[u];
           X.lat = r.x;
           X.mem = r.y;
@@ -641,30 +678,62 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
           // residency: m is resident when its nibble is among the first
           // nq4 / 4 entries; a hit takes it out of the queue (it re-enters
           // below as the most recent)
-          QT mq = (QT)(uint32_t)X.lw.z;
-          if constexpr (QB == 64) mq |= mq << 32;
-          const QT x = Q ^ mq;
-          QT z = (x - kOnes) & ~x & kHigh;  // lowest flag: first zero nibble
-          const QT valid = nq4 >= (uint32_t)QB ? ~(QT)0 : (((QT)1 << nq4) - (QT)1);
-          z &= valid;
-          const bool hit = z != (QT)0;
-          uint32_t s4;
-          if constexpr (QB == 64)
-            s4 = (uint32_t)__builtin_ctzll(z | (1ull << 63)) & ~3u;
-          else
-            s4 = (uint32_t)__builtin_ctz(z | (1u << 31)) & ~3u;
-          {
+          // (the paper's order: the resident mask)
+          bool hit;
+          if constexpr (PAPER) {
+            hit = ((rmask >> m) & 1u) != 0u;
+          } else {
+            QT mq = (QT)(uint32_t)X.lw.z;
+            if constexpr (QB == 64) mq |= mq << 32;
+            const QT x = Q ^ mq;
+            QT z = (x - kOnes) & ~x & kHigh;  // lowest flag: first zero nibble
+            const QT valid = nq4 >= (uint32_t)QB ? ~(QT)0 : (((QT)1 << nq4) - (QT)1);
+            z &= valid;
+            hit = z != (QT)0;
+            uint32_t s4;
+            if constexpr (QB == 64)
+              s4 = (uint32_t)__builtin_ctzll(z | (1ull << 63)) & ~3u;
+            else
+              s4 = (uint32_t)__builtin_ctz(z | (1u << 31)) & ~3u;
             const QT lowm = ((QT)1 << s4) - (QT)1;
             const QT rem = (Q & lowm) | ((Q >> 4) & ~lowm);
             Q = hit ? rem : Q;
+            nq4 -= hit ? 4u : 0u;
           }
-          nq4 -= hit ? 4u : 0u;
           const int32_t need = mx + (hit ? 0 : X.lw.y);
           int32_t ex;       // > 0: the unit does not fit yet
           int32_t run = 0;  // memory of the units still running (batch limits)
           int ks = 0;       // batch limits: the unit's slot, and its dispatch time
           uint32_t t0 = 0u;
-          if constexpr (BATCH) {
+          if constexpr (PAPER) {
+            ex = need - fm;
+            // reclaim (Sec. 3.5) in the paper's order: copies resident on
+            // another device of the plan first, then the longest distance to
+            // the next use per reload time, then least recently used (equal
+            // keys: the lower model id)
+            for (uint32_t cand = rmask & ~(1u << m); ex > 0 && cand != 0u;) {
+              uint32_t c = cand;
+              int v = __builtin_ctz(c);
+              uint32_t vpk = mypk[v];
+              int4 vlw = lw_d[v];
+              for (c &= c - 1u; c; c &= c - 1u) {
+                const int m2 = __builtin_ctz(c);
+                const uint32_t pk = mypk[m2];
+                const int4 lw2 = lw_d[m2];
+                if (paper_victim_before((others >> m2) & 1u, pk & 0xffffu, (uint32_t)lw2.x, pk >> 16,
+                                        (others >> v) & 1u, vpk & 0xffffu, (uint32_t)vlw.x,
+                                        vpk >> 16, kdev)) {
+                  v = m2;
+                  vpk = pk;
+                  vlw = lw2;
+                }
+              }
+              cand &= ~(1u << v);
+              rmask &= ~(1u << v);
+              ex -= vlw.y;
+              nev4 += 4u;
+            }
+          } else if constexpr (BATCH) {
             // the slot that frees first; units dispatch in order, at the
             // release (the arrival for a prefetched load) at the earliest
             uint32_t sft = bs_fin[0];
@@ -753,8 +822,13 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
           pe = ex > pe ? ex : pe;
           fm = mx + run - ex;
           // m re-enters after the no-remaining-use part when this was its
-          // last unit on the device, else at the end
-          {
+          // last unit on the device, else at the end (the paper's order: its
+          // next use and last-use stamp)
+          if constexpr (PAPER) {
+            mypk[m] = (uint32_t)s_nx[gme * N + X.slot] | (seq << 16);
+            ++seq;
+            ++kdev;
+          } else {
             const uint32_t pos = X.lst ? nd4 : nq4;
             const QT lowm = ((QT)1 << pos) - (QT)1;
             Q = (Q & lowm) | ((QT)m << pos) | ((Q & ~lowm) << 4);
@@ -762,10 +836,8 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
             nq4 += 4u;
           }
           nld += hit ? 0u : 1u;
-          if constexpr (RCAP) {
-            rmask |= 1u << m;
-            lv_hold |= 1u << m;
-          }
+          if constexpr (RCAP || PAPER) rmask |= 1u << m;
+          if constexpr (RCAP) lv_hold |= 1u << m;
           // timeline (Eq. 7): a load waits for the device and starts at the
           // release, or at the workflow arrival when prefetched; the unit
           // starts at max(release, load end), or at max(release, device
@@ -839,6 +911,7 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
           run(next_wide);
       }
       if (RCAP && act) s_hold[gme * D + d] = (uint16_t)lv_hold;
+      if (PAPER && act) s_snap[gme * D + d] = (uint16_t)rmask;
       lsync();
       // ---- replica caps (Sec. 3.5 scale-out): a model held or loaded in
       // this level on more devices than its cap; lanes over (plan, model) ----
@@ -1020,6 +1093,15 @@ hipError_t launch_score_lean(const ScoreParams& sp, const LeanParams& lp, const 
                              void* out, const SearchArgs* search, bool keys, hipStream_t stream) {
   const SearchArgs sa = search ? *search : SearchArgs{};
   wf_plan_score* o = static_cast<wf_plan_score*>(out);
+  if (lp.paper) {
+    // the paper's reclamation order: plan scores only
+    if (search || keys || lp.rcap || lp.batch) return hipErrorInvalidValue;
+    if (lp.checked)
+      return launch_lean_variant<true, -1, false, false, false, false>(sp, lp, dev, prio, flags,
+                                                                       n_plans, o, sa, stream);
+    return launch_lean_variant<false, -1, false, false, false, false>(sp, lp, dev, prio, flags,
+                                                                      n_plans, o, sa, stream);
+  }
   if (lp.batch) {
     // windows with batch limits: plan scores only
     if (search || keys || lp.rcap) return hipErrorInvalidValue;

@@ -133,27 +133,6 @@ constexpr uint32_t kChain = 1u << 23;
 constexpr uint32_t kLast = 1u << 30;
 constexpr uint32_t kSlow = 1u << 31;
 
-// The paper's reclamation preference (Sec. 3.5): whether copy x is reclaimed
-// before copy y.  red: resident on another device as the level started;
-// nu: device index of the next use (0xffff: none); ld: reload time; lru:
-// last-use stamp (0: never used); k: the current unit's device index.
-// Ratios (nu - k) / ld compare by cross-multiplication; no next use or a
-// free reload is an infinite ratio.
-__device__ __forceinline__ bool paper_victim_before(uint32_t redx, uint32_t nux, uint32_t ldx,
-                                                    uint32_t lrux, uint32_t redy, uint32_t nuy,
-                                                    uint32_t ldy, uint32_t lruy, uint32_t k) {
-  // evaluated without branches: each level of the preference decides only
-  // where all earlier levels tie
-  const bool infx = nux == 0xffffu || ldx == 0u;
-  const bool infy = nuy == 0xffffu || ldy == 0u;
-  const unsigned long long a = (unsigned long long)(nux - k) * ldy;
-  const unsigned long long b = (unsigned long long)(nuy - k) * ldx;
-  const bool ratio_tie = infx || a == b;  // both infinite, or equal finite ratios
-  const bool by_ratio = infx != infy ? infx : (!ratio_tie && a > b);
-  const bool later = infx != infy || !ratio_tie ? by_ratio : lrux < lruy;
-  return redx != redy ? redx > redy : later;
-}
-
 // What the device walk needs about one unit that does not depend on the
 // device's sequential state; it is loaded one unit ahead of its use.
 template <typename TT>

@@ -207,3 +207,55 @@ def test_batch_limits_keys_and_replica_caps():
     got, kern = score(win, plans)
     assert kern[0] == "score_plans"
     assert got.tobytes() == oracle.score(win, plans, threads=THREADS).tobytes()
+
+
+@pytest.mark.parametrize("cfg,n", [(0, 512), (1, 16384), (4, 65536)])
+def test_paper_order_in_the_lean_kernel(cfg, n):
+    """The paper's reclamation order (copies held on another device as the
+    level starts, then next-use distance per reload time, then recency) in
+    the lean kernel against the oracle and the general kernel."""
+    win, plans = W.make_config(cfg, n_plans=n)
+    win.victim_order = 1
+    log(f"[lean paper] config {cfg}: {n} plans")
+    got, kern = score(win, plans)
+    assert kern[0] == "score_lean"
+    assert got.tobytes() == oracle.score(win, plans, threads=THREADS).tobytes()
+    gen, kern_g = score(win, plans, general=True)
+    assert kern_g[0] == "score_plans"
+    assert got.tobytes() == gen.tobytes()
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_paper_order_random_windows(seed):
+    rng = np.random.default_rng(39_000 + seed)
+    kw = dict(n_wf=int(rng.integers(1, 7)), nodes=(1, 12), n_dev=int(rng.integers(1, 13)),
+              n_models=int(rng.integers(1, 17)), same_model_bias=0.6)
+    if seed % 4 == 1:  # tight memory: frequent reclamation among several copies
+        kw.update(cap_range=(3000, 12000), w_range=(1000, 9000))
+    if seed % 4 == 2:  # long loads and run times: uint32 times checked, some saturate
+        kw.update(lat_range=(1, 1 << 29), load_range=(0, 1 << 30))
+    if seed % 4 == 3:  # free reloads (infinite ratios) next to costly ones
+        kw.update(load_range=(0, 3), cap_range=(4000, 14000), w_range=(1000, 6000))
+    win = W.random_window(rng, **kw)
+    win.victim_order = 1
+    plans = W.random_plans(win, int(rng.integers(64, 700)), rng,
+                           prio_mode=("any", "perm", "globalperm")[seed % 3],
+                           p_bad_dev=0.02 if seed % 5 == 0 else 0.0)
+    got, kern = score(win, plans)
+    log(f"[lean paper] seed {seed}: N={win.n_act} D={win.n_dev} M={win.n_models} kernel={kern}")
+    if win.n_act <= 512 and kern[1] == 32:
+        assert kern[0] == "score_lean"
+    assert got.tobytes() == oracle.score(win, plans, threads=THREADS).tobytes()
+    gen, _ = score(win, plans, general=True)
+    assert got.tobytes() == gen.tobytes()
+
+
+def test_paper_order_keys_stay_general():
+    """With the paper's order the lean kernel scores plans only: ranking keys
+    come from the general kernel."""
+    win, plans = W.make_config(1, n_plans=2048)
+    win.victim_order = 1
+    win.wf_class = (np.arange(win.n_wf) % 4).astype(np.uint8)
+    got, kern = keys(win, plans)
+    assert kern == "score_lean"
+    assert got.tobytes() == oracle.phi_keys(win, plans, threads=THREADS).tobytes()
