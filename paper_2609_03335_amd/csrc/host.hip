@@ -835,7 +835,9 @@ int lean_layout(const HostWindow& h, int G, int nwa, wfp::LeanOffsets& o) {
   o.acc = take((size_t)G * 48);
   const bool paper = h.victim_order == WF_VICTIM_PAPER;
   o.hold = take(h.rcap.empty() && !paper ? 0 : (size_t)G * h.D * 2);
-  o.nx = take(paper ? (size_t)G * h.N * 2 : 0);
+  // (next uses in one byte for at most 256 activations: no next use is 0,
+  // as a device's first unit is nobody's next)
+  o.nx = take(paper ? (size_t)G * h.N * (h.N <= 256 ? 1 : 2) : 0);
   o.bytes = (int)off;
   return o.bytes;
 }

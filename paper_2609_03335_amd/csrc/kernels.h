@@ -168,8 +168,9 @@ struct LeanOffsets {
   int acc;     // LeanAcc [G]
   int hold;    // u16 [G][D]       replica caps: models each device held or loaded in the
                //                  level; the paper's order: resident models as the level starts
-  int nx;      // u16 [G][N]       the paper's order: per slot, the device index of the next
-               //                  unit of the same model on the device (0xffff: none)
+  int nx;      // u8 or u16 [G][N] the paper's order: per slot, the device index of the next
+               //                  unit of the same model on the device (u8 for N <= 256, with
+               //                  0 for none; u16 with 0xffff for none)
   int bytes;
 };
 

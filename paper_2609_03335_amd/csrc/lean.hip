@@ -211,6 +211,8 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
   // (in the replica caps' region), next use per slot
   uint16_t* s_snap = s_hold;
   uint16_t* s_nx = reinterpret_cast<uint16_t*>(wl + lp.wo.nx);
+  uint8_t* s_nx8 = wl + lp.wo.nx;  // at most 256 activations: one byte, 0 for none
+  const bool nx8 = N <= 256;
 
   const int g_me = lane / D;
   const int d_me = lane - g_me * D;
@@ -550,7 +552,6 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
       for (int m = 0; m < M; ++m) mypk[m] = 0xffffu;
       int cnt = 0;
       for (int j = 0; j < NWA; ++j) cnt += __popcll(mymask64[j]);
-      uint16_t* mynx = s_nx + gme * N;
       for (int j = NWA - 1; j >= 0; --j)
         for (unsigned long long bits = mymask64[j]; bits;) {
           const int b = 63 - __clzll(bits);
@@ -558,7 +559,10 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
           const int sl = (j << 6) + b;
           const uint32_t m = ((uint32_t)myrec[sl] >> 9) & 15u;
           --cnt;
-          mynx[sl] = (uint16_t)mypk[m];
+          if (nx8)
+            s_nx8[gme * N + sl] = mypk[m] == 0xffffu ? (uint8_t)0 : (uint8_t)mypk[m];
+          else
+            s_nx[gme * N + sl] = (uint16_t)mypk[m];
           mypk[m] = (uint32_t)cnt;
         }
       s_snap[gme * D + d] = (uint16_t)rmask;
@@ -711,26 +715,42 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
             // another device of the plan first, then the longest distance to
             // the next use per reload time, then least recently used (equal
             // keys: the lower model id)
+            auto ldw = [&](int x) { return *reinterpret_cast<const int2*>(lw_d + x); };
             for (uint32_t cand = rmask & ~(1u << m); ex > 0 && cand != 0u;) {
-              uint32_t c = cand;
-              int v = __builtin_ctz(c);
-              uint32_t vpk = mypk[v];
-              int4 vlw = lw_d[v];
-              for (c &= c - 1u; c; c &= c - 1u) {
-                const int m2 = __builtin_ctz(c);
-                const uint32_t pk = mypk[m2];
-                const int4 lw2 = lw_d[m2];
-                if (paper_victim_before((others >> m2) & 1u, pk & 0xffffu, (uint32_t)lw2.x, pk >> 16,
-                                        (others >> v) & 1u, vpk & 0xffffu, (uint32_t)vlw.x,
-                                        vpk >> 16, kdev)) {
-                  v = m2;
+              // a copy held on another device goes before any other: when
+              // there are such copies the choice is among them; the first
+              // three candidates' keys are read at once
+              const uint32_t cr = cand & others;
+              uint32_t sel = cr ? cr : cand;
+              const int ca = __builtin_ctz(sel);
+              sel &= sel - 1u;
+              const int cb = sel ? __builtin_ctz(sel) : ca;
+              sel &= sel - 1u;
+              const int cc = sel ? __builtin_ctz(sel) : ca;
+              sel &= sel - 1u;
+              const uint32_t pa = mypk[ca], pb = mypk[cb], pc = mypk[cc];
+              const int2 la = ldw(ca), lb = ldw(cb), lc = ldw(cc);
+              int v = ca;
+              uint32_t vpk = pa;
+              int2 vl = la;
+              // (ascending ids: equal keys keep the lower id)
+              auto consider = [&](int x, uint32_t pk, int2 l) {
+                if (paper_victim_before(0u, pk & 0xffffu, (uint32_t)l.x, pk >> 16, 0u, vpk & 0xffffu,
+                                        (uint32_t)vl.x, vpk >> 16, kdev)) {
+                  v = x;
                   vpk = pk;
-                  vlw = lw2;
+                  vl = l;
                 }
+              };
+              if (cb != ca) consider(cb, pb, lb);
+              if (cc != ca) consider(cc, pc, lc);
+              for (; sel; sel &= sel - 1u) {
+                const int m2 = __builtin_ctz(sel);
+                consider(m2, mypk[m2], ldw(m2));
               }
               cand &= ~(1u << v);
               rmask &= ~(1u << v);
-              ex -= vlw.y;
+              ex -= vl.y;
               nev4 += 4u;
             }
           } else if constexpr (BATCH) {
@@ -825,7 +845,14 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
           // last unit on the device, else at the end (the paper's order: its
           // next use and last-use stamp)
           if constexpr (PAPER) {
-            mypk[m] = (uint32_t)s_nx[gme * N + X.slot] | (seq << 16);
+            uint32_t nu;
+            if (nx8) {
+              nu = s_nx8[gme * N + X.slot];
+              nu = nu ? nu : 0xffffu;
+            } else {
+              nu = s_nx[gme * N + X.slot];
+            }
+            mypk[m] = nu | (seq << 16);
             ++seq;
             ++kdev;
           } else {

@@ -259,3 +259,23 @@ def test_paper_order_keys_stay_general():
     got, kern = keys(win, plans)
     assert kern == "score_lean"
     assert got.tobytes() == oracle.phi_keys(win, plans, threads=THREADS).tobytes()
+
+
+@pytest.mark.parametrize("n_act", [256, 320])
+def test_paper_order_one_device_many_units(n_act):
+    """Every unit of most plans on device 0 of eight: next-use indices up to
+    n_act - 1 (one-byte entries up to 256 activations, two-byte entries
+    beyond)."""
+    rng = np.random.default_rng(41_000 + n_act)
+    win = W.random_window(rng, n_wf=n_act // 16, nodes=(16, 16), n_dev=8, n_models=5,
+                          cap_range=(6000, 9000), w_range=(1000, 4000), mem_range=(0, 1000),
+                          q_inel=0.0, same_model_bias=0.2)
+    assert win.n_act == n_act
+    win.victim_order = 1
+    plans = W.random_plans(win, 128, rng, prio_mode="perm")
+    plans.dev[:120] = 0
+    got, kern = score(win, plans)
+    assert kern[0] == "score_lean"
+    ref = oracle.score(win, plans, threads=THREADS)
+    assert got.tobytes() == ref.tobytes()
+    assert (ref["n_evicts"][:120] > 0).all()
