@@ -829,11 +829,19 @@ int lean_layout(const HostWindow& h, int G, int nwa, wfp::LeanOffsets& o) {
   o.flags = take((size_t)G * NB);
   o.rec = take((size_t)G * h.N * 2);
   o.mask = take((size_t)G * h.D * nwa * 8);
-  o.last = take((size_t)G * h.D * h.M * 4);
+  const size_t last_bytes = (size_t)G * h.D * h.M * 4;
+  const bool paper = h.victim_order == WF_VICTIM_PAPER;
   o.fin = take((size_t)G * h.N * 4);
+  // the last slots are read before the walk starts, so they share the
+  // finish region (after the candidates' changed sites) where they fit; the
+  // paper's order keeps its per-model keys there during the walk
+  const size_t patch_bytes = align_up((size_t)G * wfp::kLeanPatchWords * 4, 16);
+  if (!paper && patch_bytes + last_bytes <= (size_t)G * h.N * 4)
+    o.last = o.fin + (int)patch_bytes;
+  else
+    o.last = take(last_bytes);
   o.wfm = take((size_t)G * std::max(1, h.W) * 4);
   o.acc = take((size_t)G * 48);
-  const bool paper = h.victim_order == WF_VICTIM_PAPER;
   o.hold = take(h.rcap.empty() && !paper ? 0 : (size_t)G * h.D * 2);
   // (next uses in one byte for at most 256 activations: no next use is 0,
   // as a device's first unit is nobody's next)
@@ -842,16 +850,13 @@ int lean_layout(const HostWindow& h, int G, int nwa, wfp::LeanOffsets& o) {
   return o.bytes;
 }
 
-// waves per workgroup of the lean kernel: two per SIMD
-constexpr int kLeanMaxWaves = 8;
 
 // Whether the lean kernel serves this window's plan scores, and its table
-// image and launch plan: uint32 times (proven or checked), the 4-bit
-// reclamation queue (at most 16 models, the default order, one unit per
-// device), at most 512 activations (9-bit slot entries), and the tables
-// plus the waves' regions in LDS.  Plans per wave: 64 / D; as many waves as
-// LDS holds, at most 8 per workgroup (two per SIMD at the kernel's register
-// use).
+// image and launch plan: uint32 times (proven or checked), at most 16
+// models, at most 512 activations (9-bit slot entries), and the tables plus
+// the waves' regions in LDS.  Plans per wave: 64 / D; as many waves as LDS
+// holds, at most 10 per workgroup for the queue variants without batch
+// limits (three per SIMD) and 8 for the others (two per SIMD).
 void plan_lean(wf_plan_ctx* ctx, const HostWindow& h, const wfp::ScoreParams& sp, bool checked,
                Image& img, wfp::LeanParams& lp) {
   lp = wfp::LeanParams{};
@@ -945,12 +950,16 @@ void plan_lean(wf_plan_ctx* ctx, const HostWindow& h, const wfp::ScoreParams& sp
   const int G = std::max(1, 64 / D);
   wfp::LeanOffsets o{};
   const int wb = lean_layout(h, G, sp.nwa, o);
-  const int waves = std::min(kLeanMaxWaves, (lds_blk - t.lds_bytes) / std::max(wb, 1));
+  const int fit = (lds_blk - t.lds_bytes) / std::max(wb, 1);
+  const int waves = std::min(wfp::kLeanWaves, fit);
   if (waves < 2) return;
   lp.G = G;
   lp.waves = waves;
   lp.lds_bytes = t.lds_bytes + waves * wb;
   lp.grid = ctx->n_cu * std::max(1, lds_cu / lp.lds_bytes);
+  lp.xwaves = std::min(wfp::kLeanPlainWaves, fit);
+  lp.xlds_bytes = t.lds_bytes + lp.xwaves * wb;
+  lp.xgrid = ctx->n_cu * std::max(1, lds_cu / lp.xlds_bytes);
   lp.wo = o;
   lp.checked = checked ? 1 : 0;
   lp.qbits = paper ? -1 : sp.queue;
@@ -1210,9 +1219,10 @@ wf_status wf_plan_upload_window(wf_plan_ctx* ctx, const wf_window_desc* w) {
                  "behind), widest level %d, %d mask words per device\n", sp.ring_size, sp.ring_a,
                  sp.ring_b, sp.ring_w, sp.nwa);
   if (std::getenv("WF_PLAN_VERBOSE") && dw.lean.ok)
-    std::fprintf(stderr, "[wf_plan] lean kernel: G=%d waves/wg=%d grid=%d tables=%d B wave=%d B lds/wg=%d\n",
-                 dw.lean.G, dw.lean.waves, dw.lean.grid, dw.lean.t.bytes, dw.lean.wo.bytes,
-                 dw.lean.lds_bytes);
+    std::fprintf(stderr, "[wf_plan] lean kernel: G=%d waves/wg=%d (queue variants %d) grid=%d (%d) "
+                 "tables=%d B wave=%d B lds/wg=%d (%d)\n",
+                 dw.lean.G, dw.lean.waves, dw.lean.xwaves, dw.lean.grid, dw.lean.xgrid,
+                 dw.lean.t.bytes, dw.lean.wo.bytes, dw.lean.lds_bytes, dw.lean.xlds_bytes);
   free_device_window(ctx->dw);
   ctx->dw = dw;
   ctx->host = std::move(h);

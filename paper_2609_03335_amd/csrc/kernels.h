@@ -72,7 +72,10 @@ struct WaveOffsets {
   int flags;   // u8 [G][NB]       staged fuse/prefetch rows
   int rec;     // u32 [G][N]       slot entry per resource-order slot (packed)
   int mask;    // u64 [G][D][NWA]  slots of each device's units
-  int last;    // u32 [G][D][M]    1 + slot of the last unit of each (device, model), 0 = none;
+  int last;    // u32 [G][D][M]    1 + slot of the last unit of each (device, model), 0 = none
+               //                  (until the walk: inside the finish region, after the
+               //                  candidates' changed sites, where it fits); the paper's
+               //                  order: next use and last-use stamp of each model;
                //                  with the in-register reclamation queues it shares storage
                //                  with fin (dead before the first finish is written)
   int fin;     // time [G][N]      latest predecessor finish, then the activation's own finish
@@ -163,6 +166,9 @@ struct LeanOffsets {
                //                  prefetch << 13 | fused successor << 14
   int mask;    // u64 [G][D][NWA]  slots of each device's units
   int last;    // u32 [G][D][M]    1 + slot of the last unit of each (device, model), 0 = none
+               //                  (until the walk: inside the finish region, after the
+               //                  candidates' changed sites, where it fits); the paper's
+               //                  order: next use and last-use stamp of each model
   int fin;     // u32 [G][N]       latest predecessor finish, then the activation's own finish
   int wfm;     // u32 [G][W]       latest finish per workflow, then its completion latency
   int acc;     // LeanAcc [G]
@@ -220,12 +226,23 @@ struct LeanParams {
   int rcap;        // 1: the window caps replicas (checked per level)
   int batch;       // 1: devices with batch limits (plan scores only)
   int paper;       // 1: the paper's reclamation order (plan scores only; qbits -1)
+  // the variants with the reclamation queue and no batch limits are built
+  // for three waves per SIMD: up to kLeanPlainWaves waves per workgroup,
+  // their own launch
+  int xwaves, xgrid, xlds_bytes;
 };
+
+// Waves per workgroup of the lean kernel: the variants above, and those with
+// batch limits or the paper's order.
+constexpr int kLeanPlainWaves = 10;
+constexpr int kLeanWaves = 8;
 
 // Generated candidates served by the lean kernel: at most this many
 // mutations each (a candidate is the incumbent plus at most 2 changed sites
 // per mutation).
 constexpr int kLeanMaxMut = 8;
+// words of one candidate's changed sites (a count, then 4 words per mutation)
+constexpr int kLeanPatchWords = 1 + 4 * kLeanMaxMut;
 
 struct SearchArgs;
 

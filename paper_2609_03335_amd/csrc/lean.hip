@@ -39,7 +39,7 @@ namespace {
 
 // A candidate as the incumbent's rows plus the changed sites: per plan a
 // count, then 2 words per site (activation | priority << 16, device).
-constexpr int kPatchWords = 1 + 4 * kLeanMaxMut;
+constexpr int kPatchWords = kLeanPatchWords;
 
 struct PatchRows {
   uint32_t* p;             // this plan's count and sites
@@ -103,6 +103,7 @@ static_assert(sizeof(LeanAcc) == 48, "LeanAcc layout");
 constexpr uint32_t kEAct = 0x1ffu;
 constexpr uint32_t kEPf = 1u << 13;
 constexpr uint32_t kEChain = 1u << 14;
+constexpr uint32_t kELast = 1u << 15;  // the model's last unit on the device (set before the walk)
 
 __device__ __forceinline__ void lsync() {
   __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
@@ -155,8 +156,18 @@ __device__ __forceinline__ uint32_t umin(uint32_t a, uint32_t b) { return a < b 
 // BATCH: devices run up to their batch limit of units at once (plan scores
 // only).  QB = -1: the paper's reclamation order over a resident mask, no
 // queue (plan scores only).
+// Variants built for three waves per SIMD (the queue without batch limits;
+// a few registers of the key and replica-cap variants spill, which costs
+// less than the waves gained); batch limits and the paper's order keep two.
+template <bool SEARCH, bool PHI, bool RCAP, bool BATCH, int QB>
+constexpr bool lean_plain() {
+  return !BATCH && QB > 0;
+}
+
 template <bool CHECKED, int QB, bool SEARCH, bool PHI, bool RCAP, bool BATCH>
-__global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
+__global__ __launch_bounds__(64 * (lean_plain<SEARCH, PHI, RCAP, BATCH, QB>() ? kLeanPlainWaves
+                                                                                : kLeanWaves))
+void score_lean(ScoreParams sp, LeanParams lp,
                                                   const int8_t* __restrict__ dev_all,
                                                   const uint16_t* __restrict__ prio_all,
                                                   const uint8_t* __restrict__ flags_all, int64_t P,
@@ -477,6 +488,23 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
     uint16_t* myrec = s_rec + gme * N;
     uint32_t* myfin = s_fin + gme * N;
     const uint8_t* myfl = s_fl + gme * NB;
+    // the last unit of each model on the device gets its flag; the models
+    // the device uses at all (read before the finish region is cleared)
+    // (every read issued before any write: M <= 16)
+    uint32_t umask = 0u;
+    if (!PAPER && act) {
+      uint32_t lv[16], ev[16];
+#pragma unroll
+      for (int m = 0; m < 16; ++m) lv[m] = m < M ? mylast[m] : 0u;
+#pragma unroll
+      for (int m = 0; m < 16; ++m) ev[m] = lv[m] ? (uint32_t)myrec[lv[m] - 1u] : 0u;
+#pragma unroll
+      for (int m = 0; m < 16; ++m)
+        if (lv[m]) {
+          myrec[lv[m] - 1u] = (uint16_t)(ev[m] | kELast);
+          umask |= 1u << m;
+        }
+    }
     // reclamation queue of the resident models, 4 bits each, next victim in
     // the low bits: first the nd4 / 4 models with no remaining use on this
     // device, then those still needed, each part least recently used first
@@ -528,7 +556,7 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
         const int m = __builtin_ctzll(r);
         used += t_wmib[m];
         if constexpr (!PAPER) {
-          if (mylast[m] == 0u) {
+          if (!((umask >> m) & 1u)) {
             Q |= (QT)m << nd4;
             nd4 += 4;
           } else {
@@ -651,7 +679,7 @@ __global__ __launch_bounds__(512) void score_lean(ScoreParams sp, LeanParams lp,
           const uint32_t e = sl >= 0 ? (uint32_t)myrec[sl] : 0u;
           X.e = e;
           const uint32_t u = e & kEAct, m = (e >> 9) & 15u;
-          X.lst = !PAPER && mylast[m] == (uint32_t)sl + 1u ? 1u : 0u;
+          X.lst = !PAPER && (e & kELast) ? 1u : 0u;
           const int2 r = um_d[u];
           X.lat = r.x;
           X.mem = r.y;
@@ -1075,9 +1103,17 @@ hipError_t launch_lean_variant(const ScoreParams& sp, const LeanParams& lp, cons
                                const uint16_t* prio, const uint8_t* flags, int64_t n_plans,
                                wf_plan_score* scores, const SearchArgs& sa, hipStream_t stream) {
   auto k = score_lean<CHECKED, QB, SEARCH, PHI, RCAP, BATCH>;
+  LeanParams l = lp;
+  if (lean_plain<SEARCH, PHI, RCAP, BATCH, QB>()) {
+    // the plain variant's own launch, its grid fitted to the plans
+    l.waves = lp.xwaves;
+    l.lds_bytes = lp.xlds_bytes;
+    const int64_t wgs = ((n_plans + lp.G - 1) / lp.G + l.waves - 1) / l.waves;
+    l.grid = wgs < lp.xgrid ? (int)wgs : lp.xgrid;
+  }
   (void)hipFuncSetAttribute(reinterpret_cast<const void*>(k),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, lp.lds_bytes);
-  hipLaunchKernelGGL(k, dim3(lp.grid), dim3(64 * lp.waves), lp.lds_bytes, stream, sp, lp, dev, prio,
+                            hipFuncAttributeMaxDynamicSharedMemorySize, l.lds_bytes);
+  hipLaunchKernelGGL(k, dim3(l.grid), dim3(64 * l.waves), l.lds_bytes, stream, sp, l, dev, prio,
                      flags, n_plans, scores, sa);
   return hipGetLastError();
 }
