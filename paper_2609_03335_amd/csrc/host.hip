@@ -855,8 +855,8 @@ int lean_layout(const HostWindow& h, int G, int nwa, wfp::LeanOffsets& o) {
 // image and launch plan: uint32 times (proven or checked), at most 16
 // models, at most 512 activations (9-bit slot entries), and the tables plus
 // the waves' regions in LDS.  Plans per wave: 64 / D; as many waves as LDS
-// holds, at most 10 per workgroup for the queue variants without batch
-// limits (three per SIMD) and 8 for the others (two per SIMD).
+// holds, at most 10 per workgroup for the queue variants (three per SIMD)
+// and 8 for the paper's order (two per SIMD).
 void plan_lean(wf_plan_ctx* ctx, const HostWindow& h, const wfp::ScoreParams& sp, bool checked,
                Image& img, wfp::LeanParams& lp) {
   lp = wfp::LeanParams{};

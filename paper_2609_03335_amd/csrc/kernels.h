@@ -226,14 +226,13 @@ struct LeanParams {
   int rcap;        // 1: the window caps replicas (checked per level)
   int batch;       // 1: devices with batch limits (plan scores only)
   int paper;       // 1: the paper's reclamation order (plan scores only; qbits -1)
-  // the variants with the reclamation queue and no batch limits are built
-  // for three waves per SIMD: up to kLeanPlainWaves waves per workgroup,
-  // their own launch
+  // the variants with the reclamation queue are built for three waves per
+  // SIMD: up to kLeanPlainWaves waves per workgroup, their own launch
   int xwaves, xgrid, xlds_bytes;
 };
 
-// Waves per workgroup of the lean kernel: the variants above, and those with
-// batch limits or the paper's order.
+// Waves per workgroup of the lean kernel: the queue variants, and the
+// paper's order.
 constexpr int kLeanPlainWaves = 10;
 constexpr int kLeanWaves = 8;
 

@@ -156,12 +156,13 @@ __device__ __forceinline__ uint32_t umin(uint32_t a, uint32_t b) { return a < b 
 // BATCH: devices run up to their batch limit of units at once (plan scores
 // only).  QB = -1: the paper's reclamation order over a resident mask, no
 // queue (plan scores only).
-// Variants built for three waves per SIMD (the queue without batch limits;
-// a few registers of the key and replica-cap variants spill, which costs
-// less than the waves gained); batch limits and the paper's order keep two.
+// Variants built for three waves per SIMD: every queue variant (some
+// registers of the key, replica-cap and batch variants spill, which costs
+// less than the waves gained where LDS holds more than eight); the paper's
+// order keeps two.
 template <bool SEARCH, bool PHI, bool RCAP, bool BATCH, int QB>
 constexpr bool lean_plain() {
-  return !BATCH && QB > 0;
+  return QB > 0;
 }
 
 template <bool CHECKED, int QB, bool SEARCH, bool PHI, bool RCAP, bool BATCH>
