@@ -231,6 +231,9 @@ struct DeviceWindow {
   void* tab_lean = nullptr;     // the lean kernel's table image
   wfp::ScoreParams sp{};        // scoring plans read from HBM
   wfp::ScoreParams sp_search{}; // scoring candidates generated around an incumbent
+  // the same with more than kPatchMaxMut mutations when sp_search keeps
+  // candidates as changed sites (the ring layout)
+  wfp::ScoreParams sp_search_wide{};
   // uint32 times without a proof that none reaches 2^32: plans whose times
   // saturate are rescored with fp64 times
   bool checked = false;
@@ -432,7 +435,7 @@ int wave_layout(const HostWindow& h, int G, int tsz, int nwa, int qmode, bool se
 // Per-wave LDS region of the ring layout for G plans (kernel PLACE 2): the
 // per-plan arrays of the current level and of the ring's levels only.
 int ring_layout(const HostWindow& h, const wfp::ScoreParams& sp, int G, int tsz, int nwl,
-                wfp::WaveOffsets& o) {
+                bool search, wfp::WaveOffsets& o) {
   size_t off = 0;
   auto take = [&](size_t n) {
     const size_t at = off;
@@ -451,6 +454,9 @@ int ring_layout(const HostWindow& h, const wfp::ScoreParams& sp, int G, int tsz,
   o.wfm = take((size_t)G * std::max(1, h.W) * tsz);
   o.hstate = take(h.D > 64 ? 2 * 64 * sizeof(wfp::HState) : 0);
   o.hold = take(h.rcap.empty() ? 0 : (size_t)G * h.D * 8);
+  // generated candidates: each one's changed sites (at most kPatchMaxMut
+  // mutations)
+  o.rows = take(search ? (size_t)G * wfp::kPatchWords * 4 : 0);
   o.bytes = (int)off;
   return o.bytes;
 }
@@ -686,7 +692,8 @@ wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, bool time64_req, Im
 
 // Plans per wave, waves per workgroup and table placement for one kernel
 // mode (scoring rows from HBM, or scoring generated candidates).
-wf_status plan_launch(wf_plan_ctx* ctx, const HostWindow& h, bool search, wfp::ScoreParams& sp) {
+wf_status plan_launch(wf_plan_ctx* ctx, const HostWindow& h, bool search, wfp::ScoreParams& sp,
+                      bool ring_search = false) {
   const int D = h.D;
   const int tsz = sp.time64 ? 8 : 4;
   const int lds_cu = std::min(ctx->lds_per_cu, 160 * 1024);
@@ -778,7 +785,7 @@ wf_status plan_launch(wf_plan_ctx* ctx, const HostWindow& h, bool search, wfp::S
   const char* ring_env = std::getenv("WF_PLAN_RING");
   const bool ring_off = ring_env && std::strcmp(ring_env, "off") == 0;
   const bool ring_force = ring_env && std::strcmp(ring_env, "on") == 0;
-  if (!search && !ring_off && sp.ring_ok && (sp.nibble == 0 || sp.nibble == -2)) {
+  if ((!search || ring_search) && !ring_off && sp.ring_ok && (sp.nibble == 0 || sp.nibble == -2)) {
     const int nwl = (sp.ring_w + 63) / 64 + 1;
     const double cur = sp.wave_global ? hbm_lanes : best;
     double rbest = -1.0;
@@ -786,7 +793,7 @@ wf_status plan_launch(wf_plan_ctx* ctx, const HostWindow& h, bool search, wfp::S
     wfp::WaveOffsets ro{};
     for (int G = gmax; G >= 1; --G) {
       wfp::WaveOffsets o{};
-      const int wb = ring_layout(h, sp, G, tsz, nwl, o);
+      const int wb = ring_layout(h, sp, G, tsz, nwl, search, o);
       const int waves = std::min(8, (lds_blk - sp.wg_ld) / std::max(wb, 1));
       if (waves < 1) continue;
       const int lds_wg = sp.wg_ld + waves * wb;
@@ -835,7 +842,7 @@ int lean_layout(const HostWindow& h, int G, int nwa, wfp::LeanOffsets& o) {
   // the last slots are read before the walk starts, so they share the
   // finish region (after the candidates' changed sites) where they fit; the
   // paper's order keeps its per-model keys there during the walk
-  const size_t patch_bytes = align_up((size_t)G * wfp::kLeanPatchWords * 4, 16);
+  const size_t patch_bytes = align_up((size_t)G * wfp::kPatchWords * 4, 16);
   if (!paper && patch_bytes + last_bytes <= (size_t)G * h.N * 4)
     o.last = o.fin + (int)patch_bytes;
   else
@@ -969,7 +976,7 @@ void plan_lean(wf_plan_ctx* ctx, const HostWindow& h, const wfp::ScoreParams& sp
   lp.ok = 1;
   // generated candidates: each plan's changed sites live in its finish
   // entries until the walk
-  lp.search_ok = N >= 1 + 4 * wfp::kLeanMaxMut ? 1 : 0;
+  lp.search_ok = N >= 1 + 4 * wfp::kPatchMaxMut ? 1 : 0;
 }
 
 // The lean kernel's launch over n plans: the grid never exceeds the groups
@@ -992,10 +999,13 @@ wfp::ScoreParams fit_grid(wfp::ScoreParams sp, int64_t n) {
 
 // Run a scoring launch with the window's parameters, then, for a window
 // whose uint32 times are not proven safe, the fp64 pass over the groups it
-// flagged (same stream, so in order).
+// flagged (same stream, so in order).  Generated candidates with more than
+// kPatchMaxMut mutations take the layout that holds whole rows.
 template <typename F>
-hipError_t two_pass(const DeviceWindow& dw, bool search, int64_t n, F&& launch) {
-  hipError_t e = launch(fit_grid(search ? dw.sp_search : dw.sp, n));
+hipError_t two_pass(const DeviceWindow& dw, bool search, int64_t n, F&& launch, int32_t n_mut = 0) {
+  const wfp::ScoreParams& s =
+      !search ? dw.sp : (n_mut <= wfp::kPatchMaxMut ? dw.sp_search : dw.sp_search_wide);
+  hipError_t e = launch(fit_grid(s, n));
   if (e == hipSuccess && dw.checked) e = launch(fit_grid(search ? dw.sp64_search : dw.sp64, n));
   return e;
 }
@@ -1104,9 +1114,15 @@ wf_status wf_plan_upload_window(wf_plan_ctx* ctx, const wf_window_desc* w) {
   wfp::ScoreParams sps = sp;
   st = plan_launch(ctx, h, false, sp);
   if (st != WF_OK) return st;
-  st = plan_launch(ctx, h, true, sps);
-  if (st != WF_OK) return st;
   const bool checked = mode == kTimeChecked;
+  // generated candidates: the ring layout where it pays and the window needs
+  // no fp64 rescoring pass (the changed sites hold at most kPatchMaxMut
+  // mutations; sps_wide serves more)
+  wfp::ScoreParams spsw = sps;
+  st = plan_launch(ctx, h, true, spsw);
+  if (st != WF_OK) return st;
+  st = plan_launch(ctx, h, true, sps, !checked);
+  if (st != WF_OK) return st;
   wfp::ScoreParams sps64{};
   if (checked) {
     st = plan_window(ctx, h, true, img64, sp64, &mode);
@@ -1164,9 +1180,9 @@ wf_status wf_plan_upload_window(wf_plan_ctx* ctx, const wf_window_desc* w) {
   dw.rule_pf = static_cast<const unsigned long long*>(dw.rules);
   dw.rule_best = static_cast<const int8_t*>(dw.rules) + rule_best_at;
   // one scratch area serves every pass (they run in order on a stream)
-  wfp::ScoreParams* all[4] = {&sp, &sps, &sp64, &sps64};
+  wfp::ScoreParams* all[5] = {&sp, &sps, &spsw, &sp64, &sps64};
   size_t need = 0;
-  for (int i = 0; i < (checked ? 4 : 2); ++i)
+  for (int i = 0; i < (checked ? 5 : 3); ++i)
     if (all[i]->wave_global)
       need = std::max(need, (size_t)all[i]->grid * all[i]->waves *
                                 (size_t)(all[i]->wo.bytes - all[i]->wo.split));
@@ -1178,11 +1194,12 @@ wf_status wf_plan_upload_window(wf_plan_ctx* ctx, const wf_window_desc* w) {
       ctx->err = "device allocation of the scoring scratch failed";
       return WF_ENOMEM;
     }
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 5; ++i)
       if (all[i]->wave_global) all[i]->scratch = static_cast<unsigned char*>(dw.scratch);
   }
   sp.tab = static_cast<const unsigned char*>(dw.tab);
   sps.tab = static_cast<const unsigned char*>(dw.tab);
+  spsw.tab = static_cast<const unsigned char*>(dw.tab);
   Image limg;
   plan_lean(ctx, h, sp, checked, limg, dw.lean);
   if (dw.lean.ok) {
@@ -1198,6 +1215,7 @@ wf_status wf_plan_upload_window(wf_plan_ctx* ctx, const wf_window_desc* w) {
   }
   dw.sp = sp;
   dw.sp_search = sps;
+  dw.sp_search_wide = spsw;
   dw.checked = checked;
   if (checked) {
     sp64.tab = static_cast<const unsigned char*>(dw.tab64);
@@ -1214,6 +1232,9 @@ wf_status wf_plan_upload_window(wf_plan_ctx* ctx, const wf_window_desc* w) {
                  sp.waves, sp.grid, sp.wave_global ? "hbm+scratch" : (sp.tab_in_lds ? "lds" : "hbm"),
                  sp.t.bytes, sp.wo.bytes, sp.wave_global ? sp.wo.split : sp.wo.bytes, sp.lds_bytes, sp.nibble == 32 ? "queue32" : sp.nibble == 64 ? "queue64" : sp.nibble == -1 ? "paper-scan" :
                  sp.nibble == -2 ? "batch-scan" : sp.nibble == -3 ? "batch-paper-scan" : "scan");
+  if (std::getenv("WF_PLAN_VERBOSE") && sps.ring)
+    std::fprintf(stderr, "[wf_plan] generated candidates: ring of recent levels (G=%d, waves/wg=%d), "
+                 "changed sites for at most %d mutations\n", sps.G, sps.waves, wfp::kPatchMaxMut);
   if (std::getenv("WF_PLAN_VERBOSE") && sp.ring)
     std::fprintf(stderr, "[wf_plan] ring of recent levels: %d positions (%d levels ahead, %d "
                  "behind), widest level %d, %d mask words per device\n", sp.ring_size, sp.ring_a,
@@ -1318,7 +1339,7 @@ wf_status wf_plan_search_batch(wf_plan_ctx* ctx, const int8_t* dev, const uint16
   const wfp::SearchArgs sa = search_params(ctx, mode, seed, n_mut, first);
   const DeviceWindow& dw = ctx->dw;
   if (dw.lean.ok && !dw.lean.batch && !dw.lean.paper && dw.lean.search_ok &&
-      n_mut <= wfp::kLeanMaxMut) {
+      n_mut <= wfp::kPatchMaxMut) {
     // the lean kernel generates the candidates as the incumbent plus their
     // changed sites; then (times not proven below 2^32) the general fp64
     // pass over the groups holding a candidate whose times saturated
@@ -1332,10 +1353,13 @@ wf_status wf_plan_search_batch(wf_plan_ctx* ctx, const int8_t* dev, const uint16
       e = wfp::launch_score(fit_grid(dw.sp64_search, n_candidates), dev, prio, flags, n_candidates,
                             scores, nullptr, &sa, static_cast<hipStream_t>(hip_stream));
   } else {
-    e = two_pass(dw, true, n_candidates, [&](const wfp::ScoreParams& sp) {
-      return wfp::launch_score(sp, dev, prio, flags, n_candidates, scores, nullptr, &sa,
-                               static_cast<hipStream_t>(hip_stream));
-    });
+    e = two_pass(
+        dw, true, n_candidates,
+        [&](const wfp::ScoreParams& sp) {
+          return wfp::launch_score(sp, dev, prio, flags, n_candidates, scores, nullptr, &sa,
+                                   static_cast<hipStream_t>(hip_stream));
+        },
+        n_mut);
   }
   (void)hipSetDevice(prev);
   if (e != hipSuccess) return hip_fail(ctx, e, "launching the scoring kernel");
@@ -1471,7 +1495,7 @@ wf_status wf_plan_search_keys(wf_plan_ctx* ctx, const int8_t* dev, const uint16_
   const wfp::SearchArgs sa = search_params(ctx, mode, seed, n_mut, first);
   const DeviceWindow& dw = ctx->dw;
   if (dw.lean.ok && !dw.lean.batch && !dw.lean.paper && dw.lean.search_ok &&
-      n_mut <= wfp::kLeanMaxMut) {
+      n_mut <= wfp::kPatchMaxMut) {
     const wfp::LeanParams lp = lean_grid(dw.lean, n_candidates);
     e = wfp::launch_score_lean(dw.sp, lp, dev, prio, flags, n_candidates, keys, &sa, true,
                                static_cast<hipStream_t>(hip_stream));
@@ -1479,10 +1503,13 @@ wf_status wf_plan_search_keys(wf_plan_ctx* ctx, const int8_t* dev, const uint16_
       e = wfp::launch_score_keys(fit_grid(dw.sp64_search, n_candidates), dev, prio, flags,
                                  n_candidates, keys, &sa, static_cast<hipStream_t>(hip_stream));
   } else {
-    e = two_pass(dw, true, n_candidates, [&](const wfp::ScoreParams& sp) {
-      return wfp::launch_score_keys(sp, dev, prio, flags, n_candidates, keys, &sa,
-                                    static_cast<hipStream_t>(hip_stream));
-    });
+    e = two_pass(
+        dw, true, n_candidates,
+        [&](const wfp::ScoreParams& sp) {
+          return wfp::launch_score_keys(sp, dev, prio, flags, n_candidates, keys, &sa,
+                                        static_cast<hipStream_t>(hip_stream));
+        },
+        n_mut);
   }
   (void)hipSetDevice(prev);
   if (e != hipSuccess) return hip_fail(ctx, e, "launching the ranking-key kernel");

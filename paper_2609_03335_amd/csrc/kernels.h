@@ -236,12 +236,12 @@ struct LeanParams {
 constexpr int kLeanPlainWaves = 10;
 constexpr int kLeanWaves = 8;
 
-// Generated candidates served by the lean kernel: at most this many
-// mutations each (a candidate is the incumbent plus at most 2 changed sites
-// per mutation).
-constexpr int kLeanMaxMut = 8;
+// Generated candidates kept as the incumbent plus their changed sites (the
+// lean kernel, and the general kernel's ring layout): at most this many
+// mutations each (at most 2 changed sites per mutation).
+constexpr int kPatchMaxMut = 8;
 // words of one candidate's changed sites (a count, then 4 words per mutation)
-constexpr int kLeanPatchWords = 1 + 4 * kLeanMaxMut;
+constexpr int kPatchWords = 1 + 4 * kPatchMaxMut;
 
 struct SearchArgs;
 

@@ -7,7 +7,7 @@
 // configuration needs: 16-bit slot entries, no schedule, key, search,
 // batch-limit or fp64 paths, and the per-unit tables of the walk in LDS.
 // With SEARCH the plans are candidates generated around an incumbent (at
-// most kLeanMaxMut mutations each): a candidate is kept as the incumbent's
+// most kPatchMaxMut mutations each): a candidate is kept as the incumbent's
 // rows plus the sites its mutations changed (in the finish array's storage,
 // dead until the walk), and the order sweep patches the incumbent's row
 // words with them, so no candidate row exists in HBM or LDS.
@@ -36,51 +36,6 @@
 
 namespace wfp {
 namespace {
-
-// A candidate as the incumbent's rows plus the changed sites: per plan a
-// count, then 2 words per site (activation | priority << 16, device).
-constexpr int kPatchWords = kLeanPatchWords;
-
-struct PatchRows {
-  uint32_t* p;             // this plan's count and sites
-  const int8_t* idev;      // incumbent rows
-  const uint16_t* iprio;
-  uint8_t* rf;             // this plan's flag row (staged)
-  __device__ __forceinline__ int find(int i) const {
-    const int n = (int)p[0];
-    for (int k = 0; k < n; ++k)
-      if ((int)(p[1 + 2 * k] & 0xffffu) == i) return k;
-    return -1;
-  }
-  __device__ __forceinline__ int site(int i) {
-    int k = find(i);
-    if (k < 0) {
-      k = (int)p[0];
-      p[1 + 2 * k] = (uint32_t)i | ((uint32_t)iprio[i] << 16);
-      p[2 + 2 * k] = (uint32_t)(int32_t)idev[i];
-      p[0] = (uint32_t)(k + 1);
-    }
-    return k;
-  }
-  __device__ __forceinline__ int dev(int i) const {
-    const int k = find(i);
-    return k >= 0 ? (int)(int32_t)p[2 + 2 * k] : (int)idev[i];
-  }
-  __device__ __forceinline__ void set_dev(int i, int d) { p[2 + 2 * site(i)] = (uint32_t)d; }
-  __device__ __forceinline__ void swap_prio(int i, int j) {
-    const int ki = site(i), kj = site(j);
-    const uint32_t pi = p[1 + 2 * ki] >> 16, pj = p[1 + 2 * kj] >> 16;
-    p[1 + 2 * ki] = (uint32_t)i | (pj << 16);
-    p[1 + 2 * kj] = (uint32_t)j | (pi << 16);
-  }
-  __device__ __forceinline__ void toggle_flag(int i, int bit) {
-    rf[i >> 2] ^= (uint8_t)(1u << (((i & 3) << 1) + bit));
-  }
-  __device__ __forceinline__ void set_prefetch(int i, bool on) {
-    const uint8_t b = (uint8_t)(2u << ((i & 3) << 1));
-    rf[i >> 2] = on ? (uint8_t)(rf[i >> 2] | b) : (uint8_t)(rf[i >> 2] & ~b);
-  }
-};
 
 // (ranking keys: loads holds the timely prefetches P_N, max_finish and p95
 // together the 64-bit count of admitted ready units per class)

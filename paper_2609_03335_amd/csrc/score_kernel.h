@@ -177,7 +177,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   constexpr bool BATCH = QB <= -2;
   constexpr bool WAVE_GLOBAL = PLACE == 1;
   constexpr bool RING = PLACE == 2;
-  static_assert(!RING || ((QB == 0 || QB == -2) && !SEARCH), "ring layout: scans, rows from HBM");
+  static_assert(!RING || QB == 0 || QB == -2, "ring layout: scans");
   using QT = std::conditional_t<QB == 32, uint32_t, uint64_t>;
   constexpr QT kOnes = (QT)0x1111111111111111ull, kHigh = (QT)0x8888888888888888ull;
   constexpr int kQBits = (int)sizeof(QT) * 8;
@@ -275,6 +275,8 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   TB* s_wfm = reinterpret_cast<TB*>(big(sp.wo.wfm));
   int8_t* s_rdev = reinterpret_cast<int8_t*>(big(sp.wo.rows));         // generated candidates
   uint16_t* s_rprio = reinterpret_cast<uint16_t*>(big(sp.wo.rows_prio));
+  // (the ring layout keeps a candidate as the incumbent plus its changed sites)
+  uint32_t* s_pat = reinterpret_cast<uint32_t*>(big(sp.wo.rows));
 
   const int g_me = lane / D;
   // every unit's finish goes through the general path when the schedule is
@@ -325,7 +327,17 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
     }
 
     // ---- stage the group's flag rows, clear the ordering state ----
-    if constexpr (SEARCH) {
+    if constexpr (SEARCH && RING) {
+      // every plan of the group starts as the incumbent; lane g then writes
+      // candidate g's changed sites and mutates its flag row
+      for (int g = 0; g < gc; ++g) copy_row(s_fl + g * NB, flags_all, NB, lane);
+      wave_sync();
+      if (lane < gc) {
+        PatchRows rows{s_pat + lane * kPatchWords, dev_all, prio_all, s_fl + lane * NB};
+        rows.p[0] = 0u;
+        mutate_rows((uint64_t)(sa.first + p0 + lane), sa, N, t_elig, t_alv, rows);
+      }
+    } else if constexpr (SEARCH) {
       // every plan of the group starts as the incumbent, then takes its
       // candidate's mutations (one lane per plan, in order)
       for (int g = 0; g < gc; ++g) {
@@ -368,6 +380,25 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
     }
     wave_sync();
 
+    // device and priority of activation u in plan g, for the ring layout's
+    // level-by-level order: the plan rows in HBM, or the incumbent's with
+    // the candidate's changed sites
+    auto ring_dev = [&](int g, int u) -> int {
+      if constexpr (SEARCH) {
+        const PatchRows rows{s_pat + g * kPatchWords, dev_all, prio_all, nullptr};
+        return rows.dev(u);
+      } else {
+        return dev_all[(p0 + g) * N + u];
+      }
+    };
+    auto ring_prio = [&](int g, int u) -> int {
+      if constexpr (SEARCH) {
+        const PatchRows rows{s_pat + g * kPatchWords, dev_all, prio_all, nullptr};
+        return rows.prio(u);
+      } else {
+        return prio_all[(p0 + g) * N + u];
+      }
+    };
     if constexpr (!RING) {
       // ---- resource order (Eq. 10), first try: a unit head's slot is its
       // priority, valid when each level's head priorities are distinct values
@@ -633,7 +664,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
         const uint32_t a = t_act[u];
         const uint32_t fb = (uint32_t)s_fl[g * NB + (u >> 2)] >> ((u & 3) << 1);
         if ((fb & 1u) && (a & 64u)) continue;  // a fused chain member
-        const int dv = dev_all[(p0 + g) * N + u];
+        const int dv = ring_dev(g, u);
         if ((unsigned)dv < (unsigned)D) {
           // 16-bit counts, two to a word (a count stays below 2^16)
           const int ci = (g * D + dv) * M + (int)(a & 63u);
@@ -917,9 +948,9 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
           const uint32_t a = t_act[u];
           const uint32_t fb = (uint32_t)s_fl[g * NB + (u >> 2)] >> ((u & 3) << 1);
           if ((fb & 1u) && (a & 64u)) continue;
-          const int dv = dev_all[(p0 + g) * N + u];
+          const int dv = ring_dev(g, u);
           if ((unsigned)dv >= (unsigned)D) continue;
-          const int pr = prio_all[(p0 + g) * N + u];
+          const int pr = ring_prio(g, u);
           if ((unsigned)(pr - lo) >= (unsigned)width) {
             s_acc[g].bad = 1u;
             continue;
@@ -946,8 +977,6 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
         const uint64_t rankedm = __ballot(lane < gc && s_acc[lane < gc ? lane : 0].bad != 0u);
         for (uint64_t rm = rankedm; rm; rm &= rm - 1ull) {
           const int g = __builtin_ctzll(rm);
-          const int8_t* pdev = dev_all + (p0 + g) * N;
-          const uint16_t* pprio = prio_all + (p0 + g) * N;
           const uint8_t* pfl = s_fl + g * NB;
           for (int i = lane; i < D * NWA; i += 64) s_mask[g * D * NWA + i] = 0ull;
           wave_sync();
@@ -955,14 +984,14 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
             const uint32_t a = t_act[u];
             const uint32_t fb = (uint32_t)pfl[u >> 2] >> ((u & 3) << 1);
             if ((fb & 1u) && (a & 64u)) continue;
-            const int dv = pdev[u];
+            const int dv = ring_dev(g, u);
             if ((unsigned)dv >= (unsigned)D) continue;
-            const int pu = pprio[u];
+            const int pu = ring_prio(g, u);
             int slot = lo;
             for (int j = lo; j < hi; ++j) {
               if (fuse_bit(pfl, j) && (t_act[j] & 64u)) continue;
-              if ((unsigned)pdev[j] >= (unsigned)D) continue;
-              const int pj = pprio[j];
+              if ((unsigned)ring_dev(g, j) >= (unsigned)D) continue;
+              const int pj = ring_prio(g, j);
               slot += (pj < pu) || (pj == pu && j < u);
             }
             s_rec[g * RW + (slot - lo)] = head_entry(g, u, a, fb);
@@ -1557,7 +1586,7 @@ template <typename TT, int QB, bool SEARCH, bool PHI, bool SCHED>
 hipError_t launch_place(const ScoreParams& sp, const int8_t* dev, const uint16_t* prio,
                         const uint8_t* flags, int64_t n_plans, OutRec<PHI>* out,
                         const wf_plan_sched& s, int has, const SearchArgs& sa, hipStream_t stream) {
-  if constexpr ((QB == 0 || QB == -2) && !SEARCH) {
+  if constexpr (QB == 0 || QB == -2) {
     if (sp.ring)
       return launch_variant<TT, false, QB, 2, SEARCH, PHI, SCHED>(sp, dev, prio, flags, n_plans,
                                                                   out, s, has, sa, stream);

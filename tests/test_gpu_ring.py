@@ -168,3 +168,83 @@ def test_ring_many_devices(ctx, capfd):
     ref = oracle.score(win, plans, threads=THREADS)
     assert gpu_scores(ctx, plans, plans.n_plans).tobytes() == ref.tobytes()
     check_schedules(ctx, win, plans, plans.n_plans, "96 devices")
+
+
+SEARCH_RING_LINE = "[wf_plan] generated candidates: ring of recent levels"
+
+
+def gpu_search(ctx, inc, seed, n_mut, first, n, keys=False, mode=0):
+    d, p, f = (torch.from_numpy(np.ascontiguousarray(inc[0])).cuda(),
+               torch.from_numpy(np.ascontiguousarray(inc[1]).view("<i2")).cuda(),
+               torch.from_numpy(np.ascontiguousarray(inc[2])).cuda())
+    out = torch.empty((n, 32), dtype=torch.uint8, device="cuda:0")
+    if keys:
+        ctx.wf_plan_search_keys(d, p, f, seed, n_mut, first, n, out, mode=mode)
+    else:
+        ctx.wf_plan_search_batch(d, p, f, seed, n_mut, first, n, out, mode=mode)
+    torch.cuda.synchronize()
+    return pkg.keys_to_numpy(out, n) if keys else pkg.scores_to_numpy(out, n)
+
+
+def upload_search(ctx, win, capfd, ring=True):
+    """Upload; returns whether generated candidates took the ring layout."""
+    os.environ["WF_PLAN_VERBOSE"] = "1"
+    if ring:
+        os.environ.pop("WF_PLAN_RING", None)
+    else:
+        os.environ["WF_PLAN_RING"] = "off"
+    try:
+        capfd.readouterr()
+        ctx.wf_plan_upload_window(win)
+        err = capfd.readouterr().err
+    finally:
+        os.environ.pop("WF_PLAN_VERBOSE", None)
+        os.environ.pop("WF_PLAN_RING", None)
+    return SEARCH_RING_LINE in err
+
+
+@pytest.mark.parametrize("n_mut", [1, 8, 9])
+def test_generated_candidates_deep_workload(ctx, capfd, n_mut):
+    """Candidates around a plan of the deep workload: kept as the incumbent
+    plus their changed sites in the ring layout (at most 8 mutations), or as
+    whole rows in the layout without the ring (more mutations), against the
+    oracle's candidates scored by the oracle."""
+    win, plans = W.make_config(3, n_plans=2)
+    inc = (plans.dev[0], plans.prio[0], plans.flags[0])
+    took = upload_search(ctx, win, capfd)
+    assert took, "generated candidates did not take the ring layout"
+    n, seed, first = 1024, 0xC0FFEE + n_mut, 5 * n_mut
+    log(f"[ring search] deep workload: {n} candidates, {n_mut} mutations")
+    cand = W.PlanBatch(*oracle.search_candidates(win, *inc, seed, n_mut, first, n))
+    ref = oracle.score(win, cand, threads=THREADS)
+    assert gpu_search(ctx, inc, seed, n_mut, first, n).tobytes() == ref.tobytes()
+    if n_mut == 8:
+        rk = oracle.phi_keys(win, cand, threads=THREADS)
+        assert gpu_search(ctx, inc, seed, n_mut, first, n, keys=True).tobytes() == rk.tobytes()
+        cr = W.PlanBatch(*oracle.search_candidates(win, *inc, seed, n_mut, first, n,
+                                                   mode=oracle.SEARCH_RULES))
+        rr = oracle.score(win, cr, threads=THREADS)
+        assert gpu_search(ctx, inc, seed, n_mut, first, n, mode=pkg.WF_SEARCH_RULES).tobytes() == rr.tobytes()
+    assert not upload_search(ctx, win, capfd, ring=False)
+    assert gpu_search(ctx, inc, seed, n_mut, first, n).tobytes() == ref.tobytes()
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_generated_candidates_random_deep_windows(ctx, capfd, seed):
+    """Candidates around a plan of random deep windows (ranked levels, batch
+    limits, replica caps, invalid incumbent devices), with and without the
+    ring, at mutation counts on both sides of the changed-site limit."""
+    win, plans = deep_case(seed)
+    inc = (plans.dev[1], plans.prio[1], plans.flags[1])
+    took = upload_search(ctx, win, capfd)
+    n_mut = [0, 2, 5, 8, 9, 16, 3, 8][seed]
+    n, s64, first = 600, 0x9E3779B97F4A7C15 ^ seed, 1000 * seed
+    log(f"[ring search] seed {seed}: N={win.n_act} D={win.n_dev} M={win.n_models} ring={took} "
+        f"n_mut={n_mut}")
+    cand = W.PlanBatch(*oracle.search_candidates(win, *inc, s64, n_mut, first, n))
+    ref = oracle.score(win, cand, threads=THREADS)
+    assert gpu_search(ctx, inc, s64, n_mut, first, n).tobytes() == ref.tobytes(), f"seed {seed}"
+    rk = oracle.phi_keys(win, cand, threads=THREADS)
+    assert gpu_search(ctx, inc, s64, n_mut, first, n, keys=True).tobytes() == rk.tobytes()
+    upload_search(ctx, win, capfd, ring=False)
+    assert gpu_search(ctx, inc, s64, n_mut, first, n).tobytes() == ref.tobytes()
