@@ -1,11 +1,12 @@
-// The lean scoring kernel: the scalar objective of plans read from HBM for
-// windows whose times fit uint32 offsets and whose resident sets fit a queue
-// of 4-bit model ids (at most 16 models), with one unit per device, the
-// default reclamation order and at most 512 activations -- the configuration
-// the throughput workload (256 activations x 1,048,576 plans) runs in.  Same
-// results as the general kernel of score_kernel.h, with only the code this
-// configuration needs: 16-bit slot entries, no schedule, key, search,
-// batch-limit or fp64 paths, and the per-unit tables of the walk in LDS.
+// The lean scoring kernel: windows whose times fit uint32 offsets, with at
+// most 16 models and at most 512 activations -- the configuration the
+// throughput workload (256 activations x 1,048,576 plans) runs in.  Same
+// results as the general kernel of score_kernel.h, with only the code these
+// windows need: 16-bit slot entries, uint32 times, no schedule, and the
+// per-unit tables of the walk in LDS.  Variants (template parameters): the
+// default reclamation order on a queue of 4-bit model ids (QB = 32 or 64)
+// or the paper's order over a resident mask (QB = -1); ranking keys of Eq.
+// 12 instead of scores (PHI); replica caps (RCAP); batch limits (BATCH).
 // With SEARCH the plans are candidates generated around an incumbent (at
 // most kPatchMaxMut mutations each): a candidate is kept as the incumbent's
 // rows plus the sites its mutations changed (in the finish array's storage,
@@ -19,12 +20,13 @@
 //      are distinct values of the level's index range (checked by counting),
 //      else at its rank by (priority, index) within the level; a 16-bit slot
 //      entry, the device's slot mask and each (device, model)'s last slot are
-//      recorded;
+//      recorded, and the last slots become flags in the slot entries;
 //   2. per topological level, releases (Eq. 2) by LDS atomic max over the
 //      level's incoming edges, then each device lane walks its units of the
-//      level in slot order: reuse / reclaim / load (Eq. 5, Eq. 11) on a
-//      4-bit queue of the resident models and the max-plus timeline of Eq. 7;
-//   3. makespan, nearest-rank p95, objective, headroom and counts.
+//      level in slot order: reuse / reclaim / load (Eq. 5, Eq. 11) and the
+//      max-plus timeline of Eq. 7;
+//   3. makespan, nearest-rank p95, objective, headroom and counts (or the
+//      ranking key).
 // Memory is tracked as the excess of a unit's need over the device's free
 // memory: a unit fits when its excess after reclamation is <= 0, the device's
 // peak is its capacity plus the largest such excess, so the peak, the
