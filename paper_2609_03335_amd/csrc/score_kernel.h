@@ -298,7 +298,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   // one 256-activation chunk and at most eight plans per group: the next
   // group's device and priority rows are loaded while this group is walked
   constexpr int kB = 8;
-  const bool pre = !SEARCH && !RING && vec && N <= 256 && G <= kB && !sp.rescore;
+  const bool pre = !SEARCH && !RING && !WAVE_GLOBAL && vec && N <= 256 && G <= kB && !sp.rescore;
   uint32_t dvp[kB];
   uint2 pvp[kB];
   auto load_rows = [&](int64_t grp_, uint32_t* dv, uint2* pv) {
