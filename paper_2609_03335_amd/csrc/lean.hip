@@ -982,18 +982,20 @@ void score_lean(ScoreParams sp, LeanParams lp,
       }
     }
     lsync();
-    // completion latencies in place, and the latest finish
+    // completion latencies in place, and the latest finish; nearest-rank
+    // p95 is the ceil(0.95 W)-th smallest latency, which for W <= 19 is the
+    // largest one
+    const int kk = (95 * W + 99) / 100;
     for (int it = lane; it < (PHI ? 0 : gc * W); it += 64) {
       const int g = it / W, a = it - g * W;
       const uint32_t fb = s_wfm[it];
       atomicMax(&s_acc[g].max_finish, fb);
       s_wfm[it] = fb - t_arr[a];
+      if (kk == W) atomicMax(&s_acc[g].p95, fb - t_arr[a]);
     }
     lsync();
-    // nearest-rank p95: the ceil(0.95 W)-th smallest completion latency,
-    // lanes over (plan, workflow)
-    const int kk = (95 * W + 99) / 100;
-    for (int it = lane; it < (PHI ? 0 : gc * W); it += 64) {
+    // otherwise counting, lanes over (plan, workflow)
+    for (int it = lane; it < (PHI || kk == W ? 0 : gc * W); it += 64) {
       const int g = it / W;
       const uint32_t* cw = s_wfm + g * W;
       const uint32_t ca = cw[it - g * W];
