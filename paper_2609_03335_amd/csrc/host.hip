@@ -362,7 +362,7 @@ struct Image {
 // small per-(device, model) arrays come first, [0, o.split), and stay in LDS;
 // the per-activation arrays follow in HBM.
 int wave_layout(const HostWindow& h, int G, int tsz, int nwa, int qmode, bool search,
-                wfp::WaveOffsets& o, bool global) {
+                wfp::WaveOffsets& o, bool global, int ring_fin = 0) {
   const bool nibble = qmode > 0, paper = qmode == -1 || qmode == -3;
   size_t off = 0;
   auto take = [&](size_t n) {
@@ -371,7 +371,11 @@ int wave_layout(const HostWindow& h, int G, int tsz, int nwa, int qmode, bool se
     return (int)at;
   };
   const int NB = (h.N + 3) / 4;
-  const size_t fin_bytes = (size_t)G * h.N * tsz, last_bytes = (size_t)G * h.D * h.M * 4;
+  // (ring_fin > 0, regions in HBM: the finishes are a ring of ring_fin
+  // positions per plan, in the LDS part with the per-workflow finishes)
+  ring_fin = global ? ring_fin : 0;
+  const size_t fin_bytes = (size_t)G * (ring_fin > 0 ? ring_fin : h.N) * tsz,
+               last_bytes = (size_t)G * h.D * h.M * 4;
   const size_t dm2 = (size_t)G * h.D * h.M * 2;
   // generated candidates keep their device and priority rows in fin's
   // storage (after last[] when that shares it) while the order is built
@@ -391,6 +395,10 @@ int wave_layout(const HostWindow& h, int G, int tsz, int nwa, int qmode, bool se
     }
     o.hstate = take(h.D > 64 ? 2 * 64 * sizeof(wfp::HState) : 0);
     o.hold = take(h.rcap.empty() ? 0 : (size_t)G * h.D * 8);
+    if (ring_fin > 0) {
+      o.fin = take(std::max(fin_bytes, rows_bytes));
+      o.wfm = take((size_t)G * std::max(1, h.W) * tsz);
+    }
     o.split = (int)off;
   }
   o.flags = take((size_t)G * NB);
@@ -402,11 +410,11 @@ int wave_layout(const HostWindow& h, int G, int tsz, int nwa, int qmode, bool se
     o.last = o.fin;
   } else if (paper) {
     // the paper order keeps no last[] (it is never written)
-    o.fin = take(std::max(fin_bytes, rows_bytes));
+    if (ring_fin == 0) o.fin = take(std::max(fin_bytes, rows_bytes));
     o.last = o.fin;
     if (!global) o.stamp = take(dm2);
   } else {
-    o.fin = take(std::max(fin_bytes, rows_bytes));
+    if (ring_fin == 0) o.fin = take(std::max(fin_bytes, rows_bytes));
     if (!global) {
       o.last = take(last_bytes);
       o.stamp = take(dm2);
@@ -414,7 +422,7 @@ int wave_layout(const HostWindow& h, int G, int tsz, int nwa, int qmode, bool se
   }
   o.rows = o.fin + (int)rows_at;
   o.rows_prio = o.rows + (int)align_up((size_t)G * h.N, 16);
-  o.wfm = take((size_t)G * std::max(1, h.W) * tsz);
+  if (ring_fin == 0) o.wfm = take((size_t)G * std::max(1, h.W) * tsz);
   // unused arrays point at the start of their part
   o.nx = global ? o.split : 0;
   if (paper) {
@@ -597,7 +605,8 @@ wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, bool time64_req, Im
   // members with the chain head, up to ring_a levels early -- to the last
   // level an edge reads it, ring_b levels later
   const bool batched_w = std::any_of(h.batch.begin(), h.batch.end(), [](int32_t b) { return b > 1; });
-  const bool scan_lru = h.victim_order != WF_VICTIM_PAPER && (batched_w || M > 16 || !h.rcap.empty());
+  // (and the paper's order, whose finishes alone may take the ring)
+  const bool scan_lru = h.victim_order == WF_VICTIM_PAPER || batched_w || M > 16 || !h.rcap.empty();
   sp.ring_ok = 0;
   if (scan_lru && N > 0) {
     std::vector<int32_t> lvl((size_t)N), wmin((size_t)N);
@@ -818,6 +827,27 @@ wf_status plan_launch(wf_plan_ctx* ctx, const HostWindow& h, bool search, wfp::S
       sp.grid = ctx->n_cu * rwgs;
       sp.wo = ro;
       sp.nwa = nwl;
+    }
+  }
+  // the paper's order in the HBM layout keeps its finishes in the ring of
+  // recent levels (LDS): the order is built before the walk, as its next use
+  // per slot needs every level's order, but the finishes and their atomics
+  // stay out of HBM (sp.ring = 2)
+  const bool paper_scan_mode = sp.nibble == -1 || sp.nibble == -3;
+  if (paper_scan_mode && !search && !ring_off && sp.ring_ok && sp.wave_global && sp.ring == 0) {
+    wfp::WaveOffsets o4{};
+    const int64_t wb4 = wave_layout(h, sp.G, tsz, sp.nwa, sp.nibble, search, o4, true, sp.ring_size);
+    const int lds4 = sp.wg_ld + sp.waves * o4.split;
+    if (lds4 <= lds_blk) {
+      const int wg_per_cu = std::max(1, std::min(2, lds_cu / lds4));
+      const int64_t hw = std::max<int64_t>((wb4 - o4.split) * sp.waves, 1);
+      const int64_t wgs = std::min<int64_t>((int64_t)ctx->n_cu * wg_per_cu, (int64_t(1) << 30) / hw);
+      if (wgs >= 1) {
+        sp.ring = 2;
+        sp.lds_bytes = lds4;
+        sp.grid = (int)wgs;
+        sp.wo = o4;
+      }
     }
   }
   return WF_OK;
@@ -1235,10 +1265,14 @@ wf_status wf_plan_upload_window(wf_plan_ctx* ctx, const wf_window_desc* w) {
   if (std::getenv("WF_PLAN_VERBOSE") && sps.ring)
     std::fprintf(stderr, "[wf_plan] generated candidates: ring of recent levels (G=%d, waves/wg=%d), "
                  "changed sites for at most %d mutations\n", sps.G, sps.waves, wfp::kPatchMaxMut);
-  if (std::getenv("WF_PLAN_VERBOSE") && sp.ring)
+  if (std::getenv("WF_PLAN_VERBOSE") && sp.ring == 1)
     std::fprintf(stderr, "[wf_plan] ring of recent levels: %d positions (%d levels ahead, %d "
                  "behind), widest level %d, %d mask words per device\n", sp.ring_size, sp.ring_a,
                  sp.ring_b, sp.ring_w, sp.nwa);
+  if (std::getenv("WF_PLAN_VERBOSE") && sp.ring == 2)
+    std::fprintf(stderr, "[wf_plan] finishes in a ring of recent levels: %d positions (%d levels "
+                 "ahead, %d behind); order and slot arrays in HBM\n", sp.ring_size, sp.ring_a,
+                 sp.ring_b);
   if (std::getenv("WF_PLAN_VERBOSE") && dw.lean.ok)
     std::fprintf(stderr, "[wf_plan] lean kernel: G=%d waves/wg=%d (queue variants %d) grid=%d (%d) "
                  "tables=%d B wave=%d B lds/wg=%d (%d)\n",

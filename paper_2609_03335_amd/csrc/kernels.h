@@ -153,7 +153,8 @@ struct ScoreParams {
   // their finish with the chain head), at positions index mod ring_size:
   // ring_size is the most activations any such span of levels holds, so
   // the live finishes never share a position
-  int ring;                   // 1: this launch uses the ring layout
+  int ring;                   // 1: the ring layout; 2: the HBM layout with the finishes in
+                              // the ring (the paper's order)
   int ring_ok;                // 1: the window admits it (tables rpos, redge, rsnk built)
   int ring_size, ring_w, ring_a, ring_b;  // ring_w: the widest level
 };

@@ -175,9 +175,15 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   // once, each in one of up to kMaxBatch slots)
   constexpr bool PAPER = QB == -1 || QB == -3;
   constexpr bool BATCH = QB <= -2;
-  constexpr bool WAVE_GLOBAL = PLACE == 1;
-  constexpr bool RING = PLACE == 2;
+  // PLACE 2: the ring of recent levels, the order built level by level, all
+  // in LDS.  PLACE 4: the finishes in the ring (LDS), the order built before
+  // the walk with the other per-activation arrays in HBM (the paper's order,
+  // whose next use per slot needs every level's order first).
+  constexpr bool RING = PLACE == 2;           // order built level by level
+  constexpr bool RING_FIN = PLACE == 2 || PLACE == 4;  // finishes in the ring
+  constexpr bool WAVE_GLOBAL = PLACE == 1 || PLACE == 4;
   static_assert(!RING || QB == 0 || QB == -2, "ring layout: scans");
+  static_assert(PLACE != 4 || ((QB == -1 || QB == -3) && !SEARCH), "ring finishes: the paper's order");
   using QT = std::conditional_t<QB == 32, uint32_t, uint64_t>;
   constexpr QT kOnes = (QT)0x1111111111111111ull, kHigh = (QT)0x8888888888888888ull;
   constexpr int kQBits = (int)sizeof(QT) * 8;
@@ -237,9 +243,9 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   // ring layout: slot entries per plan (the widest level), finishes per plan
   // (the ring), a finish's position
   const int RW = RING ? sp.ring_w : N;
-  const int FS = RING ? sp.ring_size : N;
+  const int FS = RING_FIN ? sp.ring_size : N;
   auto fpos = [&](int u) -> int {
-    if constexpr (RING) return (int)t_rpos[u];
+    if constexpr (RING_FIN) return (int)t_rpos[u];
     else return u;
   };
 
@@ -263,7 +269,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   // last[] shares fin's storage in the queue modes, else it is a small array
   // (the paper order keeps no last[]; its offset is fin's)
   uint32_t* s_last = reinterpret_cast<uint32_t*>((NIBBLE || PAPER) ? big(sp.wo.last) : small(sp.wo.last));
-  TB* s_fin = reinterpret_cast<TB*>(big(sp.wo.fin));
+  TB* s_fin = reinterpret_cast<TB*>(PLACE == 4 ? small(sp.wo.fin) : big(sp.wo.fin));
   PlanAcc* s_acc = reinterpret_cast<PlanAcc*>(small(sp.wo.acc));
   uint16_t* s_stamp = reinterpret_cast<uint16_t*>(small(sp.wo.stamp));
   uint16_t* s_nx = reinterpret_cast<uint16_t*>(big(sp.wo.nx));      // paper order only
@@ -272,7 +278,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
   HState* s_hst = reinterpret_cast<HState*>(small(sp.wo.hstate));  // more than 64 devices only
   unsigned long long* s_hold = reinterpret_cast<unsigned long long*>(small(sp.wo.hold));  // replica caps
   const int32_t* t_rcap = reinterpret_cast<const int32_t*>(tb + sp.t.rcap);
-  TB* s_wfm = reinterpret_cast<TB*>(big(sp.wo.wfm));
+  TB* s_wfm = reinterpret_cast<TB*>(PLACE == 4 ? small(sp.wo.wfm) : big(sp.wo.wfm));
   int8_t* s_rdev = reinterpret_cast<int8_t*>(big(sp.wo.rows));         // generated candidates
   uint16_t* s_rprio = reinterpret_cast<uint16_t*>(big(sp.wo.rows_prio));
   // (the ring layout keeps a candidate as the incumbent plus its changed sites)
@@ -921,11 +927,8 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
     for (int lv = 0; lv < sp.n_levels; ++lv) {
       const int lo = t_loff[lv], hi = t_loff[lv + 1];
       const int e0 = t_eoff[lv], e1 = t_eoff[lv + 1];
-      if constexpr (RING) {
-        // ---- the level leaving the ring, then this level's resource order
-        // (Eq. 10): a head's slot is its priority when the level's head
-        // priorities are distinct values in its index range, else its rank
-        // by (priority, index) ----
+      if constexpr (RING_FIN) {
+        // ---- the level leaving the ring ----
         const int lold = lv - sp.ring_b - 1, lnew = lv + sp.ring_a;
         if (lold >= 0) {
           if (!PHI) ring_level(lold, false);
@@ -934,6 +937,12 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
             ring_level(lnew, true);
           }
         }
+        if constexpr (!RING) wave_sync();
+      }
+      if constexpr (RING) {
+        // ---- this level's resource order (Eq. 10): a head's slot is its
+        // priority when the level's head priorities are distinct values in
+        // its index range, else its rank by (priority, index) ----
         const int width = hi - lo, jb = lo >> 6;
         for (int i = lane; i < gc * D * NWA; i += 64) s_mask[i] = 0ull;
         if (lane < gc) s_acc[lane].bad = 0u;
@@ -1004,7 +1013,7 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
       // one lane per incoming edge.  A fused chain member already holds its
       // own finish, which is later than its only predecessor's ----
       if (e1 > e0) {
-        const uint32_t* t_ed = RING ? reinterpret_cast<const uint32_t*>(tb + sp.t.redge) : t_edge;
+        const uint32_t* t_ed = RING_FIN ? reinterpret_cast<const uint32_t*>(tb + sp.t.redge) : t_edge;
         for (int e = e0 + lane; e < e1; e += 64) {
           const uint32_t ed = t_ed[e];
           const int src = (int)(ed & 0xffffu), dst = (int)(ed >> 16);
@@ -1472,12 +1481,12 @@ __global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
     // without a successor in the same workflow (not part of the ranking key);
     // the ring layout folded every level but its last ring_b + 1 during the
     // walk
-    if constexpr (RING) {
+    if constexpr (RING_FIN) {
       if (!PHI)
         for (int L = sp.n_levels - sp.ring_b - 1 > 0 ? sp.n_levels - sp.ring_b - 1 : 0; L < sp.n_levels; ++L)
           ring_level(L, false);
     }
-    for (int i = lane; i < ((PHI || RING) ? 0 : sp.S); i += 64) {
+    for (int i = lane; i < ((PHI || RING_FIN) ? 0 : sp.S); i += 64) {
       const uint32_t sk = t_sink[i];
       const int src = (int)(sk & 0xffffu), wf = (int)(sk >> 16);
       for (int g0 = 0; g0 < gc; g0 += kB) {
@@ -1586,6 +1595,11 @@ template <typename TT, int QB, bool SEARCH, bool PHI, bool SCHED>
 hipError_t launch_place(const ScoreParams& sp, const int8_t* dev, const uint16_t* prio,
                         const uint8_t* flags, int64_t n_plans, OutRec<PHI>* out,
                         const wf_plan_sched& s, int has, const SearchArgs& sa, hipStream_t stream) {
+  if constexpr ((QB == -1 || QB == -3) && !SEARCH) {
+    if (sp.ring == 2)
+      return launch_variant<TT, false, QB, 4, SEARCH, PHI, SCHED>(sp, dev, prio, flags, n_plans,
+                                                                  out, s, has, sa, stream);
+  }
   if constexpr (QB == 0 || QB == -2) {
     if (sp.ring)
       return launch_variant<TT, false, QB, 2, SEARCH, PHI, SCHED>(sp, dev, prio, flags, n_plans,

@@ -248,3 +248,74 @@ def test_generated_candidates_random_deep_windows(ctx, capfd, seed):
     assert gpu_search(ctx, inc, s64, n_mut, first, n, keys=True).tobytes() == rk.tobytes()
     upload_search(ctx, win, capfd, ring=False)
     assert gpu_search(ctx, inc, s64, n_mut, first, n).tobytes() == ref.tobytes()
+
+
+FIN_RING_LINE = "[wf_plan] finishes in a ring of recent levels"
+PAPER_TAKEN = []  # whether each random deep window's finishes took the ring
+
+
+def upload_paper(ctx, win, capfd, ring=True):
+    """Upload; returns whether the finishes took the ring (the paper's order
+    with the order and slot arrays in HBM)."""
+    os.environ["WF_PLAN_VERBOSE"] = "1"
+    if ring:
+        os.environ.pop("WF_PLAN_RING", None)
+    else:
+        os.environ["WF_PLAN_RING"] = "off"
+    try:
+        capfd.readouterr()
+        ctx.wf_plan_upload_window(win)
+        err = capfd.readouterr().err
+    finally:
+        os.environ.pop("WF_PLAN_VERBOSE", None)
+        os.environ.pop("WF_PLAN_RING", None)
+    return FIN_RING_LINE in err
+
+
+@pytest.mark.parametrize("batch", [False, True])
+def test_paper_order_deep_workload(ctx, capfd, batch):
+    """The paper's reclamation order on the deep workload: the order and the
+    next use per slot built before the walk in HBM, the finishes in the ring,
+    against the oracle (scores, keys, schedules) and the layout without the
+    ring."""
+    win, plans = W.make_config(3)
+    win.victim_order = 1
+    if batch:
+        win.dev_batch = np.array([1, 2, 3, 4] * 4, np.int32)
+        plans = plans.take(np.arange(0, plans.n_plans, 4))
+    P = plans.n_plans
+    assert upload_paper(ctx, win, capfd), "the finishes did not take the ring"
+    log(f"[ring paper] deep workload: {P} plans, batch limits {batch}")
+    ref = oracle.score(win, plans, threads=THREADS)
+    assert gpu_scores(ctx, plans, P).tobytes() == ref.tobytes()
+    sub = plans.take(np.arange(0, P, 16))
+    assert gpu_keys(ctx, sub, sub.n_plans).tobytes() == oracle.phi_keys(win, sub, threads=THREADS).tobytes()
+    check_schedules(ctx, win, plans.take(np.arange(0, P, 64)), (P + 63) // 64, "paper deep workload")
+    assert not upload_paper(ctx, win, capfd, ring=False)
+    assert gpu_scores(ctx, plans, P).tobytes() == ref.tobytes()
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_paper_order_random_deep_windows(ctx, capfd, seed):
+    """Random deep windows under the paper's order (chains ahead of their
+    level, edges up to three levels back, ranked levels, batch limits,
+    invalid devices): scores, keys and schedules against the oracle, with
+    and without the ring."""
+    win, plans = deep_case(seed)
+    win.victim_order = 1
+    P = plans.n_plans
+    took = upload_paper(ctx, win, capfd)
+    PAPER_TAKEN.append(took)
+    log(f"[ring paper] seed {seed}: N={win.n_act} D={win.n_dev} M={win.n_models} fin ring={took}")
+    ref = oracle.score(win, plans, threads=THREADS)
+    assert gpu_scores(ctx, plans, P).tobytes() == ref.tobytes(), f"seed {seed}"
+    assert gpu_keys(ctx, plans, P).tobytes() == oracle.phi_keys(win, plans, threads=THREADS).tobytes()
+    check_schedules(ctx, win, plans.take(np.arange(0, P, 5)), (P + 4) // 5, f"paper seed {seed}")
+    upload_paper(ctx, win, capfd, ring=False)
+    assert gpu_scores(ctx, plans, P).tobytes() == ref.tobytes()
+
+
+def test_paper_ring_was_exercised():
+    """Some of the random deep windows above kept their finishes in the ring
+    (the others fit the LDS layout or none of the HBM one's conditions)."""
+    assert len(PAPER_TAKEN) == 8 and sum(PAPER_TAKEN) >= 2, PAPER_TAKEN
