@@ -838,7 +838,10 @@ wf_status plan_launch(wf_plan_ctx* ctx, const HostWindow& h, bool search, wfp::S
     wfp::WaveOffsets o4{};
     const int64_t wb4 = wave_layout(h, sp.G, tsz, sp.nwa, sp.nibble, search, o4, true, sp.ring_size);
     const int lds4 = sp.wg_ld + sp.waves * o4.split;
-    if (lds4 <= lds_blk) {
+    // (taken only where the ring keeps the HBM layout's waves per CU: a wide
+    // level makes the ring as large as the window)
+    const int wg_hbm = std::max(1, std::min(2, lds_cu / std::max(sp.lds_bytes, 1)));
+    if (lds4 <= lds_blk && std::max(1, std::min(2, lds_cu / lds4)) >= wg_hbm) {
       const int wg_per_cu = std::max(1, std::min(2, lds_cu / lds4));
       const int64_t hw = std::max<int64_t>((wb4 - o4.split) * sp.waves, 1);
       const int64_t wgs = std::min<int64_t>((int64_t)ctx->n_cu * wg_per_cu, (int64_t(1) << 30) / hw);
