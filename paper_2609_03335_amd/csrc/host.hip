@@ -600,15 +600,15 @@ wf_status plan_window(wf_plan_ctx* ctx, const HostWindow& h, bool time64_req, Im
   const int32_t S = (int32_t)sink.size();
   if (sink.empty()) sink.push_back(0);
   t.sink = img.put(sink.data(), sink.size() * 4);
-  // ring of recent levels (scan reclamation in the default order): a
-  // finish must stay from the level where it is written -- a fused chain's
-  // members with the chain head, up to ring_a levels early -- to the last
-  // level an edge reads it, ring_b levels later
+  // ring of recent levels (the scan reclamation modes, and the paper's
+  // order, whose finishes alone may take it): a finish must stay from the
+  // level where it is written -- a fused chain's members with the chain
+  // head, up to ring_a levels early -- to the last level an edge reads it,
+  // ring_b levels later
   const bool batched_w = std::any_of(h.batch.begin(), h.batch.end(), [](int32_t b) { return b > 1; });
-  // (and the paper's order, whose finishes alone may take the ring)
-  const bool scan_lru = h.victim_order == WF_VICTIM_PAPER || batched_w || M > 16 || !h.rcap.empty();
+  const bool ring_tables = h.victim_order == WF_VICTIM_PAPER || batched_w || M > 16 || !h.rcap.empty();
   sp.ring_ok = 0;
-  if (scan_lru && N > 0) {
+  if (ring_tables && N > 0) {
     std::vector<int32_t> lvl((size_t)N), wmin((size_t)N);
     for (int32_t l = 0; l < h.n_levels; ++l)
       for (int32_t i = h.level_off[l]; i < h.level_off[l + 1]; ++i) lvl[i] = l;
