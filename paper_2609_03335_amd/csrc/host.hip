@@ -757,7 +757,11 @@ wf_status plan_launch(wf_plan_ctx* ctx, const HostWindow& h, bool search, wfp::S
   const int64_t wb_g = wave_layout(h, Gg, tsz, sp.nwa, sp.nibble, search, og, true);
   const int64_t hbm_wave = wb_g - og.split;  // HBM bytes per wave
   const int lds_wg_g = sp.wg_ld + waves_g * og.split;
-  const int wgs_per_cu = lds_wg_g <= lds_blk ? std::max(1, std::min(2, lds_cu / std::max(lds_wg_g, 1))) : 0;
+  // (up to three four-wave workgroups per CU run: the HBM layout's kernel
+  // is built for three waves per SIMD; the choices below weigh the two per
+  // CU their ratios were measured with)
+  const int wgs_fit = lds_wg_g <= lds_blk ? std::max(1, lds_cu / std::max(lds_wg_g, 1)) : 0;
+  const int wgs_per_cu = std::min(2, wgs_fit), wgs_run = std::min(3, wgs_fit);
   const double hbm_lanes = (double)std::min(Gg * D, 64) * waves_g * wgs_per_cu;
   if (best < 0 && wgs_per_cu == 0)
     return fail(&ctx->err, WF_EUNSUPPORTED, "window too large for LDS (N=%d, D=%d, M=%d)", h.N, D, h.M);
@@ -767,7 +771,7 @@ wf_status plan_launch(wf_plan_ctx* ctx, const HostWindow& h, bool search, wfp::S
     const int64_t cap_bytes = int64_t(1) << 30;
     const int G = Gg, waves = waves_g;
     const wfp::WaveOffsets o = og;
-    int64_t wgs = std::min<int64_t>((int64_t)ctx->n_cu * wgs_per_cu,
+    int64_t wgs = std::min<int64_t>((int64_t)ctx->n_cu * wgs_run,
                                     cap_bytes / std::max<int64_t>(hbm_wave * waves, 1));
     if (wgs < 1 && best >= 0) return WF_OK;  // keep the LDS layout
     if (wgs < 1)

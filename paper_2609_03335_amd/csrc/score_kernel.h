@@ -156,8 +156,11 @@ using OutRec = std::conditional_t<PHI, wf_plan_key, wf_plan_score>;
 // PLACE: 0 = per-wave regions in LDS, 1 = their per-activation arrays in HBM
 // scratch, 2 = the ring of recent levels in LDS (scan reclamation, rows from
 // HBM).
+// (the HBM layout, PLACE 1, is bound by the latency of its per-activation
+// arrays: it is built for three waves per SIMD, four-wave workgroups, three
+// per CU, although that spills registers)
 template <typename TT, bool TAB_LDS, int QB, int PLACE, bool SEARCH, bool PHI, bool SCHED>
-__global__ __launch_bounds__(512) void score_plans(ScoreParams sp,
+__global__ __launch_bounds__(PLACE == 1 ? 256 : 512, PLACE == 1 ? 3 : 1) void score_plans(ScoreParams sp,
                                                    const int8_t* __restrict__ dev_all,
                                                    const uint16_t* __restrict__ prio_all,
                                                    const uint8_t* __restrict__ flags_all, int64_t P,
