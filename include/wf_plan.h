@@ -411,11 +411,11 @@ int wf_plan_time_bits(const wf_plan_ctx *ctx);
 
 /* Name of the kernel that scores plans read from HBM for the uploaded
  * window without a schedule: "score_lean" when the window qualifies for the
- * lean kernel (uint32 times, at most 16 models, at most 512 activations, the
- * default reclamation order, not both batch limits and replica caps), else
- * "score_plans"; "" when ctx is NULL or has no window.  Both give identical
- * results.  With batch limits the lean kernel serves wf_plan_score_batch
- * only. */
+ * lean kernel (uint32 times, at most 16 models, at most 512 activations;
+ * under the paper's reclamation order or with batch limits only without
+ * replica caps, and not both), else "score_plans"; "" when ctx is NULL or
+ * has no window.  Both give identical results.  Under the paper's order or
+ * with batch limits the lean kernel serves wf_plan_score_batch only. */
 const char *wf_plan_score_kernel(const wf_plan_ctx *ctx);
 
 /* Library version string. */
